@@ -1,0 +1,374 @@
+"""CPU oracle for one UnifiedNN training step -- TEST INFRASTRUCTURE ONLY.
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
+import this module. The library's compute path never reaches it.
+
+What it computes (UnifiedNN, Trainer section, Algorithm 2): for every
+sub-model m, the gradient of m's own loss on the batch, then the plain SGD
+update theta^m <- theta^m - eta * g^m. Each sub-model has its own criterion and
+optimizer and no sub-model interferes with another (Model Unifier section), so
+the oracle trains every model ALONE: nothing here ever reads another model's
+parameters, and the merged run must equal these separate runs (the paper's
+claim that the hybrid trains each sub-model exactly as separate training would,
+Design overview).
+
+Every function below is the plain definition of its operation, written with
+numpy in float64. Readings where the paper is silent (all taken to match the
+paper's PyTorch prototype, whose defaults these are):
+
+* loss: softmax cross-entropy, mean over the batch;
+* optimizer: plain SGD, no momentum or weight decay, computed as the
+  correctly rounded fp32 fma(-lr, g, theta);
+* gradients are recomputed every step (nothing accumulates across steps);
+* the loss a step reports is the forward loss at the pre-update parameters;
+* convolution is cross-correlation, stride 1, zero padding;
+* max-pool is 2x2 / stride 2 / floor mode, the first maximum in row-major
+  window order wins ties; ReLU'(0) = 0;
+* flatten is NCHW (c, h, w) order.
+
+Precision modes:
+
+* ``"f64"``  no rounding at all (used for finite-difference checks);
+* ``"f32"``  every dot product accumulates in fp64 and is rounded to fp32 when
+  stored;
+* ``"bf16"`` as f32, and in addition the operands of every Linear/Conv layer
+  (its input activation, its weights, and the gradient arriving at its output)
+  are rounded to bf16 (round to nearest, ties to even) when read. Logits, the
+  softmax-CE arithmetic, all accumulators, dW, db and the fp32 master weights
+  stay fp32. Because ReLU, max-pool, flatten and their backward passes are
+  exact, rounding at the reader equals rounding the stored tensor.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+F64 = np.float64
+F32 = np.float32
+
+
+# ---------------------------------------------------------------------------
+# Rounding
+# ---------------------------------------------------------------------------
+def to_f32(a):
+    """Round to nearest fp32 (IEEE conversion)."""
+    return np.asarray(a, dtype=F64).astype(F32)
+
+
+def to_bf16(a):
+    """Round an fp32 array to bf16 (nearest, ties to even), returned as fp32 values.
+
+    bf16 keeps the top 16 bits of the fp32 pattern; adding 0x7FFF plus the lowest
+    kept bit before truncation rounds to nearest with ties to the even pattern.
+    NaNs stay NaN (quiet bit forced so truncation cannot turn them into inf).
+    """
+    a = np.ascontiguousarray(np.asarray(a, dtype=F32))
+    u = a.view(np.uint32)
+    r = u + np.uint32(0x7FFF)            # wraps only for NaN patterns, which are replaced below
+    r += (u >> np.uint32(16)) & np.uint32(1)
+    r &= np.uint32(0xFFFF0000)
+    nan = np.isnan(a)
+    if nan.any():
+        r[nan] = (u[nan] | np.uint32(0x00400000)) & np.uint32(0xFFFF0000)
+    return r.view(F32).reshape(a.shape)
+
+
+def fma32(a, b, c):
+    """Correctly rounded fp32 a*b + c for fp32 arrays.
+
+    a*b is exact in fp64 (24+24 bits). s = fl64(a*b + c) has exact error e
+    (TwoSum). Rounding s to fp32 is then correct unless s lies exactly on an fp32
+    midpoint, in which case the sign of e decides the direction.
+    """
+    a64 = np.asarray(a, dtype=F32).astype(F64)
+    b64 = np.asarray(b, dtype=F32).astype(F64)
+    c64 = np.asarray(c, dtype=F32).astype(F64)
+    p = a64 * b64
+    s = p + c64
+    bb = s - p
+    e = (p - (s - bb)) + (c64 - bb)
+    r = s.astype(F32)
+    d = s - r.astype(F64)
+    toward = np.where(d > 0, np.inf, -np.inf).astype(F32)
+    nb = np.nextafter(r, toward)
+    midpoint = (d != 0) & (2.0 * d == nb.astype(F64) - r.astype(F64))
+    go_nb = midpoint & (e != 0) & (np.sign(e) == np.sign(d))
+    return np.where(go_nb, nb, r).astype(F32)
+
+
+class _Mode:
+    def __init__(self, mode):
+        if mode not in ("f64", "f32", "bf16"):
+            raise ValueError(f"unknown precision mode {mode!r}")
+        self.mode = mode
+
+    def operand(self, a):
+        """A tensor as a Linear/Conv layer reads it (activation, weight or gradient)."""
+        if self.mode == "f64":
+            return np.asarray(a, dtype=F64)
+        a32 = to_f32(a)
+        if self.mode == "bf16":
+            a32 = to_bf16(a32)
+        return a32.astype(F64)
+
+    def store(self, a):
+        """The result of an fp64 accumulation as it is stored."""
+        if self.mode == "f64":
+            return np.asarray(a, dtype=F64)
+        return to_f32(a).astype(F64)
+
+
+# ---------------------------------------------------------------------------
+# Layers (definitions)
+# ---------------------------------------------------------------------------
+def linear_fwd(h, W, b):
+    """z = h W^T + b  (PyTorch Linear; W is [out, in])."""
+    return h @ W.T + b
+
+
+def linear_bwd(dz, h, W, need_dh=True):
+    """dW = dz^T h, db = sum_b dz, dh = dz W."""
+    dW = dz.T @ h
+    db = dz.sum(axis=0)
+    dh = dz @ W if need_dh else None
+    return dW, db, dh
+
+
+def conv2d_fwd(h, W, b, pad):
+    """z[n,o,p,q] = b[o] + sum_{c,u,v} W[o,c,u,v] * h[n,c,p+u-pad,q+v-pad]; outside reads are 0.
+
+    Written as the sum over the k*k kernel taps of a channel contraction.
+    """
+    n, c, H, Wd = h.shape
+    o, c2, k, k2 = W.shape
+    assert c == c2 and k == k2
+    OH, OW = H + 2 * pad - k + 1, Wd + 2 * pad - k + 1
+    hp = np.pad(h, ((0, 0), (0, 0), (pad, pad), (pad, pad)))
+    z = np.zeros((n, OH, OW, o), dtype=F64)
+    for u in range(k):
+        for v in range(k):
+            win = hp[:, :, u:u + OH, v:v + OW]                     # [n, c, OH, OW]
+            z += np.tensordot(win, W[:, :, u, v], axes=([1], [1]))  # [n, OH, OW, o]
+    return z.transpose(0, 3, 1, 2) + b[None, :, None, None]
+
+
+def conv2d_bwd(dz, h, W, pad, need_dh=True):
+    """dW[o,c,u,v] = sum_{n,p,q} dz[n,o,p,q] h[n,c,p+u-pad,q+v-pad];  db[o] = sum dz[n,o,:,:];
+    dh[n,c,y,x] = sum_{o,u,v} dz[n,o,y-u+pad,x-v+pad] W[o,c,u,v]."""
+    n, c, H, Wd = h.shape
+    o, _, k, _ = W.shape
+    OH, OW = dz.shape[2], dz.shape[3]
+    hp = np.pad(h, ((0, 0), (0, 0), (pad, pad), (pad, pad)))
+    dW = np.zeros(W.shape, dtype=F64)
+    dhp = np.zeros(hp.shape, dtype=F64) if need_dh else None
+    for u in range(k):
+        for v in range(k):
+            win = hp[:, :, u:u + OH, v:v + OW]
+            dW[:, :, u, v] = np.tensordot(dz, win, axes=([0, 2, 3], [0, 2, 3]))
+            if need_dh:
+                t = np.tensordot(dz, W[:, :, u, v], axes=([1], [0]))   # [n, OH, OW, c]
+                dhp[:, :, u:u + OH, v:v + OW] += t.transpose(0, 3, 1, 2)
+    db = dz.sum(axis=(0, 2, 3))
+    dh = dhp[:, :, pad:pad + H, pad:pad + Wd] if need_dh else None
+    return dW, db, dh
+
+
+def relu_fwd(z):
+    return np.maximum(z, 0.0)
+
+
+def relu_bwd(dy, y):
+    """ReLU' taken from the output: 1 where the output is > 0, else 0 (so ReLU'(0) = 0)."""
+    return dy * (y > 0)
+
+
+def maxpool2_fwd(h):
+    """2x2 / stride 2 / floor max-pool. Returns (out, argmax in 0..3 = dy*2+dx).
+
+    Ties go to the first maximum in row-major window order (numpy's argmax
+    returns the first occurrence).
+    """
+    n, c, H, Wd = h.shape
+    PH, PW = H // 2, Wd // 2
+    win = h[:, :, :2 * PH, :2 * PW].reshape(n, c, PH, 2, PW, 2)
+    win = win.transpose(0, 1, 2, 4, 3, 5).reshape(n, c, PH, PW, 4)
+    am = np.argmax(win, axis=-1)
+    out = np.take_along_axis(win, am[..., None], axis=-1)[..., 0]
+    return out, am
+
+
+def maxpool2_bwd(dout, am, in_shape):
+    """Route each pooled gradient to its window's argmax; everything else gets 0."""
+    n, c, H, Wd = in_shape
+    PH, PW = dout.shape[2], dout.shape[3]
+    win = np.zeros(dout.shape + (4,), dtype=F64)
+    np.put_along_axis(win, am[..., None], np.asarray(dout, dtype=F64)[..., None], axis=-1)
+    g = win.reshape(n, c, PH, PW, 2, 2).transpose(0, 1, 2, 4, 3, 5).reshape(n, c, 2 * PH, 2 * PW)
+    dh = np.zeros(in_shape, dtype=F64)
+    dh[:, :, :2 * PH, :2 * PW] = g
+    return dh
+
+
+def softmax_ce(z, y):
+    """Mean softmax cross-entropy and its gradient.
+
+    L = (1/B) sum_b (lse(z_b) - z_{b,y_b}), lse(z) = m + log sum exp(z - m);
+    dL/dz = (softmax(z) - onehot(y)) / B.
+    """
+    z = np.asarray(z, dtype=F64)
+    B = z.shape[0]
+    m = z.max(axis=1, keepdims=True)
+    e = np.exp(z - m)
+    s = e.sum(axis=1, keepdims=True)
+    lse = m[:, 0] + np.log(s[:, 0])
+    rows = np.arange(B)
+    loss = float(np.mean(lse - z[rows, y]))
+    p = e / s
+    p[rows, y] -= 1.0
+    return loss, p / B
+
+
+# ---------------------------------------------------------------------------
+# One model, alone
+# ---------------------------------------------------------------------------
+def count_params(spec, in_shape):
+    """Parameter count by walking the layer list (oracle's own shape inference)."""
+    shape = tuple(in_shape)
+    total = 0
+    for layer in spec["layers"]:
+        op = layer[0]
+        if op == "linear":
+            fin = int(np.prod(shape))
+            total += layer[1] * fin + layer[1]
+            shape = (layer[1],)
+        elif op == "conv":
+            c, H, W = shape
+            o, k, pad = layer[1], layer[2], layer[3]
+            total += o * c * k * k + o
+            shape = (o, H + 2 * pad - k + 1, W + 2 * pad - k + 1)
+        elif op == "pool":
+            c, H, W = shape
+            shape = (c, H // 2, W // 2)
+        elif op == "flatten":
+            shape = (int(np.prod(shape)),)
+        elif op != "relu":
+            raise ValueError(f"unknown op {op!r}")
+    return total
+
+
+def forward(spec, params, x, mode="f32"):
+    """Forward pass. Returns (logits as stored, cache for backward)."""
+    R = _Mode(mode)
+    h = np.asarray(x, dtype=F64)
+    cache = []
+    pi = 0
+    for layer in spec["layers"]:
+        op = layer[0]
+        if op == "linear":
+            W, b = params[pi], params[pi + 1]
+            hin, Wq = R.operand(h), R.operand(W)
+            if hin.ndim != 2:
+                raise ValueError("linear layer needs a 2-D input (add a flatten)")
+            h = R.store(linear_fwd(hin, Wq, np.asarray(b, dtype=F64)))
+            cache.append(("linear", pi, hin, Wq))
+            pi += 2
+        elif op == "conv":
+            W, b = params[pi], params[pi + 1]
+            hin, Wq = R.operand(h), R.operand(W)
+            h = R.store(conv2d_fwd(hin, Wq, np.asarray(b, dtype=F64), layer[3]))
+            cache.append(("conv", pi, hin, Wq, layer[3]))
+            pi += 2
+        elif op == "relu":
+            h = relu_fwd(h)
+            cache.append(("relu", h))
+        elif op == "pool":
+            shp = h.shape
+            h, am = maxpool2_fwd(h)
+            cache.append(("pool", am, shp))
+        elif op == "flatten":
+            cache.append(("flatten", h.shape))
+            h = h.reshape(h.shape[0], -1)
+        else:
+            raise ValueError(f"unknown op {op!r}")
+    return h, cache
+
+
+def backward(spec, params, cache, dlogits, mode="f32"):
+    """Backward pass from dL/dlogits. Returns the gradient list (state-dict order)."""
+    R = _Mode(mode)
+    grads = [None] * len(params)
+    g = np.asarray(dlogits, dtype=F64)
+    first_param_layer = min(e[1] for e in cache if e[0] in ("linear", "conv"))
+    for entry in reversed(cache):
+        kind = entry[0]
+        if kind in ("linear", "conv"):
+            pi, hin, Wq = entry[1], entry[2], entry[3]
+            gq = R.operand(g)
+            need_dh = pi != first_param_layer
+            if kind == "linear":
+                dW, db, dh = linear_bwd(gq, hin, Wq, need_dh)
+            else:
+                dW, db, dh = conv2d_bwd(gq, hin, Wq, entry[4], need_dh)
+            grads[pi], grads[pi + 1] = R.store(dW), R.store(db)
+            g = R.store(dh) if need_dh else None
+        elif kind == "relu":
+            if g is not None:
+                g = relu_bwd(g, entry[1])
+        elif kind == "pool":
+            if g is not None:
+                g = maxpool2_bwd(g, entry[1], entry[2])
+        elif kind == "flatten":
+            if g is not None:
+                g = g.reshape(entry[1])
+    return grads
+
+
+def sgd_update(params, grads, lr, mode="f32"):
+    """theta <- theta - lr * g  (Algorithm 2's update), as fp32 fma(-lr, g, theta)."""
+    if mode == "f64":
+        return [np.asarray(p, dtype=F64) - lr * np.asarray(g, dtype=F64) for p, g in zip(params, grads)]
+    nlr = np.full((), -lr, dtype=F32)
+    return [fma32(nlr, to_f32(g), p) for p, g in zip(params, grads)]
+
+
+def step(spec, params, x, y, lr, mode="f32"):
+    """One training step of one model. Returns (loss at pre-update params, new params, grads)."""
+    logits, cache = forward(spec, params, x, mode)
+    loss, dz = softmax_ce(logits, y)
+    dz = _Mode(mode).store(dz)
+    grads = backward(spec, params, cache, dz, mode)
+    return loss, sgd_update(params, grads, lr, mode), grads
+
+
+def loss_only(spec, params, x, y, mode="f64"):
+    logits, _ = forward(spec, params, x, mode)
+    return softmax_ce(logits, y)[0]
+
+
+def train(spec, params, batches, lr, mode="f32"):
+    """Train one model alone over a sequence of (x, y) batches.
+
+    Returns (losses per step, final params, grads of the last step).
+    """
+    losses = []
+    grads = None
+    params = [np.array(p, dtype=F64 if mode == "f64" else F32) for p in params]
+    for x, y in batches:
+        loss, params, grads = step(spec, params, x, y, lr, mode)
+        losses.append(loss)
+    return np.array(losses), params, grads
+
+
+def train_models(specs, theta0s, batches, lr, mode="f32", threads=1, models=None):
+    """Train each listed model alone (independently, optionally in parallel threads)."""
+    idx = list(range(len(specs))) if models is None else list(models)
+    batches = list(batches)
+
+    def run(i):
+        return train(specs[i], theta0s[i], batches, lr, mode)
+
+    if threads <= 1:
+        return {i: run(i) for i in idx}
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        res = list(ex.map(run, idx))
+    return dict(zip(idx, res))
