@@ -1,0 +1,187 @@
+/*
+ * unifiednn.h -- C ABI of the fused N-model training step on one MI355X (gfx950).
+ *
+ * The library trains N independent models that share one input batch as one
+ * "hybrid" model: every call to un_step runs, for ALL models at once, the body
+ * of the paper's hybrid training algorithm (UnifiedNN, Trainer section,
+ * Algorithm 2): each sub-model's gradient of its own loss on the batch, then
+ * each sub-model's SGD update theta^m <- theta^m - eta * g^m. The models are
+ * merged only in the sense of the Model Unifier (Algorithm 1): their layer
+ * graphs are a disjoint union with one global input; no value ever flows from
+ * one model to another, and each model trains exactly as it would alone.
+ *
+ * Conventions shared by every call:
+ *   - Every call returns a un_status; UN_OK is 0. On failure the message is
+ *     available from un_last_error(ctx) until the next call on that context.
+ *     No C++ exception crosses this boundary.
+ *   - A validation failure (UN_ERR_INVALID, UN_ERR_RANGE, UN_ERR_BUFSIZE,
+ *     UN_ERR_STATE, UN_ERR_UNSUPPORTED) changes no state. A HIP runtime failure
+ *     returns UN_ERR_DEVICE and poisons the context: every later call except
+ *     un_last_error and un_destroy returns UN_ERR_DEVICE.
+ *   - Host pointers are owned by the caller; the library copies what it needs
+ *     before returning, except where a call says it is asynchronous.
+ *   - A context owns all of its device memory (one arena, allocated in
+ *     un_create, freed in un_destroy) and one HIP stream.
+ *   - One context must not be used from two threads at once.
+ */
+#ifndef UNIFIEDNN_H
+#define UNIFIEDNN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct un_ctx un_ctx;
+
+typedef enum {
+  UN_OK = 0,
+  UN_ERR_INVALID = 1,     /* malformed argument or spec */
+  UN_ERR_STATE = 2,       /* call made in the wrong order (e.g. step before load) */
+  UN_ERR_OOM = 3,         /* the arena does not fit in device memory */
+  UN_ERR_DEVICE = 4,      /* HIP runtime error; the context is poisoned */
+  UN_ERR_RANGE = 5,       /* index or label out of range */
+  UN_ERR_BUFSIZE = 6,     /* caller's buffer too small / wrong element count */
+  UN_ERR_UNSUPPORTED = 7  /* well-formed, but a layer pattern this library does not fuse */
+} un_status;
+
+/* Arithmetic of the step.
+ * UN_F32:            every tensor fp32; fp32 MFMA with fp32 accumulation.
+ * UN_BF16_F32MASTER: activations, activation gradients and the weights the
+ *                    GEMMs read are bf16 (round to nearest even); accumulation,
+ *                    logits, the loss, dW/db and the master weights stay fp32. */
+typedef enum { UN_F32 = 0, UN_BF16_F32MASTER = 1 } un_precision;
+
+/* Layer ops of a sub-model, in the order of a PyTorch nn.Sequential (the paper
+ * defines every sub-model as a sequential module, Design overview). */
+typedef enum {
+  UN_LINEAR = 0,   /* out = features;   weight [out, in], bias [out] */
+  UN_CONV2D = 1,   /* out = channels, kernel k x k, stride 1, zero padding pad;
+                      weight [out, in, k, k], bias [out]; cross-correlation */
+  UN_RELU = 2,
+  UN_MAXPOOL2 = 3, /* 2x2, stride 2, floor mode; ties: first max in row-major order */
+  UN_FLATTEN = 4   /* NCHW (c, h, w) order */
+} un_op;
+
+typedef struct {
+  int32_t op;      /* un_op */
+  int32_t out;     /* UN_LINEAR: out features; UN_CONV2D: out channels; else 0 */
+  int32_t kernel;  /* UN_CONV2D only */
+  int32_t pad;     /* UN_CONV2D only */
+} un_layer;
+
+typedef struct {
+  int32_t n_layers;
+  const un_layer* layers;   /* read during un_create only */
+  int32_t num_classes;      /* must equal the last Linear layer's out */
+  uint64_t init_seed;       /* seed of the library's own initialisation */
+} un_model_spec;
+
+/* The one shared input: x is [batch, in_c, in_h, in_w] (images) or, with
+ * in_h = in_w = 1, [batch, in_c] (feature vectors). */
+typedef struct {
+  int32_t batch;
+  int32_t in_c, in_h, in_w;
+  int32_t precision;        /* un_precision */
+} un_input_spec;
+
+/* Build the hybrid model (Model Unifier, Algorithm 1): validate every spec,
+ * plan the fused schedule and the one device arena, allocate it, and
+ * initialise each model's parameters from its init_seed (Kaiming-uniform
+ * weights U(+-sqrt(6/fan_in)), biases U(+-1/sqrt(fan_in)), drawn with a
+ * counter-based generator; callers needing exact start values use
+ * un_set_params). Supported layer patterns per model: zero or more
+ * [Conv2d, optional ReLU, optional MaxPool2] blocks, a Flatten if any conv is
+ * present, then one or more [Linear, optional ReLU] blocks, the last Linear
+ * having no ReLU and out == num_classes.
+ * On success *out owns the context. Errors: UN_ERR_INVALID, UN_ERR_UNSUPPORTED,
+ * UN_ERR_OOM, UN_ERR_DEVICE (then *out is NULL). */
+un_status un_create(const un_model_spec* specs, int32_t n_models,
+                    const un_input_spec* in, un_ctx** out);
+
+/* Copy one shared batch to the device, once for all N models (Memory
+ * conservation section: a common dataset is loaded only once). x is host fp32
+ * laid out as in un_input_spec, y is host int32 [batch]. Labels are checked on
+ * the host: a label outside [0, num_classes) of any model returns UN_ERR_RANGE
+ * and leaves the previously loaded batch in place. Synchronous. */
+un_status un_load_batch(un_ctx* ctx, const float* x, const int32_t* y);
+
+/* As un_load_batch, with x and y already in device memory (same layouts). The
+ * labels are range-checked after a device-to-host copy. */
+un_status un_load_batch_device(un_ctx* ctx, const float* x_dev, const int32_t* y_dev);
+
+/* One fused training step of all N models on the loaded batch (Algorithm 2's
+ * loop body for every sub-model): forward, per-model mean softmax
+ * cross-entropy, backward, per-model SGD with learning rate lr.
+ * If losses is non-NULL it receives, per model, the loss at the parameters
+ * BEFORE this step's update (host fp32 [N]); the call then waits for the step.
+ * With losses == NULL the step is only enqueued on the context's stream.
+ * Errors: UN_ERR_STATE (no batch loaded), UN_ERR_INVALID (lr not finite). */
+un_status un_step(un_ctx* ctx, float lr, float* losses);
+
+/* The trained parameters of model i (Model Separator section: the sub-model's
+ * parameters copied back into the user's original layout): fp32, PyTorch
+ * state_dict order (per parameterised layer: weight then bias; Linear
+ * [out, in], Conv2d [out, in, k, k]; a Linear after Flatten indexes its input
+ * in NCHW order). With dst == NULL only *n_elems is set. Waits for the stream.
+ * Errors: UN_ERR_RANGE (i), UN_ERR_BUFSIZE (cap_elems too small). */
+un_status un_get_params(un_ctx* ctx, int32_t i, float* dst, size_t cap_elems, size_t* n_elems);
+
+/* Overwrite model i's parameters (same layout as un_get_params; n_elems must be
+ * the exact count). Used to start from given values, e.g. to compare with a
+ * reference trained elsewhere. Errors: UN_ERR_RANGE, UN_ERR_BUFSIZE. */
+un_status un_set_params(un_ctx* ctx, int32_t i, const float* src, size_t n_elems);
+
+/* The gradient of model i computed by the last un_step (same layout and order
+ * as un_get_params). Waits for the stream. Errors as un_get_params, and
+ * UN_ERR_STATE before the first step. */
+un_status un_get_grads(un_ctx* ctx, int32_t i, float* dst, size_t cap_elems, size_t* n_elems);
+
+/* Number of parameters of model i. */
+un_status un_param_count(const un_ctx* ctx, int32_t i, size_t* n_elems);
+
+/* Bytes of the device arena (the whole footprint of the hybrid model). */
+un_status un_arena_bytes(const un_ctx* ctx, size_t* bytes);
+
+/* Wait until all work enqueued on the context's stream has finished. */
+un_status un_sync(un_ctx* ctx);
+
+/* The context's HIP stream (a hipStream_t), so a caller can order its own work
+ * or record events around steps. Owned by the context. */
+un_status un_get_stream(const un_ctx* ctx, void** hip_stream);
+
+/* Kernel classes for per-kernel timing. */
+typedef enum {
+  UN_K_GEMM_FWD = 0,    /* grouped GEMM, forward levels */
+  UN_K_GEMM_BWD = 1,    /* grouped GEMM, dgrad + wgrad levels */
+  UN_K_CONV_FWD = 2,
+  UN_K_CONV_DGRAD = 3,
+  UN_K_CONV_WGRAD = 4,
+  UN_K_CE = 5,          /* softmax cross-entropy */
+  UN_K_SGD = 6,         /* multi-tensor SGD (+ shadow copies) */
+  UN_K_OTHER = 7,       /* load/convert, split-K reduction */
+  UN_K_COUNT = 8
+} un_kernel_class;
+
+/* Enable (1) or disable (0) per-kernel timing: while enabled, every launch is
+ * bracketed by HIP events on the context's stream and its duration is added to
+ * its class. Enabling resets the totals. */
+un_status un_profile_enable(un_ctx* ctx, int32_t enable);
+
+/* Totals since un_profile_enable(ctx, 1): summed milliseconds and launch count
+ * of one kernel class. Waits for the stream. */
+un_status un_profile_read(un_ctx* ctx, int32_t kernel_class, double* total_ms, int64_t* launches);
+
+/* Free the context and its arena. NULL is accepted. */
+void un_destroy(un_ctx* ctx);
+
+/* Message of the last failed call on ctx (or of the last failed un_create when
+ * ctx is NULL). Never NULL; owned by the library. */
+const char* un_last_error(const un_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* UNIFIEDNN_H */

@@ -255,12 +255,26 @@ def count_params(spec, in_shape):
     return total
 
 
-def forward(spec, params, x, mode="f32"):
-    """Forward pass. Returns (logits as stored, cache for backward)."""
+# Unit roundoff of fp32.
+U32 = 2.0 ** -24
+
+
+def forward(spec, params, x, mode="f32", flags=None):
+    """Forward pass. Returns (logits as stored, cache for backward).
+
+    If `flags` (a dict) is given, it receives, per parameterised layer (keyed by
+    the index of its weight in `params`), the set of output units (features or
+    channels) for which a discrete decision of this pass is ill-conditioned in
+    fp32: a ReLU input with |z| <= u * (sum_k |h_k w_k| + |b|), or a max-pool
+    window whose two largest values differ by no more than that, u = 2^-24.
+    Such a decision may legitimately come out either way in any fp32
+    evaluation order; everything else is decided identically.
+    """
     R = _Mode(mode)
     h = np.asarray(x, dtype=F64)
     cache = []
     pi = 0
+    mag, last_pi = None, None
     for layer in spec["layers"]:
         op = layer[0]
         if op == "linear":
@@ -269,20 +283,41 @@ def forward(spec, params, x, mode="f32"):
             if hin.ndim != 2:
                 raise ValueError("linear layer needs a 2-D input (add a flatten)")
             h = R.store(linear_fwd(hin, Wq, np.asarray(b, dtype=F64)))
+            if flags is not None:
+                mag, last_pi = linear_fwd(np.abs(hin), np.abs(Wq), np.abs(np.asarray(b, dtype=F64))), pi
             cache.append(("linear", pi, hin, Wq))
             pi += 2
         elif op == "conv":
             W, b = params[pi], params[pi + 1]
             hin, Wq = R.operand(h), R.operand(W)
             h = R.store(conv2d_fwd(hin, Wq, np.asarray(b, dtype=F64), layer[3]))
+            if flags is not None:
+                mag = conv2d_fwd(np.abs(hin), np.abs(Wq), np.abs(np.asarray(b, dtype=F64)), layer[3])
+                last_pi = pi
             cache.append(("conv", pi, hin, Wq, layer[3]))
             pi += 2
         elif op == "relu":
+            if flags is not None and mag is not None:
+                bad = np.abs(h) <= U32 * mag
+                axes = (0,) if h.ndim == 2 else (0, 2, 3)
+                flags.setdefault(last_pi, set()).update(np.nonzero(bad.any(axis=axes))[0].tolist())
             h = relu_fwd(h)
             cache.append(("relu", h))
         elif op == "pool":
             shp = h.shape
+            if flags is not None and mag is not None:
+                n, c, H, Wd = shp
+                PH, PW = H // 2, Wd // 2
+                win = h[:, :, :2 * PH, :2 * PW].reshape(n, c, PH, 2, PW, 2).transpose(0, 1, 2, 4, 3, 5)
+                wm = mag[:, :, :2 * PH, :2 * PW].reshape(n, c, PH, 2, PW, 2).transpose(0, 1, 2, 4, 3, 5)
+                win = win.reshape(n, c, PH, PW, 4)
+                top2 = np.sort(win, axis=-1)[..., 2:]
+                tol = U32 * wm.reshape(n, c, PH, PW, 4).max(axis=-1)
+                # exact zero ties (ReLU outputs) are decided identically everywhere
+                bad = (top2[..., 1] - top2[..., 0] <= tol) & ~((top2[..., 1] == 0) & (top2[..., 0] == 0))
+                flags.setdefault(last_pi, set()).update(np.nonzero(bad.any(axis=(0, 2, 3)))[0].tolist())
             h, am = maxpool2_fwd(h)
+            mag = None if mag is None else maxpool2_fwd(mag)[0]
             cache.append(("pool", am, shp))
         elif op == "flatten":
             cache.append(("flatten", h.shape))
@@ -330,9 +365,9 @@ def sgd_update(params, grads, lr, mode="f32"):
     return [fma32(nlr, to_f32(g), p) for p, g in zip(params, grads)]
 
 
-def step(spec, params, x, y, lr, mode="f32"):
+def step(spec, params, x, y, lr, mode="f32", flags=None):
     """One training step of one model. Returns (loss at pre-update params, new params, grads)."""
-    logits, cache = forward(spec, params, x, mode)
+    logits, cache = forward(spec, params, x, mode, flags)
     loss, dz = softmax_ce(logits, y)
     dz = _Mode(mode).store(dz)
     grads = backward(spec, params, cache, dz, mode)
@@ -344,31 +379,36 @@ def loss_only(spec, params, x, y, mode="f64"):
     return softmax_ce(logits, y)[0]
 
 
-def train(spec, params, batches, lr, mode="f32"):
+def train(spec, params, batches, lr, mode="f32", flags=None):
     """Train one model alone over a sequence of (x, y) batches.
 
-    Returns (losses per step, final params, grads of the last step).
+    Returns (losses per step, final params, grads of the last step). `flags`
+    (optional dict) collects the ill-conditioned decisions of every step.
     """
     losses = []
     grads = None
     params = [np.array(p, dtype=F64 if mode == "f64" else F32) for p in params]
     for x, y in batches:
-        loss, params, grads = step(spec, params, x, y, lr, mode)
+        loss, params, grads = step(spec, params, x, y, lr, mode, flags)
         losses.append(loss)
     return np.array(losses), params, grads
 
 
-def train_models(specs, theta0s, batches, lr, mode="f32", threads=1, models=None):
-    """Train each listed model alone (independently, optionally in parallel threads)."""
+def train_models(specs, theta0s, batches, lr, mode="f32", models=None, with_flags=False):
+    """Train each listed model alone, one after another.
+
+    Models are never run in concurrent Python threads: concurrent calls into
+    the BLAS library from several threads gave run-to-run different results.
+
+    Returns {model: (losses, params, grads)} or, with with_flags, (losses,
+    params, grads, flags)."""
     idx = list(range(len(specs))) if models is None else list(models)
     batches = list(batches)
-
-    def run(i):
-        return train(specs[i], theta0s[i], batches, lr, mode)
-
-    if threads <= 1:
-        return {i: run(i) for i in idx}
-    from concurrent.futures import ThreadPoolExecutor
-    with ThreadPoolExecutor(max_workers=threads) as ex:
-        res = list(ex.map(run, idx))
-    return dict(zip(idx, res))
+    out = {}
+    for i in idx:
+        if with_flags:
+            fl = {}
+            out[i] = train(specs[i], theta0s[i], batches, lr, mode, fl) + (fl,)
+        else:
+            out[i] = train(specs[i], theta0s[i], batches, lr, mode)
+    return out

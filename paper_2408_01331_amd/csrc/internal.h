@@ -1,0 +1,157 @@
+// Device-side problem descriptors shared by the host planner (un_api.cpp) and
+// the gfx950 kernels (kernels.hip). Everything here is plain data: the planner
+// fills these tables once in un_create and uploads them into the arena; a step
+// only launches kernels over them.
+#pragma once
+#include <stdint.h>
+
+#include <hip/hip_runtime.h>
+
+namespace un {
+
+// Storage element types: fp32 or bf16 (raw 16-bit pattern, round-to-nearest-even).
+typedef uint16_t bf16_t;
+
+// ---------------------------------------------------------------------------
+// Grouped GEMM:  C[m][n] = sum_k A[m][k] * B[n][k]
+// A and B are row-major with k contiguous ("NT" form). Every linear-layer
+// product of the step is brought into this form by keeping, next to each
+// activation / gradient, a transposed copy written by its producer:
+//   forward  Y[b][o]  = sum_i X[b][i]  W[o][i]      A = X,  B = W
+//   dgrad    dX[b][i] = sum_o G[b][o]  WT[i][o]     A = G,  B = WT
+//   wgrad    dW[o][i] = sum_b GT[o][b] XT[i][b]     A = GT, B = XT
+// XT carries one extra row of ones, so column n == nsplit of the wgrad product
+// is the bias gradient sum_b G[b][o].
+// ---------------------------------------------------------------------------
+enum Epi : int32_t {
+  EPI_FWD = 0,     // + bias, optional ReLU, store C (T) and optionally CT (T)
+  EPI_LOGITS = 1,  // + bias, store C as fp32
+  EPI_DGRAD = 2,   // optional ReLU' mask from `mask` ([n][m] layout, keep where > 0), store C, CT (T)
+  EPI_WGRAD = 3    // store C as fp32 for n < nsplit; column nsplit -> dbias[m]
+};
+
+struct GemmProb {
+  const void* A;
+  const void* B;
+  int64_t lda, ldb;
+  int32_t M, N, K;
+  int32_t epi, relu;
+  int32_t tiles_n;
+  int32_t tile_base;
+  int32_t nsplit;
+  void* C;
+  int64_t ldc;
+  void* CT;
+  int64_t ldct;
+  const float* bias;
+  const void* mask;
+  int64_t ldmask;
+  float* dbias;
+};
+
+// ---------------------------------------------------------------------------
+// Implicit-GEMM convolution (NHWC activations, stride 1, square kernel).
+// Pooled outputs are indexed by window w = (n*PH + ph)*PW + pw and the conv
+// output pixels feeding a pool are ordered m = 4*w + (dy*2 + dx), so the four
+// members of one 2x2 window are four consecutive GEMM rows.
+//   fwd:   C[m][o]  = sum_{(u,v,c)} Xpatch[m][(u,v,c)] * W[o][(u,v,c)]
+//   dgrad: C[m][c]  = sum_{(u,v,o)} dZ[n, y-u+pad, x-v+pad, o] * WT[c][(u,v,o)]
+//          (m = (n*H + y)*W + x over the conv's input pixels)
+//   wgrad: C[o][j]  = sum_{pixels} dZ[pix][o] * Xpatch[pix][j], j = (u,v,c);
+//          column j == KH*KW*C is the bias gradient. Split over pixel ranges;
+//          partial sums go to ws[split][o][j] and are reduced in split order.
+// dZ is never stored: it is gathered from the pooled gradient G[w][o] (which
+// already carries this block's ReLU' mask) and the window argmax.
+// ---------------------------------------------------------------------------
+struct ConvProb {
+  int32_t Nb, C, H, W, O, KH, pad, OH, OW, PH, PW;
+  int32_t pool, relu, prev_relu;
+  int32_t M, N, K;            // GEMM sizes of this pass
+  int32_t tiles_m, tiles_n, tile_base, splits, kchunk;
+  const void* X;              // conv input, NHWC, channel stride C
+  const void* Wt;             // fwd: W [O][ldw]; dgrad: WT [C][ldw]
+  int64_t ldw;
+  const float* bias;          // fwd
+  void* P;                    // fwd output (pooled or not), [pixel][O]
+  uint8_t* amax;              // fwd: window argmax, [w][O]
+  void* PT;                   // fwd: transposed output [(s*O + o)][n] for a Linear consumer, or null
+  int64_t ldpt;
+  const void* G;              // dgrad/wgrad: gradient at this block's output, [pixel][O]
+  const uint8_t* gam;         // its argmax (pool only)
+  void* Gprev;                // dgrad output [n*H*W + y*W + x][C]
+  float* ws;                  // wgrad partials [splits][O][ldws]
+  int64_t ldws;
+};
+
+// Split-K reduction of conv weight-gradient partials into dW [O][ldgw] and db [O].
+struct ReduceProb {
+  const float* ws;
+  int64_t ldws;
+  int32_t splits, O, J;       // J = KH*KW*C weight columns (+1 bias column in ws)
+  int32_t blk_base;
+  float* gW;
+  int64_t ldgw;
+  float* gb;
+};
+
+// ---------------------------------------------------------------------------
+// Softmax cross-entropy of one model: logits [B][ldl] fp32 -> per-model mean
+// loss, and dz = (softmax - onehot)/B stored as G [B][ldg] and GT [C][ldgt].
+// ---------------------------------------------------------------------------
+struct CeProb {
+  const float* logits;
+  int64_t ldl;
+  void* G;
+  int64_t ldg;
+  void* GT;
+  int64_t ldgt;
+  int32_t C;
+  int32_t model;
+};
+
+// ---------------------------------------------------------------------------
+// Multi-tensor SGD over 64x64 tiles of every parameter tensor:
+//   W <- fma(-lr, G, W)  (fp32 master), then the copies the GEMMs read:
+//   Wb  [r][ldw]          bf16 shadow in the same layout (bf16 mode), and
+//   WT  [c][j*R + r]      the transposed copy the dgrad reads (T), where the
+//                         tensor is viewed as [R][J][Cc] (J = kernel taps).
+// With use_grad false only the copies are refreshed (after set/init).
+// ---------------------------------------------------------------------------
+struct SgdTensor {
+  float* W;
+  const float* G;
+  void* Wb;
+  void* WT;
+  int64_t ldw, ldwt;
+  int32_t R, J, Cc;
+  int32_t tiles_r, tiles_c;   // per tap
+  int32_t tile_base;
+};
+
+// Kernel launch wrappers (kernels.hip). `bf16` selects the storage type.
+hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_prob, int ntiles,
+                       hipStream_t s);
+hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles,
+                           hipStream_t s);
+hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles,
+                             hipStream_t s);
+hipError_t launch_conv_wgrad(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles,
+                             hipStream_t s);
+hipError_t launch_reduce(const ReduceProb* probs, const int32_t* blk_prob, int nblocks, hipStream_t s);
+hipError_t launch_ce(bool bf16, const CeProb* probs, int nmodels, const int32_t* labels, int B,
+                     float* losses, hipStream_t s);
+hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int ntiles, float lr,
+                      bool use_grad, hipStream_t s);
+hipError_t launch_load(bool bf16, const float* x, int B, int C, int H, int W, void* X, void* XT,
+                       int64_t ldxt, hipStream_t s);
+
+// Tile shapes the planner must agree with.
+constexpr int GEMM_BM_BF16 = 128, GEMM_BN_BF16 = 128;
+constexpr int GEMM_BM_F32 = 64, GEMM_BN_F32 = 64;
+constexpr int CONV_BM_BF16 = 128, CONV_BN_BF16 = 128, CONV_BK_BF16 = 64;
+constexpr int CONV_BM_F32 = 64, CONV_BN_F32 = 64, CONV_BK_F32 = 32;
+constexpr int SGD_TILE = 64;
+constexpr int REDUCE_BLOCK = 256;
+constexpr int CE_MAX_BATCH = 8192;
+
+}  // namespace un

@@ -1,0 +1,950 @@
+// gfx950 (CDNA4) kernels of the fused N-model training step.
+//
+// One LDS-staged MFMA core (bf16: v_mfma_f32_16x16x32_bf16, fp32:
+// v_mfma_f32_16x16x4_f32; fp32 accumulation in both) is shared by
+//   - the grouped NT GEMM that runs every Linear layer's forward, dgrad and
+//     wgrad for all models of one depth level in one launch, and
+//   - the three implicit-GEMM convolution passes (forward with fused
+//     bias/ReLU/2x2 max-pool epilogue, dgrad with an un-pool gather prologue,
+//     split-K wgrad).
+// A workgroup (256 threads = 4 wave64s in a 2x2 arrangement) owns one output
+// tile of one problem; a flat tile table maps blockIdx.x to (problem, tile).
+// Every output element is reduced over k in a fixed order that depends only
+// on its own problem's shape, so a model's results are bitwise independent of
+// which other models share the launch.
+#include <hip/hip_runtime.h>
+
+#include "internal.h"
+
+namespace un {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// ---------------------------------------------------------------------------
+// Element helpers
+// ---------------------------------------------------------------------------
+// fp32 -> bf16, round to nearest, ties to even (NaN kept quiet).
+__device__ __forceinline__ bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+template <typename T> struct TT;
+template <> struct TT<float> {
+  static constexpr int VEC = 4;     // elements per 16 B
+  static constexpr int KSTEP = 16;  // k consumed per fragment load
+  __device__ static float to_f(float v) { return v; }
+  __device__ static float from_f(float v) { return v; }
+};
+template <> struct TT<bf16_t> {
+  static constexpr int VEC = 8;
+  static constexpr int KSTEP = 32;
+  __device__ static float to_f(bf16_t v) { return bf2f(v); }
+  __device__ static bf16_t from_f(float v) { return f2bf(v); }
+};
+
+// Element e of a 16-byte vector holding VEC elements of T.
+template <typename T> __device__ __forceinline__ float vget(const u32x4& v, int e);
+template <> __device__ __forceinline__ float vget<float>(const u32x4& v, int e) {
+  return __uint_as_float(v[e]);
+}
+template <> __device__ __forceinline__ float vget<bf16_t>(const u32x4& v, int e) {
+  uint32_t w = v[e >> 1];
+  return __uint_as_float((e & 1) ? (w & 0xffff0000u) : (w << 16));
+}
+// Raw bits of element e (for copying without conversion).
+template <typename T> __device__ __forceinline__ uint32_t vbits(const u32x4& v, int e);
+template <> __device__ __forceinline__ uint32_t vbits<float>(const u32x4& v, int e) { return v[e]; }
+template <> __device__ __forceinline__ uint32_t vbits<bf16_t>(const u32x4& v, int e) {
+  uint32_t w = v[e >> 1];
+  return (e & 1) ? (w >> 16) : (w & 0xffffu);
+}
+template <typename T> __device__ __forceinline__ void vset_bits(u32x4& v, int e, uint32_t bits);
+template <> __device__ __forceinline__ void vset_bits<float>(u32x4& v, int e, uint32_t bits) { v[e] = bits; }
+template <> __device__ __forceinline__ void vset_bits<bf16_t>(u32x4& v, int e, uint32_t bits) {
+  uint32_t w = v[e >> 1];
+  v[e >> 1] = (e & 1) ? ((w & 0xffffu) | (bits << 16)) : ((w & 0xffff0000u) | (bits & 0xffffu));
+}
+// Zero elements [valid, VEC).
+template <typename T> __device__ __forceinline__ void vmask_tail(u32x4& v, int valid) {
+#pragma unroll
+  for (int e = 0; e < TT<T>::VEC; ++e)
+    if (e >= valid) vset_bits<T>(v, e, 0u);
+}
+template <typename T> __device__ __forceinline__ T tbits(uint32_t b);
+template <> __device__ __forceinline__ float tbits<float>(uint32_t b) { return __uint_as_float(b); }
+template <> __device__ __forceinline__ bf16_t tbits<bf16_t>(uint32_t b) { return (bf16_t)b; }
+template <typename T> __device__ __forceinline__ uint32_t bits_of(T v);
+template <> __device__ __forceinline__ uint32_t bits_of<float>(float v) { return __float_as_uint(v); }
+template <> __device__ __forceinline__ uint32_t bits_of<bf16_t>(bf16_t v) { return v; }
+
+__device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
+
+// ---------------------------------------------------------------------------
+// MFMA core
+// ---------------------------------------------------------------------------
+template <typename T, int BM, int BN, int BK>
+struct Tile {
+  static constexpr int VEC = TT<T>::VEC;
+  static constexpr int LDK = BK + VEC;  // LDS row stride in elements (16 B pad)
+  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int FM = WM / 16, FN = WN / 16;
+  static constexpr int A_ELEMS = BM * LDK, B_ELEMS = BN * LDK;
+  static_assert(BK % TT<T>::KSTEP == 0, "BK must be a multiple of the MFMA k step");
+};
+
+// acc[i][j][r] holds C[wm + 16i + 4*(lane/16) + r][wn + 16j + lane%16].
+template <typename T, int BM, int BN, int BK>
+__device__ __forceinline__ void mma_block(const T* sA, const T* sB,
+                                          f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN]) {
+  using TL = Tile<T, BM, BN, BK>;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
+  const int lr = lane & 15, lg = lane >> 4;
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 32) {
+      bf16x8 a[TL::FM], b[TL::FN];
+#pragma unroll
+      for (int i = 0; i < TL::FM; ++i)
+        a[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(sA + (wm + 16 * i + lr) * TL::LDK + kk + 8 * lg));
+#pragma unroll
+      for (int j = 0; j < TL::FN; ++j)
+        b[j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(sB + (wn + 16 * j + lr) * TL::LDK + kk + 8 * lg));
+#pragma unroll
+      for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < TL::FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  } else {
+    // Lane group g feeds k = kk + 4g + q to the q-th MFMA; over q = 0..3 and
+    // the four groups every k of [kk, kk+16) is summed once.
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 16) {
+      f32x4 a[TL::FM], b[TL::FN];
+#pragma unroll
+      for (int i = 0; i < TL::FM; ++i) a[i] = *(const f32x4*)(sA + (wm + 16 * i + lr) * TL::LDK + kk + 4 * lg);
+#pragma unroll
+      for (int j = 0; j < TL::FN; ++j) b[j] = *(const f32x4*)(sB + (wn + 16 * j + lr) * TL::LDK + kk + 4 * lg);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+          for (int j = 0; j < TL::FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
+    }
+  }
+}
+
+// k-blocks [kb0, kb1): global loads of block kb+1 are in flight while block kb
+// is multiplied out of LDS.
+template <typename T, int BM, int BN, int BK, class LA, class LB>
+__device__ __forceinline__ void mma_loop(LA& la, LB& lb, int kb0, int kb1, T* sA, T* sB,
+                                         f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN]) {
+  if (kb0 >= kb1) return;
+  la.load(kb0);
+  lb.load(kb0);
+  for (int kb = kb0; kb < kb1; ++kb) {
+    __syncthreads();
+    la.store(sA);
+    lb.store(sB);
+    __syncthreads();
+    if (kb + 1 < kb1) {
+      la.load(kb + 1);
+      lb.load(kb + 1);
+    }
+    mma_block<T, BM, BN, BK>(sA, sB, acc);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Loaders. load(kb) fetches a k-block from global memory into registers,
+// store(s) writes it to LDS as [row][k] (k contiguous, row stride LDK).
+// ---------------------------------------------------------------------------
+// Row-major operand with k contiguous: element (row, k) = base[row*ld + k].
+template <typename T, int ROWS, int BK>
+struct RowLoader {
+  static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / 256, LDK = BK + VEC;
+  static_assert(ROWS * VPR % 256 == 0, "tile too small for 256 threads");
+  const T* base;
+  int64_t ld;
+  int rows_valid, K;
+  u32x4 r[NV];
+  __device__ void load(int kb) {
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int v = threadIdx.x + 256 * s, row = v / VPR, k = kb * BK + (v % VPR) * VEC;
+      if (row < rows_valid && k < K) {
+        r[s] = *(const u32x4*)(base + row * ld + k);
+        if (k + VEC > K) vmask_tail<T>(r[s], K - k);
+      } else {
+        r[s] = zero4();
+      }
+    }
+  }
+  __device__ void store(T* sm) const {
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int v = threadIdx.x + 256 * s;
+      *(u32x4*)(sm + (v / VPR) * LDK + (v % VPR) * VEC) = r[s];
+    }
+  }
+};
+
+// Decode a conv output pixel index into (n, y, x) (pool ordering: m = 4w + d).
+__device__ __forceinline__ void decode_out_pixel(const ConvProb& p, int m, int& n, int& y, int& x) {
+  if (p.pool) {
+    const int w = m >> 2, d = m & 3, pp = p.PH * p.PW;
+    n = w / pp;
+    const int rem = w - n * pp, ph = rem / p.PW, pw = rem - ph * p.PW;
+    y = 2 * ph + (d >> 1);
+    x = 2 * pw + (d & 1);
+  } else {
+    const int pp = p.OH * p.OW;
+    n = m / pp;
+    const int rem = m - n * pp;
+    y = rem / p.OW;
+    x = rem - y * p.OW;
+  }
+}
+
+// Conv forward A operand: rows = output pixels, k = (u, v, c).
+template <typename T, int ROWS, int BK>
+struct Im2colLoader {
+  static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / 256, LDK = BK + VEC;
+  const ConvProb* p;
+  const T* X;
+  int rn[NV], ry[NV], rx[NV];
+  u32x4 r[NV];
+  __device__ void init(const ConvProb& pr, int m0) {
+    p = &pr;
+    X = (const T*)pr.X;
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int m = m0 + (threadIdx.x + 256 * s) / VPR;
+      if (m < pr.M) decode_out_pixel(pr, m, rn[s], ry[s], rx[s]);
+      else rn[s] = -1;
+    }
+  }
+  __device__ void load(int kb) {
+    const int C = p->C, H = p->H, W = p->W, KW = p->KH, pad = p->pad, K = p->K;
+    const bool vec = (C % VEC) == 0;
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int k0 = kb * BK + ((threadIdx.x + 256 * s) % VPR) * VEC;
+      u32x4 v = zero4();
+      if (rn[s] >= 0 && k0 < K) {
+        if (vec) {
+          const int t = k0 / C, c = k0 - t * C, u = t / KW, vv = t - u * KW;
+          const int y = ry[s] + u - pad, x = rx[s] + vv - pad;
+          if (y >= 0 && y < H && x >= 0 && x < W) v = *(const u32x4*)(X + ((int64_t)(rn[s] * H + y) * W + x) * C + c);
+        } else {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            const int k = k0 + e;
+            if (k < K) {
+              const int t = k / C, c = k - t * C, u = t / KW, vv = t - u * KW;
+              const int y = ry[s] + u - pad, x = rx[s] + vv - pad;
+              if (y >= 0 && y < H && x >= 0 && x < W)
+                vset_bits<T>(v, e, bits_of<T>(X[((int64_t)(rn[s] * H + y) * W + x) * C + c]));
+            }
+          }
+        }
+      }
+      r[s] = v;
+    }
+  }
+  __device__ void store(T* sm) const {
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int v = threadIdx.x + 256 * s;
+      *(u32x4*)(sm + (v / VPR) * LDK + (v % VPR) * VEC) = r[s];
+    }
+  }
+};
+
+// dZ[n, p, q, o] of a conv block, gathered from the (already ReLU'-masked)
+// gradient at the block output and, with pooling, the window argmax.
+// Returns false when (p, q) is outside the conv output or dropped by floor pooling.
+__device__ __forceinline__ bool dz_index(const ConvProb& pr, int n, int p, int q, int64_t& idx, int& d) {
+  if (p < 0 || q < 0 || p >= pr.OH || q >= pr.OW) return false;
+  if (pr.pool) {
+    if (p >= 2 * pr.PH || q >= 2 * pr.PW) return false;
+    idx = ((int64_t)(n * pr.PH + (p >> 1)) * pr.PW + (q >> 1)) * pr.O;
+    d = ((p & 1) << 1) | (q & 1);
+  } else {
+    idx = ((int64_t)(n * pr.OH + p) * pr.OW + q) * pr.O;
+    d = -1;
+  }
+  return true;
+}
+
+// VEC argmax bytes starting at a (VEC-aligned) offset.
+template <typename T> __device__ __forceinline__ uint64_t load_am(const uint8_t* a);
+template <> __device__ __forceinline__ uint64_t load_am<float>(const uint8_t* a) { return *(const uint32_t*)a; }
+template <> __device__ __forceinline__ uint64_t load_am<bf16_t>(const uint8_t* a) { return *(const uint64_t*)a; }
+
+// Keep element e of v only where its window argmax equals d.
+template <typename T> __device__ __forceinline__ void select_am(u32x4& v, uint64_t am, int d) {
+#pragma unroll
+  for (int e = 0; e < TT<T>::VEC; ++e)
+    if ((int)((am >> (8 * e)) & 0xffu) != d) vset_bits<T>(v, e, 0u);
+}
+
+// Conv dgrad A operand: rows = conv input pixels (n, y, x), k = (u, v, o).
+template <typename T, int ROWS, int BK>
+struct DzGatherLoader {
+  static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / 256, LDK = BK + VEC;
+  const ConvProb* p;
+  const T* G;
+  int rn[NV], ry[NV], rx[NV];
+  u32x4 r[NV];
+  __device__ void init(const ConvProb& pr, int m0) {
+    p = &pr;
+    G = (const T*)pr.G;
+    const int hw = pr.H * pr.W;
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int m = m0 + (threadIdx.x + 256 * s) / VPR;
+      if (m < pr.M) {
+        rn[s] = m / hw;
+        const int rem = m - rn[s] * hw;
+        ry[s] = rem / pr.W;
+        rx[s] = rem - ry[s] * pr.W;
+      } else {
+        rn[s] = -1;
+      }
+    }
+  }
+  __device__ void load(int kb) {
+    const int O = p->O, KW = p->KH, pad = p->pad, K = p->K;
+    const bool vec = (O % VEC) == 0;
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int k0 = kb * BK + ((threadIdx.x + 256 * s) % VPR) * VEC;
+      u32x4 v = zero4();
+      if (rn[s] >= 0 && k0 < K) {
+        if (vec) {
+          const int t = k0 / O, o = k0 - t * O, u = t / KW, vv = t - u * KW;
+          int64_t idx;
+          int d;
+          if (dz_index(*p, rn[s], ry[s] - u + pad, rx[s] - vv + pad, idx, d)) {
+            v = *(const u32x4*)(G + idx + o);
+            if (d >= 0) select_am<T>(v, load_am<T>(p->gam + idx + o), d);
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            const int k = k0 + e;
+            if (k < K) {
+              const int t = k / O, o = k - t * O, u = t / KW, vv = t - u * KW;
+              int64_t idx;
+              int d;
+              if (dz_index(*p, rn[s], ry[s] - u + pad, rx[s] - vv + pad, idx, d))
+                if (d < 0 || p->gam[idx + o] == d) vset_bits<T>(v, e, bits_of<T>(G[idx + o]));
+            }
+          }
+        }
+      }
+      r[s] = v;
+    }
+  }
+  __device__ void store(T* sm) const {
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int v = threadIdx.x + 256 * s;
+      *(u32x4*)(sm + (v / VPR) * LDK + (v % VPR) * VEC) = r[s];
+    }
+  }
+};
+
+// Conv wgrad A operand: rows = output channel o, k = output pixel.
+// Global vectors run along o; they are written to LDS transposed.
+template <typename T, int ROWS, int BK>
+struct DzRowsLoader {
+  static constexpr int VEC = TT<T>::VEC, VPM = ROWS / VEC, NV = ROWS * BK / VEC / 256, LDK = BK + VEC;
+  const ConvProb* p;
+  const T* G;
+  int m0;
+  u32x4 r[NV];
+  __device__ void init(const ConvProb& pr, int m0_) {
+    p = &pr;
+    G = (const T*)pr.G;
+    m0 = m0_;
+  }
+  __device__ void load(int kb) {
+    const int O = p->O;
+    const bool vec = (O % VEC) == 0;
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int v = threadIdx.x + 256 * s, ov = v % VPM, pix = kb * BK + v / VPM, o0 = m0 + ov * VEC;
+      u32x4 val = zero4();
+      if (pix < p->K && o0 < O) {
+        int64_t idx;
+        int d;
+        if (p->pool) {
+          idx = (int64_t)(pix >> 2) * O;
+          d = pix & 3;
+        } else {
+          idx = (int64_t)pix * O;
+          d = -1;
+        }
+        if (vec) {
+          val = *(const u32x4*)(G + idx + o0);
+          if (d >= 0) select_am<T>(val, load_am<T>(p->gam + idx + o0), d);
+        } else {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e)
+            if (o0 + e < O && (d < 0 || p->gam[idx + o0 + e] == d))
+              vset_bits<T>(val, e, bits_of<T>(G[idx + o0 + e]));
+        }
+      }
+      r[s] = val;
+    }
+  }
+  __device__ void store(T* sm) const {
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int v = threadIdx.x + 256 * s, ov = v % VPM, kp = v / VPM;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) sm[(ov * VEC + e) * LDK + kp] = tbits<T>(vbits<T>(r[s], e));
+    }
+  }
+};
+
+// Conv wgrad B operand: rows = j = (u, v, c) (+ the bias column j == KH*KW*C
+// reading 1), k = output pixel. Written to LDS transposed.
+template <typename T, int ROWS, int BK>
+struct PatchRowsLoader {
+  static constexpr int VEC = TT<T>::VEC, VPN = ROWS / VEC, NV = ROWS * BK / VEC / 256, LDK = BK + VEC;
+  const ConvProb* p;
+  const T* X;
+  int n0;
+  u32x4 r[NV];
+  __device__ void init(const ConvProb& pr, int n0_) {
+    p = &pr;
+    X = (const T*)pr.X;
+    n0 = n0_;
+  }
+  __device__ void load(int kb) {
+    const int C = p->C, H = p->H, W = p->W, KW = p->KH, pad = p->pad, J = p->KH * p->KH * C;
+    const bool vec = (C % VEC) == 0;
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int v = threadIdx.x + 256 * s, jv = v % VPN, pix = kb * BK + v / VPN, j0 = n0 + jv * VEC;
+      u32x4 val = zero4();
+      if (pix < p->K && j0 <= J) {
+        int n, y, x;
+        decode_out_pixel(*p, pix, n, y, x);
+        if (vec && j0 + VEC <= J) {
+          const int t = j0 / C, c = j0 - t * C, u = t / KW, vv = t - u * KW;
+          const int iy = y + u - pad, ix = x + vv - pad;
+          if (iy >= 0 && iy < H && ix >= 0 && ix < W) val = *(const u32x4*)(X + ((int64_t)(n * H + iy) * W + ix) * C + c);
+        } else {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            const int j = j0 + e;
+            if (j < J) {
+              const int t = j / C, c = j - t * C, u = t / KW, vv = t - u * KW;
+              const int iy = y + u - pad, ix = x + vv - pad;
+              if (iy >= 0 && iy < H && ix >= 0 && ix < W)
+                vset_bits<T>(val, e, bits_of<T>(X[((int64_t)(n * H + iy) * W + ix) * C + c]));
+            } else if (j == J) {
+              vset_bits<T>(val, e, bits_of<T>(TT<T>::from_f(1.0f)));
+            }
+          }
+        }
+      }
+      r[s] = val;
+    }
+  }
+  __device__ void store(T* sm) const {
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int v = threadIdx.x + 256 * s, jv = v % VPN, kp = v / VPN;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) sm[(jv * VEC + e) * LDK + kp] = tbits<T>(vbits<T>(r[s], e));
+    }
+  }
+};
+
+// ---------------------------------------------------------------------------
+// Grouped NT GEMM
+// ---------------------------------------------------------------------------
+template <typename T> __device__ __forceinline__ void store_t(void* base, int64_t idx, float v) {
+  ((T*)base)[idx] = TT<T>::from_f(v);
+}
+
+// Store 4 consecutive values (rows m..m+3 of one column) into a [n][m] array.
+template <typename T> __device__ __forceinline__ void store4_t(T* dst, const float (&v)[4], int nvalid) {
+  if (nvalid == 4) {
+    if constexpr (sizeof(T) == 2) {
+      u32x2 w;
+      w[0] = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+      w[1] = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+      *(u32x2*)dst = w;
+    } else {
+      *(f32x4*)dst = f32x4{v[0], v[1], v[2], v[3]};
+    }
+  } else {
+    for (int r = 0; r < nvalid; ++r) dst[r] = TT<T>::from_f(v[r]);
+  }
+}
+
+template <typename T, int BM, int BN, int BK>
+__global__ __launch_bounds__(256) void gemm_kernel(const GemmProb* __restrict__ probs,
+                                                   const int32_t* __restrict__ tile_prob) {
+  using TL = Tile<T, BM, BN, BK>;
+  __shared__ __attribute__((aligned(16))) T sA[TL::A_ELEMS];
+  __shared__ __attribute__((aligned(16))) T sB[TL::B_ELEMS];
+  const int tile = blockIdx.x;
+  const GemmProb& p = probs[tile_prob[tile]];
+  const int local = tile - p.tile_base;
+  const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  f32x4 acc[TL::FM][TL::FN];
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  RowLoader<T, BM, BK> la{(const T*)p.A + (int64_t)m0 * p.lda, p.lda, p.M - m0, p.K};
+  RowLoader<T, BN, BK> lb{(const T*)p.B + (int64_t)n0 * p.ldb, p.ldb, p.N - n0, p.K};
+  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, sA, sB, acc);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i) {
+    const int mb = m0 + wm + 16 * i + 4 * (lane >> 4);
+    if (mb >= p.M) continue;
+    const int nv = min(4, p.M - mb);
+#pragma unroll
+    for (int j = 0; j < TL::FN; ++j) {
+      const int n = n0 + wn + 16 * j + (lane & 15);
+      if (n >= p.N) continue;
+      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+      if (p.epi == EPI_FWD || p.epi == EPI_LOGITS) {
+        const float b = p.bias[n];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          v[r] += b;
+          if (p.relu) v[r] = fmaxf(v[r], 0.f);
+        }
+      } else if (p.epi == EPI_DGRAD && p.relu) {
+        const T* mk = (const T*)p.mask + (int64_t)n * p.ldmask + mb;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (r < nv && !(TT<T>::to_f(mk[r]) > 0.f)) v[r] = 0.f;
+      }
+      if (p.epi == EPI_WGRAD) {
+        if (n < p.nsplit) {
+          for (int r = 0; r < nv; ++r) ((float*)p.C)[(int64_t)(mb + r) * p.ldc + n] = v[r];
+        } else if (n == p.nsplit) {
+          for (int r = 0; r < nv; ++r) p.dbias[mb + r] = v[r];
+        }
+      } else if (p.epi == EPI_LOGITS) {
+        for (int r = 0; r < nv; ++r) ((float*)p.C)[(int64_t)(mb + r) * p.ldc + n] = v[r];
+      } else {
+        if (p.C)
+          for (int r = 0; r < nv; ++r) store_t<T>(p.C, (int64_t)(mb + r) * p.ldc + n, v[r]);
+        if (p.CT) store4_t<T>((T*)p.CT + (int64_t)n * p.ldct + mb, v, nv);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Convolution passes
+// ---------------------------------------------------------------------------
+template <typename T, int BM, int BN, int BK>
+__global__ __launch_bounds__(256) void conv_fwd_kernel(const ConvProb* __restrict__ probs,
+                                                       const int32_t* __restrict__ tile_prob) {
+  using TL = Tile<T, BM, BN, BK>;
+  __shared__ __attribute__((aligned(16))) T sA[TL::A_ELEMS];
+  __shared__ __attribute__((aligned(16))) T sB[TL::B_ELEMS];
+  const int tile = blockIdx.x;
+  const ConvProb& p = probs[tile_prob[tile]];
+  const int local = tile - p.tile_base;
+  const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  f32x4 acc[TL::FM][TL::FN];
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  Im2colLoader<T, BM, BK> la;
+  la.init(p, m0);
+  RowLoader<T, BN, BK> lb{(const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K};
+  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, sA, sB, acc);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
+  const int O = p.O;
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i) {
+    const int mb = m0 + wm + 16 * i + 4 * (lane >> 4);
+    if (mb >= p.M) continue;
+#pragma unroll
+    for (int j = 0; j < TL::FN; ++j) {
+      const int o = n0 + wn + 16 * j + (lane & 15);
+      if (o >= O) continue;
+      const float b = p.bias[o];
+      float v[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        v[r] = acc[i][j][r] + b;
+        if (p.relu) v[r] = fmaxf(v[r], 0.f);
+      }
+      if (p.pool) {
+        // rows mb..mb+3 are one 2x2 window; the first maximum in (dy,dx) order wins
+        int am = 0;
+        float mx = v[0];
+#pragma unroll
+        for (int r = 1; r < 4; ++r)
+          if (v[r] > mx) {
+            mx = v[r];
+            am = r;
+          }
+        const int w = mb >> 2;
+        store_t<T>(p.P, (int64_t)w * O + o, mx);
+        p.amax[(int64_t)w * O + o] = (uint8_t)am;
+        if (p.PT) {
+          const int pp = p.PH * p.PW, n = w / pp, s = w - n * pp;
+          store_t<T>(p.PT, (int64_t)(s * O + o) * p.ldpt + n, mx);
+        }
+      } else {
+        const int nv = min(4, p.M - mb), pp = p.OH * p.OW;
+        for (int r = 0; r < nv; ++r) {
+          const int m = mb + r;
+          store_t<T>(p.P, (int64_t)m * O + o, v[r]);
+          if (p.PT) {
+            const int n = m / pp, s = m - n * pp;
+            store_t<T>(p.PT, (int64_t)(s * O + o) * p.ldpt + n, v[r]);
+          }
+        }
+      }
+    }
+  }
+}
+
+template <typename T, int BM, int BN, int BK>
+__global__ __launch_bounds__(256) void conv_dgrad_kernel(const ConvProb* __restrict__ probs,
+                                                         const int32_t* __restrict__ tile_prob) {
+  using TL = Tile<T, BM, BN, BK>;
+  __shared__ __attribute__((aligned(16))) T sA[TL::A_ELEMS];
+  __shared__ __attribute__((aligned(16))) T sB[TL::B_ELEMS];
+  const int tile = blockIdx.x;
+  const ConvProb& p = probs[tile_prob[tile]];
+  const int local = tile - p.tile_base;
+  const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  f32x4 acc[TL::FM][TL::FN];
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  DzGatherLoader<T, BM, BK> la;
+  la.init(p, m0);
+  RowLoader<T, BN, BK> lb{(const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K};
+  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, sA, sB, acc);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
+  const int C = p.C;
+  const T* X = (const T*)p.X;
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i) {
+    const int mb = m0 + wm + 16 * i + 4 * (lane >> 4);
+    if (mb >= p.M) continue;
+    const int nv = min(4, p.M - mb);
+#pragma unroll
+    for (int j = 0; j < TL::FN; ++j) {
+      const int c = n0 + wn + 16 * j + (lane & 15);
+      if (c >= C) continue;
+      for (int r = 0; r < nv; ++r) {
+        float v = acc[i][j][r];
+        const int64_t idx = (int64_t)(mb + r) * C + c;
+        if (p.prev_relu && !(TT<T>::to_f(X[idx]) > 0.f)) v = 0.f;
+        store_t<T>(p.Gprev, idx, v);
+      }
+    }
+  }
+}
+
+template <typename T, int BM, int BN, int BK>
+__global__ __launch_bounds__(256) void conv_wgrad_kernel(const ConvProb* __restrict__ probs,
+                                                         const int32_t* __restrict__ tile_prob) {
+  using TL = Tile<T, BM, BN, BK>;
+  __shared__ __attribute__((aligned(16))) T sA[TL::A_ELEMS];
+  __shared__ __attribute__((aligned(16))) T sB[TL::B_ELEMS];
+  const int tile = blockIdx.x;
+  const ConvProb& p = probs[tile_prob[tile]];
+  int local = tile - p.tile_base;
+  const int per_split = p.tiles_m * p.tiles_n;
+  const int split = local / per_split;
+  local -= split * per_split;
+  const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  f32x4 acc[TL::FM][TL::FN];
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  DzRowsLoader<T, BM, BK> la;
+  la.init(p, m0);
+  PatchRowsLoader<T, BN, BK> lb;
+  lb.init(p, n0);
+  const int nkb = (p.K + BK - 1) / BK;
+  const int kb0 = split * p.kchunk, kb1 = min(nkb, kb0 + p.kchunk);
+  mma_loop<T, BM, BN, BK>(la, lb, kb0, kb1, sA, sB, acc);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
+  float* ws = p.ws + (int64_t)split * p.O * p.ldws;
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i) {
+    const int mb = m0 + wm + 16 * i + 4 * (lane >> 4);
+    if (mb >= p.M) continue;
+    const int nv = min(4, p.M - mb);
+#pragma unroll
+    for (int j = 0; j < TL::FN; ++j) {
+      const int n = n0 + wn + 16 * j + (lane & 15);
+      if (n >= p.N) continue;
+      for (int r = 0; r < nv; ++r) ws[(int64_t)(mb + r) * p.ldws + n] = acc[i][j][r];
+    }
+  }
+}
+
+// Sum the split-K partials in split order: dW[o][j] for j < J, db[o] for j == J.
+__global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* __restrict__ probs,
+                                                              const int32_t* __restrict__ blk_prob) {
+  const ReduceProb& p = probs[blk_prob[blockIdx.x]];
+  const int64_t e = (int64_t)(blockIdx.x - p.blk_base) * REDUCE_BLOCK + threadIdx.x;
+  const int J1 = p.J + 1;
+  if (e >= (int64_t)p.O * J1) return;
+  const int o = (int)(e / J1), j = (int)(e - (int64_t)o * J1);
+  float s = 0.f;
+  for (int k = 0; k < p.splits; ++k) s += p.ws[((int64_t)k * p.O + o) * p.ldws + j];
+  if (j < p.J) p.gW[(int64_t)o * p.ldgw + j] = s;
+  else p.gb[o] = s;
+}
+
+// ---------------------------------------------------------------------------
+// Softmax cross-entropy, one workgroup per model.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void ce_kernel(const CeProb* __restrict__ probs, const int32_t* __restrict__ y,
+                                                 int B, float* __restrict__ losses) {
+  __shared__ float rowloss[CE_MAX_BATCH];
+  __shared__ float part[256];
+  const CeProb& p = probs[blockIdx.x];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const float invB = 1.0f / (float)B;
+  for (int b = wave; b < B; b += 4) {
+    const float* z = p.logits + (int64_t)b * p.ldl;
+    float mx = -INFINITY;
+    for (int c = lane; c < p.C; c += 64) mx = fmaxf(mx, z[c]);
+    mx = wave_max(mx);
+    float s = 0.f;
+    for (int c = lane; c < p.C; c += 64) s += expf(z[c] - mx);
+    s = wave_sum(s);
+    const int yb = y[b];
+    if (lane == 0) rowloss[b] = mx + logf(s) - z[yb];
+    const float inv_s = 1.0f / s;
+    for (int c = lane; c < p.C; c += 64) {
+      const float g = (expf(z[c] - mx) * inv_s - (c == yb ? 1.f : 0.f)) * invB;
+      if (p.G) ((T*)p.G)[(int64_t)b * p.ldg + c] = TT<T>::from_f(g);
+      if (p.GT) ((T*)p.GT)[(int64_t)c * p.ldgt + b] = TT<T>::from_f(g);
+    }
+  }
+  __syncthreads();
+  float s = 0.f;
+  for (int b = threadIdx.x; b < B; b += 256) s += rowloss[b];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if (threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) losses[p.model] = part[0] * invB;
+}
+
+// ---------------------------------------------------------------------------
+// Multi-tensor SGD (64x64 tiles; the transposed copy goes through LDS).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void sgd_kernel(const SgdTensor* __restrict__ ts,
+                                                  const int32_t* __restrict__ tile_tensor, float lr, int use_grad) {
+  __shared__ float sm[SGD_TILE][SGD_TILE + 1];
+  const SgdTensor& t = ts[tile_tensor[blockIdx.x]];
+  const int local = blockIdx.x - t.tile_base;
+  const int per_tap = t.tiles_r * t.tiles_c;
+  const int j = local / per_tap, rem = local - j * per_tap;
+  const int tr = rem / t.tiles_c, tc = rem - tr * t.tiles_c;
+  const int r0 = tr * SGD_TILE, c0 = tc * SGD_TILE;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const int rl = ty + 16 * s, r = r0 + rl;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int cl = 4 * tx + e, c = c0 + cl;
+      if (r < t.R && c < t.Cc) {
+        const int64_t idx = (int64_t)r * t.ldw + (int64_t)j * t.Cc + c;
+        float w = t.W[idx];
+        if (use_grad) {
+          w = fmaf(-lr, t.G[idx], w);
+          t.W[idx] = w;
+        }
+        if (t.Wb) ((bf16_t*)t.Wb)[idx] = f2bf(w);
+        sm[rl][cl] = w;
+      }
+    }
+  }
+  if (!t.WT) return;
+  __syncthreads();
+  // WT[c][j*R + r]: consecutive threads take consecutive r for coalescing
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const int cl = ty + 16 * s, c = c0 + cl;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int rl = 4 * tx + e, r = r0 + rl;
+      if (r < t.R && c < t.Cc) store_t<T>(t.WT, (int64_t)c * t.ldwt + (int64_t)j * t.R + r, sm[rl][cl]);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Batch load: fp32 NCHW -> storage-type NHWC (+ transposed [(h*W+w)*C + c][b]).
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, int B, int C, int H, int W,
+                                                   T* __restrict__ X, T* __restrict__ XT, int64_t ldxt) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total = (int64_t)B * C * H * W;
+  if (e >= total) return;
+  const int hw = H * W;
+  const int64_t b = e / ((int64_t)C * hw);
+  const int rem = (int)(e - b * C * hw);
+  const int c = rem / hw, s = rem - c * hw;
+  const T v = TT<T>::from_f(x[e]);
+  X[(b * hw + s) * C + c] = v;
+  if (XT) XT[(int64_t)(s * C + c) * ldxt + b] = v;
+}
+
+// ---------------------------------------------------------------------------
+// Launch wrappers
+// ---------------------------------------------------------------------------
+hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_prob, int ntiles, hipStream_t s) {
+  if (ntiles <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, 64>), dim3(ntiles), dim3(256), 0, s, probs,
+                       tile_prob);
+  else
+    hipLaunchKernelGGL((gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, 32>), dim3(ntiles), dim3(256), 0, s, probs,
+                       tile_prob);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles, hipStream_t s) {
+  if (ntiles <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL((conv_fwd_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>), dim3(ntiles), dim3(256),
+                       0, s, probs, tile_prob);
+  else
+    hipLaunchKernelGGL((conv_fwd_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32>), dim3(ntiles), dim3(256), 0,
+                       s, probs, tile_prob);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles, hipStream_t s) {
+  if (ntiles <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL((conv_dgrad_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>), dim3(ntiles),
+                       dim3(256), 0, s, probs, tile_prob);
+  else
+    hipLaunchKernelGGL((conv_dgrad_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32>), dim3(ntiles), dim3(256),
+                       0, s, probs, tile_prob);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_wgrad(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles, hipStream_t s) {
+  if (ntiles <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL((conv_wgrad_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>), dim3(ntiles),
+                       dim3(256), 0, s, probs, tile_prob);
+  else
+    hipLaunchKernelGGL((conv_wgrad_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32>), dim3(ntiles), dim3(256),
+                       0, s, probs, tile_prob);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce(const ReduceProb* probs, const int32_t* blk_prob, int nblocks, hipStream_t s) {
+  if (nblocks <= 0) return hipSuccess;
+  hipLaunchKernelGGL(reduce_kernel, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob);
+  return hipGetLastError();
+}
+
+hipError_t launch_ce(bool bf16, const CeProb* probs, int nmodels, const int32_t* labels, int B, float* losses,
+                     hipStream_t s) {
+  if (nmodels <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL(ce_kernel<bf16_t>, dim3(nmodels), dim3(256), 0, s, probs, labels, B, losses);
+  else
+    hipLaunchKernelGGL(ce_kernel<float>, dim3(nmodels), dim3(256), 0, s, probs, labels, B, losses);
+  return hipGetLastError();
+}
+
+hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int ntiles, float lr,
+                      bool use_grad, hipStream_t s) {
+  if (ntiles <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL(sgd_kernel<bf16_t>, dim3(ntiles), dim3(256), 0, s, t, tile_tensor, lr, (int)use_grad);
+  else
+    hipLaunchKernelGGL(sgd_kernel<float>, dim3(ntiles), dim3(256), 0, s, t, tile_tensor, lr, (int)use_grad);
+  return hipGetLastError();
+}
+
+hipError_t launch_load(bool bf16, const float* x, int B, int C, int H, int W, void* X, void* XT, int64_t ldxt,
+                       hipStream_t s) {
+  const int64_t total = (int64_t)B * C * H * W;
+  const int blocks = (int)((total + 255) / 256);
+  if (blocks <= 0) return hipSuccess;
+  if (bf16)
+    hipLaunchKernelGGL(load_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, x, B, C, H, W, (bf16_t*)X, (bf16_t*)XT,
+                       ldxt);
+  else
+    hipLaunchKernelGGL(load_kernel<float>, dim3(blocks), dim3(256), 0, s, x, B, C, H, W, (float*)X, (float*)XT,
+                       ldxt);
+  return hipGetLastError();
+}
+
+}  // namespace un

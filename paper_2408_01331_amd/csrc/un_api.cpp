@@ -1,0 +1,1249 @@
+// Host side of the fused N-model training step: spec validation, the planner
+// (fused blocks, depth-level schedule, one device arena, device descriptor
+// tables), the step executor and the C ABI declared in unifiednn.h.
+//
+// Plan overview (UnifiedNN, Model Unifier, Algorithm 1: the hybrid is the
+// disjoint union of the sub-models' graphs with one global input):
+//   * every parameterised layer plus the ReLU / MaxPool that follow it becomes
+//     one fused block; block j of every model forms depth level j;
+//   * a step (Trainer, Algorithm 2) is: forward levels 0..L-1, one softmax-CE
+//     launch for all models, backward levels L-1..0 (dgrad and wgrad of one
+//     level share a launch), one multi-tensor SGD launch;
+//   * the first hidden Linear layers of all models read the same input, so
+//     their weights live in one concatenated matrix and run as ONE GEMM.
+#include "../../include/unifiednn.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "internal.h"
+
+using namespace un;
+
+namespace {
+
+constexpr size_t NONE = ~(size_t)0;
+
+inline int64_t rup(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+struct Block {
+  int kind = 0;  // 0 linear, 1 conv
+  int level = 0, model = 0;
+  bool relu = false, pool = false, last = false, prev_relu = false, concat = false;
+  bool next_linear = false;  // the following block is a Linear (needs transposed output)
+  // linear
+  int K = 0, N = 0;
+  int in_c = 0, in_h = 1, in_w = 1;  // input viewed as an image (Flatten order mapping)
+  // conv
+  int C = 0, H = 0, W = 0, O = 0, KH = 0, pad = 0, OH = 0, OW = 0, PH = 0, PW = 0;
+  // PyTorch-layout offsets in the model's flat parameter vector
+  size_t pt_w = 0, pt_b = 0, n_w = 0, n_b = 0;
+  // arena offsets (NONE = absent)
+  size_t W32 = NONE, b32 = NONE, gW = NONE, gb = NONE, Wb = NONE, WT = NONE;
+  int64_t ldw = 0, ldwt = 0;
+  int rows = 0;            // logical weight rows (N or O)
+  size_t X = NONE, XT = NONE;
+  int64_t ldx = 0, ldxt = 0;
+  size_t Y = NONE, YT = NONE, amax = NONE;
+  int64_t ldy = 0, ldyt = 0;
+  size_t G = NONE, GT = NONE;
+  int64_t ldg = 0, ldgt = 0;
+  size_t ws = NONE;
+  int64_t ldws = 0;
+  int splits = 1, kchunk = 0;
+  // output geometry
+  int out_elems_per_sample() const { return kind == 0 ? N : (pool ? PH * PW * O : OH * OW * O); }
+};
+
+struct Model {
+  std::vector<Block> blocks;
+  int num_classes = 0;
+  size_t n_params = 0;
+  uint64_t seed = 0;
+};
+
+struct Launch {
+  int kind;   // 0 gemm, 1 conv fwd, 2 conv dgrad, 3 conv wgrad, 4 reduce, 5 ce, 6 sgd
+  int kclass;
+  size_t probs, map;  // arena offsets
+  int count;
+};
+
+struct EventRec {
+  int kclass;
+  hipEvent_t a, b;
+};
+
+thread_local std::string g_create_error;
+
+}  // namespace
+
+struct un_ctx {
+  bool bf16 = false;
+  int B = 0, in_c = 0, in_h = 0, in_w = 0;
+  int64_t Bp = 0;
+  std::vector<Model> models;
+  int levels = 0;
+  // arena
+  char* base = nullptr;
+  size_t bytes = 0;
+  hipStream_t stream = nullptr;
+  // fixed buffers
+  size_t xstage = NONE, ydev = NONE, losses_dev = NONE, Xin = NONE, XinT = NONE;
+  int64_t ldxin = 0, ldxint = 0;
+  // schedule
+  std::vector<Launch> fwd, bwd;
+  Launch ce{}, sgd{}, refresh{};
+  int ce_count = 0;
+  bool loaded = false, stepped = false, poisoned = false;
+  int min_classes = 0;
+  std::string err;
+  // profiling
+  bool profiling = false;
+  std::vector<EventRec> recs;
+  std::vector<hipEvent_t> free_events;
+  double prof_ms[UN_K_COUNT] = {0};
+  int64_t prof_n[UN_K_COUNT] = {0};
+
+  template <class T> T* at(size_t off) const { return off == NONE ? nullptr : (T*)(base + off); }
+};
+
+namespace {
+
+un_status fail(un_ctx* c, un_status s, const std::string& msg) {
+  if (c) c->err = msg;
+  else g_create_error = msg;
+  return s;
+}
+
+#define HIPCHK(ctx, expr)                                                                   \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess) {                                                                 \
+      (ctx)->poisoned = true;                                                               \
+      return fail((ctx), UN_ERR_DEVICE, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+    }                                                                                       \
+  } while (0)
+
+// --------------------------------------------------------------------------
+// Spec parsing
+// --------------------------------------------------------------------------
+un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, Model& m, std::string& why) {
+  if (s.n_layers <= 0 || !s.layers) {
+    why = "model " + std::to_string(mi) + ": no layers";
+    return UN_ERR_INVALID;
+  }
+  if (s.num_classes <= 0) {
+    why = "model " + std::to_string(mi) + ": num_classes must be positive";
+    return UN_ERR_INVALID;
+  }
+  m.num_classes = s.num_classes;
+  m.seed = s.init_seed;
+  // current shape: image (c, h, w) or flat (f); flat keeps the image it came from
+  // The input is an image [c, h, w]; a Linear may read it directly only when
+  // h = w = 1. After a Flatten or a Linear the tensor is flat.
+  int c = in.in_c, h = in.in_h, w = in.in_w;
+  bool flat = false;
+  size_t pt = 0;
+  int i = 0;
+  auto where = [&](int li) { return "model " + std::to_string(mi) + " layer " + std::to_string(li) + ": "; };
+  while (i < s.n_layers) {
+    const un_layer& L = s.layers[i];
+    if (L.op == UN_CONV2D) {
+      if (flat) {
+        why = where(i) + "conv needs an image input (got a flat tensor)";
+        return UN_ERR_INVALID;
+      }
+      if (L.out <= 0 || L.kernel <= 0 || L.pad < 0) {
+        why = where(i) + "bad conv parameters";
+        return UN_ERR_INVALID;
+      }
+      Block b;
+      b.kind = 1;
+      b.C = c;
+      b.H = h;
+      b.W = w;
+      b.O = L.out;
+      b.KH = L.kernel;
+      b.pad = L.pad;
+      b.OH = h + 2 * L.pad - L.kernel + 1;
+      b.OW = w + 2 * L.pad - L.kernel + 1;
+      if (b.OH <= 0 || b.OW <= 0) {
+        why = where(i) + "kernel larger than padded input";
+        return UN_ERR_INVALID;
+      }
+      b.n_w = (size_t)b.O * c * L.kernel * L.kernel;
+      b.n_b = b.O;
+      b.pt_w = pt;
+      b.pt_b = pt + b.n_w;
+      pt += b.n_w + b.n_b;
+      ++i;
+      if (i < s.n_layers && s.layers[i].op == UN_RELU) {
+        b.relu = true;
+        ++i;
+      }
+      if (i < s.n_layers && s.layers[i].op == UN_MAXPOOL2) {
+        b.pool = true;
+        b.PH = b.OH / 2;
+        b.PW = b.OW / 2;
+        if (b.PH <= 0 || b.PW <= 0) {
+          why = where(i) + "max-pool of a map smaller than 2x2";
+          return UN_ERR_INVALID;
+        }
+        ++i;
+      }
+      c = b.O;
+      h = b.pool ? b.PH : b.OH;
+      w = b.pool ? b.PW : b.OW;
+      flat = false;
+      m.blocks.push_back(b);
+    } else if (L.op == UN_LINEAR) {
+      if (!flat && !(h == 1 && w == 1)) {
+        why = where(i) + "linear on an image needs a flatten first";
+        return UN_ERR_INVALID;
+      }
+      if (L.out <= 0) {
+        why = where(i) + "bad linear out";
+        return UN_ERR_INVALID;
+      }
+      Block b;
+      b.kind = 0;
+      b.in_c = c;
+      b.in_h = h;
+      b.in_w = w;
+      b.K = c * h * w;
+      b.N = L.out;
+      b.n_w = (size_t)b.N * b.K;
+      b.n_b = b.N;
+      b.pt_w = pt;
+      b.pt_b = pt + b.n_w;
+      pt += b.n_w + b.n_b;
+      ++i;
+      if (i < s.n_layers && s.layers[i].op == UN_RELU) {
+        b.relu = true;
+        ++i;
+      }
+      c = b.N;
+      h = w = 1;
+      flat = true;
+      m.blocks.push_back(b);
+    } else if (L.op == UN_FLATTEN) {
+      flat = true;  // keep (c, h, w): the next Linear maps NCHW order onto NHWC storage
+      ++i;
+    } else if (L.op == UN_RELU || L.op == UN_MAXPOOL2) {
+      why = where(i) + "ReLU/MaxPool2 must directly follow a Conv2d/Linear (ReLU) or Conv2d[+ReLU] (pool)";
+      return UN_ERR_UNSUPPORTED;
+    } else {
+      why = where(i) + "unknown op " + std::to_string(L.op);
+      return UN_ERR_INVALID;
+    }
+  }
+  if (m.blocks.empty() || m.blocks.back().kind != 0) {
+    why = "model " + std::to_string(mi) + ": the last parameterised layer must be Linear";
+    return UN_ERR_UNSUPPORTED;
+  }
+  Block& last = m.blocks.back();
+  if (last.relu) {
+    why = "model " + std::to_string(mi) + ": ReLU on the logits is not supported";
+    return UN_ERR_UNSUPPORTED;
+  }
+  if (last.N != s.num_classes) {
+    why = "model " + std::to_string(mi) + ": last Linear out != num_classes";
+    return UN_ERR_INVALID;
+  }
+  last.last = true;
+  for (size_t j = 0; j < m.blocks.size(); ++j) {
+    Block& b = m.blocks[j];
+    b.level = (int)j;
+    b.model = mi;
+    b.prev_relu = j > 0 && m.blocks[j - 1].relu;
+    b.next_linear = j + 1 < m.blocks.size() && m.blocks[j + 1].kind == 0;
+    if (j + 1 < m.blocks.size() && m.blocks[j + 1].kind == 1 && b.kind == 0) {
+      why = "model " + std::to_string(mi) + ": Conv2d after Linear is not supported";
+      return UN_ERR_UNSUPPORTED;
+    }
+    if (b.kind == 1 && b.next_linear && (b.out_elems_per_sample() % 8) != 0) {
+      why = "model " + std::to_string(mi) + ": flattened conv output must be a multiple of 8 features";
+      return UN_ERR_UNSUPPORTED;
+    }
+  }
+  m.n_params = pt;
+  return UN_OK;
+}
+
+// --------------------------------------------------------------------------
+// Arena
+// --------------------------------------------------------------------------
+struct Arena {
+  size_t top = 0;
+  size_t take(size_t bytes) {
+    size_t off = rup((int64_t)top, 256);
+    top = off + rup((int64_t)std::max<size_t>(bytes, 1), 256);
+    return off;
+  }
+};
+
+// splitmix64: counter-based generator of the library's own initialisation.
+inline uint64_t splitmix(uint64_t x) {
+  x += 0x9E3779B97F4A7C15ull;
+  x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
+  x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
+  return x ^ (x >> 31);
+}
+
+}  // namespace
+
+// ==========================================================================
+// Planner
+// ==========================================================================
+static un_status plan_and_alloc(un_ctx* c) {
+  const bool bf = c->bf16;
+  const size_t es = bf ? 2 : 4;  // storage element size
+  const int B = c->B;
+  const int64_t Bp = c->Bp;
+  Arena A;
+  const int64_t in_feat = (int64_t)c->in_c * c->in_h * c->in_w;
+
+  c->xstage = A.take((size_t)B * in_feat * 4);
+  c->ydev = A.take((size_t)B * 4);
+  c->losses_dev = A.take(c->models.size() * 4);
+  c->Xin = A.take((size_t)B * in_feat * es);
+  c->ldxin = in_feat;
+  bool any_linear0 = false;
+  for (auto& m : c->models)
+    if (m.blocks[0].kind == 0) any_linear0 = true;
+  if (any_linear0) {
+    if (in_feat % 8 != 0) return fail(nullptr, UN_ERR_UNSUPPORTED, "input features must be a multiple of 8 when a model starts with Linear");
+    c->ldxint = Bp;
+    c->XinT = A.take((size_t)(in_feat + 1) * Bp * es);
+  }
+
+  // --- level-0 concatenation group: hidden Linear + ReLU reading the shared input
+  std::vector<int> cat;  // model indices
+  for (size_t i = 0; i < c->models.size(); ++i) {
+    const Block& b = c->models[i].blocks[0];
+    if (b.kind == 0 && !b.last && b.relu) cat.push_back((int)i);
+  }
+  std::vector<int64_t> cat_off(c->models.size(), -1);
+  int64_t cat_rows = 0;
+  for (int i : cat) {
+    cat_off[i] = cat_rows;
+    cat_rows += rup(c->models[i].blocks[0].N + 1, 8);  // >= 1 spare row: the ones row of YT
+  }
+  const int64_t kin_p = rup(in_feat, 8);
+  size_t catW32 = NONE, catb32 = NONE, catgW = NONE, catgb = NONE, catWb = NONE, catY = NONE, catYT = NONE,
+         catGT = NONE;
+  if (!cat.empty()) {
+    catW32 = A.take((size_t)cat_rows * kin_p * 4);
+    catb32 = A.take((size_t)cat_rows * 4);
+    catgW = A.take((size_t)cat_rows * kin_p * 4);
+    catgb = A.take((size_t)cat_rows * 4);
+    if (bf) catWb = A.take((size_t)cat_rows * kin_p * 2);
+    catY = A.take((size_t)B * cat_rows * es);
+    catYT = A.take((size_t)cat_rows * Bp * es);
+    catGT = A.take((size_t)cat_rows * Bp * es);
+  }
+
+  // --- per block buffers
+  int levels = 0;
+  for (size_t mi = 0; mi < c->models.size(); ++mi) {
+    Model& m = c->models[mi];
+    levels = std::max(levels, (int)m.blocks.size());
+    for (size_t j = 0; j < m.blocks.size(); ++j) {
+      Block& b = m.blocks[j];
+      if (b.kind == 0) {
+        b.rows = b.N;
+        b.ldw = rup(b.K, 8);
+        if (j == 0 && cat_off[mi] >= 0) {
+          b.concat = true;
+          const size_t roff = (size_t)cat_off[mi];
+          b.W32 = catW32 + roff * b.ldw * 4;
+          b.b32 = catb32 + roff * 4;
+          b.gW = catgW + roff * b.ldw * 4;
+          b.gb = catgb + roff * 4;
+          if (bf) b.Wb = catWb + roff * b.ldw * 2;
+          b.ldy = cat_rows;
+          b.Y = catY + roff * es;
+          b.ldyt = Bp;
+          b.YT = catYT + roff * Bp * es;
+          b.ldgt = Bp;
+          b.GT = catGT + roff * Bp * es;
+        } else {
+          b.W32 = A.take((size_t)b.N * b.ldw * 4);
+          b.b32 = A.take((size_t)b.N * 4);
+          b.gW = A.take((size_t)b.N * b.ldw * 4);
+          b.gb = A.take((size_t)b.N * 4);
+          if (bf) b.Wb = A.take((size_t)b.N * b.ldw * 2);
+          if (b.last) {
+            b.ldy = rup(b.N, 8);
+            b.Y = A.take((size_t)B * b.ldy * 4);  // fp32 logits
+          } else {
+            b.ldy = rup(b.N, 8);
+            b.Y = A.take((size_t)B * b.ldy * es);
+            b.ldyt = Bp;
+            b.YT = A.take((size_t)(b.N + 1) * Bp * es);  // + ones row
+          }
+          b.ldg = rup(b.N, 8);
+          if (j > 0) b.G = A.take((size_t)B * b.ldg * es);
+          b.ldgt = Bp;
+          b.GT = A.take((size_t)b.N * Bp * es);
+        }
+        if (j > 0) {
+          b.ldwt = rup(b.N, 8);
+          b.WT = A.take((size_t)b.K * b.ldwt * es);
+        }
+      } else {
+        const int J = b.KH * b.KH * b.C;
+        b.rows = b.O;
+        b.ldw = rup(J, 8);
+        b.W32 = A.take((size_t)b.O * b.ldw * 4);
+        b.b32 = A.take((size_t)b.O * 4);
+        b.gW = A.take((size_t)b.O * b.ldw * 4);
+        b.gb = A.take((size_t)b.O * 4);
+        if (bf) b.Wb = A.take((size_t)b.O * b.ldw * 2);
+        if (j > 0) {
+          b.ldwt = rup((int64_t)b.KH * b.KH * b.O, 8);
+          b.WT = A.take((size_t)b.C * b.ldwt * es);
+        }
+        const int64_t npix = (int64_t)B * (b.pool ? b.PH * b.PW : b.OH * b.OW);
+        b.Y = A.take((size_t)npix * b.O * es);
+        b.ldy = b.O;
+        if (b.pool) b.amax = A.take((size_t)npix * b.O);
+        if (b.next_linear) {
+          b.ldyt = Bp;
+          b.YT = A.take((size_t)(b.out_elems_per_sample() + 1) * Bp * es);
+        }
+        b.G = A.take((size_t)npix * b.O * es);
+        b.ldg = b.O;
+        // split-K of the weight gradient: depends only on this block's shape
+        const int BK = bf ? CONV_BK_BF16 : CONV_BK_F32;
+        const int BMc = bf ? CONV_BM_BF16 : CONV_BM_F32, BNc = bf ? CONV_BN_BF16 : CONV_BN_F32;
+        const int64_t kpix = b.pool ? (int64_t)B * b.PH * b.PW * 4 : (int64_t)B * b.OH * b.OW;
+        const int nkb = cdiv(kpix, BK);
+        const int tiles = cdiv(b.O, BMc) * cdiv(J + 1, BNc);
+        int splits = std::max(1, std::min(nkb, cdiv(1024, tiles)));
+        b.kchunk = cdiv(nkb, splits);
+        b.splits = cdiv(nkb, b.kchunk);
+        b.ldws = rup(J + 1, 4);
+        b.ws = A.take((size_t)b.splits * b.O * b.ldws * 4);
+      }
+    }
+    // wire inputs
+    for (size_t j = 0; j < m.blocks.size(); ++j) {
+      Block& b = m.blocks[j];
+      if (j == 0) {
+        b.X = c->Xin;
+        b.ldx = c->ldxin;
+        b.XT = c->XinT;
+        b.ldxt = c->ldxint;
+      } else {
+        Block& p = m.blocks[j - 1];
+        b.X = p.Y;
+        b.ldx = p.kind == 0 ? p.ldy : p.out_elems_per_sample();
+        b.XT = p.YT;
+        b.ldxt = p.ldyt;
+      }
+    }
+  }
+  c->levels = levels;
+
+  // --- descriptor tables (built on the host, copied into the arena)
+  std::vector<char> host_tables;
+  auto put = [&](const void* src, size_t n) -> size_t {
+    size_t off = rup((int64_t)host_tables.size(), 256);
+    host_tables.resize(off + n);
+    memcpy(host_tables.data() + off, src, n);
+    return off;
+  };
+  std::vector<Launch> fwd, bwd;
+  auto ptr = [&](size_t off) -> void* { return off == NONE ? nullptr : (void*)(uintptr_t)(off + 1); };
+  // Pointers are encoded as (arena offset + 1) and fixed up after the arena exists.
+  std::vector<size_t> fix;  // byte offsets (in host_tables) of pointer fields to relocate
+
+  const int GBM = bf ? GEMM_BM_BF16 : GEMM_BM_F32, GBN = bf ? GEMM_BN_BF16 : GEMM_BN_F32;
+  const int CBM = bf ? CONV_BM_BF16 : CONV_BM_F32, CBN = bf ? CONV_BN_BF16 : CONV_BN_F32;
+
+  auto emit_gemm = [&](std::vector<GemmProb>& ps, std::vector<Launch>& out, int kclass) {
+    if (ps.empty()) return;
+    std::vector<int32_t> map;
+    for (auto& p : ps) {
+      const int tm = cdiv(p.M, GBM), tn = cdiv(p.N, GBN);
+      p.tiles_n = tn;
+      p.tile_base = (int32_t)map.size();
+      for (int t = 0; t < tm * tn; ++t) map.push_back((int32_t)(&p - ps.data()));
+    }
+    size_t po = put(ps.data(), ps.size() * sizeof(GemmProb));
+    for (size_t k = 0; k < ps.size(); ++k) {
+      size_t b0 = po + k * sizeof(GemmProb);
+      for (size_t f : {offsetof(GemmProb, A), offsetof(GemmProb, B), offsetof(GemmProb, C), offsetof(GemmProb, CT),
+                       offsetof(GemmProb, bias), offsetof(GemmProb, mask), offsetof(GemmProb, dbias)})
+        fix.push_back(b0 + f);
+    }
+    size_t mo = put(map.data(), map.size() * 4);
+    out.push_back(Launch{0, kclass, po, mo, (int)map.size()});
+  };
+  auto emit_conv = [&](std::vector<ConvProb>& ps, std::vector<Launch>& out, int kind, int kclass) {
+    if (ps.empty()) return;
+    std::vector<int32_t> map;
+    for (auto& p : ps) {
+      p.tiles_m = cdiv(p.M, CBM);
+      p.tiles_n = cdiv(p.N, CBN);
+      p.tile_base = (int32_t)map.size();
+      const int nt = p.tiles_m * p.tiles_n * p.splits;
+      for (int t = 0; t < nt; ++t) map.push_back((int32_t)(&p - ps.data()));
+    }
+    size_t po = put(ps.data(), ps.size() * sizeof(ConvProb));
+    for (size_t k = 0; k < ps.size(); ++k) {
+      size_t b0 = po + k * sizeof(ConvProb);
+      for (size_t f : {offsetof(ConvProb, X), offsetof(ConvProb, Wt), offsetof(ConvProb, bias), offsetof(ConvProb, P),
+                       offsetof(ConvProb, amax), offsetof(ConvProb, PT), offsetof(ConvProb, G), offsetof(ConvProb, gam),
+                       offsetof(ConvProb, Gprev), offsetof(ConvProb, ws)})
+        fix.push_back(b0 + f);
+    }
+    size_t mo = put(map.data(), map.size() * 4);
+    out.push_back(Launch{kind, kclass, po, mo, (int)map.size()});
+  };
+
+  auto conv_base = [&](const Block& b) {
+    ConvProb p{};
+    p.Nb = B;
+    p.C = b.C;
+    p.H = b.H;
+    p.W = b.W;
+    p.O = b.O;
+    p.KH = b.KH;
+    p.pad = b.pad;
+    p.OH = b.OH;
+    p.OW = b.OW;
+    p.PH = b.PH;
+    p.PW = b.PW;
+    p.pool = b.pool;
+    p.relu = b.relu;
+    p.prev_relu = b.prev_relu;
+    p.splits = 1;
+    return p;
+  };
+
+  // forward levels
+  for (int lv = 0; lv < levels; ++lv) {
+    std::vector<GemmProb> gp;
+    std::vector<ConvProb> cp;
+    bool cat_done = false;
+    for (auto& m : c->models) {
+      if (lv >= (int)m.blocks.size()) continue;
+      Block& b = m.blocks[lv];
+      if (b.kind == 0) {
+        if (b.concat) {
+          if (cat_done) continue;
+          cat_done = true;
+          GemmProb p{};
+          p.A = ptr(c->Xin);
+          p.lda = c->ldxin;
+          p.B = ptr(bf ? catWb : catW32);
+          p.ldb = kin_p;
+          p.M = B;
+          p.N = (int)cat_rows;
+          p.K = (int)in_feat;
+          p.epi = EPI_FWD;
+          p.relu = 1;
+          p.C = ptr(catY);
+          p.ldc = cat_rows;
+          p.CT = ptr(catYT);
+          p.ldct = Bp;
+          p.bias = (const float*)ptr(catb32);
+          gp.push_back(p);
+          continue;
+        }
+        GemmProb p{};
+        p.A = ptr(b.X);
+        p.lda = b.ldx;
+        p.B = ptr(bf ? b.Wb : b.W32);
+        p.ldb = b.ldw;
+        p.M = B;
+        p.N = b.N;
+        p.K = b.K;
+        p.epi = b.last ? EPI_LOGITS : EPI_FWD;
+        p.relu = b.relu;
+        p.C = ptr(b.Y);
+        p.ldc = b.ldy;
+        p.CT = ptr(b.YT);
+        p.ldct = b.ldyt;
+        p.bias = (const float*)ptr(b.b32);
+        gp.push_back(p);
+      } else {
+        ConvProb p = conv_base(b);
+        p.M = b.pool ? B * b.PH * b.PW * 4 : B * b.OH * b.OW;
+        p.N = b.O;
+        p.K = b.KH * b.KH * b.C;
+        p.X = ptr(b.X);
+        p.Wt = ptr(bf ? b.Wb : b.W32);
+        p.ldw = b.ldw;
+        p.bias = (const float*)ptr(b.b32);
+        p.P = ptr(b.Y);
+        p.amax = (uint8_t*)ptr(b.amax);
+        p.PT = ptr(b.YT);
+        p.ldpt = b.ldyt;
+        cp.push_back(p);
+      }
+    }
+    emit_gemm(gp, fwd, UN_K_GEMM_FWD);
+    emit_conv(cp, fwd, 1, UN_K_CONV_FWD);
+  }
+
+  // softmax-CE
+  std::vector<CeProb> ces;
+  for (size_t mi = 0; mi < c->models.size(); ++mi) {
+    Block& b = c->models[mi].blocks.back();
+    CeProb p{};
+    p.logits = (const float*)ptr(b.Y);
+    p.ldl = b.ldy;
+    p.G = ptr(b.G);
+    p.ldg = b.ldg;
+    p.GT = ptr(b.GT);
+    p.ldgt = b.ldgt;
+    p.C = b.N;
+    p.model = (int)mi;
+    ces.push_back(p);
+  }
+  {
+    size_t po = put(ces.data(), ces.size() * sizeof(CeProb));
+    for (size_t k = 0; k < ces.size(); ++k) {
+      size_t b0 = po + k * sizeof(CeProb);
+      for (size_t f : {offsetof(CeProb, logits), offsetof(CeProb, G), offsetof(CeProb, GT)}) fix.push_back(b0 + f);
+    }
+    c->ce = Launch{5, UN_K_CE, po, NONE, (int)ces.size()};
+  }
+
+  // backward levels
+  for (int lv = levels - 1; lv >= 0; --lv) {
+    std::vector<GemmProb> gp;
+    std::vector<ConvProb> dp, wp;
+    std::vector<ReduceProb> rp;
+    bool cat_done = false;
+    for (auto& m : c->models) {
+      if (lv >= (int)m.blocks.size()) continue;
+      Block& b = m.blocks[lv];
+      if (b.kind == 0) {
+        // dgrad (not at level 0): gradient at the previous block's output
+        if (lv > 0) {
+          Block& pb = m.blocks[lv - 1];
+          GemmProb p{};
+          p.A = ptr(b.G);
+          p.lda = b.ldg;
+          p.B = ptr(b.WT);
+          p.ldb = b.ldwt;
+          p.M = B;
+          p.N = b.K;
+          p.K = b.N;
+          p.epi = EPI_DGRAD;
+          p.relu = pb.relu;
+          p.mask = ptr(b.XT);
+          p.ldmask = b.ldxt;
+          if (pb.kind == 0) {
+            p.C = ptr(pb.G);
+            p.ldc = pb.ldg;
+            p.CT = ptr(pb.GT);
+            p.ldct = pb.ldgt;
+          } else {
+            p.C = ptr(pb.G);
+            p.ldc = pb.out_elems_per_sample();
+          }
+          gp.push_back(p);
+        }
+        // wgrad (+ bias gradient through the ones row of XT)
+        if (b.concat) {
+          if (cat_done) continue;
+          cat_done = true;
+          GemmProb p{};
+          p.A = ptr(catGT);
+          p.lda = Bp;
+          p.B = ptr(c->XinT);
+          p.ldb = c->ldxint;
+          p.M = (int)cat_rows;
+          p.N = (int)in_feat + 1;
+          p.K = B;
+          p.epi = EPI_WGRAD;
+          p.nsplit = (int)in_feat;
+          p.C = ptr(catgW);
+          p.ldc = kin_p;
+          p.dbias = (float*)ptr(catgb);
+          gp.push_back(p);
+          continue;
+        }
+        GemmProb p{};
+        p.A = ptr(b.GT);
+        p.lda = b.ldgt;
+        p.B = ptr(b.XT);
+        p.ldb = b.ldxt;
+        p.M = b.N;
+        p.N = b.K + 1;
+        p.K = B;
+        p.epi = EPI_WGRAD;
+        p.nsplit = b.K;
+        p.C = ptr(b.gW);
+        p.ldc = b.ldw;
+        p.dbias = (float*)ptr(b.gb);
+        gp.push_back(p);
+      } else {
+        const int J = b.KH * b.KH * b.C;
+        if (lv > 0) {
+          Block& pb = m.blocks[lv - 1];
+          ConvProb p = conv_base(b);
+          p.M = B * b.H * b.W;
+          p.N = b.C;
+          p.K = b.KH * b.KH * b.O;
+          p.X = ptr(b.X);
+          p.Wt = ptr(b.WT);
+          p.ldw = b.ldwt;
+          p.G = ptr(b.G);
+          p.gam = (const uint8_t*)ptr(b.amax);
+          p.Gprev = ptr(pb.G);
+          dp.push_back(p);
+        }
+        ConvProb p = conv_base(b);
+        p.M = b.O;
+        p.N = J + 1;
+        p.K = b.pool ? B * b.PH * b.PW * 4 : B * b.OH * b.OW;
+        p.X = ptr(b.X);
+        p.G = ptr(b.G);
+        p.gam = (const uint8_t*)ptr(b.amax);
+        p.ws = (float*)ptr(b.ws);
+        p.ldws = b.ldws;
+        p.splits = b.splits;
+        p.kchunk = b.kchunk;
+        wp.push_back(p);
+        ReduceProb r{};
+        r.ws = (const float*)ptr(b.ws);
+        r.ldws = b.ldws;
+        r.splits = b.splits;
+        r.O = b.O;
+        r.J = J;
+        r.gW = (float*)ptr(b.gW);
+        r.ldgw = b.ldw;
+        r.gb = (float*)ptr(b.gb);
+        rp.push_back(r);
+      }
+    }
+    emit_gemm(gp, bwd, UN_K_GEMM_BWD);
+    emit_conv(dp, bwd, 2, UN_K_CONV_DGRAD);
+    emit_conv(wp, bwd, 3, UN_K_CONV_WGRAD);
+    if (!rp.empty()) {
+      std::vector<int32_t> map;
+      for (size_t k = 0; k < rp.size(); ++k) {
+        rp[k].blk_base = (int32_t)map.size();
+        const int nb = cdiv((int64_t)rp[k].O * (rp[k].J + 1), REDUCE_BLOCK);
+        for (int t = 0; t < nb; ++t) map.push_back((int32_t)k);
+      }
+      size_t po = put(rp.data(), rp.size() * sizeof(ReduceProb));
+      for (size_t k = 0; k < rp.size(); ++k) {
+        size_t b0 = po + k * sizeof(ReduceProb);
+        for (size_t f : {offsetof(ReduceProb, ws), offsetof(ReduceProb, gW), offsetof(ReduceProb, gb)})
+          fix.push_back(b0 + f);
+      }
+      size_t mo = put(map.data(), map.size() * 4);
+      bwd.push_back(Launch{4, UN_K_OTHER, po, mo, (int)map.size()});
+    }
+  }
+
+  // SGD tensors (weights and biases of every block)
+  for (int pass = 0; pass < 2; ++pass) {
+    std::vector<SgdTensor> ts;
+    std::vector<int32_t> map;
+    auto add = [&](SgdTensor t) {
+      t.tiles_r = cdiv(t.R, SGD_TILE);
+      t.tiles_c = cdiv(t.Cc, SGD_TILE);
+      t.tile_base = (int32_t)map.size();
+      const int nt = t.J * t.tiles_r * t.tiles_c;
+      for (int k = 0; k < nt; ++k) map.push_back((int32_t)ts.size());
+      ts.push_back(t);
+    };
+    for (auto& m : c->models)
+      for (auto& b : m.blocks) {
+        SgdTensor w{};
+        w.W = (float*)ptr(b.W32);
+        w.G = pass == 0 ? (const float*)ptr(b.gW) : nullptr;
+        w.Wb = ptr(b.Wb);
+        w.WT = ptr(b.WT);
+        w.ldw = b.ldw;
+        w.ldwt = b.ldwt;
+        w.R = b.rows;
+        if (b.kind == 0) {
+          w.J = 1;
+          w.Cc = b.K;
+        } else {
+          w.J = b.KH * b.KH;
+          w.Cc = b.C;
+        }
+        add(w);
+        if (pass == 0) {
+          SgdTensor t{};
+          t.W = (float*)ptr(b.b32);
+          t.G = (const float*)ptr(b.gb);
+          t.ldw = b.rows;
+          t.R = 1;
+          t.J = 1;
+          t.Cc = b.rows;
+          add(t);
+        }
+      }
+    size_t po = put(ts.data(), ts.size() * sizeof(SgdTensor));
+    for (size_t k = 0; k < ts.size(); ++k) {
+      size_t b0 = po + k * sizeof(SgdTensor);
+      for (size_t f : {offsetof(SgdTensor, W), offsetof(SgdTensor, G), offsetof(SgdTensor, Wb), offsetof(SgdTensor, WT)})
+        fix.push_back(b0 + f);
+    }
+    size_t mo = put(map.data(), map.size() * 4);
+    (pass == 0 ? c->sgd : c->refresh) = Launch{6, UN_K_SGD, po, mo, (int)map.size()};
+  }
+
+  // --- allocate the arena: buffers + tables
+  const size_t tables_off = A.take(host_tables.size());
+  c->bytes = A.top;
+  hipError_t e = hipMalloc((void**)&c->base, c->bytes);
+  if (e != hipSuccess) {
+    c->base = nullptr;
+    return fail(nullptr, UN_ERR_OOM, "hipMalloc of " + std::to_string(c->bytes) + " bytes failed: " + hipGetErrorString(e));
+  }
+  // relocate encoded pointers
+  for (size_t f : fix) {
+    uintptr_t v;
+    memcpy(&v, host_tables.data() + f, sizeof(v));
+    if (v != 0) v = (uintptr_t)(c->base + (v - 1));
+    memcpy(host_tables.data() + f, &v, sizeof(v));
+  }
+  auto relocate = [&](Launch& l) {
+    l.probs += tables_off;
+    if (l.map != NONE) l.map += tables_off;
+  };
+  for (auto& l : fwd) relocate(l);
+  for (auto& l : bwd) relocate(l);
+  relocate(c->ce);
+  relocate(c->sgd);
+  relocate(c->refresh);
+  c->fwd = fwd;
+  c->bwd = bwd;
+
+  HIPCHK(c, hipMemsetAsync(c->base, 0, c->bytes, c->stream));
+  HIPCHK(c, hipMemcpyAsync(c->base + tables_off, host_tables.data(), host_tables.size(), hipMemcpyHostToDevice,
+                           c->stream));
+  // ones rows of the transposed inputs (bias-gradient column of the wgrad GEMMs)
+  std::vector<uint16_t> ones16((size_t)Bp, 0x3F80);
+  std::vector<float> ones32((size_t)Bp, 1.0f);
+  const void* ones = bf ? (const void*)ones16.data() : (const void*)ones32.data();
+  auto set_ones_row = [&](size_t buf, int64_t row, int64_t ld) -> hipError_t {
+    return hipMemcpyAsync(c->base + buf + (size_t)row * ld * es, ones, (size_t)B * es, hipMemcpyHostToDevice,
+                          c->stream);
+  };
+  if (c->XinT != NONE) HIPCHK(c, set_ones_row(c->XinT, in_feat, Bp));
+  for (auto& m : c->models)
+    for (auto& b : m.blocks)
+      if (b.YT != NONE && !b.concat) HIPCHK(c, set_ones_row(b.YT, b.out_elems_per_sample(), b.ldyt));
+  // concatenated level 0: a zero-weight unit with bias 1 produces the ones row
+  if (!cat.empty()) {
+    std::vector<float> bias1(1, 1.0f);
+    for (int i : cat) {
+      const Block& b = c->models[i].blocks[0];
+      HIPCHK(c, hipMemcpyAsync(c->base + b.b32 + (size_t)b.N * 4, bias1.data(), 4, hipMemcpyHostToDevice, c->stream));
+    }
+  }
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  return UN_OK;
+}
+
+// ==========================================================================
+// Parameter layout mapping (PyTorch state_dict order <-> internal)
+// ==========================================================================
+// Internal column of PyTorch weight column `col` for a block.
+static inline int64_t lin_col(const Block& b, int64_t col) {
+  // PyTorch flattens NCHW: col = c*(h*w) + y*w + x; internal NHWC: (y*w + x)*c_count + c
+  const int hw = b.in_h * b.in_w;
+  const int64_t ch = col / hw, s = col - ch * hw;
+  return s * b.in_c + ch;
+}
+
+static void to_internal(const Block& b, const float* pt, std::vector<float>& w, std::vector<float>& bias) {
+  if (b.kind == 0) {
+    w.assign((size_t)b.N * b.ldw, 0.f);
+    for (int o = 0; o < b.N; ++o)
+      for (int k = 0; k < b.K; ++k) w[(size_t)o * b.ldw + lin_col(b, k)] = pt[b.pt_w + (size_t)o * b.K + k];
+    bias.assign(pt + b.pt_b, pt + b.pt_b + b.N);
+  } else {
+    w.assign((size_t)b.O * b.ldw, 0.f);
+    for (int o = 0; o < b.O; ++o)
+      for (int ci = 0; ci < b.C; ++ci)
+        for (int u = 0; u < b.KH; ++u)
+          for (int v = 0; v < b.KH; ++v)
+            w[(size_t)o * b.ldw + ((size_t)u * b.KH + v) * b.C + ci] =
+                pt[b.pt_w + (((size_t)o * b.C + ci) * b.KH + u) * b.KH + v];
+    bias.assign(pt + b.pt_b, pt + b.pt_b + b.O);
+  }
+}
+
+static void from_internal(const Block& b, const std::vector<float>& w, const std::vector<float>& bias, float* pt) {
+  if (b.kind == 0) {
+    for (int o = 0; o < b.N; ++o)
+      for (int k = 0; k < b.K; ++k) pt[b.pt_w + (size_t)o * b.K + k] = w[(size_t)o * b.ldw + lin_col(b, k)];
+    std::copy(bias.begin(), bias.end(), pt + b.pt_b);
+  } else {
+    for (int o = 0; o < b.O; ++o)
+      for (int ci = 0; ci < b.C; ++ci)
+        for (int u = 0; u < b.KH; ++u)
+          for (int v = 0; v < b.KH; ++v)
+            pt[b.pt_w + (((size_t)o * b.C + ci) * b.KH + u) * b.KH + v] =
+                w[(size_t)o * b.ldw + ((size_t)u * b.KH + v) * b.C + ci];
+    std::copy(bias.begin(), bias.end(), pt + b.pt_b);
+  }
+}
+
+static un_status refresh_shadows(un_ctx* c) {
+  HIPCHK(c, launch_sgd(c->bf16, c->at<SgdTensor>(c->refresh.probs), c->at<int32_t>(c->refresh.map), c->refresh.count,
+                       0.f, false, c->stream));
+  return UN_OK;
+}
+
+static un_status write_params(un_ctx* c, int i, const float* src) {
+  Model& m = c->models[i];
+  std::vector<float> w, bias;
+  for (auto& b : m.blocks) {
+    to_internal(b, src, w, bias);
+    HIPCHK(c, hipMemcpy(c->base + b.W32, w.data(), w.size() * 4, hipMemcpyHostToDevice));
+    HIPCHK(c, hipMemcpy(c->base + b.b32, bias.data(), bias.size() * 4, hipMemcpyHostToDevice));
+  }
+  return UN_OK;
+}
+
+static un_status read_tensors(un_ctx* c, int i, bool grads, float* dst) {
+  Model& m = c->models[i];
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  std::vector<float> w, bias;
+  for (auto& b : m.blocks) {
+    w.resize((size_t)b.rows * b.ldw);
+    bias.resize(b.rows);
+    HIPCHK(c, hipMemcpy(w.data(), c->base + (grads ? b.gW : b.W32), w.size() * 4, hipMemcpyDeviceToHost));
+    HIPCHK(c, hipMemcpy(bias.data(), c->base + (grads ? b.gb : b.b32), bias.size() * 4, hipMemcpyDeviceToHost));
+    from_internal(b, w, bias, dst);
+  }
+  return UN_OK;
+}
+
+// Library initialisation: Kaiming-uniform weights, U(+-1/sqrt(fan_in)) biases,
+// uniforms from splitmix64(seed, tensor, element).
+static void init_host(const Model& m, std::vector<float>& pt) {
+  pt.assign(m.n_params, 0.f);
+  int t = 0;
+  for (auto& b : m.blocks) {
+    const double fan_in = b.kind == 0 ? (double)b.K : (double)b.C * b.KH * b.KH;
+    const double wb = std::sqrt(6.0 / fan_in), bb = 1.0 / std::sqrt(fan_in);
+    for (int part = 0; part < 2; ++part, ++t) {
+      const size_t off = part == 0 ? b.pt_w : b.pt_b, n = part == 0 ? b.n_w : b.n_b;
+      const double bound = part == 0 ? wb : bb;
+      for (size_t e = 0; e < n; ++e) {
+        const uint64_t r = splitmix(m.seed ^ splitmix(((uint64_t)t << 40) ^ e));
+        const double u = (double)(r >> 11) * (1.0 / 9007199254740992.0);  // [0, 1)
+        pt[off + e] = (float)((2.0 * u - 1.0) * bound);
+      }
+    }
+  }
+}
+
+// ==========================================================================
+// Execution
+// ==========================================================================
+static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
+  hipEvent_t a = nullptr, b = nullptr;
+  if (c->profiling) {
+    auto get = [&]() {
+      hipEvent_t e = nullptr;
+      if (!c->free_events.empty()) {
+        e = c->free_events.back();
+        c->free_events.pop_back();
+      } else if (hipEventCreate(&e) != hipSuccess) {
+        e = nullptr;
+      }
+      return e;
+    };
+    a = get();
+    b = get();
+    if (a) hipEventRecord(a, c->stream);
+  }
+  hipError_t e = hipSuccess;
+  switch (l.kind) {
+    case 0:
+      e = launch_gemm(c->bf16, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
+      break;
+    case 1:
+      e = launch_conv_fwd(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
+      break;
+    case 2:
+      e = launch_conv_dgrad(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
+      break;
+    case 3:
+      e = launch_conv_wgrad(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
+      break;
+    case 4:
+      e = launch_reduce(c->at<ReduceProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
+      break;
+    case 5:
+      e = launch_ce(c->bf16, c->at<CeProb>(l.probs), l.count, c->at<int32_t>(c->ydev), c->B,
+                    c->at<float>(c->losses_dev), c->stream);
+      break;
+    case 6:
+      e = launch_sgd(c->bf16, c->at<SgdTensor>(l.probs), c->at<int32_t>(l.map), l.count, lr, true, c->stream);
+      break;
+  }
+  if (c->profiling && a && b) {
+    hipEventRecord(b, c->stream);
+    c->recs.push_back(EventRec{l.kclass, a, b});
+  }
+  return e;
+}
+
+static un_status drain_profile(un_ctx* c) {
+  if (c->recs.empty()) return UN_OK;
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  for (auto& r : c->recs) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+      c->prof_ms[r.kclass] += ms;
+      c->prof_n[r.kclass] += 1;
+    }
+    c->free_events.push_back(r.a);
+    c->free_events.push_back(r.b);
+  }
+  c->recs.clear();
+  return UN_OK;
+}
+
+#define CHECK_CTX(c)                                                         \
+  do {                                                                       \
+    if (!(c)) return fail(nullptr, UN_ERR_INVALID, "null context");          \
+    if ((c)->poisoned) return fail((c), UN_ERR_DEVICE, "context poisoned by an earlier device error"); \
+  } while (0)
+
+// ==========================================================================
+// C ABI
+// ==========================================================================
+extern "C" {
+
+un_status un_create(const un_model_spec* specs, int32_t n_models, const un_input_spec* in, un_ctx** out) {
+  if (!out) return fail(nullptr, UN_ERR_INVALID, "out is NULL");
+  *out = nullptr;
+  if (!specs || !in || n_models <= 0) return fail(nullptr, UN_ERR_INVALID, "specs/in NULL or n_models <= 0");
+  if (in->batch <= 0 || in->in_c <= 0 || in->in_h <= 0 || in->in_w <= 0)
+    return fail(nullptr, UN_ERR_INVALID, "input dimensions must be positive");
+  if (in->batch > CE_MAX_BATCH) return fail(nullptr, UN_ERR_UNSUPPORTED, "batch larger than 8192");
+  if (in->precision != UN_F32 && in->precision != UN_BF16_F32MASTER)
+    return fail(nullptr, UN_ERR_INVALID, "unknown precision");
+  un_ctx* c = new un_ctx();
+  c->bf16 = in->precision == UN_BF16_F32MASTER;
+  c->B = in->batch;
+  c->Bp = rup(in->batch, 8);
+  c->in_c = in->in_c;
+  c->in_h = in->in_h;
+  c->in_w = in->in_w;
+  c->models.resize(n_models);
+  c->min_classes = 1 << 30;
+  for (int i = 0; i < n_models; ++i) {
+    std::string why;
+    un_status s = parse_model(specs[i], *in, i, c->models[i], why);
+    if (s != UN_OK) {
+      delete c;
+      return fail(nullptr, s, why);
+    }
+    c->min_classes = std::min(c->min_classes, c->models[i].num_classes);
+  }
+  hipError_t e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
+  if (e != hipSuccess) {
+    delete c;
+    return fail(nullptr, UN_ERR_DEVICE, std::string("hipStreamCreate: ") + hipGetErrorString(e));
+  }
+  un_status s = plan_and_alloc(c);
+  if (s != UN_OK) {
+    std::string msg = c->err.empty() ? g_create_error : c->err;
+    if (c->base) hipFree(c->base);
+    hipStreamDestroy(c->stream);
+    delete c;
+    return fail(nullptr, s, msg);
+  }
+  std::vector<float> pt;
+  for (int i = 0; i < n_models; ++i) {
+    init_host(c->models[i], pt);
+    s = write_params(c, i, pt.data());
+    if (s != UN_OK) break;
+  }
+  if (s == UN_OK) s = refresh_shadows(c);
+  if (s == UN_OK && hipStreamSynchronize(c->stream) != hipSuccess) s = UN_ERR_DEVICE;
+  if (s != UN_OK) {
+    std::string msg = c->err;
+    un_destroy(c);
+    return fail(nullptr, s, msg);
+  }
+  *out = c;
+  return UN_OK;
+}
+
+static un_status load_common(un_ctx* c, const float* x, const int32_t* y, bool device) {
+  const size_t nx = (size_t)c->B * c->in_c * c->in_h * c->in_w;
+  std::vector<int32_t> yh(c->B);
+  if (device) {
+    HIPCHK(c, hipMemcpy(yh.data(), y, (size_t)c->B * 4, hipMemcpyDeviceToHost));
+  } else {
+    memcpy(yh.data(), y, (size_t)c->B * 4);
+  }
+  for (int b = 0; b < c->B; ++b)
+    if (yh[b] < 0 || yh[b] >= c->min_classes)
+      return fail(c, UN_ERR_RANGE, "label " + std::to_string(yh[b]) + " at " + std::to_string(b) + " out of range");
+  const float* xsrc = x;
+  if (!device) {
+    HIPCHK(c, hipMemcpyAsync(c->base + c->xstage, x, nx * 4, hipMemcpyHostToDevice, c->stream));
+    xsrc = c->at<float>(c->xstage);
+  }
+  HIPCHK(c, hipMemcpyAsync(c->base + c->ydev, yh.data(), (size_t)c->B * 4, hipMemcpyHostToDevice, c->stream));
+  HIPCHK(c, launch_load(c->bf16, xsrc, c->B, c->in_c, c->in_h, c->in_w, c->base + c->Xin,
+                        c->XinT == NONE ? nullptr : c->base + c->XinT, c->ldxint, c->stream));
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  c->loaded = true;
+  return UN_OK;
+}
+
+un_status un_load_batch(un_ctx* c, const float* x, const int32_t* y) {
+  CHECK_CTX(c);
+  if (!x || !y) return fail(c, UN_ERR_INVALID, "x or y is NULL");
+  return load_common(c, x, y, false);
+}
+
+un_status un_load_batch_device(un_ctx* c, const float* x, const int32_t* y) {
+  CHECK_CTX(c);
+  if (!x || !y) return fail(c, UN_ERR_INVALID, "x or y is NULL");
+  return load_common(c, x, y, true);
+}
+
+un_status un_step(un_ctx* c, float lr, float* losses) {
+  CHECK_CTX(c);
+  if (!c->loaded) return fail(c, UN_ERR_STATE, "un_step before un_load_batch");
+  if (!std::isfinite(lr)) return fail(c, UN_ERR_INVALID, "lr is not finite");
+  for (auto& l : c->fwd) HIPCHK(c, run_launch(c, l, lr));
+  HIPCHK(c, run_launch(c, c->ce, lr));
+  for (auto& l : c->bwd) HIPCHK(c, run_launch(c, l, lr));
+  HIPCHK(c, run_launch(c, c->sgd, lr));
+  c->stepped = true;
+  if (c->profiling && c->recs.size() > 4096) {
+    un_status s = drain_profile(c);
+    if (s != UN_OK) return s;
+  }
+  if (losses) {
+    HIPCHK(c, hipMemcpyAsync(losses, c->base + c->losses_dev, c->models.size() * 4, hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+  }
+  return UN_OK;
+}
+
+un_status un_param_count(const un_ctx* c, int32_t i, size_t* n) {
+  if (!c || !n) return fail(const_cast<un_ctx*>(c), UN_ERR_INVALID, "NULL argument");
+  if (i < 0 || i >= (int)c->models.size()) return fail(const_cast<un_ctx*>(c), UN_ERR_RANGE, "model index out of range");
+  *n = c->models[i].n_params;
+  return UN_OK;
+}
+
+un_status un_get_params(un_ctx* c, int32_t i, float* dst, size_t cap, size_t* n) {
+  CHECK_CTX(c);
+  if (i < 0 || i >= (int)c->models.size()) return fail(c, UN_ERR_RANGE, "model index out of range");
+  const size_t np = c->models[i].n_params;
+  if (n) *n = np;
+  if (!dst) return UN_OK;
+  if (cap < np) return fail(c, UN_ERR_BUFSIZE, "buffer holds " + std::to_string(cap) + " < " + std::to_string(np));
+  return read_tensors(c, i, false, dst);
+}
+
+un_status un_get_grads(un_ctx* c, int32_t i, float* dst, size_t cap, size_t* n) {
+  CHECK_CTX(c);
+  if (i < 0 || i >= (int)c->models.size()) return fail(c, UN_ERR_RANGE, "model index out of range");
+  const size_t np = c->models[i].n_params;
+  if (n) *n = np;
+  if (!dst) return UN_OK;
+  if (!c->stepped) return fail(c, UN_ERR_STATE, "no step has run yet");
+  if (cap < np) return fail(c, UN_ERR_BUFSIZE, "buffer too small");
+  return read_tensors(c, i, true, dst);
+}
+
+un_status un_set_params(un_ctx* c, int32_t i, const float* src, size_t n) {
+  CHECK_CTX(c);
+  if (i < 0 || i >= (int)c->models.size()) return fail(c, UN_ERR_RANGE, "model index out of range");
+  if (!src) return fail(c, UN_ERR_INVALID, "src is NULL");
+  if (n != c->models[i].n_params) return fail(c, UN_ERR_BUFSIZE, "element count mismatch");
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  un_status s = write_params(c, i, src);
+  if (s != UN_OK) return s;
+  s = refresh_shadows(c);
+  if (s != UN_OK) return s;
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  return UN_OK;
+}
+
+un_status un_arena_bytes(const un_ctx* c, size_t* bytes) {
+  if (!c || !bytes) return fail(const_cast<un_ctx*>(c), UN_ERR_INVALID, "NULL argument");
+  *bytes = c->bytes;
+  return UN_OK;
+}
+
+un_status un_sync(un_ctx* c) {
+  CHECK_CTX(c);
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  return UN_OK;
+}
+
+un_status un_get_stream(const un_ctx* c, void** s) {
+  if (!c || !s) return fail(const_cast<un_ctx*>(c), UN_ERR_INVALID, "NULL argument");
+  *s = (void*)c->stream;
+  return UN_OK;
+}
+
+un_status un_profile_enable(un_ctx* c, int32_t enable) {
+  CHECK_CTX(c);
+  un_status s = drain_profile(c);
+  if (s != UN_OK) return s;
+  c->profiling = enable != 0;
+  if (c->profiling)
+    for (int k = 0; k < UN_K_COUNT; ++k) {
+      c->prof_ms[k] = 0;
+      c->prof_n[k] = 0;
+    }
+  return UN_OK;
+}
+
+un_status un_profile_read(un_ctx* c, int32_t kc, double* ms, int64_t* n) {
+  CHECK_CTX(c);
+  if (kc < 0 || kc >= UN_K_COUNT) return fail(c, UN_ERR_RANGE, "kernel class out of range");
+  un_status s = drain_profile(c);
+  if (s != UN_OK) return s;
+  if (ms) *ms = c->prof_ms[kc];
+  if (n) *n = c->prof_n[kc];
+  return UN_OK;
+}
+
+void un_destroy(un_ctx* c) {
+  if (!c) return;
+  if (c->stream) hipStreamSynchronize(c->stream);
+  for (auto& r : c->recs) {
+    hipEventDestroy(r.a);
+    hipEventDestroy(r.b);
+  }
+  for (auto e : c->free_events) hipEventDestroy(e);
+  if (c->base) hipFree(c->base);
+  if (c->stream) hipStreamDestroy(c->stream);
+  delete c;
+}
+
+const char* un_last_error(const un_ctx* c) {
+  if (!c) return g_create_error.c_str();
+  return c->err.c_str();
+}
+
+}  // extern "C"

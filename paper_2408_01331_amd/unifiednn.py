@@ -1,0 +1,268 @@
+"""Thin Python binding of libunifiednn.so (the C ABI in include/unifiednn.h).
+
+Argument marshalling only: every step of the training path runs in the
+library's HIP kernels. The functions keep the C names (un_create, un_load_batch,
+un_step, un_get_params, ...); `Hybrid` wraps them in a small class.
+
+Importing this module fails loudly if the library has not been built: there is
+no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libunifiednn.so")
+
+UN_OK, UN_ERR_INVALID, UN_ERR_STATE, UN_ERR_OOM, UN_ERR_DEVICE, UN_ERR_RANGE, UN_ERR_BUFSIZE, UN_ERR_UNSUPPORTED = range(8)
+STATUS_NAMES = ["UN_OK", "UN_ERR_INVALID", "UN_ERR_STATE", "UN_ERR_OOM", "UN_ERR_DEVICE", "UN_ERR_RANGE",
+                "UN_ERR_BUFSIZE", "UN_ERR_UNSUPPORTED"]
+UN_F32, UN_BF16_F32MASTER = 0, 1
+OPS = {"linear": 0, "conv": 1, "relu": 2, "pool": 3, "flatten": 4}
+KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad", "ce", "sgd", "other"]
+
+# Every symbol the header declares.
+EXPORTS = ["un_create", "un_load_batch", "un_load_batch_device", "un_step", "un_get_params", "un_set_params",
+           "un_get_grads", "un_param_count", "un_arena_bytes", "un_sync", "un_get_stream", "un_profile_enable",
+           "un_profile_read", "un_destroy", "un_last_error"]
+
+
+class un_layer(ctypes.Structure):
+    _fields_ = [("op", ctypes.c_int32), ("out", ctypes.c_int32), ("kernel", ctypes.c_int32), ("pad", ctypes.c_int32)]
+
+
+class un_model_spec(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("layers", ctypes.POINTER(un_layer)),
+                ("num_classes", ctypes.c_int32), ("init_seed", ctypes.c_uint64)]
+
+
+class un_input_spec(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("in_c", ctypes.c_int32), ("in_h", ctypes.c_int32),
+                ("in_w", ctypes.c_int32), ("precision", ctypes.c_int32)]
+
+
+class UnError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS_NAMES[status] if 0 <= status < 8 else status}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load libunifiednn.so (raises if it is missing: build it first)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2408_01331_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, c_size_p = ctypes.c_void_p, ctypes.POINTER(ctypes.c_size_t)
+        f = ctypes.POINTER(ctypes.c_float)
+        i32 = ctypes.POINTER(ctypes.c_int32)
+        sig = {
+            "un_create": (ctypes.c_int, [ctypes.POINTER(un_model_spec), ctypes.c_int32, ctypes.POINTER(un_input_spec),
+                                         ctypes.POINTER(P)]),
+            "un_load_batch": (ctypes.c_int, [P, f, i32]),
+            "un_load_batch_device": (ctypes.c_int, [P, P, P]),
+            "un_step": (ctypes.c_int, [P, ctypes.c_float, f]),
+            "un_get_params": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t, c_size_p]),
+            "un_set_params": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t]),
+            "un_get_grads": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t, c_size_p]),
+            "un_param_count": (ctypes.c_int, [P, ctypes.c_int32, c_size_p]),
+            "un_arena_bytes": (ctypes.c_int, [P, c_size_p]),
+            "un_sync": (ctypes.c_int, [P]),
+            "un_get_stream": (ctypes.c_int, [P, ctypes.POINTER(P)]),
+            "un_profile_enable": (ctypes.c_int, [P, ctypes.c_int32]),
+            "un_profile_read": (ctypes.c_int, [P, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
+                                               ctypes.POINTER(ctypes.c_int64)]),
+            "un_destroy": (None, [P]),
+            "un_last_error": (ctypes.c_char_p, [P]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _fp(a):
+    return a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+
+
+def _check(status, ctx=None):
+    if status != UN_OK:
+        msg = lib().un_last_error(ctx)
+        raise UnError(status, msg.decode() if msg else "")
+
+
+# ---------------------------------------------------------------------------
+# C-named functions
+# ---------------------------------------------------------------------------
+def make_specs(specs, seeds=None):
+    """Python spec dicts -> (array of un_model_spec, keep-alive list)."""
+    keep = []
+    arr = (un_model_spec * len(specs))()
+    for i, s in enumerate(specs):
+        layers = (un_layer * len(s["layers"]))()
+        for j, l in enumerate(s["layers"]):
+            op = OPS[l[0]]
+            out = l[1] if len(l) > 1 else 0
+            k = l[2] if op == 1 else 0
+            pad = l[3] if op == 1 else 0
+            layers[j] = un_layer(op, out, k, pad)
+        keep.append(layers)
+        arr[i] = un_model_spec(len(s["layers"]), layers, s["num_classes"], 0 if seeds is None else seeds[i])
+    return arr, keep
+
+
+def un_create(specs, batch, in_shape, precision, seeds=None):
+    arr, keep = make_specs(specs, seeds)
+    c, h, w = (tuple(in_shape) + (1, 1))[:3] if len(in_shape) != 3 else tuple(in_shape)
+    ins = un_input_spec(batch, c, h, w, UN_BF16_F32MASTER if precision == "bf16" else UN_F32)
+    ctx = ctypes.c_void_p()
+    _check(lib().un_create(arr, len(specs), ctypes.byref(ins), ctypes.byref(ctx)))
+    return ctx
+
+
+def un_load_batch(ctx, x, y):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    y = np.ascontiguousarray(y, dtype=np.int32)
+    _check(lib().un_load_batch(ctx, _fp(x), y.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))), ctx)
+
+
+def un_load_batch_device(ctx, x_ptr, y_ptr):
+    _check(lib().un_load_batch_device(ctx, ctypes.c_void_p(x_ptr), ctypes.c_void_p(y_ptr)), ctx)
+
+
+def un_step(ctx, lr, n_models=None):
+    """One fused step; returns the per-model losses if n_models is given, else enqueues only."""
+    if n_models is None:
+        _check(lib().un_step(ctx, ctypes.c_float(lr), None), ctx)
+        return None
+    out = np.zeros(n_models, dtype=np.float32)
+    _check(lib().un_step(ctx, ctypes.c_float(lr), _fp(out)), ctx)
+    return out
+
+
+def un_param_count(ctx, i):
+    n = ctypes.c_size_t()
+    _check(lib().un_param_count(ctx, i, ctypes.byref(n)), ctx)
+    return n.value
+
+
+def un_get_params(ctx, i):
+    n = un_param_count(ctx, i)
+    out = np.empty(n, dtype=np.float32)
+    got = ctypes.c_size_t()
+    _check(lib().un_get_params(ctx, i, _fp(out), n, ctypes.byref(got)), ctx)
+    return out
+
+
+def un_get_grads(ctx, i):
+    n = un_param_count(ctx, i)
+    out = np.empty(n, dtype=np.float32)
+    got = ctypes.c_size_t()
+    _check(lib().un_get_grads(ctx, i, _fp(out), n, ctypes.byref(got)), ctx)
+    return out
+
+
+def un_set_params(ctx, i, flat):
+    flat = np.ascontiguousarray(flat, dtype=np.float32)
+    _check(lib().un_set_params(ctx, i, _fp(flat), flat.size), ctx)
+
+
+def un_sync(ctx):
+    _check(lib().un_sync(ctx), ctx)
+
+
+def un_get_stream(ctx):
+    s = ctypes.c_void_p()
+    _check(lib().un_get_stream(ctx, ctypes.byref(s)), ctx)
+    return s.value
+
+
+def un_arena_bytes(ctx):
+    n = ctypes.c_size_t()
+    _check(lib().un_arena_bytes(ctx, ctypes.byref(n)), ctx)
+    return n.value
+
+
+def un_profile_enable(ctx, on):
+    _check(lib().un_profile_enable(ctx, 1 if on else 0), ctx)
+
+
+def un_profile_read(ctx, kclass):
+    ms = ctypes.c_double()
+    n = ctypes.c_int64()
+    _check(lib().un_profile_read(ctx, kclass, ctypes.byref(ms), ctypes.byref(n)), ctx)
+    return ms.value, n.value
+
+
+def un_destroy(ctx):
+    if ctx:
+        lib().un_destroy(ctx)
+
+
+# ---------------------------------------------------------------------------
+# Convenience wrapper
+# ---------------------------------------------------------------------------
+def flatten_params(params):
+    return np.concatenate([np.asarray(p, dtype=np.float32).ravel() for p in params])
+
+
+def split_params(flat, shapes):
+    out, o = [], 0
+    for s in shapes:
+        n = int(np.prod(s))
+        out.append(flat[o:o + n].reshape(s))
+        o += n
+    return out
+
+
+class Hybrid:
+    """N models merged into one fused training step on the GPU."""
+
+    def __init__(self, specs, batch, in_shape, precision="f32", seeds=None):
+        self.specs = list(specs)
+        self.n = len(self.specs)
+        self.ctx = un_create(self.specs, batch, in_shape, precision, seeds)
+
+    def close(self):
+        if self.ctx:
+            un_destroy(self.ctx)
+            self.ctx = None
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *a):
+        self.close()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def load_batch(self, x, y):
+        un_load_batch(self.ctx, x, y)
+
+    def step(self, lr, losses=True):
+        return un_step(self.ctx, lr, self.n if losses else None)
+
+    def get_params(self, i):
+        return un_get_params(self.ctx, i)
+
+    def set_params(self, i, flat):
+        un_set_params(self.ctx, i, flat)
+
+    def get_grads(self, i):
+        return un_get_grads(self.ctx, i)
+
+    def sync(self):
+        un_sync(self.ctx)

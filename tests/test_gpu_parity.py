@@ -1,0 +1,206 @@
+"""GPU parity: the fused N-model step (through the C ABI) against the CPU oracle
+that trains every model alone, on the same seeded inputs.
+
+Tolerances: 1e-4 (fp32) and 2e-2 (bf16 storage, fp32 master) relative error
+on losses and parameters; the metrics (strict per-element for one step, with
+the oracle's ill-conditioned fp32 decisions excepted; Frobenius plus a
+per-element guard for free-running multi-step runs) are defined in
+tests/_parity.py. Updates theta_k - theta_0 and gradients are checked too,
+because the parameters alone are dominated by their identical start values.
+"""
+import numpy as np
+import pytest
+
+from paper_2408_01331_amd import workloads as W
+from _parity import compare_run, compare_step, run_gpu, run_oracle, theta0
+
+pytestmark = pytest.mark.gpu
+
+
+def _need_gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _report(name, worst):
+    print(f"\n[{name}] worst: " + ", ".join(f"{k}={v:.3g}" for k, v in worst.items()), flush=True)
+
+
+# ---------------------------------------------------------------------------
+# Benchmark workloads at full size. One step from the same start: strict.
+# The configured number of steps, free running: see compare_run.
+# fp32 workloads check every model; bf16 ones sample models (all N still run).
+# ---------------------------------------------------------------------------
+ONE_STEP = [("mlp2", None), ("mlp8", None), ("lenet4", None), ("mlp64", [0, 17, 63]), ("cifar16", [3])]
+
+
+@pytest.mark.parametrize("name,sample", ONE_STEP, ids=[n for n, _ in ONE_STEP])
+def test_one_step_strict(name, sample):
+    _need_gpu()
+    wl = W.get(name)
+    models = list(range(wl.n_models)) if sample is None else sample
+    gpu = run_gpu(wl, 1, models=models)
+    orc = run_oracle(wl, 1, models)
+    _report(f"{wl.name} 1 step", compare_step(wl, gpu, orc, models))
+
+
+RUNS = [("mlp2", None, None), ("mlp8", None, None), ("lenet4", None, None), ("mlp64", [0, 63], 3),
+        ("cifar16", [0, 9], 2)]
+
+
+@pytest.mark.parametrize("name,sample,steps", RUNS, ids=[n for n, _, _ in RUNS])
+def test_k_steps(name, sample, steps):
+    _need_gpu()
+    wl = W.get(name)
+    steps = wl.steps if steps is None else steps
+    models = list(range(wl.n_models)) if sample is None else sample
+    gpu = run_gpu(wl, steps, models=models)
+    orc = run_oracle(wl, steps, models)
+    _report(f"{wl.name} {steps} steps", compare_run(wl, gpu, orc, models))
+
+
+# ---------------------------------------------------------------------------
+# Ragged and degenerate shapes (several tiles plus a ragged tail)
+# ---------------------------------------------------------------------------
+def _custom(specs, batch, in_shape, precision, steps=3, lr=0.05, seed=5):
+    return W.Workload("custom", len(specs), batch, in_shape, precision, specs, lr, steps, seed)
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
+def test_ragged_mlps(precision):
+    _need_gpu()
+    specs = [
+        {"layers": [("linear", 37), ("relu",), ("linear", 129), ("relu",), ("linear", 13)], "num_classes": 13},
+        {"layers": [("linear", 13)], "num_classes": 13},                      # logistic regression
+        {"layers": [("linear", 200), ("linear", 13)], "num_classes": 13},     # no ReLU between
+        {"layers": [("linear", 1), ("relu",), ("linear", 13)], "num_classes": 13},
+        {"layers": [("linear", 300), ("relu",), ("linear", 65), ("relu",), ("linear", 7), ("relu",),
+                    ("linear", 13)], "num_classes": 13},
+    ]
+    wl = _custom(specs, 37, (104,), precision)
+    m = range(wl.n_models)
+    _report(f"ragged_mlps_{precision} 1 step", compare_step(wl, run_gpu(wl, 1), run_oracle(wl, 1, m), m))
+    _report(f"ragged_mlps_{precision} run", compare_run(wl, run_gpu(wl, wl.steps), run_oracle(wl, wl.steps, m), m))
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
+def test_ragged_cnns(precision):
+    _need_gpu()
+    specs = [
+        {"layers": [("conv", 8, 3, 1), ("relu",), ("pool",), ("conv", 16, 3, 0), ("relu",), ("pool",),
+                    ("flatten",), ("linear", 10)], "num_classes": 10},
+        {"layers": [("conv", 5, 5, 2), ("relu",), ("pool",), ("flatten",), ("linear", 24), ("relu",),
+                    ("linear", 10)], "num_classes": 10},
+        {"layers": [("conv", 16, 3, 1), ("relu",), ("conv", 8, 3, 1), ("pool",), ("flatten",),
+                    ("linear", 10)], "num_classes": 10},
+        {"layers": [("flatten",), ("linear", 40), ("relu",), ("linear", 10)], "num_classes": 10},
+    ]
+    wl = _custom(specs, 12, (3, 13, 16), precision, steps=3)
+    m = range(wl.n_models)
+    _report(f"ragged_cnns_{precision} 1 step", compare_step(wl, run_gpu(wl, 1), run_oracle(wl, 1, m), m))
+    _report(f"ragged_cnns_{precision} run", compare_run(wl, run_gpu(wl, wl.steps), run_oracle(wl, wl.steps, m), m))
+
+
+# ---------------------------------------------------------------------------
+# The paper's invariants on the device: no interference, merged == alone
+# ---------------------------------------------------------------------------
+def _bitwise_equal(a, b):
+    return all(np.array_equal(np.asarray(x).view(np.uint32), np.asarray(y).view(np.uint32)) for x, y in zip(a, b))
+
+
+@pytest.mark.parametrize("name", ["mlp8", "lenet4"])
+def test_perturbing_one_model_leaves_the_others_bitwise_unchanged(name):
+    _need_gpu()
+    wl = W.get(name)
+    steps = 3
+    base = run_gpu(wl, steps)
+    j = 1
+    pert = {j: [p + np.float32(0.01) for p in theta0(wl, j)]}
+    moved = run_gpu(wl, steps, theta=pert)
+    for i in range(wl.n_models):
+        same = (np.array_equal(base[0][:, i], moved[0][:, i]) and _bitwise_equal(base[1][i], moved[1][i])
+                and _bitwise_equal(base[2][i], moved[2][i]))
+        assert same == (i != j), f"model {i}: bitwise equality {same}, expected {i != j}"
+
+
+@pytest.mark.parametrize("name", ["mlp8", "lenet4"])
+def test_merged_run_equals_each_model_alone_bitwise(name):
+    _need_gpu()
+    wl = W.get(name)
+    steps = 2
+    merged = run_gpu(wl, steps)
+    for i in [0, wl.n_models - 1]:
+        alone_wl = W.Workload("alone", 1, wl.batch, wl.in_shape, wl.precision, [wl.specs[i]], wl.lr, steps, wl.seed)
+        alone = run_gpu(alone_wl, steps, theta={0: theta0(wl, i)})
+        assert np.array_equal(merged[0][:, i], alone[0][:, 0])
+        assert _bitwise_equal(merged[1][i], alone[1][0])
+        assert _bitwise_equal(merged[2][i], alone[2][0])
+
+
+def test_lr_zero_leaves_params_bitwise_and_sgd_is_fma():
+    _need_gpu()
+    import oracle
+    from paper_2408_01331_amd.unifiednn import Hybrid, flatten_params
+    wl = W.get("mlp8")
+    x, y = W.make_batch(wl, 0)
+    with Hybrid(wl.specs, wl.batch, wl.in_shape, wl.precision) as h:
+        th = [flatten_params(theta0(wl, i)) for i in range(wl.n_models)]
+        for i in range(wl.n_models):
+            h.set_params(i, th[i])
+        h.load_batch(x, y)
+        h.step(0.0)
+        for i in range(wl.n_models):
+            assert np.array_equal(h.get_params(i).view(np.uint32), th[i].view(np.uint32))
+        h.step(0.01)
+        for i in range(wl.n_models):
+            g = h.get_grads(i)
+            expect = oracle.fma32(np.float32(-0.01), g, th[i])
+            assert np.array_equal(h.get_params(i).view(np.uint32), expect.view(np.uint32))
+
+
+def test_errors_leave_state_unchanged():
+    _need_gpu()
+    from paper_2408_01331_amd import unifiednn as U
+    wl = W.get("mlp2")
+    with U.Hybrid(wl.specs, wl.batch, wl.in_shape, wl.precision) as h:
+        with pytest.raises(U.UnError) as e:
+            h.step(0.01)
+        assert e.value.status == U.UN_ERR_STATE
+        x, y = W.make_batch(wl, 0)
+        bad = y.copy()
+        bad[3] = 10
+        with pytest.raises(U.UnError) as e:
+            h.load_batch(x, bad)
+        assert e.value.status == U.UN_ERR_RANGE
+        with pytest.raises(U.UnError) as e:
+            h.step(0.01)
+        assert e.value.status == U.UN_ERR_STATE
+        h.load_batch(x, y)
+        with pytest.raises(U.UnError) as e:
+            h.step(float("nan"))
+        assert e.value.status == U.UN_ERR_INVALID
+        with pytest.raises(U.UnError) as e:
+            h.get_params(2)
+        assert e.value.status == U.UN_ERR_RANGE
+        with pytest.raises(U.UnError) as e:
+            h.set_params(0, np.zeros(5, np.float32))
+        assert e.value.status == U.UN_ERR_BUFSIZE
+        l1 = h.step(0.01)
+        assert np.all(np.isfinite(l1))
+
+
+def test_library_init_statistics():
+    """The library's own initialisation: Kaiming-uniform bounds, mean ~ 0, variance ~ bound^2/3."""
+    _need_gpu()
+    from paper_2408_01331_amd.unifiednn import Hybrid, split_params
+    wl = W.get("mlp2")
+    with Hybrid(wl.specs, wl.batch, wl.in_shape, wl.precision, seeds=[1, 2]) as h:
+        shapes = [s for s, _ in W.param_shapes(wl.specs[0], wl.in_shape)]
+        ps = split_params(h.get_params(0), shapes)
+    for (shape, fan_in), p in zip(W.param_shapes(wl.specs[0], wl.in_shape), ps):
+        bound = np.sqrt(6.0 / fan_in) if len(shape) > 1 else 1.0 / np.sqrt(fan_in)
+        assert np.max(np.abs(p)) <= bound
+        if p.size > 1000:
+            assert abs(p.mean()) < 0.05 * bound
+            assert abs(p.var() / (bound ** 2 / 3) - 1) < 0.05

@@ -376,3 +376,34 @@ def test_f32_mode_close_to_f64():
     assert abs(l32 - l64) < 1e-6
     for a, b in zip(g32, g64):
         assert np.max(np.abs(a - b)) <= 1e-5 * np.max(np.abs(b)) + 1e-12
+
+
+# ---------------------------------------------------------------------------
+# Ill-conditioned discrete decisions
+# ---------------------------------------------------------------------------
+def test_flags_mark_relu_inputs_within_fp32_rounding_of_zero():
+    spec = {"layers": [("linear", 3), ("relu",), ("linear", 2)], "num_classes": 2}
+    W1 = np.array([[1.0, -1.0], [1.0, 1.0], [2.0 ** -30, 0.0]], dtype=np.float32)
+    b1 = np.zeros(3, dtype=np.float32)
+    W2 = np.ones((2, 3), dtype=np.float32)
+    b2 = np.zeros(2, dtype=np.float32)
+    x = np.array([[0.5, 0.5], [1.0, 2.0]], dtype=np.float32)
+    flags = {}
+    oracle.forward(spec, [W1, b1, W2, b2], x, "f32", flags)
+    # unit 0: z = 0 exactly for sample 0; unit 2: z = 2^-31 << u * |h||w| is not
+    # the case (|z| equals the magnitude sum, so it is well conditioned)
+    assert flags[0] == {0}
+
+
+def test_flags_mark_near_tied_pool_windows():
+    spec = {"layers": [("conv", 1, 1, 0), ("pool",), ("flatten",), ("linear", 2)], "num_classes": 2}
+    Wc = np.ones((1, 1, 1, 1), dtype=np.float32)
+    bc = np.zeros(1, dtype=np.float32)
+    Wl = np.ones((2, 1), dtype=np.float32)
+    bl = np.zeros(2, dtype=np.float32)
+    near = np.array([[[[1.0, 1.0 + 2.0 ** -26], [0.5, 0.25]]]], dtype=np.float64)
+    far = np.array([[[[1.0, 1.5], [0.5, 0.25]]]], dtype=np.float64)
+    f1, f2 = {}, {}
+    oracle.forward(spec, [Wc, bc, Wl, bl], near, "f64", f1)
+    oracle.forward(spec, [Wc, bc, Wl, bl], far, "f64", f2)
+    assert f1.get(0) == {0} and not f2.get(0)
