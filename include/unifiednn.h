@@ -118,6 +118,8 @@ un_status un_load_batch_device(un_ctx* ctx, const float* x_dev, const int32_t* y
  * If losses is non-NULL it receives, per model, the loss at the parameters
  * BEFORE this step's update (host fp32 [N]); the call then waits for the step.
  * With losses == NULL the step is only enqueued on the context's stream.
+ * The update theta <- fma(-lr, g, theta) (fp32) is applied inside the
+ * weight-gradient kernels; gradients are stored only when kept (un_keep_grads).
  * Errors: UN_ERR_STATE (no batch loaded), UN_ERR_INVALID (lr not finite). */
 un_status un_step(un_ctx* ctx, float lr, float* losses);
 
@@ -134,9 +136,16 @@ un_status un_get_params(un_ctx* ctx, int32_t i, float* dst, size_t cap_elems, si
  * reference trained elsewhere. Errors: UN_ERR_RANGE, UN_ERR_BUFSIZE. */
 un_status un_set_params(un_ctx* ctx, int32_t i, const float* src, size_t n_elems);
 
+/* Keep (1) or stop keeping (0) the gradients: the update is fused into the
+ * weight-gradient kernels, so by default gradients are applied and never
+ * stored. While enabled, un_step also stores every gradient (4 more bytes of
+ * traffic per parameter) for un_get_grads. Default 0. */
+un_status un_keep_grads(un_ctx* ctx, int32_t enable);
+
 /* The gradient of model i computed by the last un_step (same layout and order
  * as un_get_params). Waits for the stream. Errors as un_get_params, and
- * UN_ERR_STATE before the first step. */
+ * UN_ERR_STATE before the first step or when that step did not keep
+ * gradients (un_keep_grads). */
 un_status un_get_grads(un_ctx* ctx, int32_t i, float* dst, size_t cap_elems, size_t* n_elems);
 
 /* Number of parameters of model i. */
@@ -160,8 +169,8 @@ typedef enum {
   UN_K_CONV_DGRAD = 3,
   UN_K_CONV_WGRAD = 4,
   UN_K_CE = 5,          /* softmax cross-entropy */
-  UN_K_SGD = 6,         /* multi-tensor SGD (+ shadow copies) */
-  UN_K_OTHER = 7,       /* load/convert, split-K reduction */
+  UN_K_SGD = 6,         /* weight copy refresh (SGD kernel without gradient) */
+  UN_K_OTHER = 7,       /* split-K reduction with the fused conv update */
   UN_K_COUNT = 8
 } un_kernel_class;
 

@@ -39,14 +39,23 @@ struct GemmProb {
   int32_t tiles_n;
   int32_t tile_base;
   int32_t nsplit;
-  void* C;
+  void* C;                    // WGRAD: gradient dW [m][ldc] (stored only when gradients are kept)
   int64_t ldc;
   void* CT;
   int64_t ldct;
   const float* bias;
   const void* mask;
   int64_t ldmask;
-  float* dbias;
+  float* dbias;               // WGRAD: bias gradient (kept gradients only)
+  // WGRAD with the SGD update fused into the epilogue:
+  //   W[m][n] <- fma(-lr, dW[m][n], W[m][n]) (fp32 master, row stride ldc),
+  //   Wb[m][n] <- bf16(W) (bf16 mode), WT[n][m] <- W (transposed copy, storage type),
+  //   bmaster[m] <- fma(-lr, db[m], bmaster[m]).
+  float* W;
+  void* Wb;
+  void* WT;
+  int64_t ldwt;
+  float* bmaster;
 };
 
 // ---------------------------------------------------------------------------
@@ -83,20 +92,29 @@ struct ConvProb {
   int64_t ldws;
 };
 
-// Split-K reduction of conv weight-gradient partials into dW [O][ldgw] and db [O].
+// Split-K reduction of conv weight-gradient partials, in split order, with
+// the SGD update fused: W[o][j] <- fma(-lr, dW, W), its bf16 shadow and its
+// transposed copy WT[c][tap*O + o] (j = tap*C + c), and the bias from column J.
+// dW / db are also stored when gradients are kept (gW / gb non-null).
 struct ReduceProb {
   const float* ws;
   int64_t ldws;
-  int32_t splits, O, J;       // J = KH*KW*C weight columns (+1 bias column in ws)
+  int32_t splits, O, J, C;    // J = KH*KW*C weight columns (+1 bias column in ws)
   int32_t blk_base;
   float* gW;
   int64_t ldgw;
   float* gb;
+  float* W;                   // master [O][ldgw]
+  void* Wb;
+  void* WT;
+  int64_t ldwt;
+  float* bmaster;
 };
 
 // ---------------------------------------------------------------------------
 // Softmax cross-entropy of one model: logits [B][ldl] fp32 -> per-model mean
 // loss, and dz = (softmax - onehot)/B stored as G [B][ldg] and GT [C][ldgt].
+// Row losses are summed per 32-row chunk, then per model, in a fixed order.
 // ---------------------------------------------------------------------------
 struct CeProb {
   const float* logits;
@@ -129,17 +147,18 @@ struct SgdTensor {
 };
 
 // Kernel launch wrappers (kernels.hip). `bf16` selects the storage type.
-hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_prob, int ntiles,
-                       hipStream_t s);
+hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_prob, int ntiles, float lr,
+                       bool keep_grads, hipStream_t s);
 hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles,
                            hipStream_t s);
 hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles,
                              hipStream_t s);
 hipError_t launch_conv_wgrad(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles,
                              hipStream_t s);
-hipError_t launch_reduce(const ReduceProb* probs, const int32_t* blk_prob, int nblocks, hipStream_t s);
+hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
+                         bool keep_grads, hipStream_t s);
 hipError_t launch_ce(bool bf16, const CeProb* probs, int nmodels, const int32_t* labels, int B,
-                     float* losses, hipStream_t s);
+                     float* partial, float* losses, hipStream_t s);
 hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int ntiles, float lr,
                       bool use_grad, hipStream_t s);
 hipError_t launch_load(bool bf16, const float* x, int B, int C, int H, int W, void* X, void* XT,
@@ -152,6 +171,8 @@ constexpr int CONV_BM_BF16 = 128, CONV_BN_BF16 = 128, CONV_BK_BF16 = 64;
 constexpr int CONV_BM_F32 = 64, CONV_BN_F32 = 64, CONV_BK_F32 = 32;
 constexpr int SGD_TILE = 64;
 constexpr int REDUCE_BLOCK = 256;
-constexpr int CE_MAX_BATCH = 8192;
+constexpr int CE_MAX_BATCH = 1 << 20;
+constexpr int CE_ROWS = 32;           // rows per softmax-CE block
+constexpr int CE_LDS_CLASSES = 256;   // classes staged through LDS for the transposed store
 
 }  // namespace un

@@ -144,49 +144,107 @@ __device__ __forceinline__ void mma_block(const T* sA, const T* sB,
   }
 }
 
-// k-blocks [kb0, kb1): global loads of block kb+1 are in flight while block kb
-// is multiplied out of LDS.
+// k-blocks [kb0, kb1), LDS double-buffered: the global loads of block kb+1
+// are in flight while block kb is multiplied out of LDS buffer kb&1, then
+// they are written to the other buffer. One barrier per k-block. `smem`
+// holds 2 * (A_ELEMS + B_ELEMS) elements of T.
 template <typename T, int BM, int BN, int BK, class LA, class LB>
-__device__ __forceinline__ void mma_loop(LA& la, LB& lb, int kb0, int kb1, T* sA, T* sB,
+__device__ __forceinline__ void mma_loop(LA& la, LB& lb, int kb0, int kb1, T* smem,
                                          f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN]) {
+  using TL = Tile<T, BM, BN, BK>;
+  constexpr int STAGE = TL::A_ELEMS + TL::B_ELEMS;
   if (kb0 >= kb1) return;
   la.load(kb0);
   lb.load(kb0);
+  la.store(smem);
+  lb.store(smem + TL::A_ELEMS);
+  __syncthreads();
   for (int kb = kb0; kb < kb1; ++kb) {
-    __syncthreads();
-    la.store(sA);
-    lb.store(sB);
-    __syncthreads();
-    if (kb + 1 < kb1) {
+    const int cur = (kb - kb0) & 1;
+    const bool more = kb + 1 < kb1;
+    if (more) {
       la.load(kb + 1);
       lb.load(kb + 1);
     }
-    mma_block<T, BM, BN, BK>(sA, sB, acc);
+    const T* s = smem + cur * STAGE;
+    mma_block<T, BM, BN, BK>(s, s + TL::A_ELEMS, acc);
+    if (more) {
+      T* d = smem + (cur ^ 1) * STAGE;
+      la.store(d);
+      lb.store(d + TL::A_ELEMS);
+    }
+    __syncthreads();
   }
+}
+
+// LDS of one MFMA kernel: the double-buffered operand tiles, reused by the
+// epilogue as an fp32 [BM][BN + 4] tile.
+template <typename T, int BM, int BN, int BK>
+struct Smem {
+  using TL = Tile<T, BM, BN, BK>;
+  static constexpr int CLD = BN + 4;
+  static constexpr size_t MAIN = 2 * (size_t)(TL::A_ELEMS + TL::B_ELEMS) * sizeof(T);
+  static constexpr size_t EPI = (size_t)BM * CLD * sizeof(float);
+  static constexpr size_t BYTES = MAIN > EPI ? MAIN : EPI;
+};
+
+// Workgroups are dispatched round-robin over the 8 XCDs. Give every XCD a
+// contiguous range of the tile list, so tiles that share an operand block
+// (consecutive tiles) share that XCD's L2.
+__device__ __forceinline__ int xcd_tile(int bid, int nblocks) {
+  const int per = nblocks >> 3;
+  if (bid >= per * 8) return bid;
+  return (bid & 7) * per + (bid >> 3);
 }
 
 // ---------------------------------------------------------------------------
 // Loaders. load(kb) fetches a k-block from global memory into registers,
 // store(s) writes it to LDS as [row][k] (k contiguous, row stride LDK).
 // ---------------------------------------------------------------------------
+// Global memory as seen by the kernels (address space 1: global_load/store
+// instead of flat accesses).
+template <class T> using gptr = __attribute__((address_space(1))) T*;
+template <class T> __device__ __forceinline__ gptr<const T> G(const T* p) { return (gptr<const T>)p; }
+template <class T> __device__ __forceinline__ gptr<T> G(T* p) { return (gptr<T>)p; }
+
+// Raw buffer resource over `bytes` bytes from `base`: loads past the end
+// return zero (CDNA buffer range checking), so tile rows beyond the matrix need
+// no branches. Word 3 is the gfx9-family default (32-bit data format).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  const int n = bytes <= 0 ? 0 : (bytes > 0x7fffffff ? 0x7fffffff : (int)bytes);
+  return __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, n, 0x00020000);
+}
+
 // Row-major operand with k contiguous: element (row, k) = base[row*ld + k].
+// Rows at or beyond rows_valid read as zero through the buffer range check;
+// columns at or beyond K are zeroed on the last, partial k-block only.
 template <typename T, int ROWS, int BK>
 struct RowLoader {
   static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / 256, LDK = BK + VEC;
   static_assert(ROWS * VPR % 256 == 0, "tile too small for 256 threads");
-  const T* base;
-  int64_t ld;
-  int rows_valid, K;
+  __amdgpu_buffer_rsrc_t rsrc;
+  int off[NV];
+  int K;
   u32x4 r[NV];
-  __device__ void load(int kb) {
+  __device__ void init(const T* base, int64_t ld, int rows_valid, int K_) {
+    K = K_;
+    rsrc = make_rsrc(base, (int64_t)rows_valid * ld * (int64_t)sizeof(T));
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
-      const int v = threadIdx.x + 256 * s, row = v / VPR, k = kb * BK + (v % VPR) * VEC;
-      if (row < rows_valid && k < K) {
-        r[s] = *(const u32x4*)(base + row * ld + k);
+      const int v = threadIdx.x + 256 * s;
+      off[s] = (int)(((int64_t)(v / VPR) * ld + (v % VPR) * VEC) * (int64_t)sizeof(T));
+    }
+  }
+  __device__ void load(int kb) {
+    const int kbytes = kb * BK * (int)sizeof(T);
+#pragma unroll
+    for (int s = 0; s < NV; ++s)
+      r[s] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off[s] + kbytes, 0, 0));
+    if ((kb + 1) * BK > K) {
+#pragma unroll
+      for (int s = 0; s < NV; ++s) {
+        const int k = kb * BK + ((threadIdx.x + 256 * s) % VPR) * VEC;
         if (k + VEC > K) vmask_tail<T>(r[s], K - k);
-      } else {
-        r[s] = zero4();
       }
     }
   }
@@ -499,16 +557,58 @@ template <typename T> __device__ __forceinline__ void store4_t(T* dst, const flo
   }
 }
 
+// 16-byte chunk of VE consecutive outputs from fp32 values, as storage type OT.
+template <typename OT> __device__ __forceinline__ void store_chunk(OT* dst, const float* v, int nvalid);
+template <> __device__ __forceinline__ void store_chunk<float>(float* dst, const float* v, int nvalid) {
+  if (nvalid == 4) *(f32x4*)dst = f32x4{v[0], v[1], v[2], v[3]};
+  else
+    for (int e = 0; e < nvalid; ++e) dst[e] = v[e];
+}
+template <> __device__ __forceinline__ void store_chunk<bf16_t>(bf16_t* dst, const float* v, int nvalid) {
+  if (nvalid == 8) {
+    u32x4 w;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) w[q] = (uint32_t)f2bf(v[2 * q]) | ((uint32_t)f2bf(v[2 * q + 1]) << 16);
+    *(u32x4*)dst = w;
+  } else {
+    for (int e = 0; e < nvalid; ++e) dst[e] = f2bf(v[e]);
+  }
+}
+
+// Row-major store of the staged fp32 tile sC [BM][CLD] into C [m][ldc] as OT,
+// one 16-byte chunk per thread and step (coalesced along n).
+template <typename OT, int BM, int BN, int CLD>
+__device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, int m0, int n0, int M, int N) {
+  constexpr int VE = 16 / sizeof(OT), CPR = BN / VE;
+  for (int idx = threadIdx.x; idx < BM * CPR; idx += 256) {
+    const int r = idx / CPR, cc = idx - r * CPR;
+    const int m = m0 + r, n = n0 + cc * VE;
+    if (m >= M || n >= N) continue;
+    float v[VE];
+#pragma unroll
+    for (int e = 0; e < VE; e += 4) {
+      const f32x4 q = *(const f32x4*)(sC + r * CLD + cc * VE + e);
+      v[e] = q[0];
+      v[e + 1] = q[1];
+      v[e + 2] = q[2];
+      v[e + 3] = q[3];
+    }
+    store_chunk<OT>(C + (int64_t)m * ldc + n, v, min(VE, N - n));
+  }
+}
+
 template <typename T, int BM, int BN, int BK>
 __global__ __launch_bounds__(256) void gemm_kernel(const GemmProb* __restrict__ probs,
-                                                   const int32_t* __restrict__ tile_prob) {
+                                                   const int32_t* __restrict__ tile_prob, float lr,
+                                                   int keep_grads) {
   using TL = Tile<T, BM, BN, BK>;
-  __shared__ __attribute__((aligned(16))) T sA[TL::A_ELEMS];
-  __shared__ __attribute__((aligned(16))) T sB[TL::B_ELEMS];
-  const int tile = blockIdx.x;
+  using SM = Smem<T, BM, BN, BK>;
+  __shared__ __attribute__((aligned(16))) char smem[SM::BYTES];
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
   const GemmProb& p = probs[tile_prob[tile]];
   const int local = tile - p.tile_base;
-  const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
+  const int tiles_m = (p.M + BM - 1) / BM;
+  const int tn = local / tiles_m, tm = local - tn * tiles_m;   // m fastest: neighbours share B
   const int m0 = tm * BM, n0 = tn * BN;
 
   f32x4 acc[TL::FM][TL::FN];
@@ -517,48 +617,113 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmProb* __restrict__ 
 #pragma unroll
     for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  RowLoader<T, BM, BK> la{(const T*)p.A + (int64_t)m0 * p.lda, p.lda, p.M - m0, p.K};
-  RowLoader<T, BN, BK> lb{(const T*)p.B + (int64_t)n0 * p.ldb, p.ldb, p.N - n0, p.K};
-  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, sA, sB, acc);
+  RowLoader<T, BM, BK> la;
+  RowLoader<T, BN, BK> lb;
+  la.init((const T*)p.A + (int64_t)m0 * p.lda, p.lda, p.M - m0, p.K);
+  lb.init((const T*)p.B + (int64_t)n0 * p.ldb, p.ldb, p.N - n0, p.K);
+  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
 
+  // Epilogue 1: per-element work in registers, transposed stores straight from
+  // the accumulator layout (4 consecutive m of one n per lane), fp32 tile to LDS.
+  float* sC = (float*)smem;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
+  const int epi = p.epi;
 #pragma unroll
   for (int i = 0; i < TL::FM; ++i) {
-    const int mb = m0 + wm + 16 * i + 4 * (lane >> 4);
-    if (mb >= p.M) continue;
-    const int nv = min(4, p.M - mb);
+    const int rl = wm + 16 * i + 4 * (lane >> 4), mb = m0 + rl;
+    const int nv = max(0, min(4, p.M - mb));
 #pragma unroll
     for (int j = 0; j < TL::FN; ++j) {
-      const int n = n0 + wn + 16 * j + (lane & 15);
-      if (n >= p.N) continue;
+      const int cl = wn + 16 * j + (lane & 15), n = n0 + cl;
       float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
-      if (p.epi == EPI_FWD || p.epi == EPI_LOGITS) {
-        const float b = p.bias[n];
+      if (n < p.N && nv > 0) {
+        if (epi == EPI_FWD || epi == EPI_LOGITS) {
+          const float b = p.bias[n];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          v[r] += b;
-          if (p.relu) v[r] = fmaxf(v[r], 0.f);
-        }
-      } else if (p.epi == EPI_DGRAD && p.relu) {
-        const T* mk = (const T*)p.mask + (int64_t)n * p.ldmask + mb;
+          for (int r = 0; r < 4; ++r) {
+            v[r] += b;
+            if (p.relu) v[r] = fmaxf(v[r], 0.f);
+          }
+        } else if (epi == EPI_DGRAD && p.relu) {
+          const T* mk = (const T*)p.mask + (int64_t)n * p.ldmask + mb;
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (r < nv && !(TT<T>::to_f(mk[r]) > 0.f)) v[r] = 0.f;
-      }
-      if (p.epi == EPI_WGRAD) {
-        if (n < p.nsplit) {
-          for (int r = 0; r < nv; ++r) ((float*)p.C)[(int64_t)(mb + r) * p.ldc + n] = v[r];
-        } else if (n == p.nsplit) {
-          for (int r = 0; r < nv; ++r) p.dbias[mb + r] = v[r];
+          for (int r = 0; r < 4; ++r)
+            if (r < nv && !(TT<T>::to_f(mk[r]) > 0.f)) v[r] = 0.f;
         }
-      } else if (p.epi == EPI_LOGITS) {
-        for (int r = 0; r < nv; ++r) ((float*)p.C)[(int64_t)(mb + r) * p.ldc + n] = v[r];
-      } else {
-        if (p.C)
-          for (int r = 0; r < nv; ++r) store_t<T>(p.C, (int64_t)(mb + r) * p.ldc + n, v[r]);
-        if (p.CT) store4_t<T>((T*)p.CT + (int64_t)n * p.ldct + mb, v, nv);
+        if ((epi == EPI_FWD || epi == EPI_DGRAD) && p.CT) store4_t<T>((T*)p.CT + (int64_t)n * p.ldct + mb, v, nv);
       }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sC[(rl + r) * SM::CLD + cl] = v[r];
+    }
+  }
+  __syncthreads();
+
+  // Epilogue 2: coalesced row-major passes over the staged tile.
+  if (epi == EPI_FWD || epi == EPI_DGRAD) {
+    if (p.C) store_rows<T, BM, BN, SM::CLD>(sC, (T*)p.C, p.ldc, m0, n0, p.M, p.N);
+    return;
+  }
+  if (epi == EPI_LOGITS) {
+    store_rows<float, BM, BN, SM::CLD>(sC, (float*)p.C, p.ldc, m0, n0, p.M, p.N);
+    return;
+  }
+  // EPI_WGRAD: fused SGD. Row pass: W[m][n..n+3] read-modify-write as float4,
+  // bf16 shadow, kept gradient; the bias column (n == nsplit) element-wise.
+  // The updated weights go back to LDS for the transposed copy.
+  constexpr int CPR = BN / 4;
+  const int ns = p.nsplit;
+  for (int idx = threadIdx.x; idx < BM * CPR; idx += 256) {
+    const int r = idx / CPR, cc = idx - r * CPR;
+    const int m = m0 + r, n = n0 + cc * 4;
+    if (m >= p.M || n > ns) continue;
+    float* s = sC + r * SM::CLD + cc * 4;
+    const int64_t base = (int64_t)m * p.ldc + n;
+    if (n + 4 <= ns) {
+      const f32x4 g = *(const f32x4*)s;
+      if (keep_grads) *(f32x4*)((float*)p.C + base) = g;
+      const f32x4 w0 = *(const f32x4*)(p.W + base);
+      const f32x4 w = f32x4{fmaf(-lr, g[0], w0[0]), fmaf(-lr, g[1], w0[1]), fmaf(-lr, g[2], w0[2]),
+                            fmaf(-lr, g[3], w0[3])};
+      *(f32x4*)(p.W + base) = w;
+      if (p.Wb) {
+        u32x2 hb;
+        hb[0] = (uint32_t)f2bf(w[0]) | ((uint32_t)f2bf(w[1]) << 16);
+        hb[1] = (uint32_t)f2bf(w[2]) | ((uint32_t)f2bf(w[3]) << 16);
+        *(u32x2*)((bf16_t*)p.Wb + base) = hb;
+      }
+      *(f32x4*)s = w;
+    } else {
+      for (int e = 0; e < 4 && n + e <= ns && n + e < p.N; ++e) {
+        const float g = s[e];
+        if (n + e < ns) {
+          if (keep_grads) ((float*)p.C)[base + e] = g;
+          const float w = fmaf(-lr, g, p.W[base + e]);
+          p.W[base + e] = w;
+          if (p.Wb) ((bf16_t*)p.Wb)[base + e] = f2bf(w);
+          s[e] = w;
+        } else {
+          if (keep_grads) p.dbias[m] = g;
+          p.bmaster[m] = fmaf(-lr, g, p.bmaster[m]);
+        }
+      }
+    }
+  }
+  if (!p.WT) return;
+  __syncthreads();
+  // Transposed copy WT[n][m]: each lane stores the 4 consecutive m it held.
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i) {
+    const int rl = wm + 16 * i + 4 * (lane >> 4), mb = m0 + rl;
+    const int nv = max(0, min(4, p.M - mb));
+#pragma unroll
+    for (int j = 0; j < TL::FN; ++j) {
+      const int cl = wn + 16 * j + (lane & 15), n = n0 + cl;
+      if (n >= ns || nv == 0) continue;
+      float w4[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) w4[r] = sC[(rl + r) * SM::CLD + cl];
+      store4_t<T>((T*)p.WT + (int64_t)n * p.ldwt + mb, w4, nv);
     }
   }
 }
@@ -570,9 +735,8 @@ template <typename T, int BM, int BN, int BK>
 __global__ __launch_bounds__(256) void conv_fwd_kernel(const ConvProb* __restrict__ probs,
                                                        const int32_t* __restrict__ tile_prob) {
   using TL = Tile<T, BM, BN, BK>;
-  __shared__ __attribute__((aligned(16))) T sA[TL::A_ELEMS];
-  __shared__ __attribute__((aligned(16))) T sB[TL::B_ELEMS];
-  const int tile = blockIdx.x;
+  __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
   const ConvProb& p = probs[tile_prob[tile]];
   const int local = tile - p.tile_base;
   const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
@@ -586,8 +750,9 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(const ConvProb* __restric
 
   Im2colLoader<T, BM, BK> la;
   la.init(p, m0);
-  RowLoader<T, BN, BK> lb{(const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K};
-  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, sA, sB, acc);
+  RowLoader<T, BN, BK> lb;
+  lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K);
+  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
@@ -643,9 +808,8 @@ template <typename T, int BM, int BN, int BK>
 __global__ __launch_bounds__(256) void conv_dgrad_kernel(const ConvProb* __restrict__ probs,
                                                          const int32_t* __restrict__ tile_prob) {
   using TL = Tile<T, BM, BN, BK>;
-  __shared__ __attribute__((aligned(16))) T sA[TL::A_ELEMS];
-  __shared__ __attribute__((aligned(16))) T sB[TL::B_ELEMS];
-  const int tile = blockIdx.x;
+  __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
   const ConvProb& p = probs[tile_prob[tile]];
   const int local = tile - p.tile_base;
   const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
@@ -659,8 +823,9 @@ __global__ __launch_bounds__(256) void conv_dgrad_kernel(const ConvProb* __restr
 
   DzGatherLoader<T, BM, BK> la;
   la.init(p, m0);
-  RowLoader<T, BN, BK> lb{(const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K};
-  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, sA, sB, acc);
+  RowLoader<T, BN, BK> lb;
+  lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K);
+  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
@@ -689,9 +854,8 @@ template <typename T, int BM, int BN, int BK>
 __global__ __launch_bounds__(256) void conv_wgrad_kernel(const ConvProb* __restrict__ probs,
                                                          const int32_t* __restrict__ tile_prob) {
   using TL = Tile<T, BM, BN, BK>;
-  __shared__ __attribute__((aligned(16))) T sA[TL::A_ELEMS];
-  __shared__ __attribute__((aligned(16))) T sB[TL::B_ELEMS];
-  const int tile = blockIdx.x;
+  __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
   const ConvProb& p = probs[tile_prob[tile]];
   int local = tile - p.tile_base;
   const int per_split = p.tiles_m * p.tiles_n;
@@ -712,7 +876,7 @@ __global__ __launch_bounds__(256) void conv_wgrad_kernel(const ConvProb* __restr
   lb.init(p, n0);
   const int nkb = (p.K + BK - 1) / BK;
   const int kb0 = split * p.kchunk, kb1 = min(nkb, kb0 + p.kchunk);
-  mma_loop<T, BM, BN, BK>(la, lb, kb0, kb1, sA, sB, acc);
+  mma_loop<T, BM, BN, BK>(la, lb, kb0, kb1, (T*)smem, acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
@@ -731,9 +895,11 @@ __global__ __launch_bounds__(256) void conv_wgrad_kernel(const ConvProb* __restr
   }
 }
 
-// Sum the split-K partials in split order: dW[o][j] for j < J, db[o] for j == J.
+// Sum the split-K partials in split order, then the fused SGD update.
+template <typename T>
 __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* __restrict__ probs,
-                                                              const int32_t* __restrict__ blk_prob) {
+                                                              const int32_t* __restrict__ blk_prob, float lr,
+                                                              int keep_grads) {
   const ReduceProb& p = probs[blk_prob[blockIdx.x]];
   const int64_t e = (int64_t)(blockIdx.x - p.blk_base) * REDUCE_BLOCK + threadIdx.x;
   const int J1 = p.J + 1;
@@ -741,8 +907,20 @@ __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* 
   const int o = (int)(e / J1), j = (int)(e - (int64_t)o * J1);
   float s = 0.f;
   for (int k = 0; k < p.splits; ++k) s += p.ws[((int64_t)k * p.O + o) * p.ldws + j];
-  if (j < p.J) p.gW[(int64_t)o * p.ldgw + j] = s;
-  else p.gb[o] = s;
+  if (j < p.J) {
+    const int64_t idx = (int64_t)o * p.ldgw + j;
+    if (keep_grads) p.gW[idx] = s;
+    const float w = fmaf(-lr, s, p.W[idx]);
+    p.W[idx] = w;
+    if (p.Wb) ((bf16_t*)p.Wb)[idx] = f2bf(w);
+    if (p.WT) {
+      const int tap = j / p.C, c = j - tap * p.C;
+      store_t<T>(p.WT, (int64_t)c * p.ldwt + (int64_t)tap * p.O + o, w);
+    }
+  } else {
+    if (keep_grads) p.gb[o] = s;
+    p.bmaster[o] = fmaf(-lr, s, p.bmaster[o]);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -759,15 +937,23 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// One block per (model, chunk of CE_ROWS rows); one wave per row at a time,
+// lanes over classes. dz goes to G row-major directly and, through LDS, to GT
+// as runs of consecutive samples. Each block sums its rows' losses in row
+// order into partial[model][chunk]; ce_finish_kernel adds the chunks in order.
 template <typename T>
-__global__ __launch_bounds__(256) void ce_kernel(const CeProb* __restrict__ probs, const int32_t* __restrict__ y,
-                                                 int B, float* __restrict__ losses) {
-  __shared__ float rowloss[CE_MAX_BATCH];
-  __shared__ float part[256];
-  const CeProb& p = probs[blockIdx.x];
+__global__ __launch_bounds__(256) void ce_rows_kernel(const CeProb* __restrict__ probs, const int32_t* __restrict__ y,
+                                                      int B, float* __restrict__ partial, int nchunks) {
+  __shared__ float sdz[CE_ROWS][CE_LDS_CLASSES + 1];
+  __shared__ float rowloss[CE_ROWS];
+  const CeProb& p = probs[blockIdx.y];
+  const int b0 = blockIdx.x * CE_ROWS;
+  const int nrows = min(CE_ROWS, B - b0);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const float invB = 1.0f / (float)B;
-  for (int b = wave; b < B; b += 4) {
+  const bool staged = p.C <= CE_LDS_CLASSES;
+  for (int r = wave; r < nrows; r += 4) {
+    const int b = b0 + r;
     const float* z = p.logits + (int64_t)b * p.ldl;
     float mx = -INFINITY;
     for (int c = lane; c < p.C; c += 64) mx = fmaxf(mx, z[c]);
@@ -776,24 +962,36 @@ __global__ __launch_bounds__(256) void ce_kernel(const CeProb* __restrict__ prob
     for (int c = lane; c < p.C; c += 64) s += expf(z[c] - mx);
     s = wave_sum(s);
     const int yb = y[b];
-    if (lane == 0) rowloss[b] = mx + logf(s) - z[yb];
+    if (lane == 0) rowloss[r] = mx + logf(s) - z[yb];
     const float inv_s = 1.0f / s;
     for (int c = lane; c < p.C; c += 64) {
       const float g = (expf(z[c] - mx) * inv_s - (c == yb ? 1.f : 0.f)) * invB;
       if (p.G) ((T*)p.G)[(int64_t)b * p.ldg + c] = TT<T>::from_f(g);
-      if (p.GT) ((T*)p.GT)[(int64_t)c * p.ldgt + b] = TT<T>::from_f(g);
+      if (staged) sdz[r][c] = g;
+      else if (p.GT) ((T*)p.GT)[(int64_t)c * p.ldgt + b] = TT<T>::from_f(g);
     }
   }
   __syncthreads();
-  float s = 0.f;
-  for (int b = threadIdx.x; b < B; b += 256) s += rowloss[b];
-  part[threadIdx.x] = s;
-  __syncthreads();
-  for (int w = 128; w >= 1; w >>= 1) {
-    if (threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
-    __syncthreads();
+  if (staged && p.GT) {
+    for (int idx = threadIdx.x; idx < p.C * CE_ROWS; idx += 256) {
+      const int c = idx / CE_ROWS, r = idx - c * CE_ROWS;
+      if (r < nrows) ((T*)p.GT)[(int64_t)c * p.ldgt + b0 + r] = TT<T>::from_f(sdz[r][c]);
+    }
   }
-  if (threadIdx.x == 0) losses[p.model] = part[0] * invB;
+  if (threadIdx.x == 0) {
+    float s = 0.f;
+    for (int r = 0; r < nrows; ++r) s += rowloss[r];
+    partial[(int64_t)p.model * nchunks + blockIdx.x] = s;
+  }
+}
+
+__global__ void ce_finish_kernel(const float* __restrict__ partial, int nchunks, int nmodels, int B,
+                                 float* __restrict__ losses) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= nmodels) return;
+  float s = 0.f;
+  for (int k = 0; k < nchunks; ++k) s += partial[(int64_t)m * nchunks + k];
+  losses[m] = s * (1.0f / (float)B);
 }
 
 // ---------------------------------------------------------------------------
@@ -863,14 +1061,15 @@ __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, 
 // ---------------------------------------------------------------------------
 // Launch wrappers
 // ---------------------------------------------------------------------------
-hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_prob, int ntiles, hipStream_t s) {
+hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_prob, int ntiles, float lr,
+                       bool keep_grads, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   if (bf16)
     hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, 64>), dim3(ntiles), dim3(256), 0, s, probs,
-                       tile_prob);
+                       tile_prob, lr, (int)keep_grads);
   else
     hipLaunchKernelGGL((gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, 32>), dim3(ntiles), dim3(256), 0, s, probs,
-                       tile_prob);
+                       tile_prob, lr, (int)keep_grads);
   return hipGetLastError();
 }
 
@@ -907,19 +1106,30 @@ hipError_t launch_conv_wgrad(bool bf16, const ConvProb* probs, const int32_t* ti
   return hipGetLastError();
 }
 
-hipError_t launch_reduce(const ReduceProb* probs, const int32_t* blk_prob, int nblocks, hipStream_t s) {
+hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
+                         bool keep_grads, hipStream_t s) {
   if (nblocks <= 0) return hipSuccess;
-  hipLaunchKernelGGL(reduce_kernel, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob);
+  if (bf16)
+    hipLaunchKernelGGL(reduce_kernel<bf16_t>, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob, lr,
+                       (int)keep_grads);
+  else
+    hipLaunchKernelGGL(reduce_kernel<float>, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob, lr,
+                       (int)keep_grads);
   return hipGetLastError();
 }
 
-hipError_t launch_ce(bool bf16, const CeProb* probs, int nmodels, const int32_t* labels, int B, float* losses,
-                     hipStream_t s) {
+hipError_t launch_ce(bool bf16, const CeProb* probs, int nmodels, const int32_t* labels, int B, float* partial,
+                     float* losses, hipStream_t s) {
   if (nmodels <= 0) return hipSuccess;
+  const int nchunks = (B + CE_ROWS - 1) / CE_ROWS;
   if (bf16)
-    hipLaunchKernelGGL(ce_kernel<bf16_t>, dim3(nmodels), dim3(256), 0, s, probs, labels, B, losses);
+    hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nmodels), dim3(256), 0, s, probs, labels, B, partial,
+                       nchunks);
   else
-    hipLaunchKernelGGL(ce_kernel<float>, dim3(nmodels), dim3(256), 0, s, probs, labels, B, losses);
+    hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nmodels), dim3(256), 0, s, probs, labels, B, partial,
+                       nchunks);
+  hipLaunchKernelGGL(ce_finish_kernel, dim3((nmodels + 63) / 64), dim3(64), 0, s, partial, nchunks, nmodels, B,
+                     losses);
   return hipGetLastError();
 }
 

@@ -47,6 +47,7 @@ struct Block {
   size_t pt_w = 0, pt_b = 0, n_w = 0, n_b = 0;
   // arena offsets (NONE = absent)
   size_t W32 = NONE, b32 = NONE, gW = NONE, gb = NONE, Wb = NONE, WT = NONE;
+  size_t WT2 = NONE;       // Linear: second transposed copy (written while the dgrad reads WT)
   int64_t ldw = 0, ldwt = 0;
   int rows = 0;            // logical weight rows (N or O)
   size_t X = NONE, XT = NONE;
@@ -96,11 +97,13 @@ struct un_ctx {
   size_t bytes = 0;
   hipStream_t stream = nullptr;
   // fixed buffers
-  size_t xstage = NONE, ydev = NONE, losses_dev = NONE, Xin = NONE, XinT = NONE;
+  size_t xstage = NONE, ydev = NONE, losses_dev = NONE, ce_partial = NONE, Xin = NONE, XinT = NONE;
   int64_t ldxin = 0, ldxint = 0;
   // schedule
-  std::vector<Launch> fwd, bwd;
-  Launch ce{}, sgd{}, refresh{};
+  std::vector<Launch> fwd, bwd[2];  // bwd[p]: dgrad reads copy p of the transposed weights
+  Launch ce{}, refresh[2]{};
+  int wt_cur = 0;                     // which transposed copy the next dgrad reads
+  bool keep_grads = false, grads_valid = false;
   int ce_count = 0;
   bool loaded = false, stepped = false, poisoned = false;
   int min_classes = 0;
@@ -314,6 +317,7 @@ static un_status plan_and_alloc(un_ctx* c) {
   c->xstage = A.take((size_t)B * in_feat * 4);
   c->ydev = A.take((size_t)B * 4);
   c->losses_dev = A.take(c->models.size() * 4);
+  c->ce_partial = A.take(c->models.size() * (size_t)cdiv(B, CE_ROWS) * 4);
   c->Xin = A.take((size_t)B * in_feat * es);
   c->ldxin = in_feat;
   bool any_linear0 = false;
@@ -398,6 +402,7 @@ static un_status plan_and_alloc(un_ctx* c) {
         if (j > 0) {
           b.ldwt = rup(b.N, 8);
           b.WT = A.take((size_t)b.K * b.ldwt * es);
+          b.WT2 = A.take((size_t)b.K * b.ldwt * es);
         }
       } else {
         const int J = b.KH * b.KH * b.C;
@@ -462,7 +467,7 @@ static un_status plan_and_alloc(un_ctx* c) {
     memcpy(host_tables.data() + off, src, n);
     return off;
   };
-  std::vector<Launch> fwd, bwd;
+  std::vector<Launch> fwd, bwd[2];
   auto ptr = [&](size_t off) -> void* { return off == NONE ? nullptr : (void*)(uintptr_t)(off + 1); };
   // Pointers are encoded as (arena offset + 1) and fixed up after the arena exists.
   std::vector<size_t> fix;  // byte offsets (in host_tables) of pointer fields to relocate
@@ -483,7 +488,9 @@ static un_status plan_and_alloc(un_ctx* c) {
     for (size_t k = 0; k < ps.size(); ++k) {
       size_t b0 = po + k * sizeof(GemmProb);
       for (size_t f : {offsetof(GemmProb, A), offsetof(GemmProb, B), offsetof(GemmProb, C), offsetof(GemmProb, CT),
-                       offsetof(GemmProb, bias), offsetof(GemmProb, mask), offsetof(GemmProb, dbias)})
+                       offsetof(GemmProb, bias), offsetof(GemmProb, mask), offsetof(GemmProb, dbias),
+                       offsetof(GemmProb, W), offsetof(GemmProb, Wb), offsetof(GemmProb, WT),
+                       offsetof(GemmProb, bmaster)})
         fix.push_back(b0 + f);
     }
     size_t mo = put(map.data(), map.size() * 4);
@@ -621,7 +628,10 @@ static un_status plan_and_alloc(un_ctx* c) {
     c->ce = Launch{5, UN_K_CE, po, NONE, (int)ces.size()};
   }
 
-  // backward levels
+  // backward levels, once per parity of the transposed-weight copies: the
+  // dgrad of a level reads copy `par` while the fused update of the same
+  // launch writes the other copy.
+  for (int par = 0; par < 2; ++par)
   for (int lv = levels - 1; lv >= 0; --lv) {
     std::vector<GemmProb> gp;
     std::vector<ConvProb> dp, wp;
@@ -637,7 +647,7 @@ static un_status plan_and_alloc(un_ctx* c) {
           GemmProb p{};
           p.A = ptr(b.G);
           p.lda = b.ldg;
-          p.B = ptr(b.WT);
+          p.B = ptr(par == 0 ? b.WT : b.WT2);
           p.ldb = b.ldwt;
           p.M = B;
           p.N = b.K;
@@ -674,6 +684,9 @@ static un_status plan_and_alloc(un_ctx* c) {
           p.C = ptr(catgW);
           p.ldc = kin_p;
           p.dbias = (float*)ptr(catgb);
+          p.W = (float*)ptr(catW32);
+          p.Wb = ptr(catWb);
+          p.bmaster = (float*)ptr(catb32);
           gp.push_back(p);
           continue;
         }
@@ -690,6 +703,11 @@ static un_status plan_and_alloc(un_ctx* c) {
         p.C = ptr(b.gW);
         p.ldc = b.ldw;
         p.dbias = (float*)ptr(b.gb);
+        p.W = (float*)ptr(b.W32);
+        p.Wb = ptr(b.Wb);
+        p.WT = ptr(par == 0 ? b.WT2 : b.WT);
+        p.ldwt = b.ldwt;
+        p.bmaster = (float*)ptr(b.b32);
         gp.push_back(p);
       } else {
         const int J = b.KH * b.KH * b.C;
@@ -725,15 +743,21 @@ static un_status plan_and_alloc(un_ctx* c) {
         r.splits = b.splits;
         r.O = b.O;
         r.J = J;
+        r.C = b.C;
         r.gW = (float*)ptr(b.gW);
         r.ldgw = b.ldw;
         r.gb = (float*)ptr(b.gb);
+        r.W = (float*)ptr(b.W32);
+        r.Wb = ptr(b.Wb);
+        r.WT = ptr(b.WT);  // conv: the dgrad launch of this level has completed
+        r.ldwt = b.ldwt;
+        r.bmaster = (float*)ptr(b.b32);
         rp.push_back(r);
       }
     }
-    emit_gemm(gp, bwd, UN_K_GEMM_BWD);
-    emit_conv(dp, bwd, 2, UN_K_CONV_DGRAD);
-    emit_conv(wp, bwd, 3, UN_K_CONV_WGRAD);
+    emit_gemm(gp, bwd[par], UN_K_GEMM_BWD);
+    emit_conv(dp, bwd[par], 2, UN_K_CONV_DGRAD);
+    emit_conv(wp, bwd[par], 3, UN_K_CONV_WGRAD);
     if (!rp.empty()) {
       std::vector<int32_t> map;
       for (size_t k = 0; k < rp.size(); ++k) {
@@ -744,15 +768,18 @@ static un_status plan_and_alloc(un_ctx* c) {
       size_t po = put(rp.data(), rp.size() * sizeof(ReduceProb));
       for (size_t k = 0; k < rp.size(); ++k) {
         size_t b0 = po + k * sizeof(ReduceProb);
-        for (size_t f : {offsetof(ReduceProb, ws), offsetof(ReduceProb, gW), offsetof(ReduceProb, gb)})
+        for (size_t f : {offsetof(ReduceProb, ws), offsetof(ReduceProb, gW), offsetof(ReduceProb, gb),
+                         offsetof(ReduceProb, W), offsetof(ReduceProb, Wb), offsetof(ReduceProb, WT),
+                         offsetof(ReduceProb, bmaster)})
           fix.push_back(b0 + f);
       }
       size_t mo = put(map.data(), map.size() * 4);
-      bwd.push_back(Launch{4, UN_K_OTHER, po, mo, (int)map.size()});
+      bwd[par].push_back(Launch{4, UN_K_OTHER, po, mo, (int)map.size()});
     }
   }
 
-  // SGD tensors (weights and biases of every block)
+  // Shadow refresh (after un_set_params / initialisation): rewrite the bf16
+  // shadow and transposed copy `pass` of every weight from the fp32 master.
   for (int pass = 0; pass < 2; ++pass) {
     std::vector<SgdTensor> ts;
     std::vector<int32_t> map;
@@ -768,9 +795,8 @@ static un_status plan_and_alloc(un_ctx* c) {
       for (auto& b : m.blocks) {
         SgdTensor w{};
         w.W = (float*)ptr(b.W32);
-        w.G = pass == 0 ? (const float*)ptr(b.gW) : nullptr;
         w.Wb = ptr(b.Wb);
-        w.WT = ptr(b.WT);
+        w.WT = ptr(pass == 1 && b.WT2 != NONE ? b.WT2 : b.WT);
         w.ldw = b.ldw;
         w.ldwt = b.ldwt;
         w.R = b.rows;
@@ -782,16 +808,6 @@ static un_status plan_and_alloc(un_ctx* c) {
           w.Cc = b.C;
         }
         add(w);
-        if (pass == 0) {
-          SgdTensor t{};
-          t.W = (float*)ptr(b.b32);
-          t.G = (const float*)ptr(b.gb);
-          t.ldw = b.rows;
-          t.R = 1;
-          t.J = 1;
-          t.Cc = b.rows;
-          add(t);
-        }
       }
     size_t po = put(ts.data(), ts.size() * sizeof(SgdTensor));
     for (size_t k = 0; k < ts.size(); ++k) {
@@ -800,7 +816,7 @@ static un_status plan_and_alloc(un_ctx* c) {
         fix.push_back(b0 + f);
     }
     size_t mo = put(map.data(), map.size() * 4);
-    (pass == 0 ? c->sgd : c->refresh) = Launch{6, UN_K_SGD, po, mo, (int)map.size()};
+    c->refresh[pass] = Launch{6, UN_K_SGD, po, mo, (int)map.size()};
   }
 
   // --- allocate the arena: buffers + tables
@@ -823,12 +839,14 @@ static un_status plan_and_alloc(un_ctx* c) {
     if (l.map != NONE) l.map += tables_off;
   };
   for (auto& l : fwd) relocate(l);
-  for (auto& l : bwd) relocate(l);
+  for (int p = 0; p < 2; ++p)
+    for (auto& l : bwd[p]) relocate(l);
   relocate(c->ce);
-  relocate(c->sgd);
-  relocate(c->refresh);
+  relocate(c->refresh[0]);
+  relocate(c->refresh[1]);
   c->fwd = fwd;
-  c->bwd = bwd;
+  c->bwd[0] = bwd[0];
+  c->bwd[1] = bwd[1];
 
   HIPCHK(c, hipMemsetAsync(c->base, 0, c->bytes, c->stream));
   HIPCHK(c, hipMemcpyAsync(c->base + tables_off, host_tables.data(), host_tables.size(), hipMemcpyHostToDevice,
@@ -903,8 +921,8 @@ static void from_internal(const Block& b, const std::vector<float>& w, const std
 }
 
 static un_status refresh_shadows(un_ctx* c) {
-  HIPCHK(c, launch_sgd(c->bf16, c->at<SgdTensor>(c->refresh.probs), c->at<int32_t>(c->refresh.map), c->refresh.count,
-                       0.f, false, c->stream));
+  const Launch& l = c->refresh[c->wt_cur];
+  HIPCHK(c, launch_sgd(c->bf16, c->at<SgdTensor>(l.probs), c->at<int32_t>(l.map), l.count, 0.f, false, c->stream));
   return UN_OK;
 }
 
@@ -913,8 +931,10 @@ static un_status write_params(un_ctx* c, int i, const float* src) {
   std::vector<float> w, bias;
   for (auto& b : m.blocks) {
     to_internal(b, src, w, bias);
-    HIPCHK(c, hipMemcpy(c->base + b.W32, w.data(), w.size() * 4, hipMemcpyHostToDevice));
-    HIPCHK(c, hipMemcpy(c->base + b.b32, bias.data(), bias.size() * 4, hipMemcpyHostToDevice));
+    // on the context's stream, completed before the host buffers go away
+    HIPCHK(c, hipMemcpyAsync(c->base + b.W32, w.data(), w.size() * 4, hipMemcpyHostToDevice, c->stream));
+    HIPCHK(c, hipMemcpyAsync(c->base + b.b32, bias.data(), bias.size() * 4, hipMemcpyHostToDevice, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
   }
   return UN_OK;
 }
@@ -926,8 +946,11 @@ static un_status read_tensors(un_ctx* c, int i, bool grads, float* dst) {
   for (auto& b : m.blocks) {
     w.resize((size_t)b.rows * b.ldw);
     bias.resize(b.rows);
-    HIPCHK(c, hipMemcpy(w.data(), c->base + (grads ? b.gW : b.W32), w.size() * 4, hipMemcpyDeviceToHost));
-    HIPCHK(c, hipMemcpy(bias.data(), c->base + (grads ? b.gb : b.b32), bias.size() * 4, hipMemcpyDeviceToHost));
+    HIPCHK(c, hipMemcpyAsync(w.data(), c->base + (grads ? b.gW : b.W32), w.size() * 4, hipMemcpyDeviceToHost,
+                             c->stream));
+    HIPCHK(c, hipMemcpyAsync(bias.data(), c->base + (grads ? b.gb : b.b32), bias.size() * 4, hipMemcpyDeviceToHost,
+                             c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
     from_internal(b, w, bias, dst);
   }
   return UN_OK;
@@ -976,7 +999,8 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
   hipError_t e = hipSuccess;
   switch (l.kind) {
     case 0:
-      e = launch_gemm(c->bf16, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
+      e = launch_gemm(c->bf16, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->keep_grads,
+                      c->stream);
       break;
     case 1:
       e = launch_conv_fwd(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
@@ -988,11 +1012,12 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
       e = launch_conv_wgrad(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
       break;
     case 4:
-      e = launch_reduce(c->at<ReduceProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
+      e = launch_reduce(c->bf16, c->at<ReduceProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->keep_grads,
+                        c->stream);
       break;
     case 5:
       e = launch_ce(c->bf16, c->at<CeProb>(l.probs), l.count, c->at<int32_t>(c->ydev), c->B,
-                    c->at<float>(c->losses_dev), c->stream);
+                    c->at<float>(c->ce_partial), c->at<float>(c->losses_dev), c->stream);
       break;
     case 6:
       e = launch_sgd(c->bf16, c->at<SgdTensor>(l.probs), c->at<int32_t>(l.map), l.count, lr, true, c->stream);
@@ -1038,7 +1063,7 @@ un_status un_create(const un_model_spec* specs, int32_t n_models, const un_input
   if (!specs || !in || n_models <= 0) return fail(nullptr, UN_ERR_INVALID, "specs/in NULL or n_models <= 0");
   if (in->batch <= 0 || in->in_c <= 0 || in->in_h <= 0 || in->in_w <= 0)
     return fail(nullptr, UN_ERR_INVALID, "input dimensions must be positive");
-  if (in->batch > CE_MAX_BATCH) return fail(nullptr, UN_ERR_UNSUPPORTED, "batch larger than 8192");
+  if (in->batch > CE_MAX_BATCH) return fail(nullptr, UN_ERR_UNSUPPORTED, "batch larger than 2^20");
   if (in->precision != UN_F32 && in->precision != UN_BF16_F32MASTER)
     return fail(nullptr, UN_ERR_INVALID, "unknown precision");
   un_ctx* c = new un_ctx();
@@ -1093,7 +1118,8 @@ static un_status load_common(un_ctx* c, const float* x, const int32_t* y, bool d
   const size_t nx = (size_t)c->B * c->in_c * c->in_h * c->in_w;
   std::vector<int32_t> yh(c->B);
   if (device) {
-    HIPCHK(c, hipMemcpy(yh.data(), y, (size_t)c->B * 4, hipMemcpyDeviceToHost));
+    HIPCHK(c, hipMemcpyAsync(yh.data(), y, (size_t)c->B * 4, hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
   } else {
     memcpy(yh.data(), y, (size_t)c->B * 4);
   }
@@ -1131,9 +1157,10 @@ un_status un_step(un_ctx* c, float lr, float* losses) {
   if (!std::isfinite(lr)) return fail(c, UN_ERR_INVALID, "lr is not finite");
   for (auto& l : c->fwd) HIPCHK(c, run_launch(c, l, lr));
   HIPCHK(c, run_launch(c, c->ce, lr));
-  for (auto& l : c->bwd) HIPCHK(c, run_launch(c, l, lr));
-  HIPCHK(c, run_launch(c, c->sgd, lr));
+  for (auto& l : c->bwd[c->wt_cur]) HIPCHK(c, run_launch(c, l, lr));
+  c->wt_cur ^= 1;
   c->stepped = true;
+  c->grads_valid = c->keep_grads;
   if (c->profiling && c->recs.size() > 4096) {
     un_status s = drain_profile(c);
     if (s != UN_OK) return s;
@@ -1169,6 +1196,7 @@ un_status un_get_grads(un_ctx* c, int32_t i, float* dst, size_t cap, size_t* n) 
   if (n) *n = np;
   if (!dst) return UN_OK;
   if (!c->stepped) return fail(c, UN_ERR_STATE, "no step has run yet");
+  if (!c->grads_valid) return fail(c, UN_ERR_STATE, "the last step did not keep gradients (see un_keep_grads)");
   if (cap < np) return fail(c, UN_ERR_BUFSIZE, "buffer too small");
   return read_tensors(c, i, true, dst);
 }
@@ -1184,6 +1212,12 @@ un_status un_set_params(un_ctx* c, int32_t i, const float* src, size_t n) {
   s = refresh_shadows(c);
   if (s != UN_OK) return s;
   HIPCHK(c, hipStreamSynchronize(c->stream));
+  return UN_OK;
+}
+
+un_status un_keep_grads(un_ctx* c, int32_t enable) {
+  CHECK_CTX(c);
+  c->keep_grads = enable != 0;
   return UN_OK;
 }
 

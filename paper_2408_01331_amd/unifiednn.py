@@ -26,7 +26,7 @@ KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad"
 
 # Every symbol the header declares.
 EXPORTS = ["un_create", "un_load_batch", "un_load_batch_device", "un_step", "un_get_params", "un_set_params",
-           "un_get_grads", "un_param_count", "un_arena_bytes", "un_sync", "un_get_stream", "un_profile_enable",
+           "un_get_grads", "un_keep_grads", "un_param_count", "un_arena_bytes", "un_sync", "un_get_stream", "un_profile_enable",
            "un_profile_read", "un_destroy", "un_last_error"]
 
 
@@ -72,6 +72,7 @@ def lib():
             "un_get_params": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t, c_size_p]),
             "un_set_params": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t]),
             "un_get_grads": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t, c_size_p]),
+            "un_keep_grads": (ctypes.c_int, [P, ctypes.c_int32]),
             "un_param_count": (ctypes.c_int, [P, ctypes.c_int32, c_size_p]),
             "un_arena_bytes": (ctypes.c_int, [P, c_size_p]),
             "un_sync": (ctypes.c_int, [P]),
@@ -171,6 +172,10 @@ def un_get_grads(ctx, i):
     return out
 
 
+def un_keep_grads(ctx, on):
+    _check(lib().un_keep_grads(ctx, 1 if on else 0), ctx)
+
+
 def un_set_params(ctx, i, flat):
     flat = np.ascontiguousarray(flat, dtype=np.float32)
     _check(lib().un_set_params(ctx, i, _fp(flat), flat.size), ctx)
@@ -263,6 +268,9 @@ class Hybrid:
 
     def get_grads(self, i):
         return un_get_grads(self.ctx, i)
+
+    def keep_grads(self, on=True):
+        un_keep_grads(self.ctx, on)
 
     def sync(self):
         un_sync(self.ctx)

@@ -31,6 +31,7 @@ def run_gpu(wl, steps, lr=None, theta=None, models=None):
     lr = wl.lr if lr is None else lr
     idx = range(wl.n_models) if models is None else models
     with Hybrid(wl.specs, wl.batch, wl.in_shape, wl.precision) as h:
+        h.keep_grads(True)
         for i in range(wl.n_models):
             p = theta0(wl, i) if theta is None or i not in theta else theta[i]
             h.set_params(i, flatten_params(p))

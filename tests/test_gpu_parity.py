@@ -148,6 +148,7 @@ def test_lr_zero_leaves_params_bitwise_and_sgd_is_fma():
         th = [flatten_params(theta0(wl, i)) for i in range(wl.n_models)]
         for i in range(wl.n_models):
             h.set_params(i, th[i])
+        h.keep_grads(True)
         h.load_batch(x, y)
         h.step(0.0)
         for i in range(wl.n_models):
