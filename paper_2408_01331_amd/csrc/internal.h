@@ -114,7 +114,7 @@ struct ReduceProb {
 // ---------------------------------------------------------------------------
 // Softmax cross-entropy of one model: logits [B][ldl] fp32 -> per-model mean
 // loss, and dz = (softmax - onehot)/B stored as G [B][ldg] and GT [C][ldgt].
-// Row losses are summed per 32-row chunk, then per model, in a fixed order.
+// Row losses are summed per 64-row chunk, then per model, in a fixed order.
 // ---------------------------------------------------------------------------
 struct CeProb {
   const float* logits;
@@ -148,7 +148,7 @@ struct SgdTensor {
 
 // Kernel launch wrappers (kernels.hip). `bf16` selects the storage type.
 hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_prob, int ntiles, float lr,
-                       bool keep_grads, hipStream_t s);
+                       bool keep_grads, bool xcd_remap, hipStream_t s);
 hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles,
                            hipStream_t s);
 hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles,
@@ -172,7 +172,6 @@ constexpr int CONV_BM_F32 = 64, CONV_BN_F32 = 64, CONV_BK_F32 = 32;
 constexpr int SGD_TILE = 64;
 constexpr int REDUCE_BLOCK = 256;
 constexpr int CE_MAX_BATCH = 1 << 20;
-constexpr int CE_ROWS = 32;           // rows per softmax-CE block
-constexpr int CE_LDS_CLASSES = 256;   // classes staged through LDS for the transposed store
+constexpr int CE_ROWS = 64;           // rows (threads) per softmax-CE block
 
 }  // namespace un

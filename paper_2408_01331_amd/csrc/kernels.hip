@@ -16,6 +16,10 @@
 
 #include "internal.h"
 
+#ifndef UN_LDS_PAD_CHUNKS
+#define UN_LDS_PAD_CHUNKS 1
+#endif
+
 namespace un {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -92,7 +96,7 @@ __device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
 template <typename T, int BM, int BN, int BK>
 struct Tile {
   static constexpr int VEC = TT<T>::VEC;
-  static constexpr int LDK = BK + VEC;  // LDS row stride in elements (16 B pad)
+  static constexpr int LDK = BK + UN_LDS_PAD_CHUNKS * VEC;  // LDS row stride in elements (16-byte pad chunks)
   static constexpr int WM = BM / 2, WN = BN / 2;
   static constexpr int FM = WM / 16, FN = WN / 16;
   static constexpr int A_ELEMS = BM * LDK, B_ELEMS = BN * LDK;
@@ -145,33 +149,34 @@ __device__ __forceinline__ void mma_block(const T* sA, const T* sB,
 }
 
 // k-blocks [kb0, kb1), LDS double-buffered: the global loads of block kb+1
-// are in flight while block kb is multiplied out of LDS buffer kb&1, then
-// they are written to the other buffer. One barrier per k-block. `smem`
-// holds 2 * (A_ELEMS + B_ELEMS) elements of T.
+// are in flight while block kb is multiplied out of LDS buffer (kb-kb0)&1,
+// then they are written to the other buffer. One barrier per k-block.
+// `smem` holds 2 * (A_ELEMS + B_ELEMS) elements of T. (Loaders have two
+// register slots; this loop uses slot 0.)
 template <typename T, int BM, int BN, int BK, class LA, class LB>
 __device__ __forceinline__ void mma_loop(LA& la, LB& lb, int kb0, int kb1, T* smem,
                                          f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN]) {
   using TL = Tile<T, BM, BN, BK>;
   constexpr int STAGE = TL::A_ELEMS + TL::B_ELEMS;
   if (kb0 >= kb1) return;
-  la.load(kb0);
-  lb.load(kb0);
-  la.store(smem);
-  lb.store(smem + TL::A_ELEMS);
+  la.template load<0>(kb0);
+  lb.template load<0>(kb0);
+  la.template store<0>(smem);
+  lb.template store<0>(smem + TL::A_ELEMS);
   __syncthreads();
   for (int kb = kb0; kb < kb1; ++kb) {
     const int cur = (kb - kb0) & 1;
     const bool more = kb + 1 < kb1;
     if (more) {
-      la.load(kb + 1);
-      lb.load(kb + 1);
+      la.template load<0>(kb + 1);
+      lb.template load<0>(kb + 1);
     }
     const T* s = smem + cur * STAGE;
     mma_block<T, BM, BN, BK>(s, s + TL::A_ELEMS, acc);
     if (more) {
       T* d = smem + (cur ^ 1) * STAGE;
-      la.store(d);
-      lb.store(d + TL::A_ELEMS);
+      la.template store<0>(d);
+      lb.template store<0>(d + TL::A_ELEMS);
     }
     __syncthreads();
   }
@@ -220,12 +225,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
 // columns at or beyond K are zeroed on the last, partial k-block only.
 template <typename T, int ROWS, int BK>
 struct RowLoader {
-  static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / 256, LDK = BK + VEC;
+  static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / 256, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
   static_assert(ROWS * VPR % 256 == 0, "tile too small for 256 threads");
   __amdgpu_buffer_rsrc_t rsrc;
   int off[NV];
   int K;
-  u32x4 r[NV];
+  u32x4 r[2][NV];
   __device__ void init(const T* base, int64_t ld, int rows_valid, int K_) {
     K = K_;
     rsrc = make_rsrc(base, (int64_t)rows_valid * ld * (int64_t)sizeof(T));
@@ -235,24 +240,26 @@ struct RowLoader {
       off[s] = (int)(((int64_t)(v / VPR) * ld + (v % VPR) * VEC) * (int64_t)sizeof(T));
     }
   }
+  template <int S>
   __device__ void load(int kb) {
     const int kbytes = kb * BK * (int)sizeof(T);
 #pragma unroll
     for (int s = 0; s < NV; ++s)
-      r[s] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off[s] + kbytes, 0, 0));
+      r[S][s] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off[s] + kbytes, 0, 0));
     if ((kb + 1) * BK > K) {
 #pragma unroll
       for (int s = 0; s < NV; ++s) {
         const int k = kb * BK + ((threadIdx.x + 256 * s) % VPR) * VEC;
-        if (k + VEC > K) vmask_tail<T>(r[s], K - k);
+        if (k + VEC > K) vmask_tail<T>(r[S][s], K - k);
       }
     }
   }
+  template <int S>
   __device__ void store(T* sm) const {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + 256 * s;
-      *(u32x4*)(sm + (v / VPR) * LDK + (v % VPR) * VEC) = r[s];
+      *(u32x4*)(sm + (v / VPR) * LDK + (v % VPR) * VEC) = r[S][s];
     }
   }
 };
@@ -277,11 +284,11 @@ __device__ __forceinline__ void decode_out_pixel(const ConvProb& p, int m, int& 
 // Conv forward A operand: rows = output pixels, k = (u, v, c).
 template <typename T, int ROWS, int BK>
 struct Im2colLoader {
-  static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / 256, LDK = BK + VEC;
+  static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / 256, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
   const ConvProb* p;
   const T* X;
   int rn[NV], ry[NV], rx[NV];
-  u32x4 r[NV];
+  u32x4 r[2][NV];
   __device__ void init(const ConvProb& pr, int m0) {
     p = &pr;
     X = (const T*)pr.X;
@@ -292,6 +299,7 @@ struct Im2colLoader {
       else rn[s] = -1;
     }
   }
+  template <int S>
   __device__ void load(int kb) {
     const int C = p->C, H = p->H, W = p->W, KW = p->KH, pad = p->pad, K = p->K;
     const bool vec = (C % VEC) == 0;
@@ -317,14 +325,15 @@ struct Im2colLoader {
           }
         }
       }
-      r[s] = v;
+      r[S][s] = v;
     }
   }
+  template <int S>
   __device__ void store(T* sm) const {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + 256 * s;
-      *(u32x4*)(sm + (v / VPR) * LDK + (v % VPR) * VEC) = r[s];
+      *(u32x4*)(sm + (v / VPR) * LDK + (v % VPR) * VEC) = r[S][s];
     }
   }
 };
@@ -360,11 +369,11 @@ template <typename T> __device__ __forceinline__ void select_am(u32x4& v, uint64
 // Conv dgrad A operand: rows = conv input pixels (n, y, x), k = (u, v, o).
 template <typename T, int ROWS, int BK>
 struct DzGatherLoader {
-  static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / 256, LDK = BK + VEC;
+  static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / 256, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
   const ConvProb* p;
   const T* G;
   int rn[NV], ry[NV], rx[NV];
-  u32x4 r[NV];
+  u32x4 r[2][NV];
   __device__ void init(const ConvProb& pr, int m0) {
     p = &pr;
     G = (const T*)pr.G;
@@ -382,6 +391,7 @@ struct DzGatherLoader {
       }
     }
   }
+  template <int S>
   __device__ void load(int kb) {
     const int O = p->O, KW = p->KH, pad = p->pad, K = p->K;
     const bool vec = (O % VEC) == 0;
@@ -412,14 +422,15 @@ struct DzGatherLoader {
           }
         }
       }
-      r[s] = v;
+      r[S][s] = v;
     }
   }
+  template <int S>
   __device__ void store(T* sm) const {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + 256 * s;
-      *(u32x4*)(sm + (v / VPR) * LDK + (v % VPR) * VEC) = r[s];
+      *(u32x4*)(sm + (v / VPR) * LDK + (v % VPR) * VEC) = r[S][s];
     }
   }
 };
@@ -428,16 +439,17 @@ struct DzGatherLoader {
 // Global vectors run along o; they are written to LDS transposed.
 template <typename T, int ROWS, int BK>
 struct DzRowsLoader {
-  static constexpr int VEC = TT<T>::VEC, VPM = ROWS / VEC, NV = ROWS * BK / VEC / 256, LDK = BK + VEC;
+  static constexpr int VEC = TT<T>::VEC, VPM = ROWS / VEC, NV = ROWS * BK / VEC / 256, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
   const ConvProb* p;
   const T* G;
   int m0;
-  u32x4 r[NV];
+  u32x4 r[2][NV];
   __device__ void init(const ConvProb& pr, int m0_) {
     p = &pr;
     G = (const T*)pr.G;
     m0 = m0_;
   }
+  template <int S>
   __device__ void load(int kb) {
     const int O = p->O;
     const bool vec = (O % VEC) == 0;
@@ -465,15 +477,16 @@ struct DzRowsLoader {
               vset_bits<T>(val, e, bits_of<T>(G[idx + o0 + e]));
         }
       }
-      r[s] = val;
+      r[S][s] = val;
     }
   }
+  template <int S>
   __device__ void store(T* sm) const {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + 256 * s, ov = v % VPM, kp = v / VPM;
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) sm[(ov * VEC + e) * LDK + kp] = tbits<T>(vbits<T>(r[s], e));
+      for (int e = 0; e < VEC; ++e) sm[(ov * VEC + e) * LDK + kp] = tbits<T>(vbits<T>(r[S][s], e));
     }
   }
 };
@@ -482,16 +495,17 @@ struct DzRowsLoader {
 // reading 1), k = output pixel. Written to LDS transposed.
 template <typename T, int ROWS, int BK>
 struct PatchRowsLoader {
-  static constexpr int VEC = TT<T>::VEC, VPN = ROWS / VEC, NV = ROWS * BK / VEC / 256, LDK = BK + VEC;
+  static constexpr int VEC = TT<T>::VEC, VPN = ROWS / VEC, NV = ROWS * BK / VEC / 256, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
   const ConvProb* p;
   const T* X;
   int n0;
-  u32x4 r[NV];
+  u32x4 r[2][NV];
   __device__ void init(const ConvProb& pr, int n0_) {
     p = &pr;
     X = (const T*)pr.X;
     n0 = n0_;
   }
+  template <int S>
   __device__ void load(int kb) {
     const int C = p->C, H = p->H, W = p->W, KW = p->KH, pad = p->pad, J = p->KH * p->KH * C;
     const bool vec = (C % VEC) == 0;
@@ -521,15 +535,16 @@ struct PatchRowsLoader {
           }
         }
       }
-      r[s] = val;
+      r[S][s] = val;
     }
   }
+  template <int S>
   __device__ void store(T* sm) const {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + 256 * s, jv = v % VPN, kp = v / VPN;
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) sm[(jv * VEC + e) * LDK + kp] = tbits<T>(vbits<T>(r[s], e));
+      for (int e = 0; e < VEC; ++e) sm[(jv * VEC + e) * LDK + kp] = tbits<T>(vbits<T>(r[S][s], e));
     }
   }
 };
@@ -576,7 +591,7 @@ template <> __device__ __forceinline__ void store_chunk<bf16_t>(bf16_t* dst, con
 }
 
 // Row-major store of the staged fp32 tile sC [BM][CLD] into C [m][ldc] as OT,
-// one 16-byte chunk per thread and step (coalesced along n).
+// one 16-byte chunk per thread and step (contiguous along n).
 template <typename OT, int BM, int BN, int CLD>
 __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, int m0, int n0, int M, int N) {
   constexpr int VE = 16 / sizeof(OT), CPR = BN / VE;
@@ -586,25 +601,36 @@ __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, 
     if (m >= M || n >= N) continue;
     float v[VE];
 #pragma unroll
-    for (int e = 0; e < VE; e += 4) {
-      const f32x4 q = *(const f32x4*)(sC + r * CLD + cc * VE + e);
-      v[e] = q[0];
-      v[e + 1] = q[1];
-      v[e + 2] = q[2];
-      v[e + 3] = q[3];
-    }
+    for (int e = 0; e < VE; ++e) v[e] = sC[r * CLD + cc * VE + e];
     store_chunk<OT>(C + (int64_t)m * ldc + n, v, min(VE, N - n));
   }
 }
 
+// Transposed store of the staged tile: CT[n][m] for n < N, 16-byte chunks
+// along m. Lanes take consecutive m-chunks of the same n, so a wave writes
+// whole contiguous runs of each CT row.
+template <typename OT, int BM, int BN, int CLD>
+__device__ __forceinline__ void store_cols(const float* sC, OT* CT, int64_t ldct, int m0, int n0, int M, int N) {
+  constexpr int VE = 16 / sizeof(OT), CPC = BM / VE;
+  for (int idx = threadIdx.x; idx < BN * CPC; idx += 256) {
+    const int c = idx / CPC, mq = idx - c * CPC;
+    const int n = n0 + c, m = m0 + mq * VE;
+    if (n >= N || m >= M) continue;
+    float v[VE];
+#pragma unroll
+    for (int e = 0; e < VE; ++e) v[e] = sC[(mq * VE + e) * CLD + c];
+    store_chunk<OT>(CT + (int64_t)n * ldct + m, v, min(VE, M - m));
+  }
+}
+
 template <typename T, int BM, int BN, int BK>
-__global__ __launch_bounds__(256) void gemm_kernel(const GemmProb* __restrict__ probs,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(const GemmProb* __restrict__ probs,
                                                    const int32_t* __restrict__ tile_prob, float lr,
-                                                   int keep_grads) {
+                                                   int keep_grads, int remap) {
   using TL = Tile<T, BM, BN, BK>;
   using SM = Smem<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[SM::BYTES];
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int tile = remap ? xcd_tile(blockIdx.x, gridDim.x) : (int)blockIdx.x;
   const GemmProb& p = probs[tile_prob[tile]];
   const int local = tile - p.tile_base;
   const int tiles_m = (p.M + BM - 1) / BM;
@@ -623,8 +649,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmProb* __restrict__ 
   lb.init((const T*)p.B + (int64_t)n0 * p.ldb, p.ldb, p.N - n0, p.K);
   mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
 
-  // Epilogue 1: per-element work in registers, transposed stores straight from
-  // the accumulator layout (4 consecutive m of one n per lane), fp32 tile to LDS.
+  // Epilogue 1: per-element work (bias, ReLU, ReLU' mask) in registers, then
+  // the fp32 tile to LDS with an odd row stride (column gathers hit distinct
+  // banks).
+  constexpr int CLD = BN + 1;
   float* sC = (float*)smem;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
@@ -651,48 +679,59 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmProb* __restrict__ 
           for (int r = 0; r < 4; ++r)
             if (r < nv && !(TT<T>::to_f(mk[r]) > 0.f)) v[r] = 0.f;
         }
-        if ((epi == EPI_FWD || epi == EPI_DGRAD) && p.CT) store4_t<T>((T*)p.CT + (int64_t)n * p.ldct + mb, v, nv);
       }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) sC[(rl + r) * SM::CLD + cl] = v[r];
+      for (int r = 0; r < 4; ++r) sC[(rl + r) * CLD + cl] = v[r];
     }
   }
   __syncthreads();
 
-  // Epilogue 2: coalesced row-major passes over the staged tile.
-  if (epi == EPI_FWD || epi == EPI_DGRAD) {
-    if (p.C) store_rows<T, BM, BN, SM::CLD>(sC, (T*)p.C, p.ldc, m0, n0, p.M, p.N);
+  if (epi != EPI_WGRAD) {
+    // Row pass: C[m][n] in 16-byte chunks along n.
+    if (p.C) {
+      if (epi == EPI_LOGITS) store_rows<float, BM, BN, CLD>(sC, (float*)p.C, p.ldc, m0, n0, p.M, p.N);
+      else store_rows<T, BM, BN, CLD>(sC, (T*)p.C, p.ldc, m0, n0, p.M, p.N);
+    }
+    // Column pass: CT[n][m] in 16-byte chunks along m.
+    if (p.CT) store_cols<T, BM, BN, CLD>(sC, (T*)p.CT, p.ldct, m0, n0, p.M, p.N);
     return;
   }
-  if (epi == EPI_LOGITS) {
-    store_rows<float, BM, BN, SM::CLD>(sC, (float*)p.C, p.ldc, m0, n0, p.M, p.N);
-    return;
-  }
-  // EPI_WGRAD: fused SGD. Row pass: W[m][n..n+3] read-modify-write as float4,
-  // bf16 shadow, kept gradient; the bias column (n == nsplit) element-wise.
-  // The updated weights go back to LDS for the transposed copy.
-  constexpr int CPR = BN / 4;
+
+  // EPI_WGRAD, SGD fused. Row pass over float4 chunks of W[m][n..n+3]: all
+  // master-weight loads of this thread are issued first, then the update, the
+  // bf16 shadow, the kept gradient; the updated weights go back to LDS. The
+  // bias column (n == nsplit) is done element-wise.
+  constexpr int CPR = BN / 4, NCH = BM * CPR / 256;
   const int ns = p.nsplit;
-  for (int idx = threadIdx.x; idx < BM * CPR; idx += 256) {
-    const int r = idx / CPR, cc = idx - r * CPR;
+  f32x4 w0[NCH];
+#pragma unroll
+  for (int q = 0; q < NCH; ++q) {
+    const int idx = threadIdx.x + 256 * q, r = idx / CPR, n = n0 + (idx - r * CPR) * 4, m = m0 + r;
+    w0[q] = (m < p.M && n + 4 <= ns) ? *(gptr<const f32x4>)(p.W + (int64_t)m * p.ldc + n) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+#pragma unroll
+  for (int q = 0; q < NCH; ++q) {
+    const int idx = threadIdx.x + 256 * q, r = idx / CPR, cc = idx - r * CPR;
     const int m = m0 + r, n = n0 + cc * 4;
     if (m >= p.M || n > ns) continue;
-    float* s = sC + r * SM::CLD + cc * 4;
+    float* s = sC + r * CLD + cc * 4;
     const int64_t base = (int64_t)m * p.ldc + n;
     if (n + 4 <= ns) {
-      const f32x4 g = *(const f32x4*)s;
-      if (keep_grads) *(f32x4*)((float*)p.C + base) = g;
-      const f32x4 w0 = *(const f32x4*)(p.W + base);
-      const f32x4 w = f32x4{fmaf(-lr, g[0], w0[0]), fmaf(-lr, g[1], w0[1]), fmaf(-lr, g[2], w0[2]),
-                            fmaf(-lr, g[3], w0[3])};
-      *(f32x4*)(p.W + base) = w;
+      const f32x4 g = f32x4{s[0], s[1], s[2], s[3]};
+      if (keep_grads) *(gptr<f32x4>)((float*)p.C + base) = g;
+      const f32x4 w = f32x4{fmaf(-lr, g[0], w0[q][0]), fmaf(-lr, g[1], w0[q][1]), fmaf(-lr, g[2], w0[q][2]),
+                            fmaf(-lr, g[3], w0[q][3])};
+      *(gptr<f32x4>)(p.W + base) = w;
       if (p.Wb) {
         u32x2 hb;
         hb[0] = (uint32_t)f2bf(w[0]) | ((uint32_t)f2bf(w[1]) << 16);
         hb[1] = (uint32_t)f2bf(w[2]) | ((uint32_t)f2bf(w[3]) << 16);
-        *(u32x2*)((bf16_t*)p.Wb + base) = hb;
+        *(gptr<u32x2>)((bf16_t*)p.Wb + base) = hb;
       }
-      *(f32x4*)s = w;
+      s[0] = w[0];
+      s[1] = w[1];
+      s[2] = w[2];
+      s[3] = w[3];
     } else {
       for (int e = 0; e < 4 && n + e <= ns && n + e < p.N; ++e) {
         const float g = s[e];
@@ -711,32 +750,19 @@ __global__ __launch_bounds__(256) void gemm_kernel(const GemmProb* __restrict__ 
   }
   if (!p.WT) return;
   __syncthreads();
-  // Transposed copy WT[n][m]: each lane stores the 4 consecutive m it held.
-#pragma unroll
-  for (int i = 0; i < TL::FM; ++i) {
-    const int rl = wm + 16 * i + 4 * (lane >> 4), mb = m0 + rl;
-    const int nv = max(0, min(4, p.M - mb));
-#pragma unroll
-    for (int j = 0; j < TL::FN; ++j) {
-      const int cl = wn + 16 * j + (lane & 15), n = n0 + cl;
-      if (n >= ns || nv == 0) continue;
-      float w4[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) w4[r] = sC[(rl + r) * SM::CLD + cl];
-      store4_t<T>((T*)p.WT + (int64_t)n * p.ldwt + mb, w4, nv);
-    }
-  }
+  // Column pass: the updated weights transposed, WT[n][m] for n < nsplit.
+  store_cols<T, BM, BN, CLD>(sC, (T*)p.WT, p.ldwt, m0, n0, p.M, min(p.N, ns));
 }
 
 // ---------------------------------------------------------------------------
 // Convolution passes
 // ---------------------------------------------------------------------------
 template <typename T, int BM, int BN, int BK>
-__global__ __launch_bounds__(256) void conv_fwd_kernel(const ConvProb* __restrict__ probs,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_fwd_kernel(const ConvProb* __restrict__ probs,
                                                        const int32_t* __restrict__ tile_prob) {
   using TL = Tile<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int tile = blockIdx.x;
   const ConvProb& p = probs[tile_prob[tile]];
   const int local = tile - p.tile_base;
   const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
@@ -805,11 +831,11 @@ __global__ __launch_bounds__(256) void conv_fwd_kernel(const ConvProb* __restric
 }
 
 template <typename T, int BM, int BN, int BK>
-__global__ __launch_bounds__(256) void conv_dgrad_kernel(const ConvProb* __restrict__ probs,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_dgrad_kernel(const ConvProb* __restrict__ probs,
                                                          const int32_t* __restrict__ tile_prob) {
   using TL = Tile<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int tile = blockIdx.x;
   const ConvProb& p = probs[tile_prob[tile]];
   const int local = tile - p.tile_base;
   const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
@@ -851,11 +877,11 @@ __global__ __launch_bounds__(256) void conv_dgrad_kernel(const ConvProb* __restr
 }
 
 template <typename T, int BM, int BN, int BK>
-__global__ __launch_bounds__(256) void conv_wgrad_kernel(const ConvProb* __restrict__ probs,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_wgrad_kernel(const ConvProb* __restrict__ probs,
                                                          const int32_t* __restrict__ tile_prob) {
   using TL = Tile<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int tile = blockIdx.x;
   const ConvProb& p = probs[tile_prob[tile]];
   int local = tile - p.tile_base;
   const int per_split = p.tiles_m * p.tiles_n;
@@ -937,51 +963,66 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// One block per (model, chunk of CE_ROWS rows); one wave per row at a time,
-// lanes over classes. dz goes to G row-major directly and, through LDS, to GT
-// as runs of consecutive samples. Each block sums its rows' losses in row
+// One thread per sample row (CE_ROWS rows per block, blockIdx.y = model):
+// the row's logits are read as 16-byte vectors, dz = (softmax - onehot)/B goes
+// to G in 16-byte chunks of the row and to GT as stores that are contiguous
+// across the threads of a block. Each block sums its rows' losses in row
 // order into partial[model][chunk]; ce_finish_kernel adds the chunks in order.
 template <typename T>
-__global__ __launch_bounds__(256) void ce_rows_kernel(const CeProb* __restrict__ probs, const int32_t* __restrict__ y,
-                                                      int B, float* __restrict__ partial, int nchunks) {
-  __shared__ float sdz[CE_ROWS][CE_LDS_CLASSES + 1];
+__global__ __launch_bounds__(CE_ROWS) void ce_rows_kernel(const CeProb* __restrict__ probs,
+                                                          const int32_t* __restrict__ y, int B,
+                                                          float* __restrict__ partial, int nchunks) {
   __shared__ float rowloss[CE_ROWS];
   const CeProb& p = probs[blockIdx.y];
-  const int b0 = blockIdx.x * CE_ROWS;
-  const int nrows = min(CE_ROWS, B - b0);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const float invB = 1.0f / (float)B;
-  const bool staged = p.C <= CE_LDS_CLASSES;
-  for (int r = wave; r < nrows; r += 4) {
-    const int b = b0 + r;
+  const int b = blockIdx.x * CE_ROWS + threadIdx.x;
+  const int C = p.C;
+  float loss = 0.f;
+  if (b < B) {
     const float* z = p.logits + (int64_t)b * p.ldl;
+    const int C4 = C & ~3;
     float mx = -INFINITY;
-    for (int c = lane; c < p.C; c += 64) mx = fmaxf(mx, z[c]);
-    mx = wave_max(mx);
+    for (int c = 0; c < C4; c += 4) {
+      const f32x4 v = *(const f32x4*)(z + c);
+      mx = fmaxf(mx, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
+    }
+    for (int c = C4; c < C; ++c) mx = fmaxf(mx, z[c]);
     float s = 0.f;
-    for (int c = lane; c < p.C; c += 64) s += expf(z[c] - mx);
-    s = wave_sum(s);
+    for (int c = 0; c < C4; c += 4) {
+      const f32x4 v = *(const f32x4*)(z + c);
+      s += expf(v[0] - mx);
+      s += expf(v[1] - mx);
+      s += expf(v[2] - mx);
+      s += expf(v[3] - mx);
+    }
+    for (int c = C4; c < C; ++c) s += expf(z[c] - mx);
     const int yb = y[b];
-    if (lane == 0) rowloss[r] = mx + logf(s) - z[yb];
-    const float inv_s = 1.0f / s;
-    for (int c = lane; c < p.C; c += 64) {
-      const float g = (expf(z[c] - mx) * inv_s - (c == yb ? 1.f : 0.f)) * invB;
-      if (p.G) ((T*)p.G)[(int64_t)b * p.ldg + c] = TT<T>::from_f(g);
-      if (staged) sdz[r][c] = g;
-      else if (p.GT) ((T*)p.GT)[(int64_t)c * p.ldgt + b] = TT<T>::from_f(g);
+    loss = mx + logf(s) - z[yb];
+    const float inv_s = 1.0f / s, invB = 1.0f / (float)B;
+    constexpr int VE = TT<T>::VEC;
+    T* G = (T*)p.G + (int64_t)b * p.ldg;
+    T* GT = (T*)p.GT;
+    for (int c0 = 0; c0 < C; c0 += VE) {
+      float g[VE];
+#pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        const int c = c0 + e;
+        g[e] = c < C ? (expf(z[c] - mx) * inv_s - (c == yb ? 1.f : 0.f)) * invB : 0.f;
+      }
+      if (p.G) store_chunk<T>(G + c0, g, min(VE, C - c0));
+      if (GT) {
+#pragma unroll
+        for (int e = 0; e < VE; ++e)
+          if (c0 + e < C) GT[(int64_t)(c0 + e) * p.ldgt + b] = TT<T>::from_f(g[e]);
+      }
     }
   }
+  rowloss[threadIdx.x] = loss;
   __syncthreads();
-  if (staged && p.GT) {
-    for (int idx = threadIdx.x; idx < p.C * CE_ROWS; idx += 256) {
-      const int c = idx / CE_ROWS, r = idx - c * CE_ROWS;
-      if (r < nrows) ((T*)p.GT)[(int64_t)c * p.ldgt + b0 + r] = TT<T>::from_f(sdz[r][c]);
-    }
-  }
   if (threadIdx.x == 0) {
-    float s = 0.f;
-    for (int r = 0; r < nrows; ++r) s += rowloss[r];
-    partial[(int64_t)p.model * nchunks + blockIdx.x] = s;
+    const int nrows = min(CE_ROWS, B - (int)blockIdx.x * CE_ROWS);
+    float t = 0.f;
+    for (int r = 0; r < nrows; ++r) t += rowloss[r];
+    partial[(int64_t)p.model * nchunks + blockIdx.x] = t;
   }
 }
 
@@ -1062,14 +1103,14 @@ __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, 
 // Launch wrappers
 // ---------------------------------------------------------------------------
 hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_prob, int ntiles, float lr,
-                       bool keep_grads, hipStream_t s) {
+                       bool keep_grads, bool xcd_remap, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   if (bf16)
     hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, 64>), dim3(ntiles), dim3(256), 0, s, probs,
-                       tile_prob, lr, (int)keep_grads);
+                       tile_prob, lr, (int)keep_grads, (int)xcd_remap);
   else
     hipLaunchKernelGGL((gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, 32>), dim3(ntiles), dim3(256), 0, s, probs,
-                       tile_prob, lr, (int)keep_grads);
+                       tile_prob, lr, (int)keep_grads, (int)xcd_remap);
   return hipGetLastError();
 }
 
@@ -1123,10 +1164,10 @@ hipError_t launch_ce(bool bf16, const CeProb* probs, int nmodels, const int32_t*
   if (nmodels <= 0) return hipSuccess;
   const int nchunks = (B + CE_ROWS - 1) / CE_ROWS;
   if (bf16)
-    hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nmodels), dim3(256), 0, s, probs, labels, B, partial,
+    hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nmodels), dim3(CE_ROWS), 0, s, probs, labels, B, partial,
                        nchunks);
   else
-    hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nmodels), dim3(256), 0, s, probs, labels, B, partial,
+    hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nmodels), dim3(CE_ROWS), 0, s, probs, labels, B, partial,
                        nchunks);
   hipLaunchKernelGGL(ce_finish_kernel, dim3((nmodels + 63) / 64), dim3(64), 0, s, partial, nchunks, nmodels, B,
                      losses);

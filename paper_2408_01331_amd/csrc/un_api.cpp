@@ -75,6 +75,7 @@ struct Launch {
   int kclass;
   size_t probs, map;  // arena offsets
   int count;
+  int remap = 0;      // XCD-contiguous tile ranges (uniform-cost tile lists only)
 };
 
 struct EventRec {
@@ -475,8 +476,14 @@ static un_status plan_and_alloc(un_ctx* c) {
   const int GBM = bf ? GEMM_BM_BF16 : GEMM_BM_F32, GBN = bf ? GEMM_BN_BF16 : GEMM_BN_F32;
   const int CBM = bf ? CONV_BM_BF16 : CONV_BM_F32, CBN = bf ? CONV_BN_BF16 : CONV_BN_F32;
 
+  // Problems of one launch are ordered longest-K first (their tiles are the
+  // longest-running), so the ragged tail of a level is made of short tiles.
+  // Order affects scheduling only: every tile computes the same values.
   auto emit_gemm = [&](std::vector<GemmProb>& ps, std::vector<Launch>& out, int kclass) {
     if (ps.empty()) return;
+    std::stable_sort(ps.begin(), ps.end(), [](const GemmProb& x, const GemmProb& y) { return x.K > y.K; });
+    bool uniform = true;
+    for (auto& p : ps) uniform = uniform && p.K == ps[0].K;
     std::vector<int32_t> map;
     for (auto& p : ps) {
       const int tm = cdiv(p.M, GBM), tn = cdiv(p.N, GBN);
@@ -494,10 +501,12 @@ static un_status plan_and_alloc(un_ctx* c) {
         fix.push_back(b0 + f);
     }
     size_t mo = put(map.data(), map.size() * 4);
-    out.push_back(Launch{0, kclass, po, mo, (int)map.size()});
+    out.push_back(Launch{0, kclass, po, mo, (int)map.size(), uniform ? 1 : 0});
   };
   auto emit_conv = [&](std::vector<ConvProb>& ps, std::vector<Launch>& out, int kind, int kclass) {
     if (ps.empty()) return;
+    std::stable_sort(ps.begin(), ps.end(),
+                     [](const ConvProb& x, const ConvProb& y) { return (int64_t)x.K * x.splits > (int64_t)y.K * y.splits; });
     std::vector<int32_t> map;
     for (auto& p : ps) {
       p.tiles_m = cdiv(p.M, CBM);
@@ -1000,7 +1009,7 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
   switch (l.kind) {
     case 0:
       e = launch_gemm(c->bf16, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->keep_grads,
-                      c->stream);
+                      l.remap != 0, c->stream);
       break;
     case 1:
       e = launch_conv_fwd(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
