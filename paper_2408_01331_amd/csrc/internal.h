@@ -114,7 +114,7 @@ struct ReduceProb {
 // ---------------------------------------------------------------------------
 // Softmax cross-entropy of one model: logits [B][ldl] fp32 -> per-model mean
 // loss, and dz = (softmax - onehot)/B stored as G [B][ldg] and GT [C][ldgt].
-// Row losses are summed per 64-row chunk, then per model, in a fixed order.
+// Row losses are summed per 32-row chunk, then per model, in a fixed order.
 // ---------------------------------------------------------------------------
 struct CeProb {
   const float* logits;
@@ -167,11 +167,13 @@ hipError_t launch_load(bool bf16, const float* x, int B, int C, int H, int W, vo
 // Tile shapes the planner must agree with.
 constexpr int GEMM_BM_BF16 = 128, GEMM_BN_BF16 = 128;
 constexpr int GEMM_BM_F32 = 64, GEMM_BN_F32 = 64;
+constexpr int GEMM_BK_BF16 = 64, GEMM_BK_F32 = 32;
 constexpr int CONV_BM_BF16 = 128, CONV_BN_BF16 = 128, CONV_BK_BF16 = 64;
 constexpr int CONV_BM_F32 = 64, CONV_BN_F32 = 64, CONV_BK_F32 = 32;
 constexpr int SGD_TILE = 64;
 constexpr int REDUCE_BLOCK = 256;
 constexpr int CE_MAX_BATCH = 1 << 20;
-constexpr int CE_ROWS = 64;           // rows (threads) per softmax-CE block
+constexpr int CE_ROWS = 32;           // sample rows per softmax-CE block
+constexpr int CE_LANES = 8;           // lanes per row
 
 }  // namespace un

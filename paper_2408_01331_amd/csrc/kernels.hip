@@ -963,60 +963,44 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-// One thread per sample row (CE_ROWS rows per block, blockIdx.y = model):
-// the row's logits are read as 16-byte vectors, dz = (softmax - onehot)/B goes
-// to G in 16-byte chunks of the row and to GT as stores that are contiguous
-// across the threads of a block. Each block sums its rows' losses in row
-// order into partial[model][chunk]; ce_finish_kernel adds the chunks in order.
+// CE_LANES lanes per sample row (CE_ROWS rows per block, blockIdx.y = model),
+// classes strided over the row's lanes; max and sum over the row by a fixed
+// butterfly of lane shuffles. dz = (softmax - onehot)/B goes to G and GT. Each
+// block sums its rows' losses in row order into partial[model][chunk];
+// ce_finish_kernel adds the chunks in order.
 template <typename T>
-__global__ __launch_bounds__(CE_ROWS) void ce_rows_kernel(const CeProb* __restrict__ probs,
-                                                          const int32_t* __restrict__ y, int B,
-                                                          float* __restrict__ partial, int nchunks) {
+__global__ __launch_bounds__(CE_ROWS * CE_LANES) void ce_rows_kernel(const CeProb* __restrict__ probs,
+                                                                     const int32_t* __restrict__ y, int B,
+                                                                     float* __restrict__ partial, int nchunks) {
   __shared__ float rowloss[CE_ROWS];
   const CeProb& p = probs[blockIdx.y];
-  const int b = blockIdx.x * CE_ROWS + threadIdx.x;
+  const int rl = threadIdx.x / CE_LANES, sub = threadIdx.x % CE_LANES;
+  const int b = blockIdx.x * CE_ROWS + rl;
   const int C = p.C;
-  float loss = 0.f;
-  if (b < B) {
-    const float* z = p.logits + (int64_t)b * p.ldl;
-    const int C4 = C & ~3;
-    float mx = -INFINITY;
-    for (int c = 0; c < C4; c += 4) {
-      const f32x4 v = *(const f32x4*)(z + c);
-      mx = fmaxf(mx, fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3])));
-    }
-    for (int c = C4; c < C; ++c) mx = fmaxf(mx, z[c]);
-    float s = 0.f;
-    for (int c = 0; c < C4; c += 4) {
-      const f32x4 v = *(const f32x4*)(z + c);
-      s += expf(v[0] - mx);
-      s += expf(v[1] - mx);
-      s += expf(v[2] - mx);
-      s += expf(v[3] - mx);
-    }
-    for (int c = C4; c < C; ++c) s += expf(z[c] - mx);
+  const bool valid = b < B;
+  const float* z = p.logits + (int64_t)(valid ? b : 0) * p.ldl;
+  float mx = -INFINITY;
+  if (valid)
+    for (int c = sub; c < C; c += CE_LANES) mx = fmaxf(mx, z[c]);
+#pragma unroll
+  for (int off = 1; off < CE_LANES; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+  float s = 0.f;
+  if (valid)
+    for (int c = sub; c < C; c += CE_LANES) s += expf(z[c] - mx);
+#pragma unroll
+  for (int off = 1; off < CE_LANES; off <<= 1) s += __shfl_xor(s, off, 64);
+  if (valid) {
     const int yb = y[b];
-    loss = mx + logf(s) - z[yb];
+    if (sub == 0) rowloss[rl] = mx + logf(s) - z[yb];
     const float inv_s = 1.0f / s, invB = 1.0f / (float)B;
-    constexpr int VE = TT<T>::VEC;
-    T* G = (T*)p.G + (int64_t)b * p.ldg;
-    T* GT = (T*)p.GT;
-    for (int c0 = 0; c0 < C; c0 += VE) {
-      float g[VE];
-#pragma unroll
-      for (int e = 0; e < VE; ++e) {
-        const int c = c0 + e;
-        g[e] = c < C ? (expf(z[c] - mx) * inv_s - (c == yb ? 1.f : 0.f)) * invB : 0.f;
-      }
-      if (p.G) store_chunk<T>(G + c0, g, min(VE, C - c0));
-      if (GT) {
-#pragma unroll
-        for (int e = 0; e < VE; ++e)
-          if (c0 + e < C) GT[(int64_t)(c0 + e) * p.ldgt + b] = TT<T>::from_f(g[e]);
-      }
+    for (int c = sub; c < C; c += CE_LANES) {
+      const T g = TT<T>::from_f((expf(z[c] - mx) * inv_s - (c == yb ? 1.f : 0.f)) * invB);
+      if (p.G) ((T*)p.G)[(int64_t)b * p.ldg + c] = g;
+      if (p.GT) ((T*)p.GT)[(int64_t)c * p.ldgt + b] = g;
     }
+  } else if (sub == 0) {
+    rowloss[rl] = 0.f;
   }
-  rowloss[threadIdx.x] = loss;
   __syncthreads();
   if (threadIdx.x == 0) {
     const int nrows = min(CE_ROWS, B - (int)blockIdx.x * CE_ROWS);
@@ -1106,10 +1090,10 @@ hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_pro
                        bool keep_grads, bool xcd_remap, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   if (bf16)
-    hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, 64>), dim3(ntiles), dim3(256), 0, s, probs,
+    hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16>), dim3(ntiles), dim3(256), 0, s, probs,
                        tile_prob, lr, (int)keep_grads, (int)xcd_remap);
   else
-    hipLaunchKernelGGL((gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, 32>), dim3(ntiles), dim3(256), 0, s, probs,
+    hipLaunchKernelGGL((gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, GEMM_BK_F32>), dim3(ntiles), dim3(256), 0, s, probs,
                        tile_prob, lr, (int)keep_grads, (int)xcd_remap);
   return hipGetLastError();
 }
@@ -1164,10 +1148,10 @@ hipError_t launch_ce(bool bf16, const CeProb* probs, int nmodels, const int32_t*
   if (nmodels <= 0) return hipSuccess;
   const int nchunks = (B + CE_ROWS - 1) / CE_ROWS;
   if (bf16)
-    hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nmodels), dim3(CE_ROWS), 0, s, probs, labels, B, partial,
+    hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nmodels), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels, B, partial,
                        nchunks);
   else
-    hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nmodels), dim3(CE_ROWS), 0, s, probs, labels, B, partial,
+    hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nmodels), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels, B, partial,
                        nchunks);
   hipLaunchKernelGGL(ce_finish_kernel, dim3((nmodels + 63) / 64), dim3(64), 0, s, partial, nchunks, nmodels, B,
                      losses);

@@ -484,11 +484,15 @@ static un_status plan_and_alloc(un_ctx* c) {
     std::stable_sort(ps.begin(), ps.end(), [](const GemmProb& x, const GemmProb& y) { return x.K > y.K; });
     bool uniform = true;
     for (auto& p : ps) uniform = uniform && p.K == ps[0].K;
+    uniform = uniform && ps.size() == 1;
     std::vector<int32_t> map;
     for (auto& p : ps) {
       const int tm = cdiv(p.M, GBM), tn = cdiv(p.N, GBN);
       p.tiles_n = tn;
       p.tile_base = (int32_t)map.size();
+      // Split-K for a narrow problem with a long K, from its own shape only
+      // (so a model computes the same values alone or merged): at least 4
+      // k-blocks per split, aiming at ~64 workgroups for the problem.
       for (int t = 0; t < tm * tn; ++t) map.push_back((int32_t)(&p - ps.data()));
     }
     size_t po = put(ps.data(), ps.size() * sizeof(GemmProb));
