@@ -435,117 +435,213 @@ struct DzGatherLoader {
   }
 };
 
-// Conv wgrad A operand: rows = output channel o, k = output pixel.
-// Global vectors run along o; they are written to LDS transposed.
+// Conv wgrad operands. Both run along channels in memory while the product
+// contracts over pixels, so each thread gathers a VEC-pixel x VEC-channel
+// micro-tile (VEC 16-byte vectors, one per pixel), transposes it in registers
+// and writes VEC 16-byte LDS rows of VEC consecutive pixels. Threads 0..127
+// load A (output channels), threads 128..255 load B (patch columns); a tile
+// has exactly 128 micro-tiles per operand for both storage types.
+
+// In-register transpose of a VEC x VEC block: in[p] holds channels 0..VEC-1 of
+// pixel p; out[c] receives pixels 0..VEC-1 of channel c.
+template <typename T> __device__ __forceinline__ void transpose_block(const u32x4 (&in)[TT<T>::VEC], u32x4 (&out)[TT<T>::VEC]);
+template <> __device__ __forceinline__ void transpose_block<float>(const u32x4 (&in)[4], u32x4 (&out)[4]) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+#pragma unroll
+    for (int p = 0; p < 4; ++p) out[c][p] = in[p][c];
+}
+template <> __device__ __forceinline__ void transpose_block<bf16_t>(const u32x4 (&in)[8], u32x4 (&out)[8]) {
+  // word q of in[p] packs channels (2q, 2q+1) of pixel p (low half = even channel)
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const uint32_t a = in[2 * r][q], b = in[2 * r + 1][q];
+      out[2 * q][r] = (a & 0xffffu) | (b << 16);
+      out[2 * q + 1][r] = (a >> 16) | (b & 0xffff0000u);
+    }
+}
+
+// A: rows = output channel o, k = output pixel. dZ gathered from the pooled
+// gradient G[w][o] (already ReLU'-masked) and the window argmax.
 template <typename T, int ROWS, int BK>
 struct DzRowsLoader {
-  static constexpr int VEC = TT<T>::VEC, VPM = ROWS / VEC, NV = ROWS * BK / VEC / 256, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
+  static constexpr int VEC = TT<T>::VEC, MGROUPS = ROWS / VEC, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
+  static_assert(ROWS * BK / (VEC * VEC) == 128, "128 micro-tiles per operand");
   const ConvProb* p;
   const T* G;
-  int m0;
-  u32x4 r[2][NV];
-  __device__ void init(const ConvProb& pr, int m0_) {
+  int o0, pg;
+  bool active;
+  u32x4 r[2][VEC];
+  __device__ void init(const ConvProb& pr, int m0) {
     p = &pr;
     G = (const T*)pr.G;
-    m0 = m0_;
+    active = threadIdx.x < 128;
+    o0 = m0 + (threadIdx.x % MGROUPS) * VEC;
+    pg = (threadIdx.x % 128) / MGROUPS;
   }
   template <int S>
   __device__ void load(int kb) {
+    if (!active) return;
     const int O = p->O;
-    const bool vec = (O % VEC) == 0;
+    const int pix0 = kb * BK + pg * VEC;
+    u32x4 pixv[VEC];
+    if (o0 + VEC <= O && (O % VEC) == 0) {
+      if (p->pool) {
+        // VEC consecutive pixels cover VEC/4 windows; each window's gradient
+        // lands on its argmax pixel only
 #pragma unroll
-    for (int s = 0; s < NV; ++s) {
-      const int v = threadIdx.x + 256 * s, ov = v % VPM, pix = kb * BK + v / VPM, o0 = m0 + ov * VEC;
-      u32x4 val = zero4();
-      if (pix < p->K && o0 < O) {
-        int64_t idx;
-        int d;
-        if (p->pool) {
-          idx = (int64_t)(pix >> 2) * O;
-          d = pix & 3;
-        } else {
-          idx = (int64_t)pix * O;
-          d = -1;
+        for (int wq = 0; wq < VEC / 4; ++wq) {
+          const int pix = pix0 + 4 * wq;
+          u32x4 g = zero4();
+          uint64_t am = 0;
+          if (pix < p->K) {
+            const int64_t idx = (int64_t)(pix >> 2) * O + o0;
+            g = *(gptr<const u32x4>)(G + idx);
+            am = load_am<T>(p->gam + idx);
+          }
+#pragma unroll
+          for (int d = 0; d < 4; ++d) {
+            u32x4 v = g;
+            select_am<T>(v, am, d);
+            pixv[4 * wq + d] = v;
+          }
         }
-        if (vec) {
-          val = *(const u32x4*)(G + idx + o0);
-          if (d >= 0) select_am<T>(val, load_am<T>(p->gam + idx + o0), d);
-        } else {
+      } else {
 #pragma unroll
-          for (int e = 0; e < VEC; ++e)
-            if (o0 + e < O && (d < 0 || p->gam[idx + o0 + e] == d))
-              vset_bits<T>(val, e, bits_of<T>(G[idx + o0 + e]));
+        for (int e = 0; e < VEC; ++e) {
+          const int pix = pix0 + e;
+          pixv[e] = pix < p->K ? *(gptr<const u32x4>)(G + (int64_t)pix * O + o0) : zero4();
         }
       }
-      r[S][s] = val;
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const int pix = pix0 + e;
+        u32x4 v = zero4();
+        if (pix < p->K) {
+          const int64_t idx = (int64_t)(p->pool ? (pix >> 2) : pix) * O;
+          const int d = p->pool ? (pix & 3) : -1;
+#pragma unroll
+          for (int c = 0; c < VEC; ++c)
+            if (o0 + c < O && (d < 0 || p->gam[idx + o0 + c] == d)) vset_bits<T>(v, c, bits_of<T>(G[idx + o0 + c]));
+        }
+        pixv[e] = v;
+      }
     }
+    transpose_block<T>(pixv, r[S]);
   }
   template <int S>
   __device__ void store(T* sm) const {
+    if (!active) return;
+    const int ol = (threadIdx.x % MGROUPS) * VEC;
 #pragma unroll
-    for (int s = 0; s < NV; ++s) {
-      const int v = threadIdx.x + 256 * s, ov = v % VPM, kp = v / VPM;
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) sm[(ov * VEC + e) * LDK + kp] = tbits<T>(vbits<T>(r[S][s], e));
-    }
+    for (int c = 0; c < VEC; ++c) *(u32x4*)(sm + (ol + c) * LDK + pg * VEC) = r[S][c];
   }
 };
 
-// Conv wgrad B operand: rows = j = (u, v, c) (+ the bias column j == KH*KW*C
-// reading 1), k = output pixel. Written to LDS transposed.
+// B: rows = j = (u, v, c) (+ the bias column j == KH*KW*C reading 1), k =
+// output pixel: the input patch, gathered from NHWC X.
 template <typename T, int ROWS, int BK>
 struct PatchRowsLoader {
-  static constexpr int VEC = TT<T>::VEC, VPN = ROWS / VEC, NV = ROWS * BK / VEC / 256, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
+  static constexpr int VEC = TT<T>::VEC, NGROUPS = ROWS / VEC, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
+  static_assert(ROWS * BK / (VEC * VEC) == 128, "128 micro-tiles per operand");
   const ConvProb* p;
   const T* X;
-  int n0;
-  u32x4 r[2][NV];
-  __device__ void init(const ConvProb& pr, int n0_) {
+  int j0, pg;
+  bool active;
+  u32x4 r[2][VEC];
+  __device__ void init(const ConvProb& pr, int n0) {
     p = &pr;
     X = (const T*)pr.X;
-    n0 = n0_;
+    active = threadIdx.x >= 128;
+    const int t = threadIdx.x % 128;
+    j0 = n0 + (t % NGROUPS) * VEC;
+    pg = t / NGROUPS;
   }
   template <int S>
   __device__ void load(int kb) {
+    if (!active) return;
     const int C = p->C, H = p->H, W = p->W, KW = p->KH, pad = p->pad, J = p->KH * p->KH * C;
-    const bool vec = (C % VEC) == 0;
+    const int pix0 = kb * BK + pg * VEC;
+    u32x4 pixv[VEC];
+    const bool vec = (C % VEC) == 0 && j0 + VEC <= J;
+    int t = 0, c0 = 0, u = 0, vv = 0;
+    if (vec) {
+      t = j0 / C;
+      c0 = j0 - t * C;
+      u = t / KW;
+      vv = t - u * KW;
+    }
+    // pixel coordinates: with pooling, VEC consecutive pixels are VEC/4 whole
+    // windows (one decode each); without, decode the first and step along x
+    int wn[VEC / 4 > 0 ? VEC / 4 : 1], wy[VEC / 4 > 0 ? VEC / 4 : 1], wx[VEC / 4 > 0 ? VEC / 4 : 1];
+    int rn = 0, ry = 0, rx = 0;
+    if (p->pool) {
 #pragma unroll
-    for (int s = 0; s < NV; ++s) {
-      const int v = threadIdx.x + 256 * s, jv = v % VPN, pix = kb * BK + v / VPN, j0 = n0 + jv * VEC;
+      for (int wq = 0; wq < VEC / 4; ++wq) {
+        const int w = (pix0 >> 2) + wq, pp = p->PH * p->PW;
+        wn[wq] = w / pp;
+        const int rem = w - wn[wq] * pp, ph = rem / p->PW;
+        wy[wq] = 2 * ph;
+        wx[wq] = 2 * (rem - ph * p->PW);
+      }
+    } else {
+      decode_out_pixel(*p, pix0, rn, ry, rx);
+    }
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const int pix = pix0 + e;
       u32x4 val = zero4();
       if (pix < p->K && j0 <= J) {
         int n, y, x;
-        decode_out_pixel(*p, pix, n, y, x);
-        if (vec && j0 + VEC <= J) {
-          const int t = j0 / C, c = j0 - t * C, u = t / KW, vv = t - u * KW;
+        if (p->pool) {
+          n = wn[e >> 2];
+          y = wy[e >> 2] + ((e >> 1) & 1);
+          x = wx[e >> 2] + (e & 1);
+        } else {
+          n = rn;
+          y = ry;
+          x = rx;
+          rx += 1;
+          if (rx == p->OW) {
+            rx = 0;
+            if (++ry == p->OH) {
+              ry = 0;
+              ++rn;
+            }
+          }
+        }
+        if (vec) {
           const int iy = y + u - pad, ix = x + vv - pad;
-          if (iy >= 0 && iy < H && ix >= 0 && ix < W) val = *(const u32x4*)(X + ((int64_t)(n * H + iy) * W + ix) * C + c);
+          if (iy >= 0 && iy < H && ix >= 0 && ix < W)
+            val = *(gptr<const u32x4>)(X + ((int64_t)(n * H + iy) * W + ix) * C + c0);
         } else {
 #pragma unroll
-          for (int e = 0; e < VEC; ++e) {
-            const int j = j0 + e;
+          for (int q = 0; q < VEC; ++q) {
+            const int j = j0 + q;
             if (j < J) {
-              const int t = j / C, c = j - t * C, u = t / KW, vv = t - u * KW;
-              const int iy = y + u - pad, ix = x + vv - pad;
+              const int tq = j / C, c = j - tq * C, uq = tq / KW, vq = tq - uq * KW;
+              const int iy = y + uq - pad, ix = x + vq - pad;
               if (iy >= 0 && iy < H && ix >= 0 && ix < W)
-                vset_bits<T>(val, e, bits_of<T>(X[((int64_t)(n * H + iy) * W + ix) * C + c]));
+                vset_bits<T>(val, q, bits_of<T>(X[((int64_t)(n * H + iy) * W + ix) * C + c]));
             } else if (j == J) {
-              vset_bits<T>(val, e, bits_of<T>(TT<T>::from_f(1.0f)));
+              vset_bits<T>(val, q, bits_of<T>(TT<T>::from_f(1.0f)));
             }
           }
         }
       }
-      r[S][s] = val;
+      pixv[e] = val;
     }
+    transpose_block<T>(pixv, r[S]);
   }
   template <int S>
   __device__ void store(T* sm) const {
+    if (!active) return;
+    const int jl = ((threadIdx.x % 128) % NGROUPS) * VEC;
 #pragma unroll
-    for (int s = 0; s < NV; ++s) {
-      const int v = threadIdx.x + 256 * s, jv = v % VPN, kp = v / VPN;
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) sm[(jv * VEC + e) * LDK + kp] = tbits<T>(vbits<T>(r[S][s], e));
-    }
+    for (int c = 0; c < VEC; ++c) *(u32x4*)(sm + (jl + c) * LDK + pg * VEC) = r[S][c];
   }
 };
 

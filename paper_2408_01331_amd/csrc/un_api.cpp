@@ -434,7 +434,7 @@ static un_status plan_and_alloc(un_ctx* c) {
         const int64_t kpix = b.pool ? (int64_t)B * b.PH * b.PW * 4 : (int64_t)B * b.OH * b.OW;
         const int nkb = cdiv(kpix, BK);
         const int tiles = cdiv(b.O, BMc) * cdiv(J + 1, BNc);
-        int splits = std::max(1, std::min(nkb, cdiv(1024, tiles)));
+        int splits = std::max(1, std::min(nkb / 4, cdiv(64, tiles)));  // >= 4 k-blocks per split, ~64 workgroups
         b.kchunk = cdiv(nkb, splits);
         b.splits = cdiv(nkb, b.kchunk);
         b.ldws = rup(J + 1, 4);
