@@ -161,8 +161,11 @@ hipError_t launch_ce(bool bf16, const CeProb* probs, int nmodels, const int32_t*
                      float* partial, float* losses, hipStream_t s);
 hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int ntiles, float lr,
                       bool use_grad, hipStream_t s);
+// fp32 NCHW batch -> storage type: NHWC X, its transpose XT (rows (h, w, c),
+// columns b; optional) and NHWC XC with Cs >= C channels (optional; the
+// channels from C on are left untouched).
 hipError_t launch_load(bool bf16, const float* x, int B, int C, int H, int W, void* X, void* XT,
-                       int64_t ldxt, hipStream_t s);
+                       int64_t ldxt, void* XC, int Cs, hipStream_t s);
 
 // Tile shapes the planner must agree with.
 constexpr int GEMM_BM_BF16 = 128, GEMM_BN_BF16 = 128;

@@ -295,8 +295,11 @@ struct Im2colLoader {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int m = m0 + (threadIdx.x + 256 * s) / VPR;
-      if (m < pr.M) decode_out_pixel(pr, m, rn[s], ry[s], rx[s]);
-      else rn[s] = -1;
+      int n, y, x;
+      decode_out_pixel(pr, m, n, y, x);
+      rn[s] = m < pr.M ? n : -1;
+      ry[s] = y;
+      rx[s] = x;
     }
   }
   template <int S>
@@ -313,7 +316,9 @@ struct Im2colLoader {
           const int y = ry[s] + u - pad, x = rx[s] + vv - pad;
           if (y >= 0 && y < H && x >= 0 && x < W) v = *(const u32x4*)(X + ((int64_t)(rn[s] * H + y) * W + x) * C + c);
         } else {
-#pragma unroll
+          // channels not a whole number of vectors: element by element (kept
+          // rolled so that the vector paths around it unroll fully)
+#pragma unroll 1
           for (int e = 0; e < VEC; ++e) {
             const int k = k0 + e;
             if (k < K) {
@@ -380,15 +385,12 @@ struct DzGatherLoader {
     const int hw = pr.H * pr.W;
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
+      // every field written on both sides of the bound (no address select)
       const int m = m0 + (threadIdx.x + 256 * s) / VPR;
-      if (m < pr.M) {
-        rn[s] = m / hw;
-        const int rem = m - rn[s] * hw;
-        ry[s] = rem / pr.W;
-        rx[s] = rem - ry[s] * pr.W;
-      } else {
-        rn[s] = -1;
-      }
+      const int n = m / hw, rem = m - n * hw, y = rem / pr.W;
+      rn[s] = m < pr.M ? n : -1;
+      ry[s] = y;
+      rx[s] = rem - y * pr.W;
     }
   }
   template <int S>
@@ -409,7 +411,7 @@ struct DzGatherLoader {
             if (d >= 0) select_am<T>(v, load_am<T>(p->gam + idx + o), d);
           }
         } else {
-#pragma unroll
+#pragma unroll 1
           for (int e = 0; e < VEC; ++e) {
             const int k = k0 + e;
             if (k < K) {
@@ -463,28 +465,42 @@ template <> __device__ __forceinline__ void transpose_block<bf16_t>(const u32x4 
     }
 }
 
+// Micro-tile of thread t (0..127): 16 row groups x 8 pixel groups. Each run
+// of 8 threads takes the 8 pixel groups of one row group, so its 16-byte LDS
+// stores (same row, 8 column chunks) fall in distinct banks; the next 8 take
+// the adjacent row group (the neighbouring 16 bytes in global memory).
+__device__ __forceinline__ void microtile_of(int t, int& rg, int& pg) {
+  pg = t & 7;
+  rg = ((t >> 3) & 1) | ((t >> 4) << 1);
+}
+
 // A: rows = output channel o, k = output pixel. dZ gathered from the pooled
 // gradient G[w][o] (already ReLU'-masked) and the window argmax.
 template <typename T, int ROWS, int BK>
 struct DzRowsLoader {
-  static constexpr int VEC = TT<T>::VEC, MGROUPS = ROWS / VEC, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
-  static_assert(ROWS * BK / (VEC * VEC) == 128, "128 micro-tiles per operand");
+  static constexpr int VEC = TT<T>::VEC, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
+  static_assert(ROWS / VEC == 16 && BK / VEC == 8, "16 x 8 micro-tiles per operand");
   const ConvProb* p;
   const T* G;
-  int o0, pg;
+  int o0, rg, pg;
   bool active;
   u32x4 r[2][VEC];
   __device__ void init(const ConvProb& pr, int m0) {
     p = &pr;
     G = (const T*)pr.G;
     active = threadIdx.x < 128;
-    o0 = m0 + (threadIdx.x % MGROUPS) * VEC;
-    pg = (threadIdx.x % 128) / MGROUPS;
+    microtile_of(threadIdx.x % 128, rg, pg);
+    o0 = m0 + rg * VEC;
   }
   template <int S>
   __device__ void load(int kb) {
     if (!active) return;
     const int O = p->O;
+    if (o0 >= O) {  // rows past the last output channel
+#pragma unroll
+      for (int c = 0; c < VEC; ++c) r[S][c] = zero4();
+      return;
+    }
     const int pix0 = kb * BK + pg * VEC;
     u32x4 pixv[VEC];
     if (o0 + VEC <= O && (O % VEC) == 0) {
@@ -516,6 +532,7 @@ struct DzRowsLoader {
         }
       }
     } else {
+      // output channels not a whole number of vectors: element by element
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
         const int pix = pix0 + e;
@@ -523,7 +540,7 @@ struct DzRowsLoader {
         if (pix < p->K) {
           const int64_t idx = (int64_t)(p->pool ? (pix >> 2) : pix) * O;
           const int d = p->pool ? (pix & 3) : -1;
-#pragma unroll
+#pragma unroll 1
           for (int c = 0; c < VEC; ++c)
             if (o0 + c < O && (d < 0 || p->gam[idx + o0 + c] == d)) vset_bits<T>(v, c, bits_of<T>(G[idx + o0 + c]));
         }
@@ -535,7 +552,7 @@ struct DzRowsLoader {
   template <int S>
   __device__ void store(T* sm) const {
     if (!active) return;
-    const int ol = (threadIdx.x % MGROUPS) * VEC;
+    const int ol = rg * VEC;
 #pragma unroll
     for (int c = 0; c < VEC; ++c) *(u32x4*)(sm + (ol + c) * LDK + pg * VEC) = r[S][c];
   }
@@ -545,28 +562,35 @@ struct DzRowsLoader {
 // output pixel: the input patch, gathered from NHWC X.
 template <typename T, int ROWS, int BK>
 struct PatchRowsLoader {
-  static constexpr int VEC = TT<T>::VEC, NGROUPS = ROWS / VEC, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
-  static_assert(ROWS * BK / (VEC * VEC) == 128, "128 micro-tiles per operand");
+  static constexpr int VEC = TT<T>::VEC, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
+  static_assert(ROWS / VEC == 16 && BK / VEC == 8, "16 x 8 micro-tiles per operand");
   const ConvProb* p;
   const T* X;
-  int j0, pg;
+  int j0, rg, pg;
   bool active;
   u32x4 r[2][VEC];
   __device__ void init(const ConvProb& pr, int n0) {
     p = &pr;
     X = (const T*)pr.X;
     active = threadIdx.x >= 128;
-    const int t = threadIdx.x % 128;
-    j0 = n0 + (t % NGROUPS) * VEC;
-    pg = t / NGROUPS;
+    microtile_of(threadIdx.x % 128, rg, pg);
+    j0 = n0 + rg * VEC;
   }
   template <int S>
   __device__ void load(int kb) {
     if (!active) return;
     const int C = p->C, H = p->H, W = p->W, KW = p->KH, pad = p->pad, J = p->KH * p->KH * C;
+    if (j0 > J) {  // rows past the bias column
+#pragma unroll
+      for (int c = 0; c < VEC; ++c) r[S][c] = zero4();
+      return;
+    }
     const int pix0 = kb * BK + pg * VEC;
     u32x4 pixv[VEC];
-    const bool vec = (C % VEC) == 0 && j0 + VEC <= J;
+    // vector path: whole-vector channels; the chunk at j0 == J is then the
+    // bias column (1, 0, ..., 0)
+    const bool vec = (C % VEC) == 0;
+    const bool bias_chunk = j0 == J;
     int t = 0, c0 = 0, u = 0, vv = 0;
     if (vec) {
       t = j0 / C;
@@ -615,10 +639,12 @@ struct PatchRowsLoader {
         }
         if (vec) {
           const int iy = y + u - pad, ix = x + vv - pad;
-          if (iy >= 0 && iy < H && ix >= 0 && ix < W)
+          if (bias_chunk)
+            vset_bits<T>(val, 0, bits_of<T>(TT<T>::from_f(1.0f)));
+          else if (iy >= 0 && iy < H && ix >= 0 && ix < W)
             val = *(gptr<const u32x4>)(X + ((int64_t)(n * H + iy) * W + ix) * C + c0);
         } else {
-#pragma unroll
+#pragma unroll 1
           for (int q = 0; q < VEC; ++q) {
             const int j = j0 + q;
             if (j < J) {
@@ -639,7 +665,7 @@ struct PatchRowsLoader {
   template <int S>
   __device__ void store(T* sm) const {
     if (!active) return;
-    const int jl = ((threadIdx.x % 128) % NGROUPS) * VEC;
+    const int jl = rg * VEC;
 #pragma unroll
     for (int c = 0; c < VEC; ++c) *(u32x4*)(sm + (jl + c) * LDK + pg * VEC) = r[S][c];
   }
@@ -913,7 +939,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
         }
       } else {
         const int nv = min(4, p.M - mb), pp = p.OH * p.OW;
-        for (int r = 0; r < nv; ++r) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if (r >= nv) break;
           const int m = mb + r;
           store_t<T>(p.P, (int64_t)m * O + o, v[r]);
           if (p.PT) {
@@ -962,7 +990,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     for (int j = 0; j < TL::FN; ++j) {
       const int c = n0 + wn + 16 * j + (lane & 15);
       if (c >= C) continue;
-      for (int r = 0; r < nv; ++r) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if (r >= nv) break;
         float v = acc[i][j][r];
         const int64_t idx = (int64_t)(mb + r) * C + c;
         if (p.prev_relu && !(TT<T>::to_f(X[idx]) > 0.f)) v = 0.f;
@@ -1012,7 +1042,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
     for (int j = 0; j < TL::FN; ++j) {
       const int n = n0 + wn + 16 * j + (lane & 15);
       if (n >= p.N) continue;
-      for (int r = 0; r < nv; ++r) ws[(int64_t)(mb + r) * p.ldws + n] = acc[i][j][r];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (r < nv) ws[(int64_t)(mb + r) * p.ldws + n] = acc[i][j][r];
     }
   }
 }
@@ -1162,11 +1194,13 @@ __global__ __launch_bounds__(256) void sgd_kernel(const SgdTensor* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
-// Batch load: fp32 NCHW -> storage-type NHWC (+ transposed [(h*W+w)*C + c][b]).
+// Batch load: fp32 NCHW -> storage-type NHWC (+ transposed [(h*W+w)*C + c][b],
+// + NHWC with Cs stored channels).
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, int B, int C, int H, int W,
-                                                   T* __restrict__ X, T* __restrict__ XT, int64_t ldxt) {
+                                                   T* __restrict__ X, T* __restrict__ XT, int64_t ldxt,
+                                                   T* __restrict__ XC, int Cs) {
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t total = (int64_t)B * C * H * W;
   if (e >= total) return;
@@ -1175,8 +1209,9 @@ __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, 
   const int rem = (int)(e - b * C * hw);
   const int c = rem / hw, s = rem - c * hw;
   const T v = TT<T>::from_f(x[e]);
-  X[(b * hw + s) * C + c] = v;
+  if (X) X[(b * hw + s) * C + c] = v;
   if (XT) XT[(int64_t)(s * C + c) * ldxt + b] = v;
+  if (XC) XC[(b * hw + s) * Cs + c] = v;
 }
 
 // ---------------------------------------------------------------------------
@@ -1265,16 +1300,16 @@ hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor,
 }
 
 hipError_t launch_load(bool bf16, const float* x, int B, int C, int H, int W, void* X, void* XT, int64_t ldxt,
-                       hipStream_t s) {
+                       void* XC, int Cs, hipStream_t s) {
   const int64_t total = (int64_t)B * C * H * W;
   const int blocks = (int)((total + 255) / 256);
   if (blocks <= 0) return hipSuccess;
   if (bf16)
     hipLaunchKernelGGL(load_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, x, B, C, H, W, (bf16_t*)X, (bf16_t*)XT,
-                       ldxt);
+                       ldxt, (bf16_t*)XC, Cs);
   else
     hipLaunchKernelGGL(load_kernel<float>, dim3(blocks), dim3(256), 0, s, x, B, C, H, W, (float*)X, (float*)XT,
-                       ldxt);
+                       ldxt, (float*)XC, Cs);
   return hipGetLastError();
 }
 

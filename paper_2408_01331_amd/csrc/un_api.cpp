@@ -43,6 +43,7 @@ struct Block {
   int in_c = 0, in_h = 1, in_w = 1;  // input viewed as an image (Flatten order mapping)
   // conv
   int C = 0, H = 0, W = 0, O = 0, KH = 0, pad = 0, OH = 0, OW = 0, PH = 0, PW = 0;
+  int Cr = 0;  // the model's input channels; C (stored channels) is larger for a padded network input
   // PyTorch-layout offsets in the model's flat parameter vector
   size_t pt_w = 0, pt_b = 0, n_w = 0, n_b = 0;
   // arena offsets (NONE = absent)
@@ -99,6 +100,8 @@ struct un_ctx {
   hipStream_t stream = nullptr;
   // fixed buffers
   size_t xstage = NONE, ydev = NONE, losses_dev = NONE, ce_partial = NONE, Xin = NONE, XinT = NONE;
+  size_t XinC = NONE;  // NHWC input with channels padded to a 16-byte multiple (first convs only)
+  int in_cs = 0;       // stored channels of XinC
   int64_t ldxin = 0, ldxint = 0;
   // schedule
   std::vector<Launch> fwd, bwd[2];  // bwd[p]: dgrad reads copy p of the transposed weights
@@ -172,6 +175,7 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
       Block b;
       b.kind = 1;
       b.C = c;
+      b.Cr = c;
       b.H = h;
       b.W = w;
       b.O = L.out;
@@ -319,11 +323,25 @@ static un_status plan_and_alloc(un_ctx* c) {
   c->ydev = A.take((size_t)B * 4);
   c->losses_dev = A.take(c->models.size() * 4);
   c->ce_partial = A.take(c->models.size() * (size_t)cdiv(B, CE_ROWS) * 4);
-  c->Xin = A.take((size_t)B * in_feat * es);
-  c->ldxin = in_feat;
-  bool any_linear0 = false;
-  for (auto& m : c->models)
+  bool any_linear0 = false, any_conv0 = false;
+  for (auto& m : c->models) {
     if (m.blocks[0].kind == 0) any_linear0 = true;
+    else any_conv0 = true;
+  }
+  // A first conv whose input channels are not a whole number of 16-byte
+  // vectors (RGB, grey-scale) reads a copy of the input with zero channels
+  // appended: its loaders then take whole vectors, and the padded weight
+  // columns meet zeros only, so their gradient is exactly 0 and they stay 0.
+  const int vec = bf ? 8 : 4;
+  c->in_cs = c->in_c;
+  if (any_conv0 && c->in_c % vec != 0) {
+    c->in_cs = (int)rup(c->in_c, vec);
+    c->XinC = A.take((size_t)B * c->in_h * c->in_w * c->in_cs * es);
+    for (auto& m : c->models)
+      if (m.blocks[0].kind == 1) m.blocks[0].C = c->in_cs;
+  }
+  if (c->XinC == NONE || any_linear0) c->Xin = A.take((size_t)B * in_feat * es);
+  c->ldxin = in_feat;
   if (any_linear0) {
     if (in_feat % 8 != 0) return fail(nullptr, UN_ERR_UNSUPPORTED, "input features must be a multiple of 8 when a model starts with Linear");
     c->ldxint = Bp;
@@ -445,7 +463,7 @@ static un_status plan_and_alloc(un_ctx* c) {
     for (size_t j = 0; j < m.blocks.size(); ++j) {
       Block& b = m.blocks[j];
       if (j == 0) {
-        b.X = c->Xin;
+        b.X = (b.kind == 1 && c->XinC != NONE) ? c->XinC : c->Xin;
         b.ldx = c->ldxin;
         b.XT = c->XinT;
         b.ldxt = c->ldxint;
@@ -873,6 +891,9 @@ static un_status plan_and_alloc(un_ctx* c) {
                           c->stream);
   };
   if (c->XinT != NONE) HIPCHK(c, set_ones_row(c->XinT, in_feat, Bp));
+  // the padding channels of XinC are written here only, once
+  if (c->XinC != NONE)
+    HIPCHK(c, hipMemsetAsync(c->base + c->XinC, 0, (size_t)B * c->in_h * c->in_w * c->in_cs * es, c->stream));
   for (auto& m : c->models)
     for (auto& b : m.blocks)
       if (b.YT != NONE && !b.concat) HIPCHK(c, set_ones_row(b.YT, b.out_elems_per_sample(), b.ldyt));
@@ -908,11 +929,11 @@ static void to_internal(const Block& b, const float* pt, std::vector<float>& w, 
   } else {
     w.assign((size_t)b.O * b.ldw, 0.f);
     for (int o = 0; o < b.O; ++o)
-      for (int ci = 0; ci < b.C; ++ci)
+      for (int ci = 0; ci < b.Cr; ++ci)
         for (int u = 0; u < b.KH; ++u)
           for (int v = 0; v < b.KH; ++v)
             w[(size_t)o * b.ldw + ((size_t)u * b.KH + v) * b.C + ci] =
-                pt[b.pt_w + (((size_t)o * b.C + ci) * b.KH + u) * b.KH + v];
+                pt[b.pt_w + (((size_t)o * b.Cr + ci) * b.KH + u) * b.KH + v];
     bias.assign(pt + b.pt_b, pt + b.pt_b + b.O);
   }
 }
@@ -924,10 +945,10 @@ static void from_internal(const Block& b, const std::vector<float>& w, const std
     std::copy(bias.begin(), bias.end(), pt + b.pt_b);
   } else {
     for (int o = 0; o < b.O; ++o)
-      for (int ci = 0; ci < b.C; ++ci)
+      for (int ci = 0; ci < b.Cr; ++ci)
         for (int u = 0; u < b.KH; ++u)
           for (int v = 0; v < b.KH; ++v)
-            pt[b.pt_w + (((size_t)o * b.C + ci) * b.KH + u) * b.KH + v] =
+            pt[b.pt_w + (((size_t)o * b.Cr + ci) * b.KH + u) * b.KH + v] =
                 w[(size_t)o * b.ldw + ((size_t)u * b.KH + v) * b.C + ci];
     std::copy(bias.begin(), bias.end(), pt + b.pt_b);
   }
@@ -975,7 +996,7 @@ static void init_host(const Model& m, std::vector<float>& pt) {
   pt.assign(m.n_params, 0.f);
   int t = 0;
   for (auto& b : m.blocks) {
-    const double fan_in = b.kind == 0 ? (double)b.K : (double)b.C * b.KH * b.KH;
+    const double fan_in = b.kind == 0 ? (double)b.K : (double)b.Cr * b.KH * b.KH;
     const double wb = std::sqrt(6.0 / fan_in), bb = 1.0 / std::sqrt(fan_in);
     for (int part = 0; part < 2; ++part, ++t) {
       const size_t off = part == 0 ? b.pt_w : b.pt_b, n = part == 0 ? b.n_w : b.n_b;
@@ -1145,8 +1166,9 @@ static un_status load_common(un_ctx* c, const float* x, const int32_t* y, bool d
     xsrc = c->at<float>(c->xstage);
   }
   HIPCHK(c, hipMemcpyAsync(c->base + c->ydev, yh.data(), (size_t)c->B * 4, hipMemcpyHostToDevice, c->stream));
-  HIPCHK(c, launch_load(c->bf16, xsrc, c->B, c->in_c, c->in_h, c->in_w, c->base + c->Xin,
-                        c->XinT == NONE ? nullptr : c->base + c->XinT, c->ldxint, c->stream));
+  HIPCHK(c, launch_load(c->bf16, xsrc, c->B, c->in_c, c->in_h, c->in_w, c->Xin == NONE ? nullptr : c->base + c->Xin,
+                        c->XinT == NONE ? nullptr : c->base + c->XinT, c->ldxint,
+                        c->XinC == NONE ? nullptr : c->base + c->XinC, c->in_cs, c->stream));
   HIPCHK(c, hipStreamSynchronize(c->stream));
   c->loaded = true;
   return UN_OK;
