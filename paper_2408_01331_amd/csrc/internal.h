@@ -37,7 +37,6 @@ struct GemmProb {
   int32_t M, N, K;
   int32_t epi, relu;
   int32_t tiles_n;
-  int32_t tile_base;
   int32_t nsplit;
   void* C;                    // WGRAD: gradient dW [m][ldc] (stored only when gradients are kept)
   int64_t ldc;
@@ -76,7 +75,7 @@ struct ConvProb {
   int32_t Nb, C, H, W, O, KH, pad, OH, OW, PH, PW;
   int32_t pool, relu, prev_relu;
   int32_t M, N, K;            // GEMM sizes of this pass
-  int32_t tiles_m, tiles_n, tile_base, splits, kchunk;
+  int32_t tiles_m, tiles_n, splits, kchunk;
   const void* X;              // conv input, NHWC, channel stride C
   const void* Wt;             // fwd: W [O][ldw]; dgrad: WT [C][ldw]
   int64_t ldw;
@@ -147,13 +146,16 @@ struct SgdTensor {
 };
 
 // Kernel launch wrappers (kernels.hip). `bf16` selects the storage type.
-hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_prob, int ntiles, float lr,
-                       bool keep_grads, bool xcd_remap, hipStream_t s);
-hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles,
+// `tile_map` holds one (problem index, tile index within the problem) pair of
+// int32 per workgroup, in launch order; a pair with problem -1 is padding and
+// its workgroup does nothing.
+hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
+                       bool keep_grads, hipStream_t s);
+hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                            hipStream_t s);
-hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles,
+hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                              hipStream_t s);
-hipError_t launch_conv_wgrad(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles,
+hipError_t launch_conv_wgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                              hipStream_t s);
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
                          bool keep_grads, hipStream_t s);

@@ -193,15 +193,6 @@ struct Smem {
   static constexpr size_t BYTES = MAIN > EPI ? MAIN : EPI;
 };
 
-// Workgroups are dispatched round-robin over the 8 XCDs. Give every XCD a
-// contiguous range of the tile list, so tiles that share an operand block
-// (consecutive tiles) share that XCD's L2.
-__device__ __forceinline__ int xcd_tile(int bid, int nblocks) {
-  const int per = nblocks >> 3;
-  if (bid >= per * 8) return bid;
-  return (bid & 7) * per + (bid >> 3);
-}
-
 // ---------------------------------------------------------------------------
 // Loaders. load(kb) fetches a k-block from global memory into registers,
 // store(s) writes it to LDS as [row][k] (k contiguous, row stride LDK).
@@ -747,14 +738,14 @@ __device__ __forceinline__ void store_cols(const float* sC, OT* CT, int64_t ldct
 
 template <typename T, int BM, int BN, int BK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(const GemmProb* __restrict__ probs,
-                                                   const int32_t* __restrict__ tile_prob, float lr,
-                                                   int keep_grads, int remap) {
+                                                   const int32_t* __restrict__ tile_map, float lr,
+                                                   int keep_grads) {
   using TL = Tile<T, BM, BN, BK>;
   using SM = Smem<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[SM::BYTES];
-  const int tile = remap ? xcd_tile(blockIdx.x, gridDim.x) : (int)blockIdx.x;
-  const GemmProb& p = probs[tile_prob[tile]];
-  const int local = tile - p.tile_base;
+  const int prob = tile_map[2 * blockIdx.x], local = tile_map[2 * blockIdx.x + 1];
+  if (prob < 0) return;  // padding of the XCD-ordered tile list
+  const GemmProb& p = probs[prob];
   const int tiles_m = (p.M + BM - 1) / BM;
   const int tn = local / tiles_m, tm = local - tn * tiles_m;   // m fastest: neighbours share B
   const int m0 = tm * BM, n0 = tn * BN;
@@ -881,12 +872,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
 // ---------------------------------------------------------------------------
 template <typename T, int BM, int BN, int BK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_fwd_kernel(const ConvProb* __restrict__ probs,
-                                                       const int32_t* __restrict__ tile_prob) {
+                                                       const int32_t* __restrict__ tile_map) {
   using TL = Tile<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
-  const int tile = blockIdx.x;
-  const ConvProb& p = probs[tile_prob[tile]];
-  const int local = tile - p.tile_base;
+  const int prob = tile_map[2 * blockIdx.x], local = tile_map[2 * blockIdx.x + 1];
+  if (prob < 0) return;  // padding of the XCD-ordered tile list
+  const ConvProb& p = probs[prob];
   const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
 
@@ -956,12 +947,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 
 template <typename T, int BM, int BN, int BK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_dgrad_kernel(const ConvProb* __restrict__ probs,
-                                                         const int32_t* __restrict__ tile_prob) {
+                                                         const int32_t* __restrict__ tile_map) {
   using TL = Tile<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
-  const int tile = blockIdx.x;
-  const ConvProb& p = probs[tile_prob[tile]];
-  const int local = tile - p.tile_base;
+  const int prob = tile_map[2 * blockIdx.x], local = tile_map[2 * blockIdx.x + 1];
+  if (prob < 0) return;  // padding of the XCD-ordered tile list
+  const ConvProb& p = probs[prob];
   const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
 
@@ -1004,12 +995,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 
 template <typename T, int BM, int BN, int BK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_wgrad_kernel(const ConvProb* __restrict__ probs,
-                                                         const int32_t* __restrict__ tile_prob) {
+                                                         const int32_t* __restrict__ tile_map) {
   using TL = Tile<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
-  const int tile = blockIdx.x;
-  const ConvProb& p = probs[tile_prob[tile]];
-  int local = tile - p.tile_base;
+  const int prob = tile_map[2 * blockIdx.x];
+  int local = tile_map[2 * blockIdx.x + 1];
+  if (prob < 0) return;  // padding of the XCD-ordered tile list
+  const ConvProb& p = probs[prob];
   const int per_split = p.tiles_m * p.tiles_n;
   const int split = local / per_split;
   local -= split * per_split;
@@ -1217,48 +1209,48 @@ __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, 
 // ---------------------------------------------------------------------------
 // Launch wrappers
 // ---------------------------------------------------------------------------
-hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_prob, int ntiles, float lr,
-                       bool keep_grads, bool xcd_remap, hipStream_t s) {
+hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
+                       bool keep_grads, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   if (bf16)
     hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16>), dim3(ntiles), dim3(256), 0, s, probs,
-                       tile_prob, lr, (int)keep_grads, (int)xcd_remap);
+                       tile_map, lr, (int)keep_grads);
   else
     hipLaunchKernelGGL((gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, GEMM_BK_F32>), dim3(ntiles), dim3(256), 0, s, probs,
-                       tile_prob, lr, (int)keep_grads, (int)xcd_remap);
+                       tile_map, lr, (int)keep_grads);
   return hipGetLastError();
 }
 
-hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles, hipStream_t s) {
+hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   if (bf16)
     hipLaunchKernelGGL((conv_fwd_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>), dim3(ntiles), dim3(256),
-                       0, s, probs, tile_prob);
+                       0, s, probs, tile_map);
   else
     hipLaunchKernelGGL((conv_fwd_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32>), dim3(ntiles), dim3(256), 0,
-                       s, probs, tile_prob);
+                       s, probs, tile_map);
   return hipGetLastError();
 }
 
-hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles, hipStream_t s) {
+hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   if (bf16)
     hipLaunchKernelGGL((conv_dgrad_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>), dim3(ntiles),
-                       dim3(256), 0, s, probs, tile_prob);
+                       dim3(256), 0, s, probs, tile_map);
   else
     hipLaunchKernelGGL((conv_dgrad_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32>), dim3(ntiles), dim3(256),
-                       0, s, probs, tile_prob);
+                       0, s, probs, tile_map);
   return hipGetLastError();
 }
 
-hipError_t launch_conv_wgrad(bool bf16, const ConvProb* probs, const int32_t* tile_prob, int ntiles, hipStream_t s) {
+hipError_t launch_conv_wgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   if (bf16)
     hipLaunchKernelGGL((conv_wgrad_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>), dim3(ntiles),
-                       dim3(256), 0, s, probs, tile_prob);
+                       dim3(256), 0, s, probs, tile_map);
   else
     hipLaunchKernelGGL((conv_wgrad_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32>), dim3(ntiles), dim3(256),
-                       0, s, probs, tile_prob);
+                       0, s, probs, tile_map);
   return hipGetLastError();
 }
 

@@ -76,7 +76,6 @@ struct Launch {
   int kclass;
   size_t probs, map;  // arena offsets
   int count;
-  int remap = 0;      // XCD-contiguous tile ranges (uniform-cost tile lists only)
 };
 
 struct EventRec {
@@ -309,6 +308,48 @@ inline uint64_t splitmix(uint64_t x) {
 }  // namespace
 
 // ==========================================================================
+// XCD-aware dispatch order
+// ==========================================================================
+// Workgroup b of a launch runs on XCD b % 8 (round-robin dispatch), and each
+// XCD starts its workgroups in increasing b. The tiles of a launch are cut
+// into groups that share operands (a run of one problem's tiles); groups are
+// given out longest first, each to the XCD with the least work so far, and
+// the per-XCD lists are interleaved back into launch order, so a group's tiles
+// run on one XCD, close together in time, out of that XCD's L2. Short lists
+// are padded with empty entries (the workgroup exits at once). The order
+// decides where and when a tile runs, never what it computes.
+struct TileGroup {
+  int32_t prob, first, count;  // tiles [first, first + count) of problem prob
+  double cost;                 // estimated time of the whole group
+};
+
+static std::vector<int32_t> xcd_order(std::vector<TileGroup> groups) {
+  constexpr int NX = 8;
+  std::stable_sort(groups.begin(), groups.end(), [](const TileGroup& a, const TileGroup& b) { return a.cost > b.cost; });
+  std::vector<std::vector<int32_t>> q(NX);  // (prob, local) pairs per XCD
+  double load[NX] = {0};
+  for (const TileGroup& g : groups) {
+    int x = 0;
+    for (int i = 1; i < NX; ++i)
+      if (load[i] < load[x]) x = i;
+    load[x] += g.cost;
+    for (int t = 0; t < g.count; ++t) {
+      q[x].push_back(g.prob);
+      q[x].push_back(g.first + t);
+    }
+  }
+  size_t len = 0;
+  for (auto& v : q) len = std::max(len, v.size() / 2);
+  std::vector<int32_t> map(2 * NX * len, -1);
+  for (int x = 0; x < NX; ++x)
+    for (size_t i = 0; i < q[x].size() / 2; ++i) {
+      map[2 * (i * NX + x)] = q[x][2 * i];
+      map[2 * (i * NX + x) + 1] = q[x][2 * i + 1];
+    }
+  return map;
+}
+
+// ==========================================================================
 // Planner
 // ==========================================================================
 static un_status plan_and_alloc(un_ctx* c) {
@@ -500,18 +541,19 @@ static un_status plan_and_alloc(un_ctx* c) {
   auto emit_gemm = [&](std::vector<GemmProb>& ps, std::vector<Launch>& out, int kclass) {
     if (ps.empty()) return;
     std::stable_sort(ps.begin(), ps.end(), [](const GemmProb& x, const GemmProb& y) { return x.K > y.K; });
-    bool uniform = true;
-    for (auto& p : ps) uniform = uniform && p.K == ps[0].K;
-    uniform = uniform && ps.size() == 1;
+    // Launch order = problem order (longest K first), tiles in order: the
+    // operands of a level's GEMMs are reused from the shared L2/MALL well
+    // enough that XCD grouping did not pay here, while tile-grain
+    // longest-first order keeps the tail short.
     std::vector<int32_t> map;
-    for (auto& p : ps) {
+    for (size_t k = 0; k < ps.size(); ++k) {
+      GemmProb& p = ps[k];
       const int tm = cdiv(p.M, GBM), tn = cdiv(p.N, GBN);
       p.tiles_n = tn;
-      p.tile_base = (int32_t)map.size();
-      // Split-K for a narrow problem with a long K, from its own shape only
-      // (so a model computes the same values alone or merged): at least 4
-      // k-blocks per split, aiming at ~64 workgroups for the problem.
-      for (int t = 0; t < tm * tn; ++t) map.push_back((int32_t)(&p - ps.data()));
+      for (int t = 0; t < tm * tn; ++t) {
+        map.push_back((int32_t)k);
+        map.push_back(t);
+      }
     }
     size_t po = put(ps.data(), ps.size() * sizeof(GemmProb));
     for (size_t k = 0; k < ps.size(); ++k) {
@@ -523,19 +565,36 @@ static un_status plan_and_alloc(un_ctx* c) {
         fix.push_back(b0 + f);
     }
     size_t mo = put(map.data(), map.size() * 4);
-    out.push_back(Launch{0, kclass, po, mo, (int)map.size(), uniform ? 1 : 0});
+    out.push_back(Launch{0, kclass, po, mo, (int)(map.size() / 2)});
   };
   auto emit_conv = [&](std::vector<ConvProb>& ps, std::vector<Launch>& out, int kind, int kclass) {
     if (ps.empty()) return;
     std::stable_sort(ps.begin(), ps.end(),
                      [](const ConvProb& x, const ConvProb& y) { return (int64_t)x.K * x.splits > (int64_t)y.K * y.splits; });
-    std::vector<int32_t> map;
-    for (auto& p : ps) {
+    const int BK = bf ? CONV_BK_BF16 : CONV_BK_F32;
+    std::vector<TileGroup> gs;
+    for (size_t k = 0; k < ps.size(); ++k) {
+      ConvProb& p = ps[k];
       p.tiles_m = cdiv(p.M, CBM);
       p.tiles_n = cdiv(p.N, CBN);
-      p.tile_base = (int32_t)map.size();
-      const int nt = p.tiles_m * p.tiles_n * p.splits;
-      for (int t = 0; t < nt; ++t) map.push_back((int32_t)(&p - ps.data()));
+      const int per_split = p.tiles_m * p.tiles_n;
+      if (kind == 3) {
+        // weight gradient: one group per split (its tiles read the same pixels)
+        for (int sp = 0; sp < p.splits; ++sp)
+          gs.push_back(TileGroup{(int32_t)k, sp * per_split, per_split, per_split * (p.kchunk + 1.0)});
+      } else {
+        // forward / data gradient: tiles in order (n-fastest), one tile per group
+        for (int t = 0; t < per_split; ++t) gs.push_back(TileGroup{(int32_t)k, t, 1, cdiv(p.K, BK) + 2.0});
+      }
+    }
+    std::vector<int32_t> map;
+    if (kind == 3) {
+      map = xcd_order(gs);
+    } else {
+      for (auto& g : gs) {
+        map.push_back(g.prob);
+        map.push_back(g.first);
+      }
     }
     size_t po = put(ps.data(), ps.size() * sizeof(ConvProb));
     for (size_t k = 0; k < ps.size(); ++k) {
@@ -546,7 +605,7 @@ static un_status plan_and_alloc(un_ctx* c) {
         fix.push_back(b0 + f);
     }
     size_t mo = put(map.data(), map.size() * 4);
-    out.push_back(Launch{kind, kclass, po, mo, (int)map.size()});
+    out.push_back(Launch{kind, kclass, po, mo, (int)(map.size() / 2)});
   };
 
   auto conv_base = [&](const Block& b) {
@@ -1034,7 +1093,7 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
   switch (l.kind) {
     case 0:
       e = launch_gemm(c->bf16, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->keep_grads,
-                      l.remap != 0, c->stream);
+                      c->stream);
       break;
     case 1:
       e = launch_conv_fwd(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
