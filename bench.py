@@ -1,15 +1,18 @@
 """Benchmark of the fused N-model training step on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload mlp64]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload mlp64] [--also cifar16]
+    python bench.py --copy-probe      # calibration copy for the HBM byte counters only
 
 Prints ONE JSON line. A step is one fused forward + softmax-CE + backward +
 SGD pass of all N models over one resident synthetic batch (un_step with no
 loss read-back). `value` is model-samples/s = N * batch * K / elapsed.
 
 Alongside: the dominant kernel class against its roofline (algorithmic FLOPs
-or bytes per step divided by its HIP-event time on the library's stream), the
-same N models stepped as N separate one-model contexts back to back (the
-unfused baseline), and the CPU oracle timed on a bounded sample.
+or bytes per launch divided by its HIP-event time on the library's stream;
+HBM traffic per launch from the committed counter summary under profiles/
+when it was taken on the current kernels), the other workloads named by
+--also, the same N models stepped as N separate one-model contexts back to
+back (the unfused baseline), and the CPU oracle timed on a bounded sample.
 """
 from __future__ import annotations
 
@@ -35,22 +38,42 @@ KCLASS = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad", "ce", 
 # Algorithmic work per step (the definition, not what the kernels happen to do)
 # ---------------------------------------------------------------------------
 def algorithmic_work(wl):
-    """FLOPs per kernel class and SGD bytes, per step, from the layer shapes."""
+    """Algorithmic FLOPs and HBM bytes per step and kernel class, from the layer shapes.
+
+    FLOPs: 2 per multiply-add of forward, weight gradient and data gradient
+    (none for the first layer), with no padding counted. Bytes: the minimum
+    under fusion, each tensor moved once per use: a stored activation is
+    written once and read by the next layer's forward and by this layer's
+    weight gradient; its gradient likewise; the weights the products read are
+    read once per use (forward, data gradient); the fused update reads and
+    writes the fp32 master (8 B per parameter) plus the bf16 copy (2 B) in bf16
+    mode. Returns (flops, bytes, n_params)."""
     B = wl.batch
+    es = 2 if wl.precision == "bf16" else 4
+    upd = 10 if wl.precision == "bf16" else 8
     flops = {k: 0.0 for k in KCLASS}
+    nbytes = {k: 0.0 for k in KCLASS}
     n_params = 0
     for spec in wl.specs:
         shape = tuple(wl.in_shape)
         first = True
-        for layer in spec["layers"]:
+        layers = spec["layers"]
+        for li, layer in enumerate(layers):
             op = layer[0]
             if op == "linear":
                 K = int(np.prod(shape))
                 N = layer[1]
-                flops["gemm_fwd"] += 2.0 * B * K * N
-                flops["gemm_bwd"] += 2.0 * B * K * N          # wgrad
-                if not first:
-                    flops["gemm_bwd"] += 2.0 * B * K * N      # dgrad
+                last = li == len(layers) - 1
+                f = 2.0 * B * K * N
+                flops["gemm_fwd"] += f
+                nbytes["gemm_fwd"] += B * K * es + N * K * es + N * 4 + B * N * (4 if last else es)
+                flops["gemm_bwd"] += f                                   # weight gradient + update
+                nbytes["gemm_bwd"] += B * N * es + B * K * es + (N * K + N) * upd
+                if not first:                                            # data gradient
+                    flops["gemm_bwd"] += f
+                    nbytes["gemm_bwd"] += B * N * es + N * K * es + B * K * es
+                if last:                                                 # softmax-CE: logits in, dZ out
+                    nbytes["ce"] += B * N * 4 + B * N * es
                 n_params += K * N + N
                 shape = (N,)
                 first = False
@@ -58,11 +81,21 @@ def algorithmic_work(wl):
                 C, H, Wd = shape
                 O, k, pad = layer[1], layer[2], layer[3]
                 OH, OW = H + 2 * pad - k + 1, Wd + 2 * pad - k + 1
+                pool = li + 1 < len(layers) and layers[li + 1][0] == "pool" or \
+                    li + 2 < len(layers) and layers[li + 1][0] == "relu" and layers[li + 2][0] == "pool"
+                out_el = B * (OH // 2) * (OW // 2) * O if pool else B * OH * OW * O
+                out_b = out_el * (es + 1 if pool else es)                # pooled values + argmax byte
+                in_b = B * H * Wd * C * es
+                w_b = O * C * k * k * es
                 f = 2.0 * B * OH * OW * O * C * k * k
                 flops["conv_fwd"] += f
+                nbytes["conv_fwd"] += in_b + w_b + out_b
                 flops["conv_wgrad"] += f
+                nbytes["conv_wgrad"] += out_b + in_b
+                nbytes["other"] += (O * C * k * k + O) * upd           # update (split-K reduction kernel)
                 if not first:
                     flops["conv_dgrad"] += f
+                    nbytes["conv_dgrad"] += out_b + w_b + in_b
                 n_params += O * C * k * k + O
                 shape = (O, OH, OW)
                 first = False
@@ -71,11 +104,7 @@ def algorithmic_work(wl):
                 shape = (C, H // 2, Wd // 2)
             elif op == "flatten":
                 shape = (int(np.prod(shape)),)
-    # SGD per parameter: read master + grad, write master (12 B), then the copies
-    # the GEMMs read: bf16 shadow (2 B) and transposed copy (2 B) in bf16 mode,
-    # transposed fp32 copy (4 B) in fp32 mode.
-    per_param = 12 + (4 if wl.precision == "bf16" else 4)
-    return flops, n_params, n_params * per_param
+    return flops, nbytes, n_params
 
 
 def run_gpu(wl, steps, warmup):
@@ -148,8 +177,43 @@ def run_unfused(wl, steps, warmup):
     return elapsed, arena
 
 
-def cpu_baseline(wl, budget_s=15.0):
-    """The oracle (as it stands) on a bounded sample: whole models, one step each."""
+def copy_probe(nbytes=1 << 30, reps=4):
+    """A plain device-to-device copy of known size (calibrates the HBM byte
+    counters: FETCH_SIZE / WRITE_SIZE read for it vs. the bytes it moves)."""
+    import torch
+    torch.cuda.set_device(0)
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        torch.mul(src, 1.0, out=dst)      # one elementwise kernel: reads and writes nbytes
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes_read": nbytes, "copy_probe_bytes_written": nbytes, "copies": reps}),
+          flush=True)
+
+
+def source_digest():
+    """sha256 of the HIP kernel source (identifies the kernels a profile was taken on)."""
+    import hashlib
+    path = os.path.join(ROOT, "paper_2408_01331_amd", "csrc", "kernels.hip")
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` on `workload` from the committed counter
+    summary, or None when there is none or the kernels changed since."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None, None
+    rec = json.load(open(path))
+    if rec.get("kernels_sha256") != source_digest():
+        return None, path
+    return rec["hbm_bytes_per_launch"], path
+
+
+def cpu_baseline(wl, budget_s=12.0):
+    """The oracle (as it stands) on a bounded sample: whole one-model steps on
+    the same batch, models taken in turn (cycling) until the budget is spent."""
     import oracle
 
     try:
@@ -159,41 +223,30 @@ def cpu_baseline(wl, budget_s=15.0):
         blas_threads = None
     cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     x, y = W.make_batch(wl, 0)
+    params = {}
     t0 = time.perf_counter()
     done = 0
-    for i in range(wl.n_models):
-        p = W.init_params(wl.specs[i], wl.in_shape, wl.seed, i)
-        oracle.step(wl.specs[i], p, x, y, wl.lr, wl.precision)
+    while True:
+        i = done % wl.n_models
+        if i not in params:
+            params[i] = W.init_params(wl.specs[i], wl.in_shape, wl.seed, i)
+        oracle.step(wl.specs[i], params[i], x, y, wl.lr, wl.precision)
         done += 1
         if time.perf_counter() - t0 > budget_s:
             break
     el = time.perf_counter() - t0
     return {"value": done * wl.batch / el, "unit": "model-samples/s",
             "cores": blas_threads if blas_threads else cores, "host_cpus": cores, "kind": "oracle",
-            "sample": f"one step of models 0..{done - 1} of {wl.n_models} (batch {wl.batch}), "
-                      f"{el:.1f} s, numpy fp64 with BLAS threads={blas_threads}"}
+            "sample": f"{done} one-model steps (models 0..{min(done, wl.n_models) - 1} of {wl.n_models} in turn, "
+                      f"batch {wl.batch}) in {el:.1f} s, numpy fp64 with BLAS threads={blas_threads}"}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="mlp64", choices=list(W.WORKLOADS))
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-unfused", action="store_true")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); the N-model step is a "
-              "single-GPU path and multi-GPU runs are not part of this build.", file=sys.stderr)
-        sys.exit(2)
-
-    wl = W.get(args.workload)
-    flops, n_params, sgd_bytes = algorithmic_work(wl)
-    elapsed, kern, losses, arena = run_gpu(wl, args.steps, args.warmup)
-    ms_step = elapsed / args.steps * 1e3
+def measure(wl, steps, warmup):
+    """Time `steps` fused steps of workload `wl`; per-kernel rooflines."""
+    flops, nbytes, n_params = algorithmic_work(wl)
+    elapsed, kern, losses, arena = run_gpu(wl, steps, warmup)
+    ms_step = elapsed / steps * 1e3
     value = wl.n_models * wl.batch / (ms_step / 1e3)
-
     mfma_peak = PEAK["bf16_mfma_tflops"] if wl.precision == "bf16" else PEAK["f32_mfma_tflops"]
     total_flops = sum(flops.values())
     # Kernel symbols: the grouped GEMM serves both gemm_fwd and gemm_bwd launches.
@@ -205,54 +258,105 @@ def main():
         n = sum(kern[c]["launches_per_step"] for c in classes if c in kern)
         if n:
             per_sym[name] = {"ms_per_step": ms, "launches_per_step": n, "avg_launch_ms": ms / n,
-                             "flops_per_step": sum(flops[c] for c in classes)}
-    dom = max((k for k in per_sym if k != "other"), key=lambda k: per_sym[k]["ms_per_step"])
+                             "flops_per_step": sum(flops[c] for c in classes),
+                             "bytes_per_step": sum(nbytes[c] for c in classes)}
+    dom = max(per_sym, key=lambda k: per_sym[k]["ms_per_step"])
     d = per_sym[dom]
-    if dom in ("sgd", "ce"):
-        achieved = (sgd_bytes if dom == "sgd" else 0.0) / (d["ms_per_step"] / 1e3) / 1e9
+    # The kernel's bound: its algorithmic arithmetic intensity against the
+    # ridge point of the peaks. achieved = algorithmic work of one launch (the
+    # step's work / launches per step) over the average launch duration, both
+    # from HIP events on the library's stream.
+    ridge = mfma_peak * 1e12 / (PEAK["hbm_gbs"] * 1e9)
+    ai = d["flops_per_step"] / d["bytes_per_step"] if d["bytes_per_step"] else float("inf")
+    launch_s = d["avg_launch_ms"] / 1e3
+    if ai < ridge:
+        achieved = d["bytes_per_step"] / d["launches_per_step"] / launch_s / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": PEAK["hbm_gbs"], "unit": "GB/s"}
     else:
-        achieved = d["flops_per_step"] / (d["ms_per_step"] / 1e3) / 1e12
+        achieved = d["flops_per_step"] / d["launches_per_step"] / launch_s / 1e12
         roof = {"bound": "mfma", "achieved": achieved, "peak": mfma_peak, "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
+    kname = f"{dom}_{wl.precision}"
+    traffic, tpath = measured_traffic(kname, wl.name)
+    roof["traffic"] = traffic
+    roof["traffic_unit"] = "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE scaled by a plain copy)"
     roof["kernel"] = dom
     roof["avg_launch_ms"] = d["avg_launch_ms"]
+    roof["launches_per_step"] = d["launches_per_step"]
+    roof["algorithmic_flops_per_launch"] = d["flops_per_step"] / d["launches_per_step"]
+    roof["algorithmic_bytes_per_launch"] = d["bytes_per_step"] / d["launches_per_step"]
+    roof["arith_intensity"] = ai
+    roof["ridge"] = ridge
+    roof["mfma_frac"] = d["flops_per_step"] / d["launches_per_step"] / launch_s / 1e12 / mfma_peak
     per_kernel = {}
     for k, v in kern.items():
         e = dict(v)
-        if k == "sgd":
-            e["achieved_gbs"] = sgd_bytes / (v["ms_per_step"] / 1e3) / 1e9
-        elif flops.get(k):
+        if flops.get(k):
             e["achieved_tflops"] = flops[k] / (v["ms_per_step"] / 1e3) / 1e12
+        if nbytes.get(k):
+            e["achieved_gbs"] = nbytes[k] / (v["ms_per_step"] / 1e3) / 1e9
         per_kernel[k] = e
+    return {
+        "value": value, "ms_per_step": ms_step, "steps": steps, "warmup": warmup,
+        "config": {"workload": wl.name, "description": wl.description, "n_models": wl.n_models,
+                   "batch": wl.batch, "in_shape": list(wl.in_shape), "params": n_params,
+                   "parallelism": "none (one GPU, N models fused)"},
+        "dtype": wl.precision,
+        "mfma_util_step": total_flops / (ms_step / 1e3) / 1e12 / mfma_peak,
+        "train_gflop_per_step": total_flops / 1e9,
+        "roofline": roof, "kernels": per_kernel, "arena_bytes": arena,
+        "final_losses_mean": float(np.mean(losses)),
+    }
 
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="mlp64", choices=list(W.WORKLOADS))
+    ap.add_argument("--also", default="cifar16",
+                    help="comma-separated workloads also timed and reported under other_workloads ('' for none)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="only run a plain 1 GiB device copy (calibration run for the HBM byte counters)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on exactly one GPU (asked for {args.gpus}); the N-model step is a "
+              "single-GPU path and multi-GPU runs are not part of this build.", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_probe:
+        copy_probe()
+        return
+
+    wl = W.get(args.workload)
+    rec = measure(wl, args.steps, args.warmup)
     out = {
         "metric": "model-samples/sec (N x batch / step time) at 1 GPU",
-        "value": value,
+        "value": rec["value"],
         "unit": "model-samples/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_step,
+        "ms_per_step": rec["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": wl.precision,
+        "dtype": rec["dtype"],
         "data": "synthetic (seeded N(0,1) inputs, uniform labels; random-init weights)",
-        "config": {"workload": wl.name, "description": wl.description, "n_models": wl.n_models,
-                   "batch": wl.batch, "in_shape": list(wl.in_shape), "params": n_params,
-                   "parallelism": "none (one GPU, N models fused)"},
-        "mfma_util_step": total_flops / (ms_step / 1e3) / 1e12 / mfma_peak,
-        "train_gflop_per_step": total_flops / 1e9,
-        "roofline": roof,
-        "kernels": per_kernel,
-        "arena_bytes": arena,
-        "final_losses_mean": float(np.mean(losses)),
     }
+    out.update({k: rec[k] for k in ("config", "mfma_util_step", "train_gflop_per_step", "roofline", "kernels",
+                                    "arena_bytes", "final_losses_mean")})
+    others = {}
+    for name in [w for w in args.also.split(",") if w and w != wl.name]:
+        owl = W.get(name)
+        others[name] = measure(owl, max(5, args.steps // 5), max(2, args.warmup // 5))
+    if others:
+        out["other_workloads"] = others
     if not args.no_unfused:
-        ue, uarena = run_unfused(wl, max(3, args.steps // 5), 2)
         usteps = max(3, args.steps // 5)
+        ue, uarena = run_unfused(wl, usteps, 2)
         out["unfused_baseline"] = {
             "value": wl.n_models * wl.batch / (ue / usteps), "unit": "model-samples/s",
             "ms_per_round": ue / usteps * 1e3, "arena_bytes_sum": uarena,

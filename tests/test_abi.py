@@ -140,8 +140,30 @@ def test_workload_architectures():
 def test_bench_flop_count_by_hand():
     import bench
     wl = W.get("mlp2")
-    flops, n_params, _ = bench.algorithmic_work(wl)
+    flops, nbytes, n_params = bench.algorithmic_work(wl)
     fwd = 2 * 64 * (784 * 128 + 128 * 10 + 784 * 64 + 64 * 10)
     assert flops["gemm_fwd"] == fwd
     assert flops["gemm_bwd"] == fwd + 2 * 64 * (128 * 10 + 64 * 10)   # wgrad all, dgrad not for layer 1
     assert n_params == 101770 + 50890
+    # fp32: 4-byte tensors, update = read + write of the master (8 B per parameter)
+    B = 64
+    fwd_b = sum(B * 784 * 4 + h * 784 * 4 + h * 4 + B * h * 4 + B * h * 4 + 10 * h * 4 + 10 * 4 + B * 10 * 4
+                for h in (128, 64))
+    assert nbytes["gemm_fwd"] == fwd_b
+    bwd_b = sum((B * h * 4 + B * 784 * 4) + (B * 10 * 4 + B * h * 4) + 8 * (784 * h + h + 10 * h + 10)
+                + (B * 10 * 4 + 10 * h * 4 + B * h * 4) for h in (128, 64))
+    assert nbytes["gemm_bwd"] == bwd_b
+    assert nbytes["ce"] == 2 * (B * 10 * 4 + B * 10 * 4)
+
+
+def test_bench_conv_bytes_by_hand():
+    import bench
+    wl = W.Workload(name="t", n_models=1, description="", specs=[{"layers": [("conv", 8, 3, 1), ("relu",), ("pool",), ("flatten",),
+                                                                ("linear", 10)], "num_classes": 10}],
+                    batch=2, in_shape=(3, 6, 6), precision="bf16", steps=1, lr=0.01, seed=0)
+    flops, nbytes, _ = bench.algorithmic_work(wl)
+    assert flops["conv_fwd"] == 2 * 2 * 36 * 8 * 27 and flops["conv_dgrad"] == 0
+    pooled = 2 * 3 * 3 * 8
+    assert nbytes["conv_fwd"] == 2 * 36 * 3 * 2 + 8 * 27 * 2 + pooled * 3
+    assert nbytes["conv_wgrad"] == pooled * 3 + 2 * 36 * 3 * 2
+    assert nbytes["other"] == (8 * 27 + 8) * 10
