@@ -70,12 +70,22 @@ struct GemmProb {
 //          partial sums go to ws[split][o][j] and are reduced in split order.
 // dZ is never stored: it is gathered from the pooled gradient G[w][o] (which
 // already carries this block's ReLU' mask) and the window argmax.
+//
+// Halo tiling (fwd and dgrad, when the row-tile geometry fits, halo != 0): a
+// tile of BM rows is `imgs` whole images or `tr` whole rows of one image of
+// the pass's pixel space (fwd: conv output OHxOW; dgrad: conv input HxW). The
+// workgroup stages the operand rows that tile reads - `hr` rows x `hc`
+// columns per image, channels in blocks of `cb` (LDS stride `cs`) - once per
+// channel block in LDS, and reads every kernel tap from there; k runs over
+// (channel block, tap, channel in block). Weight columns keep the (tap, c)
+// order, so a k-block gathers its weight columns by tap.
 // ---------------------------------------------------------------------------
 struct ConvProb {
   int32_t Nb, C, H, W, O, KH, pad, OH, OW, PH, PW;
   int32_t pool, relu, prev_relu;
   int32_t M, N, K;            // GEMM sizes of this pass
   int32_t tiles_m, tiles_n, splits, kchunk;
+  int32_t halo, tr, imgs, hr, hc, cb, cs;  // halo tiling (see above)
   const void* X;              // conv input, NHWC, channel stride C
   const void* Wt;             // fwd: W [O][ldw]; dgrad: WT [C][ldw]
   int64_t ldw;
@@ -157,6 +167,10 @@ hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* ti
                              hipStream_t s);
 hipError_t launch_conv_wgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                              hipStream_t s);
+// Halo-tiled forward (dgrad = false) or data gradient (dgrad = true); every
+// problem of the launch has halo != 0.
+hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const int32_t* tile_map, int ntiles,
+                            hipStream_t s);
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
                          bool keep_grads, hipStream_t s);
 hipError_t launch_ce(bool bf16, const CeProb* probs, int nmodels, const int32_t* labels, int B,
@@ -180,5 +194,8 @@ constexpr int REDUCE_BLOCK = 256;
 constexpr int CE_MAX_BATCH = 1 << 20;
 constexpr int CE_ROWS = 32;           // sample rows per softmax-CE block
 constexpr int CE_LANES = 8;           // lanes per row
+// Halo tiles: LDS elements of the staged operand rows, and chunk-table entries.
+constexpr int HALO_ELEMS_BF16 = 20480, HALO_ELEMS_F32 = 8192;
+constexpr int HALO_QMAX = 256;
 
 }  // namespace un

@@ -870,29 +870,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
 // ---------------------------------------------------------------------------
 // Convolution passes
 // ---------------------------------------------------------------------------
+// Conv forward epilogue: bias, ReLU, 2x2 max-pool in registers (pool rows
+// are window-ordered, so a lane's four accumulator rows are one window), then
+// the pooled value, its argmax and the optional transposed copy.
 template <typename T, int BM, int BN, int BK>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_fwd_kernel(const ConvProb* __restrict__ probs,
-                                                       const int32_t* __restrict__ tile_map) {
+__device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int n0,
+                                                  const f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN]) {
   using TL = Tile<T, BM, BN, BK>;
-  __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
-  const int prob = tile_map[2 * blockIdx.x], local = tile_map[2 * blockIdx.x + 1];
-  if (prob < 0) return;  // padding of the XCD-ordered tile list
-  const ConvProb& p = probs[prob];
-  const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
-  const int m0 = tm * BM, n0 = tn * BN;
-
-  f32x4 acc[TL::FM][TL::FN];
-#pragma unroll
-  for (int i = 0; i < TL::FM; ++i)
-#pragma unroll
-    for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  Im2colLoader<T, BM, BK> la;
-  la.init(p, m0);
-  RowLoader<T, BN, BK> lb;
-  lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K);
-  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
-
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
   const int O = p.O;
@@ -945,29 +929,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   }
 }
 
+// Conv data-gradient epilogue: the previous block's ReLU' (its stored output
+// > 0) and the store of the gradient at that output.
 template <typename T, int BM, int BN, int BK>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_dgrad_kernel(const ConvProb* __restrict__ probs,
-                                                         const int32_t* __restrict__ tile_map) {
+__device__ __forceinline__ void conv_dgrad_epilogue(const ConvProb& p, int m0, int n0,
+                                                    const f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN]) {
   using TL = Tile<T, BM, BN, BK>;
-  __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
-  const int prob = tile_map[2 * blockIdx.x], local = tile_map[2 * blockIdx.x + 1];
-  if (prob < 0) return;  // padding of the XCD-ordered tile list
-  const ConvProb& p = probs[prob];
-  const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
-  const int m0 = tm * BM, n0 = tn * BN;
-
-  f32x4 acc[TL::FM][TL::FN];
-#pragma unroll
-  for (int i = 0; i < TL::FM; ++i)
-#pragma unroll
-    for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  DzGatherLoader<T, BM, BK> la;
-  la.init(p, m0);
-  RowLoader<T, BN, BK> lb;
-  lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K);
-  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
-
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
   const int C = p.C;
@@ -991,6 +958,281 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
       }
     }
   }
+}
+
+template <typename T, int BM, int BN, int BK>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_fwd_kernel(const ConvProb* __restrict__ probs,
+                                                       const int32_t* __restrict__ tile_map) {
+  using TL = Tile<T, BM, BN, BK>;
+  __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
+  const int prob = tile_map[2 * blockIdx.x], local = tile_map[2 * blockIdx.x + 1];
+  if (prob < 0) return;  // padding of the XCD-ordered tile list
+  const ConvProb& p = probs[prob];
+  const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  f32x4 acc[TL::FM][TL::FN];
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  Im2colLoader<T, BM, BK> la;
+  la.init(p, m0);
+  RowLoader<T, BN, BK> lb;
+  lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K);
+  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
+
+  conv_fwd_epilogue<T, BM, BN, BK>(p, m0, n0, acc);
+}
+
+template <typename T, int BM, int BN, int BK>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_dgrad_kernel(const ConvProb* __restrict__ probs,
+                                                         const int32_t* __restrict__ tile_map) {
+  using TL = Tile<T, BM, BN, BK>;
+  __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
+  const int prob = tile_map[2 * blockIdx.x], local = tile_map[2 * blockIdx.x + 1];
+  if (prob < 0) return;  // padding of the XCD-ordered tile list
+  const ConvProb& p = probs[prob];
+  const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  f32x4 acc[TL::FM][TL::FN];
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  DzGatherLoader<T, BM, BK> la;
+  la.init(p, m0);
+  RowLoader<T, BN, BK> lb;
+  lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K);
+  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
+
+  conv_dgrad_epilogue<T, BM, BN, BK>(p, m0, n0, acc);
+}
+
+// ---------------------------------------------------------------------------
+// Halo-tiled implicit-GEMM convolution: forward and data gradient
+// ---------------------------------------------------------------------------
+// Weight operand of a halo k-block: rows n (output channels in the forward
+// pass, input channels in the data gradient); chunk c of the k-block is chunk
+// q = kb*CPB + c of the channel block, whose weight column comes from the
+// chunk table. Every thread owns the same chunk c = tid % CPB in all its rows.
+template <typename T, int ROWS, int BK>
+struct TapRowLoader {
+  static constexpr int VEC = TT<T>::VEC, CPB = BK / VEC, NV = ROWS * CPB / 256, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
+  static_assert(ROWS * CPB % 256 == 0 && 256 % CPB == 0, "tile too small for 256 threads");
+  __amdgpu_buffer_rsrc_t rsrc;
+  int rowoff[NV];
+  u32x4 r[NV];
+  __device__ void init(const T* base, int64_t ld, int rows_valid) {
+    rsrc = make_rsrc(base, (int64_t)rows_valid * ld * (int64_t)sizeof(T));
+#pragma unroll
+    for (int s = 0; s < NV; ++s) rowoff[s] = (int)((int64_t)((threadIdx.x + 256 * s) / CPB) * ld * (int64_t)sizeof(T));
+  }
+  // col: weight column of this thread's chunk, or -1 for a chunk past the block's end
+  __device__ void load(int col) {
+#pragma unroll
+    for (int s = 0; s < NV; ++s)
+      r[s] = col < 0 ? zero4()
+                     : __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, rowoff[s] + col * (int)sizeof(T), 0, 0));
+  }
+  __device__ void store(T* sm) const {
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int v = threadIdx.x + 256 * s;
+      *(u32x4*)(sm + (v / CPB) * LDK + (v % CPB) * VEC) = r[s];
+    }
+  }
+};
+
+// Stage channels [c0, c0 + cbw) of the operand rows a halo tile reads into
+// LDS, [img][hr][hc][cs]; positions outside the image (padding), past the
+// batch, or - data gradient - not receiving the window's gradient are zero.
+// Forward: the conv input X. Data gradient: dZ, expanded from the pooled
+// gradient G and the window argmax.
+template <typename T, bool DGRAD>
+__device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, int y0, int c0, int cbw) {
+  constexpr int VEC = TT<T>::VEC, UNR = 4;
+  const int cpp = cbw / VEC, plane = p.hr * p.hc;
+  const int total = p.imgs * plane * cpp;
+  const int CH = DGRAD ? p.O : p.C;
+  const T* src = (const T*)(DGRAD ? p.G : p.X);
+  for (int e0 = threadIdx.x; e0 < total; e0 += 256 * UNR) {
+    u32x4 v[UNR];
+    int dst[UNR];
+#pragma unroll
+    for (int k = 0; k < UNR; ++k) {
+      const int e = e0 + 256 * k;
+      v[k] = zero4();
+      dst[k] = -1;
+      if (e < total) {
+        const int pos = e / cpp, ch = (e - pos * cpp) * VEC;
+        const int img = pos / plane, rem = pos - img * plane, hrow = rem / p.hc, hcol = rem - hrow * p.hc;
+        const int n = img0 + img;
+        dst[k] = pos * p.cs + ch;
+        if (n < p.Nb) {
+          if (!DGRAD) {
+            const int y = y0 - p.pad + hrow, x = hcol - p.pad;
+            if (y >= 0 && y < p.H && x >= 0 && x < p.W)
+              v[k] = *(gptr<const u32x4>)(src + ((int64_t)(n * p.H + y) * p.W + x) * CH + c0 + ch);
+          } else {
+            int64_t idx;
+            int d;
+            if (dz_index(p, n, y0 + p.pad - (p.KH - 1) + hrow, p.pad - (p.KH - 1) + hcol, idx, d)) {
+              v[k] = *(gptr<const u32x4>)(src + idx + c0 + ch);
+              if (d >= 0) select_am<T>(v[k], load_am<T>(p.gam + idx + c0 + ch), d);
+            }
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < UNR; ++k)
+      if (dst[k] >= 0) *(u32x4*)(sH + dst[k]) = v[k];
+  }
+}
+
+// One k-block of a halo tile: A rows read from the staged halo at the lane's
+// row base plus the chunk's tap offset, B from the weight stage. Chunks at or
+// past nq have zero weights; their A reads are clamped to a valid chunk.
+template <typename T, int BM, int BN, int BK>
+__device__ __forceinline__ void mma_halo(const T* sH, const int (&hbase)[Tile<T, BM, BN, BK>::FM], const int* qa,
+                                         int q0, int nq, const T* sB,
+                                         f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN]) {
+  using TL = Tile<T, BM, BN, BK>;
+  constexpr int VEC = TT<T>::VEC;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wn = (wave & 1) * TL::WN;
+  const int lr = lane & 15, lg = lane >> 4;
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 32) {
+      const int qs = q0 + kk / VEC;
+      if (qs < nq) {
+        const int ao = qa[min(qs + lg, nq - 1)];
+        bf16x8 a[TL::FM], b[TL::FN];
+#pragma unroll
+        for (int i = 0; i < TL::FM; ++i) a[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(sH + hbase[i] + ao));
+#pragma unroll
+        for (int j = 0; j < TL::FN; ++j)
+          b[j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(sB + (wn + 16 * j + lr) * TL::LDK + kk + 8 * lg));
+#pragma unroll
+        for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+          for (int j = 0; j < TL::FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 16) {
+      const int qs = q0 + kk / VEC;
+      if (qs < nq) {
+        const int ao = qa[min(qs + lg, nq - 1)];
+        f32x4 a[TL::FM], b[TL::FN];
+#pragma unroll
+        for (int i = 0; i < TL::FM; ++i) a[i] = *(const f32x4*)(sH + hbase[i] + ao);
+#pragma unroll
+        for (int j = 0; j < TL::FN; ++j) b[j] = *(const f32x4*)(sB + (wn + 16 * j + lr) * TL::LDK + kk + 4 * lg);
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+            for (int j = 0; j < TL::FN; ++j)
+              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
+      }
+    }
+  }
+}
+
+template <typename T, int BM, int BN, int BK, bool DGRAD>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_halo_kernel(const ConvProb* __restrict__ probs,
+                                                        const int32_t* __restrict__ tile_map) {
+  using TL = Tile<T, BM, BN, BK>;
+  constexpr int VEC = TT<T>::VEC, CPB = BK / VEC;
+  constexpr int HALO = sizeof(T) == 2 ? HALO_ELEMS_BF16 : HALO_ELEMS_F32;
+  __shared__ __attribute__((aligned(16))) T sB[2 * TL::B_ELEMS];
+  __shared__ __attribute__((aligned(16))) T sH[HALO];
+  __shared__ int qa[HALO_QMAX], qb[HALO_QMAX];
+  const int prob = tile_map[2 * blockIdx.x], local = tile_map[2 * blockIdx.x + 1];
+  if (prob < 0) return;  // padding of the XCD-ordered tile list
+  const ConvProb& p = probs[prob];
+  const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int SH = DGRAD ? p.H : p.OH, SW = DGRAD ? p.W : p.OW;
+  int img0, y0;
+  if (p.imgs > 1) {
+    img0 = tm * p.imgs;
+    y0 = 0;
+  } else {
+    const int tpi = SH / p.tr;
+    img0 = tm / tpi;
+    y0 = (tm - img0 * tpi) * p.tr;
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = (wave >> 1) * TL::WM;
+  // halo offset of the first tap of each of this lane's MFMA rows
+  int hbase[TL::FM];
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i) {
+    const int r = wm + 16 * i + (lane & 15);
+    int img, y, x;
+    if (!DGRAD && p.pool) {  // window order: r = 4 * window + (dy, dx)
+      const int lw = r >> 2, d = r & 3, wpr = SW >> 1, wpi = (p.tr >> 1) * wpr;
+      img = lw / wpi;
+      const int rem = lw - img * wpi, wy = rem / wpr;
+      y = 2 * wy + (d >> 1);
+      x = 2 * (rem - wy * wpr) + (d & 1);
+    } else {
+      const int ppi = p.tr * SW;
+      img = r / ppi;
+      const int rem = r - img * ppi;
+      y = rem / SW;
+      x = rem - y * SW;
+    }
+    hbase[i] = ((img * p.hr + y) * p.hc + x) * p.cs;
+  }
+
+  f32x4 acc[TL::FM][TL::FN];
+#pragma unroll
+  for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+    for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  TapRowLoader<T, BN, BK> lb;
+  lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0);
+  const int KH = p.KH, Cin = DGRAD ? p.O : p.C, cq = threadIdx.x % CPB;
+  for (int c0 = 0; c0 < Cin; c0 += p.cb) {
+    const int cbw = min(p.cb, Cin - c0), cpt = cbw / VEC, nq = KH * KH * cpt;
+    __syncthreads();  // the previous channel block's halo and tables are no longer read
+    for (int q = threadIdx.x; q < nq; q += 256) {
+      const int tap = q / cpt, ch = (q - tap * cpt) * VEC, u = tap / KH, v = tap - u * KH;
+      qa[q] = (DGRAD ? (KH - 1 - u) * p.hc + (KH - 1 - v) : u * p.hc + v) * p.cs + ch;
+      qb[q] = tap * Cin + c0 + ch;  // fwd: W[o][(tap, c)]; dgrad: WT[c][(tap, o)]
+    }
+    stage_halo<T, DGRAD>(p, sH, img0, y0, c0, cbw);
+    __syncthreads();
+    const int nkb = (nq + CPB - 1) / CPB;
+    lb.load(cq < nq ? qb[cq] : -1);
+    lb.store(sB);
+    __syncthreads();
+    for (int kb = 0; kb < nkb; ++kb) {
+      const int cur = kb & 1;
+      const bool more = kb + 1 < nkb;
+      if (more) {
+        const int q = (kb + 1) * CPB + cq;
+        lb.load(q < nq ? qb[q] : -1);
+      }
+      mma_halo<T, BM, BN, BK>(sH, hbase, qa, kb * CPB, nq, sB + cur * TL::B_ELEMS, acc);
+      if (more) lb.store(sB + (cur ^ 1) * TL::B_ELEMS);
+      __syncthreads();
+    }
+  }
+  if constexpr (DGRAD) conv_dgrad_epilogue<T, BM, BN, BK>(p, m0, n0, acc);
+  else conv_fwd_epilogue<T, BM, BN, BK>(p, m0, n0, acc);
 }
 
 template <typename T, int BM, int BN, int BK>
@@ -1240,6 +1482,27 @@ hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* ti
   else
     hipLaunchKernelGGL((conv_dgrad_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32>), dim3(ntiles), dim3(256),
                        0, s, probs, tile_map);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const int32_t* tile_map, int ntiles,
+                            hipStream_t s) {
+  if (ntiles <= 0) return hipSuccess;
+  if (bf16) {
+    if (dgrad)
+      hipLaunchKernelGGL((conv_halo_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, true>), dim3(ntiles),
+                         dim3(256), 0, s, probs, tile_map);
+    else
+      hipLaunchKernelGGL((conv_halo_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, false>), dim3(ntiles),
+                         dim3(256), 0, s, probs, tile_map);
+  } else {
+    if (dgrad)
+      hipLaunchKernelGGL((conv_halo_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, true>), dim3(ntiles),
+                         dim3(256), 0, s, probs, tile_map);
+    else
+      hipLaunchKernelGGL((conv_halo_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, false>), dim3(ntiles),
+                         dim3(256), 0, s, probs, tile_map);
+  }
   return hipGetLastError();
 }
 

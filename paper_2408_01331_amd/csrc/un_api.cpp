@@ -72,7 +72,7 @@ struct Model {
 };
 
 struct Launch {
-  int kind;   // 0 gemm, 1 conv fwd, 2 conv dgrad, 3 conv wgrad, 4 reduce, 5 ce, 6 sgd
+  int kind;   // 0 gemm, 1 conv fwd, 2 conv dgrad, 3 conv wgrad, 4 reduce, 5 ce, 6 sgd, 7/8 halo conv fwd/dgrad
   int kclass;
   size_t probs, map;  // arena offsets
   int count;
@@ -349,6 +349,43 @@ static std::vector<int32_t> xcd_order(std::vector<TileGroup> groups) {
   return map;
 }
 
+// Halo tiling of a conv forward / data-gradient pass (see ConvProb): a tile
+// of BM rows must be whole rows of one image or whole images of the pass's
+// pixel space, a pooled forward tile must hold whole windows with nothing
+// dropped by floor pooling, the operand channels must be whole 16-byte
+// vectors, and the staged rows must fit the LDS budget. Otherwise halo = 0
+// and the pass gathers its operand per k-block.
+static void plan_halo(ConvProb& p, bool bf, bool dgrad) {
+  const int BM = bf ? CONV_BM_BF16 : CONV_BM_F32, BK = bf ? CONV_BK_BF16 : CONV_BK_F32, VEC = bf ? 8 : 4;
+  const int SH = dgrad ? p.H : p.OH, SW = dgrad ? p.W : p.OW, Cin = dgrad ? p.O : p.C;
+  p.halo = 0;
+  if (Cin % VEC != 0) return;
+  int tr, imgs;
+  if (SH * SW >= BM) {
+    if (BM % SW != 0) return;
+    tr = BM / SW;
+    if (SH % tr != 0) return;
+    imgs = 1;
+  } else {
+    if (BM % (SH * SW) != 0) return;
+    tr = SH;
+    imgs = BM / (SH * SW);
+  }
+  if (!dgrad && p.pool && (tr % 2 != 0 || SW % 2 != 0 || SH % 2 != 0)) return;
+  const int cb = std::min(Cin, BK);
+  const int cs = cb + ((cb / VEC) % 2 == 0 ? VEC : 0);  // odd number of 16-byte chunks per position
+  const int hr = tr + p.KH - 1, hc = SW + p.KH - 1;
+  if ((int64_t)imgs * hr * hc * cs > (bf ? HALO_ELEMS_BF16 : HALO_ELEMS_F32)) return;
+  if (p.KH * p.KH * (cb / VEC) > HALO_QMAX) return;
+  p.halo = 1;
+  p.tr = tr;
+  p.imgs = imgs;
+  p.hr = hr;
+  p.hc = hc;
+  p.cb = cb;
+  p.cs = cs;
+}
+
 // ==========================================================================
 // Planner
 // ==========================================================================
@@ -567,7 +604,7 @@ static un_status plan_and_alloc(un_ctx* c) {
     size_t mo = put(map.data(), map.size() * 4);
     out.push_back(Launch{0, kclass, po, mo, (int)(map.size() / 2)});
   };
-  auto emit_conv = [&](std::vector<ConvProb>& ps, std::vector<Launch>& out, int kind, int kclass) {
+  auto emit_conv_one = [&](std::vector<ConvProb>& ps, std::vector<Launch>& out, int kind, int kclass) {
     if (ps.empty()) return;
     std::stable_sort(ps.begin(), ps.end(),
                      [](const ConvProb& x, const ConvProb& y) { return (int64_t)x.K * x.splits > (int64_t)y.K * y.splits; });
@@ -606,6 +643,16 @@ static un_status plan_and_alloc(un_ctx* c) {
     }
     size_t mo = put(map.data(), map.size() * 4);
     out.push_back(Launch{kind, kclass, po, mo, (int)(map.size() / 2)});
+  };
+  auto emit_conv = [&](std::vector<ConvProb>& all, std::vector<Launch>& out, int kind, int kclass) {
+    if (kind == 1 || kind == 2) {  // forward / data gradient: halo-tiled problems get their own launch
+      std::vector<ConvProb> halo, plain;
+      for (auto& p : all) (p.halo ? halo : plain).push_back(p);
+      emit_conv_one(halo, out, kind == 1 ? 7 : 8, kclass);
+      emit_conv_one(plain, out, kind, kclass);
+    } else {
+      emit_conv_one(all, out, kind, kclass);
+    }
   };
 
   auto conv_base = [&](const Block& b) {
@@ -687,6 +734,7 @@ static un_status plan_and_alloc(un_ctx* c) {
         p.amax = (uint8_t*)ptr(b.amax);
         p.PT = ptr(b.YT);
         p.ldpt = b.ldyt;
+        plan_halo(p, bf, false);
         cp.push_back(p);
       }
     }
@@ -813,6 +861,7 @@ static un_status plan_and_alloc(un_ctx* c) {
           p.G = ptr(b.G);
           p.gam = (const uint8_t*)ptr(b.amax);
           p.Gprev = ptr(pb.G);
+          plan_halo(p, bf, true);
           dp.push_back(p);
         }
         ConvProb p = conv_base(b);
@@ -1103,6 +1152,10 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
       break;
     case 3:
       e = launch_conv_wgrad(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
+      break;
+    case 7:
+    case 8:
+      e = launch_conv_halo(c->bf16, l.kind == 8, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
       break;
     case 4:
       e = launch_reduce(c->bf16, c->at<ReduceProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->keep_grads,

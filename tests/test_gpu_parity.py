@@ -102,6 +102,27 @@ def test_ragged_cnns(precision):
     _report(f"ragged_cnns_{precision} run", compare_run(wl, run_gpu(wl, wl.steps), run_oracle(wl, wl.steps, m), m))
 
 
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
+def test_halo_tiled_cnns(precision):
+    # Shapes the row-tiled (halo) conv kernels take: whole image rows or whole
+    # images per tile, 3x3 and 5x5 kernels, pooled and unpooled outputs, more
+    # operand channels than one channel block (72), and a batch of 6 that
+    # leaves the last multi-image tile partly empty.
+    _need_gpu()
+    specs = [
+        {"layers": [("conv", 16, 3, 1), ("relu",), ("pool",), ("conv", 72, 3, 1), ("relu",), ("pool",),
+                    ("flatten",), ("linear", 10)], "num_classes": 10},
+        {"layers": [("conv", 24, 5, 2), ("relu",), ("pool",), ("conv", 16, 3, 1), ("relu",),
+                    ("flatten",), ("linear", 10)], "num_classes": 10},
+        {"layers": [("conv", 8, 3, 1), ("relu",), ("conv", 16, 3, 1), ("relu",), ("pool",),
+                    ("flatten",), ("linear", 10)], "num_classes": 10},
+    ]
+    wl = _custom(specs, 6, (8, 16, 16), precision, steps=3)
+    m = range(wl.n_models)
+    _report(f"halo_cnns_{precision} 1 step", compare_step(wl, run_gpu(wl, 1), run_oracle(wl, 1, m), m))
+    _report(f"halo_cnns_{precision} run", compare_run(wl, run_gpu(wl, wl.steps), run_oracle(wl, wl.steps, m), m))
+
+
 # ---------------------------------------------------------------------------
 # The paper's invariants on the device: no interference, merged == alone
 # ---------------------------------------------------------------------------
