@@ -165,7 +165,8 @@ hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile
                            hipStream_t s);
 hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                              hipStream_t s);
-hipError_t launch_conv_wgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
+// mode: 0 any layer; 1 pooled, 2 unpooled, both with O and C whole 16-byte vectors
+hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                              hipStream_t s);
 // Halo-tiled forward (dgrad = false) or data gradient (dgrad = true); every
 // problem of the launch has halo != 0.

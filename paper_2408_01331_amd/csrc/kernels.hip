@@ -182,6 +182,27 @@ __device__ __forceinline__ void mma_loop(LA& la, LB& lb, int kb0, int kb1, T* sm
   }
 }
 
+// mma_loop for one loader `ld` that fills a whole stage (both operands).
+template <typename T, int BM, int BN, int BK, class L>
+__device__ __forceinline__ void mma_loop1(L& ld, int kb0, int kb1, T* smem,
+                                          f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN]) {
+  using TL = Tile<T, BM, BN, BK>;
+  constexpr int STAGE = TL::A_ELEMS + TL::B_ELEMS;
+  if (kb0 >= kb1) return;
+  ld.template load<0>(kb0);
+  ld.template store<0>(smem);
+  __syncthreads();
+  for (int kb = kb0; kb < kb1; ++kb) {
+    const int cur = (kb - kb0) & 1;
+    const bool more = kb + 1 < kb1;
+    if (more) ld.template load<0>(kb + 1);
+    const T* st = smem + cur * STAGE;
+    mma_block<T, BM, BN, BK>(st, st + TL::A_ELEMS, acc);
+    if (more) ld.template store<0>(smem + (cur ^ 1) * STAGE);
+    __syncthreads();
+  }
+}
+
 // LDS of one MFMA kernel: the double-buffered operand tiles, reused by the
 // epilogue as an fp32 [BM][BN + 4] tile.
 template <typename T, int BM, int BN, int BK>
@@ -222,7 +243,7 @@ struct RowLoader {
   int off[NV];
   int K;
   u32x4 r[2][NV];
-  __device__ void init(const T* base, int64_t ld, int rows_valid, int K_) {
+  __device__ __forceinline__ void init(const T* base, int64_t ld, int rows_valid, int K_) {
     K = K_;
     rsrc = make_rsrc(base, (int64_t)rows_valid * ld * (int64_t)sizeof(T));
 #pragma unroll
@@ -232,7 +253,7 @@ struct RowLoader {
     }
   }
   template <int S>
-  __device__ void load(int kb) {
+  __device__ __forceinline__ void load(int kb) {
     const int kbytes = kb * BK * (int)sizeof(T);
 #pragma unroll
     for (int s = 0; s < NV; ++s)
@@ -246,7 +267,7 @@ struct RowLoader {
     }
   }
   template <int S>
-  __device__ void store(T* sm) const {
+  __device__ __forceinline__ void store(T* sm) const {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + 256 * s;
@@ -280,7 +301,7 @@ struct Im2colLoader {
   const T* X;
   int rn[NV], ry[NV], rx[NV];
   u32x4 r[2][NV];
-  __device__ void init(const ConvProb& pr, int m0) {
+  __device__ __forceinline__ void init(const ConvProb& pr, int m0) {
     p = &pr;
     X = (const T*)pr.X;
 #pragma unroll
@@ -294,7 +315,7 @@ struct Im2colLoader {
     }
   }
   template <int S>
-  __device__ void load(int kb) {
+  __device__ __forceinline__ void load(int kb) {
     const int C = p->C, H = p->H, W = p->W, KW = p->KH, pad = p->pad, K = p->K;
     const bool vec = (C % VEC) == 0;
 #pragma unroll
@@ -325,7 +346,7 @@ struct Im2colLoader {
     }
   }
   template <int S>
-  __device__ void store(T* sm) const {
+  __device__ __forceinline__ void store(T* sm) const {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + 256 * s;
@@ -355,6 +376,16 @@ template <typename T> __device__ __forceinline__ uint64_t load_am(const uint8_t*
 template <> __device__ __forceinline__ uint64_t load_am<float>(const uint8_t* a) { return *(const uint32_t*)a; }
 template <> __device__ __forceinline__ uint64_t load_am<bf16_t>(const uint8_t* a) { return *(const uint64_t*)a; }
 
+// VEC argmax bytes at byte offset off of a buffer resource.
+template <typename T> __device__ __forceinline__ uint64_t load_am_buf(__amdgpu_buffer_rsrc_t r, int off);
+template <> __device__ __forceinline__ uint64_t load_am_buf<float>(__amdgpu_buffer_rsrc_t r, int off) {
+  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+template <> __device__ __forceinline__ uint64_t load_am_buf<bf16_t>(__amdgpu_buffer_rsrc_t r, int off) {
+  const u32x2 v = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0));
+  return (uint64_t)v[0] | ((uint64_t)v[1] << 32);
+}
+
 // Keep element e of v only where its window argmax equals d.
 template <typename T> __device__ __forceinline__ void select_am(u32x4& v, uint64_t am, int d) {
 #pragma unroll
@@ -370,7 +401,7 @@ struct DzGatherLoader {
   const T* G;
   int rn[NV], ry[NV], rx[NV];
   u32x4 r[2][NV];
-  __device__ void init(const ConvProb& pr, int m0) {
+  __device__ __forceinline__ void init(const ConvProb& pr, int m0) {
     p = &pr;
     G = (const T*)pr.G;
     const int hw = pr.H * pr.W;
@@ -385,7 +416,7 @@ struct DzGatherLoader {
     }
   }
   template <int S>
-  __device__ void load(int kb) {
+  __device__ __forceinline__ void load(int kb) {
     const int O = p->O, KW = p->KH, pad = p->pad, K = p->K;
     const bool vec = (O % VEC) == 0;
 #pragma unroll
@@ -419,7 +450,7 @@ struct DzGatherLoader {
     }
   }
   template <int S>
-  __device__ void store(T* sm) const {
+  __device__ __forceinline__ void store(T* sm) const {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + 256 * s;
@@ -465,200 +496,200 @@ __device__ __forceinline__ void microtile_of(int t, int& rg, int& pg) {
   rg = ((t >> 3) & 1) | ((t >> 4) << 1);
 }
 
-// A: rows = output channel o, k = output pixel. dZ gathered from the pooled
-// gradient G[w][o] (already ReLU'-masked) and the window argmax.
-template <typename T, int ROWS, int BK>
-struct DzRowsLoader {
-  static constexpr int VEC = TT<T>::VEC, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
-  static_assert(ROWS / VEC == 16 && BK / VEC == 8, "16 x 8 micro-tiles per operand");
+// Weight-gradient operands of one k-block (BK output pixels), both written to
+// LDS as [row][pixel]: threads 0..127 build A, rows = output channel o, from
+// dZ (the pooled gradient G[w][o], already ReLU'-masked, and the window
+// argmax); threads 128..255 build B, rows = j = (u, v, c) plus the bias column
+// j == KH*KW*C reading 1, from the input patch in NHWC X. load() only issues
+// the global loads into a register slot; the argmax selection, the transpose
+// and the LDS writes happen in store(), after the current k-block's products,
+// so the loads overlap them. Both roles share the register slots.
+// MODE selects the code compiled into the k-loop (a loop body holding every
+// path overflows the instruction cache): WG_POOLED / WG_PLAIN for a pooled /
+// unpooled block whose channel counts O and C are whole 16-byte vectors,
+// WG_GENERIC for anything else (element by element where needed).
+enum { WG_GENERIC = 0, WG_POOLED = 1, WG_PLAIN = 2 };
+
+template <typename T, int BM, int BN, int BK, int MODE>
+struct WgradLoader {
+  static constexpr int VEC = TT<T>::VEC, NW = VEC / 4, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
+  static constexpr int OOB = 0x7ffffff0;  // a buffer offset past every range: the load returns zero
+  static constexpr bool POOL = MODE == WG_POOLED;
+  static_assert(BM / VEC == 16 && BN / VEC == 16 && BK / VEC == 8, "16 x 8 micro-tiles per operand");
+  static_assert(VEC % 4 == 0, "a micro-tile holds whole 2x2 windows");
   const ConvProb* p;
-  const T* G;
-  int o0, rg, pg;
-  bool active;
-  u32x4 r[2][VEC];
-  __device__ void init(const ConvProb& pr, int m0) {
+  bool isA;
+  int r0, rg, pg;          // first row (o or j) of this thread's micro-tile
+  u32x4 raw[2][VEC];       // A pooled: raw[S][0..NW) = window gradients; else the pixel vectors
+  uint64_t am[2][NW];      // A pooled: window argmaxes
+  __device__ __forceinline__ void init(const ConvProb& pr, int m0, int n0) {
     p = &pr;
-    G = (const T*)pr.G;
-    active = threadIdx.x < 128;
+    isA = __builtin_amdgcn_readfirstlane(threadIdx.x) < 128;  // waves 0-1: A, waves 2-3: B (wave-uniform)
     microtile_of(threadIdx.x % 128, rg, pg);
-    o0 = m0 + rg * VEC;
+    r0 = (isA ? m0 : n0) + rg * VEC;
+  }
+  __device__ __forceinline__ int64_t out_rows() const {
+    return p->pool ? (int64_t)p->Nb * p->PH * p->PW : (int64_t)p->Nb * p->OH * p->OW;
   }
   template <int S>
-  __device__ void load(int kb) {
-    if (!active) return;
-    const int O = p->O;
-    if (o0 >= O) {  // rows past the last output channel
-#pragma unroll
-      for (int c = 0; c < VEC; ++c) r[S][c] = zero4();
-      return;
+  __device__ __forceinline__ void load(int kb) {
+    if constexpr (MODE == WG_GENERIC) {
+      if (isA) loadA_generic<S>(kb);
+      else loadB_generic<S>(kb);
+    } else {
+      if (isA) loadA_fast<S>(kb);
+      else loadB_fast<S>(kb);
     }
+  }
+  // A, whole-vector channels: a micro-tile is entirely below O or entirely past it
+  template <int S>
+  __device__ __forceinline__ void loadA_fast(int kb) {
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(p->G, out_rows() * p->O * (int64_t)sizeof(T));
+    const int O = p->O, o0 = r0, K = p->K;
+    const bool rows_in = o0 < O;
     const int pix0 = kb * BK + pg * VEC;
-    u32x4 pixv[VEC];
-    if (o0 + VEC <= O && (O % VEC) == 0) {
-      if (p->pool) {
-        // VEC consecutive pixels cover VEC/4 windows; each window's gradient
-        // lands on its argmax pixel only
+    if constexpr (POOL) {
+      const __amdgpu_buffer_rsrc_t rs_am = make_rsrc(p->gam, out_rows() * p->O);
+      // VEC consecutive pixels are NW whole windows; past the last pixel or
+      // channel: zero gradient and an argmax no d matches
 #pragma unroll
-        for (int wq = 0; wq < VEC / 4; ++wq) {
-          const int pix = pix0 + 4 * wq;
-          u32x4 g = zero4();
-          uint64_t am = 0;
-          if (pix < p->K) {
-            const int64_t idx = (int64_t)(pix >> 2) * O + o0;
-            g = *(gptr<const u32x4>)(G + idx);
-            am = load_am<T>(p->gam + idx);
-          }
-#pragma unroll
-          for (int d = 0; d < 4; ++d) {
-            u32x4 v = g;
-            select_am<T>(v, am, d);
-            pixv[4 * wq + d] = v;
-          }
-        }
-      } else {
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) {
-          const int pix = pix0 + e;
-          pixv[e] = pix < p->K ? *(gptr<const u32x4>)(G + (int64_t)pix * O + o0) : zero4();
-        }
+      for (int wq = 0; wq < NW; ++wq) {
+        const int pix = pix0 + 4 * wq, idx = (pix >> 2) * O + o0;
+        const bool in = rows_in && pix < K;
+        raw[S][wq] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? idx * (int)sizeof(T) : OOB, 0, 0));
+        am[S][wq] = in ? load_am_buf<T>(rs_am, idx) : ~0ull;
       }
     } else {
-      // output channels not a whole number of vectors: element by element
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
         const int pix = pix0 + e;
-        u32x4 v = zero4();
-        if (pix < p->K) {
-          const int64_t idx = (int64_t)(p->pool ? (pix >> 2) : pix) * O;
-          const int d = p->pool ? (pix & 3) : -1;
-#pragma unroll 1
-          for (int c = 0; c < VEC; ++c)
-            if (o0 + c < O && (d < 0 || p->gam[idx + o0 + c] == d)) vset_bits<T>(v, c, bits_of<T>(G[idx + o0 + c]));
-        }
-        pixv[e] = v;
+        raw[S][e] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, rows_in && pix < K ? (pix * O + o0) * (int)sizeof(T) : OOB, 0, 0));
       }
     }
-    transpose_block<T>(pixv, r[S]);
   }
+  // B, whole-vector channels: a micro-tile's VEC columns are one tap's
+  // channels, or the bias chunk (1, 0, ..., 0), or past the bias column
   template <int S>
-  __device__ void store(T* sm) const {
-    if (!active) return;
-    const int ol = rg * VEC;
-#pragma unroll
-    for (int c = 0; c < VEC; ++c) *(u32x4*)(sm + (ol + c) * LDK + pg * VEC) = r[S][c];
-  }
-};
-
-// B: rows = j = (u, v, c) (+ the bias column j == KH*KW*C reading 1), k =
-// output pixel: the input patch, gathered from NHWC X.
-template <typename T, int ROWS, int BK>
-struct PatchRowsLoader {
-  static constexpr int VEC = TT<T>::VEC, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
-  static_assert(ROWS / VEC == 16 && BK / VEC == 8, "16 x 8 micro-tiles per operand");
-  const ConvProb* p;
-  const T* X;
-  int j0, rg, pg;
-  bool active;
-  u32x4 r[2][VEC];
-  __device__ void init(const ConvProb& pr, int n0) {
-    p = &pr;
-    X = (const T*)pr.X;
-    active = threadIdx.x >= 128;
-    microtile_of(threadIdx.x % 128, rg, pg);
-    j0 = n0 + rg * VEC;
-  }
-  template <int S>
-  __device__ void load(int kb) {
-    if (!active) return;
-    const int C = p->C, H = p->H, W = p->W, KW = p->KH, pad = p->pad, J = p->KH * p->KH * C;
-    if (j0 > J) {  // rows past the bias column
-#pragma unroll
-      for (int c = 0; c < VEC; ++c) r[S][c] = zero4();
-      return;
-    }
+  __device__ __forceinline__ void loadB_fast(int kb) {
+    const __amdgpu_buffer_rsrc_t rs = make_rsrc(p->X, (int64_t)p->Nb * p->H * p->W * p->C * (int64_t)sizeof(T));
+    const int C = p->C, H = p->H, W = p->W, KW = p->KH, pad = p->pad, J = p->KH * p->KH * C, j0 = r0;
+    const bool bias_chunk = j0 == J, rows_in = j0 < J;
+    const int t = j0 / C, c0 = j0 - t * C, u = t / KW, vv = t - u * KW;
     const int pix0 = kb * BK + pg * VEC;
-    u32x4 pixv[VEC];
-    // vector path: whole-vector channels; the chunk at j0 == J is then the
-    // bias column (1, 0, ..., 0)
-    const bool vec = (C % VEC) == 0;
-    const bool bias_chunk = j0 == J;
-    int t = 0, c0 = 0, u = 0, vv = 0;
-    if (vec) {
-      t = j0 / C;
-      c0 = j0 - t * C;
-      u = t / KW;
-      vv = t - u * KW;
-    }
-    // pixel coordinates: with pooling, VEC consecutive pixels are VEC/4 whole
-    // windows (one decode each); without, decode the first and step along x
-    int wn[VEC / 4 > 0 ? VEC / 4 : 1], wy[VEC / 4 > 0 ? VEC / 4 : 1], wx[VEC / 4 > 0 ? VEC / 4 : 1];
-    int rn = 0, ry = 0, rx = 0;
-    if (p->pool) {
+    if constexpr (POOL) {
+      // VEC consecutive pixels are NW whole windows (one decode each)
 #pragma unroll
-      for (int wq = 0; wq < VEC / 4; ++wq) {
+      for (int wq = 0; wq < NW; ++wq) {
         const int w = (pix0 >> 2) + wq, pp = p->PH * p->PW;
-        wn[wq] = w / pp;
-        const int rem = w - wn[wq] * pp, ph = rem / p->PW;
-        wy[wq] = 2 * ph;
-        wx[wq] = 2 * (rem - ph * p->PW);
+        const int n = w / pp, rem = w - n * pp, ph = rem / p->PW;
+        const int y0 = 2 * ph, x0 = 2 * (rem - ph * p->PW);
+        const bool pin = pix0 + 4 * wq < p->K;
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const int iy = y0 + (d >> 1) + u - pad, ix = x0 + (d & 1) + vv - pad;
+          const bool in = rows_in && pin && iy >= 0 && iy < H && ix >= 0 && ix < W;
+          u32x4 val = __builtin_bit_cast(
+              u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? (((n * H + iy) * W + ix) * C + c0) * (int)sizeof(T) : OOB, 0, 0));
+          if (bias_chunk && pin) vset_bits<T>(val, 0, bits_of<T>(TT<T>::from_f(1.0f)));
+          raw[S][4 * wq + d] = val;
+        }
       }
     } else {
-      decode_out_pixel(*p, pix0, rn, ry, rx);
+      // decode the first pixel and step along x
+      int n, y, x;
+      decode_out_pixel(*p, pix0, n, y, x);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const bool pin = pix0 + e < p->K;
+        const int iy = y + u - pad, ix = x + vv - pad;
+        const bool in = rows_in && pin && iy >= 0 && iy < H && ix >= 0 && ix < W;
+        u32x4 val = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? (((n * H + iy) * W + ix) * C + c0) * (int)sizeof(T) : OOB, 0, 0));
+        if (bias_chunk && pin) vset_bits<T>(val, 0, bits_of<T>(TT<T>::from_f(1.0f)));
+        raw[S][e] = val;
+        if (++x == p->OW) {
+          x = 0;
+          if (++y == p->OH) {
+            y = 0;
+            ++n;
+          }
+        }
+      }
     }
+  }
+  // A, any channel count, pooled or not: final pixel vectors, element by element
+  template <int S>
+  __device__ __forceinline__ void loadA_generic(int kb) {
+    const T* G = (const T*)p->G;
+    const int O = p->O, o0 = r0;
+    const int pix0 = kb * BK + pg * VEC;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) {
+      const int pix = pix0 + e;
+      u32x4 v = zero4();
+      if (pix < p->K && o0 < O) {
+        const int64_t idx = (int64_t)(p->pool ? (pix >> 2) : pix) * O;
+        const int d = p->pool ? (pix & 3) : -1;
+#pragma unroll 1
+        for (int c = 0; c < VEC; ++c)
+          if (o0 + c < O && (d < 0 || p->gam[idx + o0 + c] == d)) vset_bits<T>(v, c, bits_of<T>(G[idx + o0 + c]));
+      }
+      raw[S][e] = v;
+    }
+  }
+  // B, any channel count, pooled or not: element by element
+  template <int S>
+  __device__ __forceinline__ void loadB_generic(int kb) {
+    const T* X = (const T*)p->X;
+    const int C = p->C, H = p->H, W = p->W, KW = p->KH, pad = p->pad, J = p->KH * p->KH * C, j0 = r0;
+    const int pix0 = kb * BK + pg * VEC;
 #pragma unroll
     for (int e = 0; e < VEC; ++e) {
       const int pix = pix0 + e;
       u32x4 val = zero4();
       if (pix < p->K && j0 <= J) {
         int n, y, x;
-        if (p->pool) {
-          n = wn[e >> 2];
-          y = wy[e >> 2] + ((e >> 1) & 1);
-          x = wx[e >> 2] + (e & 1);
-        } else {
-          n = rn;
-          y = ry;
-          x = rx;
-          rx += 1;
-          if (rx == p->OW) {
-            rx = 0;
-            if (++ry == p->OH) {
-              ry = 0;
-              ++rn;
-            }
-          }
-        }
-        if (vec) {
-          const int iy = y + u - pad, ix = x + vv - pad;
-          if (bias_chunk)
-            vset_bits<T>(val, 0, bits_of<T>(TT<T>::from_f(1.0f)));
-          else if (iy >= 0 && iy < H && ix >= 0 && ix < W)
-            val = *(gptr<const u32x4>)(X + ((int64_t)(n * H + iy) * W + ix) * C + c0);
-        } else {
+        decode_out_pixel(*p, pix, n, y, x);
 #pragma unroll 1
-          for (int q = 0; q < VEC; ++q) {
-            const int j = j0 + q;
-            if (j < J) {
-              const int tq = j / C, c = j - tq * C, uq = tq / KW, vq = tq - uq * KW;
-              const int iy = y + uq - pad, ix = x + vq - pad;
-              if (iy >= 0 && iy < H && ix >= 0 && ix < W)
-                vset_bits<T>(val, q, bits_of<T>(X[((int64_t)(n * H + iy) * W + ix) * C + c]));
-            } else if (j == J) {
-              vset_bits<T>(val, q, bits_of<T>(TT<T>::from_f(1.0f)));
-            }
+        for (int q = 0; q < VEC; ++q) {
+          const int j = j0 + q;
+          if (j < J) {
+            const int tq = j / C, c = j - tq * C, uq = tq / KW, vq = tq - uq * KW;
+            const int iy = y + uq - pad, ix = x + vq - pad;
+            if (iy >= 0 && iy < H && ix >= 0 && ix < W)
+              vset_bits<T>(val, q, bits_of<T>(X[((int64_t)(n * H + iy) * W + ix) * C + c]));
+          } else if (j == J) {
+            vset_bits<T>(val, q, bits_of<T>(TT<T>::from_f(1.0f)));
           }
         }
       }
-      pixv[e] = val;
+      raw[S][e] = val;
     }
-    transpose_block<T>(pixv, r[S]);
   }
+  // stage: A tile at stage[0], B tile at stage[BM * LDK]
   template <int S>
-  __device__ void store(T* sm) const {
-    if (!active) return;
-    const int jl = rg * VEC;
+  __device__ __forceinline__ void store(T* stage) {
+    u32x4 pixv[VEC], out[VEC];
+    if (POOL && isA) {
+      // each window's gradient lands on its argmax pixel only
 #pragma unroll
-    for (int c = 0; c < VEC; ++c) *(u32x4*)(sm + (jl + c) * LDK + pg * VEC) = r[S][c];
+      for (int wq = 0; wq < NW; ++wq)
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          u32x4 v = raw[S][wq];
+          select_am<T>(v, am[S][wq], d);
+          pixv[4 * wq + d] = v;
+        }
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) pixv[e] = raw[S][e];
+    }
+    transpose_block<T>(pixv, out);
+    T* sm = isA ? stage : stage + BM * LDK;
+    const int rl = rg * VEC;
+#pragma unroll
+    for (int c = 0; c < VEC; ++c) *(u32x4*)(sm + (rl + c) * LDK + pg * VEC) = out[c];
   }
 };
 
@@ -1026,19 +1057,19 @@ struct TapRowLoader {
   __amdgpu_buffer_rsrc_t rsrc;
   int rowoff[NV];
   u32x4 r[NV];
-  __device__ void init(const T* base, int64_t ld, int rows_valid) {
+  __device__ __forceinline__ void init(const T* base, int64_t ld, int rows_valid) {
     rsrc = make_rsrc(base, (int64_t)rows_valid * ld * (int64_t)sizeof(T));
 #pragma unroll
     for (int s = 0; s < NV; ++s) rowoff[s] = (int)((int64_t)((threadIdx.x + 256 * s) / CPB) * ld * (int64_t)sizeof(T));
   }
   // col: weight column of this thread's chunk, or -1 for a chunk past the block's end
-  __device__ void load(int col) {
+  __device__ __forceinline__ void load(int col) {
 #pragma unroll
     for (int s = 0; s < NV; ++s)
       r[s] = col < 0 ? zero4()
                      : __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, rowoff[s] + col * (int)sizeof(T), 0, 0));
   }
-  __device__ void store(T* sm) const {
+  __device__ __forceinline__ void store(T* sm) const {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + 256 * s;
@@ -1235,7 +1266,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   else conv_fwd_epilogue<T, BM, BN, BK>(p, m0, n0, acc);
 }
 
-template <typename T, int BM, int BN, int BK>
+template <typename T, int BM, int BN, int BK, int MODE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_wgrad_kernel(const ConvProb* __restrict__ probs,
                                                          const int32_t* __restrict__ tile_map) {
   using TL = Tile<T, BM, BN, BK>;
@@ -1256,13 +1287,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 #pragma unroll
     for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  DzRowsLoader<T, BM, BK> la;
-  la.init(p, m0);
-  PatchRowsLoader<T, BN, BK> lb;
-  lb.init(p, n0);
+  WgradLoader<T, BM, BN, BK, MODE> ld;
+  ld.init(p, m0, n0);
   const int nkb = (p.K + BK - 1) / BK;
   const int kb0 = split * p.kchunk, kb1 = min(nkb, kb0 + p.kchunk);
-  mma_loop<T, BM, BN, BK>(la, lb, kb0, kb1, (T*)smem, acc);
+  mma_loop1<T, BM, BN, BK>(ld, kb0, kb1, (T*)smem, acc);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
@@ -1506,14 +1535,21 @@ hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const 
   return hipGetLastError();
 }
 
-hipError_t launch_conv_wgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles, hipStream_t s) {
+hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const int32_t* tile_map, int ntiles,
+                             hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
-  if (bf16)
-    hipLaunchKernelGGL((conv_wgrad_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>), dim3(ntiles),
-                       dim3(256), 0, s, probs, tile_map);
-  else
-    hipLaunchKernelGGL((conv_wgrad_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32>), dim3(ntiles), dim3(256),
-                       0, s, probs, tile_map);
+#define UN_WGRAD_LAUNCH(T, BM, BN, BK, M) \
+  hipLaunchKernelGGL((conv_wgrad_kernel<T, BM, BN, BK, M>), dim3(ntiles), dim3(256), 0, s, probs, tile_map)
+  if (bf16) {
+    if (mode == WG_POOLED) UN_WGRAD_LAUNCH(bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, WG_POOLED);
+    else if (mode == WG_PLAIN) UN_WGRAD_LAUNCH(bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, WG_PLAIN);
+    else UN_WGRAD_LAUNCH(bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, WG_GENERIC);
+  } else {
+    if (mode == WG_POOLED) UN_WGRAD_LAUNCH(float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, WG_POOLED);
+    else if (mode == WG_PLAIN) UN_WGRAD_LAUNCH(float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, WG_PLAIN);
+    else UN_WGRAD_LAUNCH(float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, WG_GENERIC);
+  }
+#undef UN_WGRAD_LAUNCH
   return hipGetLastError();
 }
 

@@ -76,6 +76,7 @@ struct Launch {
   int kclass;
   size_t probs, map;  // arena offsets
   int count;
+  int mode = 0;       // conv weight gradient: code variant (launch_conv_wgrad)
 };
 
 struct EventRec {
@@ -651,7 +652,19 @@ static un_status plan_and_alloc(un_ctx* c) {
       emit_conv_one(halo, out, kind == 1 ? 7 : 8, kclass);
       emit_conv_one(plain, out, kind, kclass);
     } else {
-      emit_conv_one(all, out, kind, kclass);
+      // weight gradient: one launch per code variant (pooled / unpooled with
+      // whole-vector channels, anything else)
+      const int vec = bf ? 8 : 4;
+      std::vector<ConvProb> by[3];
+      for (auto& p : all) {
+        const bool whole = p.O % vec == 0 && p.C % vec == 0;
+        by[!whole ? 0 : p.pool ? 1 : 2].push_back(p);
+      }
+      for (int m = 0; m < 3; ++m) {
+        const size_t before = out.size();
+        emit_conv_one(by[m], out, kind, kclass);
+        if (out.size() > before) out.back().mode = m;
+      }
     }
   };
 
@@ -1151,7 +1164,7 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
       e = launch_conv_dgrad(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
       break;
     case 3:
-      e = launch_conv_wgrad(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
+      e = launch_conv_wgrad(c->bf16, l.mode, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
       break;
     case 7:
     case 8:
