@@ -86,6 +86,7 @@ struct ConvProb {
   int32_t M, N, K;            // GEMM sizes of this pass
   int32_t tiles_m, tiles_n, splits, kchunk;
   int32_t halo, tr, imgs, hr, hc, cb, cs;  // halo tiling (see above)
+  int32_t bm, bn;                          // halo tile shape
   const void* X;              // conv input, NHWC, channel stride C
   const void* Wt;             // fwd: W [O][ldw]; dgrad: WT [C][ldw]
   int64_t ldw;
@@ -169,7 +170,7 @@ hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* ti
 hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                              hipStream_t s);
 // Halo-tiled forward (dgrad = false) or data gradient (dgrad = true); every
-// problem of the launch has halo != 0.
+// problem of the launch has halo != 0 (either tile shape).
 hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                             hipStream_t s);
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
@@ -195,8 +196,14 @@ constexpr int REDUCE_BLOCK = 256;
 constexpr int CE_MAX_BATCH = 1 << 20;
 constexpr int CE_ROWS = 32;           // sample rows per softmax-CE block
 constexpr int CE_LANES = 8;           // lanes per row
-// Halo tiles: LDS elements of the staged operand rows, and chunk-table entries.
-constexpr int HALO_ELEMS_BF16 = 20480, HALO_ELEMS_F32 = 8192;
+// Halo tiles. Two shapes: wide BM x BN = CONV_BM x CONV_BN, and narrow
+// (2*CONV_BM) x (CONV_BN/2) for passes with at most CONV_BN/2 output columns.
+// LDS per workgroup: the double-buffered weight stage, two chunk tables of
+// HALO_QMAX ints, and the staged rows - halo_elems() elements.
 constexpr int HALO_QMAX = 256;
+constexpr int HALO_LDS_BF16 = 80 * 1024, HALO_LDS_F32 = 52 * 1024;  // two (bf16) / three (fp32) per CU
+constexpr int halo_elems(int es, int BN, int BK) {
+  return ((es == 2 ? HALO_LDS_BF16 : HALO_LDS_F32) - 2 * HALO_QMAX * 4 - 2 * BN * (BK + 16 / es) * es) / es;
+}
 
 }  // namespace un

@@ -1179,18 +1179,25 @@ __device__ __forceinline__ void mma_halo(const T* sH, const int (&hbase)[Tile<T,
   }
 }
 
+// LDS of a halo tile: [weight stages][qa][qb][staged rows], halo_elems() of them.
+template <typename T, int BN, int BK>
+struct HaloSmem {
+  static constexpr int B_ELEMS = BN * (BK + 16 / (int)sizeof(T));
+  static constexpr int HALO = halo_elems(sizeof(T), BN, BK);
+  static constexpr size_t BYTES = (2 * (size_t)B_ELEMS + HALO) * sizeof(T) + 2 * HALO_QMAX * sizeof(int);
+};
+
+// One BM x BN halo tile `local` of problem p.
 template <typename T, int BM, int BN, int BK, bool DGRAD>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_halo_kernel(const ConvProb* __restrict__ probs,
-                                                        const int32_t* __restrict__ tile_map) {
+__device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* smem) {
   using TL = Tile<T, BM, BN, BK>;
+  using HS = HaloSmem<T, BN, BK>;
   constexpr int VEC = TT<T>::VEC, CPB = BK / VEC;
-  constexpr int HALO = sizeof(T) == 2 ? HALO_ELEMS_BF16 : HALO_ELEMS_F32;
-  __shared__ __attribute__((aligned(16))) T sB[2 * TL::B_ELEMS];
-  __shared__ __attribute__((aligned(16))) T sH[HALO];
-  __shared__ int qa[HALO_QMAX], qb[HALO_QMAX];
-  const int prob = tile_map[2 * blockIdx.x], local = tile_map[2 * blockIdx.x + 1];
-  if (prob < 0) return;  // padding of the XCD-ordered tile list
-  const ConvProb& p = probs[prob];
+  static_assert(TL::B_ELEMS == HS::B_ELEMS, "halo LDS budget assumes one pad chunk per row");
+  T* sB = (T*)smem;
+  int* qa = (int*)(sB + 2 * TL::B_ELEMS);
+  int* qb = qa + HALO_QMAX;
+  T* sH = (T*)(qb + HALO_QMAX);
   const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
   const int SH = DGRAD ? p.H : p.OH, SW = DGRAD ? p.W : p.OW;
@@ -1264,6 +1271,21 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   }
   if constexpr (DGRAD) conv_dgrad_epilogue<T, BM, BN, BK>(p, m0, n0, acc);
   else conv_fwd_epilogue<T, BM, BN, BK>(p, m0, n0, acc);
+}
+
+// Halo-tiled conv pass; each problem's tile shape (p.bn) is the wide BM x BN
+// or the narrow 2BM x BN/2 one, so a launch mixes both.
+template <typename T, int BM, int BN, int BK, bool DGRAD>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_halo_kernel(const ConvProb* __restrict__ probs,
+                                                        const int32_t* __restrict__ tile_map) {
+  constexpr size_t BYTES = HaloSmem<T, BN, BK>::BYTES > HaloSmem<T, BN / 2, BK>::BYTES ? HaloSmem<T, BN, BK>::BYTES
+                                                                                       : HaloSmem<T, BN / 2, BK>::BYTES;
+  __shared__ __attribute__((aligned(16))) char smem[BYTES];
+  const int prob = tile_map[2 * blockIdx.x], local = tile_map[2 * blockIdx.x + 1];
+  if (prob < 0) return;  // padding of the XCD-ordered tile list
+  const ConvProb& p = probs[prob];
+  if (p.bn == BN) halo_tile<T, BM, BN, BK, DGRAD>(p, local, smem);
+  else halo_tile<T, 2 * BM, BN / 2, BK, DGRAD>(p, local, smem);
 }
 
 template <typename T, int BM, int BN, int BK, int MODE>

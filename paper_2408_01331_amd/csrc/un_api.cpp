@@ -356,28 +356,27 @@ static std::vector<int32_t> xcd_order(std::vector<TileGroup> groups) {
 // dropped by floor pooling, the operand channels must be whole 16-byte
 // vectors, and the staged rows must fit the LDS budget. Otherwise halo = 0
 // and the pass gathers its operand per k-block.
-static void plan_halo(ConvProb& p, bool bf, bool dgrad) {
-  const int BM = bf ? CONV_BM_BF16 : CONV_BM_F32, BK = bf ? CONV_BK_BF16 : CONV_BK_F32, VEC = bf ? 8 : 4;
+static bool try_halo(ConvProb& p, bool bf, bool dgrad, int BM, int BN) {
+  const int BK = bf ? CONV_BK_BF16 : CONV_BK_F32, VEC = bf ? 8 : 4;
   const int SH = dgrad ? p.H : p.OH, SW = dgrad ? p.W : p.OW, Cin = dgrad ? p.O : p.C;
-  p.halo = 0;
-  if (Cin % VEC != 0) return;
+  if (Cin % VEC != 0) return false;
   int tr, imgs;
   if (SH * SW >= BM) {
-    if (BM % SW != 0) return;
+    if (BM % SW != 0) return false;
     tr = BM / SW;
-    if (SH % tr != 0) return;
+    if (SH % tr != 0) return false;
     imgs = 1;
   } else {
-    if (BM % (SH * SW) != 0) return;
+    if (BM % (SH * SW) != 0) return false;
     tr = SH;
     imgs = BM / (SH * SW);
   }
-  if (!dgrad && p.pool && (tr % 2 != 0 || SW % 2 != 0 || SH % 2 != 0)) return;
+  if (!dgrad && p.pool && (tr % 2 != 0 || SW % 2 != 0 || SH % 2 != 0)) return false;
   const int cb = std::min(Cin, BK);
   const int cs = cb + ((cb / VEC) % 2 == 0 ? VEC : 0);  // odd number of 16-byte chunks per position
   const int hr = tr + p.KH - 1, hc = SW + p.KH - 1;
-  if ((int64_t)imgs * hr * hc * cs > (bf ? HALO_ELEMS_BF16 : HALO_ELEMS_F32)) return;
-  if (p.KH * p.KH * (cb / VEC) > HALO_QMAX) return;
+  if ((int64_t)imgs * hr * hc * cs > halo_elems(bf ? 2 : 4, BN, BK)) return false;
+  if (p.KH * p.KH * (cb / VEC) > HALO_QMAX) return false;
   p.halo = 1;
   p.tr = tr;
   p.imgs = imgs;
@@ -385,6 +384,17 @@ static void plan_halo(ConvProb& p, bool bf, bool dgrad) {
   p.hc = hc;
   p.cb = cb;
   p.cs = cs;
+  p.bm = BM;
+  p.bn = BN;
+  return true;
+}
+
+static void plan_halo(ConvProb& p, bool bf, bool dgrad) {
+  const int BM = bf ? CONV_BM_BF16 : CONV_BM_F32, BN = bf ? CONV_BN_BF16 : CONV_BN_F32;
+  p.halo = 0;
+  // at most BN/2 output columns: the narrow tile wastes no half of each product
+  if (p.N <= BN / 2 && try_halo(p, bf, dgrad, 2 * BM, BN / 2)) return;
+  try_halo(p, bf, dgrad, BM, BN);
 }
 
 // ==========================================================================
@@ -613,8 +623,8 @@ static un_status plan_and_alloc(un_ctx* c) {
     std::vector<TileGroup> gs;
     for (size_t k = 0; k < ps.size(); ++k) {
       ConvProb& p = ps[k];
-      p.tiles_m = cdiv(p.M, CBM);
-      p.tiles_n = cdiv(p.N, CBN);
+      p.tiles_m = cdiv(p.M, p.halo ? p.bm : CBM);
+      p.tiles_n = cdiv(p.N, p.halo ? p.bn : CBN);
       const int per_split = p.tiles_m * p.tiles_n;
       if (kind == 3) {
         // weight gradient: one group per split (its tiles read the same pixels)
@@ -646,7 +656,7 @@ static un_status plan_and_alloc(un_ctx* c) {
     out.push_back(Launch{kind, kclass, po, mo, (int)(map.size() / 2)});
   };
   auto emit_conv = [&](std::vector<ConvProb>& all, std::vector<Launch>& out, int kind, int kclass) {
-    if (kind == 1 || kind == 2) {  // forward / data gradient: halo-tiled problems get their own launch
+    if (kind == 1 || kind == 2) {  // forward / data gradient: halo-tiled problems get their own launch per tile shape
       std::vector<ConvProb> halo, plain;
       for (auto& p : all) (p.halo ? halo : plain).push_back(p);
       emit_conv_one(halo, out, kind == 1 ? 7 : 8, kclass);
