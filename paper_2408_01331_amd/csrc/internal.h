@@ -92,7 +92,7 @@ struct ConvProb {
   int64_t ldw;
   const float* bias;          // fwd
   void* P;                    // fwd output (pooled or not), [pixel][O]
-  uint8_t* amax;              // fwd: window argmax, [w][O]
+  uint8_t* amax;              // fwd: window argmax as the one-hot byte 1 << (dy*2 + dx), [w][O]
   void* PT;                   // fwd: transposed output [(s*O + o)][n] for a Linear consumer, or null
   int64_t ldpt;
   const void* G;              // dgrad/wgrad: gradient at this block's output, [pixel][O]
@@ -172,7 +172,7 @@ hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const i
 // Halo-tiled forward (dgrad = false) or data gradient (dgrad = true); every
 // problem of the launch has halo != 0 (either tile shape).
 hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const int32_t* tile_map, int ntiles,
-                            hipStream_t s);
+                            size_t lds_bytes, hipStream_t s);
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
                          bool keep_grads, hipStream_t s);
 hipError_t launch_ce(bool bf16, const CeProb* probs, int nmodels, const int32_t* labels, int B,
@@ -204,6 +204,11 @@ constexpr int HALO_QMAX = 256;
 constexpr int HALO_LDS_BF16 = 80 * 1024, HALO_LDS_F32 = 52 * 1024;  // two (bf16) / three (fp32) per CU
 constexpr int halo_elems(int es, int BN, int BK) {
   return ((es == 2 ? HALO_LDS_BF16 : HALO_LDS_F32) - 2 * HALO_QMAX * 4 - 2 * BN * (BK + 16 / es) * es) / es;
+}
+
+// LDS bytes of a halo problem: weight stages, chunk tables, staged rows.
+inline size_t halo_lds_bytes(const ConvProb& p, int es, int BK) {
+  return (size_t)2 * p.bn * (BK + 16 / es) * es + 2 * HALO_QMAX * 4 + (size_t)p.imgs * p.hr * p.hc * p.cs * es;
 }
 
 }  // namespace un

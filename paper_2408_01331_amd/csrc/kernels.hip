@@ -387,11 +387,25 @@ template <> __device__ __forceinline__ uint64_t load_am_buf<bf16_t>(__amdgpu_buf
 }
 
 // Keep element e of v only where its window argmax equals d.
-template <typename T> __device__ __forceinline__ void select_am(u32x4& v, uint64_t am, int d) {
+// The forward pass stores, per window and channel, the byte 1 << (dy*2 + dx)
+// of the window's maximum (one-hot), so a selection is a bit test.
+template <typename T> __device__ __forceinline__ void select_am(u32x4& v, uint64_t am, int d);
+template <> __device__ __forceinline__ void select_am<float>(u32x4& v, uint64_t am, int d) {
 #pragma unroll
-  for (int e = 0; e < TT<T>::VEC; ++e)
-    if ((int)((am >> (8 * e)) & 0xffu) != d) vset_bits<T>(v, e, 0u);
+  for (int e = 0; e < 4; ++e)
+    if (!((am >> (8 * e + d)) & 1u)) v[e] = 0u;
 }
+template <> __device__ __forceinline__ void select_am<bf16_t>(u32x4& v, uint64_t am, int d) {
+  // byte masks (0x00 / 0xff) of elements 0-3 and 4-7, widened to 16 bits by byte permutes
+  const uint32_t ml = ((uint32_t)(am >> d) & 0x01010101u) * 0xffu;
+  const uint32_t mh = ((uint32_t)(am >> (32 + d)) & 0x01010101u) * 0xffu;
+  v[0] &= __builtin_amdgcn_perm(ml, ml, 0x01010000u);
+  v[1] &= __builtin_amdgcn_perm(ml, ml, 0x03030202u);
+  v[2] &= __builtin_amdgcn_perm(mh, mh, 0x01010000u);
+  v[3] &= __builtin_amdgcn_perm(mh, mh, 0x03030202u);
+}
+// Is pixel d the maximum of its window (argmax byte a)?
+__device__ __forceinline__ bool am_is(uint8_t a, int d) { return (a >> d) & 1u; }
 
 // Conv dgrad A operand: rows = conv input pixels (n, y, x), k = (u, v, o).
 template <typename T, int ROWS, int BK>
@@ -441,7 +455,7 @@ struct DzGatherLoader {
               int64_t idx;
               int d;
               if (dz_index(*p, rn[s], ry[s] - u + pad, rx[s] - vv + pad, idx, d))
-                if (d < 0 || p->gam[idx + o] == d) vset_bits<T>(v, e, bits_of<T>(G[idx + o]));
+                if (d < 0 || am_is(p->gam[idx + o], d)) vset_bits<T>(v, e, bits_of<T>(G[idx + o]));
             }
           }
         }
@@ -522,11 +536,24 @@ struct WgradLoader {
   int r0, rg, pg;          // first row (o or j) of this thread's micro-tile
   u32x4 raw[2][VEC];       // A pooled: raw[S][0..NW) = window gradients; else the pixel vectors
   uint64_t am[2][NW];      // A pooled: window argmaxes
+  int wkb, wn, wph, wpw;   // B pooled: (image, row, column) of this thread's first window of k-block wkb
   __device__ __forceinline__ void init(const ConvProb& pr, int m0, int n0) {
     p = &pr;
     isA = __builtin_amdgcn_readfirstlane(threadIdx.x) < 128;  // waves 0-1: A, waves 2-3: B (wave-uniform)
     microtile_of(threadIdx.x % 128, rg, pg);
     r0 = (isA ? m0 : n0) + rg * VEC;
+    wkb = -1;
+  }
+  // advance a pooled window position by `by` windows (row-major over images)
+  __device__ __forceinline__ void win_step(int& n, int& ph, int& pw, int by) const {
+    pw += by;
+    while (pw >= p->PW) {
+      pw -= p->PW;
+      if (++ph == p->PH) {
+        ph = 0;
+        ++n;
+      }
+    }
   }
   __device__ __forceinline__ int64_t out_rows() const {
     return p->pool ? (int64_t)p->Nb * p->PH * p->PW : (int64_t)p->Nb * p->OH * p->OW;
@@ -551,13 +578,13 @@ struct WgradLoader {
     if constexpr (POOL) {
       const __amdgpu_buffer_rsrc_t rs_am = make_rsrc(p->gam, out_rows() * p->O);
       // VEC consecutive pixels are NW whole windows; past the last pixel or
-      // channel: zero gradient and an argmax no d matches
+      // channel: zero gradient and no argmax bit
 #pragma unroll
       for (int wq = 0; wq < NW; ++wq) {
         const int pix = pix0 + 4 * wq, idx = (pix >> 2) * O + o0;
         const bool in = rows_in && pix < K;
         raw[S][wq] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? idx * (int)sizeof(T) : OOB, 0, 0));
-        am[S][wq] = in ? load_am_buf<T>(rs_am, idx) : ~0ull;
+        am[S][wq] = in ? load_am_buf<T>(rs_am, idx) : 0ull;
       }
     } else {
 #pragma unroll
@@ -578,12 +605,22 @@ struct WgradLoader {
     const int t = j0 / C, c0 = j0 - t * C, u = t / KW, vv = t - u * KW;
     const int pix0 = kb * BK + pg * VEC;
     if constexpr (POOL) {
-      // VEC consecutive pixels are NW whole windows (one decode each)
+      // VEC consecutive pixels are NW whole windows; their positions are
+      // decoded once and then stepped (k-blocks arrive in order)
+      if (kb != wkb) {
+        const int w = pix0 >> 2, pp = p->PH * p->PW;
+        wn = w / pp;
+        const int rem = w - wn * pp;
+        wph = rem / p->PW;
+        wpw = rem - wph * p->PW;
+      }
+      int n = wn, ph = wph, pw = wpw;
+      win_step(wn, wph, wpw, BK / 4);
+      wkb = kb + 1;
 #pragma unroll
       for (int wq = 0; wq < NW; ++wq) {
-        const int w = (pix0 >> 2) + wq, pp = p->PH * p->PW;
-        const int n = w / pp, rem = w - n * pp, ph = rem / p->PW;
-        const int y0 = 2 * ph, x0 = 2 * (rem - ph * p->PW);
+        if (wq > 0) win_step(n, ph, pw, 1);
+        const int y0 = 2 * ph, x0 = 2 * pw;
         const bool pin = pix0 + 4 * wq < p->K;
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
@@ -633,7 +670,7 @@ struct WgradLoader {
         const int d = p->pool ? (pix & 3) : -1;
 #pragma unroll 1
         for (int c = 0; c < VEC; ++c)
-          if (o0 + c < O && (d < 0 || p->gam[idx + o0 + c] == d)) vset_bits<T>(v, c, bits_of<T>(G[idx + o0 + c]));
+          if (o0 + c < O && (d < 0 || am_is(p->gam[idx + o0 + c], d))) vset_bits<T>(v, c, bits_of<T>(G[idx + o0 + c]));
       }
       raw[S][e] = v;
     }
@@ -938,7 +975,7 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
           }
         const int w = mb >> 2;
         store_t<T>(p.P, (int64_t)w * O + o, mx);
-        p.amax[(int64_t)w * O + o] = (uint8_t)am;
+        p.amax[(int64_t)w * O + o] = (uint8_t)(1u << am);
         if (p.PT) {
           const int pp = p.PH * p.PW, n = w / pp, s = w - n * pp;
           store_t<T>(p.PT, (int64_t)(s * O + o) * p.ldpt + n, mx);
@@ -1245,18 +1282,24 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
   const int KH = p.KH, Cin = DGRAD ? p.O : p.C, cq = threadIdx.x % CPB;
   for (int c0 = 0; c0 < Cin; c0 += p.cb) {
     const int cbw = min(p.cb, Cin - c0), cpt = cbw / VEC, nq = KH * KH * cpt;
-    __syncthreads();  // the previous channel block's halo and tables are no longer read
+    // the weights of k-block 0 first (column computed directly), so their
+    // loads overlap the staging of the operand rows
+    if (cq < nq) {
+      const int tap = cq / cpt;
+      lb.load(tap * Cin + c0 + (cq - tap * cpt) * VEC);
+    } else {
+      lb.load(-1);
+    }
+    __syncthreads();  // the previous channel block's halo, tables and weight stages are no longer read
     for (int q = threadIdx.x; q < nq; q += 256) {
       const int tap = q / cpt, ch = (q - tap * cpt) * VEC, u = tap / KH, v = tap - u * KH;
       qa[q] = (DGRAD ? (KH - 1 - u) * p.hc + (KH - 1 - v) : u * p.hc + v) * p.cs + ch;
       qb[q] = tap * Cin + c0 + ch;  // fwd: W[o][(tap, c)]; dgrad: WT[c][(tap, o)]
     }
     stage_halo<T, DGRAD>(p, sH, img0, y0, c0, cbw);
-    __syncthreads();
-    const int nkb = (nq + CPB - 1) / CPB;
-    lb.load(cq < nq ? qb[cq] : -1);
     lb.store(sB);
     __syncthreads();
+    const int nkb = (nq + CPB - 1) / CPB;
     for (int kb = 0; kb < nkb; ++kb) {
       const int cur = kb & 1;
       const bool more = kb + 1 < nkb;
@@ -1274,13 +1317,13 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
 }
 
 // Halo-tiled conv pass; each problem's tile shape (p.bn) is the wide BM x BN
-// or the narrow 2BM x BN/2 one, so a launch mixes both.
+// or the narrow 2BM x BN/2 one, so a launch mixes both. LDS is dynamic, sized
+// by the host for the launch's largest staged block (small halos leave room
+// for more workgroups per CU).
 template <typename T, int BM, int BN, int BK, bool DGRAD>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_halo_kernel(const ConvProb* __restrict__ probs,
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void conv_halo_kernel(const ConvProb* __restrict__ probs,
                                                         const int32_t* __restrict__ tile_map) {
-  constexpr size_t BYTES = HaloSmem<T, BN, BK>::BYTES > HaloSmem<T, BN / 2, BK>::BYTES ? HaloSmem<T, BN, BK>::BYTES
-                                                                                       : HaloSmem<T, BN / 2, BK>::BYTES;
-  __shared__ __attribute__((aligned(16))) char smem[BYTES];
+  extern __shared__ __attribute__((aligned(16))) char smem[];
   const int prob = tile_map[2 * blockIdx.x], local = tile_map[2 * blockIdx.x + 1];
   if (prob < 0) return;  // padding of the XCD-ordered tile list
   const ConvProb& p = probs[prob];
@@ -1537,22 +1580,40 @@ hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* ti
 }
 
 hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const int32_t* tile_map, int ntiles,
-                            hipStream_t s) {
+                            size_t lds_bytes, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
+  // allow dynamic LDS up to the halo budget (above the default cap)
+  static const hipError_t attr = [] {
+    hipError_t e = hipSuccess, r;
+    r = hipFuncSetAttribute(reinterpret_cast<const void*>(&conv_halo_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, true>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, HALO_LDS_BF16);
+    if (r != hipSuccess) e = r;
+    r = hipFuncSetAttribute(reinterpret_cast<const void*>(&conv_halo_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, false>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, HALO_LDS_BF16);
+    if (r != hipSuccess) e = r;
+    r = hipFuncSetAttribute(reinterpret_cast<const void*>(&conv_halo_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, true>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, HALO_LDS_F32);
+    if (r != hipSuccess) e = r;
+    r = hipFuncSetAttribute(reinterpret_cast<const void*>(&conv_halo_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, false>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, HALO_LDS_F32);
+    if (r != hipSuccess) e = r;
+    return e;
+  }();
+  if (attr != hipSuccess) return attr;
   if (bf16) {
     if (dgrad)
       hipLaunchKernelGGL((conv_halo_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, true>), dim3(ntiles),
-                         dim3(256), 0, s, probs, tile_map);
+                         dim3(256), lds_bytes, s, probs, tile_map);
     else
       hipLaunchKernelGGL((conv_halo_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, false>), dim3(ntiles),
-                         dim3(256), 0, s, probs, tile_map);
+                         dim3(256), lds_bytes, s, probs, tile_map);
   } else {
     if (dgrad)
       hipLaunchKernelGGL((conv_halo_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, true>), dim3(ntiles),
-                         dim3(256), 0, s, probs, tile_map);
+                         dim3(256), lds_bytes, s, probs, tile_map);
     else
       hipLaunchKernelGGL((conv_halo_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, false>), dim3(ntiles),
-                         dim3(256), 0, s, probs, tile_map);
+                         dim3(256), lds_bytes, s, probs, tile_map);
   }
   return hipGetLastError();
 }

@@ -77,6 +77,7 @@ struct Launch {
   size_t probs, map;  // arena offsets
   int count;
   int mode = 0;       // conv weight gradient: code variant (launch_conv_wgrad)
+  size_t lds = 0;     // halo conv: dynamic LDS bytes
 };
 
 struct EventRec {
@@ -541,7 +542,10 @@ static un_status plan_and_alloc(un_ctx* c) {
         const int64_t kpix = b.pool ? (int64_t)B * b.PH * b.PW * 4 : (int64_t)B * b.OH * b.OW;
         const int nkb = cdiv(kpix, BK);
         const int tiles = cdiv(b.O, BMc) * cdiv(J + 1, BNc);
-        int splits = std::max(1, std::min(nkb / 4, cdiv(64, tiles)));  // >= 4 k-blocks per split, ~64 workgroups
+        // >= 4 k-blocks per split and at most 64 workgroups: 64 is the
+        // concurrent capacity of one XCD (32 CUs x 2), so the problems of a
+        // launch fill whole rounds instead of leaving a short extra one
+        int splits = std::max(1, std::min(nkb / 4, 64 / tiles));
         b.kchunk = cdiv(nkb, splits);
         b.splits = cdiv(nkb, b.kchunk);
         b.ldws = rup(J + 1, 4);
@@ -658,8 +662,13 @@ static un_status plan_and_alloc(un_ctx* c) {
   auto emit_conv = [&](std::vector<ConvProb>& all, std::vector<Launch>& out, int kind, int kclass) {
     if (kind == 1 || kind == 2) {  // forward / data gradient: halo-tiled problems get their own launch per tile shape
       std::vector<ConvProb> halo, plain;
-      for (auto& p : all) (p.halo ? halo : plain).push_back(p);
+      size_t lds = 0;
+      for (auto& p : all) {
+        (p.halo ? halo : plain).push_back(p);
+        if (p.halo) lds = std::max(lds, halo_lds_bytes(p, bf ? 2 : 4, bf ? CONV_BK_BF16 : CONV_BK_F32));
+      }
       emit_conv_one(halo, out, kind == 1 ? 7 : 8, kclass);
+      if (!halo.empty()) out.back().lds = lds;
       emit_conv_one(plain, out, kind, kclass);
     } else {
       // weight gradient: one launch per code variant (pooled / unpooled with
@@ -1178,7 +1187,8 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
       break;
     case 7:
     case 8:
-      e = launch_conv_halo(c->bf16, l.kind == 8, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
+      e = launch_conv_halo(c->bf16, l.kind == 8, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, l.lds,
+                           c->stream);
       break;
     case 4:
       e = launch_reduce(c->bf16, c->at<ReduceProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->keep_grads,
