@@ -593,19 +593,46 @@ static un_status plan_and_alloc(un_ctx* c) {
   auto emit_gemm = [&](std::vector<GemmProb>& ps, std::vector<Launch>& out, int kclass) {
     if (ps.empty()) return;
     std::stable_sort(ps.begin(), ps.end(), [](const GemmProb& x, const GemmProb& y) { return x.K > y.K; });
-    // Launch order = problem order (longest K first), tiles in order: the
-    // operands of a level's GEMMs are reused from the shared L2/MALL well
-    // enough that XCD grouping did not pay here, while tile-grain
-    // longest-first order keeps the tail short.
-    std::vector<int32_t> map;
+    // Launch order = problem order (longest K first), tiles m-fastest, then
+    // swizzled for the XCDs: the tiles are cut into runs of up to 8 that share
+    // a B tile (one column of m-tiles), and every 8 consecutive runs are
+    // interleaved so that run r lands on XCD r % 8 with its members 8 launch
+    // slots apart - they run together on one XCD and read their B tile from
+    // its L2 once - while the order stays longest-first at the grain of 8 runs.
+    std::vector<int32_t> nat;  // (problem, tile) pairs in natural order, with run ids
+    std::vector<int32_t> run_of;
+    int runs = 0;
     for (size_t k = 0; k < ps.size(); ++k) {
       GemmProb& p = ps[k];
       const int tm = cdiv(p.M, GBM), tn = cdiv(p.N, GBN);
       p.tiles_n = tn;
+      const int rl = std::min(tm, 8);
       for (int t = 0; t < tm * tn; ++t) {
-        map.push_back((int32_t)k);
-        map.push_back(t);
+        nat.push_back((int32_t)k);
+        nat.push_back(t);
+        const int col = t / tm, row = t - col * tm;
+        if (row % rl == 0) ++runs;
+        run_of.push_back(runs - 1);
       }
+    }
+    std::vector<std::vector<int32_t>> members(runs);
+    for (size_t i = 0; i < run_of.size(); ++i) members[run_of[i]].push_back((int32_t)i);
+    std::vector<int32_t> map;
+    for (int r0 = 0; r0 < runs; r0 += 8) {
+      const int nr = std::min(8, runs - r0);
+      size_t longest = 0;
+      for (int r = r0; r < r0 + nr; ++r) longest = std::max(longest, members[r].size());
+      for (size_t i = 0; i < longest; ++i)
+        for (int x = 0; x < 8; ++x) {
+          const int r = r0 + x;
+          if (x < nr && i < members[r].size()) {
+            map.push_back(nat[2 * members[r][i]]);
+            map.push_back(nat[2 * members[r][i] + 1]);
+          } else {
+            map.push_back(-1);  // keeps the next run member on the same XCD
+            map.push_back(0);
+          }
+        }
     }
     size_t po = put(ps.data(), ps.size() * sizeof(GemmProb));
     for (size_t k = 0; k < ps.size(); ++k) {
