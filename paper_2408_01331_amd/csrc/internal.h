@@ -206,9 +206,12 @@ constexpr int halo_elems(int es, int BN, int BK) {
   return ((es == 2 ? HALO_LDS_BF16 : HALO_LDS_F32) - 2 * HALO_QMAX * 4 - 2 * BN * (BK + 16 / es) * es) / es;
 }
 
-// LDS bytes of a halo problem: weight stages, chunk tables, staged rows.
-inline size_t halo_lds_bytes(const ConvProb& p, int es, int BK) {
-  return (size_t)2 * p.bn * (BK + 16 / es) * es + 2 * HALO_QMAX * 4 + (size_t)p.imgs * p.hr * p.hc * p.cs * es;
+// LDS bytes of a halo problem: weight stages, chunk tables and staged rows
+// during the main loop; the data gradient's staged output tile in the epilogue.
+inline size_t halo_lds_bytes(const ConvProb& p, int es, int BK, bool dgrad) {
+  const size_t main = (size_t)2 * p.bn * (BK + 16 / es) * es + 2 * HALO_QMAX * 4 + (size_t)p.imgs * p.hr * p.hc * p.cs * es;
+  const size_t epi = dgrad ? (size_t)p.bm * (p.bn + 16 / es) * es : 0;
+  return main > epi ? main : epi;
 }
 
 }  // namespace un

@@ -938,12 +938,24 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
 // ---------------------------------------------------------------------------
 // Convolution passes
 // ---------------------------------------------------------------------------
+// The conv data-gradient epilogue stages the tile in LDS (after the main
+// loop's last barrier) and writes whole 16-byte vectors along the channels.
+template <typename T, int BM, int BN>
+struct ConvEpiSmem {
+  static constexpr int VE = 16 / (int)sizeof(T);          // elements per 16-byte vector
+  static constexpr int SLD = BN + VE;                      // staged row stride (elements)
+  static constexpr size_t BYTES = (size_t)BM * SLD * sizeof(T);
+};
+
 // Conv forward epilogue: bias, ReLU, 2x2 max-pool in registers (pool rows
 // are window-ordered, so a lane's four accumulator rows are one window), then
-// the pooled value, its argmax and the optional transposed copy.
+// the pooled value, its one-hot argmax and the optional transposed copy,
+// stored straight from registers (staging this small output in LDS measured
+// slower).
 template <typename T, int BM, int BN, int BK>
 __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int n0,
-                                                  const f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN]) {
+                                                  const f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN],
+                                                  char*) {
   using TL = Tile<T, BM, BN, BK>;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
@@ -998,31 +1010,51 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
 }
 
 // Conv data-gradient epilogue: the previous block's ReLU' (its stored output
-// > 0) and the store of the gradient at that output.
+// > 0) and the store of the gradient at that output, in 16-byte vectors.
 template <typename T, int BM, int BN, int BK>
 __device__ __forceinline__ void conv_dgrad_epilogue(const ConvProb& p, int m0, int n0,
-                                                    const f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN]) {
+                                                    const f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN],
+                                                    char* smem) {
   using TL = Tile<T, BM, BN, BK>;
+  using ES = ConvEpiSmem<T, BM, BN>;
+  constexpr int VE = ES::VE, CPR = BN / VE;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
   const int C = p.C;
-  const T* X = (const T*)p.X;
+  T* sG = (T*)smem;
 #pragma unroll
   for (int i = 0; i < TL::FM; ++i) {
-    const int mb = m0 + wm + 16 * i + 4 * (lane >> 4);
-    if (mb >= p.M) continue;
-    const int nv = min(4, p.M - mb);
+    const int rl = wm + 16 * i + 4 * (lane >> 4);
 #pragma unroll
     for (int j = 0; j < TL::FN; ++j) {
-      const int c = n0 + wn + 16 * j + (lane & 15);
-      if (c >= C) continue;
+      const int cl = wn + 16 * j + (lane & 15);
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        if (r >= nv) break;
-        float v = acc[i][j][r];
-        const int64_t idx = (int64_t)(mb + r) * C + c;
-        if (p.prev_relu && !(TT<T>::to_f(X[idx]) > 0.f)) v = 0.f;
-        store_t<T>(p.Gprev, idx, v);
+      for (int r = 0; r < 4; ++r) sG[(rl + r) * ES::SLD + cl] = TT<T>::from_f(acc[i][j][r]);
+    }
+  }
+  __syncthreads();
+  const T* X = (const T*)p.X;
+  T* Gp = (T*)p.Gprev;
+  const bool vec = (C % VE) == 0;
+  for (int idx = threadIdx.x; idx < BM * CPR; idx += 256) {
+    const int r = idx / CPR, c = n0 + (idx - r * CPR) * VE, m = m0 + r;
+    if (m >= p.M || c >= C) continue;
+    const int64_t g = (int64_t)m * C + c;
+    const T* sv = sG + r * ES::SLD + (c - n0);
+    if (vec) {
+      u32x4 v = *(const u32x4*)sv;
+      if (p.prev_relu) {
+        const u32x4 x = *(gptr<const u32x4>)(X + g);
+#pragma unroll
+        for (int e = 0; e < VE; ++e)
+          if (!(vget<T>(x, e) > 0.f)) vset_bits<T>(v, e, 0u);
+      }
+      *(gptr<u32x4>)(Gp + g) = v;
+    } else {
+      for (int e = 0; e < VE && c + e < C; ++e) {
+        T v = sv[e];
+        if (p.prev_relu && !(TT<T>::to_f(X[g + e]) > 0.f)) v = TT<T>::from_f(0.f);
+        Gp[g + e] = v;
       }
     }
   }
@@ -1051,7 +1083,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K);
   mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
 
-  conv_fwd_epilogue<T, BM, BN, BK>(p, m0, n0, acc);
+  conv_fwd_epilogue<T, BM, BN, BK>(p, m0, n0, acc, smem);
 }
 
 template <typename T, int BM, int BN, int BK>
@@ -1077,7 +1109,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K);
   mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
 
-  conv_dgrad_epilogue<T, BM, BN, BK>(p, m0, n0, acc);
+  conv_dgrad_epilogue<T, BM, BN, BK>(p, m0, n0, acc, smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -1312,8 +1344,8 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
       __syncthreads();
     }
   }
-  if constexpr (DGRAD) conv_dgrad_epilogue<T, BM, BN, BK>(p, m0, n0, acc);
-  else conv_fwd_epilogue<T, BM, BN, BK>(p, m0, n0, acc);
+  if constexpr (DGRAD) conv_dgrad_epilogue<T, BM, BN, BK>(p, m0, n0, acc, smem);
+  else conv_fwd_epilogue<T, BM, BN, BK>(p, m0, n0, acc, smem);
 }
 
 // Halo-tiled conv pass; each problem's tile shape (p.bn) is the wide BM x BN

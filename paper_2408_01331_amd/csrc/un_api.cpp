@@ -692,7 +692,7 @@ static un_status plan_and_alloc(un_ctx* c) {
       size_t lds = 0;
       for (auto& p : all) {
         (p.halo ? halo : plain).push_back(p);
-        if (p.halo) lds = std::max(lds, halo_lds_bytes(p, bf ? 2 : 4, bf ? CONV_BK_BF16 : CONV_BK_F32));
+        if (p.halo) lds = std::max(lds, halo_lds_bytes(p, bf ? 2 : 4, bf ? CONV_BK_BF16 : CONV_BK_F32, kind == 2));
       }
       emit_conv_one(halo, out, kind == 1 ? 7 : 8, kclass);
       if (!halo.empty()) out.back().lds = lds;
