@@ -737,6 +737,23 @@ template <typename T> __device__ __forceinline__ void store_t(void* base, int64_
   ((T*)base)[idx] = TT<T>::from_f(v);
 }
 
+// Load 4 consecutive values (8- or 16-byte aligned) as floats.
+template <typename T> __device__ __forceinline__ void load4_t(const T* src, float (&v)[4]);
+template <> __device__ __forceinline__ void load4_t<float>(const float* src, float (&v)[4]) {
+  const f32x4 x = *(gptr<const f32x4>)src;
+  v[0] = x[0];
+  v[1] = x[1];
+  v[2] = x[2];
+  v[3] = x[3];
+}
+template <> __device__ __forceinline__ void load4_t<bf16_t>(const bf16_t* src, float (&v)[4]) {
+  const u32x2 x = *(gptr<const u32x2>)src;
+  v[0] = __uint_as_float(x[0] << 16);
+  v[1] = __uint_as_float(x[0] & 0xffff0000u);
+  v[2] = __uint_as_float(x[1] << 16);
+  v[3] = __uint_as_float(x[1] & 0xffff0000u);
+}
+
 // Store 4 consecutive values (rows m..m+3 of one column) into a [n][m] array.
 template <typename T> __device__ __forceinline__ void store4_t(T* dst, const float (&v)[4], int nvalid) {
   if (nvalid == 4) {
@@ -772,29 +789,37 @@ template <> __device__ __forceinline__ void store_chunk<bf16_t>(bf16_t* dst, con
 }
 
 // Row-major store of the staged fp32 tile sC [BM][CLD] into C [m][ldc] as OT,
-// one 16-byte chunk per thread and step (contiguous along n).
+// one 16-byte chunk per thread and step (contiguous along n); the tile rows
+// (stride CLD, a multiple of 4) are read as float4s.
 template <typename OT, int BM, int BN, int CLD>
 __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, int m0, int n0, int M, int N) {
   constexpr int VE = 16 / sizeof(OT), CPR = BN / VE;
+  static_assert(CLD % 4 == 0, "float4 rows");
   for (int idx = threadIdx.x; idx < BM * CPR; idx += 256) {
     const int r = idx / CPR, cc = idx - r * CPR;
     const int m = m0 + r, n = n0 + cc * VE;
     if (m >= M || n >= N) continue;
     float v[VE];
 #pragma unroll
-    for (int e = 0; e < VE; ++e) v[e] = sC[r * CLD + cc * VE + e];
+    for (int e = 0; e < VE; e += 4) {
+      const f32x4 x = *(const f32x4*)(sC + r * CLD + cc * VE + e);
+      v[e] = x[0];
+      v[e + 1] = x[1];
+      v[e + 2] = x[2];
+      v[e + 3] = x[3];
+    }
     store_chunk<OT>(C + (int64_t)m * ldc + n, v, min(VE, N - n));
   }
 }
 
 // Transposed store of the staged tile: CT[n][m] for n < N, 16-byte chunks
-// along m. Lanes take consecutive m-chunks of the same n, so a wave writes
-// whole contiguous runs of each CT row.
+// along m. Consecutive threads take consecutive columns, so the strided LDS
+// gathers hit distinct banks.
 template <typename OT, int BM, int BN, int CLD>
 __device__ __forceinline__ void store_cols(const float* sC, OT* CT, int64_t ldct, int m0, int n0, int M, int N) {
-  constexpr int VE = 16 / sizeof(OT), CPC = BM / VE;
-  for (int idx = threadIdx.x; idx < BN * CPC; idx += 256) {
-    const int c = idx / CPC, mq = idx - c * CPC;
+  constexpr int VE = 16 / sizeof(OT);
+  for (int idx = threadIdx.x; idx < BN * (BM / VE); idx += 256) {
+    const int mq = idx / BN, c = idx - mq * BN;
     const int n = n0 + c, m = m0 + mq * VE;
     if (n >= N || m >= M) continue;
     float v[VE];
@@ -831,9 +856,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
   mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
 
   // Epilogue 1: per-element work (bias, ReLU, ReLU' mask) in registers, then
-  // the fp32 tile to LDS with an odd row stride (column gathers hit distinct
-  // banks).
-  constexpr int CLD = BN + 1;
+  // the fp32 tile to LDS (rows of BN + 4 floats: float4-aligned).
+  constexpr int CLD = BN + 4;
   float* sC = (float*)smem;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
@@ -855,10 +879,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
             if (p.relu) v[r] = fmaxf(v[r], 0.f);
           }
         } else if (epi == EPI_DGRAD && p.relu) {
+          // four consecutive rows of one column of the transposed activation
+          // (rows padded to a multiple of 8: one aligned vector load)
           const T* mk = (const T*)p.mask + (int64_t)n * p.ldmask + mb;
+          float mv[4];
+          load4_t<T>(mk, mv);
 #pragma unroll
           for (int r = 0; r < 4; ++r)
-            if (r < nv && !(TT<T>::to_f(mk[r]) > 0.f)) v[r] = 0.f;
+            if (r < nv && !(mv[r] > 0.f)) v[r] = 0.f;
         }
       }
 #pragma unroll
@@ -898,7 +926,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
     float* s = sC + r * CLD + cc * 4;
     const int64_t base = (int64_t)m * p.ldc + n;
     if (n + 4 <= ns) {
-      const f32x4 g = f32x4{s[0], s[1], s[2], s[3]};
+      const f32x4 g = *(const f32x4*)s;
       if (keep_grads) *(gptr<f32x4>)((float*)p.C + base) = g;
       const f32x4 w = f32x4{fmaf(-lr, g[0], w0[q][0]), fmaf(-lr, g[1], w0[q][1]), fmaf(-lr, g[2], w0[q][2]),
                             fmaf(-lr, g[3], w0[q][3])};
@@ -909,10 +937,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
         hb[1] = (uint32_t)f2bf(w[2]) | ((uint32_t)f2bf(w[3]) << 16);
         *(gptr<u32x2>)((bf16_t*)p.Wb + base) = hb;
       }
-      s[0] = w[0];
-      s[1] = w[1];
-      s[2] = w[2];
-      s[3] = w[3];
+      *(f32x4*)s = w;
     } else {
       for (int e = 0; e < 4 && n + e <= ns && n + e < p.N; ++e) {
         const float g = s[e];
