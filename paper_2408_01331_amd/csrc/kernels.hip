@@ -855,6 +855,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
   lb.init((const T*)p.B + (int64_t)n0 * p.ldb, p.ldb, p.N - n0, p.K);
   mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
 
+  // Weight gradient with the SGD update fused: the master-weight loads of
+  // this thread's float4 chunks of W[m][n..n+3] are issued first, so their
+  // latency overlaps the staging below.
+  constexpr int CPR = BN / 4, NCH = BM * CPR / 256;
+  const int ns = p.nsplit;
+  f32x4 w0[NCH];
+  if (p.epi == EPI_WGRAD) {
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) {
+      const int idx = threadIdx.x + 256 * q, r = idx / CPR, n = n0 + (idx - r * CPR) * 4, m = m0 + r;
+      w0[q] = (m < p.M && n + 4 <= ns) ? *(gptr<const f32x4>)(p.W + (int64_t)m * p.ldc + n) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+
   // Epilogue 1: per-element work (bias, ReLU, ReLU' mask) in registers, then
   // the fp32 tile to LDS (rows of BN + 4 floats: float4-aligned).
   constexpr int CLD = BN + 4;
@@ -906,18 +920,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
     return;
   }
 
-  // EPI_WGRAD, SGD fused. Row pass over float4 chunks of W[m][n..n+3]: all
-  // master-weight loads of this thread are issued first, then the update, the
+  // EPI_WGRAD, SGD fused. Row pass over the float4 chunks: the update, the
   // bf16 shadow, the kept gradient; the updated weights go back to LDS. The
   // bias column (n == nsplit) is done element-wise.
-  constexpr int CPR = BN / 4, NCH = BM * CPR / 256;
-  const int ns = p.nsplit;
-  f32x4 w0[NCH];
-#pragma unroll
-  for (int q = 0; q < NCH; ++q) {
-    const int idx = threadIdx.x + 256 * q, r = idx / CPR, n = n0 + (idx - r * CPR) * 4, m = m0 + r;
-    w0[q] = (m < p.M && n + 4 <= ns) ? *(gptr<const f32x4>)(p.W + (int64_t)m * p.ldc + n) : f32x4{0.f, 0.f, 0.f, 0.f};
-  }
 #pragma unroll
   for (int q = 0; q < NCH; ++q) {
     const int idx = threadIdx.x + 256 * q, r = idx / CPR, cc = idx - r * CPR;
