@@ -123,6 +123,19 @@ un_status un_load_batch_device(un_ctx* ctx, const float* x_dev, const int32_t* y
  * Errors: UN_ERR_STATE (no batch loaded), UN_ERR_INVALID (lr not finite). */
 un_status un_step(un_ctx* ctx, float lr, float* losses);
 
+/* Active set of the following steps (Trainer section: a scheduler - first
+ * come first serve, priority, shortest job first, round robin - decides which
+ * sub-models train; a sub-model whose training is done is returned through the
+ * Model Separator while the others go on). mask is host uint8 [N]; mask[i] != 0
+ * keeps model i in the steps. A model outside the set is neither run nor
+ * updated (its parameters stay bitwise as they are), un_step reports NaN as its
+ * loss, and un_get_params returns it at any time. The active models compute
+ * exactly what they compute in any other set. Re-plans the launch tables in
+ * the context's arena (no allocation); waits for the stream; gradients kept
+ * by earlier steps are no longer available. Default: all models active.
+ * Errors: UN_ERR_INVALID (mask NULL or no model active). */
+un_status un_set_active(un_ctx* ctx, const uint8_t* mask);
+
 /* The trained parameters of model i (Model Separator section: the sub-model's
  * parameters copied back into the user's original layout): fp32, PyTorch
  * state_dict order (per parameterised layer: weight then bias; Linear
@@ -144,8 +157,9 @@ un_status un_keep_grads(un_ctx* ctx, int32_t enable);
 
 /* The gradient of model i computed by the last un_step (same layout and order
  * as un_get_params). Waits for the stream. Errors as un_get_params, and
- * UN_ERR_STATE before the first step or when that step did not keep
- * gradients (un_keep_grads). */
+ * UN_ERR_STATE before the first step, when that step did not keep gradients
+ * (un_keep_grads), or after un_set_active; model i must have been active in
+ * that step. */
 un_status un_get_grads(un_ctx* ctx, int32_t i, float* dst, size_t cap_elems, size_t* n_elems);
 
 /* Number of parameters of model i. */

@@ -175,7 +175,7 @@ hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const 
                             size_t lds_bytes, hipStream_t s);
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
                          bool keep_grads, hipStream_t s);
-hipError_t launch_ce(bool bf16, const CeProb* probs, int nmodels, const int32_t* labels, int B,
+hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, const int32_t* labels, int B,
                      float* partial, float* losses, hipStream_t s);
 hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int ntiles, float lr,
                       bool use_grad, hipStream_t s);

@@ -1528,10 +1528,12 @@ __global__ __launch_bounds__(CE_ROWS * CE_LANES) void ce_rows_kernel(const CePro
   }
 }
 
-__global__ void ce_finish_kernel(const float* __restrict__ partial, int nchunks, int nmodels, int B,
-                                 float* __restrict__ losses) {
-  const int m = blockIdx.x * blockDim.x + threadIdx.x;
-  if (m >= nmodels) return;
+// One lane per problem of the list (the active models), writing that model's slot.
+__global__ void ce_finish_kernel(const CeProb* __restrict__ probs, const float* __restrict__ partial, int nchunks,
+                                 int nprobs, int B, float* __restrict__ losses) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= nprobs) return;
+  const int m = probs[i].model;
   float s = 0.f;
   for (int k = 0; k < nchunks; ++k) s += partial[(int64_t)m * nchunks + k];
   losses[m] = s * (1.0f / (float)B);
@@ -1710,18 +1712,18 @@ hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_
   return hipGetLastError();
 }
 
-hipError_t launch_ce(bool bf16, const CeProb* probs, int nmodels, const int32_t* labels, int B, float* partial,
+hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, const int32_t* labels, int B, float* partial,
                      float* losses, hipStream_t s) {
-  if (nmodels <= 0) return hipSuccess;
+  if (nprobs <= 0) return hipSuccess;
   const int nchunks = (B + CE_ROWS - 1) / CE_ROWS;
   if (bf16)
-    hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nmodels), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels, B, partial,
+    hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nprobs), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels, B, partial,
                        nchunks);
   else
-    hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nmodels), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels, B, partial,
+    hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nprobs), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels, B, partial,
                        nchunks);
-  hipLaunchKernelGGL(ce_finish_kernel, dim3((nmodels + 63) / 64), dim3(64), 0, s, partial, nchunks, nmodels, B,
-                     losses);
+  hipLaunchKernelGGL(ce_finish_kernel, dim3((nprobs + 63) / 64), dim3(64), 0, s, probs, partial, nchunks, nprobs,
+                     B, losses);
   return hipGetLastError();
 }
 

@@ -107,6 +107,16 @@ struct un_ctx {
   // schedule
   std::vector<Launch> fwd, bwd[2];  // bwd[p]: dgrad reads copy p of the transposed weights
   Launch ce{}, refresh[2]{};
+  std::vector<char> active;          // models in the step (un_set_active)
+  size_t tables_off = NONE, tables_cap = 0;  // arena region of the descriptor tables
+  // planning results the tables are built from
+  struct Plan {
+    int64_t in_feat = 0, kin_p = 0, cat_rows = 0;
+    std::vector<int> cat;        // models whose first layer is in the concatenated level-0 GEMM
+    std::vector<int64_t> cat_off;  // their first row in it (-1: not in it)
+    size_t catW32 = NONE, catb32 = NONE, catgW = NONE, catgb = NONE, catWb = NONE, catY = NONE, catYT = NONE,
+           catGT = NONE;
+  } plan;
   int wt_cur = 0;                     // which transposed copy the next dgrad reads
   bool keep_grads = false, grads_valid = false;
   int ce_count = 0;
@@ -399,6 +409,525 @@ static void plan_halo(ConvProb& p, bool bf, bool dgrad) {
 }
 
 // ==========================================================================
+// Descriptor tables of one step (the models in c->active only)
+// ==========================================================================
+struct Tables {
+  std::vector<char> host;    // tables as uploaded (pointers encoded as arena offset + 1)
+  std::vector<size_t> fix;   // byte offsets of the encoded pointer fields
+  std::vector<Launch> fwd, bwd[2];
+  Launch ce{}, refresh[2]{};
+};
+
+static void build_tables(un_ctx* c, Tables& T) {
+  const bool bf = c->bf16;
+  const int B = c->B;
+  const int64_t Bp = c->Bp;
+  const int levels = c->levels;
+  const size_t es = bf ? 2 : 4;
+  const int64_t in_feat = c->plan.in_feat, kin_p = c->plan.kin_p, cat_rows = c->plan.cat_rows;
+  auto sub = [](size_t off, int64_t bytes) { return off == NONE ? NONE : off + (size_t)bytes; };
+  const size_t catW32 = c->plan.catW32, catb32 = c->plan.catb32, catgW = c->plan.catgW, catgb = c->plan.catgb,
+               catWb = c->plan.catWb, catY = c->plan.catY, catYT = c->plan.catYT, catGT = c->plan.catGT;
+  // runs of consecutive active models of the concatenated level-0 GEMM: [first row, rows)
+  std::vector<std::pair<int64_t, int64_t>> cat_runs;
+  {
+    const auto& cat = c->plan.cat;
+    for (size_t k = 0; k < cat.size(); ++k) {
+      if (!c->active[cat[k]]) continue;
+      const int64_t r0 = c->plan.cat_off[cat[k]];
+      const int64_t r1 = k + 1 < cat.size() ? c->plan.cat_off[cat[k + 1]] : c->plan.cat_rows;
+      if (!cat_runs.empty() && cat_runs.back().first + cat_runs.back().second == r0) cat_runs.back().second += r1 - r0;
+      else cat_runs.push_back({r0, r1 - r0});
+    }
+  }
+  std::vector<char>& host_tables = T.host;
+  std::vector<size_t>& fix = T.fix;  // byte offsets (in host_tables) of pointer fields to relocate
+  std::vector<Launch>& fwd = T.fwd;
+  std::vector<Launch>* bwd = T.bwd;
+  auto put = [&](const void* src, size_t n) -> size_t {
+    size_t off = rup((int64_t)host_tables.size(), 256);
+    host_tables.resize(off + n);
+    memcpy(host_tables.data() + off, src, n);
+    return off;
+  };
+  // Pointers are encoded as (arena offset + 1) and fixed up after the arena exists.
+  auto ptr = [&](size_t off) -> void* { return off == NONE ? nullptr : (void*)(uintptr_t)(off + 1); };
+
+  const int GBM = bf ? GEMM_BM_BF16 : GEMM_BM_F32, GBN = bf ? GEMM_BN_BF16 : GEMM_BN_F32;
+  const int CBM = bf ? CONV_BM_BF16 : CONV_BM_F32, CBN = bf ? CONV_BN_BF16 : CONV_BN_F32;
+
+  // Problems of one launch are ordered longest-K first (their tiles are the
+  // longest-running), so the ragged tail of a level is made of short tiles.
+  // Order affects scheduling only: every tile computes the same values.
+  auto emit_gemm = [&](std::vector<GemmProb>& ps, std::vector<Launch>& out, int kclass) {
+    if (ps.empty()) return;
+    std::stable_sort(ps.begin(), ps.end(), [](const GemmProb& x, const GemmProb& y) { return x.K > y.K; });
+    // Launch order = problem order (longest K first), tiles m-fastest, then
+    // swizzled for the XCDs: the tiles are cut into runs of up to 8 that share
+    // a B tile (one column of m-tiles), and every 8 consecutive runs are
+    // interleaved so that run r lands on XCD r % 8 with its members 8 launch
+    // slots apart - they run together on one XCD and read their B tile from
+    // its L2 once - while the order stays longest-first at the grain of 8 runs.
+    std::vector<int32_t> nat;  // (problem, tile) pairs in natural order, with run ids
+    std::vector<int32_t> run_of;
+    int runs = 0;
+    for (size_t k = 0; k < ps.size(); ++k) {
+      GemmProb& p = ps[k];
+      const int tm = cdiv(p.M, GBM), tn = cdiv(p.N, GBN);
+      p.tiles_n = tn;
+      const int rl = std::min(tm, 8);
+      for (int t = 0; t < tm * tn; ++t) {
+        nat.push_back((int32_t)k);
+        nat.push_back(t);
+        const int col = t / tm, row = t - col * tm;
+        if (row % rl == 0) ++runs;
+        run_of.push_back(runs - 1);
+      }
+    }
+    std::vector<std::vector<int32_t>> members(runs);
+    for (size_t i = 0; i < run_of.size(); ++i) members[run_of[i]].push_back((int32_t)i);
+    std::vector<int32_t> map;
+    for (int r0 = 0; r0 < runs; r0 += 8) {
+      const int nr = std::min(8, runs - r0);
+      size_t longest = 0;
+      for (int r = r0; r < r0 + nr; ++r) longest = std::max(longest, members[r].size());
+      for (size_t i = 0; i < longest; ++i)
+        for (int x = 0; x < 8; ++x) {
+          const int r = r0 + x;
+          if (x < nr && i < members[r].size()) {
+            map.push_back(nat[2 * members[r][i]]);
+            map.push_back(nat[2 * members[r][i] + 1]);
+          } else {
+            map.push_back(-1);  // keeps the next run member on the same XCD
+            map.push_back(0);
+          }
+        }
+    }
+    size_t po = put(ps.data(), ps.size() * sizeof(GemmProb));
+    for (size_t k = 0; k < ps.size(); ++k) {
+      size_t b0 = po + k * sizeof(GemmProb);
+      for (size_t f : {offsetof(GemmProb, A), offsetof(GemmProb, B), offsetof(GemmProb, C), offsetof(GemmProb, CT),
+                       offsetof(GemmProb, bias), offsetof(GemmProb, mask), offsetof(GemmProb, dbias),
+                       offsetof(GemmProb, W), offsetof(GemmProb, Wb), offsetof(GemmProb, WT),
+                       offsetof(GemmProb, bmaster)})
+        fix.push_back(b0 + f);
+    }
+    size_t mo = put(map.data(), map.size() * 4);
+    out.push_back(Launch{0, kclass, po, mo, (int)(map.size() / 2)});
+  };
+  auto emit_conv_one = [&](std::vector<ConvProb>& ps, std::vector<Launch>& out, int kind, int kclass) {
+    if (ps.empty()) return;
+    std::stable_sort(ps.begin(), ps.end(),
+                     [](const ConvProb& x, const ConvProb& y) { return (int64_t)x.K * x.splits > (int64_t)y.K * y.splits; });
+    const int BK = bf ? CONV_BK_BF16 : CONV_BK_F32;
+    std::vector<TileGroup> gs;
+    for (size_t k = 0; k < ps.size(); ++k) {
+      ConvProb& p = ps[k];
+      p.tiles_m = cdiv(p.M, p.halo ? p.bm : CBM);
+      p.tiles_n = cdiv(p.N, p.halo ? p.bn : CBN);
+      const int per_split = p.tiles_m * p.tiles_n;
+      if (kind == 3) {
+        // weight gradient: one group per split (its tiles read the same pixels)
+        for (int sp = 0; sp < p.splits; ++sp)
+          gs.push_back(TileGroup{(int32_t)k, sp * per_split, per_split, per_split * (p.kchunk + 1.0)});
+      } else {
+        // forward / data gradient: tiles in order (n-fastest), one tile per group
+        for (int t = 0; t < per_split; ++t) gs.push_back(TileGroup{(int32_t)k, t, 1, cdiv(p.K, BK) + 2.0});
+      }
+    }
+    std::vector<int32_t> map;
+    if (kind == 3) {
+      map = xcd_order(gs);
+    } else {
+      for (auto& g : gs) {
+        map.push_back(g.prob);
+        map.push_back(g.first);
+      }
+    }
+    size_t po = put(ps.data(), ps.size() * sizeof(ConvProb));
+    for (size_t k = 0; k < ps.size(); ++k) {
+      size_t b0 = po + k * sizeof(ConvProb);
+      for (size_t f : {offsetof(ConvProb, X), offsetof(ConvProb, Wt), offsetof(ConvProb, bias), offsetof(ConvProb, P),
+                       offsetof(ConvProb, amax), offsetof(ConvProb, PT), offsetof(ConvProb, G), offsetof(ConvProb, gam),
+                       offsetof(ConvProb, Gprev), offsetof(ConvProb, ws)})
+        fix.push_back(b0 + f);
+    }
+    size_t mo = put(map.data(), map.size() * 4);
+    out.push_back(Launch{kind, kclass, po, mo, (int)(map.size() / 2)});
+  };
+  auto emit_conv = [&](std::vector<ConvProb>& all, std::vector<Launch>& out, int kind, int kclass) {
+    if (kind == 1 || kind == 2) {  // forward / data gradient: halo-tiled problems get their own launch per tile shape
+      std::vector<ConvProb> halo, plain;
+      size_t lds = 0;
+      for (auto& p : all) {
+        (p.halo ? halo : plain).push_back(p);
+        if (p.halo) lds = std::max(lds, halo_lds_bytes(p, bf ? 2 : 4, bf ? CONV_BK_BF16 : CONV_BK_F32, kind == 2));
+      }
+      emit_conv_one(halo, out, kind == 1 ? 7 : 8, kclass);
+      if (!halo.empty()) out.back().lds = lds;
+      emit_conv_one(plain, out, kind, kclass);
+    } else {
+      // weight gradient: one launch per code variant (pooled / unpooled with
+      // whole-vector channels, anything else)
+      const int vec = bf ? 8 : 4;
+      std::vector<ConvProb> by[3];
+      for (auto& p : all) {
+        const bool whole = p.O % vec == 0 && p.C % vec == 0;
+        by[!whole ? 0 : p.pool ? 1 : 2].push_back(p);
+      }
+      for (int m = 0; m < 3; ++m) {
+        const size_t before = out.size();
+        emit_conv_one(by[m], out, kind, kclass);
+        if (out.size() > before) out.back().mode = m;
+      }
+    }
+  };
+
+  auto conv_base = [&](const Block& b) {
+    ConvProb p{};
+    p.Nb = B;
+    p.C = b.C;
+    p.H = b.H;
+    p.W = b.W;
+    p.O = b.O;
+    p.KH = b.KH;
+    p.pad = b.pad;
+    p.OH = b.OH;
+    p.OW = b.OW;
+    p.PH = b.PH;
+    p.PW = b.PW;
+    p.pool = b.pool;
+    p.relu = b.relu;
+    p.prev_relu = b.prev_relu;
+    p.splits = 1;
+    return p;
+  };
+
+  // forward levels
+  for (int lv = 0; lv < levels; ++lv) {
+    std::vector<GemmProb> gp;
+    std::vector<ConvProb> cp;
+    bool cat_done = false;
+    for (auto& m : c->models) {
+      if (lv >= (int)m.blocks.size() || !c->active[m.blocks[0].model]) continue;
+      Block& b = m.blocks[lv];
+      if (b.kind == 0) {
+        if (b.concat) {
+          // one problem per run of consecutive active models of the concatenation
+          if (cat_done) continue;
+          cat_done = true;
+          for (const auto& run : cat_runs) {
+            GemmProb p{};
+            p.A = ptr(c->Xin);
+            p.lda = c->ldxin;
+            p.B = ptr(bf ? sub(catWb, run.first * kin_p * 2) : sub(catW32, run.first * kin_p * 4));
+            p.ldb = kin_p;
+            p.M = B;
+            p.N = (int)run.second;
+            p.K = (int)in_feat;
+            p.epi = EPI_FWD;
+            p.relu = 1;
+            p.C = ptr(sub(catY, run.first * (int64_t)es));
+            p.ldc = cat_rows;
+            p.CT = ptr(sub(catYT, run.first * Bp * (int64_t)es));
+            p.ldct = Bp;
+            p.bias = (const float*)ptr(sub(catb32, run.first * 4));
+            gp.push_back(p);
+          }
+          continue;
+        }
+        GemmProb p{};
+        p.A = ptr(b.X);
+        p.lda = b.ldx;
+        p.B = ptr(bf ? b.Wb : b.W32);
+        p.ldb = b.ldw;
+        p.M = B;
+        p.N = b.N;
+        p.K = b.K;
+        p.epi = b.last ? EPI_LOGITS : EPI_FWD;
+        p.relu = b.relu;
+        p.C = ptr(b.Y);
+        p.ldc = b.ldy;
+        p.CT = ptr(b.YT);
+        p.ldct = b.ldyt;
+        p.bias = (const float*)ptr(b.b32);
+        gp.push_back(p);
+      } else {
+        ConvProb p = conv_base(b);
+        p.M = b.pool ? B * b.PH * b.PW * 4 : B * b.OH * b.OW;
+        p.N = b.O;
+        p.K = b.KH * b.KH * b.C;
+        p.X = ptr(b.X);
+        p.Wt = ptr(bf ? b.Wb : b.W32);
+        p.ldw = b.ldw;
+        p.bias = (const float*)ptr(b.b32);
+        p.P = ptr(b.Y);
+        p.amax = (uint8_t*)ptr(b.amax);
+        p.PT = ptr(b.YT);
+        p.ldpt = b.ldyt;
+        plan_halo(p, bf, false);
+        cp.push_back(p);
+      }
+    }
+    emit_gemm(gp, fwd, UN_K_GEMM_FWD);
+    emit_conv(cp, fwd, 1, UN_K_CONV_FWD);
+  }
+
+  // softmax-CE
+  std::vector<CeProb> ces;
+  for (size_t mi = 0; mi < c->models.size(); ++mi) {
+    if (!c->active[mi]) continue;
+    Block& b = c->models[mi].blocks.back();
+    CeProb p{};
+    p.logits = (const float*)ptr(b.Y);
+    p.ldl = b.ldy;
+    p.G = ptr(b.G);
+    p.ldg = b.ldg;
+    p.GT = ptr(b.GT);
+    p.ldgt = b.ldgt;
+    p.C = b.N;
+    p.model = (int)mi;
+    ces.push_back(p);
+  }
+  {
+    size_t po = put(ces.data(), ces.size() * sizeof(CeProb));
+    for (size_t k = 0; k < ces.size(); ++k) {
+      size_t b0 = po + k * sizeof(CeProb);
+      for (size_t f : {offsetof(CeProb, logits), offsetof(CeProb, G), offsetof(CeProb, GT)}) fix.push_back(b0 + f);
+    }
+    T.ce = Launch{5, UN_K_CE, po, NONE, (int)ces.size()};
+  }
+
+  // backward levels, once per parity of the transposed-weight copies: the
+  // dgrad of a level reads copy `par` while the fused update of the same
+  // launch writes the other copy.
+  for (int par = 0; par < 2; ++par)
+  for (int lv = levels - 1; lv >= 0; --lv) {
+    std::vector<GemmProb> gp;
+    std::vector<ConvProb> dp, wp;
+    std::vector<ReduceProb> rp;
+    bool cat_done = false;
+    for (auto& m : c->models) {
+      if (lv >= (int)m.blocks.size() || !c->active[m.blocks[0].model]) continue;
+      Block& b = m.blocks[lv];
+      if (b.kind == 0) {
+        // dgrad (not at level 0): gradient at the previous block's output
+        if (lv > 0) {
+          Block& pb = m.blocks[lv - 1];
+          GemmProb p{};
+          p.A = ptr(b.G);
+          p.lda = b.ldg;
+          p.B = ptr(par == 0 ? b.WT : b.WT2);
+          p.ldb = b.ldwt;
+          p.M = B;
+          p.N = b.K;
+          p.K = b.N;
+          p.epi = EPI_DGRAD;
+          p.relu = pb.relu;
+          p.mask = ptr(b.XT);
+          p.ldmask = b.ldxt;
+          if (pb.kind == 0) {
+            p.C = ptr(pb.G);
+            p.ldc = pb.ldg;
+            p.CT = ptr(pb.GT);
+            p.ldct = pb.ldgt;
+          } else {
+            p.C = ptr(pb.G);
+            p.ldc = pb.out_elems_per_sample();
+          }
+          gp.push_back(p);
+        }
+        // wgrad (+ bias gradient through the ones row of XT)
+        if (b.concat) {
+          if (cat_done) continue;
+          cat_done = true;
+          for (const auto& run : cat_runs) {
+            GemmProb p{};
+            p.A = ptr(sub(catGT, run.first * Bp * (int64_t)es));
+            p.lda = Bp;
+            p.B = ptr(c->XinT);
+            p.ldb = c->ldxint;
+            p.M = (int)run.second;
+            p.N = (int)in_feat + 1;
+            p.K = B;
+            p.epi = EPI_WGRAD;
+            p.nsplit = (int)in_feat;
+            p.C = ptr(sub(catgW, run.first * kin_p * 4));
+            p.ldc = kin_p;
+            p.dbias = (float*)ptr(sub(catgb, run.first * 4));
+            p.W = (float*)ptr(sub(catW32, run.first * kin_p * 4));
+            p.Wb = ptr(sub(catWb, run.first * kin_p * 2));
+            p.bmaster = (float*)ptr(sub(catb32, run.first * 4));
+            gp.push_back(p);
+          }
+          continue;
+        }
+        GemmProb p{};
+        p.A = ptr(b.GT);
+        p.lda = b.ldgt;
+        p.B = ptr(b.XT);
+        p.ldb = b.ldxt;
+        p.M = b.N;
+        p.N = b.K + 1;
+        p.K = B;
+        p.epi = EPI_WGRAD;
+        p.nsplit = b.K;
+        p.C = ptr(b.gW);
+        p.ldc = b.ldw;
+        p.dbias = (float*)ptr(b.gb);
+        p.W = (float*)ptr(b.W32);
+        p.Wb = ptr(b.Wb);
+        p.WT = ptr(par == 0 ? b.WT2 : b.WT);
+        p.ldwt = b.ldwt;
+        p.bmaster = (float*)ptr(b.b32);
+        gp.push_back(p);
+      } else {
+        const int J = b.KH * b.KH * b.C;
+        if (lv > 0) {
+          Block& pb = m.blocks[lv - 1];
+          ConvProb p = conv_base(b);
+          p.M = B * b.H * b.W;
+          p.N = b.C;
+          p.K = b.KH * b.KH * b.O;
+          p.X = ptr(b.X);
+          p.Wt = ptr(b.WT);
+          p.ldw = b.ldwt;
+          p.G = ptr(b.G);
+          p.gam = (const uint8_t*)ptr(b.amax);
+          p.Gprev = ptr(pb.G);
+          plan_halo(p, bf, true);
+          dp.push_back(p);
+        }
+        ConvProb p = conv_base(b);
+        p.M = b.O;
+        p.N = J + 1;
+        p.K = b.pool ? B * b.PH * b.PW * 4 : B * b.OH * b.OW;
+        p.X = ptr(b.X);
+        p.G = ptr(b.G);
+        p.gam = (const uint8_t*)ptr(b.amax);
+        p.ws = (float*)ptr(b.ws);
+        p.ldws = b.ldws;
+        p.splits = b.splits;
+        p.kchunk = b.kchunk;
+        wp.push_back(p);
+        ReduceProb r{};
+        r.ws = (const float*)ptr(b.ws);
+        r.ldws = b.ldws;
+        r.splits = b.splits;
+        r.O = b.O;
+        r.J = J;
+        r.C = b.C;
+        r.gW = (float*)ptr(b.gW);
+        r.ldgw = b.ldw;
+        r.gb = (float*)ptr(b.gb);
+        r.W = (float*)ptr(b.W32);
+        r.Wb = ptr(b.Wb);
+        r.WT = ptr(b.WT);  // conv: the dgrad launch of this level has completed
+        r.ldwt = b.ldwt;
+        r.bmaster = (float*)ptr(b.b32);
+        rp.push_back(r);
+      }
+    }
+    emit_gemm(gp, bwd[par], UN_K_GEMM_BWD);
+    emit_conv(dp, bwd[par], 2, UN_K_CONV_DGRAD);
+    emit_conv(wp, bwd[par], 3, UN_K_CONV_WGRAD);
+    if (!rp.empty()) {
+      std::vector<int32_t> map;
+      for (size_t k = 0; k < rp.size(); ++k) {
+        rp[k].blk_base = (int32_t)map.size();
+        const int nb = cdiv((int64_t)rp[k].O * (rp[k].J + 1), REDUCE_BLOCK);
+        for (int t = 0; t < nb; ++t) map.push_back((int32_t)k);
+      }
+      size_t po = put(rp.data(), rp.size() * sizeof(ReduceProb));
+      for (size_t k = 0; k < rp.size(); ++k) {
+        size_t b0 = po + k * sizeof(ReduceProb);
+        for (size_t f : {offsetof(ReduceProb, ws), offsetof(ReduceProb, gW), offsetof(ReduceProb, gb),
+                         offsetof(ReduceProb, W), offsetof(ReduceProb, Wb), offsetof(ReduceProb, WT),
+                         offsetof(ReduceProb, bmaster)})
+          fix.push_back(b0 + f);
+      }
+      size_t mo = put(map.data(), map.size() * 4);
+      bwd[par].push_back(Launch{4, UN_K_OTHER, po, mo, (int)map.size()});
+    }
+  }
+
+  // Shadow refresh (after un_set_params / initialisation): rewrite the bf16
+  // shadow and transposed copy `pass` of every weight from the fp32 master.
+  for (int pass = 0; pass < 2; ++pass) {
+    std::vector<SgdTensor> ts;
+    std::vector<int32_t> map;
+    auto add = [&](SgdTensor t) {
+      t.tiles_r = cdiv(t.R, SGD_TILE);
+      t.tiles_c = cdiv(t.Cc, SGD_TILE);
+      t.tile_base = (int32_t)map.size();
+      const int nt = t.J * t.tiles_r * t.tiles_c;
+      for (int k = 0; k < nt; ++k) map.push_back((int32_t)ts.size());
+      ts.push_back(t);
+    };
+    for (auto& m : c->models)
+      for (auto& b : m.blocks) {
+        SgdTensor w{};
+        w.W = (float*)ptr(b.W32);
+        w.Wb = ptr(b.Wb);
+        w.WT = ptr(pass == 1 && b.WT2 != NONE ? b.WT2 : b.WT);
+        w.ldw = b.ldw;
+        w.ldwt = b.ldwt;
+        w.R = b.rows;
+        if (b.kind == 0) {
+          w.J = 1;
+          w.Cc = b.K;
+        } else {
+          w.J = b.KH * b.KH;
+          w.Cc = b.C;
+        }
+        add(w);
+      }
+    size_t po = put(ts.data(), ts.size() * sizeof(SgdTensor));
+    for (size_t k = 0; k < ts.size(); ++k) {
+      size_t b0 = po + k * sizeof(SgdTensor);
+      for (size_t f : {offsetof(SgdTensor, W), offsetof(SgdTensor, G), offsetof(SgdTensor, Wb), offsetof(SgdTensor, WT)})
+        fix.push_back(b0 + f);
+    }
+    size_t mo = put(map.data(), map.size() * 4);
+    T.refresh[pass] = Launch{6, UN_K_SGD, po, mo, (int)map.size()};
+  }
+
+}
+
+// Relocate a freshly built table set into the arena's table region, upload it
+// (the stream must be idle: the previous tables may still be in use by it
+// otherwise) and make it the context's schedule.
+static un_status install_tables(un_ctx* c, Tables& T) {
+  if (T.host.size() > c->tables_cap)
+    return fail(c, UN_ERR_UNSUPPORTED, "schedule tables exceed the reserved region");
+  for (size_t f : T.fix) {
+    uintptr_t v;
+    memcpy(&v, T.host.data() + f, sizeof(v));
+    if (v != 0) v = (uintptr_t)(c->base + (v - 1));
+    memcpy(T.host.data() + f, &v, sizeof(v));
+  }
+  auto relocate = [&](Launch& l) {
+    l.probs += c->tables_off;
+    if (l.map != NONE) l.map += c->tables_off;
+  };
+  for (auto& l : T.fwd) relocate(l);
+  for (int p = 0; p < 2; ++p)
+    for (auto& l : T.bwd[p]) relocate(l);
+  relocate(T.ce);
+  relocate(T.refresh[0]);
+  relocate(T.refresh[1]);
+  HIPCHK(c, hipMemcpyAsync(c->base + c->tables_off, T.host.data(), T.host.size(), hipMemcpyHostToDevice, c->stream));
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  c->fwd = T.fwd;
+  c->bwd[0] = T.bwd[0];
+  c->bwd[1] = T.bwd[1];
+  c->ce = T.ce;
+  c->refresh[0] = T.refresh[0];
+  c->refresh[1] = T.refresh[1];
+  return UN_OK;
+}
+
+// ==========================================================================
 // Planner
 // ==========================================================================
 static un_status plan_and_alloc(un_ctx* c) {
@@ -571,484 +1100,39 @@ static un_status plan_and_alloc(un_ctx* c) {
   }
   c->levels = levels;
 
-  // --- descriptor tables (built on the host, copied into the arena)
-  std::vector<char> host_tables;
-  auto put = [&](const void* src, size_t n) -> size_t {
-    size_t off = rup((int64_t)host_tables.size(), 256);
-    host_tables.resize(off + n);
-    memcpy(host_tables.data() + off, src, n);
-    return off;
-  };
-  std::vector<Launch> fwd, bwd[2];
-  auto ptr = [&](size_t off) -> void* { return off == NONE ? nullptr : (void*)(uintptr_t)(off + 1); };
-  // Pointers are encoded as (arena offset + 1) and fixed up after the arena exists.
-  std::vector<size_t> fix;  // byte offsets (in host_tables) of pointer fields to relocate
+  // --- planning results the descriptor tables are built from
+  c->plan.in_feat = in_feat;
+  c->plan.kin_p = kin_p;
+  c->plan.cat_rows = cat_rows;
+  c->plan.cat = cat;
+  c->plan.cat_off = cat_off;
+  c->plan.catW32 = catW32;
+  c->plan.catb32 = catb32;
+  c->plan.catgW = catgW;
+  c->plan.catgb = catgb;
+  c->plan.catWb = catWb;
+  c->plan.catY = catY;
+  c->plan.catYT = catYT;
+  c->plan.catGT = catGT;
+  c->active.assign(c->models.size(), 1);
+  Tables T;
+  build_tables(c, T);
 
-  const int GBM = bf ? GEMM_BM_BF16 : GEMM_BM_F32, GBN = bf ? GEMM_BN_BF16 : GEMM_BN_F32;
-  const int CBM = bf ? CONV_BM_BF16 : CONV_BM_F32, CBN = bf ? CONV_BN_BF16 : CONV_BN_F32;
-
-  // Problems of one launch are ordered longest-K first (their tiles are the
-  // longest-running), so the ragged tail of a level is made of short tiles.
-  // Order affects scheduling only: every tile computes the same values.
-  auto emit_gemm = [&](std::vector<GemmProb>& ps, std::vector<Launch>& out, int kclass) {
-    if (ps.empty()) return;
-    std::stable_sort(ps.begin(), ps.end(), [](const GemmProb& x, const GemmProb& y) { return x.K > y.K; });
-    // Launch order = problem order (longest K first), tiles m-fastest, then
-    // swizzled for the XCDs: the tiles are cut into runs of up to 8 that share
-    // a B tile (one column of m-tiles), and every 8 consecutive runs are
-    // interleaved so that run r lands on XCD r % 8 with its members 8 launch
-    // slots apart - they run together on one XCD and read their B tile from
-    // its L2 once - while the order stays longest-first at the grain of 8 runs.
-    std::vector<int32_t> nat;  // (problem, tile) pairs in natural order, with run ids
-    std::vector<int32_t> run_of;
-    int runs = 0;
-    for (size_t k = 0; k < ps.size(); ++k) {
-      GemmProb& p = ps[k];
-      const int tm = cdiv(p.M, GBM), tn = cdiv(p.N, GBN);
-      p.tiles_n = tn;
-      const int rl = std::min(tm, 8);
-      for (int t = 0; t < tm * tn; ++t) {
-        nat.push_back((int32_t)k);
-        nat.push_back(t);
-        const int col = t / tm, row = t - col * tm;
-        if (row % rl == 0) ++runs;
-        run_of.push_back(runs - 1);
-      }
-    }
-    std::vector<std::vector<int32_t>> members(runs);
-    for (size_t i = 0; i < run_of.size(); ++i) members[run_of[i]].push_back((int32_t)i);
-    std::vector<int32_t> map;
-    for (int r0 = 0; r0 < runs; r0 += 8) {
-      const int nr = std::min(8, runs - r0);
-      size_t longest = 0;
-      for (int r = r0; r < r0 + nr; ++r) longest = std::max(longest, members[r].size());
-      for (size_t i = 0; i < longest; ++i)
-        for (int x = 0; x < 8; ++x) {
-          const int r = r0 + x;
-          if (x < nr && i < members[r].size()) {
-            map.push_back(nat[2 * members[r][i]]);
-            map.push_back(nat[2 * members[r][i] + 1]);
-          } else {
-            map.push_back(-1);  // keeps the next run member on the same XCD
-            map.push_back(0);
-          }
-        }
-    }
-    size_t po = put(ps.data(), ps.size() * sizeof(GemmProb));
-    for (size_t k = 0; k < ps.size(); ++k) {
-      size_t b0 = po + k * sizeof(GemmProb);
-      for (size_t f : {offsetof(GemmProb, A), offsetof(GemmProb, B), offsetof(GemmProb, C), offsetof(GemmProb, CT),
-                       offsetof(GemmProb, bias), offsetof(GemmProb, mask), offsetof(GemmProb, dbias),
-                       offsetof(GemmProb, W), offsetof(GemmProb, Wb), offsetof(GemmProb, WT),
-                       offsetof(GemmProb, bmaster)})
-        fix.push_back(b0 + f);
-    }
-    size_t mo = put(map.data(), map.size() * 4);
-    out.push_back(Launch{0, kclass, po, mo, (int)(map.size() / 2)});
-  };
-  auto emit_conv_one = [&](std::vector<ConvProb>& ps, std::vector<Launch>& out, int kind, int kclass) {
-    if (ps.empty()) return;
-    std::stable_sort(ps.begin(), ps.end(),
-                     [](const ConvProb& x, const ConvProb& y) { return (int64_t)x.K * x.splits > (int64_t)y.K * y.splits; });
-    const int BK = bf ? CONV_BK_BF16 : CONV_BK_F32;
-    std::vector<TileGroup> gs;
-    for (size_t k = 0; k < ps.size(); ++k) {
-      ConvProb& p = ps[k];
-      p.tiles_m = cdiv(p.M, p.halo ? p.bm : CBM);
-      p.tiles_n = cdiv(p.N, p.halo ? p.bn : CBN);
-      const int per_split = p.tiles_m * p.tiles_n;
-      if (kind == 3) {
-        // weight gradient: one group per split (its tiles read the same pixels)
-        for (int sp = 0; sp < p.splits; ++sp)
-          gs.push_back(TileGroup{(int32_t)k, sp * per_split, per_split, per_split * (p.kchunk + 1.0)});
-      } else {
-        // forward / data gradient: tiles in order (n-fastest), one tile per group
-        for (int t = 0; t < per_split; ++t) gs.push_back(TileGroup{(int32_t)k, t, 1, cdiv(p.K, BK) + 2.0});
-      }
-    }
-    std::vector<int32_t> map;
-    if (kind == 3) {
-      map = xcd_order(gs);
-    } else {
-      for (auto& g : gs) {
-        map.push_back(g.prob);
-        map.push_back(g.first);
-      }
-    }
-    size_t po = put(ps.data(), ps.size() * sizeof(ConvProb));
-    for (size_t k = 0; k < ps.size(); ++k) {
-      size_t b0 = po + k * sizeof(ConvProb);
-      for (size_t f : {offsetof(ConvProb, X), offsetof(ConvProb, Wt), offsetof(ConvProb, bias), offsetof(ConvProb, P),
-                       offsetof(ConvProb, amax), offsetof(ConvProb, PT), offsetof(ConvProb, G), offsetof(ConvProb, gam),
-                       offsetof(ConvProb, Gprev), offsetof(ConvProb, ws)})
-        fix.push_back(b0 + f);
-    }
-    size_t mo = put(map.data(), map.size() * 4);
-    out.push_back(Launch{kind, kclass, po, mo, (int)(map.size() / 2)});
-  };
-  auto emit_conv = [&](std::vector<ConvProb>& all, std::vector<Launch>& out, int kind, int kclass) {
-    if (kind == 1 || kind == 2) {  // forward / data gradient: halo-tiled problems get their own launch per tile shape
-      std::vector<ConvProb> halo, plain;
-      size_t lds = 0;
-      for (auto& p : all) {
-        (p.halo ? halo : plain).push_back(p);
-        if (p.halo) lds = std::max(lds, halo_lds_bytes(p, bf ? 2 : 4, bf ? CONV_BK_BF16 : CONV_BK_F32, kind == 2));
-      }
-      emit_conv_one(halo, out, kind == 1 ? 7 : 8, kclass);
-      if (!halo.empty()) out.back().lds = lds;
-      emit_conv_one(plain, out, kind, kclass);
-    } else {
-      // weight gradient: one launch per code variant (pooled / unpooled with
-      // whole-vector channels, anything else)
-      const int vec = bf ? 8 : 4;
-      std::vector<ConvProb> by[3];
-      for (auto& p : all) {
-        const bool whole = p.O % vec == 0 && p.C % vec == 0;
-        by[!whole ? 0 : p.pool ? 1 : 2].push_back(p);
-      }
-      for (int m = 0; m < 3; ++m) {
-        const size_t before = out.size();
-        emit_conv_one(by[m], out, kind, kclass);
-        if (out.size() > before) out.back().mode = m;
-      }
-    }
-  };
-
-  auto conv_base = [&](const Block& b) {
-    ConvProb p{};
-    p.Nb = B;
-    p.C = b.C;
-    p.H = b.H;
-    p.W = b.W;
-    p.O = b.O;
-    p.KH = b.KH;
-    p.pad = b.pad;
-    p.OH = b.OH;
-    p.OW = b.OW;
-    p.PH = b.PH;
-    p.PW = b.PW;
-    p.pool = b.pool;
-    p.relu = b.relu;
-    p.prev_relu = b.prev_relu;
-    p.splits = 1;
-    return p;
-  };
-
-  // forward levels
-  for (int lv = 0; lv < levels; ++lv) {
-    std::vector<GemmProb> gp;
-    std::vector<ConvProb> cp;
-    bool cat_done = false;
-    for (auto& m : c->models) {
-      if (lv >= (int)m.blocks.size()) continue;
-      Block& b = m.blocks[lv];
-      if (b.kind == 0) {
-        if (b.concat) {
-          if (cat_done) continue;
-          cat_done = true;
-          GemmProb p{};
-          p.A = ptr(c->Xin);
-          p.lda = c->ldxin;
-          p.B = ptr(bf ? catWb : catW32);
-          p.ldb = kin_p;
-          p.M = B;
-          p.N = (int)cat_rows;
-          p.K = (int)in_feat;
-          p.epi = EPI_FWD;
-          p.relu = 1;
-          p.C = ptr(catY);
-          p.ldc = cat_rows;
-          p.CT = ptr(catYT);
-          p.ldct = Bp;
-          p.bias = (const float*)ptr(catb32);
-          gp.push_back(p);
-          continue;
-        }
-        GemmProb p{};
-        p.A = ptr(b.X);
-        p.lda = b.ldx;
-        p.B = ptr(bf ? b.Wb : b.W32);
-        p.ldb = b.ldw;
-        p.M = B;
-        p.N = b.N;
-        p.K = b.K;
-        p.epi = b.last ? EPI_LOGITS : EPI_FWD;
-        p.relu = b.relu;
-        p.C = ptr(b.Y);
-        p.ldc = b.ldy;
-        p.CT = ptr(b.YT);
-        p.ldct = b.ldyt;
-        p.bias = (const float*)ptr(b.b32);
-        gp.push_back(p);
-      } else {
-        ConvProb p = conv_base(b);
-        p.M = b.pool ? B * b.PH * b.PW * 4 : B * b.OH * b.OW;
-        p.N = b.O;
-        p.K = b.KH * b.KH * b.C;
-        p.X = ptr(b.X);
-        p.Wt = ptr(bf ? b.Wb : b.W32);
-        p.ldw = b.ldw;
-        p.bias = (const float*)ptr(b.b32);
-        p.P = ptr(b.Y);
-        p.amax = (uint8_t*)ptr(b.amax);
-        p.PT = ptr(b.YT);
-        p.ldpt = b.ldyt;
-        plan_halo(p, bf, false);
-        cp.push_back(p);
-      }
-    }
-    emit_gemm(gp, fwd, UN_K_GEMM_FWD);
-    emit_conv(cp, fwd, 1, UN_K_CONV_FWD);
-  }
-
-  // softmax-CE
-  std::vector<CeProb> ces;
-  for (size_t mi = 0; mi < c->models.size(); ++mi) {
-    Block& b = c->models[mi].blocks.back();
-    CeProb p{};
-    p.logits = (const float*)ptr(b.Y);
-    p.ldl = b.ldy;
-    p.G = ptr(b.G);
-    p.ldg = b.ldg;
-    p.GT = ptr(b.GT);
-    p.ldgt = b.ldgt;
-    p.C = b.N;
-    p.model = (int)mi;
-    ces.push_back(p);
-  }
-  {
-    size_t po = put(ces.data(), ces.size() * sizeof(CeProb));
-    for (size_t k = 0; k < ces.size(); ++k) {
-      size_t b0 = po + k * sizeof(CeProb);
-      for (size_t f : {offsetof(CeProb, logits), offsetof(CeProb, G), offsetof(CeProb, GT)}) fix.push_back(b0 + f);
-    }
-    c->ce = Launch{5, UN_K_CE, po, NONE, (int)ces.size()};
-  }
-
-  // backward levels, once per parity of the transposed-weight copies: the
-  // dgrad of a level reads copy `par` while the fused update of the same
-  // launch writes the other copy.
-  for (int par = 0; par < 2; ++par)
-  for (int lv = levels - 1; lv >= 0; --lv) {
-    std::vector<GemmProb> gp;
-    std::vector<ConvProb> dp, wp;
-    std::vector<ReduceProb> rp;
-    bool cat_done = false;
-    for (auto& m : c->models) {
-      if (lv >= (int)m.blocks.size()) continue;
-      Block& b = m.blocks[lv];
-      if (b.kind == 0) {
-        // dgrad (not at level 0): gradient at the previous block's output
-        if (lv > 0) {
-          Block& pb = m.blocks[lv - 1];
-          GemmProb p{};
-          p.A = ptr(b.G);
-          p.lda = b.ldg;
-          p.B = ptr(par == 0 ? b.WT : b.WT2);
-          p.ldb = b.ldwt;
-          p.M = B;
-          p.N = b.K;
-          p.K = b.N;
-          p.epi = EPI_DGRAD;
-          p.relu = pb.relu;
-          p.mask = ptr(b.XT);
-          p.ldmask = b.ldxt;
-          if (pb.kind == 0) {
-            p.C = ptr(pb.G);
-            p.ldc = pb.ldg;
-            p.CT = ptr(pb.GT);
-            p.ldct = pb.ldgt;
-          } else {
-            p.C = ptr(pb.G);
-            p.ldc = pb.out_elems_per_sample();
-          }
-          gp.push_back(p);
-        }
-        // wgrad (+ bias gradient through the ones row of XT)
-        if (b.concat) {
-          if (cat_done) continue;
-          cat_done = true;
-          GemmProb p{};
-          p.A = ptr(catGT);
-          p.lda = Bp;
-          p.B = ptr(c->XinT);
-          p.ldb = c->ldxint;
-          p.M = (int)cat_rows;
-          p.N = (int)in_feat + 1;
-          p.K = B;
-          p.epi = EPI_WGRAD;
-          p.nsplit = (int)in_feat;
-          p.C = ptr(catgW);
-          p.ldc = kin_p;
-          p.dbias = (float*)ptr(catgb);
-          p.W = (float*)ptr(catW32);
-          p.Wb = ptr(catWb);
-          p.bmaster = (float*)ptr(catb32);
-          gp.push_back(p);
-          continue;
-        }
-        GemmProb p{};
-        p.A = ptr(b.GT);
-        p.lda = b.ldgt;
-        p.B = ptr(b.XT);
-        p.ldb = b.ldxt;
-        p.M = b.N;
-        p.N = b.K + 1;
-        p.K = B;
-        p.epi = EPI_WGRAD;
-        p.nsplit = b.K;
-        p.C = ptr(b.gW);
-        p.ldc = b.ldw;
-        p.dbias = (float*)ptr(b.gb);
-        p.W = (float*)ptr(b.W32);
-        p.Wb = ptr(b.Wb);
-        p.WT = ptr(par == 0 ? b.WT2 : b.WT);
-        p.ldwt = b.ldwt;
-        p.bmaster = (float*)ptr(b.b32);
-        gp.push_back(p);
-      } else {
-        const int J = b.KH * b.KH * b.C;
-        if (lv > 0) {
-          Block& pb = m.blocks[lv - 1];
-          ConvProb p = conv_base(b);
-          p.M = B * b.H * b.W;
-          p.N = b.C;
-          p.K = b.KH * b.KH * b.O;
-          p.X = ptr(b.X);
-          p.Wt = ptr(b.WT);
-          p.ldw = b.ldwt;
-          p.G = ptr(b.G);
-          p.gam = (const uint8_t*)ptr(b.amax);
-          p.Gprev = ptr(pb.G);
-          plan_halo(p, bf, true);
-          dp.push_back(p);
-        }
-        ConvProb p = conv_base(b);
-        p.M = b.O;
-        p.N = J + 1;
-        p.K = b.pool ? B * b.PH * b.PW * 4 : B * b.OH * b.OW;
-        p.X = ptr(b.X);
-        p.G = ptr(b.G);
-        p.gam = (const uint8_t*)ptr(b.amax);
-        p.ws = (float*)ptr(b.ws);
-        p.ldws = b.ldws;
-        p.splits = b.splits;
-        p.kchunk = b.kchunk;
-        wp.push_back(p);
-        ReduceProb r{};
-        r.ws = (const float*)ptr(b.ws);
-        r.ldws = b.ldws;
-        r.splits = b.splits;
-        r.O = b.O;
-        r.J = J;
-        r.C = b.C;
-        r.gW = (float*)ptr(b.gW);
-        r.ldgw = b.ldw;
-        r.gb = (float*)ptr(b.gb);
-        r.W = (float*)ptr(b.W32);
-        r.Wb = ptr(b.Wb);
-        r.WT = ptr(b.WT);  // conv: the dgrad launch of this level has completed
-        r.ldwt = b.ldwt;
-        r.bmaster = (float*)ptr(b.b32);
-        rp.push_back(r);
-      }
-    }
-    emit_gemm(gp, bwd[par], UN_K_GEMM_BWD);
-    emit_conv(dp, bwd[par], 2, UN_K_CONV_DGRAD);
-    emit_conv(wp, bwd[par], 3, UN_K_CONV_WGRAD);
-    if (!rp.empty()) {
-      std::vector<int32_t> map;
-      for (size_t k = 0; k < rp.size(); ++k) {
-        rp[k].blk_base = (int32_t)map.size();
-        const int nb = cdiv((int64_t)rp[k].O * (rp[k].J + 1), REDUCE_BLOCK);
-        for (int t = 0; t < nb; ++t) map.push_back((int32_t)k);
-      }
-      size_t po = put(rp.data(), rp.size() * sizeof(ReduceProb));
-      for (size_t k = 0; k < rp.size(); ++k) {
-        size_t b0 = po + k * sizeof(ReduceProb);
-        for (size_t f : {offsetof(ReduceProb, ws), offsetof(ReduceProb, gW), offsetof(ReduceProb, gb),
-                         offsetof(ReduceProb, W), offsetof(ReduceProb, Wb), offsetof(ReduceProb, WT),
-                         offsetof(ReduceProb, bmaster)})
-          fix.push_back(b0 + f);
-      }
-      size_t mo = put(map.data(), map.size() * 4);
-      bwd[par].push_back(Launch{4, UN_K_OTHER, po, mo, (int)map.size()});
-    }
-  }
-
-  // Shadow refresh (after un_set_params / initialisation): rewrite the bf16
-  // shadow and transposed copy `pass` of every weight from the fp32 master.
-  for (int pass = 0; pass < 2; ++pass) {
-    std::vector<SgdTensor> ts;
-    std::vector<int32_t> map;
-    auto add = [&](SgdTensor t) {
-      t.tiles_r = cdiv(t.R, SGD_TILE);
-      t.tiles_c = cdiv(t.Cc, SGD_TILE);
-      t.tile_base = (int32_t)map.size();
-      const int nt = t.J * t.tiles_r * t.tiles_c;
-      for (int k = 0; k < nt; ++k) map.push_back((int32_t)ts.size());
-      ts.push_back(t);
-    };
-    for (auto& m : c->models)
-      for (auto& b : m.blocks) {
-        SgdTensor w{};
-        w.W = (float*)ptr(b.W32);
-        w.Wb = ptr(b.Wb);
-        w.WT = ptr(pass == 1 && b.WT2 != NONE ? b.WT2 : b.WT);
-        w.ldw = b.ldw;
-        w.ldwt = b.ldwt;
-        w.R = b.rows;
-        if (b.kind == 0) {
-          w.J = 1;
-          w.Cc = b.K;
-        } else {
-          w.J = b.KH * b.KH;
-          w.Cc = b.C;
-        }
-        add(w);
-      }
-    size_t po = put(ts.data(), ts.size() * sizeof(SgdTensor));
-    for (size_t k = 0; k < ts.size(); ++k) {
-      size_t b0 = po + k * sizeof(SgdTensor);
-      for (size_t f : {offsetof(SgdTensor, W), offsetof(SgdTensor, G), offsetof(SgdTensor, Wb), offsetof(SgdTensor, WT)})
-        fix.push_back(b0 + f);
-    }
-    size_t mo = put(map.data(), map.size() * 4);
-    c->refresh[pass] = Launch{6, UN_K_SGD, po, mo, (int)map.size()};
-  }
-
-  // --- allocate the arena: buffers + tables
-  const size_t tables_off = A.take(host_tables.size());
+  // --- allocate the arena: buffers + tables (room for the tables of any
+  // active subset, which are never larger than twice the full set's)
+  c->tables_cap = 2 * T.host.size() + ((size_t)1 << 20);
+  c->tables_off = A.take(c->tables_cap);
   c->bytes = A.top;
   hipError_t e = hipMalloc((void**)&c->base, c->bytes);
   if (e != hipSuccess) {
     c->base = nullptr;
     return fail(nullptr, UN_ERR_OOM, "hipMalloc of " + std::to_string(c->bytes) + " bytes failed: " + hipGetErrorString(e));
   }
-  // relocate encoded pointers
-  for (size_t f : fix) {
-    uintptr_t v;
-    memcpy(&v, host_tables.data() + f, sizeof(v));
-    if (v != 0) v = (uintptr_t)(c->base + (v - 1));
-    memcpy(host_tables.data() + f, &v, sizeof(v));
-  }
-  auto relocate = [&](Launch& l) {
-    l.probs += tables_off;
-    if (l.map != NONE) l.map += tables_off;
-  };
-  for (auto& l : fwd) relocate(l);
-  for (int p = 0; p < 2; ++p)
-    for (auto& l : bwd[p]) relocate(l);
-  relocate(c->ce);
-  relocate(c->refresh[0]);
-  relocate(c->refresh[1]);
-  c->fwd = fwd;
-  c->bwd[0] = bwd[0];
-  c->bwd[1] = bwd[1];
-
   HIPCHK(c, hipMemsetAsync(c->base, 0, c->bytes, c->stream));
-  HIPCHK(c, hipMemcpyAsync(c->base + tables_off, host_tables.data(), host_tables.size(), hipMemcpyHostToDevice,
-                           c->stream));
+  {
+    un_status st = install_tables(c, T);
+    if (st != UN_OK) return st;
+  }
   // ones rows of the transposed inputs (bias-gradient column of the wgrad GEMMs)
   std::vector<uint16_t> ones16((size_t)Bp, 0x3F80);
   std::vector<float> ones32((size_t)Bp, 1.0f);
@@ -1375,7 +1459,39 @@ un_status un_step(un_ctx* c, float lr, float* losses) {
   if (losses) {
     HIPCHK(c, hipMemcpyAsync(losses, c->base + c->losses_dev, c->models.size() * 4, hipMemcpyDeviceToHost, c->stream));
     HIPCHK(c, hipStreamSynchronize(c->stream));
+    for (size_t i = 0; i < c->models.size(); ++i)
+      if (!c->active[i]) losses[i] = std::nanf("");
   }
+  return UN_OK;
+}
+
+un_status un_set_active(un_ctx* c, const uint8_t* mask) {
+  CHECK_CTX(c);
+  if (!mask) return fail(c, UN_ERR_INVALID, "mask is NULL");
+  std::vector<char> act(c->models.size());
+  bool any = false;
+  for (size_t i = 0; i < act.size(); ++i) {
+    act[i] = mask[i] != 0;
+    any = any || act[i];
+  }
+  if (!any) return fail(c, UN_ERR_INVALID, "no active model");
+  if (act == c->active) return UN_OK;
+  HIPCHK(c, hipStreamSynchronize(c->stream));  // the current tables are no longer in use
+  const std::vector<char> before = c->active;
+  c->active = act;
+  Tables T;
+  build_tables(c, T);
+  un_status st = install_tables(c, T);
+  if (st != UN_OK) {
+    c->active = before;
+    return st;
+  }
+  // Models that sat out some steps kept their transposed weight copy in the
+  // buffer of that time; rewrite every model's current copies from the master.
+  st = refresh_shadows(c);
+  if (st != UN_OK) return st;
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  c->grads_valid = false;
   return UN_OK;
 }
 
@@ -1404,6 +1520,7 @@ un_status un_get_grads(un_ctx* c, int32_t i, float* dst, size_t cap, size_t* n) 
   if (!dst) return UN_OK;
   if (!c->stepped) return fail(c, UN_ERR_STATE, "no step has run yet");
   if (!c->grads_valid) return fail(c, UN_ERR_STATE, "the last step did not keep gradients (see un_keep_grads)");
+  if (!c->active[i]) return fail(c, UN_ERR_STATE, "model " + std::to_string(i) + " was not active in the last step");
   if (cap < np) return fail(c, UN_ERR_BUFSIZE, "buffer too small");
   return read_tensors(c, i, true, dst);
 }

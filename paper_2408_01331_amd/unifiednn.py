@@ -25,9 +25,9 @@ OPS = {"linear": 0, "conv": 1, "relu": 2, "pool": 3, "flatten": 4}
 KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad", "ce", "sgd", "other"]
 
 # Every symbol the header declares.
-EXPORTS = ["un_create", "un_load_batch", "un_load_batch_device", "un_step", "un_get_params", "un_set_params",
-           "un_get_grads", "un_keep_grads", "un_param_count", "un_arena_bytes", "un_sync", "un_get_stream", "un_profile_enable",
-           "un_profile_read", "un_destroy", "un_last_error"]
+EXPORTS = ["un_create", "un_load_batch", "un_load_batch_device", "un_step", "un_set_active", "un_get_params",
+           "un_set_params", "un_get_grads", "un_keep_grads", "un_param_count", "un_arena_bytes", "un_sync", "un_get_stream",
+           "un_profile_enable", "un_profile_read", "un_destroy", "un_last_error"]
 
 
 class un_layer(ctypes.Structure):
@@ -69,6 +69,7 @@ def lib():
             "un_load_batch": (ctypes.c_int, [P, f, i32]),
             "un_load_batch_device": (ctypes.c_int, [P, P, P]),
             "un_step": (ctypes.c_int, [P, ctypes.c_float, f]),
+            "un_set_active": (ctypes.c_int, [P, ctypes.POINTER(ctypes.c_uint8)]),
             "un_get_params": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t, c_size_p]),
             "un_set_params": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t]),
             "un_get_grads": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t, c_size_p]),
@@ -148,6 +149,13 @@ def un_step(ctx, lr, n_models=None):
     out = np.zeros(n_models, dtype=np.float32)
     _check(lib().un_step(ctx, ctypes.c_float(lr), _fp(out)), ctx)
     return out
+
+
+def un_set_active(ctx, mask, n_models):
+    m = np.ascontiguousarray(np.asarray(mask, dtype=bool), dtype=np.uint8)
+    if m.shape != (n_models,):
+        raise ValueError(f"mask must have one entry per model ({n_models}), got shape {m.shape}")
+    _check(lib().un_set_active(ctx, m.ctypes.data_as(ctypes.POINTER(ctypes.c_uint8))), ctx)
 
 
 def un_param_count(ctx, i):
@@ -259,6 +267,9 @@ class Hybrid:
 
     def step(self, lr, losses=True):
         return un_step(self.ctx, lr, self.n if losses else None)
+
+    def set_active(self, mask):
+        un_set_active(self.ctx, mask, self.n)
 
     def get_params(self, i):
         return un_get_params(self.ctx, i)
