@@ -14,8 +14,13 @@
 // which other models share the launch.
 #include <hip/hip_runtime.h>
 
+#include <type_traits>
+
 #include "internal.h"
 
+#ifndef UN_GEMM_DEPTH
+#define UN_GEMM_DEPTH 2
+#endif
 #ifndef UN_LDS_PAD_CHUNKS
 #define UN_LDS_PAD_CHUNKS 1
 #endif
@@ -26,6 +31,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 // ---------------------------------------------------------------------------
 // Element helpers
@@ -203,12 +209,167 @@ __device__ __forceinline__ void mma_loop1(L& ld, int kb0, int kb1, T* smem,
   }
 }
 
+// The grouped GEMM's MFMA policy. bf16 runs v_mfma_f32_32x32x16_bf16, which
+// sustains about twice the rate of the 16x16x32 form on gfx950 (2.2 vs 1.2
+// PFLOP/s with register operands): each of the 4 waves owns a (BM/2) x (BN/2)
+// tile of 32x32 blocks, acc[I][J][e] holding
+//   C[wm + 32I + 8(e/4) + 4(lane/32) + e%4][wn + 32J + lane%32].
+// fp32 keeps the 16x16x4 blocks of mma_block. for_groups visits every run of
+// four consecutive rows of one column a lane holds: f(row, col, v[4]) in tile
+// coordinates. CLD is the row stride (floats) of the epilogue's LDS tile,
+// chosen so that a wave's accumulator writes hit 64 distinct banks.
+template <typename T, int BM, int BN, int BK> struct GemmMma;
+
+template <int BM, int BN, int BK>
+struct GemmMma<bf16_t, BM, BN, BK> {
+  static constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;
+  static constexpr int LDK = Tile<bf16_t, BM, BN, BK>::LDK;
+  static constexpr int CLD = BN + 8;
+  static_assert(BK % 16 == 0, "BK must be a multiple of 16");
+  using Acc = f32x16[FM][FN];
+  __device__ __forceinline__ static void zero(Acc& acc) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+  }
+  __device__ __forceinline__ static void block(const bf16_t* sA, const bf16_t* sB, Acc& acc) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = (wave >> 1) * WM, wn = (wave & 1) * WN;
+    const int lr = lane & 31, lg = lane >> 5;
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 16) {
+      bf16x8 a[FM], b[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        a[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(sA + (wm + 32 * i + lr) * LDK + kk + 8 * lg));
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        b[j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(sB + (wn + 32 * j + lr) * LDK + kk + 8 * lg));
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  template <class F>
+  __device__ __forceinline__ static void for_groups(const Acc& acc, F&& f) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = (wave >> 1) * WM, wn = (wave & 1) * WN;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          float v[4] = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+          f(wm + 32 * i + 8 * q + 4 * (lane >> 5), wn + 32 * j + (lane & 31), v);
+        }
+  }
+};
+
+template <int BM, int BN, int BK>
+struct GemmMma<float, BM, BN, BK> {
+  using TL = Tile<float, BM, BN, BK>;
+  static constexpr int CLD = BN + 4;
+  using Acc = f32x4[TL::FM][TL::FN];
+  __device__ __forceinline__ static void zero(Acc& acc) {
+#pragma unroll
+    for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  __device__ __forceinline__ static void block(const float* sA, const float* sB, Acc& acc) {
+    mma_block<float, BM, BN, BK>(sA, sB, acc);
+  }
+  template <class F>
+  __device__ __forceinline__ static void for_groups(const Acc& acc, F&& f) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
+#pragma unroll
+    for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+      for (int j = 0; j < TL::FN; ++j) {
+        float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+        f(wm + 16 * i + 4 * (lane >> 4), wn + 16 * j + (lane & 15), v);
+      }
+  }
+};
+
+// The GEMM's k loop over nkb k-blocks: LDS double-buffered, and the global
+// loads run DEPTH (1 or 2) k-blocks ahead in the loaders' two register slots,
+// so a block's load latency is covered by DEPTH blocks of MFMA work. Loads
+// past the last block re-read it (harmless, and branch-free so that the
+// waits stay exact). One barrier per k-block.
+template <typename T, int BM, int BN, int BK, int DEPTH, class MM, class LA, class LB>
+__device__ __forceinline__ void gemm_loop(LA& la, LB& lb, int nkb, T* smem, typename MM::Acc& acc) {
+  using TL = Tile<T, BM, BN, BK>;
+  constexpr int STAGE = TL::A_ELEMS + TL::B_ELEMS;
+  if (nkb <= 0) return;
+  if constexpr (DEPTH == 1) {
+    la.template load<0>(0);
+    lb.template load<0>(0);
+    la.template store<0>(smem);
+    lb.template store<0>(smem + TL::A_ELEMS);
+    __syncthreads();
+    for (int kb = 0; kb < nkb; ++kb) {
+      const int cur = kb & 1;
+      const int nxt = min(kb + 1, nkb - 1);
+      la.template load<0>(nxt);
+      lb.template load<0>(nxt);
+      const T* st = smem + cur * STAGE;
+      MM::block(st, st + TL::A_ELEMS, acc);
+      if (kb + 1 < nkb) {
+        T* d = smem + (cur ^ 1) * STAGE;
+        la.template store<0>(d);
+        lb.template store<0>(d + TL::A_ELEMS);
+      }
+      __syncthreads();
+    }
+  } else {
+    la.template load<0>(0);
+    lb.template load<0>(0);
+    la.template load<1>(min(1, nkb - 1));
+    lb.template load<1>(min(1, nkb - 1));
+    la.template store<0>(smem);
+    lb.template store<0>(smem + TL::A_ELEMS);
+    __syncthreads();
+    // Block kb sits in LDS buffer kb & 1 and came through register slot kb & 1.
+    // Inside the loop every load and store is unconditional (the copies made
+    // past the last block are never read), so the compiler's wait counts
+    // stay exact and block kb + 2 stays in flight across block kb's MFMAs.
+    auto step = [&](auto slot, int kb) {
+      constexpr int S = decltype(slot)::value;
+      const int ahead = min(kb + 2, nkb - 1);
+      la.template load<S>(ahead);
+      lb.template load<S>(ahead);
+      const T* st = smem + S * STAGE;
+      MM::block(st, st + TL::A_ELEMS, acc);
+      T* d = smem + (S ^ 1) * STAGE;
+      la.template store<S ^ 1>(d);
+      lb.template store<S ^ 1>(d + TL::A_ELEMS);
+      __syncthreads();
+    };
+    int kb = 0;
+    for (; kb + 1 < nkb; kb += 2) {
+      step(std::integral_constant<int, 0>{}, kb);
+      step(std::integral_constant<int, 1>{}, kb + 1);
+    }
+    if (kb < nkb) {  // odd count: the last block, from buffer 0
+      MM::block(smem, smem + TL::A_ELEMS, acc);
+      __syncthreads();
+    }
+  }
+}
+
 // LDS of one MFMA kernel: the double-buffered operand tiles, reused by the
-// epilogue as an fp32 [BM][BN + 4] tile.
+// epilogue as an fp32 [BM][BN + 8] tile.
 template <typename T, int BM, int BN, int BK>
 struct Smem {
   using TL = Tile<T, BM, BN, BK>;
-  static constexpr int CLD = BN + 4;
+  static constexpr int CLD = BN + 8;
   static constexpr size_t MAIN = 2 * (size_t)(TL::A_ELEMS + TL::B_ELEMS) * sizeof(T);
   static constexpr size_t EPI = (size_t)BM * CLD * sizeof(float);
   static constexpr size_t BYTES = MAIN > EPI ? MAIN : EPI;
@@ -843,17 +1004,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
   const int tn = local / tiles_m, tm = local - tn * tiles_m;   // m fastest: neighbours share B
   const int m0 = tm * BM, n0 = tn * BN;
 
-  f32x4 acc[TL::FM][TL::FN];
-#pragma unroll
-  for (int i = 0; i < TL::FM; ++i)
-#pragma unroll
-    for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  using MM = GemmMma<T, BM, BN, BK>;
+  typename MM::Acc acc;
+  MM::zero(acc);
 
   RowLoader<T, BM, BK> la;
   RowLoader<T, BN, BK> lb;
   la.init((const T*)p.A + (int64_t)m0 * p.lda, p.lda, p.M - m0, p.K);
   lb.init((const T*)p.B + (int64_t)n0 * p.ldb, p.ldb, p.N - n0, p.K);
-  mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
+  gemm_loop<T, BM, BN, BK, UN_GEMM_DEPTH, MM>(la, lb, (p.K + BK - 1) / BK, (T*)smem, acc);
 
   // Weight gradient with the SGD update fused: the master-weight loads of
   // this thread's float4 chunks of W[m][n..n+3] are issued first, so their
@@ -870,20 +1029,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
   }
 
   // Epilogue 1: per-element work (bias, ReLU, ReLU' mask) in registers, then
-  // the fp32 tile to LDS (rows of BN + 4 floats: float4-aligned).
-  constexpr int CLD = BN + 4;
+  // the fp32 tile to LDS (rows of CLD floats: float4-aligned).
+  constexpr int CLD = MM::CLD;
+  static_assert(CLD <= SM::CLD, "epilogue tile exceeds its LDS");
   float* sC = (float*)smem;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
   const int epi = p.epi;
-#pragma unroll
-  for (int i = 0; i < TL::FM; ++i) {
-    const int rl = wm + 16 * i + 4 * (lane >> 4), mb = m0 + rl;
-    const int nv = max(0, min(4, p.M - mb));
-#pragma unroll
-    for (int j = 0; j < TL::FN; ++j) {
-      const int cl = wn + 16 * j + (lane & 15), n = n0 + cl;
-      float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+  MM::for_groups(acc, [&](int rl, int cl, float (&v)[4]) {
+      const int mb = m0 + rl, n = n0 + cl;
+      const int nv = max(0, min(4, p.M - mb));
       if (n < p.N && nv > 0) {
         if (epi == EPI_FWD || epi == EPI_LOGITS) {
           const float b = p.bias[n];
@@ -905,8 +1058,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) sC[(rl + r) * CLD + cl] = v[r];
-    }
-  }
+  });
   __syncthreads();
 
   if (epi != EPI_WGRAD) {
