@@ -112,6 +112,14 @@ un_status un_load_batch(un_ctx* ctx, const float* x, const int32_t* y);
  * labels are range-checked after a device-to-host copy. */
 un_status un_load_batch_device(un_ctx* ctx, const float* x_dev, const int32_t* y_dev);
 
+/* Labels per model for the batch already loaded (Algorithm 2 gives every
+ * sub-model its own batches; the input x stays shared). y is host int32
+ * [N][batch], row i holding model i's labels, each in [0, num_classes of
+ * model i) or UN_ERR_RANGE (nothing changes). They replace the labels of the
+ * last un_load_batch until the next un_load_batch, which goes back to one
+ * label row for all models. Synchronous. UN_ERR_STATE before any batch. */
+un_status un_load_labels(un_ctx* ctx, const int32_t* y);
+
 /* One fused training step of all N models on the loaded batch (Algorithm 2's
  * loop body for every sub-model): forward, per-model mean softmax
  * cross-entropy, backward, per-model SGD with learning rate lr.
@@ -122,6 +130,14 @@ un_status un_load_batch_device(un_ctx* ctx, const float* x_dev, const int32_t* y
  * weight-gradient kernels; gradients are stored only when kept (un_keep_grads).
  * Errors: UN_ERR_STATE (no batch loaded), UN_ERR_INVALID (lr not finite). */
 un_status un_step(un_ctx* ctx, float lr, float* losses);
+
+/* As un_step with a learning rate per model: model i updates with lrs[i]
+ * (host fp32 [N], each finite, else UN_ERR_INVALID and nothing runs). The
+ * paper indexes the rate by the batch (Algorithm 2) and gives every sub-model
+ * its own hyper-parameters; a schedule eta_t is this call with the step's
+ * rates. The rates are copied when the call returns (the host array may be
+ * reused at once); inactive models ignore theirs. */
+un_status un_step_lr(un_ctx* ctx, const float* lrs, float* losses);
 
 /* Active set of the following steps (Trainer section: a scheduler - first
  * come first serve, priority, shortest job first, round robin - decides which

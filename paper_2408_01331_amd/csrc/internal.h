@@ -38,6 +38,7 @@ struct GemmProb {
   int32_t epi, relu;
   int32_t tiles_n;
   int32_t nsplit;
+  int32_t model;              // WGRAD: the model whose learning rate applies (single-model problems)
   void* C;                    // WGRAD: gradient dW [m][ldc] (stored only when gradients are kept)
   int64_t ldc;
   void* CT;
@@ -55,6 +56,7 @@ struct GemmProb {
   void* WT;
   int64_t ldwt;
   float* bmaster;
+  const int32_t* row_model;   // WGRAD of the concatenated first layers: model of each row m (else null)
 };
 
 // ---------------------------------------------------------------------------
@@ -111,6 +113,7 @@ struct ReduceProb {
   int64_t ldws;
   int32_t splits, O, J, C;    // J = KH*KW*C weight columns (+1 bias column in ws)
   int32_t blk_base;
+  int32_t model;
   float* gW;
   int64_t ldgw;
   float* gb;
@@ -160,8 +163,11 @@ struct SgdTensor {
 // `tile_map` holds one (problem index, tile index within the problem) pair of
 // int32 per workgroup, in launch order; a pair with problem -1 is padding and
 // its workgroup does nothing.
+// Learning rates: `lr` for every model, or per model lrv[model] when lrv is
+// not null (device array). Labels: labels[b] for every model, or
+// labels[model * B + b] when per_model_labels is set.
 hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
-                       bool keep_grads, hipStream_t s);
+                       const float* lrv, bool keep_grads, hipStream_t s);
 hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                            hipStream_t s);
 hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
@@ -174,8 +180,10 @@ hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const i
 hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                             size_t lds_bytes, hipStream_t s);
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
+                         const float* lrv,
                          bool keep_grads, hipStream_t s);
-hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, const int32_t* labels, int B,
+hipError_t launch_set_values(float* dst, const float* vals, int n, hipStream_t s);
+hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, const int32_t* labels, bool per_model_labels, int B,
                      float* partial, float* losses, hipStream_t s);
 hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int ntiles, float lr,
                       bool use_grad, hipStream_t s);

@@ -993,7 +993,7 @@ __device__ __forceinline__ void store_cols(const float* sC, OT* CT, int64_t ldct
 template <typename T, int BM, int BN, int BK>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(const GemmProb* __restrict__ probs,
                                                    const int32_t* __restrict__ tile_map, float lr,
-                                                   int keep_grads) {
+                                                   const float* __restrict__ lrv, int keep_grads) {
   using TL = Tile<T, BM, BN, BK>;
   using SM = Smem<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[SM::BYTES];
@@ -1080,13 +1080,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
     const int idx = threadIdx.x + 256 * q, r = idx / CPR, cc = idx - r * CPR;
     const int m = m0 + r, n = n0 + cc * 4;
     if (m >= p.M || n > ns) continue;
+    // this row's model: its own learning rate when rates are per model
+    const float lr_m = lrv ? lrv[p.row_model ? p.row_model[m] : p.model] : lr;
     float* s = sC + r * CLD + cc * 4;
     const int64_t base = (int64_t)m * p.ldc + n;
     if (n + 4 <= ns) {
       const f32x4 g = *(const f32x4*)s;
       if (keep_grads) *(gptr<f32x4>)((float*)p.C + base) = g;
-      const f32x4 w = f32x4{fmaf(-lr, g[0], w0[q][0]), fmaf(-lr, g[1], w0[q][1]), fmaf(-lr, g[2], w0[q][2]),
-                            fmaf(-lr, g[3], w0[q][3])};
+      const f32x4 w = f32x4{fmaf(-lr_m, g[0], w0[q][0]), fmaf(-lr_m, g[1], w0[q][1]), fmaf(-lr_m, g[2], w0[q][2]),
+                            fmaf(-lr_m, g[3], w0[q][3])};
       *(gptr<f32x4>)(p.W + base) = w;
       if (p.Wb) {
         u32x2 hb;
@@ -1100,13 +1102,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
         const float g = s[e];
         if (n + e < ns) {
           if (keep_grads) ((float*)p.C)[base + e] = g;
-          const float w = fmaf(-lr, g, p.W[base + e]);
+          const float w = fmaf(-lr_m, g, p.W[base + e]);
           p.W[base + e] = w;
           if (p.Wb) ((bf16_t*)p.Wb)[base + e] = f2bf(w);
           s[e] = w;
         } else {
           if (keep_grads) p.dbias[m] = g;
-          p.bmaster[m] = fmaf(-lr, g, p.bmaster[m]);
+          p.bmaster[m] = fmaf(-lr_m, g, p.bmaster[m]);
         }
       }
     }
@@ -1595,8 +1597,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 template <typename T>
 __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* __restrict__ probs,
                                                               const int32_t* __restrict__ blk_prob, float lr,
-                                                              int keep_grads) {
+                                                              const float* __restrict__ lrv, int keep_grads) {
   const ReduceProb& p = probs[blk_prob[blockIdx.x]];
+  if (lrv) lr = lrv[p.model];
   const int64_t e = (int64_t)(blockIdx.x - p.blk_base) * REDUCE_BLOCK + threadIdx.x;
   const int J1 = p.J + 1;
   if (e >= (int64_t)p.O * J1) return;
@@ -1640,10 +1643,12 @@ __device__ __forceinline__ float wave_sum(float v) {
 // ce_finish_kernel adds the chunks in order.
 template <typename T>
 __global__ __launch_bounds__(CE_ROWS * CE_LANES) void ce_rows_kernel(const CeProb* __restrict__ probs,
-                                                                     const int32_t* __restrict__ y, int B,
+                                                                     const int32_t* __restrict__ labels,
+                                                                     int per_model_labels, int B,
                                                                      float* __restrict__ partial, int nchunks) {
   __shared__ float rowloss[CE_ROWS];
   const CeProb& p = probs[blockIdx.y];
+  const int32_t* y = labels + (per_model_labels ? (int64_t)p.model * B : 0);
   const int rl = threadIdx.x / CE_LANES, sub = threadIdx.x % CE_LANES;
   const int b = blockIdx.x * CE_ROWS + rl;
   const int C = p.C;
@@ -1762,14 +1767,14 @@ __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, 
 // Launch wrappers
 // ---------------------------------------------------------------------------
 hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
-                       bool keep_grads, hipStream_t s) {
+                       const float* lrv, bool keep_grads, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   if (bf16)
     hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16>), dim3(ntiles), dim3(256), 0, s, probs,
-                       tile_map, lr, (int)keep_grads);
+                       tile_map, lr, lrv, (int)keep_grads);
   else
     hipLaunchKernelGGL((gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, GEMM_BK_F32>), dim3(ntiles), dim3(256), 0, s, probs,
-                       tile_map, lr, (int)keep_grads);
+                       tile_map, lr, lrv, (int)keep_grads);
   return hipGetLastError();
 }
 
@@ -1853,27 +1858,48 @@ hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const i
 }
 
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
-                         bool keep_grads, hipStream_t s) {
+                         const float* lrv, bool keep_grads, hipStream_t s) {
   if (nblocks <= 0) return hipSuccess;
   if (bf16)
-    hipLaunchKernelGGL(reduce_kernel<bf16_t>, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob, lr,
+    hipLaunchKernelGGL(reduce_kernel<bf16_t>, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob, lr, lrv,
                        (int)keep_grads);
   else
-    hipLaunchKernelGGL(reduce_kernel<float>, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob, lr,
+    hipLaunchKernelGGL(reduce_kernel<float>, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob, lr, lrv,
                        (int)keep_grads);
   return hipGetLastError();
 }
 
-hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, const int32_t* labels, int B, float* partial,
-                     float* losses, hipStream_t s) {
+// Values passed by value in the kernel arguments, SETV_CHUNK per launch: no
+// host buffer has to outlive the call.
+constexpr int SETV_CHUNK = 256;
+struct SetValues {
+  float v[SETV_CHUNK];
+};
+__global__ void set_values_kernel(float* __restrict__ dst, SetValues vals, int n) {
+  const int i = threadIdx.x;
+  if (i < n) dst[i] = vals.v[i];
+}
+
+hipError_t launch_set_values(float* dst, const float* vals, int n, hipStream_t s) {
+  for (int i0 = 0; i0 < n; i0 += SETV_CHUNK) {
+    const int k = n - i0 < SETV_CHUNK ? n - i0 : SETV_CHUNK;
+    SetValues sv{};
+    for (int i = 0; i < k; ++i) sv.v[i] = vals[i0 + i];
+    hipLaunchKernelGGL(set_values_kernel, dim3(1), dim3(SETV_CHUNK), 0, s, dst + i0, sv, k);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, const int32_t* labels, bool per_model_labels, int B,
+                     float* partial, float* losses, hipStream_t s) {
   if (nprobs <= 0) return hipSuccess;
   const int nchunks = (B + CE_ROWS - 1) / CE_ROWS;
   if (bf16)
-    hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nprobs), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels, B, partial,
-                       nchunks);
+    hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nprobs), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels,
+                       (int)per_model_labels, B, partial, nchunks);
   else
-    hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nprobs), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels, B, partial,
-                       nchunks);
+    hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nprobs), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels,
+                       (int)per_model_labels, B, partial, nchunks);
   hipLaunchKernelGGL(ce_finish_kernel, dim3((nprobs + 63) / 64), dim3(64), 0, s, probs, partial, nchunks, nprobs,
                      B, losses);
   return hipGetLastError();

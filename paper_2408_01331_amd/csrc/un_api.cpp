@@ -102,6 +102,9 @@ struct un_ctx {
   // fixed buffers
   size_t xstage = NONE, ydev = NONE, losses_dev = NONE, ce_partial = NONE, Xin = NONE, XinT = NONE;
   size_t XinC = NONE;  // NHWC input with channels padded to a 16-byte multiple (first convs only)
+  size_t lr_dev = NONE;          // per-model learning rates of the current un_step_lr call
+  const float* lrv = nullptr;    // lr_dev while such a step is being launched, else null (one rate)
+  bool labels_per_model = false; // ydev holds N rows of B labels (un_load_labels) instead of one
   int in_cs = 0;       // stored channels of XinC
   int64_t ldxin = 0, ldxint = 0;
   // schedule
@@ -116,6 +119,7 @@ struct un_ctx {
     std::vector<int64_t> cat_off;  // their first row in it (-1: not in it)
     size_t catW32 = NONE, catb32 = NONE, catgW = NONE, catgb = NONE, catWb = NONE, catY = NONE, catYT = NONE,
            catGT = NONE;
+    size_t cat_row_model = NONE;  // int32 per concatenated row: the model owning it
   } plan;
   int wt_cur = 0;                     // which transposed copy the next dgrad reads
   bool keep_grads = false, grads_valid = false;
@@ -509,7 +513,7 @@ static void build_tables(un_ctx* c, Tables& T) {
       for (size_t f : {offsetof(GemmProb, A), offsetof(GemmProb, B), offsetof(GemmProb, C), offsetof(GemmProb, CT),
                        offsetof(GemmProb, bias), offsetof(GemmProb, mask), offsetof(GemmProb, dbias),
                        offsetof(GemmProb, W), offsetof(GemmProb, Wb), offsetof(GemmProb, WT),
-                       offsetof(GemmProb, bmaster)})
+                       offsetof(GemmProb, bmaster), offsetof(GemmProb, row_model)})
         fix.push_back(b0 + f);
     }
     size_t mo = put(map.data(), map.size() * 4);
@@ -758,6 +762,7 @@ static void build_tables(un_ctx* c, Tables& T) {
             p.W = (float*)ptr(sub(catW32, run.first * kin_p * 4));
             p.Wb = ptr(sub(catWb, run.first * kin_p * 2));
             p.bmaster = (float*)ptr(sub(catb32, run.first * 4));
+            p.row_model = (const int32_t*)ptr(sub(c->plan.cat_row_model, run.first * 4));
             gp.push_back(p);
           }
           continue;
@@ -780,6 +785,7 @@ static void build_tables(un_ctx* c, Tables& T) {
         p.WT = ptr(par == 0 ? b.WT2 : b.WT);
         p.ldwt = b.ldwt;
         p.bmaster = (float*)ptr(b.b32);
+        p.model = b.model;
         gp.push_back(p);
       } else {
         const int J = b.KH * b.KH * b.C;
@@ -825,6 +831,7 @@ static void build_tables(un_ctx* c, Tables& T) {
         r.WT = ptr(b.WT);  // conv: the dgrad launch of this level has completed
         r.ldwt = b.ldwt;
         r.bmaster = (float*)ptr(b.b32);
+        r.model = b.model;
         rp.push_back(r);
       }
     }
@@ -939,7 +946,8 @@ static un_status plan_and_alloc(un_ctx* c) {
   const int64_t in_feat = (int64_t)c->in_c * c->in_h * c->in_w;
 
   c->xstage = A.take((size_t)B * in_feat * 4);
-  c->ydev = A.take((size_t)B * 4);
+  c->ydev = A.take(c->models.size() * (size_t)B * 4);  // one row of labels, or one per model
+  c->lr_dev = A.take(c->models.size() * 4);
   c->losses_dev = A.take(c->models.size() * 4);
   c->ce_partial = A.take(c->models.size() * (size_t)cdiv(B, CE_ROWS) * 4);
   bool any_linear0 = false, any_conv0 = false;
@@ -991,6 +999,7 @@ static un_status plan_and_alloc(un_ctx* c) {
     catY = A.take((size_t)B * cat_rows * es);
     catYT = A.take((size_t)cat_rows * Bp * es);
     catGT = A.take((size_t)cat_rows * Bp * es);
+    c->plan.cat_row_model = A.take((size_t)cat_rows * 4);
   }
 
   // --- per block buffers
@@ -1142,6 +1151,15 @@ static un_status plan_and_alloc(un_ctx* c) {
                           c->stream);
   };
   if (c->XinT != NONE) HIPCHK(c, set_ones_row(c->XinT, in_feat, Bp));
+  std::vector<int32_t> row_model((size_t)cat_rows);
+  if (!cat.empty()) {
+    for (size_t k = 0; k < cat.size(); ++k) {
+      const int64_t r1 = k + 1 < cat.size() ? cat_off[cat[k + 1]] : cat_rows;
+      for (int64_t r = cat_off[cat[k]]; r < r1; ++r) row_model[(size_t)r] = cat[k];
+    }
+    HIPCHK(c, hipMemcpyAsync(c->base + c->plan.cat_row_model, row_model.data(), row_model.size() * 4,
+                             hipMemcpyHostToDevice, c->stream));
+  }
   // the padding channels of XinC are written here only, once
   if (c->XinC != NONE)
     HIPCHK(c, hipMemsetAsync(c->base + c->XinC, 0, (size_t)B * c->in_h * c->in_w * c->in_cs * es, c->stream));
@@ -1284,7 +1302,7 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
   hipError_t e = hipSuccess;
   switch (l.kind) {
     case 0:
-      e = launch_gemm(c->bf16, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->keep_grads,
+      e = launch_gemm(c->bf16, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->lrv, c->keep_grads,
                       c->stream);
       break;
     case 1:
@@ -1302,11 +1320,11 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
                            c->stream);
       break;
     case 4:
-      e = launch_reduce(c->bf16, c->at<ReduceProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->keep_grads,
+      e = launch_reduce(c->bf16, c->at<ReduceProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->lrv, c->keep_grads,
                         c->stream);
       break;
     case 5:
-      e = launch_ce(c->bf16, c->at<CeProb>(l.probs), l.count, c->at<int32_t>(c->ydev), c->B,
+      e = launch_ce(c->bf16, c->at<CeProb>(l.probs), l.count, c->at<int32_t>(c->ydev), c->labels_per_model, c->B,
                     c->at<float>(c->ce_partial), c->at<float>(c->losses_dev), c->stream);
       break;
     case 6:
@@ -1427,6 +1445,7 @@ static un_status load_common(un_ctx* c, const float* x, const int32_t* y, bool d
                         c->XinC == NONE ? nullptr : c->base + c->XinC, c->in_cs, c->stream));
   HIPCHK(c, hipStreamSynchronize(c->stream));
   c->loaded = true;
+  c->labels_per_model = false;
   return UN_OK;
 }
 
@@ -1442,10 +1461,14 @@ un_status un_load_batch_device(un_ctx* c, const float* x, const int32_t* y) {
   return load_common(c, x, y, true);
 }
 
-un_status un_step(un_ctx* c, float lr, float* losses) {
-  CHECK_CTX(c);
-  if (!c->loaded) return fail(c, UN_ERR_STATE, "un_step before un_load_batch");
-  if (!std::isfinite(lr)) return fail(c, UN_ERR_INVALID, "lr is not finite");
+// The step's launches; `lrv` (device) holds per-model rates, else `lr` is
+// every model's.
+static un_status step_common(un_ctx* c, float lr, const float* lrv, float* losses) {
+  c->lrv = lrv;
+  struct Reset {
+    un_ctx* c;
+    ~Reset() { c->lrv = nullptr; }
+  } reset{c};
   for (auto& l : c->fwd) HIPCHK(c, run_launch(c, l, lr));
   HIPCHK(c, run_launch(c, c->ce, lr));
   for (auto& l : c->bwd[c->wt_cur]) HIPCHK(c, run_launch(c, l, lr));
@@ -1462,6 +1485,42 @@ un_status un_step(un_ctx* c, float lr, float* losses) {
     for (size_t i = 0; i < c->models.size(); ++i)
       if (!c->active[i]) losses[i] = std::nanf("");
   }
+  return UN_OK;
+}
+
+un_status un_step(un_ctx* c, float lr, float* losses) {
+  CHECK_CTX(c);
+  if (!c->loaded) return fail(c, UN_ERR_STATE, "un_step before un_load_batch");
+  if (!std::isfinite(lr)) return fail(c, UN_ERR_INVALID, "lr is not finite");
+  return step_common(c, lr, nullptr, losses);
+}
+
+un_status un_step_lr(un_ctx* c, const float* lrs, float* losses) {
+  CHECK_CTX(c);
+  if (!lrs) return fail(c, UN_ERR_INVALID, "lrs is NULL");
+  if (!c->loaded) return fail(c, UN_ERR_STATE, "un_step_lr before un_load_batch");
+  for (size_t i = 0; i < c->models.size(); ++i)
+    if (!std::isfinite(lrs[i])) return fail(c, UN_ERR_INVALID, "lr of model " + std::to_string(i) + " is not finite");
+  // the rates travel in the kernel arguments, ordered before the step on the stream
+  HIPCHK(c, launch_set_values(c->at<float>(c->lr_dev), lrs, (int)c->models.size(), c->stream));
+  return step_common(c, 0.f, c->at<float>(c->lr_dev), losses);
+}
+
+un_status un_load_labels(un_ctx* c, const int32_t* y) {
+  CHECK_CTX(c);
+  if (!y) return fail(c, UN_ERR_INVALID, "y is NULL");
+  if (!c->loaded) return fail(c, UN_ERR_STATE, "un_load_labels before un_load_batch");
+  const size_t n = c->models.size(), B = (size_t)c->B;
+  for (size_t i = 0; i < n; ++i)
+    for (size_t b = 0; b < B; ++b) {
+      const int32_t v = y[i * B + b];
+      if (v < 0 || v >= c->models[i].num_classes)
+        return fail(c, UN_ERR_RANGE, "label " + std::to_string(v) + " of model " + std::to_string(i) + " at " +
+                                         std::to_string(b) + " out of range");
+    }
+  HIPCHK(c, hipMemcpyAsync(c->base + c->ydev, y, n * B * 4, hipMemcpyHostToDevice, c->stream));
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  c->labels_per_model = true;
   return UN_OK;
 }
 

@@ -25,7 +25,8 @@ OPS = {"linear": 0, "conv": 1, "relu": 2, "pool": 3, "flatten": 4}
 KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad", "ce", "sgd", "other"]
 
 # Every symbol the header declares.
-EXPORTS = ["un_create", "un_load_batch", "un_load_batch_device", "un_step", "un_set_active", "un_get_params",
+EXPORTS = ["un_create", "un_load_batch", "un_load_batch_device", "un_load_labels", "un_step", "un_step_lr",
+           "un_set_active", "un_get_params",
            "un_set_params", "un_get_grads", "un_keep_grads", "un_param_count", "un_arena_bytes", "un_sync", "un_get_stream",
            "un_profile_enable", "un_profile_read", "un_destroy", "un_last_error"]
 
@@ -69,6 +70,8 @@ def lib():
             "un_load_batch": (ctypes.c_int, [P, f, i32]),
             "un_load_batch_device": (ctypes.c_int, [P, P, P]),
             "un_step": (ctypes.c_int, [P, ctypes.c_float, f]),
+            "un_step_lr": (ctypes.c_int, [P, f, f]),
+            "un_load_labels": (ctypes.c_int, [P, ctypes.POINTER(ctypes.c_int32)]),
             "un_set_active": (ctypes.c_int, [P, ctypes.POINTER(ctypes.c_uint8)]),
             "un_get_params": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t, c_size_p]),
             "un_set_params": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t]),
@@ -139,6 +142,27 @@ def un_load_batch(ctx, x, y):
 
 def un_load_batch_device(ctx, x_ptr, y_ptr):
     _check(lib().un_load_batch_device(ctx, ctypes.c_void_p(x_ptr), ctypes.c_void_p(y_ptr)), ctx)
+
+
+def un_load_labels(ctx, y, n_models, batch):
+    """Per-model labels [n_models][batch] for the loaded batch."""
+    y = np.ascontiguousarray(y, dtype=np.int32)
+    if y.shape != (n_models, batch):
+        raise ValueError(f"labels must have shape ({n_models}, {batch}), got {y.shape}")
+    _check(lib().un_load_labels(ctx, y.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))), ctx)
+
+
+def un_step_lr(ctx, lrs, n_models, losses=True):
+    """One fused step with a learning rate per model; returns the losses unless losses=False."""
+    lr = np.ascontiguousarray(lrs, dtype=np.float32)
+    if lr.shape != (n_models,):
+        raise ValueError(f"one learning rate per model ({n_models}) expected, got shape {lr.shape}")
+    if not losses:
+        _check(lib().un_step_lr(ctx, _fp(lr), None), ctx)
+        return None
+    out = np.zeros(n_models, dtype=np.float32)
+    _check(lib().un_step_lr(ctx, _fp(lr), _fp(out)), ctx)
+    return out
 
 
 def un_step(ctx, lr, n_models=None):
@@ -243,6 +267,7 @@ class Hybrid:
     def __init__(self, specs, batch, in_shape, precision="f32", seeds=None):
         self.specs = list(specs)
         self.n = len(self.specs)
+        self.batch = int(batch)
         self.ctx = un_create(self.specs, batch, in_shape, precision, seeds)
 
     def close(self):
@@ -266,7 +291,13 @@ class Hybrid:
         un_load_batch(self.ctx, x, y)
 
     def step(self, lr, losses=True):
-        return un_step(self.ctx, lr, self.n if losses else None)
+        """lr: one rate for every model, or a sequence of N per-model rates."""
+        if np.ndim(lr) == 0:
+            return un_step(self.ctx, lr, self.n if losses else None)
+        return un_step_lr(self.ctx, lr, self.n, losses)
+
+    def load_labels(self, y):
+        un_load_labels(self.ctx, y, self.n, self.batch)
 
     def set_active(self, mask):
         un_set_active(self.ctx, mask, self.n)
