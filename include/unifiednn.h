@@ -178,6 +178,47 @@ un_status un_keep_grads(un_ctx* ctx, int32_t enable);
  * that step. */
 un_status un_get_grads(un_ctx* ctx, int32_t i, float* dst, size_t cap_elems, size_t* n_elems);
 
+/* Optimizer of one model (each sub-model has its own optimizer: Model
+ * Unifier section; the paper's models use SGD, Adam for the transformer).
+ * Element-wise, fp32, with g the gradient and lr the step's rate of the model:
+ *   UN_OPT_SGD       w <- fma(-lr, g, w)                       (the default)
+ *   UN_OPT_MOMENTUM  b <- fma(momentum, b, g);  w <- fma(-lr, b, w)
+ *                    (b starts at 0: the first step is plain SGD)
+ *   UN_OPT_ADAM      m <- fma(beta1, m, (1-beta1) g);  v <- fma(beta2, v, (1-beta2) g^2);
+ *                    w <- w - (lr / (1 - beta1^t)) * m / (sqrt(v) / sqrt(1 - beta2^t) + eps)
+ *                    (t = the model's update count, from 1; m, v start at 0)
+ * These are torch.optim.SGD (momentum, no dampening, not Nesterov) and
+ * torch.optim.Adam (no weight decay, no amsgrad) without weight decay. */
+typedef enum { UN_OPT_SGD = 0, UN_OPT_MOMENTUM = 1, UN_OPT_ADAM = 2 } un_opt_kind;
+typedef struct {
+  int32_t kind;      /* un_opt_kind */
+  float momentum;    /* UN_OPT_MOMENTUM: in [0, 1) */
+  float beta1, beta2;/* UN_OPT_ADAM: in [0, 1) */
+  float eps;         /* UN_OPT_ADAM: > 0 */
+} un_optimizer;
+
+/* Give model i a fresh optimizer: its state is zeroed and its update count
+ * reset (as a new torch optimizer would). The first non-SGD optimizer of a
+ * context allocates the state of all models (two fp32 values per parameter,
+ * outside the arena) and rebuilds the step's tables. Waits for the stream.
+ * Errors: UN_ERR_RANGE (i), UN_ERR_INVALID (kind or hyper-parameters),
+ * UN_ERR_OOM. */
+un_status un_set_optimizer(un_ctx* ctx, int32_t i, const un_optimizer* opt);
+
+/* Model i's optimizer state for a checkpoint: k * n_params floats, k = 0
+ * (SGD), 1 (momentum buffer) or 2 (Adam: first moments, then second
+ * moments), each block in un_get_params layout and order; *step receives the
+ * number of updates the model has taken under this optimizer. With dst ==
+ * NULL only *n_elems and *step are set. Waits for the stream.
+ * Errors: UN_ERR_RANGE, UN_ERR_BUFSIZE. */
+un_status un_get_opt_state(un_ctx* ctx, int32_t i, float* dst, size_t cap_elems, size_t* n_elems, int64_t* step);
+
+/* Restore model i's optimizer state and update count (layout as
+ * un_get_opt_state for the model's current optimizer; n_elems exact), e.g.
+ * to resume from a checkpoint. Errors: UN_ERR_RANGE, UN_ERR_BUFSIZE,
+ * UN_ERR_INVALID (negative step, NULL src). */
+un_status un_set_opt_state(un_ctx* ctx, int32_t i, const float* src, size_t n_elems, int64_t step);
+
 /* Number of parameters of model i. */
 un_status un_param_count(const un_ctx* ctx, int32_t i, size_t* n_elems);
 

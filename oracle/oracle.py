@@ -18,7 +18,9 @@ paper's PyTorch prototype, whose defaults these are):
 
 * loss: softmax cross-entropy, mean over the batch;
 * optimizer: plain SGD, no momentum or weight decay, computed as the
-  correctly rounded fp32 fma(-lr, g, theta);
+  correctly rounded fp32 fma(-lr, g, theta); each sub-model may instead have
+  SGD with momentum or Adam (its own optimizer, Model Unifier section), with
+  torch.optim's definitions (momentum_update, adam_update);
 * gradients are recomputed every step (nothing accumulates across steps);
 * the loss a step reports is the forward loss at the pre-update parameters;
 * convolution is cross-correlation, stride 1, zero padding;
@@ -363,6 +365,71 @@ def sgd_update(params, grads, lr, mode="f32"):
         return [np.asarray(p, dtype=F64) - lr * np.asarray(g, dtype=F64) for p, g in zip(params, grads)]
     nlr = np.full((), -lr, dtype=F32)
     return [fma32(nlr, to_f32(g), p) for p, g in zip(params, grads)]
+
+
+def momentum_update(params, grads, bufs, lr, momentum, mode="f32"):
+    """SGD with momentum (the per-model optimizer option; torch.optim.SGD's
+    definition without dampening, weight decay or Nesterov):
+    b <- momentum * b + g,  theta <- theta - lr * b, with b = 0 before the first
+    step. Returns (new params, new buffers). In the fp32 modes every stored
+    value (b, theta) is the fp32 rounding of its exact value from fp32 inputs."""
+    out_p, out_b = [], []
+    for p, g, b in zip(params, grads, bufs):
+        p64, g64, b64 = (np.asarray(a, dtype=F64) for a in (p, g, b))
+        nb = momentum * b64 + g64
+        if mode != "f64":
+            nb = to_f32(nb).astype(F64)
+        npar = p64 - lr * nb
+        out_b.append(nb if mode == "f64" else to_f32(nb))
+        out_p.append(npar if mode == "f64" else to_f32(npar))
+    return out_p, out_b
+
+
+def adam_update(params, grads, m, v, t, lr, beta1, beta2, eps, mode="f32"):
+    """Adam (torch.optim.Adam's definition without weight decay or amsgrad),
+    update number t >= 1:
+    m <- beta1 m + (1 - beta1) g;  v <- beta2 v + (1 - beta2) g^2;
+    theta <- theta - (lr / (1 - beta1^t)) m / (sqrt(v) / sqrt(1 - beta2^t) + eps).
+    Returns (new params, new m, new v); rounding as in momentum_update."""
+    bc1 = 1.0 - beta1 ** t
+    bc2 = 1.0 - beta2 ** t
+    out_p, out_m, out_v = [], [], []
+    for p, g, mm, vv in zip(params, grads, m, v):
+        p64, g64, m64, v64 = (np.asarray(a, dtype=F64) for a in (p, g, mm, vv))
+        nm = beta1 * m64 + (1.0 - beta1) * g64
+        nv = beta2 * v64 + (1.0 - beta2) * g64 * g64
+        if mode != "f64":
+            nm = to_f32(nm).astype(F64)
+            nv = to_f32(nv).astype(F64)
+        npar = p64 - (lr / bc1) * nm / (np.sqrt(nv) / np.sqrt(bc2) + eps)
+        out_m.append(nm if mode == "f64" else to_f32(nm))
+        out_v.append(nv if mode == "f64" else to_f32(nv))
+        out_p.append(npar if mode == "f64" else to_f32(npar))
+    return out_p, out_m, out_v
+
+
+def step_opt(spec, params, x, y, lr, opt, state, mode="f32", flags=None):
+    """One training step of one model under its optimizer.
+
+    opt: {"kind": "sgd" | "momentum" | "adam", "momentum", "betas", "eps"};
+    state: {"t": updates taken, "s1": [...], "s2": [...]} (zeros / absent at
+    the start). Returns (loss, new params, grads, new state)."""
+    logits, cache = forward(spec, params, x, mode, flags)
+    loss, dz = softmax_ce(logits, y)
+    dz = _Mode(mode).store(dz)
+    grads = backward(spec, params, cache, dz, mode)
+    zeros = [np.zeros(np.shape(p), dtype=F64 if mode == "f64" else F32) for p in params]
+    t = state.get("t", 0) + 1
+    kind = opt["kind"]
+    if kind == "sgd":
+        return loss, sgd_update(params, grads, lr, mode), grads, {"t": t}
+    if kind == "momentum":
+        newp, b = momentum_update(params, grads, state.get("s1", zeros), lr, opt["momentum"], mode)
+        return loss, newp, grads, {"t": t, "s1": b}
+    b1, b2 = opt["betas"]
+    newp, m, v = adam_update(params, grads, state.get("s1", zeros), state.get("s2", zeros), t, lr, b1, b2,
+                             opt["eps"], mode)
+    return loss, newp, grads, {"t": t, "s1": m, "s2": v}
 
 
 def step(spec, params, x, y, lr, mode="f32", flags=None):

@@ -57,6 +57,12 @@ struct GemmProb {
   int64_t ldwt;
   float* bmaster;
   const int32_t* row_model;   // WGRAD of the concatenated first layers: model of each row m (else null)
+  // optimizer state (same layouts as W and bmaster; null for plain SGD):
+  // momentum buffer or Adam's first moment, and Adam's second moment
+  float* s1;
+  float* s2;
+  float* sb1;
+  float* sb2;
 };
 
 // ---------------------------------------------------------------------------
@@ -122,7 +128,26 @@ struct ReduceProb {
   void* WT;
   int64_t ldwt;
   float* bmaster;
+  float* s1;                  // optimizer state, as in GemmProb
+  float* s2;
+  float* sb1;
+  float* sb2;
 };
+
+// ---------------------------------------------------------------------------
+// Optimizer of one model for one step, computed on the host per step (all
+// fields fp32 so that the array travels as plain floats):
+//   kind 0  SGD:           w <- fma(-lr, g, w)
+//   kind 1  SGD momentum:  b <- fma(b1, b, g);  w <- fma(-lr, b, w)   (b1 = momentum)
+//   kind 2  Adam:          m <- fma(b1, m, c1*g);  v <- fma(b2, v, c2*g*g);
+//                          w <- w - lr * (m / (sqrt(v) * isb2 + eps))
+// with, for Adam at its step t: lr = rate / (1 - beta1^t), c1 = 1 - beta1,
+// c2 = 1 - beta2, isb2 = 1 / sqrt(1 - beta2^t).
+// ---------------------------------------------------------------------------
+struct OptHp {
+  float kind, lr, b1, b2, c1, c2, isb2, eps;
+};
+constexpr int OPT_FLOATS = 8;
 
 // ---------------------------------------------------------------------------
 // Softmax cross-entropy of one model: logits [B][ldl] fp32 -> per-model mean
@@ -166,8 +191,9 @@ struct SgdTensor {
 // Learning rates: `lr` for every model, or per model lrv[model] when lrv is
 // not null (device array). Labels: labels[b] for every model, or
 // labels[model * B + b] when per_model_labels is set.
+// `opt` (device, one OptHp per model) replaces lr/lrv when not null.
 hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
-                       const float* lrv, bool keep_grads, hipStream_t s);
+                       const float* lrv, const OptHp* opt, bool keep_grads, hipStream_t s);
 hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                            hipStream_t s);
 hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
@@ -180,8 +206,7 @@ hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const i
 hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                             size_t lds_bytes, hipStream_t s);
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
-                         const float* lrv,
-                         bool keep_grads, hipStream_t s);
+                         const float* lrv, const OptHp* opt, bool keep_grads, hipStream_t s);
 hipError_t launch_set_values(float* dst, const float* vals, int n, hipStream_t s);
 hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, const int32_t* labels, bool per_model_labels, int B,
                      float* partial, float* losses, hipStream_t s);

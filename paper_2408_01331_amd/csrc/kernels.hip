@@ -952,6 +952,50 @@ template <> __device__ __forceinline__ void store_chunk<bf16_t>(bf16_t* dst, con
 // Row-major store of the staged fp32 tile sC [BM][CLD] into C [m][ldc] as OT,
 // one 16-byte chunk per thread and step (contiguous along n); the tile rows
 // (stride CLD, a multiple of 4) are read as float4s.
+// The optimizer step of one element (OptHp): returns the new weight and
+// updates the state in place.
+__device__ __forceinline__ float opt_update1(const OptHp& h, float g, float w, float* s1, float* s2) {
+  if (h.kind == 0.f) return fmaf(-h.lr, g, w);
+  if (h.kind == 1.f) {
+    const float b = fmaf(h.b1, *s1, g);
+    *s1 = b;
+    return fmaf(-h.lr, b, w);
+  }
+  const float m = fmaf(h.b1, *s1, h.c1 * g);
+  const float v = fmaf(h.b2, *s2, h.c2 * g * g);
+  *s1 = m;
+  *s2 = v;
+  return w - h.lr * (m / (sqrtf(v) * h.isb2 + h.eps));
+}
+
+// Four consecutive elements (16-byte aligned state).
+__device__ __forceinline__ void opt_update4(const OptHp& h, const f32x4& g, f32x4& w, float* s1, float* s2) {
+  if (h.kind == 0.f) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) w[e] = fmaf(-h.lr, g[e], w[e]);
+    return;
+  }
+  f32x4 a = *(gptr<const f32x4>)s1;
+  if (h.kind == 1.f) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      a[e] = fmaf(h.b1, a[e], g[e]);
+      w[e] = fmaf(-h.lr, a[e], w[e]);
+    }
+    *(gptr<f32x4>)s1 = a;
+    return;
+  }
+  f32x4 v = *(gptr<const f32x4>)s2;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    a[e] = fmaf(h.b1, a[e], h.c1 * g[e]);
+    v[e] = fmaf(h.b2, v[e], h.c2 * g[e] * g[e]);
+    w[e] = w[e] - h.lr * (a[e] / (sqrtf(v[e]) * h.isb2 + h.eps));
+  }
+  *(gptr<f32x4>)s1 = a;
+  *(gptr<f32x4>)s2 = v;
+}
+
 template <typename OT, int BM, int BN, int CLD>
 __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, int m0, int n0, int M, int N) {
   constexpr int VE = 16 / sizeof(OT), CPR = BN / VE;
@@ -990,10 +1034,13 @@ __device__ __forceinline__ void store_cols(const float* sC, OT* CT, int64_t ldct
   }
 }
 
-template <typename T, int BM, int BN, int BK>
+// OPT: the update follows a per-model OptHp (`opt`, not null) instead of
+// fma(-lr, g, w); a separate instantiation, so that plain SGD pays nothing.
+template <typename T, int BM, int BN, int BK, bool OPT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(const GemmProb* __restrict__ probs,
                                                    const int32_t* __restrict__ tile_map, float lr,
-                                                   const float* __restrict__ lrv, int keep_grads) {
+                                                   const float* __restrict__ lrv, const OptHp* __restrict__ opt,
+                                                   int keep_grads) {
   using TL = Tile<T, BM, BN, BK>;
   using SM = Smem<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[SM::BYTES];
@@ -1080,15 +1127,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
     const int idx = threadIdx.x + 256 * q, r = idx / CPR, cc = idx - r * CPR;
     const int m = m0 + r, n = n0 + cc * 4;
     if (m >= p.M || n > ns) continue;
-    // this row's model: its own learning rate when rates are per model
-    const float lr_m = lrv ? lrv[p.row_model ? p.row_model[m] : p.model] : lr;
+    // this row's model: its own learning rate (or optimizer) when set per model
+    const int mdl = p.row_model ? p.row_model[m] : p.model;
+    const float lr_m = lrv ? lrv[mdl] : lr;
     float* s = sC + r * CLD + cc * 4;
     const int64_t base = (int64_t)m * p.ldc + n;
     if (n + 4 <= ns) {
       const f32x4 g = *(const f32x4*)s;
       if (keep_grads) *(gptr<f32x4>)((float*)p.C + base) = g;
-      const f32x4 w = f32x4{fmaf(-lr_m, g[0], w0[q][0]), fmaf(-lr_m, g[1], w0[q][1]), fmaf(-lr_m, g[2], w0[q][2]),
-                            fmaf(-lr_m, g[3], w0[q][3])};
+      f32x4 w;
+      if constexpr (OPT) {
+        w = w0[q];
+        opt_update4(opt[mdl], g, w, p.s1 + base, p.s2 + base);
+      } else {
+        w = f32x4{fmaf(-lr_m, g[0], w0[q][0]), fmaf(-lr_m, g[1], w0[q][1]), fmaf(-lr_m, g[2], w0[q][2]),
+                  fmaf(-lr_m, g[3], w0[q][3])};
+      }
       *(gptr<f32x4>)(p.W + base) = w;
       if (p.Wb) {
         u32x2 hb;
@@ -1102,13 +1156,16 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
         const float g = s[e];
         if (n + e < ns) {
           if (keep_grads) ((float*)p.C)[base + e] = g;
-          const float w = fmaf(-lr_m, g, p.W[base + e]);
+          float w;
+          if constexpr (OPT) w = opt_update1(opt[mdl], g, p.W[base + e], p.s1 + base + e, p.s2 + base + e);
+          else w = fmaf(-lr_m, g, p.W[base + e]);
           p.W[base + e] = w;
           if (p.Wb) ((bf16_t*)p.Wb)[base + e] = f2bf(w);
           s[e] = w;
         } else {
           if (keep_grads) p.dbias[m] = g;
-          p.bmaster[m] = fmaf(-lr_m, g, p.bmaster[m]);
+          if constexpr (OPT) p.bmaster[m] = opt_update1(opt[mdl], g, p.bmaster[m], p.sb1 + m, p.sb2 + m);
+          else p.bmaster[m] = fmaf(-lr_m, g, p.bmaster[m]);
         }
       }
     }
@@ -1597,7 +1654,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 template <typename T>
 __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* __restrict__ probs,
                                                               const int32_t* __restrict__ blk_prob, float lr,
-                                                              const float* __restrict__ lrv, int keep_grads) {
+                                                              const float* __restrict__ lrv,
+                                                              const OptHp* __restrict__ opt, int keep_grads) {
   const ReduceProb& p = probs[blk_prob[blockIdx.x]];
   if (lrv) lr = lrv[p.model];
   const int64_t e = (int64_t)(blockIdx.x - p.blk_base) * REDUCE_BLOCK + threadIdx.x;
@@ -1609,7 +1667,7 @@ __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* 
   if (j < p.J) {
     const int64_t idx = (int64_t)o * p.ldgw + j;
     if (keep_grads) p.gW[idx] = s;
-    const float w = fmaf(-lr, s, p.W[idx]);
+    const float w = opt ? opt_update1(opt[p.model], s, p.W[idx], p.s1 + idx, p.s2 + idx) : fmaf(-lr, s, p.W[idx]);
     p.W[idx] = w;
     if (p.Wb) ((bf16_t*)p.Wb)[idx] = f2bf(w);
     if (p.WT) {
@@ -1618,7 +1676,7 @@ __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* 
     }
   } else {
     if (keep_grads) p.gb[o] = s;
-    p.bmaster[o] = fmaf(-lr, s, p.bmaster[o]);
+    p.bmaster[o] = opt ? opt_update1(opt[p.model], s, p.bmaster[o], p.sb1 + o, p.sb2 + o) : fmaf(-lr, s, p.bmaster[o]);
   }
 }
 
@@ -1767,14 +1825,23 @@ __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, 
 // Launch wrappers
 // ---------------------------------------------------------------------------
 hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
-                       const float* lrv, bool keep_grads, hipStream_t s) {
+                       const float* lrv, const OptHp* opt, bool keep_grads, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
-  if (bf16)
-    hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16>), dim3(ntiles), dim3(256), 0, s, probs,
-                       tile_map, lr, lrv, (int)keep_grads);
-  else
-    hipLaunchKernelGGL((gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, GEMM_BK_F32>), dim3(ntiles), dim3(256), 0, s, probs,
-                       tile_map, lr, lrv, (int)keep_grads);
+  if (bf16) {
+    if (opt)
+      hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16, true>), dim3(ntiles), dim3(256), 0,
+                         s, probs, tile_map, lr, lrv, opt, (int)keep_grads);
+    else
+      hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16, false>), dim3(ntiles), dim3(256),
+                         0, s, probs, tile_map, lr, lrv, opt, (int)keep_grads);
+  } else {
+    if (opt)
+      hipLaunchKernelGGL((gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, GEMM_BK_F32, true>), dim3(ntiles), dim3(256), 0, s,
+                         probs, tile_map, lr, lrv, opt, (int)keep_grads);
+    else
+      hipLaunchKernelGGL((gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, GEMM_BK_F32, false>), dim3(ntiles), dim3(256), 0, s,
+                         probs, tile_map, lr, lrv, opt, (int)keep_grads);
+  }
   return hipGetLastError();
 }
 
@@ -1858,13 +1925,13 @@ hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const i
 }
 
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
-                         const float* lrv, bool keep_grads, hipStream_t s) {
+                         const float* lrv, const OptHp* opt, bool keep_grads, hipStream_t s) {
   if (nblocks <= 0) return hipSuccess;
   if (bf16)
-    hipLaunchKernelGGL(reduce_kernel<bf16_t>, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob, lr, lrv,
+    hipLaunchKernelGGL(reduce_kernel<bf16_t>, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob, lr, lrv, opt,
                        (int)keep_grads);
   else
-    hipLaunchKernelGGL(reduce_kernel<float>, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob, lr, lrv,
+    hipLaunchKernelGGL(reduce_kernel<float>, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob, lr, lrv, opt,
                        (int)keep_grads);
   return hipGetLastError();
 }

@@ -49,6 +49,8 @@ struct Block {
   // arena offsets (NONE = absent)
   size_t W32 = NONE, b32 = NONE, gW = NONE, gb = NONE, Wb = NONE, WT = NONE;
   size_t WT2 = NONE;       // Linear: second transposed copy (written while the dgrad reads WT)
+  // optimizer state, offsets in the context's state allocation (same layouts as W32 / b32)
+  size_t S1 = NONE, S1b = NONE, S2 = NONE, S2b = NONE;
   int64_t ldw = 0, ldwt = 0;
   int rows = 0;            // logical weight rows (N or O)
   size_t X = NONE, XT = NONE;
@@ -105,6 +107,19 @@ struct un_ctx {
   size_t lr_dev = NONE;          // per-model learning rates of the current un_step_lr call
   const float* lrv = nullptr;    // lr_dev while such a step is being launched, else null (one rate)
   bool labels_per_model = false; // ydev holds N rows of B labels (un_load_labels) instead of one
+  // optimizers (un_set_optimizer): kind and hyper-parameters per model, and
+  // the number of updates each model has taken under it
+  struct Opt {
+    int kind = UN_OPT_SGD;
+    double momentum = 0, beta1 = 0.9, beta2 = 0.999, eps = 1e-8;
+    int64_t t = 0;
+  };
+  std::vector<Opt> opts;
+  bool any_opt = false;          // some model is not plain SGD: the step uploads OptHp per model
+  char* sbase = nullptr;         // optimizer state (allocated when first needed)
+  size_t sbytes = 0;
+  size_t opt_dev = NONE;         // OptHp per model
+  const OptHp* optp = nullptr;   // opt_dev while a step with optimizers is being launched
   int in_cs = 0;       // stored channels of XinC
   int64_t ldxin = 0, ldxint = 0;
   // schedule
@@ -120,6 +135,7 @@ struct un_ctx {
     size_t catW32 = NONE, catb32 = NONE, catgW = NONE, catgb = NONE, catWb = NONE, catY = NONE, catYT = NONE,
            catGT = NONE;
     size_t cat_row_model = NONE;  // int32 per concatenated row: the model owning it
+    size_t catS1 = NONE, catS1b = NONE, catS2 = NONE, catS2b = NONE;  // state of the concatenation (sbase)
   } plan;
   int wt_cur = 0;                     // which transposed copy the next dgrad reads
   bool keep_grads = false, grads_valid = false;
@@ -456,6 +472,10 @@ static void build_tables(un_ctx* c, Tables& T) {
   };
   // Pointers are encoded as (arena offset + 1) and fixed up after the arena exists.
   auto ptr = [&](size_t off) -> void* { return off == NONE ? nullptr : (void*)(uintptr_t)(off + 1); };
+  // Optimizer state lives in its own allocation: plain device pointers (not relocated).
+  auto sp = [&](size_t off, int64_t add) -> float* {
+    return (c->sbase && off != NONE) ? (float*)(c->sbase + off + (size_t)add) : nullptr;
+  };
 
   const int GBM = bf ? GEMM_BM_BF16 : GEMM_BM_F32, GBN = bf ? GEMM_BN_BF16 : GEMM_BN_F32;
   const int CBM = bf ? CONV_BM_BF16 : CONV_BM_F32, CBN = bf ? CONV_BN_BF16 : CONV_BN_F32;
@@ -763,6 +783,10 @@ static void build_tables(un_ctx* c, Tables& T) {
             p.Wb = ptr(sub(catWb, run.first * kin_p * 2));
             p.bmaster = (float*)ptr(sub(catb32, run.first * 4));
             p.row_model = (const int32_t*)ptr(sub(c->plan.cat_row_model, run.first * 4));
+            p.s1 = sp(c->plan.catS1, run.first * kin_p * 4);
+            p.s2 = sp(c->plan.catS2, run.first * kin_p * 4);
+            p.sb1 = sp(c->plan.catS1b, run.first * 4);
+            p.sb2 = sp(c->plan.catS2b, run.first * 4);
             gp.push_back(p);
           }
           continue;
@@ -786,6 +810,10 @@ static void build_tables(un_ctx* c, Tables& T) {
         p.ldwt = b.ldwt;
         p.bmaster = (float*)ptr(b.b32);
         p.model = b.model;
+        p.s1 = sp(b.S1, 0);
+        p.s2 = sp(b.S2, 0);
+        p.sb1 = sp(b.S1b, 0);
+        p.sb2 = sp(b.S2b, 0);
         gp.push_back(p);
       } else {
         const int J = b.KH * b.KH * b.C;
@@ -832,6 +860,10 @@ static void build_tables(un_ctx* c, Tables& T) {
         r.ldwt = b.ldwt;
         r.bmaster = (float*)ptr(b.b32);
         r.model = b.model;
+        r.s1 = sp(b.S1, 0);
+        r.s2 = sp(b.S2, 0);
+        r.sb1 = sp(b.S1b, 0);
+        r.sb2 = sp(b.S2b, 0);
         rp.push_back(r);
       }
     }
@@ -948,6 +980,7 @@ static un_status plan_and_alloc(un_ctx* c) {
   c->xstage = A.take((size_t)B * in_feat * 4);
   c->ydev = A.take(c->models.size() * (size_t)B * 4);  // one row of labels, or one per model
   c->lr_dev = A.take(c->models.size() * 4);
+  c->opt_dev = A.take(c->models.size() * sizeof(OptHp));
   c->losses_dev = A.take(c->models.size() * 4);
   c->ce_partial = A.take(c->models.size() * (size_t)cdiv(B, CE_ROWS) * 4);
   bool any_linear0 = false, any_conv0 = false;
@@ -1229,34 +1262,43 @@ static un_status refresh_shadows(un_ctx* c) {
   return UN_OK;
 }
 
-static un_status write_params(un_ctx* c, int i, const float* src) {
+// Model i's tensors of one kind (weights and biases at the Block offsets wf,
+// bf from `base`) from / to the PyTorch layout.
+static un_status write_blocks(un_ctx* c, int i, char* base, size_t Block::*wf, size_t Block::*bf, const float* src) {
   Model& m = c->models[i];
   std::vector<float> w, bias;
   for (auto& b : m.blocks) {
     to_internal(b, src, w, bias);
     // on the context's stream, completed before the host buffers go away
-    HIPCHK(c, hipMemcpyAsync(c->base + b.W32, w.data(), w.size() * 4, hipMemcpyHostToDevice, c->stream));
-    HIPCHK(c, hipMemcpyAsync(c->base + b.b32, bias.data(), bias.size() * 4, hipMemcpyHostToDevice, c->stream));
+    HIPCHK(c, hipMemcpyAsync(base + b.*wf, w.data(), w.size() * 4, hipMemcpyHostToDevice, c->stream));
+    HIPCHK(c, hipMemcpyAsync(base + b.*bf, bias.data(), bias.size() * 4, hipMemcpyHostToDevice, c->stream));
     HIPCHK(c, hipStreamSynchronize(c->stream));
   }
   return UN_OK;
 }
 
-static un_status read_tensors(un_ctx* c, int i, bool grads, float* dst) {
+static un_status read_blocks(un_ctx* c, int i, const char* base, size_t Block::*wf, size_t Block::*bf, float* dst) {
   Model& m = c->models[i];
   HIPCHK(c, hipStreamSynchronize(c->stream));
   std::vector<float> w, bias;
   for (auto& b : m.blocks) {
     w.resize((size_t)b.rows * b.ldw);
     bias.resize(b.rows);
-    HIPCHK(c, hipMemcpyAsync(w.data(), c->base + (grads ? b.gW : b.W32), w.size() * 4, hipMemcpyDeviceToHost,
-                             c->stream));
-    HIPCHK(c, hipMemcpyAsync(bias.data(), c->base + (grads ? b.gb : b.b32), bias.size() * 4, hipMemcpyDeviceToHost,
-                             c->stream));
+    HIPCHK(c, hipMemcpyAsync(w.data(), base + b.*wf, w.size() * 4, hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipMemcpyAsync(bias.data(), base + b.*bf, bias.size() * 4, hipMemcpyDeviceToHost, c->stream));
     HIPCHK(c, hipStreamSynchronize(c->stream));
     from_internal(b, w, bias, dst);
   }
   return UN_OK;
+}
+
+static un_status write_params(un_ctx* c, int i, const float* src) {
+  return write_blocks(c, i, c->base, &Block::W32, &Block::b32, src);
+}
+
+static un_status read_tensors(un_ctx* c, int i, bool grads, float* dst) {
+  return grads ? read_blocks(c, i, c->base, &Block::gW, &Block::gb, dst)
+               : read_blocks(c, i, c->base, &Block::W32, &Block::b32, dst);
 }
 
 // Library initialisation: Kaiming-uniform weights, U(+-1/sqrt(fan_in)) biases,
@@ -1302,7 +1344,7 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
   hipError_t e = hipSuccess;
   switch (l.kind) {
     case 0:
-      e = launch_gemm(c->bf16, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->lrv, c->keep_grads,
+      e = launch_gemm(c->bf16, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->lrv, c->optp, c->keep_grads,
                       c->stream);
       break;
     case 1:
@@ -1320,7 +1362,7 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
                            c->stream);
       break;
     case 4:
-      e = launch_reduce(c->bf16, c->at<ReduceProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->lrv, c->keep_grads,
+      e = launch_reduce(c->bf16, c->at<ReduceProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->lrv, c->optp, c->keep_grads,
                         c->stream);
       break;
     case 5:
@@ -1382,6 +1424,7 @@ un_status un_create(const un_model_spec* specs, int32_t n_models, const un_input
   c->in_h = in->in_h;
   c->in_w = in->in_w;
   c->models.resize(n_models);
+  c->opts.resize(n_models);
   c->min_classes = 1 << 30;
   for (int i = 0; i < n_models; ++i) {
     std::string why;
@@ -1461,17 +1504,51 @@ un_status un_load_batch_device(un_ctx* c, const float* x, const int32_t* y) {
   return load_common(c, x, y, true);
 }
 
-// The step's launches; `lrv` (device) holds per-model rates, else `lr` is
-// every model's.
-static un_status step_common(un_ctx* c, float lr, const float* lrv, float* losses) {
-  c->lrv = lrv;
+// The step's launches. Rates: lrs (host, per model) or else lr for every
+// model. With an optimizer other than SGD on some model, every model's
+// OptHp (rate folded in) goes to the device first and the update kernels
+// follow it; otherwise per-model rates go to lr_dev, or lr is passed as is.
+static un_status step_common(un_ctx* c, float lr, const float* lrs, float* losses) {
   struct Reset {
     un_ctx* c;
-    ~Reset() { c->lrv = nullptr; }
+    ~Reset() {
+      c->lrv = nullptr;
+      c->optp = nullptr;
+    }
   } reset{c};
+  const size_t n = c->models.size();
+  if (c->any_opt) {
+    std::vector<OptHp> hp(n);
+    for (size_t i = 0; i < n; ++i) {
+      const auto& o = c->opts[i];
+      const double rate = lrs ? (double)lrs[i] : (double)lr;
+      OptHp& h = hp[i];
+      h.kind = (float)o.kind;
+      h.lr = (float)rate;
+      h.eps = (float)o.eps;
+      if (o.kind == UN_OPT_MOMENTUM) {
+        h.b1 = (float)o.momentum;
+      } else if (o.kind == UN_OPT_ADAM) {
+        const double t = (double)(o.t + 1);  // this step's count
+        h.b1 = (float)o.beta1;
+        h.b2 = (float)o.beta2;
+        h.c1 = (float)(1.0 - o.beta1);
+        h.c2 = (float)(1.0 - o.beta2);
+        h.lr = (float)(rate / (1.0 - std::pow(o.beta1, t)));
+        h.isb2 = (float)(1.0 / std::sqrt(1.0 - std::pow(o.beta2, t)));
+      }
+    }
+    HIPCHK(c, launch_set_values(c->at<float>(c->opt_dev), (const float*)hp.data(), (int)(n * OPT_FLOATS), c->stream));
+    c->optp = c->at<OptHp>(c->opt_dev);
+  } else if (lrs) {
+    HIPCHK(c, launch_set_values(c->at<float>(c->lr_dev), lrs, (int)n, c->stream));
+    c->lrv = c->at<float>(c->lr_dev);
+  }
   for (auto& l : c->fwd) HIPCHK(c, run_launch(c, l, lr));
   HIPCHK(c, run_launch(c, c->ce, lr));
   for (auto& l : c->bwd[c->wt_cur]) HIPCHK(c, run_launch(c, l, lr));
+  for (size_t i = 0; i < n; ++i)
+    if (c->active[i]) ++c->opts[i].t;
   c->wt_cur ^= 1;
   c->stepped = true;
   c->grads_valid = c->keep_grads;
@@ -1501,9 +1578,125 @@ un_status un_step_lr(un_ctx* c, const float* lrs, float* losses) {
   if (!c->loaded) return fail(c, UN_ERR_STATE, "un_step_lr before un_load_batch");
   for (size_t i = 0; i < c->models.size(); ++i)
     if (!std::isfinite(lrs[i])) return fail(c, UN_ERR_INVALID, "lr of model " + std::to_string(i) + " is not finite");
-  // the rates travel in the kernel arguments, ordered before the step on the stream
-  HIPCHK(c, launch_set_values(c->at<float>(c->lr_dev), lrs, (int)c->models.size(), c->stream));
-  return step_common(c, 0.f, c->at<float>(c->lr_dev), losses);
+  // the rates travel in kernel arguments, ordered before the step on the stream
+  return step_common(c, 0.f, lrs, losses);
+}
+
+// ---- optimizers -----------------------------------------------------------
+// The state allocation mirrors the parameter layout: one momentum / first
+// moment and one second moment per parameter, for every model (made once, on
+// the first optimizer that needs state; the step's tables are rebuilt to point
+// at it).
+static un_status alloc_state(un_ctx* c) {
+  Arena S;
+  auto& pl = c->plan;
+  if (!pl.cat.empty()) {
+    pl.catS1 = S.take((size_t)pl.cat_rows * pl.kin_p * 4);
+    pl.catS1b = S.take((size_t)pl.cat_rows * 4);
+    pl.catS2 = S.take((size_t)pl.cat_rows * pl.kin_p * 4);
+    pl.catS2b = S.take((size_t)pl.cat_rows * 4);
+  }
+  for (size_t mi = 0; mi < c->models.size(); ++mi)
+    for (auto& b : c->models[mi].blocks) {
+      if (b.concat) {
+        const size_t roff = (size_t)pl.cat_off[mi];
+        b.S1 = pl.catS1 + roff * b.ldw * 4;
+        b.S2 = pl.catS2 + roff * b.ldw * 4;
+        b.S1b = pl.catS1b + roff * 4;
+        b.S2b = pl.catS2b + roff * 4;
+      } else {
+        b.S1 = S.take((size_t)b.rows * b.ldw * 4);
+        b.S1b = S.take((size_t)b.rows * 4);
+        b.S2 = S.take((size_t)b.rows * b.ldw * 4);
+        b.S2b = S.take((size_t)b.rows * 4);
+      }
+    }
+  char* p = nullptr;
+  hipError_t e = hipMalloc((void**)&p, S.top);
+  if (e != hipSuccess) return fail(c, UN_ERR_OOM, "optimizer state: hipMalloc of " + std::to_string(S.top) + " bytes failed");
+  HIPCHK(c, hipMemsetAsync(p, 0, S.top, c->stream));
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  c->sbase = p;
+  c->sbytes = S.top;
+  Tables T;
+  build_tables(c, T);
+  return install_tables(c, T);
+}
+
+// Zero model i's optimizer state.
+static un_status clear_state(un_ctx* c, int i) {
+  if (!c->sbase) return UN_OK;
+  for (auto& b : c->models[i].blocks) {
+    HIPCHK(c, hipMemsetAsync(c->sbase + b.S1, 0, (size_t)b.rows * b.ldw * 4, c->stream));
+    HIPCHK(c, hipMemsetAsync(c->sbase + b.S2, 0, (size_t)b.rows * b.ldw * 4, c->stream));
+    HIPCHK(c, hipMemsetAsync(c->sbase + b.S1b, 0, (size_t)b.rows * 4, c->stream));
+    HIPCHK(c, hipMemsetAsync(c->sbase + b.S2b, 0, (size_t)b.rows * 4, c->stream));
+  }
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  return UN_OK;
+}
+
+static int state_tensors(int kind) { return kind == UN_OPT_ADAM ? 2 : kind == UN_OPT_MOMENTUM ? 1 : 0; }
+
+un_status un_set_optimizer(un_ctx* c, int32_t i, const un_optimizer* o) {
+  CHECK_CTX(c);
+  if (i < 0 || i >= (int)c->models.size()) return fail(c, UN_ERR_RANGE, "model index out of range");
+  if (!o) return fail(c, UN_ERR_INVALID, "optimizer is NULL");
+  auto unit = [](float x) { return std::isfinite(x) && x >= 0.f && x < 1.f; };
+  if (o->kind != UN_OPT_SGD && o->kind != UN_OPT_MOMENTUM && o->kind != UN_OPT_ADAM)
+    return fail(c, UN_ERR_INVALID, "unknown optimizer kind");
+  if (o->kind == UN_OPT_MOMENTUM && !unit(o->momentum)) return fail(c, UN_ERR_INVALID, "momentum must be in [0, 1)");
+  if (o->kind == UN_OPT_ADAM && (!unit(o->beta1) || !unit(o->beta2) || !std::isfinite(o->eps) || !(o->eps > 0.f)))
+    return fail(c, UN_ERR_INVALID, "Adam needs beta1, beta2 in [0, 1) and eps > 0");
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  if (o->kind != UN_OPT_SGD && !c->sbase) {
+    un_status st = alloc_state(c);
+    if (st != UN_OK) return st;
+  }
+  un_status st = clear_state(c, i);
+  if (st != UN_OK) return st;
+  un_ctx::Opt& d = c->opts[i];
+  d.kind = o->kind;
+  d.momentum = o->momentum;
+  d.beta1 = o->beta1;
+  d.beta2 = o->beta2;
+  d.eps = o->eps;
+  d.t = 0;
+  c->any_opt = false;
+  for (auto& x : c->opts) c->any_opt = c->any_opt || x.kind != UN_OPT_SGD;
+  return UN_OK;
+}
+
+un_status un_get_opt_state(un_ctx* c, int32_t i, float* dst, size_t cap, size_t* n, int64_t* step) {
+  CHECK_CTX(c);
+  if (i < 0 || i >= (int)c->models.size()) return fail(c, UN_ERR_RANGE, "model index out of range");
+  const int k = state_tensors(c->opts[i].kind);
+  const size_t np = c->models[i].n_params;
+  if (n) *n = k * np;
+  if (step) *step = c->opts[i].t;
+  if (!dst || k == 0) return UN_OK;
+  if (cap < k * np) return fail(c, UN_ERR_BUFSIZE, "buffer holds " + std::to_string(cap) + " < " + std::to_string(k * np));
+  un_status st = read_blocks(c, i, c->sbase, &Block::S1, &Block::S1b, dst);
+  if (st == UN_OK && k == 2) st = read_blocks(c, i, c->sbase, &Block::S2, &Block::S2b, dst + np);
+  return st;
+}
+
+un_status un_set_opt_state(un_ctx* c, int32_t i, const float* src, size_t n, int64_t step) {
+  CHECK_CTX(c);
+  if (i < 0 || i >= (int)c->models.size()) return fail(c, UN_ERR_RANGE, "model index out of range");
+  const int k = state_tensors(c->opts[i].kind);
+  const size_t np = c->models[i].n_params;
+  if (n != k * np) return fail(c, UN_ERR_BUFSIZE, "state of this optimizer holds " + std::to_string(k * np) + " floats");
+  if (step < 0) return fail(c, UN_ERR_INVALID, "negative step count");
+  if (k > 0 && !src) return fail(c, UN_ERR_INVALID, "src is NULL");
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  if (k > 0) {
+    un_status st = write_blocks(c, i, c->sbase, &Block::S1, &Block::S1b, src);
+    if (st == UN_OK && k == 2) st = write_blocks(c, i, c->sbase, &Block::S2, &Block::S2b, src + np);
+    if (st != UN_OK) return st;
+  }
+  c->opts[i].t = step;
+  return UN_OK;
 }
 
 un_status un_load_labels(un_ctx* c, const int32_t* y) {
@@ -1654,6 +1847,7 @@ void un_destroy(un_ctx* c) {
   }
   for (auto e : c->free_events) hipEventDestroy(e);
   if (c->base) hipFree(c->base);
+  if (c->sbase) hipFree(c->sbase);
   if (c->stream) hipStreamDestroy(c->stream);
   delete c;
 }

@@ -21,12 +21,14 @@ UN_OK, UN_ERR_INVALID, UN_ERR_STATE, UN_ERR_OOM, UN_ERR_DEVICE, UN_ERR_RANGE, UN
 STATUS_NAMES = ["UN_OK", "UN_ERR_INVALID", "UN_ERR_STATE", "UN_ERR_OOM", "UN_ERR_DEVICE", "UN_ERR_RANGE",
                 "UN_ERR_BUFSIZE", "UN_ERR_UNSUPPORTED"]
 UN_F32, UN_BF16_F32MASTER = 0, 1
+UN_OPT_SGD, UN_OPT_MOMENTUM, UN_OPT_ADAM = 0, 1, 2
+OPT_KINDS = {"sgd": UN_OPT_SGD, "momentum": UN_OPT_MOMENTUM, "adam": UN_OPT_ADAM}
 OPS = {"linear": 0, "conv": 1, "relu": 2, "pool": 3, "flatten": 4}
 KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad", "ce", "sgd", "other"]
 
 # Every symbol the header declares.
 EXPORTS = ["un_create", "un_load_batch", "un_load_batch_device", "un_load_labels", "un_step", "un_step_lr",
-           "un_set_active", "un_get_params",
+           "un_set_active", "un_set_optimizer", "un_get_opt_state", "un_set_opt_state", "un_get_params",
            "un_set_params", "un_get_grads", "un_keep_grads", "un_param_count", "un_arena_bytes", "un_sync", "un_get_stream",
            "un_profile_enable", "un_profile_read", "un_destroy", "un_last_error"]
 
@@ -43,6 +45,11 @@ class un_model_spec(ctypes.Structure):
 class un_input_spec(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("in_c", ctypes.c_int32), ("in_h", ctypes.c_int32),
                 ("in_w", ctypes.c_int32), ("precision", ctypes.c_int32)]
+
+
+class un_optimizer(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("momentum", ctypes.c_float), ("beta1", ctypes.c_float),
+                ("beta2", ctypes.c_float), ("eps", ctypes.c_float)]
 
 
 class UnError(RuntimeError):
@@ -71,6 +78,10 @@ def lib():
             "un_load_batch_device": (ctypes.c_int, [P, P, P]),
             "un_step": (ctypes.c_int, [P, ctypes.c_float, f]),
             "un_step_lr": (ctypes.c_int, [P, f, f]),
+            "un_set_optimizer": (ctypes.c_int, [P, ctypes.c_int32, ctypes.POINTER(un_optimizer)]),
+            "un_get_opt_state": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t, c_size_p,
+                                                ctypes.POINTER(ctypes.c_int64)]),
+            "un_set_opt_state": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t, ctypes.c_int64]),
             "un_load_labels": (ctypes.c_int, [P, ctypes.POINTER(ctypes.c_int32)]),
             "un_set_active": (ctypes.c_int, [P, ctypes.POINTER(ctypes.c_uint8)]),
             "un_get_params": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t, c_size_p]),
@@ -204,6 +215,29 @@ def un_get_grads(ctx, i):
     return out
 
 
+def un_set_optimizer(ctx, i, kind="sgd", momentum=0.0, betas=(0.9, 0.999), eps=1e-8):
+    if kind not in OPT_KINDS:
+        raise ValueError(f"optimizer kind must be one of {sorted(OPT_KINDS)}")
+    o = un_optimizer(OPT_KINDS[kind], float(momentum), float(betas[0]), float(betas[1]), float(eps))
+    _check(lib().un_set_optimizer(ctx, i, ctypes.byref(o)), ctx)
+
+
+def un_get_opt_state(ctx, i):
+    """(flat fp32 state [k * n_params], update count) of model i's optimizer."""
+    n = ctypes.c_size_t()
+    step = ctypes.c_int64()
+    _check(lib().un_get_opt_state(ctx, i, None, 0, ctypes.byref(n), ctypes.byref(step)), ctx)
+    out = np.empty(n.value, dtype=np.float32)
+    if n.value:
+        _check(lib().un_get_opt_state(ctx, i, _fp(out), n.value, ctypes.byref(n), ctypes.byref(step)), ctx)
+    return out, int(step.value)
+
+
+def un_set_opt_state(ctx, i, state, step):
+    state = np.ascontiguousarray(state, dtype=np.float32).reshape(-1)
+    _check(lib().un_set_opt_state(ctx, i, _fp(state) if state.size else None, state.size, int(step)), ctx)
+
+
 def un_keep_grads(ctx, on):
     _check(lib().un_keep_grads(ctx, 1 if on else 0), ctx)
 
@@ -268,6 +302,9 @@ class Hybrid:
         self.specs = list(specs)
         self.n = len(self.specs)
         self.batch = int(batch)
+        self.in_shape = tuple(in_shape)
+        self.precision = precision
+        self.optimizers = {i: dict(kind="sgd", momentum=0.0, betas=[0.9, 0.999], eps=1e-8) for i in range(self.n)}
         self.ctx = un_create(self.specs, batch, in_shape, precision, seeds)
 
     def close(self):
@@ -310,6 +347,18 @@ class Hybrid:
 
     def get_grads(self, i):
         return un_get_grads(self.ctx, i)
+
+    def set_optimizer(self, i, kind="sgd", momentum=0.0, betas=(0.9, 0.999), eps=1e-8):
+        """Fresh optimizer for model i ("sgd", "momentum" or "adam")."""
+        un_set_optimizer(self.ctx, i, kind, momentum, betas, eps)
+        self.optimizers[i] = dict(kind=kind, momentum=float(momentum), betas=[float(b) for b in betas],
+                                  eps=float(eps))
+
+    def get_opt_state(self, i):
+        return un_get_opt_state(self.ctx, i)
+
+    def set_opt_state(self, i, state, step):
+        un_set_opt_state(self.ctx, i, state, step)
 
     def keep_grads(self, on=True):
         un_keep_grads(self.ctx, on)
