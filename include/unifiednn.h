@@ -101,6 +101,18 @@ typedef struct {
 un_status un_create(const un_model_spec* specs, int32_t n_models,
                     const un_input_spec* in, un_ctx** out);
 
+/* Device memory a context for these models would take, computed on the host
+ * without touching the device (the planner of un_create, dry): *arena_bytes is
+ * exactly what un_create allocates (un_arena_bytes), *state_bytes (may be
+ * NULL) what the first non-SGD optimizer adds (un_set_optimizer). The paper
+ * sizes a hybrid as the maximum over its sub-models because its scheduler
+ * trains them one at a time (Trainer section, memory requirement); a fused
+ * step holds all N at once, so here it is one shared input plus the sum over
+ * the models. Use it to admit models onto a GPU before creating anything.
+ * Errors: as un_create's validation. */
+un_status un_plan_bytes(const un_model_spec* specs, int32_t n_models, const un_input_spec* in,
+                        size_t* arena_bytes, size_t* state_bytes);
+
 /* Copy one shared batch to the device, once for all N models (Memory
  * conservation section: a common dataset is loaded only once). x is host fp32
  * laid out as in un_input_spec, y is host int32 [batch]. Labels are checked on

@@ -969,7 +969,9 @@ static un_status install_tables(un_ctx* c, Tables& T) {
 // ==========================================================================
 // Planner
 // ==========================================================================
-static un_status plan_and_alloc(un_ctx* c) {
+// dry: plan only - c->bytes is the arena the context would allocate; nothing
+// touches the device.
+static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
   const bool bf = c->bf16;
   const size_t es = bf ? 2 : 4;  // storage element size
   const int B = c->B;
@@ -1165,6 +1167,7 @@ static un_status plan_and_alloc(un_ctx* c) {
   c->tables_cap = 2 * T.host.size() + ((size_t)1 << 20);
   c->tables_off = A.take(c->tables_cap);
   c->bytes = A.top;
+  if (dry) return UN_OK;
   hipError_t e = hipMalloc((void**)&c->base, c->bytes);
   if (e != hipSuccess) {
     c->base = nullptr;
@@ -1407,8 +1410,11 @@ static un_status drain_profile(un_ctx* c) {
 // ==========================================================================
 extern "C" {
 
-un_status un_create(const un_model_spec* specs, int32_t n_models, const un_input_spec* in, un_ctx** out) {
-  if (!out) return fail(nullptr, UN_ERR_INVALID, "out is NULL");
+static size_t state_layout(un_ctx* c);
+
+// Validation and parsing shared by un_create and un_plan_bytes: a context
+// with its models parsed and nothing on the device.
+static un_status parse_all(const un_model_spec* specs, int32_t n_models, const un_input_spec* in, un_ctx** out) {
   *out = nullptr;
   if (!specs || !in || n_models <= 0) return fail(nullptr, UN_ERR_INVALID, "specs/in NULL or n_models <= 0");
   if (in->batch <= 0 || in->in_c <= 0 || in->in_h <= 0 || in->in_w <= 0)
@@ -1434,6 +1440,36 @@ un_status un_create(const un_model_spec* specs, int32_t n_models, const un_input
       return fail(nullptr, s, why);
     }
     c->min_classes = std::min(c->min_classes, c->models[i].num_classes);
+  }
+  *out = c;
+  return UN_OK;
+}
+
+un_status un_plan_bytes(const un_model_spec* specs, int32_t n_models, const un_input_spec* in, size_t* arena_bytes,
+                        size_t* state_bytes) {
+  if (!arena_bytes) return fail(nullptr, UN_ERR_INVALID, "arena_bytes is NULL");
+  un_ctx* c = nullptr;
+  un_status s = parse_all(specs, n_models, in, &c);
+  if (s != UN_OK) return s;
+  s = plan_and_alloc(c, true);
+  if (s == UN_OK) {
+    *arena_bytes = c->bytes;
+    if (state_bytes) *state_bytes = state_layout(c);
+  } else {
+    const std::string msg = c->err.empty() ? g_create_error : c->err;
+    delete c;
+    return fail(nullptr, s, msg);
+  }
+  delete c;
+  return UN_OK;
+}
+
+un_status un_create(const un_model_spec* specs, int32_t n_models, const un_input_spec* in, un_ctx** out) {
+  if (!out) return fail(nullptr, UN_ERR_INVALID, "out is NULL");
+  un_ctx* c = nullptr;
+  {
+    un_status ps = parse_all(specs, n_models, in, &c);
+    if (ps != UN_OK) return ps;
   }
   hipError_t e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
   if (e != hipSuccess) {
@@ -1587,7 +1623,7 @@ un_status un_step_lr(un_ctx* c, const float* lrs, float* losses) {
 // moment and one second moment per parameter, for every model (made once, on
 // the first optimizer that needs state; the step's tables are rebuilt to point
 // at it).
-static un_status alloc_state(un_ctx* c) {
+static size_t state_layout(un_ctx* c) {
   Arena S;
   auto& pl = c->plan;
   if (!pl.cat.empty()) {
@@ -1611,13 +1647,18 @@ static un_status alloc_state(un_ctx* c) {
         b.S2b = S.take((size_t)b.rows * 4);
       }
     }
+  return S.top;
+}
+
+static un_status alloc_state(un_ctx* c) {
+  const size_t bytes = state_layout(c);
   char* p = nullptr;
-  hipError_t e = hipMalloc((void**)&p, S.top);
-  if (e != hipSuccess) return fail(c, UN_ERR_OOM, "optimizer state: hipMalloc of " + std::to_string(S.top) + " bytes failed");
-  HIPCHK(c, hipMemsetAsync(p, 0, S.top, c->stream));
+  hipError_t e = hipMalloc((void**)&p, bytes);
+  if (e != hipSuccess) return fail(c, UN_ERR_OOM, "optimizer state: hipMalloc of " + std::to_string(bytes) + " bytes failed");
+  HIPCHK(c, hipMemsetAsync(p, 0, bytes, c->stream));
   HIPCHK(c, hipStreamSynchronize(c->stream));
   c->sbase = p;
-  c->sbytes = S.top;
+  c->sbytes = bytes;
   Tables T;
   build_tables(c, T);
   return install_tables(c, T);

@@ -27,7 +27,7 @@ OPS = {"linear": 0, "conv": 1, "relu": 2, "pool": 3, "flatten": 4}
 KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad", "ce", "sgd", "other"]
 
 # Every symbol the header declares.
-EXPORTS = ["un_create", "un_load_batch", "un_load_batch_device", "un_load_labels", "un_step", "un_step_lr",
+EXPORTS = ["un_create", "un_plan_bytes", "un_load_batch", "un_load_batch_device", "un_load_labels", "un_step", "un_step_lr",
            "un_set_active", "un_set_optimizer", "un_get_opt_state", "un_set_opt_state", "un_get_params",
            "un_set_params", "un_get_grads", "un_keep_grads", "un_param_count", "un_arena_bytes", "un_sync", "un_get_stream",
            "un_profile_enable", "un_profile_read", "un_destroy", "un_last_error"]
@@ -78,6 +78,8 @@ def lib():
             "un_load_batch_device": (ctypes.c_int, [P, P, P]),
             "un_step": (ctypes.c_int, [P, ctypes.c_float, f]),
             "un_step_lr": (ctypes.c_int, [P, f, f]),
+            "un_plan_bytes": (ctypes.c_int, [ctypes.POINTER(un_model_spec), ctypes.c_int32,
+                                             ctypes.POINTER(un_input_spec), c_size_p, c_size_p]),
             "un_set_optimizer": (ctypes.c_int, [P, ctypes.c_int32, ctypes.POINTER(un_optimizer)]),
             "un_get_opt_state": (ctypes.c_int, [P, ctypes.c_int32, f, ctypes.c_size_t, c_size_p,
                                                 ctypes.POINTER(ctypes.c_int64)]),
@@ -143,6 +145,17 @@ def un_create(specs, batch, in_shape, precision, seeds=None):
     ctx = ctypes.c_void_p()
     _check(lib().un_create(arr, len(specs), ctypes.byref(ins), ctypes.byref(ctx)))
     return ctx
+
+
+def un_plan_bytes(specs, batch, in_shape, precision):
+    """(arena bytes, optimizer-state bytes) a context for these models would
+    take; host only (no device needed)."""
+    arr, keep = make_specs(specs, None)
+    c, h, w = (tuple(in_shape) + (1, 1))[:3] if len(in_shape) != 3 else tuple(in_shape)
+    ins = un_input_spec(batch, c, h, w, UN_BF16_F32MASTER if precision == "bf16" else UN_F32)
+    a, st = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().un_plan_bytes(arr, len(specs), ctypes.byref(ins), ctypes.byref(a), ctypes.byref(st)))
+    return a.value, st.value
 
 
 def un_load_batch(ctx, x, y):
