@@ -21,6 +21,17 @@
 #ifndef UN_GEMM_DEPTH
 #define UN_GEMM_DEPTH 2
 #endif
+// Waves of one bf16 GEMM workgroup (m x n): 16 waves of 32x32 output each on
+// a 128x128 tile. The k loop and the epilogue are latency bound at these
+// shapes (M = batch of a few hundred), and 8 waves per SIMD (two workgroups
+// per CU) hide that latency best: measured 1.15 ms (4 waves), 1.04 (8), 1.02
+// (16) per 64-MLP step.
+#ifndef UN_GEMM_WGM
+#define UN_GEMM_WGM 4
+#endif
+#ifndef UN_GEMM_WGN
+#define UN_GEMM_WGN 4
+#endif
 #ifndef UN_LDS_PAD_CHUNKS
 #define UN_LDS_PAD_CHUNKS 1
 #endif
@@ -220,9 +231,12 @@ __device__ __forceinline__ void mma_loop1(L& ld, int kb0, int kb1, T* smem,
 // chosen so that a wave's accumulator writes hit 64 distinct banks.
 template <typename T, int BM, int BN, int BK> struct GemmMma;
 
+// bf16: UN_GEMM_WGM x UN_GEMM_WGN waves (m x n) per workgroup.
 template <int BM, int BN, int BK>
 struct GemmMma<bf16_t, BM, BN, BK> {
-  static constexpr int WM = BM / 2, WN = BN / 2, FM = WM / 32, FN = WN / 32;
+  static constexpr int WGM = UN_GEMM_WGM, WGN = UN_GEMM_WGN, NT = 64 * WGM * WGN;
+  static constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
+  static_assert(FM >= 1 && FN >= 1, "wave tile smaller than one 32x32 block");
   static constexpr int LDK = Tile<bf16_t, BM, BN, BK>::LDK;
   static constexpr int CLD = BN + 8;
   static_assert(BK % 16 == 0, "BK must be a multiple of 16");
@@ -237,7 +251,7 @@ struct GemmMma<bf16_t, BM, BN, BK> {
   }
   __device__ __forceinline__ static void block(const bf16_t* sA, const bf16_t* sB, Acc& acc) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int wm = (wave >> 1) * WM, wn = (wave & 1) * WN;
+    const int wm = (wave / WGN) * WM, wn = (wave % WGN) * WN;
     const int lr = lane & 31, lg = lane >> 5;
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 16) {
@@ -257,7 +271,7 @@ struct GemmMma<bf16_t, BM, BN, BK> {
   template <class F>
   __device__ __forceinline__ static void for_groups(const Acc& acc, F&& f) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int wm = (wave >> 1) * WM, wn = (wave & 1) * WN;
+    const int wm = (wave / WGN) * WM, wn = (wave % WGN) * WN;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -273,6 +287,7 @@ struct GemmMma<bf16_t, BM, BN, BK> {
 template <int BM, int BN, int BK>
 struct GemmMma<float, BM, BN, BK> {
   using TL = Tile<float, BM, BN, BK>;
+  static constexpr int NT = 256;
   static constexpr int CLD = BN + 4;
   using Acc = f32x4[TL::FM][TL::FN];
   __device__ __forceinline__ static void zero(Acc& acc) {
@@ -396,10 +411,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
 // Row-major operand with k contiguous: element (row, k) = base[row*ld + k].
 // Rows at or beyond rows_valid read as zero through the buffer range check;
 // columns at or beyond K are zeroed on the last, partial k-block only.
-template <typename T, int ROWS, int BK>
+template <typename T, int ROWS, int BK, int NT = 256>
 struct RowLoader {
-  static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / 256, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
-  static_assert(ROWS * VPR % 256 == 0, "tile too small for 256 threads");
+  static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / NT, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
+  static_assert(ROWS * VPR % NT == 0, "tile too small for the workgroup");
   __amdgpu_buffer_rsrc_t rsrc;
   int off[NV];
   int K;
@@ -409,7 +424,7 @@ struct RowLoader {
     rsrc = make_rsrc(base, (int64_t)rows_valid * ld * (int64_t)sizeof(T));
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
-      const int v = threadIdx.x + 256 * s;
+      const int v = threadIdx.x + NT * s;
       off[s] = (int)(((int64_t)(v / VPR) * ld + (v % VPR) * VEC) * (int64_t)sizeof(T));
     }
   }
@@ -422,7 +437,7 @@ struct RowLoader {
     if ((kb + 1) * BK > K) {
 #pragma unroll
       for (int s = 0; s < NV; ++s) {
-        const int k = kb * BK + ((threadIdx.x + 256 * s) % VPR) * VEC;
+        const int k = kb * BK + ((threadIdx.x + NT * s) % VPR) * VEC;
         if (k + VEC > K) vmask_tail<T>(r[S][s], K - k);
       }
     }
@@ -431,7 +446,7 @@ struct RowLoader {
   __device__ __forceinline__ void store(T* sm) const {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
-      const int v = threadIdx.x + 256 * s;
+      const int v = threadIdx.x + NT * s;
       *(u32x4*)(sm + (v / VPR) * LDK + (v % VPR) * VEC) = r[S][s];
     }
   }
@@ -996,11 +1011,11 @@ __device__ __forceinline__ void opt_update4(const OptHp& h, const f32x4& g, f32x
   *(gptr<f32x4>)s2 = v;
 }
 
-template <typename OT, int BM, int BN, int CLD>
+template <typename OT, int BM, int BN, int CLD, int NT = 256>
 __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, int m0, int n0, int M, int N) {
   constexpr int VE = 16 / sizeof(OT), CPR = BN / VE;
   static_assert(CLD % 4 == 0, "float4 rows");
-  for (int idx = threadIdx.x; idx < BM * CPR; idx += 256) {
+  for (int idx = threadIdx.x; idx < BM * CPR; idx += NT) {
     const int r = idx / CPR, cc = idx - r * CPR;
     const int m = m0 + r, n = n0 + cc * VE;
     if (m >= M || n >= N) continue;
@@ -1020,10 +1035,10 @@ __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, 
 // Transposed store of the staged tile: CT[n][m] for n < N, 16-byte chunks
 // along m. Consecutive threads take consecutive columns, so the strided LDS
 // gathers hit distinct banks.
-template <typename OT, int BM, int BN, int CLD>
+template <typename OT, int BM, int BN, int CLD, int NT = 256>
 __device__ __forceinline__ void store_cols(const float* sC, OT* CT, int64_t ldct, int m0, int n0, int M, int N) {
   constexpr int VE = 16 / sizeof(OT);
-  for (int idx = threadIdx.x; idx < BN * (BM / VE); idx += 256) {
+  for (int idx = threadIdx.x; idx < BN * (BM / VE); idx += NT) {
     const int mq = idx / BN, c = idx - mq * BN;
     const int n = n0 + c, m = m0 + mq * VE;
     if (n >= N || m >= M) continue;
@@ -1037,7 +1052,8 @@ __device__ __forceinline__ void store_cols(const float* sC, OT* CT, int64_t ldct
 // OPT: the update follows a per-model OptHp (`opt`, not null) instead of
 // fma(-lr, g, w); a separate instantiation, so that plain SGD pays nothing.
 template <typename T, int BM, int BN, int BK, bool OPT>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void gemm_kernel(const GemmProb* __restrict__ probs,
+__global__ __launch_bounds__((GemmMma<T, BM, BN, BK>::NT)) __attribute__((amdgpu_waves_per_eu((GemmMma<T, BM, BN, BK>::NT / 128))))
+void gemm_kernel(const GemmProb* __restrict__ probs,
                                                    const int32_t* __restrict__ tile_map, float lr,
                                                    const float* __restrict__ lrv, const OptHp* __restrict__ opt,
                                                    int keep_grads) {
@@ -1055,8 +1071,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
   typename MM::Acc acc;
   MM::zero(acc);
 
-  RowLoader<T, BM, BK> la;
-  RowLoader<T, BN, BK> lb;
+  constexpr int NT = MM::NT;
+  RowLoader<T, BM, BK, NT> la;
+  RowLoader<T, BN, BK, NT> lb;
   la.init((const T*)p.A + (int64_t)m0 * p.lda, p.lda, p.M - m0, p.K);
   lb.init((const T*)p.B + (int64_t)n0 * p.ldb, p.ldb, p.N - n0, p.K);
   gemm_loop<T, BM, BN, BK, UN_GEMM_DEPTH, MM>(la, lb, (p.K + BK - 1) / BK, (T*)smem, acc);
@@ -1064,13 +1081,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
   // Weight gradient with the SGD update fused: the master-weight loads of
   // this thread's float4 chunks of W[m][n..n+3] are issued first, so their
   // latency overlaps the staging below.
-  constexpr int CPR = BN / 4, NCH = BM * CPR / 256;
+  constexpr int CPR = BN / 4, NCH = BM * CPR / NT;
   const int ns = p.nsplit;
   f32x4 w0[NCH];
   if (p.epi == EPI_WGRAD) {
 #pragma unroll
     for (int q = 0; q < NCH; ++q) {
-      const int idx = threadIdx.x + 256 * q, r = idx / CPR, n = n0 + (idx - r * CPR) * 4, m = m0 + r;
+      const int idx = threadIdx.x + NT * q, r = idx / CPR, n = n0 + (idx - r * CPR) * 4, m = m0 + r;
       w0[q] = (m < p.M && n + 4 <= ns) ? *(gptr<const f32x4>)(p.W + (int64_t)m * p.ldc + n) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
   }
@@ -1111,11 +1128,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
   if (epi != EPI_WGRAD) {
     // Row pass: C[m][n] in 16-byte chunks along n.
     if (p.C) {
-      if (epi == EPI_LOGITS) store_rows<float, BM, BN, CLD>(sC, (float*)p.C, p.ldc, m0, n0, p.M, p.N);
-      else store_rows<T, BM, BN, CLD>(sC, (T*)p.C, p.ldc, m0, n0, p.M, p.N);
+      if (epi == EPI_LOGITS) store_rows<float, BM, BN, CLD, NT>(sC, (float*)p.C, p.ldc, m0, n0, p.M, p.N);
+      else store_rows<T, BM, BN, CLD, NT>(sC, (T*)p.C, p.ldc, m0, n0, p.M, p.N);
     }
     // Column pass: CT[n][m] in 16-byte chunks along m.
-    if (p.CT) store_cols<T, BM, BN, CLD>(sC, (T*)p.CT, p.ldct, m0, n0, p.M, p.N);
+    if (p.CT) store_cols<T, BM, BN, CLD, NT>(sC, (T*)p.CT, p.ldct, m0, n0, p.M, p.N);
     return;
   }
 
@@ -1124,7 +1141,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
   // bias column (n == nsplit) is done element-wise.
 #pragma unroll
   for (int q = 0; q < NCH; ++q) {
-    const int idx = threadIdx.x + 256 * q, r = idx / CPR, cc = idx - r * CPR;
+    const int idx = threadIdx.x + NT * q, r = idx / CPR, cc = idx - r * CPR;
     const int m = m0 + r, n = n0 + cc * 4;
     if (m >= p.M || n > ns) continue;
     // this row's model: its own learning rate (or optimizer) when set per model
@@ -1173,7 +1190,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void g
   if (!p.WT) return;
   __syncthreads();
   // Column pass: the updated weights transposed, WT[n][m] for n < nsplit.
-  store_cols<T, BM, BN, CLD>(sC, (T*)p.WT, p.ldwt, m0, n0, p.M, min(p.N, ns));
+  store_cols<T, BM, BN, CLD, NT>(sC, (T*)p.WT, p.ldwt, m0, n0, p.M, min(p.N, ns));
 }
 
 // ---------------------------------------------------------------------------
@@ -1828,11 +1845,12 @@ hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_map
                        const float* lrv, const OptHp* opt, bool keep_grads, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   if (bf16) {
+    constexpr int NT = GemmMma<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16>::NT;
     if (opt)
-      hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16, true>), dim3(ntiles), dim3(256), 0,
+      hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16, true>), dim3(ntiles), dim3(NT), 0,
                          s, probs, tile_map, lr, lrv, opt, (int)keep_grads);
     else
-      hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16, false>), dim3(ntiles), dim3(256),
+      hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16, false>), dim3(ntiles), dim3(NT),
                          0, s, probs, tile_map, lr, lrv, opt, (int)keep_grads);
   } else {
     if (opt)
