@@ -32,6 +32,9 @@
 #ifndef UN_GEMM_WGN
 #define UN_GEMM_WGN 4
 #endif
+#ifndef UN_HALO_WAVES
+#define UN_HALO_WAVES 8
+#endif
 #ifndef UN_LDS_PAD_CHUNKS
 #define UN_LDS_PAD_CHUNKS 1
 #endif
@@ -110,12 +113,19 @@ __device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
 // ---------------------------------------------------------------------------
 // MFMA core
 // ---------------------------------------------------------------------------
-template <typename T, int BM, int BN, int BK>
+// NW waves per workgroup: 4 as 2 x 2 (m x n), 8 as 2 x 4, 16 as 4 x 4.
+template <typename T, int BM, int BN, int BK, int NW = 4>
 struct Tile {
   static constexpr int VEC = TT<T>::VEC;
   static constexpr int LDK = BK + UN_LDS_PAD_CHUNKS * VEC;  // LDS row stride in elements (16-byte pad chunks)
-  static constexpr int WM = BM / 2, WN = BN / 2;
+  static constexpr int WGN = NW == 4 ? 2 : 4, WGM = NW / WGN, NT = 64 * NW;
+  static constexpr int WM = BM / WGM, WN = BN / WGN;
   static constexpr int FM = WM / 16, FN = WN / 16;
+  static_assert(NW == 4 || NW == 8 || NW == 16, "4, 8 or 16 waves");
+  static_assert(FM >= 1 && FN >= 1, "wave tile smaller than one 16x16 block");
+  // this wave's first row and column in the tile
+  __device__ __forceinline__ static int wave_m() { return ((int)(threadIdx.x >> 6) / WGN) * WM; }
+  __device__ __forceinline__ static int wave_n() { return ((int)(threadIdx.x >> 6) % WGN) * WN; }
   static constexpr int A_ELEMS = BM * LDK, B_ELEMS = BN * LDK;
   static_assert(BK % TT<T>::KSTEP == 0, "BK must be a multiple of the MFMA k step");
 };
@@ -1210,13 +1220,13 @@ struct ConvEpiSmem {
 // the pooled value, its one-hot argmax and the optional transposed copy,
 // stored straight from registers (staging this small output in LDS measured
 // slower).
-template <typename T, int BM, int BN, int BK>
+template <typename T, int BM, int BN, int BK, int NW = 4>
 __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int n0,
-                                                  const f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN],
+                                                  const f32x4 (&acc)[Tile<T, BM, BN, BK, NW>::FM][Tile<T, BM, BN, BK, NW>::FN],
                                                   char*) {
-  using TL = Tile<T, BM, BN, BK>;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
+  using TL = Tile<T, BM, BN, BK, NW>;
+  const int lane = threadIdx.x & 63;
+  const int wm = TL::wave_m(), wn = TL::wave_n();
   const int O = p.O;
 #pragma unroll
   for (int i = 0; i < TL::FM; ++i) {
@@ -1269,15 +1279,15 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
 
 // Conv data-gradient epilogue: the previous block's ReLU' (its stored output
 // > 0) and the store of the gradient at that output, in 16-byte vectors.
-template <typename T, int BM, int BN, int BK>
+template <typename T, int BM, int BN, int BK, int NW = 4>
 __device__ __forceinline__ void conv_dgrad_epilogue(const ConvProb& p, int m0, int n0,
-                                                    const f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN],
+                                                    const f32x4 (&acc)[Tile<T, BM, BN, BK, NW>::FM][Tile<T, BM, BN, BK, NW>::FN],
                                                     char* smem) {
-  using TL = Tile<T, BM, BN, BK>;
+  using TL = Tile<T, BM, BN, BK, NW>;
   using ES = ConvEpiSmem<T, BM, BN>;
   constexpr int VE = ES::VE, CPR = BN / VE;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
+  const int lane = threadIdx.x & 63;
+  const int wm = TL::wave_m(), wn = TL::wave_n();
   const int C = p.C;
   T* sG = (T*)smem;
 #pragma unroll
@@ -1294,7 +1304,7 @@ __device__ __forceinline__ void conv_dgrad_epilogue(const ConvProb& p, int m0, i
   const T* X = (const T*)p.X;
   T* Gp = (T*)p.Gprev;
   const bool vec = (C % VE) == 0;
-  for (int idx = threadIdx.x; idx < BM * CPR; idx += 256) {
+  for (int idx = threadIdx.x; idx < BM * CPR; idx += TL::NT) {
     const int r = idx / CPR, c = n0 + (idx - r * CPR) * VE, m = m0 + r;
     if (m >= p.M || c >= C) continue;
     const int64_t g = (int64_t)m * C + c;
@@ -1377,29 +1387,36 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 // pass, input channels in the data gradient); chunk c of the k-block is chunk
 // q = kb*CPB + c of the channel block, whose weight column comes from the
 // chunk table. Every thread owns the same chunk c = tid % CPB in all its rows.
-template <typename T, int ROWS, int BK>
+template <typename T, int ROWS, int BK, int NT = 256>
 struct TapRowLoader {
-  static constexpr int VEC = TT<T>::VEC, CPB = BK / VEC, NV = ROWS * CPB / 256, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
-  static_assert(ROWS * CPB % 256 == 0 && 256 % CPB == 0, "tile too small for 256 threads");
+  static constexpr int VEC = TT<T>::VEC, CPB = BK / VEC, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
+  static constexpr int CHUNKS = ROWS * CPB, NV = CHUNKS >= NT ? CHUNKS / NT : 1;
+  // fewer chunks than threads: the first CHUNKS threads (whole waves) move them
+  static constexpr bool PART = CHUNKS < NT;
+  static_assert((CHUNKS % NT == 0 || NT % CHUNKS == 0) && NT % CPB == 0 && CHUNKS % 64 == 0,
+                "chunks must spread evenly over whole waves");
   __amdgpu_buffer_rsrc_t rsrc;
   int rowoff[NV];
   u32x4 r[NV];
+  __device__ __forceinline__ bool active() const { return !PART || (int)threadIdx.x < CHUNKS; }
   __device__ __forceinline__ void init(const T* base, int64_t ld, int rows_valid) {
     rsrc = make_rsrc(base, (int64_t)rows_valid * ld * (int64_t)sizeof(T));
 #pragma unroll
-    for (int s = 0; s < NV; ++s) rowoff[s] = (int)((int64_t)((threadIdx.x + 256 * s) / CPB) * ld * (int64_t)sizeof(T));
+    for (int s = 0; s < NV; ++s) rowoff[s] = (int)((int64_t)((threadIdx.x + NT * s) / CPB) * ld * (int64_t)sizeof(T));
   }
   // col: weight column of this thread's chunk, or -1 for a chunk past the block's end
   __device__ __forceinline__ void load(int col) {
+    if (!active()) return;
 #pragma unroll
     for (int s = 0; s < NV; ++s)
       r[s] = col < 0 ? zero4()
                      : __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, rowoff[s] + col * (int)sizeof(T), 0, 0));
   }
   __device__ __forceinline__ void store(T* sm) const {
+    if (!active()) return;
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
-      const int v = threadIdx.x + 256 * s;
+      const int v = threadIdx.x + NT * s;
       *(u32x4*)(sm + (v / CPB) * LDK + (v % CPB) * VEC) = r[s];
     }
   }
@@ -1410,19 +1427,19 @@ struct TapRowLoader {
 // batch, or - data gradient - not receiving the window's gradient are zero.
 // Forward: the conv input X. Data gradient: dZ, expanded from the pooled
 // gradient G and the window argmax.
-template <typename T, bool DGRAD>
+template <typename T, bool DGRAD, int NT = 256>
 __device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, int y0, int c0, int cbw) {
   constexpr int VEC = TT<T>::VEC, UNR = 4;
   const int cpp = cbw / VEC, plane = p.hr * p.hc;
   const int total = p.imgs * plane * cpp;
   const int CH = DGRAD ? p.O : p.C;
   const T* src = (const T*)(DGRAD ? p.G : p.X);
-  for (int e0 = threadIdx.x; e0 < total; e0 += 256 * UNR) {
+  for (int e0 = threadIdx.x; e0 < total; e0 += NT * UNR) {
     u32x4 v[UNR];
     int dst[UNR];
 #pragma unroll
     for (int k = 0; k < UNR; ++k) {
-      const int e = e0 + 256 * k;
+      const int e = e0 + NT * k;
       v[k] = zero4();
       dst[k] = -1;
       if (e < total) {
@@ -1455,14 +1472,14 @@ __device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, i
 // One k-block of a halo tile: A rows read from the staged halo at the lane's
 // row base plus the chunk's tap offset, B from the weight stage. Chunks at or
 // past nq have zero weights; their A reads are clamped to a valid chunk.
-template <typename T, int BM, int BN, int BK>
-__device__ __forceinline__ void mma_halo(const T* sH, const int (&hbase)[Tile<T, BM, BN, BK>::FM], const int* qa,
+template <typename T, int BM, int BN, int BK, int NW>
+__device__ __forceinline__ void mma_halo(const T* sH, const int (&hbase)[Tile<T, BM, BN, BK, NW>::FM], const int* qa,
                                          int q0, int nq, const T* sB,
-                                         f32x4 (&acc)[Tile<T, BM, BN, BK>::FM][Tile<T, BM, BN, BK>::FN]) {
-  using TL = Tile<T, BM, BN, BK>;
+                                         f32x4 (&acc)[Tile<T, BM, BN, BK, NW>::FM][Tile<T, BM, BN, BK, NW>::FN]) {
+  using TL = Tile<T, BM, BN, BK, NW>;
   constexpr int VEC = TT<T>::VEC;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wn = (wave & 1) * TL::WN;
+  const int lane = threadIdx.x & 63;
+  const int wn = TL::wave_n();
   const int lr = lane & 15, lg = lane >> 4;
   if constexpr (sizeof(T) == 2) {
 #pragma unroll
@@ -1515,9 +1532,10 @@ struct HaloSmem {
 };
 
 // One BM x BN halo tile `local` of problem p.
-template <typename T, int BM, int BN, int BK, bool DGRAD>
+template <typename T, int BM, int BN, int BK, bool DGRAD, int NW>
 __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* smem) {
-  using TL = Tile<T, BM, BN, BK>;
+  using TL = Tile<T, BM, BN, BK, NW>;
+  constexpr int NT = TL::NT;
   using HS = HaloSmem<T, BN, BK>;
   constexpr int VEC = TT<T>::VEC, CPB = BK / VEC;
   static_assert(TL::B_ELEMS == HS::B_ELEMS, "halo LDS budget assumes one pad chunk per row");
@@ -1537,8 +1555,8 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
     img0 = tm / tpi;
     y0 = (tm - img0 * tpi) * p.tr;
   }
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = (wave >> 1) * TL::WM;
+  const int lane = threadIdx.x & 63;
+  const int wm = TL::wave_m();
   // halo offset of the first tap of each of this lane's MFMA rows
   int hbase[TL::FM];
 #pragma unroll
@@ -1567,7 +1585,7 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
 #pragma unroll
     for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  TapRowLoader<T, BN, BK> lb;
+  TapRowLoader<T, BN, BK, NT> lb;
   lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0);
   const int KH = p.KH, Cin = DGRAD ? p.O : p.C, cq = threadIdx.x % CPB;
   for (int c0 = 0; c0 < Cin; c0 += p.cb) {
@@ -1581,12 +1599,12 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
       lb.load(-1);
     }
     __syncthreads();  // the previous channel block's halo, tables and weight stages are no longer read
-    for (int q = threadIdx.x; q < nq; q += 256) {
+    for (int q = threadIdx.x; q < nq; q += NT) {
       const int tap = q / cpt, ch = (q - tap * cpt) * VEC, u = tap / KH, v = tap - u * KH;
       qa[q] = (DGRAD ? (KH - 1 - u) * p.hc + (KH - 1 - v) : u * p.hc + v) * p.cs + ch;
       qb[q] = tap * Cin + c0 + ch;  // fwd: W[o][(tap, c)]; dgrad: WT[c][(tap, o)]
     }
-    stage_halo<T, DGRAD>(p, sH, img0, y0, c0, cbw);
+    stage_halo<T, DGRAD, NT>(p, sH, img0, y0, c0, cbw);
     lb.store(sB);
     __syncthreads();
     const int nkb = (nq + CPB - 1) / CPB;
@@ -1597,28 +1615,34 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
         const int q = (kb + 1) * CPB + cq;
         lb.load(q < nq ? qb[q] : -1);
       }
-      mma_halo<T, BM, BN, BK>(sH, hbase, qa, kb * CPB, nq, sB + cur * TL::B_ELEMS, acc);
+      mma_halo<T, BM, BN, BK, NW>(sH, hbase, qa, kb * CPB, nq, sB + cur * TL::B_ELEMS, acc);
       if (more) lb.store(sB + (cur ^ 1) * TL::B_ELEMS);
       __syncthreads();
     }
   }
-  if constexpr (DGRAD) conv_dgrad_epilogue<T, BM, BN, BK>(p, m0, n0, acc, smem);
-  else conv_fwd_epilogue<T, BM, BN, BK>(p, m0, n0, acc, smem);
+  if constexpr (DGRAD) conv_dgrad_epilogue<T, BM, BN, BK, NW>(p, m0, n0, acc, smem);
+  else conv_fwd_epilogue<T, BM, BN, BK, NW>(p, m0, n0, acc, smem);
 }
 
 // Halo-tiled conv pass; each problem's tile shape (p.bn) is the wide BM x BN
 // or the narrow 2BM x BN/2 one, so a launch mixes both. LDS is dynamic, sized
 // by the host for the launch's largest staged block (small halos leave room
 // for more workgroups per CU).
+// Waves of a halo workgroup (bf16; fp32 keeps 4): a 4-wave workgroup runs
+// three per CU, larger ones two.
+template <typename T> constexpr int halo_waves() { return sizeof(T) == 2 ? UN_HALO_WAVES : 4; }
+template <typename T> constexpr int halo_wpe() { return halo_waves<T>() == 4 ? 3 : halo_waves<T>() / 2; }
+
 template <typename T, int BM, int BN, int BK, bool DGRAD>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(3))) void conv_halo_kernel(const ConvProb* __restrict__ probs,
-                                                        const int32_t* __restrict__ tile_map) {
+__global__ __launch_bounds__((64 * halo_waves<T>())) __attribute__((amdgpu_waves_per_eu((halo_wpe<T>()))))
+void conv_halo_kernel(const ConvProb* __restrict__ probs, const int32_t* __restrict__ tile_map) {
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int prob = tile_map[2 * blockIdx.x], local = tile_map[2 * blockIdx.x + 1];
   if (prob < 0) return;  // padding of the XCD-ordered tile list
   const ConvProb& p = probs[prob];
-  if (p.bn == BN) halo_tile<T, BM, BN, BK, DGRAD>(p, local, smem);
-  else halo_tile<T, 2 * BM, BN / 2, BK, DGRAD>(p, local, smem);
+  constexpr int NW = halo_waves<T>();
+  if (p.bn == BN) halo_tile<T, BM, BN, BK, DGRAD, NW>(p, local, smem);
+  else halo_tile<T, 2 * BM, BN / 2, BK, DGRAD, NW>(p, local, smem);
 }
 
 template <typename T, int BM, int BN, int BK, int MODE>
@@ -1907,12 +1931,13 @@ hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const 
   }();
   if (attr != hipSuccess) return attr;
   if (bf16) {
+    constexpr int NT = 64 * halo_waves<bf16_t>();
     if (dgrad)
       hipLaunchKernelGGL((conv_halo_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, true>), dim3(ntiles),
-                         dim3(256), lds_bytes, s, probs, tile_map);
+                         dim3(NT), lds_bytes, s, probs, tile_map);
     else
       hipLaunchKernelGGL((conv_halo_kernel<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, false>), dim3(ntiles),
-                         dim3(256), lds_bytes, s, probs, tile_map);
+                         dim3(NT), lds_bytes, s, probs, tile_map);
   } else {
     if (dgrad)
       hipLaunchKernelGGL((conv_halo_kernel<float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, true>), dim3(ntiles),
