@@ -324,68 +324,77 @@ struct GemmMma<float, BM, BN, BK> {
 };
 
 // The GEMM's k loop over nkb k-blocks: LDS double-buffered, and the global
-// loads run DEPTH (1 or 2) k-blocks ahead in the loaders' two register slots,
-// so a block's load latency is covered by DEPTH blocks of MFMA work. Loads
-// past the last block re-read it (harmless, and branch-free so that the
-// waits stay exact). One barrier per k-block.
+// loads run DEPTH k-blocks ahead in the loaders' DEPTH register slots, so a
+// block's load latency is covered by DEPTH blocks of work (with 16 waves a
+// slot is one 16-byte vector per operand and thread, so depth is cheap).
+// Block kb sits in register slot kb % DEPTH and in LDS buffer kb % 2. Inside
+// the loop every load and store is unconditional (loads past the last block
+// re-read it and the copies made of them are never read), so the compiler's
+// wait counts stay exact. One barrier per k-block.
 template <typename T, int BM, int BN, int BK, int DEPTH, class MM, class LA, class LB>
 __device__ __forceinline__ void gemm_loop(LA& la, LB& lb, int nkb, T* smem, typename MM::Acc& acc) {
   using TL = Tile<T, BM, BN, BK>;
   constexpr int STAGE = TL::A_ELEMS + TL::B_ELEMS;
+  static_assert(DEPTH >= 1 && DEPTH <= 4, "prefetch depth 1 to 4");
   if (nkb <= 0) return;
-  if constexpr (DEPTH == 1) {
-    la.template load<0>(0);
-    lb.template load<0>(0);
-    la.template store<0>(smem);
-    lb.template store<0>(smem + TL::A_ELEMS);
+  // slot S takes block b (clamped to the last block)
+  auto issue = [&](auto slot, int b) {
+    constexpr int S = decltype(slot)::value;
+    const int bb = min(b, nkb - 1);
+    la.template load<S>(bb);
+    lb.template load<S>(bb);
+  };
+  issue(std::integral_constant<int, 0>{}, 0);
+  if constexpr (DEPTH > 1) issue(std::integral_constant<int, 1 % DEPTH>{}, 1);
+  if constexpr (DEPTH > 2) issue(std::integral_constant<int, 2 % DEPTH>{}, 2);
+  if constexpr (DEPTH > 3) issue(std::integral_constant<int, 3 % DEPTH>{}, 3);
+  la.template store<0>(smem);
+  lb.template store<0>(smem + TL::A_ELEMS);
+  __syncthreads();
+  // iteration kb (slot S = kb % DEPTH, LDS buffer kb % 2, both compile-time
+  // in the unrolled group below): refill slot S with block kb + DEPTH (for
+  // DEPTH 1 with block kb + 1, after the block's own copy has reached LDS),
+  // run block kb from LDS, then move block kb + 1 from its slot to LDS.
+  auto step = [&](auto pos, int kb) {
+    constexpr int U = decltype(pos)::value, S = U % DEPTH, N1 = (U + 1) % DEPTH, BUF = U & 1;
+    issue(std::integral_constant<int, S>{}, kb + (DEPTH > 1 ? DEPTH : 1));
+    const T* st = smem + BUF * STAGE;
+    MM::block(st, st + TL::A_ELEMS, acc);
+    T* d = smem + (BUF ^ 1) * STAGE;
+    la.template store<N1>(d);
+    lb.template store<N1>(d + TL::A_ELEMS);
     __syncthreads();
-    for (int kb = 0; kb < nkb; ++kb) {
-      const int cur = kb & 1;
-      const int nxt = min(kb + 1, nkb - 1);
-      la.template load<0>(nxt);
-      lb.template load<0>(nxt);
-      const T* st = smem + cur * STAGE;
-      MM::block(st, st + TL::A_ELEMS, acc);
-      if (kb + 1 < nkb) {
-        T* d = smem + (cur ^ 1) * STAGE;
-        la.template store<0>(d);
-        lb.template store<0>(d + TL::A_ELEMS);
-      }
-      __syncthreads();
+  };
+  // a group of G iterations: a multiple of DEPTH (slots) and of 2 (buffers)
+  constexpr int G = DEPTH == 1 ? 2 : (DEPTH == 3 ? 6 : DEPTH);
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using I4 = std::integral_constant<int, 4>;
+  using I5 = std::integral_constant<int, 5>;
+  int kb = 0;
+  for (; kb + G <= nkb; kb += G) {
+    step(I0{}, kb);
+    step(I1{}, kb + 1);
+    if constexpr (G > 2) {
+      step(I2{}, kb + 2);
+      step(I3{}, kb + 3);
     }
-  } else {
-    la.template load<0>(0);
-    lb.template load<0>(0);
-    la.template load<1>(min(1, nkb - 1));
-    lb.template load<1>(min(1, nkb - 1));
-    la.template store<0>(smem);
-    lb.template store<0>(smem + TL::A_ELEMS);
-    __syncthreads();
-    // Block kb sits in LDS buffer kb & 1 and came through register slot kb & 1.
-    // Inside the loop every load and store is unconditional (the copies made
-    // past the last block are never read), so the compiler's wait counts
-    // stay exact and block kb + 2 stays in flight across block kb's MFMAs.
-    auto step = [&](auto slot, int kb) {
-      constexpr int S = decltype(slot)::value;
-      const int ahead = min(kb + 2, nkb - 1);
-      la.template load<S>(ahead);
-      lb.template load<S>(ahead);
-      const T* st = smem + S * STAGE;
-      MM::block(st, st + TL::A_ELEMS, acc);
-      T* d = smem + (S ^ 1) * STAGE;
-      la.template store<S ^ 1>(d);
-      lb.template store<S ^ 1>(d + TL::A_ELEMS);
-      __syncthreads();
-    };
-    int kb = 0;
-    for (; kb + 1 < nkb; kb += 2) {
-      step(std::integral_constant<int, 0>{}, kb);
-      step(std::integral_constant<int, 1>{}, kb + 1);
+    if constexpr (G > 4) {
+      step(I4{}, kb + 4);
+      step(I5{}, kb + 5);
     }
-    if (kb < nkb) {  // odd count: the last block, from buffer 0
-      MM::block(smem, smem + TL::A_ELEMS, acc);
-      __syncthreads();
-    }
+  }
+  // the last nkb % G blocks (no loop back-edge follows them)
+  if (kb < nkb) step(I0{}, kb);
+  if (kb + 1 < nkb) step(I1{}, kb + 1);
+  if constexpr (G > 2) {
+    if (kb + 2 < nkb) step(I2{}, kb + 2);
+    if (kb + 3 < nkb) step(I3{}, kb + 3);
+  }
+  if constexpr (G > 4) {
+    if (kb + 4 < nkb) step(I4{}, kb + 4);
   }
 }
 
@@ -421,14 +430,14 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, in
 // Row-major operand with k contiguous: element (row, k) = base[row*ld + k].
 // Rows at or beyond rows_valid read as zero through the buffer range check;
 // columns at or beyond K are zeroed on the last, partial k-block only.
-template <typename T, int ROWS, int BK, int NT = 256>
+template <typename T, int ROWS, int BK, int NT = 256, int SLOTS = 2>
 struct RowLoader {
   static constexpr int VEC = TT<T>::VEC, VPR = BK / VEC, NV = ROWS * VPR / NT, LDK = BK + UN_LDS_PAD_CHUNKS * VEC;
   static_assert(ROWS * VPR % NT == 0, "tile too small for the workgroup");
   __amdgpu_buffer_rsrc_t rsrc;
   int off[NV];
   int K;
-  u32x4 r[2][NV];
+  u32x4 r[SLOTS][NV];
   __device__ __forceinline__ void init(const T* base, int64_t ld, int rows_valid, int K_) {
     K = K_;
     rsrc = make_rsrc(base, (int64_t)rows_valid * ld * (int64_t)sizeof(T));
@@ -1021,6 +1030,12 @@ __device__ __forceinline__ void opt_update4(const OptHp& h, const f32x4& g, f32x
   *(gptr<f32x4>)s2 = v;
 }
 
+// Column of element (r, c) in the GEMM epilogue's LDS tile: c XOR a multiple
+// of 8 that changes every 8 rows. Groups of 8 (float4 pairs) stay contiguous,
+// and a column read down 8-row groups spreads over the banks, so the
+// transposed copy can be stored with consecutive lanes along one output row.
+__device__ __forceinline__ int sc_col(int r, int c) { return c ^ (((r >> 3) & 7) << 3); }
+
 template <typename OT, int BM, int BN, int CLD, int NT = 256>
 __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, int m0, int n0, int M, int N) {
   constexpr int VE = 16 / sizeof(OT), CPR = BN / VE;
@@ -1032,7 +1047,7 @@ __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, 
     float v[VE];
 #pragma unroll
     for (int e = 0; e < VE; e += 4) {
-      const f32x4 x = *(const f32x4*)(sC + r * CLD + cc * VE + e);
+      const f32x4 x = *(const f32x4*)(sC + r * CLD + sc_col(r, cc * VE + e));
       v[e] = x[0];
       v[e + 1] = x[1];
       v[e + 2] = x[2];
@@ -1043,18 +1058,18 @@ __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, 
 }
 
 // Transposed store of the staged tile: CT[n][m] for n < N, 16-byte chunks
-// along m. Consecutive threads take consecutive columns, so the strided LDS
-// gathers hit distinct banks.
+// along m; consecutive lanes take consecutive chunks of one CT row, so a
+// wave writes whole rows of the transposed copy.
 template <typename OT, int BM, int BN, int CLD, int NT = 256>
 __device__ __forceinline__ void store_cols(const float* sC, OT* CT, int64_t ldct, int m0, int n0, int M, int N) {
-  constexpr int VE = 16 / sizeof(OT);
-  for (int idx = threadIdx.x; idx < BN * (BM / VE); idx += NT) {
-    const int mq = idx / BN, c = idx - mq * BN;
+  constexpr int VE = 16 / sizeof(OT), MQ = BM / VE;
+  for (int idx = threadIdx.x; idx < BN * MQ; idx += NT) {
+    const int c = idx / MQ, mq = idx - c * MQ;
     const int n = n0 + c, m = m0 + mq * VE;
     if (n >= N || m >= M) continue;
     float v[VE];
 #pragma unroll
-    for (int e = 0; e < VE; ++e) v[e] = sC[(mq * VE + e) * CLD + c];
+    for (int e = 0; e < VE; ++e) v[e] = sC[(mq * VE + e) * CLD + sc_col(mq * VE + e, c)];
     store_chunk<OT>(CT + (int64_t)n * ldct + m, v, min(VE, M - m));
   }
 }
@@ -1082,8 +1097,8 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
   MM::zero(acc);
 
   constexpr int NT = MM::NT;
-  RowLoader<T, BM, BK, NT> la;
-  RowLoader<T, BN, BK, NT> lb;
+  RowLoader<T, BM, BK, NT, UN_GEMM_DEPTH> la;
+  RowLoader<T, BN, BK, NT, UN_GEMM_DEPTH> lb;
   la.init((const T*)p.A + (int64_t)m0 * p.lda, p.lda, p.M - m0, p.K);
   lb.init((const T*)p.B + (int64_t)n0 * p.ldb, p.ldb, p.N - n0, p.K);
   gemm_loop<T, BM, BN, BK, UN_GEMM_DEPTH, MM>(la, lb, (p.K + BK - 1) / BK, (T*)smem, acc);
@@ -1131,7 +1146,7 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
         }
       }
 #pragma unroll
-      for (int r = 0; r < 4; ++r) sC[(rl + r) * CLD + cl] = v[r];
+      for (int r = 0; r < 4; ++r) sC[(rl + r) * CLD + sc_col(rl + r, cl)] = v[r];
   });
   __syncthreads();
 
@@ -1157,7 +1172,7 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
     // this row's model: its own learning rate (or optimizer) when set per model
     const int mdl = p.row_model ? p.row_model[m] : p.model;
     const float lr_m = lrv ? lrv[mdl] : lr;
-    float* s = sC + r * CLD + cc * 4;
+    float* s = sC + r * CLD + sc_col(r, cc * 4);
     const int64_t base = (int64_t)m * p.ldc + n;
     if (n + 4 <= ns) {
       const f32x4 g = *(const f32x4*)s;
