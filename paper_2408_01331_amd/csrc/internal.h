@@ -14,19 +14,23 @@ typedef uint16_t bf16_t;
 
 // ---------------------------------------------------------------------------
 // Grouped GEMM:  C[m][n] = sum_k A[m][k] * B[n][k]
-// A and B are row-major with k contiguous ("NT" form). Every linear-layer
-// product of the step is brought into this form by keeping, next to each
-// activation / gradient, a transposed copy written by its producer:
-//   forward  Y[b][o]  = sum_i X[b][i]  W[o][i]      A = X,  B = W
-//   dgrad    dX[b][i] = sum_o G[b][o]  WT[i][o]     A = G,  B = WT
-//   wgrad    dW[o][i] = sum_b GT[o][b] XT[i][b]     A = GT, B = XT
-// XT carries one extra row of ones, so column n == nsplit of the wgrad product
-// is the bias gradient sum_b G[b][o].
+// Each operand is row-major (element (r, k) at base[r*ld + k], k contiguous)
+// or k-major (element (r, k) at base[k*ld + r]). A k-major operand is staged
+// in LDS as it lies in memory and turned into MFMA operands by the LDS
+// transpose reads of gfx950, so no layer keeps a transposed copy of its
+// weights, activations or gradients:
+//   forward  Y[b][o]  = sum_i X[b][i] W[o][i]    A = X row-major,  B = W row-major
+//   dgrad    dX[b][i] = sum_o G[b][o] W[o][i]    A = G row-major,  B = W k-major
+//   wgrad    dW[o][i] = sum_b G[b][o] X[b][i]    A = G k-major,    B = X k-major
+// The wgrad's B loader reads 1 in column n == nsplit (for every k < K): that
+// column of the product is the bias gradient sum_b G[b][o].
 // ---------------------------------------------------------------------------
+enum OpLayout : int32_t { OP_ROW = 0, OP_KMAJ = 1 };
+
 enum Epi : int32_t {
-  EPI_FWD = 0,     // + bias, optional ReLU, store C (T) and optionally CT (T)
+  EPI_FWD = 0,     // + bias, optional ReLU, store C (T)
   EPI_LOGITS = 1,  // + bias, store C as fp32
-  EPI_DGRAD = 2,   // optional ReLU' mask from `mask` ([n][m] layout, keep where > 0), store C, CT (T)
+  EPI_DGRAD = 2,   // optional ReLU' mask from `mask` (row-major [m][n], keep where > 0), store C (T)
   EPI_WGRAD = 3    // store C as fp32 for n < nsplit; column nsplit -> dbias[m]
 };
 
@@ -36,25 +40,21 @@ struct GemmProb {
   int64_t lda, ldb;
   int32_t M, N, K;
   int32_t epi, relu;
+  int32_t amode, bmode;       // OpLayout of A and B
   int32_t tiles_n;
   int32_t nsplit;
   int32_t model;              // WGRAD: the model whose learning rate applies (single-model problems)
   void* C;                    // WGRAD: gradient dW [m][ldc] (stored only when gradients are kept)
   int64_t ldc;
-  void* CT;
-  int64_t ldct;
   const float* bias;
   const void* mask;
   int64_t ldmask;
   float* dbias;               // WGRAD: bias gradient (kept gradients only)
   // WGRAD with the SGD update fused into the epilogue:
   //   W[m][n] <- fma(-lr, dW[m][n], W[m][n]) (fp32 master, row stride ldc),
-  //   Wb[m][n] <- bf16(W) (bf16 mode), WT[n][m] <- W (transposed copy, storage type),
-  //   bmaster[m] <- fma(-lr, db[m], bmaster[m]).
+  //   Wb[m][n] <- bf16(W) (bf16 mode), bmaster[m] <- fma(-lr, db[m], bmaster[m]).
   float* W;
   void* Wb;
-  void* WT;
-  int64_t ldwt;
   float* bmaster;
   const int32_t* row_model;   // WGRAD of the concatenated first layers: model of each row m (else null)
   // optimizer state (same layouts as W and bmaster; null for plain SGD):
@@ -192,7 +192,9 @@ struct SgdTensor {
 // not null (device array). Labels: labels[b] for every model, or
 // labels[model * B + b] when per_model_labels is set.
 // `opt` (device, one OptHp per model) replaces lr/lrv when not null.
-hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
+// bwd: the launch holds data- and weight-gradient problems (k-major operands),
+// else forward problems (row-major operands only).
+hipError_t launch_gemm(bool bf16, bool bwd, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
                        const float* lrv, const OptHp* opt, bool keep_grads, hipStream_t s);
 hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                            hipStream_t s);

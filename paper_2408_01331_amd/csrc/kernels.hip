@@ -32,6 +32,10 @@
 #ifndef UN_GEMM_WGN
 #define UN_GEMM_WGN 4
 #endif
+// Padding (elements) of a k-major LDS stage row: the stage holds BK rows of
+// R + pad elements, the same size as the row-major R x (BK + 1 chunk) stage,
+// and 4 consecutive rows start 8 banks apart (conflict-free transpose reads).
+constexpr int KMAJ_PAD_BF16 = 16, KMAJ_PAD_F32 = 8;
 #ifndef UN_HALO_WAVES
 #define UN_HALO_WAVES 8
 #endif
@@ -248,6 +252,7 @@ struct GemmMma<bf16_t, BM, BN, BK> {
   static constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
   static_assert(FM >= 1 && FN >= 1, "wave tile smaller than one 32x32 block");
   static constexpr int LDK = Tile<bf16_t, BM, BN, BK>::LDK;
+  static constexpr int LDR_A = BM + KMAJ_PAD_BF16, LDR_B = BN + KMAJ_PAD_BF16;  // k-major row strides
   static constexpr int CLD = BN + 8;
   static_assert(BK % 16 == 0, "BK must be a multiple of 16");
   using Acc = f32x16[FM][FN];
@@ -259,19 +264,40 @@ struct GemmMma<bf16_t, BM, BN, BK> {
 #pragma unroll
         for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
   }
+  // The 8 k-consecutive operand values of lane (r = lane % 32, k group
+  // lane / 32) for tile row `row0 + lane % 32`, k-step kk.
+  // Row-major stage [row][LDK]: one 16-byte read.
+  __device__ __forceinline__ static bf16x8 frag_row(const bf16_t* s, int row0, int kk) {
+    const int lane = threadIdx.x & 63;
+    return __builtin_bit_cast(bf16x8, *(const u32x4*)(s + (row0 + (lane & 31)) * LDK + kk + 8 * (lane >> 5)));
+  }
+  // k-major stage [k][ldr]: two LDS transpose reads. In each group of 16 lanes
+  // (rows rb..rb+15 of the fragment, k group kg), address lane a points at
+  // row k = k0 + a/4, columns rb + 4(a%4) .. +3; lane i then receives
+  // stage[k0 + e][rb + i] for e = 0..3 - four consecutive k of its own row.
+  template <int LDR>
+  __device__ __forceinline__ static bf16x8 frag_kmaj(const bf16_t* s, int row0, int kk) {
+    const int lane = threadIdx.x & 63, h = lane >> 4, a = lane & 15;
+    const int rb = row0 + 16 * (h & 1) + 4 * (a & 3), k0 = kk + 8 * (h >> 1) + (a >> 2);
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(s + k0 * LDR + rb));
+    const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(s + (k0 + 4) * LDR + rb));
+    const u32x2 l = __builtin_bit_cast(u32x2, lo), u = __builtin_bit_cast(u32x2, hi);
+    return __builtin_bit_cast(bf16x8, u32x4{l[0], l[1], u[0], u[1]});
+  }
+  template <int AM, int BMODE>
   __device__ __forceinline__ static void block(const bf16_t* sA, const bf16_t* sB, Acc& acc) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wave = threadIdx.x >> 6;
     const int wm = (wave / WGN) * WM, wn = (wave % WGN) * WN;
-    const int lr = lane & 31, lg = lane >> 5;
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 16) {
       bf16x8 a[FM], b[FN];
 #pragma unroll
       for (int i = 0; i < FM; ++i)
-        a[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(sA + (wm + 32 * i + lr) * LDK + kk + 8 * lg));
+        a[i] = AM == OP_ROW ? frag_row(sA, wm + 32 * i, kk) : frag_kmaj<LDR_A>(sA, wm + 32 * i, kk);
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        b[j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(sB + (wn + 32 * j + lr) * LDK + kk + 8 * lg));
+        b[j] = BMODE == OP_ROW ? frag_row(sB, wn + 32 * j, kk) : frag_kmaj<LDR_B>(sB, wn + 32 * j, kk);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -298,6 +324,8 @@ template <int BM, int BN, int BK>
 struct GemmMma<float, BM, BN, BK> {
   using TL = Tile<float, BM, BN, BK>;
   static constexpr int NT = 256;
+  static constexpr int LDK = TL::LDK;
+  static constexpr int LDR_A = BM + KMAJ_PAD_F32, LDR_B = BN + KMAJ_PAD_F32;
   static constexpr int CLD = BN + 4;
   using Acc = f32x4[TL::FM][TL::FN];
   __device__ __forceinline__ static void zero(Acc& acc) {
@@ -306,8 +334,33 @@ struct GemmMma<float, BM, BN, BK> {
 #pragma unroll
       for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  // Lane (r = lane % 16, g = lane / 16) feeds k = kk + 4g + q to the q-th
+  // 16x16x4 MFMA: its four values of tile row row0 + r.
+  template <int MODE, int LDR>
+  __device__ __forceinline__ static f32x4 frag(const float* s, int row0, int kk) {
+    const int lane = threadIdx.x & 63, r = row0 + (lane & 15), k = kk + 4 * (lane >> 4);
+    if constexpr (MODE == OP_ROW) return *(const f32x4*)(s + r * LDK + k);
+    else return f32x4{s[k * LDR + r], s[(k + 1) * LDR + r], s[(k + 2) * LDR + r], s[(k + 3) * LDR + r]};
+  }
+  template <int AM, int BMODE>
   __device__ __forceinline__ static void block(const float* sA, const float* sB, Acc& acc) {
-    mma_block<float, BM, BN, BK>(sA, sB, acc);
+    const int wave = threadIdx.x >> 6;
+    const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 16) {
+      f32x4 a[TL::FM], b[TL::FN];
+#pragma unroll
+      for (int i = 0; i < TL::FM; ++i) a[i] = frag<AM, LDR_A>(sA, wm + 16 * i, kk);
+#pragma unroll
+      for (int j = 0; j < TL::FN; ++j) b[j] = frag<BMODE, LDR_B>(sB, wn + 16 * j, kk);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int i = 0; i < TL::FM; ++i)
+#pragma unroll
+          for (int j = 0; j < TL::FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
+    }
   }
   template <class F>
   __device__ __forceinline__ static void for_groups(const Acc& acc, F&& f) {
@@ -331,7 +384,7 @@ struct GemmMma<float, BM, BN, BK> {
 // the loop every load and store is unconditional (loads past the last block
 // re-read it and the copies made of them are never read), so the compiler's
 // wait counts stay exact. One barrier per k-block.
-template <typename T, int BM, int BN, int BK, int DEPTH, class MM, class LA, class LB>
+template <typename T, int BM, int BN, int BK, int DEPTH, class MM, int AM, int BMODE, class LA, class LB>
 __device__ __forceinline__ void gemm_loop(LA& la, LB& lb, int nkb, T* smem, typename MM::Acc& acc) {
   using TL = Tile<T, BM, BN, BK>;
   constexpr int STAGE = TL::A_ELEMS + TL::B_ELEMS;
@@ -359,7 +412,7 @@ __device__ __forceinline__ void gemm_loop(LA& la, LB& lb, int nkb, T* smem, type
     constexpr int U = decltype(pos)::value, S = U % DEPTH, N1 = (U + 1) % DEPTH, BUF = U & 1;
     issue(std::integral_constant<int, S>{}, kb + (DEPTH > 1 ? DEPTH : 1));
     const T* st = smem + BUF * STAGE;
-    MM::block(st, st + TL::A_ELEMS, acc);
+    MM::template block<AM, BMODE>(st, st + TL::A_ELEMS, acc);
     T* d = smem + (BUF ^ 1) * STAGE;
     la.template store<N1>(d);
     lb.template store<N1>(d + TL::A_ELEMS);
@@ -467,6 +520,53 @@ struct RowLoader {
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + NT * s;
       *(u32x4*)(sm + (v / VPR) * LDK + (v % VPR) * VEC) = r[S][s];
+    }
+  }
+};
+
+// k-major operand: element (row, k) = mat[k*ld + col0 + row] for the tile
+// starting at column col0. A k-block is BK rows of ROWS contiguous elements,
+// copied to LDS as they are, [k][ROWS + pad] (the MFMA fragments come out of
+// it through transpose reads). The buffer range ends with row K - 1 of the
+// matrix, so rows k >= K and anything past the matrix read as zero; columns
+// past the tile's valid ones within the matrix only feed output rows /
+// columns that are never stored. With bias_col >= 0, column bias_col reads 1
+// for every k < K.
+template <typename T, int ROWS, int BK, int NT, int SLOTS, int PAD>
+struct KRowLoader {
+  static constexpr int VEC = TT<T>::VEC, CPR = ROWS / VEC, NV = BK * CPR / NT, LDR = ROWS + PAD;
+  static_assert(BK * CPR % NT == 0, "tile too small for the workgroup");
+  __amdgpu_buffer_rsrc_t rsrc;
+  int off[NV];
+  int K, kstride, bias_chunk, bias_e;
+  u32x4 r[SLOTS][NV];
+  __device__ __forceinline__ void init(const T* mat, int64_t ld, int col0, int K_, int bias_col) {
+    K = K_;
+    kstride = BK * (int)ld * (int)sizeof(T);
+    rsrc = make_rsrc(mat + col0, ((int64_t)K_ * ld - col0) * (int64_t)sizeof(T));
+    bias_chunk = bias_col >= 0 ? bias_col / VEC : -1;
+    bias_e = bias_col >= 0 ? bias_col % VEC : 0;
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int v = threadIdx.x + NT * s;
+      off[s] = (int)(((int64_t)(v / CPR) * ld + (v % CPR) * VEC) * (int64_t)sizeof(T));
+    }
+  }
+  template <int S>
+  __device__ __forceinline__ void load(int kb) {
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      r[S][s] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, off[s] + kb * kstride, 0, 0));
+      const int v = threadIdx.x + NT * s;
+      if ((v % CPR) == bias_chunk && kb * BK + v / CPR < K) vset_bits<T>(r[S][s], bias_e, bits_of<T>(TT<T>::from_f(1.0f)));
+    }
+  }
+  template <int S>
+  __device__ __forceinline__ void store(T* sm) const {
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int v = threadIdx.x + NT * s;
+      *(u32x4*)(sm + (v / CPR) * LDR + (v % CPR) * VEC) = r[S][s];
     }
   }
 };
@@ -1036,8 +1136,19 @@ __device__ __forceinline__ void opt_update4(const OptHp& h, const f32x4& g, f32x
 // transposed copy can be stored with consecutive lanes along one output row.
 __device__ __forceinline__ int sc_col(int r, int c) { return c ^ (((r >> 3) & 7) << 3); }
 
+// VE consecutive values (one 16-byte vector) as floats.
+template <typename T, int VE> __device__ __forceinline__ void load_chunk_f(const T* src, float (&v)[VE]) {
+  const u32x4 x = *(gptr<const u32x4>)src;
+#pragma unroll
+  for (int e = 0; e < VE; ++e) v[e] = vget<T>(x, e);
+}
+
+// Row pass of the staged tile: C[m][n] in 16-byte chunks along n. With a
+// mask (row-major, same shape), values where the mask is not > 0 become 0
+// (ReLU' of the previous layer's output).
 template <typename OT, int BM, int BN, int CLD, int NT = 256>
-__device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, int m0, int n0, int M, int N) {
+__device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, int m0, int n0, int M, int N,
+                                           const OT* mask = nullptr, int64_t ldmask = 0) {
   constexpr int VE = 16 / sizeof(OT), CPR = BN / VE;
   static_assert(CLD % 4 == 0, "float4 rows");
   for (int idx = threadIdx.x; idx < BM * CPR; idx += NT) {
@@ -1053,30 +1164,23 @@ __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, 
       v[e + 2] = x[2];
       v[e + 3] = x[3];
     }
-    store_chunk<OT>(C + (int64_t)m * ldc + n, v, min(VE, N - n));
-  }
-}
-
-// Transposed store of the staged tile: CT[n][m] for n < N, 16-byte chunks
-// along m; consecutive lanes take consecutive chunks of one CT row, so a
-// wave writes whole rows of the transposed copy.
-template <typename OT, int BM, int BN, int CLD, int NT = 256>
-__device__ __forceinline__ void store_cols(const float* sC, OT* CT, int64_t ldct, int m0, int n0, int M, int N) {
-  constexpr int VE = 16 / sizeof(OT), MQ = BM / VE;
-  for (int idx = threadIdx.x; idx < BN * MQ; idx += NT) {
-    const int c = idx / MQ, mq = idx - c * MQ;
-    const int n = n0 + c, m = m0 + mq * VE;
-    if (n >= N || m >= M) continue;
-    float v[VE];
+    if (mask) {
+      float mv[VE];
+      load_chunk_f<OT, VE>(mask + (int64_t)m * ldmask + n, mv);
 #pragma unroll
-    for (int e = 0; e < VE; ++e) v[e] = sC[(mq * VE + e) * CLD + sc_col(mq * VE + e, c)];
-    store_chunk<OT>(CT + (int64_t)n * ldct + m, v, min(VE, M - m));
+      for (int e = 0; e < VE; ++e)
+        if (!(mv[e] > 0.f)) v[e] = 0.f;
+    }
+    store_chunk<OT>(C + (int64_t)m * ldc + n, v, min(VE, N - n));
   }
 }
 
 // OPT: the update follows a per-model OptHp (`opt`, not null) instead of
 // fma(-lr, g, w); a separate instantiation, so that plain SGD pays nothing.
-template <typename T, int BM, int BN, int BK, bool OPT>
+// BWD: the launch's problems are data gradients (A row-major, B k-major) and
+// weight gradients (both k-major), told apart by p.amode; else forward
+// problems (both row-major). Each variant compiles only its own k-loops.
+template <typename T, int BM, int BN, int BK, bool OPT, bool BWD>
 __global__ __launch_bounds__((GemmMma<T, BM, BN, BK>::NT)) __attribute__((amdgpu_waves_per_eu((GemmMma<T, BM, BN, BK>::NT / 128))))
 void gemm_kernel(const GemmProb* __restrict__ probs,
                                                    const int32_t* __restrict__ tile_map, float lr,
@@ -1096,12 +1200,32 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
   typename MM::Acc acc;
   MM::zero(acc);
 
-  constexpr int NT = MM::NT;
-  RowLoader<T, BM, BK, NT, UN_GEMM_DEPTH> la;
-  RowLoader<T, BN, BK, NT, UN_GEMM_DEPTH> lb;
-  la.init((const T*)p.A + (int64_t)m0 * p.lda, p.lda, p.M - m0, p.K);
-  lb.init((const T*)p.B + (int64_t)n0 * p.ldb, p.ldb, p.N - n0, p.K);
-  gemm_loop<T, BM, BN, BK, UN_GEMM_DEPTH, MM>(la, lb, (p.K + BK - 1) / BK, (T*)smem, acc);
+  constexpr int NT = MM::NT, D = UN_GEMM_DEPTH;
+  constexpr int PAD = sizeof(T) == 2 ? KMAJ_PAD_BF16 : KMAJ_PAD_F32;
+  const int nkb = (p.K + BK - 1) / BK;
+  if constexpr (!BWD) {
+    RowLoader<T, BM, BK, NT, D> la;
+    RowLoader<T, BN, BK, NT, D> lb;
+    la.init((const T*)p.A + (int64_t)m0 * p.lda, p.lda, p.M - m0, p.K);
+    lb.init((const T*)p.B + (int64_t)n0 * p.ldb, p.ldb, p.N - n0, p.K);
+    gemm_loop<T, BM, BN, BK, D, MM, OP_ROW, OP_ROW>(la, lb, nkb, (T*)smem, acc);
+  } else if (p.amode == OP_ROW) {
+    // data gradient: A = G row-major, B = W k-major (rows k = output units)
+    RowLoader<T, BM, BK, NT, D> la;
+    KRowLoader<T, BN, BK, NT, D, PAD> lb;
+    la.init((const T*)p.A + (int64_t)m0 * p.lda, p.lda, p.M - m0, p.K);
+    lb.init((const T*)p.B, p.ldb, n0, p.K, -1);
+    gemm_loop<T, BM, BN, BK, D, MM, OP_ROW, OP_KMAJ>(la, lb, nkb, (T*)smem, acc);
+  } else {
+    // weight gradient: A = G k-major, B = X k-major (rows k = batch), with
+    // the ones column of the bias gradient at n == nsplit
+    KRowLoader<T, BM, BK, NT, D, PAD> la;
+    KRowLoader<T, BN, BK, NT, D, PAD> lb;
+    const int bcol = p.nsplit - n0;
+    la.init((const T*)p.A, p.lda, m0, p.K, -1);
+    lb.init((const T*)p.B, p.ldb, n0, p.K, bcol >= 0 && bcol < BN ? bcol : -1);
+    gemm_loop<T, BM, BN, BK, D, MM, OP_KMAJ, OP_KMAJ>(la, lb, nkb, (T*)smem, acc);
+  }
 
   // Weight gradient with the SGD update fused: the master-weight loads of
   // this thread's float4 chunks of W[m][n..n+3] are issued first, so their
@@ -1117,8 +1241,8 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
     }
   }
 
-  // Epilogue 1: per-element work (bias, ReLU, ReLU' mask) in registers, then
-  // the fp32 tile to LDS (rows of CLD floats: float4-aligned).
+  // Epilogue 1: per-element work (bias, ReLU) in registers, then the fp32
+  // tile to LDS (rows of CLD floats: float4-aligned).
   constexpr int CLD = MM::CLD;
   static_assert(CLD <= SM::CLD, "epilogue tile exceeds its LDS");
   float* sC = (float*)smem;
@@ -1134,15 +1258,6 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
             v[r] += b;
             if (p.relu) v[r] = fmaxf(v[r], 0.f);
           }
-        } else if (epi == EPI_DGRAD && p.relu) {
-          // four consecutive rows of one column of the transposed activation
-          // (rows padded to a multiple of 8: one aligned vector load)
-          const T* mk = (const T*)p.mask + (int64_t)n * p.ldmask + mb;
-          float mv[4];
-          load4_t<T>(mk, mv);
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            if (r < nv && !(mv[r] > 0.f)) v[r] = 0.f;
         }
       }
 #pragma unroll
@@ -1151,19 +1266,20 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
   __syncthreads();
 
   if (epi != EPI_WGRAD) {
-    // Row pass: C[m][n] in 16-byte chunks along n.
+    // Row pass: C[m][n] in 16-byte chunks along n (data gradient: with the
+    // previous layer's ReLU' from its stored output).
     if (p.C) {
       if (epi == EPI_LOGITS) store_rows<float, BM, BN, CLD, NT>(sC, (float*)p.C, p.ldc, m0, n0, p.M, p.N);
+      else if (epi == EPI_DGRAD && p.relu)
+        store_rows<T, BM, BN, CLD, NT>(sC, (T*)p.C, p.ldc, m0, n0, p.M, p.N, (const T*)p.mask, p.ldmask);
       else store_rows<T, BM, BN, CLD, NT>(sC, (T*)p.C, p.ldc, m0, n0, p.M, p.N);
     }
-    // Column pass: CT[n][m] in 16-byte chunks along m.
-    if (p.CT) store_cols<T, BM, BN, CLD, NT>(sC, (T*)p.CT, p.ldct, m0, n0, p.M, p.N);
     return;
   }
 
   // EPI_WGRAD, SGD fused. Row pass over the float4 chunks: the update, the
-  // bf16 shadow, the kept gradient; the updated weights go back to LDS. The
-  // bias column (n == nsplit) is done element-wise.
+  // bf16 shadow, the kept gradient. The bias column (n == nsplit) is done
+  // element-wise.
 #pragma unroll
   for (int q = 0; q < NCH; ++q) {
     const int idx = threadIdx.x + NT * q, r = idx / CPR, cc = idx - r * CPR;
@@ -1192,7 +1308,6 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
         hb[1] = (uint32_t)f2bf(w[2]) | ((uint32_t)f2bf(w[3]) << 16);
         *(gptr<u32x2>)((bf16_t*)p.Wb + base) = hb;
       }
-      *(f32x4*)s = w;
     } else {
       for (int e = 0; e < 4 && n + e <= ns && n + e < p.N; ++e) {
         const float g = s[e];
@@ -1203,7 +1318,6 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
           else w = fmaf(-lr_m, g, p.W[base + e]);
           p.W[base + e] = w;
           if (p.Wb) ((bf16_t*)p.Wb)[base + e] = f2bf(w);
-          s[e] = w;
         } else {
           if (keep_grads) p.dbias[m] = g;
           if constexpr (OPT) p.bmaster[m] = opt_update1(opt[mdl], g, p.bmaster[m], p.sb1 + m, p.sb2 + m);
@@ -1212,10 +1326,6 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
       }
     }
   }
-  if (!p.WT) return;
-  __syncthreads();
-  // Column pass: the updated weights transposed, WT[n][m] for n < nsplit.
-  store_cols<T, BM, BN, CLD, NT>(sC, (T*)p.WT, p.ldwt, m0, n0, p.M, min(p.N, ns));
 }
 
 // ---------------------------------------------------------------------------
@@ -1880,24 +1990,21 @@ __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, 
 // ---------------------------------------------------------------------------
 // Launch wrappers
 // ---------------------------------------------------------------------------
-hipError_t launch_gemm(bool bf16, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
+hipError_t launch_gemm(bool bf16, bool bwd, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
                        const float* lrv, const OptHp* opt, bool keep_grads, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
+  auto go = [&](auto kern, int nt) {
+    hipLaunchKernelGGL(kern, dim3(ntiles), dim3(nt), 0, s, probs, tile_map, lr, lrv, opt, (int)keep_grads);
+  };
   if (bf16) {
     constexpr int NT = GemmMma<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16>::NT;
-    if (opt)
-      hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16, true>), dim3(ntiles), dim3(NT), 0,
-                         s, probs, tile_map, lr, lrv, opt, (int)keep_grads);
-    else
-      hipLaunchKernelGGL((gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16, false>), dim3(ntiles), dim3(NT),
-                         0, s, probs, tile_map, lr, lrv, opt, (int)keep_grads);
+    if (!bwd) go(gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16, false, false>, NT);
+    else if (opt) go(gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16, true, true>, NT);
+    else go(gemm_kernel<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16, false, true>, NT);
   } else {
-    if (opt)
-      hipLaunchKernelGGL((gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, GEMM_BK_F32, true>), dim3(ntiles), dim3(256), 0, s,
-                         probs, tile_map, lr, lrv, opt, (int)keep_grads);
-    else
-      hipLaunchKernelGGL((gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, GEMM_BK_F32, false>), dim3(ntiles), dim3(256), 0, s,
-                         probs, tile_map, lr, lrv, opt, (int)keep_grads);
+    if (!bwd) go(gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, GEMM_BK_F32, false, false>, 256);
+    else if (opt) go(gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, GEMM_BK_F32, true, true>, 256);
+    else go(gemm_kernel<float, GEMM_BM_F32, GEMM_BN_F32, GEMM_BK_F32, false, true>, 256);
   }
   return hipGetLastError();
 }

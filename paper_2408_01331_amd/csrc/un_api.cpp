@@ -47,18 +47,18 @@ struct Block {
   // PyTorch-layout offsets in the model's flat parameter vector
   size_t pt_w = 0, pt_b = 0, n_w = 0, n_b = 0;
   // arena offsets (NONE = absent)
-  size_t W32 = NONE, b32 = NONE, gW = NONE, gb = NONE, Wb = NONE, WT = NONE;
-  size_t WT2 = NONE;       // Linear: second transposed copy (written while the dgrad reads WT)
+  size_t W32 = NONE, b32 = NONE, gW = NONE, gb = NONE, Wb = NONE;
+  size_t WT = NONE;        // conv: transposed weights [c][(tap, o)] of the data gradient
   // optimizer state, offsets in the context's state allocation (same layouts as W32 / b32)
   size_t S1 = NONE, S1b = NONE, S2 = NONE, S2b = NONE;
   int64_t ldw = 0, ldwt = 0;
   int rows = 0;            // logical weight rows (N or O)
-  size_t X = NONE, XT = NONE;
-  int64_t ldx = 0, ldxt = 0;
-  size_t Y = NONE, YT = NONE, amax = NONE;
-  int64_t ldy = 0, ldyt = 0;
-  size_t G = NONE, GT = NONE;
-  int64_t ldg = 0, ldgt = 0;
+  size_t X = NONE;         // input (the previous block's output), row-major
+  int64_t ldx = 0;
+  size_t Y = NONE, amax = NONE;
+  int64_t ldy = 0;
+  size_t G = NONE;         // gradient at this block's output, row-major
+  int64_t ldg = 0;
   size_t ws = NONE;
   int64_t ldws = 0;
   int splits = 1, kchunk = 0;
@@ -102,7 +102,7 @@ struct un_ctx {
   size_t bytes = 0;
   hipStream_t stream = nullptr;
   // fixed buffers
-  size_t xstage = NONE, ydev = NONE, losses_dev = NONE, ce_partial = NONE, Xin = NONE, XinT = NONE;
+  size_t xstage = NONE, ydev = NONE, losses_dev = NONE, ce_partial = NONE, Xin = NONE;
   size_t XinC = NONE;  // NHWC input with channels padded to a 16-byte multiple (first convs only)
   size_t lr_dev = NONE;          // per-model learning rates of the current un_step_lr call
   const float* lrv = nullptr;    // lr_dev while such a step is being launched, else null (one rate)
@@ -121,7 +121,7 @@ struct un_ctx {
   size_t opt_dev = NONE;         // OptHp per model
   const OptHp* optp = nullptr;   // opt_dev while a step with optimizers is being launched
   int in_cs = 0;       // stored channels of XinC
-  int64_t ldxin = 0, ldxint = 0;
+  int64_t ldxin = 0;
   // schedule
   std::vector<Launch> fwd, bwd[2];  // bwd[p]: dgrad reads copy p of the transposed weights
   Launch ce{}, refresh[2]{};
@@ -132,8 +132,7 @@ struct un_ctx {
     int64_t in_feat = 0, kin_p = 0, cat_rows = 0;
     std::vector<int> cat;        // models whose first layer is in the concatenated level-0 GEMM
     std::vector<int64_t> cat_off;  // their first row in it (-1: not in it)
-    size_t catW32 = NONE, catb32 = NONE, catgW = NONE, catgb = NONE, catWb = NONE, catY = NONE, catYT = NONE,
-           catGT = NONE;
+    size_t catW32 = NONE, catb32 = NONE, catgW = NONE, catgb = NONE, catWb = NONE, catY = NONE, catG = NONE;
     size_t cat_row_model = NONE;  // int32 per concatenated row: the model owning it
     size_t catS1 = NONE, catS1b = NONE, catS2 = NONE, catS2b = NONE;  // state of the concatenation (sbase)
   } plan;
@@ -447,7 +446,7 @@ static void build_tables(un_ctx* c, Tables& T) {
   const int64_t in_feat = c->plan.in_feat, kin_p = c->plan.kin_p, cat_rows = c->plan.cat_rows;
   auto sub = [](size_t off, int64_t bytes) { return off == NONE ? NONE : off + (size_t)bytes; };
   const size_t catW32 = c->plan.catW32, catb32 = c->plan.catb32, catgW = c->plan.catgW, catgb = c->plan.catgb,
-               catWb = c->plan.catWb, catY = c->plan.catY, catYT = c->plan.catYT, catGT = c->plan.catGT;
+               catWb = c->plan.catWb, catY = c->plan.catY, catG = c->plan.catG;
   // runs of consecutive active models of the concatenated level-0 GEMM: [first row, rows)
   std::vector<std::pair<int64_t, int64_t>> cat_runs;
   {
@@ -530,9 +529,8 @@ static void build_tables(un_ctx* c, Tables& T) {
     size_t po = put(ps.data(), ps.size() * sizeof(GemmProb));
     for (size_t k = 0; k < ps.size(); ++k) {
       size_t b0 = po + k * sizeof(GemmProb);
-      for (size_t f : {offsetof(GemmProb, A), offsetof(GemmProb, B), offsetof(GemmProb, C), offsetof(GemmProb, CT),
-                       offsetof(GemmProb, bias), offsetof(GemmProb, mask), offsetof(GemmProb, dbias),
-                       offsetof(GemmProb, W), offsetof(GemmProb, Wb), offsetof(GemmProb, WT),
+      for (size_t f : {offsetof(GemmProb, A), offsetof(GemmProb, B), offsetof(GemmProb, C), offsetof(GemmProb, bias),
+                       offsetof(GemmProb, mask), offsetof(GemmProb, dbias), offsetof(GemmProb, W), offsetof(GemmProb, Wb),
                        offsetof(GemmProb, bmaster), offsetof(GemmProb, row_model)})
         fix.push_back(b0 + f);
     }
@@ -653,8 +651,6 @@ static void build_tables(un_ctx* c, Tables& T) {
             p.relu = 1;
             p.C = ptr(sub(catY, run.first * (int64_t)es));
             p.ldc = cat_rows;
-            p.CT = ptr(sub(catYT, run.first * Bp * (int64_t)es));
-            p.ldct = Bp;
             p.bias = (const float*)ptr(sub(catb32, run.first * 4));
             gp.push_back(p);
           }
@@ -672,8 +668,6 @@ static void build_tables(un_ctx* c, Tables& T) {
         p.relu = b.relu;
         p.C = ptr(b.Y);
         p.ldc = b.ldy;
-        p.CT = ptr(b.YT);
-        p.ldct = b.ldyt;
         p.bias = (const float*)ptr(b.b32);
         gp.push_back(p);
       } else {
@@ -687,8 +681,6 @@ static void build_tables(un_ctx* c, Tables& T) {
         p.bias = (const float*)ptr(b.b32);
         p.P = ptr(b.Y);
         p.amax = (uint8_t*)ptr(b.amax);
-        p.PT = ptr(b.YT);
-        p.ldpt = b.ldyt;
         plan_halo(p, bf, false);
         cp.push_back(p);
       }
@@ -707,8 +699,6 @@ static void build_tables(un_ctx* c, Tables& T) {
     p.ldl = b.ldy;
     p.G = ptr(b.G);
     p.ldg = b.ldg;
-    p.GT = ptr(b.GT);
-    p.ldgt = b.ldgt;
     p.C = b.N;
     p.model = (int)mi;
     ces.push_back(p);
@@ -722,99 +712,104 @@ static void build_tables(un_ctx* c, Tables& T) {
     T.ce = Launch{5, UN_K_CE, po, NONE, (int)ces.size()};
   }
 
-  // backward levels, once per parity of the transposed-weight copies: the
-  // dgrad of a level reads copy `par` while the fused update of the same
-  // launch writes the other copy.
-  for (int par = 0; par < 2; ++par)
+  // Backward launches, one per level lv from the deepest: the Linear data
+  // gradients of level lv and the Linear weight gradients of level lv + 1
+  // (at lv == 0 also those of level 0). A block's weights are updated one
+  // launch after its data gradient has read them, so no launch both reads and
+  // writes the same weights. Conv blocks keep their own per-level launches
+  // (data gradient, then split-K weight gradient, then the reduction with the
+  // update).
+  auto add_wgrad = [&](const Block& b, std::vector<GemmProb>& gp, bool& cat_done) {
+    if (b.concat) {
+      // one problem per run of consecutive active models of the concatenation
+      if (cat_done) return;
+      cat_done = true;
+      for (const auto& run : cat_runs) {
+        GemmProb p{};
+        p.A = ptr(sub(catG, run.first * (int64_t)es));
+        p.lda = cat_rows;
+        p.amode = OP_KMAJ;
+        p.B = ptr(c->Xin);
+        p.ldb = c->ldxin;
+        p.bmode = OP_KMAJ;
+        p.M = (int)run.second;
+        p.N = (int)in_feat + 1;
+        p.K = B;
+        p.epi = EPI_WGRAD;
+        p.nsplit = (int)in_feat;
+        p.C = ptr(sub(catgW, run.first * kin_p * 4));
+        p.ldc = kin_p;
+        p.dbias = (float*)ptr(sub(catgb, run.first * 4));
+        p.W = (float*)ptr(sub(catW32, run.first * kin_p * 4));
+        p.Wb = ptr(sub(catWb, run.first * kin_p * 2));
+        p.bmaster = (float*)ptr(sub(catb32, run.first * 4));
+        p.row_model = (const int32_t*)ptr(sub(c->plan.cat_row_model, run.first * 4));
+        p.s1 = sp(c->plan.catS1, run.first * kin_p * 4);
+        p.s2 = sp(c->plan.catS2, run.first * kin_p * 4);
+        p.sb1 = sp(c->plan.catS1b, run.first * 4);
+        p.sb2 = sp(c->plan.catS2b, run.first * 4);
+        gp.push_back(p);
+      }
+      return;
+    }
+    GemmProb p{};
+    p.A = ptr(b.G);
+    p.lda = b.ldg;
+    p.amode = OP_KMAJ;
+    p.B = ptr(b.X);
+    p.ldb = b.ldx;
+    p.bmode = OP_KMAJ;
+    p.M = b.N;
+    p.N = b.K + 1;
+    p.K = B;
+    p.epi = EPI_WGRAD;
+    p.nsplit = b.K;
+    p.C = ptr(b.gW);
+    p.ldc = b.ldw;
+    p.dbias = (float*)ptr(b.gb);
+    p.W = (float*)ptr(b.W32);
+    p.Wb = ptr(b.Wb);
+    p.bmaster = (float*)ptr(b.b32);
+    p.model = b.model;
+    p.s1 = sp(b.S1, 0);
+    p.s2 = sp(b.S2, 0);
+    p.sb1 = sp(b.S1b, 0);
+    p.sb2 = sp(b.S2b, 0);
+    gp.push_back(p);
+  };
   for (int lv = levels - 1; lv >= 0; --lv) {
     std::vector<GemmProb> gp;
     std::vector<ConvProb> dp, wp;
     std::vector<ReduceProb> rp;
     bool cat_done = false;
     for (auto& m : c->models) {
-      if (lv >= (int)m.blocks.size() || !c->active[m.blocks[0].model]) continue;
+      if (!c->active[m.blocks[0].model]) continue;
+      const int depth = (int)m.blocks.size();
+      if (lv + 1 < depth && m.blocks[lv + 1].kind == 0) add_wgrad(m.blocks[lv + 1], gp, cat_done);
+      if (lv >= depth) continue;
       Block& b = m.blocks[lv];
       if (b.kind == 0) {
-        // dgrad (not at level 0): gradient at the previous block's output
+        // data gradient (not at level 0): the gradient at the previous block's output
         if (lv > 0) {
           Block& pb = m.blocks[lv - 1];
           GemmProb p{};
           p.A = ptr(b.G);
           p.lda = b.ldg;
-          p.B = ptr(par == 0 ? b.WT : b.WT2);
-          p.ldb = b.ldwt;
+          p.B = ptr(bf ? b.Wb : b.W32);
+          p.ldb = b.ldw;
+          p.bmode = OP_KMAJ;
           p.M = B;
           p.N = b.K;
           p.K = b.N;
           p.epi = EPI_DGRAD;
           p.relu = pb.relu;
-          p.mask = ptr(b.XT);
-          p.ldmask = b.ldxt;
-          if (pb.kind == 0) {
-            p.C = ptr(pb.G);
-            p.ldc = pb.ldg;
-            p.CT = ptr(pb.GT);
-            p.ldct = pb.ldgt;
-          } else {
-            p.C = ptr(pb.G);
-            p.ldc = pb.out_elems_per_sample();
-          }
+          p.mask = ptr(b.X);  // the previous block's stored output, row-major
+          p.ldmask = b.ldx;
+          p.C = ptr(pb.G);
+          p.ldc = pb.kind == 0 ? pb.ldg : pb.out_elems_per_sample();
           gp.push_back(p);
         }
-        // wgrad (+ bias gradient through the ones row of XT)
-        if (b.concat) {
-          if (cat_done) continue;
-          cat_done = true;
-          for (const auto& run : cat_runs) {
-            GemmProb p{};
-            p.A = ptr(sub(catGT, run.first * Bp * (int64_t)es));
-            p.lda = Bp;
-            p.B = ptr(c->XinT);
-            p.ldb = c->ldxint;
-            p.M = (int)run.second;
-            p.N = (int)in_feat + 1;
-            p.K = B;
-            p.epi = EPI_WGRAD;
-            p.nsplit = (int)in_feat;
-            p.C = ptr(sub(catgW, run.first * kin_p * 4));
-            p.ldc = kin_p;
-            p.dbias = (float*)ptr(sub(catgb, run.first * 4));
-            p.W = (float*)ptr(sub(catW32, run.first * kin_p * 4));
-            p.Wb = ptr(sub(catWb, run.first * kin_p * 2));
-            p.bmaster = (float*)ptr(sub(catb32, run.first * 4));
-            p.row_model = (const int32_t*)ptr(sub(c->plan.cat_row_model, run.first * 4));
-            p.s1 = sp(c->plan.catS1, run.first * kin_p * 4);
-            p.s2 = sp(c->plan.catS2, run.first * kin_p * 4);
-            p.sb1 = sp(c->plan.catS1b, run.first * 4);
-            p.sb2 = sp(c->plan.catS2b, run.first * 4);
-            gp.push_back(p);
-          }
-          continue;
-        }
-        GemmProb p{};
-        p.A = ptr(b.GT);
-        p.lda = b.ldgt;
-        p.B = ptr(b.XT);
-        p.ldb = b.ldxt;
-        p.M = b.N;
-        p.N = b.K + 1;
-        p.K = B;
-        p.epi = EPI_WGRAD;
-        p.nsplit = b.K;
-        p.C = ptr(b.gW);
-        p.ldc = b.ldw;
-        p.dbias = (float*)ptr(b.gb);
-        p.W = (float*)ptr(b.W32);
-        p.Wb = ptr(b.Wb);
-        p.WT = ptr(par == 0 ? b.WT2 : b.WT);
-        p.ldwt = b.ldwt;
-        p.bmaster = (float*)ptr(b.b32);
-        p.model = b.model;
-        p.s1 = sp(b.S1, 0);
-        p.s2 = sp(b.S2, 0);
-        p.sb1 = sp(b.S1b, 0);
-        p.sb2 = sp(b.S2b, 0);
-        gp.push_back(p);
+        if (lv == 0) add_wgrad(b, gp, cat_done);
       } else {
         const int J = b.KH * b.KH * b.C;
         if (lv > 0) {
@@ -867,9 +862,9 @@ static void build_tables(un_ctx* c, Tables& T) {
         rp.push_back(r);
       }
     }
-    emit_gemm(gp, bwd[par], UN_K_GEMM_BWD);
-    emit_conv(dp, bwd[par], 2, UN_K_CONV_DGRAD);
-    emit_conv(wp, bwd[par], 3, UN_K_CONV_WGRAD);
+    emit_gemm(gp, bwd[0], UN_K_GEMM_BWD);
+    emit_conv(dp, bwd[0], 2, UN_K_CONV_DGRAD);
+    emit_conv(wp, bwd[0], 3, UN_K_CONV_WGRAD);
     if (!rp.empty()) {
       std::vector<int32_t> map;
       for (size_t k = 0; k < rp.size(); ++k) {
@@ -886,9 +881,11 @@ static void build_tables(un_ctx* c, Tables& T) {
           fix.push_back(b0 + f);
       }
       size_t mo = put(map.data(), map.size() * 4);
-      bwd[par].push_back(Launch{4, UN_K_OTHER, po, mo, (int)map.size()});
+      bwd[0].push_back(Launch{4, UN_K_OTHER, po, mo, (int)map.size()});
     }
   }
+  // (the two step parities now share one backward schedule)
+  bwd[1] = bwd[0];
 
   // Shadow refresh (after un_set_params / initialisation): rewrite the bf16
   // shadow and transposed copy `pass` of every weight from the fp32 master.
@@ -908,7 +905,8 @@ static void build_tables(un_ctx* c, Tables& T) {
         SgdTensor w{};
         w.W = (float*)ptr(b.W32);
         w.Wb = ptr(b.Wb);
-        w.WT = ptr(pass == 1 && b.WT2 != NONE ? b.WT2 : b.WT);
+        if (b.Wb == NONE && b.WT == NONE) continue;  // fp32 Linear: nothing besides the master
+        w.WT = ptr(b.WT);
         w.ldw = b.ldw;
         w.ldwt = b.ldwt;
         w.R = b.rows;
@@ -1004,11 +1002,8 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
   }
   if (c->XinC == NONE || any_linear0) c->Xin = A.take((size_t)B * in_feat * es);
   c->ldxin = in_feat;
-  if (any_linear0) {
-    if (in_feat % 8 != 0) return fail(nullptr, UN_ERR_UNSUPPORTED, "input features must be a multiple of 8 when a model starts with Linear");
-    c->ldxint = Bp;
-    c->XinT = A.take((size_t)(in_feat + 1) * Bp * es);
-  }
+  if (any_linear0 && in_feat % 8 != 0)
+    return fail(nullptr, UN_ERR_UNSUPPORTED, "input features must be a multiple of 8 when a model starts with Linear");
 
   // --- level-0 concatenation group: hidden Linear + ReLU reading the shared input
   std::vector<int> cat;  // model indices
@@ -1023,8 +1018,7 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
     cat_rows += rup(c->models[i].blocks[0].N + 1, 8);  // >= 1 spare row: the ones row of YT
   }
   const int64_t kin_p = rup(in_feat, 8);
-  size_t catW32 = NONE, catb32 = NONE, catgW = NONE, catgb = NONE, catWb = NONE, catY = NONE, catYT = NONE,
-         catGT = NONE;
+  size_t catW32 = NONE, catb32 = NONE, catgW = NONE, catgb = NONE, catWb = NONE, catY = NONE, catG = NONE;
   if (!cat.empty()) {
     catW32 = A.take((size_t)cat_rows * kin_p * 4);
     catb32 = A.take((size_t)cat_rows * 4);
@@ -1032,8 +1026,7 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
     catgb = A.take((size_t)cat_rows * 4);
     if (bf) catWb = A.take((size_t)cat_rows * kin_p * 2);
     catY = A.take((size_t)B * cat_rows * es);
-    catYT = A.take((size_t)cat_rows * Bp * es);
-    catGT = A.take((size_t)cat_rows * Bp * es);
+    catG = A.take((size_t)B * cat_rows * es);
     c->plan.cat_row_model = A.take((size_t)cat_rows * 4);
   }
 
@@ -1057,10 +1050,8 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
           if (bf) b.Wb = catWb + roff * b.ldw * 2;
           b.ldy = cat_rows;
           b.Y = catY + roff * es;
-          b.ldyt = Bp;
-          b.YT = catYT + roff * Bp * es;
-          b.ldgt = Bp;
-          b.GT = catGT + roff * Bp * es;
+          b.ldg = cat_rows;
+          b.G = catG + roff * es;
         } else {
           b.W32 = A.take((size_t)b.N * b.ldw * 4);
           b.b32 = A.take((size_t)b.N * 4);
@@ -1073,18 +1064,9 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
           } else {
             b.ldy = rup(b.N, 8);
             b.Y = A.take((size_t)B * b.ldy * es);
-            b.ldyt = Bp;
-            b.YT = A.take((size_t)(b.N + 1) * Bp * es);  // + ones row
           }
           b.ldg = rup(b.N, 8);
-          if (j > 0) b.G = A.take((size_t)B * b.ldg * es);
-          b.ldgt = Bp;
-          b.GT = A.take((size_t)b.N * Bp * es);
-        }
-        if (j > 0) {
-          b.ldwt = rup(b.N, 8);
-          b.WT = A.take((size_t)b.K * b.ldwt * es);
-          b.WT2 = A.take((size_t)b.K * b.ldwt * es);
+          b.G = A.take((size_t)B * b.ldg * es);
         }
       } else {
         const int J = b.KH * b.KH * b.C;
@@ -1103,10 +1085,6 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
         b.Y = A.take((size_t)npix * b.O * es);
         b.ldy = b.O;
         if (b.pool) b.amax = A.take((size_t)npix * b.O);
-        if (b.next_linear) {
-          b.ldyt = Bp;
-          b.YT = A.take((size_t)(b.out_elems_per_sample() + 1) * Bp * es);
-        }
         b.G = A.take((size_t)npix * b.O * es);
         b.ldg = b.O;
         // split-K of the weight gradient: depends only on this block's shape
@@ -1131,14 +1109,10 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
       if (j == 0) {
         b.X = (b.kind == 1 && c->XinC != NONE) ? c->XinC : c->Xin;
         b.ldx = c->ldxin;
-        b.XT = c->XinT;
-        b.ldxt = c->ldxint;
       } else {
         Block& p = m.blocks[j - 1];
         b.X = p.Y;
         b.ldx = p.kind == 0 ? p.ldy : p.out_elems_per_sample();
-        b.XT = p.YT;
-        b.ldxt = p.ldyt;
       }
     }
   }
@@ -1156,8 +1130,7 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
   c->plan.catgb = catgb;
   c->plan.catWb = catWb;
   c->plan.catY = catY;
-  c->plan.catYT = catYT;
-  c->plan.catGT = catGT;
+  c->plan.catG = catG;
   c->active.assign(c->models.size(), 1);
   Tables T;
   build_tables(c, T);
@@ -1178,15 +1151,6 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
     un_status st = install_tables(c, T);
     if (st != UN_OK) return st;
   }
-  // ones rows of the transposed inputs (bias-gradient column of the wgrad GEMMs)
-  std::vector<uint16_t> ones16((size_t)Bp, 0x3F80);
-  std::vector<float> ones32((size_t)Bp, 1.0f);
-  const void* ones = bf ? (const void*)ones16.data() : (const void*)ones32.data();
-  auto set_ones_row = [&](size_t buf, int64_t row, int64_t ld) -> hipError_t {
-    return hipMemcpyAsync(c->base + buf + (size_t)row * ld * es, ones, (size_t)B * es, hipMemcpyHostToDevice,
-                          c->stream);
-  };
-  if (c->XinT != NONE) HIPCHK(c, set_ones_row(c->XinT, in_feat, Bp));
   std::vector<int32_t> row_model((size_t)cat_rows);
   if (!cat.empty()) {
     for (size_t k = 0; k < cat.size(); ++k) {
@@ -1199,17 +1163,6 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
   // the padding channels of XinC are written here only, once
   if (c->XinC != NONE)
     HIPCHK(c, hipMemsetAsync(c->base + c->XinC, 0, (size_t)B * c->in_h * c->in_w * c->in_cs * es, c->stream));
-  for (auto& m : c->models)
-    for (auto& b : m.blocks)
-      if (b.YT != NONE && !b.concat) HIPCHK(c, set_ones_row(b.YT, b.out_elems_per_sample(), b.ldyt));
-  // concatenated level 0: a zero-weight unit with bias 1 produces the ones row
-  if (!cat.empty()) {
-    std::vector<float> bias1(1, 1.0f);
-    for (int i : cat) {
-      const Block& b = c->models[i].blocks[0];
-      HIPCHK(c, hipMemcpyAsync(c->base + b.b32 + (size_t)b.N * 4, bias1.data(), 4, hipMemcpyHostToDevice, c->stream));
-    }
-  }
   HIPCHK(c, hipStreamSynchronize(c->stream));
   return UN_OK;
 }
@@ -1347,7 +1300,8 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
   hipError_t e = hipSuccess;
   switch (l.kind) {
     case 0:
-      e = launch_gemm(c->bf16, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->lrv, c->optp, c->keep_grads,
+      e = launch_gemm(c->bf16, l.kclass == UN_K_GEMM_BWD, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, lr,
+                      c->lrv, c->optp, c->keep_grads,
                       c->stream);
       break;
     case 1:
@@ -1520,7 +1474,7 @@ static un_status load_common(un_ctx* c, const float* x, const int32_t* y, bool d
   }
   HIPCHK(c, hipMemcpyAsync(c->base + c->ydev, yh.data(), (size_t)c->B * 4, hipMemcpyHostToDevice, c->stream));
   HIPCHK(c, launch_load(c->bf16, xsrc, c->B, c->in_c, c->in_h, c->in_w, c->Xin == NONE ? nullptr : c->base + c->Xin,
-                        c->XinT == NONE ? nullptr : c->base + c->XinT, c->ldxint,
+                        nullptr, 0,
                         c->XinC == NONE ? nullptr : c->base + c->XinC, c->in_cs, c->stream));
   HIPCHK(c, hipStreamSynchronize(c->stream));
   c->loaded = true;
