@@ -145,7 +145,12 @@ def compare_run(wl, gpu, orc, models, tol=None, update_tol=None):
       parameters: Frobenius relative error <= tol per tensor, and per-element
         max relative error <= FLAGGED_TOL (guard against localised gross errors);
       updates theta_k - theta_0 and last-step gradients: Frobenius relative
-        error <= update_tol per tensor (UPDATE_TOL by default).
+        error <= update_tol per tensor (UPDATE_TOL by default), over the
+        parameters of units the oracle did not flag. A flipped decision at a
+        flagged unit changes one sample's share of that unit's gradient; an
+        optimizer that normalises the step per element (Adam) turns that into
+        a change of the whole step of those parameters, however small the
+        share, so their updates are held by the per-element guard only.
     """
     tol = TOL[wl.precision] if tol is None else tol
     # One flipped decision moves its unit's row of one step's update by a few
@@ -161,10 +166,13 @@ def compare_run(wl, gpu, orc, models, tol=None, update_tol=None):
         _losses(wl, losses_g, i, losses_o, tol, worst)
         worst["flagged_units"] += sum(len(v) for v in flags.values())
         th0 = theta0(wl, i)
+        fm = flagged_masks(params_o, flags)
         for t, (pg, po, gg, go) in enumerate(zip(params_g[i], params_o, grads_g[i], grads_o)):
+            keep = ~fm[t]
+            ug, uo = np.asarray(pg - th0[t])[keep], np.asarray(po - th0[t])[keep]
             checks = (("param_fro", fro_err(pg, po), tol), ("param_max", tensor_err(pg, po), FLAGGED_TOL),
-                      ("update_fro", fro_err(pg - th0[t], po - th0[t]), update_tol),
-                      ("grad_fro", fro_err(gg, go), update_tol))
+                      ("update_fro", fro_err(ug, uo), update_tol),
+                      ("grad_fro", fro_err(np.asarray(gg)[keep], np.asarray(go)[keep]), update_tol))
             for key, e, bound in checks:
                 worst[key] = max(worst[key], e)
                 assert e <= bound, f"model {i} tensor {t}: {key} {e:.3g} > {bound}"
