@@ -1228,16 +1228,24 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
   }
 
   // Weight gradient with the SGD update fused: the master-weight loads of
-  // this thread's float4 chunks of W[m][n..n+3] are issued first, so their
-  // latency overlaps the staging below.
+  // this thread's float4 chunks of W[m][n..n+3] (and, with per-model rates,
+  // each tile row's rate, to LDS) are issued first, so their latency
+  // overlaps the staging below.
   constexpr int CPR = BN / 4, NCH = BM * CPR / NT;
   const int ns = p.nsplit;
   f32x4 w0[NCH];
+  __shared__ float s_lr[BM];
   if (p.epi == EPI_WGRAD) {
 #pragma unroll
     for (int q = 0; q < NCH; ++q) {
       const int idx = threadIdx.x + NT * q, r = idx / CPR, n = n0 + (idx - r * CPR) * 4, m = m0 + r;
       w0[q] = (m < p.M && n + 4 <= ns) ? *(gptr<const f32x4>)(p.W + (int64_t)m * p.ldc + n) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    if constexpr (!OPT) {
+      if (lrv && (int)threadIdx.x < BM) {
+        const int m = m0 + threadIdx.x;
+        s_lr[threadIdx.x] = m < p.M ? G(lrv)[p.row_model ? G(p.row_model)[m] : p.model] : 0.f;
+      }
     }
   }
 
@@ -1278,16 +1286,19 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
   }
 
   // EPI_WGRAD, SGD fused. Row pass over the float4 chunks: the update, the
-  // bf16 shadow, the kept gradient. The bias column (n == nsplit) is done
-  // element-wise.
+  // bf16 copy, the kept gradient. The bias column (n == nsplit) is done
+  // element-wise. The master weights this loop reads have all landed before
+  // its first store (one wait here): a wait for a load issued before a store
+  // still in flight would wait for that store as well, every chunk.
+  __builtin_amdgcn_s_waitcnt(0);
 #pragma unroll
   for (int q = 0; q < NCH; ++q) {
     const int idx = threadIdx.x + NT * q, r = idx / CPR, cc = idx - r * CPR;
     const int m = m0 + r, n = n0 + cc * 4;
     if (m >= p.M || n > ns) continue;
-    // this row's model: its own learning rate (or optimizer) when set per model
-    const int mdl = p.row_model ? p.row_model[m] : p.model;
-    const float lr_m = lrv ? lrv[mdl] : lr;
+    // this row's model: its own optimizer, or its own rate (staged in s_lr)
+    const int mdl = OPT ? (p.row_model ? p.row_model[m] : p.model) : 0;
+    const float lr_m = (!OPT && lrv) ? s_lr[r] : lr;
     float* s = sC + r * CLD + sc_col(r, cc * 4);
     const int64_t base = (int64_t)m * p.ldc + n;
     if (n + 4 <= ns) {
