@@ -1827,6 +1827,137 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 conv weight gradient on the grouped GEMM's machinery: 16 waves of
+// 32x32x16 MFMA tiles, loads two k-blocks ahead, and both operands staged in
+// LDS k-major - as they lie in memory, [pixel][channel] - and turned into MFMA
+// operands by the LDS transpose reads. For blocks whose channel counts O and
+// C are whole 16-byte vectors (pooled or not).
+//   A (rows o):      dZ[pixel][o], gathered from the pooled gradient G[w][o]
+//                    and the window argmax (pooled), or G[pixel][o] itself;
+//   B (rows j):      the input patch X[n][y+u-pad][x+v-pad][c], j = (u,v,c),
+//                    and the bias column j == KH*KW*C reading 1.
+// Each thread moves one 16-byte chunk of each operand per k-block: pixel
+// k = t / CPR of the block, rows 8*(t % CPR) .. +7. Pixels of a pooled block
+// are ordered m = 4*w + (dy*2 + dx), so k % 4 is the window position.
+template <int ROWS, int BK, int NT, int SLOTS, int PAD, bool POOL>
+struct ConvKA {
+  static constexpr int VEC = 8, CPR = ROWS / VEC, LDR = ROWS + PAD;
+  static constexpr int OOB = 0x7ffffff0;  // a buffer offset past every range: the load returns zero
+  static_assert(BK * CPR == NT, "one chunk per thread and k-block");
+  static_assert(BK % 4 == 0, "k-blocks hold whole windows");
+  __amdgpu_buffer_rsrc_t rs, rs_am;
+  int O, K, o, k, kpix0;
+  u32x4 r[SLOTS];
+  uint64_t am[SLOTS];
+  __device__ __forceinline__ void init(const ConvProb& p, int o0, int kb0) {
+    k = threadIdx.x / CPR;
+    o = o0 + (threadIdx.x % CPR) * VEC;
+    O = p.O;
+    K = p.K;
+    kpix0 = kb0 * BK + k;
+    const int64_t rows = POOL ? (int64_t)p.Nb * p.PH * p.PW : (int64_t)p.Nb * p.OH * p.OW;
+    rs = make_rsrc(p.G, rows * p.O * (int64_t)sizeof(bf16_t));
+    if constexpr (POOL) rs_am = make_rsrc(p.gam, rows * p.O);
+  }
+  template <int S>
+  __device__ __forceinline__ void load(int kb) {
+    const int pix = kpix0 + kb * BK;
+    const bool in = o < O && pix < K;
+    const int row = POOL ? pix >> 2 : pix, off = row * O + o;
+    r[S] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? off * 2 : OOB, 0, 0));
+    if constexpr (POOL) am[S] = in ? load_am_buf<bf16_t>(rs_am, off) : 0ull;
+  }
+  template <int S>
+  __device__ __forceinline__ void store(bf16_t* sm) const {
+    u32x4 v = r[S];
+    if constexpr (POOL) select_am<bf16_t>(v, am[S], k & 3);
+    *(u32x4*)(sm + k * LDR + (threadIdx.x % CPR) * VEC) = v;
+  }
+};
+
+template <int ROWS, int BK, int NT, int SLOTS, int PAD, bool POOL>
+struct ConvKB {
+  static constexpr int VEC = 8, CPR = ROWS / VEC, LDR = ROWS + PAD;
+  static constexpr int OOB = 0x7ffffff0;
+  static_assert(BK * CPR == NT, "one chunk per thread and k-block");
+  __amdgpu_buffer_rsrc_t rs;
+  const ConvProb* p;
+  int k, kpix0, c0, u, v;
+  bool jin, bias;
+  u32x4 r[SLOTS];
+  __device__ __forceinline__ void init(const ConvProb& pr, int j0, int kb0) {
+    p = &pr;
+    k = threadIdx.x / CPR;
+    const int j = j0 + (threadIdx.x % CPR) * VEC, J = pr.KH * pr.KH * pr.C;
+    jin = j < J;
+    bias = j == J;
+    const int tap = j / pr.C;
+    c0 = j - tap * pr.C;
+    u = tap / pr.KH;
+    v = tap - u * pr.KH;
+    kpix0 = kb0 * BK + k;
+    rs = make_rsrc(pr.X, (int64_t)pr.Nb * pr.H * pr.W * pr.C * (int64_t)sizeof(bf16_t));
+  }
+  template <int S>
+  __device__ __forceinline__ void load(int kb) {
+    const int pix = kpix0 + kb * BK;
+    const bool pin = pix < p->K;
+    int n, y, x;
+    decode_out_pixel(*p, pin ? pix : 0, n, y, x);
+    const int iy = y + u - p->pad, ix = x + v - p->pad;
+    const bool in = jin && pin && iy >= 0 && iy < p->H && ix >= 0 && ix < p->W;
+    u32x4 val = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? (((n * p->H + iy) * p->W + ix) * p->C + c0) * 2 : OOB, 0, 0));
+    if (bias && pin) vset_bits<bf16_t>(val, 0, bits_of<bf16_t>(TT<bf16_t>::from_f(1.0f)));
+    r[S] = val;
+  }
+  template <int S>
+  __device__ __forceinline__ void store(bf16_t* sm) const {
+    *(u32x4*)(sm + k * LDR + (threadIdx.x % CPR) * VEC) = r[S];
+  }
+};
+
+template <bool POOL>
+__global__ __launch_bounds__((GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>::NT))
+__attribute__((amdgpu_waves_per_eu((GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>::NT / 128))))
+void conv_wgrad_mfma_kernel(const ConvProb* __restrict__ probs, const int32_t* __restrict__ tile_map) {
+  constexpr int BM = CONV_BM_BF16, BN = CONV_BN_BF16, BK = CONV_BK_BF16;
+  using MM = GemmMma<bf16_t, BM, BN, BK>;
+  constexpr int NT = MM::NT, D = UN_GEMM_DEPTH;
+  static_assert(MM::LDR_A * BK <= Tile<bf16_t, BM, BN, BK>::A_ELEMS &&
+                    MM::LDR_B * BK <= Tile<bf16_t, BM, BN, BK>::B_ELEMS, "k-major stages fit the stage buffers");
+  __shared__ __attribute__((aligned(16))) char smem[Smem<bf16_t, BM, BN, BK>::BYTES];
+  const int prob = tile_map[2 * blockIdx.x];
+  int local = tile_map[2 * blockIdx.x + 1];
+  if (prob < 0) return;  // padding of the XCD-ordered tile list
+  const ConvProb& p = probs[prob];
+  const int per_split = p.tiles_m * p.tiles_n;
+  const int split = local / per_split;
+  local -= split * per_split;
+  const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int kb0 = split * p.kchunk, nkb = min((p.K + BK - 1) / BK, kb0 + p.kchunk) - kb0;
+
+  typename MM::Acc acc;
+  MM::zero(acc);
+  ConvKA<BM, BK, NT, D, KMAJ_PAD_BF16, POOL> la;
+  ConvKB<BN, BK, NT, D, KMAJ_PAD_BF16, POOL> lb;
+  la.init(p, m0, kb0);
+  lb.init(p, n0, kb0);
+  gemm_loop<bf16_t, BM, BN, BK, D, MM, OP_KMAJ, OP_KMAJ>(la, lb, nkb, (bf16_t*)smem, acc);
+
+  // this split's partial sums to ws[split][o][j]
+  float* ws = p.ws + (int64_t)split * p.O * p.ldws;
+  MM::for_groups(acc, [&](int rl, int cl, float (&v)[4]) {
+    const int mb = m0 + rl, n = n0 + cl;
+    if (n >= p.N) return;
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      if (mb + r < p.M) ws[(int64_t)(mb + r) * p.ldws + n] = v[r];
+  });
+}
+
 // Sum the split-K partials in split order, then the fused SGD update.
 template <typename T>
 __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* __restrict__ probs,
@@ -2088,8 +2219,11 @@ hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const i
 #define UN_WGRAD_LAUNCH(T, BM, BN, BK, M) \
   hipLaunchKernelGGL((conv_wgrad_kernel<T, BM, BN, BK, M>), dim3(ntiles), dim3(256), 0, s, probs, tile_map)
   if (bf16) {
-    if (mode == WG_POOLED) UN_WGRAD_LAUNCH(bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, WG_POOLED);
-    else if (mode == WG_PLAIN) UN_WGRAD_LAUNCH(bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, WG_PLAIN);
+    constexpr int NT = GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>::NT;
+    if (mode == WG_POOLED)
+      hipLaunchKernelGGL(conv_wgrad_mfma_kernel<true>, dim3(ntiles), dim3(NT), 0, s, probs, tile_map);
+    else if (mode == WG_PLAIN)
+      hipLaunchKernelGGL(conv_wgrad_mfma_kernel<false>, dim3(ntiles), dim3(NT), 0, s, probs, tile_map);
     else UN_WGRAD_LAUNCH(bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, WG_GENERIC);
   } else {
     if (mode == WG_POOLED) UN_WGRAD_LAUNCH(float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, WG_POOLED);
