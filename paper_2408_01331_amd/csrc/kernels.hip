@@ -1109,25 +1109,25 @@ __device__ __forceinline__ void opt_update4(const OptHp& h, const f32x4& g, f32x
     for (int e = 0; e < 4; ++e) w[e] = fmaf(-h.lr, g[e], w[e]);
     return;
   }
-  f32x4 a = *(gptr<const f32x4>)s1;
+  f32x4 a = __builtin_nontemporal_load((gptr<const f32x4>)s1);
   if (h.kind == 1.f) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       a[e] = fmaf(h.b1, a[e], g[e]);
       w[e] = fmaf(-h.lr, a[e], w[e]);
     }
-    *(gptr<f32x4>)s1 = a;
+    __builtin_nontemporal_store(a, (gptr<f32x4>)s1);
     return;
   }
-  f32x4 v = *(gptr<const f32x4>)s2;
+  f32x4 v = __builtin_nontemporal_load((gptr<const f32x4>)s2);
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     a[e] = fmaf(h.b1, a[e], h.c1 * g[e]);
     v[e] = fmaf(h.b2, v[e], h.c2 * g[e] * g[e]);
     w[e] = w[e] - h.lr * (a[e] / (sqrtf(v[e]) * h.isb2 + h.eps));
   }
-  *(gptr<f32x4>)s1 = a;
-  *(gptr<f32x4>)s2 = v;
+  __builtin_nontemporal_store(a, (gptr<f32x4>)s1);
+  __builtin_nontemporal_store(v, (gptr<f32x4>)s2);
 }
 
 // Column of element (r, c) in the GEMM epilogue's LDS tile: c XOR a multiple
@@ -1230,7 +1230,9 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
   // Weight gradient with the SGD update fused: the master-weight loads of
   // this thread's float4 chunks of W[m][n..n+3] (and, with per-model rates,
   // each tile row's rate, to LDS) are issued first, so their latency
-  // overlaps the staging below.
+  // overlaps the staging below. Master weights, their bf16 copies and the
+  // optimizer state are touched once per step: they are loaded and stored
+  // non-temporally, so they do not evict the launch's reused operands from L2.
   constexpr int CPR = BN / 4, NCH = BM * CPR / NT;
   const int ns = p.nsplit;
   f32x4 w0[NCH];
@@ -1239,7 +1241,7 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
 #pragma unroll
     for (int q = 0; q < NCH; ++q) {
       const int idx = threadIdx.x + NT * q, r = idx / CPR, n = n0 + (idx - r * CPR) * 4, m = m0 + r;
-      w0[q] = (m < p.M && n + 4 <= ns) ? *(gptr<const f32x4>)(p.W + (int64_t)m * p.ldc + n) : f32x4{0.f, 0.f, 0.f, 0.f};
+      w0[q] = (m < p.M && n + 4 <= ns) ? __builtin_nontemporal_load((gptr<const f32x4>)(p.W + (int64_t)m * p.ldc + n)) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
     if constexpr (!OPT) {
       if (lrv && (int)threadIdx.x < BM) {
@@ -1312,12 +1314,12 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
         w = f32x4{fmaf(-lr_m, g[0], w0[q][0]), fmaf(-lr_m, g[1], w0[q][1]), fmaf(-lr_m, g[2], w0[q][2]),
                   fmaf(-lr_m, g[3], w0[q][3])};
       }
-      *(gptr<f32x4>)(p.W + base) = w;
+      __builtin_nontemporal_store(w, (gptr<f32x4>)(p.W + base));
       if (p.Wb) {
         u32x2 hb;
         hb[0] = (uint32_t)f2bf(w[0]) | ((uint32_t)f2bf(w[1]) << 16);
         hb[1] = (uint32_t)f2bf(w[2]) | ((uint32_t)f2bf(w[3]) << 16);
-        *(gptr<u32x2>)((bf16_t*)p.Wb + base) = hb;
+        __builtin_nontemporal_store(hb, (gptr<u32x2>)((bf16_t*)p.Wb + base));
       }
     } else {
       for (int e = 0; e < 4 && n + e <= ns && n + e < p.N; ++e) {
@@ -1975,9 +1977,11 @@ __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* 
   if (j < p.J) {
     const int64_t idx = (int64_t)o * p.ldgw + j;
     if (keep_grads) p.gW[idx] = s;
-    const float w = opt ? opt_update1(opt[p.model], s, p.W[idx], p.s1 + idx, p.s2 + idx) : fmaf(-lr, s, p.W[idx]);
-    p.W[idx] = w;
-    if (p.Wb) ((bf16_t*)p.Wb)[idx] = f2bf(w);
+    // master weight and its copies: touched once per step (non-temporal)
+    const float w0 = __builtin_nontemporal_load(G(p.W + idx));
+    const float w = opt ? opt_update1(opt[p.model], s, w0, p.s1 + idx, p.s2 + idx) : fmaf(-lr, s, w0);
+    __builtin_nontemporal_store(w, G(p.W + idx));
+    if (p.Wb) __builtin_nontemporal_store(f2bf(w), G((bf16_t*)p.Wb + idx));
     if (p.WT) {
       const int tap = j / p.C, c = j - tap * p.C;
       store_t<T>(p.WT, (int64_t)c * p.ldwt + (int64_t)tap * p.O + o, w);
