@@ -243,12 +243,12 @@ __device__ __forceinline__ void mma_loop1(L& ld, int kb0, int kb1, T* smem,
 // four consecutive rows of one column a lane holds: f(row, col, v[4]) in tile
 // coordinates. CLD is the row stride (floats) of the epilogue's LDS tile,
 // chosen so that a wave's accumulator writes hit 64 distinct banks.
-template <typename T, int BM, int BN, int BK> struct GemmMma;
+template <typename T, int BM, int BN, int BK, int WGM_ = UN_GEMM_WGM, int WGN_ = UN_GEMM_WGN> struct GemmMma;
 
 // bf16: UN_GEMM_WGM x UN_GEMM_WGN waves (m x n) per workgroup.
-template <int BM, int BN, int BK>
-struct GemmMma<bf16_t, BM, BN, BK> {
-  static constexpr int WGM = UN_GEMM_WGM, WGN = UN_GEMM_WGN, NT = 64 * WGM * WGN;
+template <int BM, int BN, int BK, int WGM_, int WGN_>
+struct GemmMma<bf16_t, BM, BN, BK, WGM_, WGN_> {
+  static constexpr int WGM = WGM_, WGN = WGN_, NT = 64 * WGM * WGN;
   static constexpr int WM = BM / WGM, WN = BN / WGN, FM = WM / 32, FN = WN / 32;
   static_assert(FM >= 1 && FN >= 1, "wave tile smaller than one 32x32 block");
   static constexpr int LDK = Tile<bf16_t, BM, BN, BK>::LDK;
@@ -320,8 +320,8 @@ struct GemmMma<bf16_t, BM, BN, BK> {
   }
 };
 
-template <int BM, int BN, int BK>
-struct GemmMma<float, BM, BN, BK> {
+template <int BM, int BN, int BK, int WGM_, int WGN_>
+struct GemmMma<float, BM, BN, BK, WGM_, WGN_> {
   using TL = Tile<float, BM, BN, BK>;
   static constexpr int NT = 256;
   static constexpr int LDK = TL::LDK;
@@ -1921,11 +1921,11 @@ struct ConvKB {
 };
 
 template <bool POOL>
-__global__ __launch_bounds__((GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>::NT))
-__attribute__((amdgpu_waves_per_eu((GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>::NT / 128))))
+__global__ __launch_bounds__((GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, 4, 4>::NT))
+__attribute__((amdgpu_waves_per_eu((GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, 4, 4>::NT / 128))))
 void conv_wgrad_mfma_kernel(const ConvProb* __restrict__ probs, const int32_t* __restrict__ tile_map) {
   constexpr int BM = CONV_BM_BF16, BN = CONV_BN_BF16, BK = CONV_BK_BF16;
-  using MM = GemmMma<bf16_t, BM, BN, BK>;
+  using MM = GemmMma<bf16_t, BM, BN, BK, 4, 4>;  // 16 waves: one operand chunk per thread
   constexpr int NT = MM::NT, D = UN_GEMM_DEPTH;
   static_assert(MM::LDR_A * BK <= Tile<bf16_t, BM, BN, BK>::A_ELEMS &&
                     MM::LDR_B * BK <= Tile<bf16_t, BM, BN, BK>::B_ELEMS, "k-major stages fit the stage buffers");
@@ -2223,7 +2223,7 @@ hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const i
 #define UN_WGRAD_LAUNCH(T, BM, BN, BK, M) \
   hipLaunchKernelGGL((conv_wgrad_kernel<T, BM, BN, BK, M>), dim3(ntiles), dim3(256), 0, s, probs, tile_map)
   if (bf16) {
-    constexpr int NT = GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16>::NT;
+    constexpr int NT = GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, 4, 4>::NT;
     if (mode == WG_POOLED)
       hipLaunchKernelGGL(conv_wgrad_mfma_kernel<true>, dim3(ntiles), dim3(NT), 0, s, probs, tile_map);
     else if (mode == WG_PLAIN)
