@@ -32,10 +32,17 @@
 #ifndef UN_GEMM_WGN
 #define UN_GEMM_WGN 4
 #endif
-// Padding (elements) of a k-major LDS stage row: the stage holds BK rows of
-// R + pad elements, the same size as the row-major R x (BK + 1 chunk) stage,
-// and 4 consecutive rows start 8 banks apart (conflict-free transpose reads).
-constexpr int KMAJ_PAD_BF16 = 16, KMAJ_PAD_F32 = 8;
+// k-major LDS stages (BK rows of R elements). bf16: no padding, and the
+// 16-byte chunk c of row k is stored at chunk c ^ 4*(k % 4) (kmaj_bf16): a
+// half-wave of transpose reads takes 64 bytes from each of four consecutive
+// rows, which this places in four disjoint 64-byte bank windows. With padded
+// rows instead (stride of 8 banks) the same reads measured twice the LDS
+// cycles (SQ_LDS_BANK_CONFLICT half of SQ_LDS_IDX_ACTIVE). fp32: rows padded
+// by 8 elements.
+constexpr int KMAJ_PAD_BF16 = 0, KMAJ_PAD_F32 = 8;
+__device__ __forceinline__ int kmaj_bf16(int k, int col, int ldr) {
+  return k * ldr + (((col >> 3) ^ ((k & 3) << 2)) << 3) + (col & 7);
+}
 #ifndef UN_HALO_WAVES
 #define UN_HALO_WAVES 8
 #endif
@@ -271,17 +278,19 @@ struct GemmMma<bf16_t, BM, BN, BK, WGM_, WGN_> {
     const int lane = threadIdx.x & 63;
     return __builtin_bit_cast(bf16x8, *(const u32x4*)(s + (row0 + (lane & 31)) * LDK + kk + 8 * (lane >> 5)));
   }
-  // k-major stage [k][ldr]: two LDS transpose reads. In each group of 16 lanes
+  // k-major stage [k][ldr] (chunks swizzled, kmaj_bf16): two LDS transpose
+  // reads. In each group of 16 lanes
   // (rows rb..rb+15 of the fragment, k group kg), address lane a points at
   // row k = k0 + a/4, columns rb + 4(a%4) .. +3; lane i then receives
   // stage[k0 + e][rb + i] for e = 0..3 - four consecutive k of its own row.
   template <int LDR>
   __device__ __forceinline__ static bf16x8 frag_kmaj(const bf16_t* s, int row0, int kk) {
+    static_assert(LDR % 128 == 0, "whole 16-chunk rows for the chunk swizzle");
     const int lane = threadIdx.x & 63, h = lane >> 4, a = lane & 15;
     const int rb = row0 + 16 * (h & 1) + 4 * (a & 3), k0 = kk + 8 * (h >> 1) + (a >> 2);
     typedef short s4 __attribute__((ext_vector_type(4)));
-    const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(s + k0 * LDR + rb));
-    const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(s + (k0 + 4) * LDR + rb));
+    const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(s + kmaj_bf16(k0, rb, LDR)));
+    const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(s + kmaj_bf16(k0 + 4, rb, LDR)));
     const u32x2 l = __builtin_bit_cast(u32x2, lo), u = __builtin_bit_cast(u32x2, hi);
     return __builtin_bit_cast(bf16x8, u32x4{l[0], l[1], u[0], u[1]});
   }
@@ -526,8 +535,9 @@ struct RowLoader {
 
 // k-major operand: element (row, k) = mat[k*ld + col0 + row] for the tile
 // starting at column col0. A k-block is BK rows of ROWS contiguous elements,
-// copied to LDS as they are, [k][ROWS + pad] (the MFMA fragments come out of
-// it through transpose reads). The buffer range ends with row K - 1 of the
+// copied to LDS as they are, [k][ROWS + pad] (bf16: no pad, chunks swizzled
+// by kmaj_bf16; the MFMA fragments come out of it through transpose reads).
+// The buffer range ends with row K - 1 of the
 // matrix, so rows k >= K and anything past the matrix read as zero; columns
 // past the tile's valid ones within the matrix only feed output rows /
 // columns that are never stored. With bias_col >= 0, column bias_col reads 1
@@ -566,7 +576,8 @@ struct KRowLoader {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + NT * s;
-      *(u32x4*)(sm + (v / CPR) * LDR + (v % CPR) * VEC) = r[S][s];
+      if constexpr (sizeof(T) == 2) *(u32x4*)(sm + kmaj_bf16(v / CPR, (v % CPR) * VEC, LDR)) = r[S][s];
+      else *(u32x4*)(sm + (v / CPR) * LDR + (v % CPR) * VEC) = r[S][s];
     }
   }
 };
@@ -1874,7 +1885,7 @@ struct ConvKA {
   __device__ __forceinline__ void store(bf16_t* sm) const {
     u32x4 v = r[S];
     if constexpr (POOL) select_am<bf16_t>(v, am[S], k & 3);
-    *(u32x4*)(sm + k * LDR + (threadIdx.x % CPR) * VEC) = v;
+    *(u32x4*)(sm + kmaj_bf16(k, (threadIdx.x % CPR) * VEC, LDR)) = v;
   }
 };
 
@@ -1916,7 +1927,7 @@ struct ConvKB {
   }
   template <int S>
   __device__ __forceinline__ void store(bf16_t* sm) const {
-    *(u32x4*)(sm + k * LDR + (threadIdx.x % CPR) * VEC) = r[S];
+    *(u32x4*)(sm + kmaj_bf16(k, (threadIdx.x % CPR) * VEC, LDR)) = r[S];
   }
 };
 
