@@ -57,6 +57,11 @@ struct GemmProb {
   void* Wb;
   float* bmaster;
   const int32_t* row_model;   // WGRAD of the concatenated first layers: model of each row m (else null)
+  // LOGITS with softmax-CE fused (N <= the tile width, so a tile holds whole
+  // rows): C/ldc is the gradient dL/dz (storage type) of model `model`, and
+  // the tile's summed row losses go to ce_part[m-tile]. Null: C is the fp32
+  // logits and a separate CE pass follows.
+  float* ce_part;
   // optimizer state (same layouts as W and bmaster; null for plain SGD):
   // momentum buffer or Adam's first moment, and Adam's second moment
   float* s1;
@@ -163,6 +168,7 @@ struct CeProb {
   int64_t ldgt;
   int32_t C;
   int32_t model;
+  int32_t nchunks;            // loss partials of this model (row chunks or GEMM m-tiles)
 };
 
 // ---------------------------------------------------------------------------
@@ -194,8 +200,11 @@ struct SgdTensor {
 // `opt` (device, one OptHp per model) replaces lr/lrv when not null.
 // bwd: the launch holds data- and weight-gradient problems (k-major operands),
 // else forward problems (row-major operands only).
+// labels / lab_stride: the labels of the fused softmax-CE (model m's at
+// labels + m * lab_stride; stride 0 when all models share one row).
 hipError_t launch_gemm(bool bf16, bool bwd, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
-                       const float* lrv, const OptHp* opt, bool keep_grads, hipStream_t s);
+                       const float* lrv, const OptHp* opt, bool keep_grads, const int32_t* labels, int lab_stride,
+                       hipStream_t s);
 hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                            hipStream_t s);
 hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
@@ -210,8 +219,11 @@ hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const 
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
                          const float* lrv, const OptHp* opt, bool keep_grads, hipStream_t s);
 hipError_t launch_set_values(float* dst, const float* vals, int n, hipStream_t s);
-hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, const int32_t* labels, bool per_model_labels, int B,
-                     float* partial, float* losses, hipStream_t s);
+// probs: the first nrows problems need the row pass (their CE is not fused
+// into the logits GEMM); the loss of every one of the nprobs is finished.
+// Partials of model m are at partial + m * pstride.
+hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, int nrows, const int32_t* labels,
+                     bool per_model_labels, int B, float* partial, int pstride, float* losses, hipStream_t s);
 hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int ntiles, float lr,
                       bool use_grad, hipStream_t s);
 // fp32 NCHW batch -> storage type: NHWC X, its transpose XT (rows (h, w, c),

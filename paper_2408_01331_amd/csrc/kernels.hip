@@ -1186,6 +1186,64 @@ __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, 
   }
 }
 
+// Softmax cross-entropy of a logits tile staged in LDS (whole rows: N <= BN),
+// fused into the logits GEMM: CE_LANES lanes per row reduce max and sum with
+// lane shuffles in the same order as ce_rows_kernel, write dL/dz =
+// (softmax - onehot) / B to C, and the row losses of the tile are summed in
+// row order into ce_part[tm].
+template <typename T, int BM, int CLD, int NT>
+__device__ __forceinline__ void fused_softmax_ce(float* sC, const GemmProb& p, int m0, int tm,
+                                                 const int32_t* __restrict__ labels, int lab_stride) {
+  constexpr int RPP = NT / CE_LANES;  // rows per pass
+  static_assert(NT % CE_LANES == 0 && BM % RPP == 0, "whole rows per pass");
+  __shared__ float s_loss[BM];
+  const int sub = threadIdx.x % CE_LANES, C = p.N;
+  const float invB = 1.0f / (float)p.M;
+  const int32_t* y = labels + (int64_t)p.model * lab_stride;
+  for (int r0 = 0; r0 < BM; r0 += RPP) {
+    const int rl = r0 + (int)threadIdx.x / CE_LANES, b = m0 + rl;
+    const bool valid = b < p.M;
+    const float* z = sC + rl * CLD;
+    float mx = -INFINITY;
+    if (valid)
+      for (int c = sub; c < C; c += CE_LANES) mx = fmaxf(mx, z[sc_col(rl, c)]);
+#pragma unroll
+    for (int off = 1; off < CE_LANES; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+    // the exponentials replace the logits in LDS (each lane its own
+    // columns), so the gradient pass does not recompute them
+    float* ze = sC + rl * CLD;
+    float sm = 0.f;
+    float zy = 0.f;
+    const int yb = valid ? y[b] : 0;
+    if (valid) {
+      zy = z[sc_col(rl, yb)];
+      for (int c = sub; c < C; c += CE_LANES) {
+        const float e = expf(z[sc_col(rl, c)] - mx);
+        ze[sc_col(rl, c)] = e;
+        sm += e;
+      }
+    }
+#pragma unroll
+    for (int off = 1; off < CE_LANES; off <<= 1) sm += __shfl_xor(sm, off, 64);
+    if (valid) {
+      if (sub == 0) s_loss[rl] = mx + logf(sm) - zy;
+      const float inv_s = 1.0f / sm;
+      T* g = (T*)p.C + (int64_t)b * p.ldc;
+      for (int c = sub; c < C; c += CE_LANES)
+        g[c] = TT<T>::from_f((ze[sc_col(rl, c)] * inv_s - (c == yb ? 1.f : 0.f)) * invB);
+    } else if (sub == 0) {
+      s_loss[rl] = 0.f;
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int nrows = min(BM, p.M - m0);
+    float t = 0.f;
+    for (int r = 0; r < nrows; ++r) t += s_loss[r];
+    p.ce_part[tm] = t;
+  }
+}
+
 // OPT: the update follows a per-model OptHp (`opt`, not null) instead of
 // fma(-lr, g, w); a separate instantiation, so that plain SGD pays nothing.
 // BWD: the launch's problems are data gradients (A row-major, B k-major) and
@@ -1196,7 +1254,8 @@ __global__ __launch_bounds__((GemmMma<T, BM, BN, BK>::NT)) __attribute__((amdgpu
 void gemm_kernel(const GemmProb* __restrict__ probs,
                                                    const int32_t* __restrict__ tile_map, float lr,
                                                    const float* __restrict__ lrv, const OptHp* __restrict__ opt,
-                                                   int keep_grads) {
+                                                   int keep_grads, const int32_t* __restrict__ labels,
+                                                   int lab_stride) {
   using TL = Tile<T, BM, BN, BK>;
   using SM = Smem<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[SM::BYTES];
@@ -1287,6 +1346,10 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
   __syncthreads();
 
   if (epi != EPI_WGRAD) {
+    if (!BWD && epi == EPI_LOGITS && p.ce_part) {
+      fused_softmax_ce<T, BM, CLD, NT>(sC, p, m0, tm, labels, lab_stride);
+      return;
+    }
     // Row pass: C[m][n] in 16-byte chunks along n (data gradient: with the
     // previous layer's ReLU' from its stored output).
     if (p.C) {
@@ -2026,7 +2089,7 @@ template <typename T>
 __global__ __launch_bounds__(CE_ROWS * CE_LANES) void ce_rows_kernel(const CeProb* __restrict__ probs,
                                                                      const int32_t* __restrict__ labels,
                                                                      int per_model_labels, int B,
-                                                                     float* __restrict__ partial, int nchunks) {
+                                                                     float* __restrict__ partial, int pstride) {
   __shared__ float rowloss[CE_ROWS];
   const CeProb& p = probs[blockIdx.y];
   const int32_t* y = labels + (per_model_labels ? (int64_t)p.model * B : 0);
@@ -2062,18 +2125,20 @@ __global__ __launch_bounds__(CE_ROWS * CE_LANES) void ce_rows_kernel(const CePro
     const int nrows = min(CE_ROWS, B - (int)blockIdx.x * CE_ROWS);
     float t = 0.f;
     for (int r = 0; r < nrows; ++r) t += rowloss[r];
-    partial[(int64_t)p.model * nchunks + blockIdx.x] = t;
+    partial[(int64_t)p.model * pstride + blockIdx.x] = t;
   }
 }
 
-// One lane per problem of the list (the active models), writing that model's slot.
-__global__ void ce_finish_kernel(const CeProb* __restrict__ probs, const float* __restrict__ partial, int nchunks,
+// One lane per problem of the list (the active models), writing that model's
+// slot: its partials (row chunks, or the m-tiles of its fused logits GEMM)
+// added in order.
+__global__ void ce_finish_kernel(const CeProb* __restrict__ probs, const float* __restrict__ partial, int pstride,
                                  int nprobs, int B, float* __restrict__ losses) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= nprobs) return;
-  const int m = probs[i].model;
+  const int m = probs[i].model, n = probs[i].nchunks;
   float s = 0.f;
-  for (int k = 0; k < nchunks; ++k) s += partial[(int64_t)m * nchunks + k];
+  for (int k = 0; k < n; ++k) s += partial[(int64_t)m * pstride + k];
   losses[m] = s * (1.0f / (float)B);
 }
 
@@ -2148,10 +2213,12 @@ __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, 
 // Launch wrappers
 // ---------------------------------------------------------------------------
 hipError_t launch_gemm(bool bf16, bool bwd, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
-                       const float* lrv, const OptHp* opt, bool keep_grads, hipStream_t s) {
+                       const float* lrv, const OptHp* opt, bool keep_grads, const int32_t* labels, int lab_stride,
+                       hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   auto go = [&](auto kern, int nt) {
-    hipLaunchKernelGGL(kern, dim3(ntiles), dim3(nt), 0, s, probs, tile_map, lr, lrv, opt, (int)keep_grads);
+    hipLaunchKernelGGL(kern, dim3(ntiles), dim3(nt), 0, s, probs, tile_map, lr, lrv, opt, (int)keep_grads, labels,
+                       lab_stride);
   };
   if (bf16) {
     constexpr int NT = GemmMma<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16>::NT;
@@ -2282,17 +2349,19 @@ hipError_t launch_set_values(float* dst, const float* vals, int n, hipStream_t s
   return hipGetLastError();
 }
 
-hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, const int32_t* labels, bool per_model_labels, int B,
-                     float* partial, float* losses, hipStream_t s) {
+hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, int nrows, const int32_t* labels,
+                     bool per_model_labels, int B, float* partial, int pstride, float* losses, hipStream_t s) {
   if (nprobs <= 0) return hipSuccess;
   const int nchunks = (B + CE_ROWS - 1) / CE_ROWS;
-  if (bf16)
-    hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nprobs), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels,
-                       (int)per_model_labels, B, partial, nchunks);
-  else
-    hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nprobs), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels,
-                       (int)per_model_labels, B, partial, nchunks);
-  hipLaunchKernelGGL(ce_finish_kernel, dim3((nprobs + 63) / 64), dim3(64), 0, s, probs, partial, nchunks, nprobs,
+  if (nrows > 0) {
+    if (bf16)
+      hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nrows), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels,
+                         (int)per_model_labels, B, partial, pstride);
+    else
+      hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nrows), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels,
+                         (int)per_model_labels, B, partial, pstride);
+  }
+  hipLaunchKernelGGL(ce_finish_kernel, dim3((nprobs + 63) / 64), dim3(64), 0, s, probs, partial, pstride, nprobs,
                      B, losses);
   return hipGetLastError();
 }

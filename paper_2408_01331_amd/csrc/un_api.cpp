@@ -78,7 +78,7 @@ struct Launch {
   int kclass;
   size_t probs, map;  // arena offsets
   int count;
-  int mode = 0;       // conv weight gradient: code variant (launch_conv_wgrad)
+  int mode = 0;       // conv weight gradient: code variant (launch_conv_wgrad); CE: problems needing the row pass
   size_t lds = 0;     // halo conv: dynamic LDS bytes
 };
 
@@ -478,6 +478,10 @@ static void build_tables(un_ctx* c, Tables& T) {
 
   const int GBM = bf ? GEMM_BM_BF16 : GEMM_BM_F32, GBN = bf ? GEMM_BN_BF16 : GEMM_BN_F32;
   const int CBM = bf ? CONV_BM_BF16 : CONV_BM_F32, CBN = bf ? CONV_BN_BF16 : CONV_BN_F32;
+  // softmax-CE is fused into a model's logits GEMM when a tile holds whole
+  // rows of logits; the loss partials of model m start at m * ce_pstride
+  const int ce_pstride = cdiv(B, CE_ROWS);
+  auto ce_fused = [&](const Block& b) { return b.kind == 0 && b.N <= GBN; };
 
   // Problems of one launch are ordered longest-K first (their tiles are the
   // longest-running), so the ragged tail of a level is made of short tiles.
@@ -531,7 +535,7 @@ static void build_tables(un_ctx* c, Tables& T) {
       size_t b0 = po + k * sizeof(GemmProb);
       for (size_t f : {offsetof(GemmProb, A), offsetof(GemmProb, B), offsetof(GemmProb, C), offsetof(GemmProb, bias),
                        offsetof(GemmProb, mask), offsetof(GemmProb, dbias), offsetof(GemmProb, W), offsetof(GemmProb, Wb),
-                       offsetof(GemmProb, bmaster), offsetof(GemmProb, row_model)})
+                       offsetof(GemmProb, bmaster), offsetof(GemmProb, row_model), offsetof(GemmProb, ce_part)})
         fix.push_back(b0 + f);
     }
     size_t mo = put(map.data(), map.size() * 4);
@@ -669,6 +673,13 @@ static void build_tables(un_ctx* c, Tables& T) {
         p.C = ptr(b.Y);
         p.ldc = b.ldy;
         p.bias = (const float*)ptr(b.b32);
+        if (b.last && ce_fused(b)) {
+          // softmax-CE in the logits GEMM's epilogue: it writes dL/dz
+          p.C = ptr(b.G);
+          p.ldc = b.ldg;
+          p.model = b.model;
+          p.ce_part = (float*)ptr(sub(c->ce_partial, (int64_t)b.model * ce_pstride * 4));
+        }
         gp.push_back(p);
       } else {
         ConvProb p = conv_base(b);
@@ -689,20 +700,26 @@ static void build_tables(un_ctx* c, Tables& T) {
     emit_conv(cp, fwd, 1, UN_K_CONV_FWD);
   }
 
-  // softmax-CE
+  // softmax-CE: the row pass for the models whose CE is not fused (listed
+  // first), the loss sum for all
   std::vector<CeProb> ces;
-  for (size_t mi = 0; mi < c->models.size(); ++mi) {
-    if (!c->active[mi]) continue;
-    Block& b = c->models[mi].blocks.back();
-    CeProb p{};
-    p.logits = (const float*)ptr(b.Y);
-    p.ldl = b.ldy;
-    p.G = ptr(b.G);
-    p.ldg = b.ldg;
-    p.C = b.N;
-    p.model = (int)mi;
-    ces.push_back(p);
-  }
+  int ce_rows = 0;
+  for (int pass = 0; pass < 2; ++pass)
+    for (size_t mi = 0; mi < c->models.size(); ++mi) {
+      if (!c->active[mi]) continue;
+      Block& b = c->models[mi].blocks.back();
+      if (ce_fused(b) != (pass == 1)) continue;
+      CeProb p{};
+      p.logits = (const float*)ptr(b.Y);
+      p.ldl = b.ldy;
+      p.G = ptr(b.G);
+      p.ldg = b.ldg;
+      p.C = b.N;
+      p.model = (int)mi;
+      p.nchunks = pass == 1 ? cdiv(B, GBM) : ce_pstride;
+      ces.push_back(p);
+      if (pass == 0) ++ce_rows;
+    }
   {
     size_t po = put(ces.data(), ces.size() * sizeof(CeProb));
     for (size_t k = 0; k < ces.size(); ++k) {
@@ -710,6 +727,7 @@ static void build_tables(un_ctx* c, Tables& T) {
       for (size_t f : {offsetof(CeProb, logits), offsetof(CeProb, G), offsetof(CeProb, GT)}) fix.push_back(b0 + f);
     }
     T.ce = Launch{5, UN_K_CE, po, NONE, (int)ces.size()};
+    T.ce.mode = ce_rows;
   }
 
   // Backward launches, one per level lv from the deepest: the Linear data
@@ -1301,7 +1319,7 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
   switch (l.kind) {
     case 0:
       e = launch_gemm(c->bf16, l.kclass == UN_K_GEMM_BWD, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, lr,
-                      c->lrv, c->optp, c->keep_grads,
+                      c->lrv, c->optp, c->keep_grads, c->at<int32_t>(c->ydev), c->labels_per_model ? c->B : 0,
                       c->stream);
       break;
     case 1:
@@ -1323,8 +1341,8 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
                         c->stream);
       break;
     case 5:
-      e = launch_ce(c->bf16, c->at<CeProb>(l.probs), l.count, c->at<int32_t>(c->ydev), c->labels_per_model, c->B,
-                    c->at<float>(c->ce_partial), c->at<float>(c->losses_dev), c->stream);
+      e = launch_ce(c->bf16, c->at<CeProb>(l.probs), l.count, l.mode, c->at<int32_t>(c->ydev), c->labels_per_model,
+                    c->B, c->at<float>(c->ce_partial), cdiv(c->B, CE_ROWS), c->at<float>(c->losses_dev), c->stream);
       break;
     case 6:
       e = launch_sgd(c->bf16, c->at<SgdTensor>(l.probs), c->at<int32_t>(l.map), l.count, lr, true, c->stream);
