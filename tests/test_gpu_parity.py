@@ -85,6 +85,26 @@ def test_ragged_mlps(precision):
 
 
 @pytest.mark.parametrize("precision", ["f32", "bf16"])
+def test_softmax_ce_fused_and_row_pass(precision):
+    """Class counts on both sides of one GEMM tile's width (bf16 128, fp32 64):
+    the models whose classes fit get softmax-CE in their logits GEMM's
+    epilogue, the others the separate row pass, all in the same step."""
+    _need_gpu()
+    specs = [
+        {"layers": [("linear", 40), ("relu",), ("linear", 10)], "num_classes": 10},
+        {"layers": [("linear", 150)], "num_classes": 150},
+        {"layers": [("linear", 33), ("relu",), ("linear", 70)], "num_classes": 70},
+        {"layers": [("linear", 128)], "num_classes": 128},
+        {"layers": [("linear", 64)], "num_classes": 64},
+        {"layers": [("linear", 129)], "num_classes": 129},
+    ]
+    wl = _custom(specs, 45, (72,), precision)      # labels < 10, the first model's classes
+    m = range(wl.n_models)
+    _report(f"ce_paths_{precision} 1 step", compare_step(wl, run_gpu(wl, 1), run_oracle(wl, 1, m), m))
+    _report(f"ce_paths_{precision} run", compare_run(wl, run_gpu(wl, wl.steps), run_oracle(wl, wl.steps, m), m))
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
 def test_ragged_cnns(precision):
     _need_gpu()
     specs = [
