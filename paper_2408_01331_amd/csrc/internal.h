@@ -106,8 +106,6 @@ struct ConvProb {
   const float* bias;          // fwd
   void* P;                    // fwd output (pooled or not), [pixel][O]
   uint8_t* amax;              // fwd: window argmax as the one-hot byte 1 << (dy*2 + dx), [w][O]
-  void* PT;                   // fwd: transposed output [(s*O + o)][n] for a Linear consumer, or null
-  int64_t ldpt;
   const void* G;              // dgrad/wgrad: gradient at this block's output, [pixel][O]
   const uint8_t* gam;         // its argmax (pool only)
   void* Gprev;                // dgrad output [n*H*W + y*W + x][C]
@@ -116,8 +114,9 @@ struct ConvProb {
 };
 
 // Split-K reduction of conv weight-gradient partials, in split order, with
-// the SGD update fused: W[o][j] <- fma(-lr, dW, W), its bf16 shadow and its
-// transposed copy WT[c][tap*O + o] (j = tap*C + c), and the bias from column J.
+// the SGD update fused: W[o][j] <- fma(-lr, dW, W), its bf16 copy and its
+// transposed copy WT[c][tap*O + o] (j = tap*C + c) that the conv data gradient
+// reads, and the bias from column J.
 // dW / db are also stored when gradients are kept (gW / gb non-null).
 struct ReduceProb {
   const float* ws;
@@ -156,7 +155,7 @@ constexpr int OPT_FLOATS = 8;
 
 // ---------------------------------------------------------------------------
 // Softmax cross-entropy of one model: logits [B][ldl] fp32 -> per-model mean
-// loss, and dz = (softmax - onehot)/B stored as G [B][ldg] and GT [C][ldgt].
+// loss, and dz = (softmax - onehot)/B stored as G [B][ldg].
 // Row losses are summed per 32-row chunk, then per model, in a fixed order.
 // ---------------------------------------------------------------------------
 struct CeProb {
@@ -164,8 +163,6 @@ struct CeProb {
   int64_t ldl;
   void* G;
   int64_t ldg;
-  void* GT;
-  int64_t ldgt;
   int32_t C;
   int32_t model;
   int32_t nchunks;            // loss partials of this model (row chunks or GEMM m-tiles)
@@ -174,9 +171,10 @@ struct CeProb {
 // ---------------------------------------------------------------------------
 // Multi-tensor SGD over 64x64 tiles of every parameter tensor:
 //   W <- fma(-lr, G, W)  (fp32 master), then the copies the GEMMs read:
-//   Wb  [r][ldw]          bf16 shadow in the same layout (bf16 mode), and
-//   WT  [c][j*R + r]      the transposed copy the dgrad reads (T), where the
-//                         tensor is viewed as [R][J][Cc] (J = kernel taps).
+//   Wb  [r][ldw]          bf16 copy in the same layout (bf16 mode), and
+//   WT  [c][j*R + r]      a conv block's transposed copy that its data
+//                         gradient reads (T), where the tensor is viewed as
+//                         [R][J][Cc] (J = kernel taps).
 // With use_grad false only the copies are refreshed (after set/init).
 // ---------------------------------------------------------------------------
 struct SgdTensor {
@@ -226,11 +224,10 @@ hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, int nrows, cons
                      bool per_model_labels, int B, float* partial, int pstride, float* losses, hipStream_t s);
 hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int ntiles, float lr,
                       bool use_grad, hipStream_t s);
-// fp32 NCHW batch -> storage type: NHWC X, its transpose XT (rows (h, w, c),
-// columns b; optional) and NHWC XC with Cs >= C channels (optional; the
-// channels from C on are left untouched).
-hipError_t launch_load(bool bf16, const float* x, int B, int C, int H, int W, void* X, void* XT,
-                       int64_t ldxt, void* XC, int Cs, hipStream_t s);
+// fp32 NCHW batch -> storage type: NHWC X (optional) and NHWC XC with
+// Cs >= C channels (optional; the channels from C on are left untouched).
+hipError_t launch_load(bool bf16, const float* x, int B, int C, int H, int W, void* X, void* XC, int Cs,
+                       hipStream_t s);
 
 // Tile shapes the planner must agree with.
 constexpr int GEMM_BM_BF16 = 128, GEMM_BN_BF16 = 128;

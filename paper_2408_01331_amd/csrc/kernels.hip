@@ -1142,9 +1142,9 @@ __device__ __forceinline__ void opt_update4(const OptHp& h, const f32x4& g, f32x
 }
 
 // Column of element (r, c) in the GEMM epilogue's LDS tile: c XOR a multiple
-// of 8 that changes every 8 rows. Groups of 8 (float4 pairs) stay contiguous,
-// and a column read down 8-row groups spreads over the banks, so the
-// transposed copy can be stored with consecutive lanes along one output row.
+// of 8 that changes every 8 rows. Groups of 8 (float4 pairs) stay contiguous
+// for the row passes' float4 reads, and the accumulator writes of a wave
+// spread over the banks.
 __device__ __forceinline__ int sc_col(int r, int c) { return c ^ (((r >> 3) & 7) << 3); }
 
 // VE consecutive values (one 16-byte vector) as floats.
@@ -1429,9 +1429,8 @@ struct ConvEpiSmem {
 
 // Conv forward epilogue: bias, ReLU, 2x2 max-pool in registers (pool rows
 // are window-ordered, so a lane's four accumulator rows are one window), then
-// the pooled value, its one-hot argmax and the optional transposed copy,
-// stored straight from registers (staging this small output in LDS measured
-// slower).
+// the pooled value and its one-hot argmax, stored straight from registers
+// (staging this small output in LDS measured slower).
 template <typename T, int BM, int BN, int BK, int NW = 4>
 __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int n0,
                                                   const f32x4 (&acc)[Tile<T, BM, BN, BK, NW>::FM][Tile<T, BM, BN, BK, NW>::FN],
@@ -1468,21 +1467,12 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
         const int w = mb >> 2;
         store_t<T>(p.P, (int64_t)w * O + o, mx);
         p.amax[(int64_t)w * O + o] = (uint8_t)(1u << am);
-        if (p.PT) {
-          const int pp = p.PH * p.PW, n = w / pp, s = w - n * pp;
-          store_t<T>(p.PT, (int64_t)(s * O + o) * p.ldpt + n, mx);
-        }
       } else {
-        const int nv = min(4, p.M - mb), pp = p.OH * p.OW;
+        const int nv = min(4, p.M - mb);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           if (r >= nv) break;
-          const int m = mb + r;
-          store_t<T>(p.P, (int64_t)m * O + o, v[r]);
-          if (p.PT) {
-            const int n = m / pp, s = m - n * pp;
-            store_t<T>(p.PT, (int64_t)(s * O + o) * p.ldpt + n, v[r]);
-          }
+          store_t<T>(p.P, (int64_t)(mb + r) * O + o, v[r]);
         }
       }
     }
@@ -2082,7 +2072,7 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 // CE_LANES lanes per sample row (CE_ROWS rows per block, blockIdx.y = model),
 // classes strided over the row's lanes; max and sum over the row by a fixed
-// butterfly of lane shuffles. dz = (softmax - onehot)/B goes to G and GT. Each
+// butterfly of lane shuffles. dz = (softmax - onehot)/B goes to G. Each
 // block sums its rows' losses in row order into partial[model][chunk];
 // ce_finish_kernel adds the chunks in order.
 template <typename T>
@@ -2114,8 +2104,7 @@ __global__ __launch_bounds__(CE_ROWS * CE_LANES) void ce_rows_kernel(const CePro
     const float inv_s = 1.0f / s, invB = 1.0f / (float)B;
     for (int c = sub; c < C; c += CE_LANES) {
       const T g = TT<T>::from_f((expf(z[c] - mx) * inv_s - (c == yb ? 1.f : 0.f)) * invB);
-      if (p.G) ((T*)p.G)[(int64_t)b * p.ldg + c] = g;
-      if (p.GT) ((T*)p.GT)[(int64_t)c * p.ldgt + b] = g;
+      ((T*)p.G)[(int64_t)b * p.ldg + c] = g;
     }
   } else if (sub == 0) {
     rowloss[rl] = 0.f;
@@ -2189,13 +2178,11 @@ __global__ __launch_bounds__(256) void sgd_kernel(const SgdTensor* __restrict__ 
 }
 
 // ---------------------------------------------------------------------------
-// Batch load: fp32 NCHW -> storage-type NHWC (+ transposed [(h*W+w)*C + c][b],
-// + NHWC with Cs stored channels).
+// Batch load: fp32 NCHW -> storage-type NHWC (+ NHWC with Cs stored channels).
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, int B, int C, int H, int W,
-                                                   T* __restrict__ X, T* __restrict__ XT, int64_t ldxt,
-                                                   T* __restrict__ XC, int Cs) {
+                                                   T* __restrict__ X, T* __restrict__ XC, int Cs) {
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int64_t total = (int64_t)B * C * H * W;
   if (e >= total) return;
@@ -2205,7 +2192,6 @@ __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, 
   const int c = rem / hw, s = rem - c * hw;
   const T v = TT<T>::from_f(x[e]);
   if (X) X[(b * hw + s) * C + c] = v;
-  if (XT) XT[(int64_t)(s * C + c) * ldxt + b] = v;
   if (XC) XC[(b * hw + s) * Cs + c] = v;
 }
 
@@ -2376,17 +2362,16 @@ hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor,
   return hipGetLastError();
 }
 
-hipError_t launch_load(bool bf16, const float* x, int B, int C, int H, int W, void* X, void* XT, int64_t ldxt,
+hipError_t launch_load(bool bf16, const float* x, int B, int C, int H, int W, void* X,
                        void* XC, int Cs, hipStream_t s) {
   const int64_t total = (int64_t)B * C * H * W;
   const int blocks = (int)((total + 255) / 256);
   if (blocks <= 0) return hipSuccess;
   if (bf16)
-    hipLaunchKernelGGL(load_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, x, B, C, H, W, (bf16_t*)X, (bf16_t*)XT,
-                       ldxt, (bf16_t*)XC, Cs);
+    hipLaunchKernelGGL(load_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, x, B, C, H, W, (bf16_t*)X, (bf16_t*)XC,
+                       Cs);
   else
-    hipLaunchKernelGGL(load_kernel<float>, dim3(blocks), dim3(256), 0, s, x, B, C, H, W, (float*)X, (float*)XT,
-                       ldxt, (float*)XC, Cs);
+    hipLaunchKernelGGL(load_kernel<float>, dim3(blocks), dim3(256), 0, s, x, B, C, H, W, (float*)X, (float*)XC, Cs);
   return hipGetLastError();
 }
 

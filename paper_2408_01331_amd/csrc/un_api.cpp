@@ -123,8 +123,8 @@ struct un_ctx {
   int in_cs = 0;       // stored channels of XinC
   int64_t ldxin = 0;
   // schedule
-  std::vector<Launch> fwd, bwd[2];  // bwd[p]: dgrad reads copy p of the transposed weights
-  Launch ce{}, refresh[2]{};
+  std::vector<Launch> fwd, bwd;
+  Launch ce{}, refresh{};
   std::vector<char> active;          // models in the step (un_set_active)
   size_t tables_off = NONE, tables_cap = 0;  // arena region of the descriptor tables
   // planning results the tables are built from
@@ -136,7 +136,6 @@ struct un_ctx {
     size_t cat_row_model = NONE;  // int32 per concatenated row: the model owning it
     size_t catS1 = NONE, catS1b = NONE, catS2 = NONE, catS2b = NONE;  // state of the concatenation (sbase)
   } plan;
-  int wt_cur = 0;                     // which transposed copy the next dgrad reads
   bool keep_grads = false, grads_valid = false;
   int ce_count = 0;
   bool loaded = false, stepped = false, poisoned = false;
@@ -433,8 +432,8 @@ static void plan_halo(ConvProb& p, bool bf, bool dgrad) {
 struct Tables {
   std::vector<char> host;    // tables as uploaded (pointers encoded as arena offset + 1)
   std::vector<size_t> fix;   // byte offsets of the encoded pointer fields
-  std::vector<Launch> fwd, bwd[2];
-  Launch ce{}, refresh[2]{};
+  std::vector<Launch> fwd, bwd;
+  Launch ce{}, refresh{};
 };
 
 static void build_tables(un_ctx* c, Tables& T) {
@@ -462,7 +461,7 @@ static void build_tables(un_ctx* c, Tables& T) {
   std::vector<char>& host_tables = T.host;
   std::vector<size_t>& fix = T.fix;  // byte offsets (in host_tables) of pointer fields to relocate
   std::vector<Launch>& fwd = T.fwd;
-  std::vector<Launch>* bwd = T.bwd;
+  std::vector<Launch>& bwd = T.bwd;
   auto put = [&](const void* src, size_t n) -> size_t {
     size_t off = rup((int64_t)host_tables.size(), 256);
     host_tables.resize(off + n);
@@ -574,7 +573,7 @@ static void build_tables(un_ctx* c, Tables& T) {
     for (size_t k = 0; k < ps.size(); ++k) {
       size_t b0 = po + k * sizeof(ConvProb);
       for (size_t f : {offsetof(ConvProb, X), offsetof(ConvProb, Wt), offsetof(ConvProb, bias), offsetof(ConvProb, P),
-                       offsetof(ConvProb, amax), offsetof(ConvProb, PT), offsetof(ConvProb, G), offsetof(ConvProb, gam),
+                       offsetof(ConvProb, amax), offsetof(ConvProb, G), offsetof(ConvProb, gam),
                        offsetof(ConvProb, Gprev), offsetof(ConvProb, ws)})
         fix.push_back(b0 + f);
     }
@@ -724,7 +723,7 @@ static void build_tables(un_ctx* c, Tables& T) {
     size_t po = put(ces.data(), ces.size() * sizeof(CeProb));
     for (size_t k = 0; k < ces.size(); ++k) {
       size_t b0 = po + k * sizeof(CeProb);
-      for (size_t f : {offsetof(CeProb, logits), offsetof(CeProb, G), offsetof(CeProb, GT)}) fix.push_back(b0 + f);
+      for (size_t f : {offsetof(CeProb, logits), offsetof(CeProb, G)}) fix.push_back(b0 + f);
     }
     T.ce = Launch{5, UN_K_CE, po, NONE, (int)ces.size()};
     T.ce.mode = ce_rows;
@@ -880,9 +879,9 @@ static void build_tables(un_ctx* c, Tables& T) {
         rp.push_back(r);
       }
     }
-    emit_gemm(gp, bwd[0], UN_K_GEMM_BWD);
-    emit_conv(dp, bwd[0], 2, UN_K_CONV_DGRAD);
-    emit_conv(wp, bwd[0], 3, UN_K_CONV_WGRAD);
+    emit_gemm(gp, bwd, UN_K_GEMM_BWD);
+    emit_conv(dp, bwd, 2, UN_K_CONV_DGRAD);
+    emit_conv(wp, bwd, 3, UN_K_CONV_WGRAD);
     if (!rp.empty()) {
       std::vector<int32_t> map;
       for (size_t k = 0; k < rp.size(); ++k) {
@@ -899,15 +898,13 @@ static void build_tables(un_ctx* c, Tables& T) {
           fix.push_back(b0 + f);
       }
       size_t mo = put(map.data(), map.size() * 4);
-      bwd[0].push_back(Launch{4, UN_K_OTHER, po, mo, (int)map.size()});
+      bwd.push_back(Launch{4, UN_K_OTHER, po, mo, (int)map.size()});
     }
   }
-  // (the two step parities now share one backward schedule)
-  bwd[1] = bwd[0];
-
-  // Shadow refresh (after un_set_params / initialisation): rewrite the bf16
-  // shadow and transposed copy `pass` of every weight from the fp32 master.
-  for (int pass = 0; pass < 2; ++pass) {
+  // Copy refresh (after un_set_params / initialisation / a set change):
+  // rewrite the bf16 copy (and a conv block's transposed copy) of every weight
+  // from the fp32 master.
+  {
     std::vector<SgdTensor> ts;
     std::vector<int32_t> map;
     auto add = [&](SgdTensor t) {
@@ -944,7 +941,7 @@ static void build_tables(un_ctx* c, Tables& T) {
         fix.push_back(b0 + f);
     }
     size_t mo = put(map.data(), map.size() * 4);
-    T.refresh[pass] = Launch{6, UN_K_SGD, po, mo, (int)map.size()};
+    T.refresh = Launch{6, UN_K_SGD, po, mo, (int)map.size()};
   }
 
 }
@@ -966,19 +963,15 @@ static un_status install_tables(un_ctx* c, Tables& T) {
     if (l.map != NONE) l.map += c->tables_off;
   };
   for (auto& l : T.fwd) relocate(l);
-  for (int p = 0; p < 2; ++p)
-    for (auto& l : T.bwd[p]) relocate(l);
+  for (auto& l : T.bwd) relocate(l);
   relocate(T.ce);
-  relocate(T.refresh[0]);
-  relocate(T.refresh[1]);
+  relocate(T.refresh);
   HIPCHK(c, hipMemcpyAsync(c->base + c->tables_off, T.host.data(), T.host.size(), hipMemcpyHostToDevice, c->stream));
   HIPCHK(c, hipStreamSynchronize(c->stream));
   c->fwd = T.fwd;
-  c->bwd[0] = T.bwd[0];
-  c->bwd[1] = T.bwd[1];
+  c->bwd = T.bwd;
   c->ce = T.ce;
-  c->refresh[0] = T.refresh[0];
-  c->refresh[1] = T.refresh[1];
+  c->refresh = T.refresh;
   return UN_OK;
 }
 
@@ -1230,8 +1223,8 @@ static void from_internal(const Block& b, const std::vector<float>& w, const std
   }
 }
 
-static un_status refresh_shadows(un_ctx* c) {
-  const Launch& l = c->refresh[c->wt_cur];
+static un_status refresh_copies(un_ctx* c) {
+  const Launch& l = c->refresh;
   HIPCHK(c, launch_sgd(c->bf16, c->at<SgdTensor>(l.probs), c->at<int32_t>(l.map), l.count, 0.f, false, c->stream));
   return UN_OK;
 }
@@ -1462,7 +1455,7 @@ un_status un_create(const un_model_spec* specs, int32_t n_models, const un_input
     s = write_params(c, i, pt.data());
     if (s != UN_OK) break;
   }
-  if (s == UN_OK) s = refresh_shadows(c);
+  if (s == UN_OK) s = refresh_copies(c);
   if (s == UN_OK && hipStreamSynchronize(c->stream) != hipSuccess) s = UN_ERR_DEVICE;
   if (s != UN_OK) {
     std::string msg = c->err;
@@ -1492,7 +1485,6 @@ static un_status load_common(un_ctx* c, const float* x, const int32_t* y, bool d
   }
   HIPCHK(c, hipMemcpyAsync(c->base + c->ydev, yh.data(), (size_t)c->B * 4, hipMemcpyHostToDevice, c->stream));
   HIPCHK(c, launch_load(c->bf16, xsrc, c->B, c->in_c, c->in_h, c->in_w, c->Xin == NONE ? nullptr : c->base + c->Xin,
-                        nullptr, 0,
                         c->XinC == NONE ? nullptr : c->base + c->XinC, c->in_cs, c->stream));
   HIPCHK(c, hipStreamSynchronize(c->stream));
   c->loaded = true;
@@ -1554,10 +1546,9 @@ static un_status step_common(un_ctx* c, float lr, const float* lrs, float* losse
   }
   for (auto& l : c->fwd) HIPCHK(c, run_launch(c, l, lr));
   HIPCHK(c, run_launch(c, c->ce, lr));
-  for (auto& l : c->bwd[c->wt_cur]) HIPCHK(c, run_launch(c, l, lr));
+  for (auto& l : c->bwd) HIPCHK(c, run_launch(c, l, lr));
   for (size_t i = 0; i < n; ++i)
     if (c->active[i]) ++c->opts[i].t;
-  c->wt_cur ^= 1;
   c->stepped = true;
   c->grads_valid = c->keep_grads;
   if (c->profiling && c->recs.size() > 4096) {
@@ -1753,7 +1744,7 @@ un_status un_set_active(un_ctx* c, const uint8_t* mask) {
   }
   // Models that sat out some steps kept their transposed weight copy in the
   // buffer of that time; rewrite every model's current copies from the master.
-  st = refresh_shadows(c);
+  st = refresh_copies(c);
   if (st != UN_OK) return st;
   HIPCHK(c, hipStreamSynchronize(c->stream));
   c->grads_valid = false;
@@ -1798,7 +1789,7 @@ un_status un_set_params(un_ctx* c, int32_t i, const float* src, size_t n) {
   HIPCHK(c, hipStreamSynchronize(c->stream));
   un_status s = write_params(c, i, src);
   if (s != UN_OK) return s;
-  s = refresh_shadows(c);
+  s = refresh_copies(c);
   if (s != UN_OK) return s;
   HIPCHK(c, hipStreamSynchronize(c->stream));
   return UN_OK;
