@@ -1826,8 +1826,9 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
   else conv_fwd_epilogue<T, BM, BN, BK, NW>(p, m0, n0, acc, smem);
 }
 
-// Halo-tiled conv pass; each problem's tile shape (p.bn) is the wide BM x BN
-// or the narrow 2BM x BN/2 one, so a launch mixes both. LDS is dynamic, sized
+// Halo-tiled conv pass; each problem's tile shape (p.bm x p.bn) is the wide
+// BM x BN, the narrow 2BM x BN/2 or (bf16 forward only) the tall 4BM x BN/2 one,
+// so a launch mixes them. LDS is dynamic, sized
 // by the host for the launch's largest staged block (small halos leave room
 // for more workgroups per CU).
 // Waves of a halo workgroup (bf16; fp32 keeps 4): a 4-wave workgroup runs
@@ -1843,8 +1844,13 @@ void conv_halo_kernel(const ConvProb* __restrict__ probs, const int32_t* __restr
   if (prob < 0) return;  // padding of the XCD-ordered tile list
   const ConvProb& p = probs[prob];
   constexpr int NW = halo_waves<T>();
-  if (p.bn == BN) halo_tile<T, BM, BN, BK, DGRAD, NW>(p, local, smem);
-  else halo_tile<T, 2 * BM, BN / 2, BK, DGRAD, NW>(p, local, smem);
+  if (p.bn == BN) {
+    halo_tile<T, BM, BN, BK, DGRAD, NW>(p, local, smem);
+  } else if (DGRAD || sizeof(T) != 2 || p.bm == 2 * BM) {
+    halo_tile<T, 2 * BM, BN / 2, BK, DGRAD, NW>(p, local, smem);
+  } else {
+    if constexpr (!DGRAD && sizeof(T) == 2) halo_tile<T, 4 * BM, BN / 2, BK, DGRAD, NW>(p, local, smem);
+  }
 }
 
 template <typename T, int BM, int BN, int BK, int MODE>

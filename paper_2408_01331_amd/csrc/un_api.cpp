@@ -421,7 +421,11 @@ static bool try_halo(ConvProb& p, bool bf, bool dgrad, int BM, int BN) {
 static void plan_halo(ConvProb& p, bool bf, bool dgrad) {
   const int BM = bf ? CONV_BM_BF16 : CONV_BM_F32, BN = bf ? CONV_BN_BF16 : CONV_BN_F32;
   p.halo = 0;
-  // at most BN/2 output columns: the narrow tile wastes no half of each product
+  // at most BN/2 output columns: the narrow tile wastes no half of each
+  // product; a large bf16 forward pass takes the tall one (4BM rows), which
+  // halves the workgroups whose fixed costs dominate a short K (a first conv
+  // has K = 9 * 8)
+  if (bf && !dgrad && p.N <= BN / 2 && p.M >= 64 * 4 * BM && try_halo(p, bf, dgrad, 4 * BM, BN / 2)) return;
   if (p.N <= BN / 2 && try_halo(p, bf, dgrad, 2 * BM, BN / 2)) return;
   try_halo(p, bf, dgrad, BM, BN);
 }
