@@ -235,6 +235,9 @@ constexpr int GEMM_BM_F32 = 64, GEMM_BN_F32 = 64;
 constexpr int GEMM_BK_BF16 = 64, GEMM_BK_F32 = 32;
 constexpr int CONV_BM_BF16 = 128, CONV_BN_BF16 = 128, CONV_BK_BF16 = 64;
 constexpr int CONV_BM_F32 = 64, CONV_BN_F32 = 64, CONV_BK_F32 = 32;
+// bf16 conv weight gradients whose blocks all have at most this many output
+// channels run 64-row tiles (launch mode bit WG_NARROW_BIT)
+constexpr int CONV_WG_NARROW_BM = 64, WG_NARROW_BIT = 4;
 constexpr int SGD_TILE = 64;
 constexpr int REDUCE_BLOCK = 256;
 constexpr int CE_MAX_BATCH = 1 << 20;

@@ -32,16 +32,20 @@
 #ifndef UN_GEMM_WGN
 #define UN_GEMM_WGN 4
 #endif
-// k-major LDS stages (BK rows of R elements). bf16: no padding, and the
-// 16-byte chunk c of row k is stored at chunk c ^ 4*(k % 4) (kmaj_bf16): a
-// half-wave of transpose reads takes 64 bytes from each of four consecutive
-// rows, which this places in four disjoint 64-byte bank windows. With padded
-// rows instead (stride of 8 banks) the same reads measured twice the LDS
-// cycles (SQ_LDS_BANK_CONFLICT half of SQ_LDS_IDX_ACTIVE). fp32: rows padded
-// by 8 elements.
+// k-major LDS stages (BK rows of R elements). bf16: no padding; a half-wave
+// of transpose reads takes 64 bytes (4 chunks of 16) from each of four
+// consecutive rows, and kmaj_bf16 swizzles the 16-byte chunks so that those
+// land in four disjoint 64-byte bank windows: rows of >= 128 elements store
+// chunk c of row k at c ^ 4*(k % 4); 64-element rows (two rows per 256 bytes
+// of banks) at c ^ 4*((k / 2) % 2). With padded rows instead (stride of 8
+// banks) the same reads measured twice the LDS cycles (SQ_LDS_BANK_CONFLICT
+// half of SQ_LDS_IDX_ACTIVE). fp32: rows padded by 8 elements.
 constexpr int KMAJ_PAD_BF16 = 0, KMAJ_PAD_F32 = 8;
-__device__ __forceinline__ int kmaj_bf16(int k, int col, int ldr) {
-  return k * ldr + (((col >> 3) ^ ((k & 3) << 2)) << 3) + (col & 7);
+template <int LDR>
+__device__ __forceinline__ int kmaj_bf16(int k, int col) {
+  static_assert(LDR % 128 == 0 || LDR == 64, "rows of 64 or a multiple of 128 elements");
+  const int x = LDR == 64 ? ((k >> 1) & 1) << 2 : (k & 3) << 2;
+  return k * LDR + (((col >> 3) ^ x) << 3) + (col & 7);
 }
 #ifndef UN_HALO_WAVES
 #define UN_HALO_WAVES 8
@@ -285,12 +289,11 @@ struct GemmMma<bf16_t, BM, BN, BK, WGM_, WGN_> {
   // stage[k0 + e][rb + i] for e = 0..3 - four consecutive k of its own row.
   template <int LDR>
   __device__ __forceinline__ static bf16x8 frag_kmaj(const bf16_t* s, int row0, int kk) {
-    static_assert(LDR % 128 == 0, "whole 16-chunk rows for the chunk swizzle");
     const int lane = threadIdx.x & 63, h = lane >> 4, a = lane & 15;
     const int rb = row0 + 16 * (h & 1) + 4 * (a & 3), k0 = kk + 8 * (h >> 1) + (a >> 2);
     typedef short s4 __attribute__((ext_vector_type(4)));
-    const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(s + kmaj_bf16(k0, rb, LDR)));
-    const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(s + kmaj_bf16(k0 + 4, rb, LDR)));
+    const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(s + kmaj_bf16<LDR>(k0, rb)));
+    const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(s + kmaj_bf16<LDR>(k0 + 4, rb)));
     const u32x2 l = __builtin_bit_cast(u32x2, lo), u = __builtin_bit_cast(u32x2, hi);
     return __builtin_bit_cast(bf16x8, u32x4{l[0], l[1], u[0], u[1]});
   }
@@ -576,7 +579,7 @@ struct KRowLoader {
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + NT * s;
-      if constexpr (sizeof(T) == 2) *(u32x4*)(sm + kmaj_bf16(v / CPR, (v % CPR) * VEC, LDR)) = r[S][s];
+      if constexpr (sizeof(T) == 2) *(u32x4*)(sm + kmaj_bf16<LDR>(v / CPR, (v % CPR) * VEC)) = r[S][s];
       else *(u32x4*)(sm + (v / CPR) * LDR + (v % CPR) * VEC) = r[S][s];
     }
   }
@@ -828,7 +831,7 @@ __device__ __forceinline__ void microtile_of(int t, int& rg, int& pg) {
 // path overflows the instruction cache): WG_POOLED / WG_PLAIN for a pooled /
 // unpooled block whose channel counts O and C are whole 16-byte vectors,
 // WG_GENERIC for anything else (element by element where needed).
-enum { WG_GENERIC = 0, WG_POOLED = 1, WG_PLAIN = 2 };
+enum { WG_GENERIC = 0, WG_POOLED = 1, WG_PLAIN = 2, WG_NARROW = WG_NARROW_BIT };
 
 template <typename T, int BM, int BN, int BK, int MODE>
 struct WgradLoader {
@@ -1944,20 +1947,22 @@ struct ConvKA {
   __device__ __forceinline__ void store(bf16_t* sm) const {
     u32x4 v = r[S];
     if constexpr (POOL) select_am<bf16_t>(v, am[S], k & 3);
-    *(u32x4*)(sm + kmaj_bf16(k, (threadIdx.x % CPR) * VEC, LDR)) = v;
+    *(u32x4*)(sm + kmaj_bf16<LDR>(k, (threadIdx.x % CPR) * VEC)) = v;
   }
 };
 
 template <int ROWS, int BK, int NT, int SLOTS, int PAD, bool POOL>
 struct ConvKB {
-  static constexpr int VEC = 8, CPR = ROWS / VEC, LDR = ROWS + PAD;
+  static constexpr int VEC = 8, CPR = ROWS / VEC, LDR = ROWS + PAD, NV = BK * CPR / NT;
   static constexpr int OOB = 0x7ffffff0;
-  static_assert(BK * CPR == NT, "one chunk per thread and k-block");
+  static_assert(NV >= 1 && BK * CPR == NV * NT, "whole chunks per thread and k-block");
+  static_assert(NT % CPR == 0, "a thread's chunks share one row set");
+  // chunk s of a thread: pixel k + s * (NT / CPR) of the block, the same rows
   __amdgpu_buffer_rsrc_t rs;
   const ConvProb* p;
   int k, kpix0, c0, u, v;
   bool jin, bias;
-  u32x4 r[SLOTS];
+  u32x4 r[SLOTS][NV];
   __device__ __forceinline__ void init(const ConvProb& pr, int j0, int kb0) {
     p = &pr;
     k = threadIdx.x / CPR;
@@ -1973,29 +1978,36 @@ struct ConvKB {
   }
   template <int S>
   __device__ __forceinline__ void load(int kb) {
-    const int pix = kpix0 + kb * BK;
-    const bool pin = pix < p->K;
-    int n, y, x;
-    decode_out_pixel(*p, pin ? pix : 0, n, y, x);
-    const int iy = y + u - p->pad, ix = x + v - p->pad;
-    const bool in = jin && pin && iy >= 0 && iy < p->H && ix >= 0 && ix < p->W;
-    u32x4 val = __builtin_bit_cast(
-        u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? (((n * p->H + iy) * p->W + ix) * p->C + c0) * 2 : OOB, 0, 0));
-    if (bias && pin) vset_bits<bf16_t>(val, 0, bits_of<bf16_t>(TT<bf16_t>::from_f(1.0f)));
-    r[S] = val;
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int pix = kpix0 + kb * BK + s * (NT / CPR);
+      const bool pin = pix < p->K;
+      int n, y, x;
+      decode_out_pixel(*p, pin ? pix : 0, n, y, x);
+      const int iy = y + u - p->pad, ix = x + v - p->pad;
+      const bool in = jin && pin && iy >= 0 && iy < p->H && ix >= 0 && ix < p->W;
+      u32x4 val = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? (((n * p->H + iy) * p->W + ix) * p->C + c0) * 2 : OOB, 0, 0));
+      if (bias && pin) vset_bits<bf16_t>(val, 0, bits_of<bf16_t>(TT<bf16_t>::from_f(1.0f)));
+      r[S][s] = val;
+    }
   }
   template <int S>
   __device__ __forceinline__ void store(bf16_t* sm) const {
-    *(u32x4*)(sm + kmaj_bf16(k, (threadIdx.x % CPR) * VEC, LDR)) = r[S];
+#pragma unroll
+    for (int s = 0; s < NV; ++s)
+      *(u32x4*)(sm + kmaj_bf16<LDR>(k + s * (NT / CPR), (threadIdx.x % CPR) * VEC)) = r[S][s];
   }
 };
 
-template <bool POOL>
-__global__ __launch_bounds__((GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, 4, 4>::NT))
-__attribute__((amdgpu_waves_per_eu((GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, 4, 4>::NT / 128))))
+// NARROW: tiles of CONV_WG_NARROW_BM output channels (8 waves), for launches
+// whose blocks have at most that many; else 128 rows (16 waves).
+template <bool POOL, bool NARROW>
+__global__ __launch_bounds__((NARROW ? 512 : 1024)) __attribute__((amdgpu_waves_per_eu((NARROW ? 4 : 8))))
 void conv_wgrad_mfma_kernel(const ConvProb* __restrict__ probs, const int32_t* __restrict__ tile_map) {
-  constexpr int BM = CONV_BM_BF16, BN = CONV_BN_BF16, BK = CONV_BK_BF16;
-  using MM = GemmMma<bf16_t, BM, BN, BK, 4, 4>;  // 16 waves: one operand chunk per thread
+  constexpr int BM = NARROW ? CONV_WG_NARROW_BM : CONV_BM_BF16, BN = CONV_BN_BF16, BK = CONV_BK_BF16;
+  using MM = GemmMma<bf16_t, BM, BN, BK, NARROW ? 2 : 4, 4>;  // 32x32 wave tiles
+  static_assert(MM::NT == (NARROW ? 512 : 1024), "launch bounds");
   constexpr int NT = MM::NT, D = UN_GEMM_DEPTH;
   static_assert(MM::LDR_A * BK <= Tile<bf16_t, BM, BN, BK>::A_ELEMS &&
                     MM::LDR_B * BK <= Tile<bf16_t, BM, BN, BK>::B_ELEMS, "k-major stages fit the stage buffers");
@@ -2294,10 +2306,16 @@ hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const i
   hipLaunchKernelGGL((conv_wgrad_kernel<T, BM, BN, BK, M>), dim3(ntiles), dim3(256), 0, s, probs, tile_map)
   if (bf16) {
     constexpr int NT = GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, 4, 4>::NT;
-    if (mode == WG_POOLED)
-      hipLaunchKernelGGL(conv_wgrad_mfma_kernel<true>, dim3(ntiles), dim3(NT), 0, s, probs, tile_map);
+    const bool narrow = (mode & WG_NARROW) != 0;
+    mode &= ~WG_NARROW;
+    if (mode == WG_POOLED && narrow)
+      hipLaunchKernelGGL((conv_wgrad_mfma_kernel<true, true>), dim3(ntiles), dim3(NT / 2), 0, s, probs, tile_map);
+    else if (mode == WG_POOLED)
+      hipLaunchKernelGGL((conv_wgrad_mfma_kernel<true, false>), dim3(ntiles), dim3(NT), 0, s, probs, tile_map);
+    else if (mode == WG_PLAIN && narrow)
+      hipLaunchKernelGGL((conv_wgrad_mfma_kernel<false, true>), dim3(ntiles), dim3(NT / 2), 0, s, probs, tile_map);
     else if (mode == WG_PLAIN)
-      hipLaunchKernelGGL(conv_wgrad_mfma_kernel<false>, dim3(ntiles), dim3(NT), 0, s, probs, tile_map);
+      hipLaunchKernelGGL((conv_wgrad_mfma_kernel<false, false>), dim3(ntiles), dim3(NT), 0, s, probs, tile_map);
     else UN_WGRAD_LAUNCH(bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, WG_GENERIC);
   } else {
     if (mode == WG_POOLED) UN_WGRAD_LAUNCH(float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, WG_POOLED);

@@ -552,7 +552,7 @@ static void build_tables(un_ctx* c, Tables& T) {
     std::vector<TileGroup> gs;
     for (size_t k = 0; k < ps.size(); ++k) {
       ConvProb& p = ps[k];
-      p.tiles_m = cdiv(p.M, p.halo ? p.bm : CBM);
+      p.tiles_m = cdiv(p.M, p.bm ? p.bm : CBM);  // halo tiles and narrow weight-gradient tiles set bm
       p.tiles_n = cdiv(p.N, p.halo ? p.bn : CBN);
       const int per_split = p.tiles_m * p.tiles_n;
       if (kind == 3) {
@@ -605,9 +605,14 @@ static void build_tables(un_ctx* c, Tables& T) {
         by[!whole ? 0 : p.pool ? 1 : 2].push_back(p);
       }
       for (int m = 0; m < 3; ++m) {
+        // bf16 whole-vector blocks that all have few output channels: 64-row tiles
+        bool narrow = bf && m != 0 && !by[m].empty();
+        for (auto& p : by[m]) narrow = narrow && p.O <= CONV_WG_NARROW_BM;
+        if (narrow)
+          for (auto& p : by[m]) p.bm = CONV_WG_NARROW_BM;
         const size_t before = out.size();
         emit_conv_one(by[m], out, kind, kclass);
-        if (out.size() > before) out.back().mode = m;
+        if (out.size() > before) out.back().mode = m | (narrow ? WG_NARROW_BIT : 0);
       }
     }
   };
