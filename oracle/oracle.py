@@ -26,7 +26,11 @@ paper's PyTorch prototype, whose defaults these are):
 * convolution is cross-correlation, stride 1, zero padding;
 * max-pool is 2x2 / stride 2 / floor mode, the first maximum in row-major
   window order wins ties; ReLU'(0) = 0;
-* flatten is NCHW (c, h, w) order.
+* flatten is NCHW (c, h, w) order;
+* a residual block (``res_begin`` ... ``res_end``) is a module returning
+  inner(x) + x, the standard skip connection: the sum is formed before any
+  ReLU that follows the block, and in backward the gradient at the sum flows
+  both through the enclosed layers and unchanged to x, where the two add.
 
 Precision modes:
 
@@ -252,7 +256,7 @@ def count_params(spec, in_shape):
             shape = (c, H // 2, W // 2)
         elif op == "flatten":
             shape = (int(np.prod(shape)),)
-        elif op != "relu":
+        elif op not in ("relu", "res_begin", "res_end"):
             raise ValueError(f"unknown op {op!r}")
     return total
 
@@ -277,18 +281,39 @@ def forward(spec, params, x, mode="f32", flags=None):
     cache = []
     pi = 0
     mag, last_pi = None, None
-    for layer in spec["layers"]:
+    layers = spec["layers"]
+    skip = None  # input of the open residual block
+    for li, layer in enumerate(layers):
         op = layer[0]
         if op == "linear":
             W, b = params[pi], params[pi + 1]
             hin, Wq = R.operand(h), R.operand(W)
             if hin.ndim != 2:
                 raise ValueError("linear layer needs a 2-D input (add a flatten)")
-            h = R.store(linear_fwd(hin, Wq, np.asarray(b, dtype=F64)))
+            z = linear_fwd(hin, Wq, np.asarray(b, dtype=F64))
+            ends_block = li + 1 < len(layers) and layers[li + 1][0] == "res_end"
+            if ends_block:
+                # the residual sum is the stored tensor: x joins before rounding
+                if skip is None or skip.shape != z.shape:
+                    raise ValueError("residual block: missing begin or feature mismatch")
+                z = z + R.operand(skip)
+            h = R.store(z)
             if flags is not None:
                 mag, last_pi = linear_fwd(np.abs(hin), np.abs(Wq), np.abs(np.asarray(b, dtype=F64))), pi
+                if ends_block:
+                    mag = mag + np.abs(R.operand(skip))
             cache.append(("linear", pi, hin, Wq))
             pi += 2
+        elif op == "res_begin":
+            if skip is not None:
+                raise ValueError("nested residual blocks")
+            skip = h
+            cache.append(("res_begin",))
+        elif op == "res_end":
+            if skip is None or layers[li - 1][0] != "linear":
+                raise ValueError("residual end must directly follow the block's last linear")
+            skip = None
+            cache.append(("res_end",))
         elif op == "conv":
             W, b = params[pi], params[pi + 1]
             hin, Wq = R.operand(h), R.operand(W)
@@ -335,8 +360,17 @@ def backward(spec, params, cache, dlogits, mode="f32"):
     grads = [None] * len(params)
     g = np.asarray(dlogits, dtype=F64)
     first_param_layer = min(e[1] for e in cache if e[0] in ("linear", "conv"))
+    gskip = None  # gradient at the sum of the open residual block
     for entry in reversed(cache):
         kind = entry[0]
+        if kind == "res_end":
+            gskip = g
+            continue
+        if kind == "res_begin":
+            # both paths reach the block's input: the enclosed layers' and the skip
+            g = R.store(g + R.operand(gskip))
+            gskip = None
+            continue
         if kind in ("linear", "conv"):
             pi, hin, Wq = entry[1], entry[2], entry[3]
             gq = R.operand(g)

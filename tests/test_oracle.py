@@ -285,6 +285,65 @@ def test_fd_lenet_like_small():
     assert _fd_check(spec, (1, 10, 10), 23, n_samples=20) > 20
 
 
+# Residual blocks: inner(x) + x, with a ReLU after the block applied to the sum
+_RES_SPEC = {"layers": [("linear", 6), ("relu",),
+                        ("res_begin",), ("linear", 6), ("res_end",), ("relu",),
+                        ("res_begin",), ("linear", 5), ("relu",), ("linear", 6), ("res_end",), ("relu",),
+                        ("linear", 4)], "num_classes": 4}
+
+
+def test_fd_residual_blocks():
+    # the backward (both paths into a block's input) against the forward's own loss
+    assert _fd_check(_RES_SPEC, (7,), 24) > 150
+
+
+def test_residual_forward_matches_torch_modules():
+    # the forward against an nn.Module graph with the skip written as x + inner(x)
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(25)
+    params = [p.astype(np.float64) for p in W.init_params(_RES_SPEC, (7,), 25, 0)]
+    x = rng.standard_normal((5, 7))
+    lin = lambda i, h: torch.nn.functional.linear(h, torch.from_numpy(params[2 * i]), torch.from_numpy(params[2 * i + 1]))
+    h = torch.relu(lin(0, torch.from_numpy(x)))
+    h = torch.relu(lin(1, h) + h)
+    h = torch.relu(lin(3, torch.relu(lin(2, h))) + h)
+    ref = lin(4, h).numpy()
+    got, _ = oracle.forward(_RES_SPEC, params, x, "f64")
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_residual_with_zero_inner_layers_is_the_identity():
+    # zero weights and biases inside a block: the block passes x through, so the
+    # model equals the one without the block (forward, and gradients of the rest)
+    spec = {"layers": [("linear", 6), ("relu",), ("res_begin",), ("linear", 6), ("res_end",), ("relu",),
+                       ("linear", 4)], "num_classes": 4}
+    plain = {"layers": [("linear", 6), ("relu",), ("linear", 4)], "num_classes": 4}
+    rng = np.random.default_rng(26)
+    params = [p.astype(np.float64) for p in W.init_params(spec, (7,), 26, 0)]
+    params[2][:] = 0.0
+    params[3][:] = 0.0
+    x = rng.standard_normal((5, 7))
+    y = rng.integers(0, 4, 5)
+    keep = [params[0], params[1], params[4], params[5]]
+    z1, c1 = oracle.forward(spec, params, x, "f64")
+    z0, c0 = oracle.forward(plain, keep, x, "f64")
+    np.testing.assert_array_equal(z1, z0)
+    g1 = oracle.backward(spec, params, c1, oracle.softmax_ce(z1, y)[1], "f64")
+    g0 = oracle.backward(plain, keep, c0, oracle.softmax_ce(z0, y)[1], "f64")
+    for a, b in zip([g1[0], g1[1], g1[4], g1[5]], g0):
+        np.testing.assert_allclose(a, b, rtol=1e-13, atol=1e-15)
+
+
+def test_residual_spec_errors():
+    params = [p.astype(np.float64) for p in W.init_params(_RES_SPEC, (7,), 27, 0)]
+    x = np.zeros((2, 7))
+    bad = {"layers": [("linear", 6), ("res_begin",), ("linear", 5), ("res_end",), ("linear", 4)],
+           "num_classes": 4}
+    with pytest.raises(ValueError):
+        oracle.forward(bad, [p.astype(np.float64) for p in W.init_params(bad, (7,), 27, 0)], x, "f64")
+    assert oracle.count_params(_RES_SPEC, (7,)) == sum(p.size for p in params)
+
+
 # ---------------------------------------------------------------------------
 # Shapes and parameter counts
 # ---------------------------------------------------------------------------
