@@ -62,7 +62,19 @@ typedef enum {
                       weight [out, in, k, k], bias [out]; cross-correlation */
   UN_RELU = 2,
   UN_MAXPOOL2 = 3, /* 2x2, stride 2, floor mode; ties: first max in row-major order */
-  UN_FLATTEN = 4   /* NCHW (c, h, w) order */
+  UN_FLATTEN = 4,  /* NCHW (c, h, w) order */
+  /* A skip connection around the layers between the two markers (a residual
+   * block): the layers run on the block's input x as usual and, at the END
+   * marker, x is added to their result, before any ReLU that follows the END
+   * marker. In PyTorch terms the markers wrap the enclosed layers in a module
+   * whose forward returns inner(x) + x. The enclosed layers are one or more
+   * [Linear, optional ReLU] blocks (no ReLU directly before the END marker),
+   * the result has as many features as x, x is the output of a Linear (a
+   * block never starts at the network input or after a Flatten), the block
+   * does not end at the logits layer and blocks do not nest. The markers have
+   * no parameters. */
+  UN_RESIDUAL_BEGIN = 5,
+  UN_RESIDUAL_END = 6
 } un_op;
 
 typedef struct {
@@ -95,7 +107,8 @@ typedef struct {
  * un_set_params). Supported layer patterns per model: zero or more
  * [Conv2d, optional ReLU, optional MaxPool2] blocks, a Flatten if any conv is
  * present, then one or more [Linear, optional ReLU] blocks, the last Linear
- * having no ReLU and out == num_classes.
+ * having no ReLU and out == num_classes; residual markers may enclose runs of
+ * the Linear blocks as UN_RESIDUAL_BEGIN describes.
  * On success *out owns the context. Errors: UN_ERR_INVALID, UN_ERR_UNSUPPORTED,
  * UN_ERR_OOM, UN_ERR_DEVICE (then *out is NULL). */
 un_status un_create(const un_model_spec* specs, int32_t n_models,

@@ -62,6 +62,11 @@ struct GemmProb {
   // the tile's summed row losses go to ce_part[m-tile]. Null: C is the fp32
   // logits and a separate CE pass follows.
   float* ce_part;
+  // Skip connection (residual blocks), row-major [m][n] in the storage type,
+  // added in fp32 before the ReLU (FWD) or before the ReLU' mask (DGRAD):
+  // FWD: the block's input x; DGRAD: the gradient at the block's output. Null: none.
+  const void* R;
+  int64_t ldr;
   // optimizer state (same layouts as W and bmaster; null for plain SGD):
   // momentum buffer or Adam's first moment, and Adam's second moment
   float* s1;

@@ -1162,7 +1162,8 @@ template <typename T, int VE> __device__ __forceinline__ void load_chunk_f(const
 // (ReLU' of the previous layer's output).
 template <typename OT, int BM, int BN, int CLD, int NT = 256>
 __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, int m0, int n0, int M, int N,
-                                           const OT* mask = nullptr, int64_t ldmask = 0) {
+                                           const OT* mask = nullptr, int64_t ldmask = 0,
+                                           const OT* add = nullptr, int64_t ldadd = 0, bool relu = false) {
   constexpr int VE = 16 / sizeof(OT), CPR = BN / VE;
   static_assert(CLD % 4 == 0, "float4 rows");
   for (int idx = threadIdx.x; idx < BM * CPR; idx += NT) {
@@ -1177,6 +1178,15 @@ __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, 
       v[e + 1] = x[1];
       v[e + 2] = x[2];
       v[e + 3] = x[3];
+    }
+    if (add) {
+      float av[VE];
+      load_chunk_f<OT, VE>(add + (int64_t)m * ldadd + n, av);
+#pragma unroll
+      for (int e = 0; e < VE; ++e) {
+        v[e] += av[e];
+        if (relu) v[e] = fmaxf(v[e], 0.f);
+      }
     }
     if (mask) {
       float mv[VE];
@@ -1339,7 +1349,7 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             v[r] += b;
-            if (p.relu) v[r] = fmaxf(v[r], 0.f);
+            if (p.relu && !p.R) v[r] = fmaxf(v[r], 0.f);  // with a skip input: after the sum
           }
         }
       }
@@ -1354,12 +1364,16 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
       return;
     }
     // Row pass: C[m][n] in 16-byte chunks along n (data gradient: with the
-    // previous layer's ReLU' from its stored output).
+    // previous layer's ReLU' from its stored output), adding the skip input
+    // of a residual block first where there is one.
     if (p.C) {
       if (epi == EPI_LOGITS) store_rows<float, BM, BN, CLD, NT>(sC, (float*)p.C, p.ldc, m0, n0, p.M, p.N);
-      else if (epi == EPI_DGRAD && p.relu)
-        store_rows<T, BM, BN, CLD, NT>(sC, (T*)p.C, p.ldc, m0, n0, p.M, p.N, (const T*)p.mask, p.ldmask);
-      else store_rows<T, BM, BN, CLD, NT>(sC, (T*)p.C, p.ldc, m0, n0, p.M, p.N);
+      else if constexpr (!BWD)
+        store_rows<T, BM, BN, CLD, NT>(sC, (T*)p.C, p.ldc, m0, n0, p.M, p.N, nullptr, 0, (const T*)p.R, p.ldr,
+                                       p.relu && p.R);
+      else
+        store_rows<T, BM, BN, CLD, NT>(sC, (T*)p.C, p.ldc, m0, n0, p.M, p.N, p.relu ? (const T*)p.mask : nullptr,
+                                       p.ldmask, (const T*)p.R, p.ldr);
     }
     return;
   }

@@ -38,6 +38,10 @@ struct Block {
   int level = 0, model = 0;
   bool relu = false, pool = false, last = false, prev_relu = false, concat = false;
   bool next_linear = false;  // the following block is a Linear (needs transposed output)
+  // residual blocks: on the block that ends one, the index of the block whose
+  // input is added to its output (res_from); on that first block, the index
+  // of the end block, whose output gradient joins its input gradient (res_to)
+  int res_from = -1, res_to = -1;
   // linear
   int K = 0, N = 0;
   int in_c = 0, in_h = 1, in_w = 1;  // input viewed as an image (Flatten order mapping)
@@ -189,9 +193,57 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
   bool flat = false;
   size_t pt = 0;
   int i = 0;
+  int res_open = -1, res_feat = 0;  // first block and input features of an open residual block
   auto where = [&](int li) { return "model " + std::to_string(mi) + " layer " + std::to_string(li) + ": "; };
   while (i < s.n_layers) {
     const un_layer& L = s.layers[i];
+    if (L.op == UN_RESIDUAL_BEGIN) {
+      if (res_open >= 0) {
+        why = where(i) + "nested residual blocks are not supported";
+        return UN_ERR_UNSUPPORTED;
+      }
+      if (m.blocks.empty() || m.blocks.back().kind != 0) {
+        why = where(i) + "a residual block must start at the output of a Linear";
+        return UN_ERR_UNSUPPORTED;
+      }
+      res_open = (int)m.blocks.size();
+      res_feat = c;
+      ++i;
+      continue;
+    }
+    if (L.op == UN_RESIDUAL_END) {
+      if (res_open < 0) {
+        why = where(i) + "residual end without a begin";
+        return UN_ERR_INVALID;
+      }
+      if ((int)m.blocks.size() == res_open) {
+        why = where(i) + "empty residual block";
+        return UN_ERR_INVALID;
+      }
+      if (s.layers[i - 1].op != UN_LINEAR) {
+        why = where(i) + "a residual block must end with a Linear (a ReLU goes after the end marker)";
+        return UN_ERR_UNSUPPORTED;
+      }
+      Block& e = m.blocks.back();
+      if (e.N != res_feat) {
+        why = where(i) + "residual output features " + std::to_string(e.N) + " != input features " +
+              std::to_string(res_feat);
+        return UN_ERR_INVALID;
+      }
+      e.res_from = res_open;
+      m.blocks[res_open].res_to = (int)m.blocks.size() - 1;
+      res_open = -1;
+      ++i;
+      if (i < s.n_layers && s.layers[i].op == UN_RELU) {
+        e.relu = true;
+        ++i;
+      }
+      continue;
+    }
+    if (res_open >= 0 && L.op != UN_LINEAR && L.op != UN_RELU) {
+      why = where(i) + "a residual block may enclose only Linear and ReLU layers";
+      return UN_ERR_UNSUPPORTED;
+    }
     if (L.op == UN_CONV2D) {
       if (flat) {
         why = where(i) + "conv needs an image input (got a flat tensor)";
@@ -282,8 +334,16 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
       return UN_ERR_INVALID;
     }
   }
+  if (res_open >= 0) {
+    why = "model " + std::to_string(mi) + ": residual block without an end";
+    return UN_ERR_INVALID;
+  }
   if (m.blocks.empty() || m.blocks.back().kind != 0) {
     why = "model " + std::to_string(mi) + ": the last parameterised layer must be Linear";
+    return UN_ERR_UNSUPPORTED;
+  }
+  if (m.blocks.back().res_from >= 0) {
+    why = "model " + std::to_string(mi) + ": a residual block may not end at the logits layer";
     return UN_ERR_UNSUPPORTED;
   }
   Block& last = m.blocks.back();
@@ -538,7 +598,8 @@ static void build_tables(un_ctx* c, Tables& T) {
       size_t b0 = po + k * sizeof(GemmProb);
       for (size_t f : {offsetof(GemmProb, A), offsetof(GemmProb, B), offsetof(GemmProb, C), offsetof(GemmProb, bias),
                        offsetof(GemmProb, mask), offsetof(GemmProb, dbias), offsetof(GemmProb, W), offsetof(GemmProb, Wb),
-                       offsetof(GemmProb, bmaster), offsetof(GemmProb, row_model), offsetof(GemmProb, ce_part)})
+                       offsetof(GemmProb, bmaster), offsetof(GemmProb, row_model), offsetof(GemmProb, ce_part),
+                       offsetof(GemmProb, R)})
         fix.push_back(b0 + f);
     }
     size_t mo = put(map.data(), map.size() * 4);
@@ -681,6 +742,11 @@ static void build_tables(un_ctx* c, Tables& T) {
         p.C = ptr(b.Y);
         p.ldc = b.ldy;
         p.bias = (const float*)ptr(b.b32);
+        if (b.res_from >= 0) {
+          const Block& rb = m.blocks[b.res_from];
+          p.R = ptr(rb.X);
+          p.ldr = rb.ldx;
+        }
         if (b.last && ce_fused(b)) {
           // softmax-CE in the logits GEMM's epilogue: it writes dL/dz
           p.C = ptr(b.G);
@@ -833,6 +899,11 @@ static void build_tables(un_ctx* c, Tables& T) {
           p.ldmask = b.ldx;
           p.C = ptr(pb.G);
           p.ldc = pb.kind == 0 ? pb.ldg : pb.out_elems_per_sample();
+          if (b.res_to >= 0) {
+            const Block& eb = m.blocks[b.res_to];
+            p.R = ptr(eb.G);
+            p.ldr = eb.ldg;
+          }
           gp.push_back(p);
         }
         if (lv == 0) add_wgrad(b, gp, cat_done);

@@ -25,6 +25,9 @@ Design overview):
 * ``("relu",)``
 * ``("pool",)``                    2x2 max-pool, stride 2, floor mode
 * ``("flatten",)``                 NCHW flatten order
+* ``("res_begin",)`` ... ``("res_end",)``  a residual block: the enclosed
+  Linear layers' result plus the block's input (a module returning
+  ``inner(x) + x``); a ReLU after ``res_end`` applies to the sum
 """
 from __future__ import annotations
 
@@ -34,7 +37,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-OP_CODES = {"linear": 0, "conv": 1, "relu": 2, "pool": 3, "flatten": 4}
+OP_CODES = {"linear": 0, "conv": 1, "relu": 2, "pool": 3, "flatten": 4, "res_begin": 5, "res_end": 6}
 
 
 @dataclass

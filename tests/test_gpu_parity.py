@@ -85,6 +85,26 @@ def test_ragged_mlps(precision):
 
 
 @pytest.mark.parametrize("precision", ["f32", "bf16"])
+def test_residual_mlps(precision):
+    """Residual blocks (inner(x) + x, the sum before the following ReLU): the
+    skip input joins in the forward GEMM's epilogue and the skip gradient in
+    the data gradient's, over widths of several tiles and a ragged tail, with
+    and without ReLUs around the block, beside a plain model."""
+    _need_gpu()
+    L, RELU, RB, RE = (lambda n: ("linear", n)), ("relu",), ("res_begin",), ("res_end",)
+    specs = [
+        {"layers": [L(96), RELU, RB, L(96), RE, RELU, L(13)], "num_classes": 13},
+        {"layers": [L(200), RELU, RB, L(70), RELU, L(200), RE, RELU, RB, L(200), RE, L(13)], "num_classes": 13},
+        {"layers": [L(37), RELU, L(13)], "num_classes": 13},
+        {"layers": [L(300), RB, L(300), RELU, L(300), RE, L(13)], "num_classes": 13},
+    ]
+    wl = _custom(specs, 37, (104,), precision)
+    m = range(wl.n_models)
+    _report(f"residual_{precision} 1 step", compare_step(wl, run_gpu(wl, 1), run_oracle(wl, 1, m), m))
+    _report(f"residual_{precision} run", compare_run(wl, run_gpu(wl, wl.steps), run_oracle(wl, wl.steps, m), m))
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
 def test_softmax_ce_fused_and_row_pass(precision):
     """Class counts on both sides of one GEMM tile's width (bf16 128, fp32 64):
     the models whose classes fit get softmax-CE in their logits GEMM's

@@ -1,0 +1,58 @@
+"""Residual blocks in model specs: the planner's validation (un_plan_bytes runs
+on the host, no device needed) of what is a well-formed block, with the status
+each malformed one returns."""
+import pytest
+
+from paper_2408_01331_amd import unifiednn as U
+
+
+def _need_lib():
+    try:
+        U.lib()
+    except OSError as e:  # not built
+        pytest.skip(f"library not built: {e}")
+
+
+def _spec(*layers, classes=5):
+    return {"layers": list(layers), "num_classes": classes}
+
+
+L, RELU, RB, RE = (lambda n: ("linear", n)), ("relu",), ("res_begin",), ("res_end",)
+
+GOOD = [
+    _spec(L(8), RELU, RB, L(8), RE, RELU, L(5)),
+    _spec(L(8), RB, L(3), RELU, L(8), RE, RB, L(8), RE, L(5)),       # two blocks, no ReLUs after them
+    _spec(L(8), RELU, RB, L(8), RE, RELU, RB, L(8), RE, RELU, L(5)),
+]
+
+BAD = [
+    (_spec(RB, L(8), RE, L(5)), U.UN_ERR_UNSUPPORTED),                 # starts at the network input
+    (_spec(L(8), RB, L(8), RELU, RE, L(5)), U.UN_ERR_UNSUPPORTED),     # ReLU inside, right before the end
+    (_spec(L(8), RB, L(7), RE, L(5)), U.UN_ERR_INVALID),               # width changes
+    (_spec(L(8), RB, RE, L(5)), U.UN_ERR_INVALID),                     # empty
+    (_spec(L(8), RE, L(5)), U.UN_ERR_INVALID),                         # end without begin
+    (_spec(L(8), RB, L(8), L(5)), U.UN_ERR_INVALID),                   # never closed
+    (_spec(L(5), RB, L(5), RE), U.UN_ERR_UNSUPPORTED),                 # ends at the logits
+    (_spec(L(8), RB, L(8), RB, L(8), RE, RE, L(5)), U.UN_ERR_UNSUPPORTED),  # nested
+]
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
+def test_residual_specs_accepted(precision):
+    _need_lib()
+    base, _ = U.un_plan_bytes([_spec(L(8), RELU, L(8), RELU, L(5))], 16, (16,), precision)
+    for s in GOOD:
+        arena, _ = U.un_plan_bytes([s], 16, (16,), precision)
+        assert arena > 0
+    # the markers hold no parameters and no buffers of their own
+    same, _ = U.un_plan_bytes([GOOD[0]], 16, (16,), precision)
+    assert same == base
+
+
+@pytest.mark.parametrize("case", range(len(BAD)))
+def test_residual_specs_rejected(case):
+    _need_lib()
+    spec, status = BAD[case]
+    with pytest.raises(U.UnError) as e:
+        U.un_plan_bytes([spec], 16, (16,), "f32")
+    assert e.value.status == status
