@@ -310,16 +310,24 @@ def forward(spec, params, x, mode="f32", flags=None):
             skip = h
             cache.append(("res_begin",))
         elif op == "res_end":
-            if skip is None or layers[li - 1][0] != "linear":
-                raise ValueError("residual end must directly follow the block's last linear")
+            if skip is None or layers[li - 1][0] not in ("linear", "conv"):
+                raise ValueError("residual end must directly follow the block's last linear or conv")
             skip = None
             cache.append(("res_end",))
         elif op == "conv":
             W, b = params[pi], params[pi + 1]
             hin, Wq = R.operand(h), R.operand(W)
-            h = R.store(conv2d_fwd(hin, Wq, np.asarray(b, dtype=F64), layer[3]))
+            z = conv2d_fwd(hin, Wq, np.asarray(b, dtype=F64), layer[3])
+            ends_block = li + 1 < len(layers) and layers[li + 1][0] == "res_end"
+            if ends_block:
+                if skip is None or skip.shape != z.shape:
+                    raise ValueError("residual block: missing begin or shape mismatch")
+                z = z + R.operand(skip)
+            h = R.store(z)
             if flags is not None:
                 mag = conv2d_fwd(np.abs(hin), np.abs(Wq), np.abs(np.asarray(b, dtype=F64)), layer[3])
+                if ends_block:
+                    mag = mag + np.abs(R.operand(skip))
                 last_pi = pi
             cache.append(("conv", pi, hin, Wq, layer[3]))
             pi += 2

@@ -334,6 +334,29 @@ def test_residual_with_zero_inner_layers_is_the_identity():
         np.testing.assert_allclose(a, b, rtol=1e-13, atol=1e-15)
 
 
+_RES_CNN = {"layers": [("conv", 3, 3, 1), ("relu",),
+                       ("res_begin",), ("conv", 4, 3, 1), ("relu",), ("conv", 3, 3, 1), ("res_end",), ("relu",),
+                       ("pool",), ("flatten",), ("linear", 3)], "num_classes": 3}
+
+
+def test_fd_residual_conv_block():
+    assert _fd_check(_RES_CNN, (2, 6, 6), 28, n_samples=12) > 50
+
+
+def test_residual_conv_forward_matches_torch_modules():
+    torch = pytest.importorskip("torch")
+    F = torch.nn.functional
+    rng = np.random.default_rng(29)
+    params = [p.astype(np.float64) for p in W.init_params(_RES_CNN, (2, 6, 6), 29, 0)]
+    t = [torch.from_numpy(p) for p in params]
+    x = rng.standard_normal((3, 2, 6, 6))
+    h = torch.relu(F.conv2d(torch.from_numpy(x), t[0], t[1], padding=1))
+    h = torch.relu(F.conv2d(torch.relu(F.conv2d(h, t[2], t[3], padding=1)), t[4], t[5], padding=1) + h)
+    ref = F.linear(F.max_pool2d(h, 2).flatten(1), t[6], t[7]).numpy()
+    got, _ = oracle.forward(_RES_CNN, params, x, "f64")
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
 def test_residual_spec_errors():
     params = [p.astype(np.float64) for p in W.init_params(_RES_SPEC, (7,), 27, 0)]
     x = np.zeros((2, 7))
