@@ -68,11 +68,13 @@ typedef enum {
    * marker, x is added to their result, before any ReLU that follows the END
    * marker. In PyTorch terms the markers wrap the enclosed layers in a module
    * whose forward returns inner(x) + x. The enclosed layers are one or more
-   * [Linear, optional ReLU] blocks (no ReLU directly before the END marker),
-   * the result has as many features as x, x is the output of a Linear (a
+   * [Linear, optional ReLU] or [Conv2d, optional ReLU] blocks (no ReLU
+   * directly before the END marker, no MaxPool2 inside or right after), the
+   * result has the shape of x, x is the output of a Linear or Conv2d block (a
    * block never starts at the network input or after a Flatten), the block
-   * does not end at the logits layer and blocks do not nest. The markers have
-   * no parameters. */
+   * does not end at the logits layer and blocks do not nest; other patterns
+   * return UN_ERR_UNSUPPORTED (shape mismatches UN_ERR_INVALID). The markers
+   * have no parameters. */
   UN_RESIDUAL_BEGIN = 5,
   UN_RESIDUAL_END = 6
 } un_op;

@@ -116,6 +116,11 @@ struct ConvProb {
   void* Gprev;                // dgrad output [n*H*W + y*W + x][C]
   float* ws;                  // wgrad partials [splits][O][ldws]
   int64_t ldws;
+  // Skip connection (residual blocks; pool == 0, pixel-ordered rows), added in
+  // fp32 before the ReLU (fwd: the block's input x [pixel][O]) or before the
+  // previous block's ReLU' (dgrad: the gradient at the block's output
+  // [pixel][C]). Null: none.
+  const void* R;
 };
 
 // Split-K reduction of conv weight-gradient partials, in split order, with

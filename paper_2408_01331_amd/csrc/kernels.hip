@@ -1469,6 +1469,8 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         v[r] = acc[i][j][r] + b;
+        // skip input of a residual block (never pooled): rows are pixels
+        if (p.R && mb + r < p.M) v[r] += TT<T>::to_f(((const T*)p.R)[(int64_t)(mb + r) * O + o]);
         if (p.relu) v[r] = fmaxf(v[r], 0.f);
       }
       if (p.pool) {
@@ -1515,8 +1517,19 @@ __device__ __forceinline__ void conv_dgrad_epilogue(const ConvProb& p, int m0, i
 #pragma unroll
     for (int j = 0; j < TL::FN; ++j) {
       const int cl = wn + 16 * j + (lane & 15);
+      if (p.R) {
+        // gradient at a residual block's output joins before the rounding
+        const int c = n0 + cl;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) sG[(rl + r) * ES::SLD + cl] = TT<T>::from_f(acc[i][j][r]);
+        for (int r = 0; r < 4; ++r) {
+          const int m = m0 + rl + r;
+          const float add = (m < p.M && c < C) ? TT<T>::to_f(((const T*)p.R)[(int64_t)m * C + c]) : 0.f;
+          sG[(rl + r) * ES::SLD + cl] = TT<T>::from_f(acc[i][j][r] + add);
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sG[(rl + r) * ES::SLD + cl] = TT<T>::from_f(acc[i][j][r]);
+      }
     }
   }
   __syncthreads();

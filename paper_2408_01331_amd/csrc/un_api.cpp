@@ -193,7 +193,7 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
   bool flat = false;
   size_t pt = 0;
   int i = 0;
-  int res_open = -1, res_feat = 0;  // first block and input features of an open residual block
+  int res_open = -1, res_c = 0, res_h = 0, res_w = 0;  // first block and input shape of an open residual block
   auto where = [&](int li) { return "model " + std::to_string(mi) + " layer " + std::to_string(li) + ": "; };
   while (i < s.n_layers) {
     const un_layer& L = s.layers[i];
@@ -202,12 +202,14 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
         why = where(i) + "nested residual blocks are not supported";
         return UN_ERR_UNSUPPORTED;
       }
-      if (m.blocks.empty() || m.blocks.back().kind != 0) {
-        why = where(i) + "a residual block must start at the output of a Linear";
+      if (m.blocks.empty() || s.layers[i - 1].op == UN_FLATTEN) {
+        why = where(i) + "a residual block must start at the output of a Linear or Conv2d block";
         return UN_ERR_UNSUPPORTED;
       }
       res_open = (int)m.blocks.size();
-      res_feat = c;
+      res_c = c;
+      res_h = h;
+      res_w = w;
       ++i;
       continue;
     }
@@ -220,14 +222,13 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
         why = where(i) + "empty residual block";
         return UN_ERR_INVALID;
       }
-      if (s.layers[i - 1].op != UN_LINEAR) {
-        why = where(i) + "a residual block must end with a Linear (a ReLU goes after the end marker)";
+      if (s.layers[i - 1].op != UN_LINEAR && s.layers[i - 1].op != UN_CONV2D) {
+        why = where(i) + "a residual block must end with a Linear or Conv2d (a ReLU goes after the end marker)";
         return UN_ERR_UNSUPPORTED;
       }
       Block& e = m.blocks.back();
-      if (e.N != res_feat) {
-        why = where(i) + "residual output features " + std::to_string(e.N) + " != input features " +
-              std::to_string(res_feat);
+      if (e.kind == 0 ? e.N != res_c : (e.O != res_c || e.OH != res_h || e.OW != res_w)) {
+        why = where(i) + "a residual block's output shape differs from its input's";
         return UN_ERR_INVALID;
       }
       e.res_from = res_open;
@@ -238,10 +239,20 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
         e.relu = true;
         ++i;
       }
+      if (i < s.n_layers && s.layers[i].op == UN_MAXPOOL2) {
+        why = where(i) + "max-pool of a residual sum is not supported";
+        return UN_ERR_UNSUPPORTED;
+      }
       continue;
     }
-    if (res_open >= 0 && L.op != UN_LINEAR && L.op != UN_RELU) {
-      why = where(i) + "a residual block may enclose only Linear and ReLU layers";
+    if (res_open >= 0 && L.op != UN_LINEAR && L.op != UN_CONV2D && L.op != UN_RELU) {
+      why = where(i) + "a residual block may enclose only Linear, Conv2d and ReLU layers";
+      return UN_ERR_UNSUPPORTED;
+    }
+    if (res_open >= 0 && L.op == UN_CONV2D && i + 1 < s.n_layers &&
+        (s.layers[i + 1].op == UN_MAXPOOL2 ||
+         (s.layers[i + 1].op == UN_RELU && i + 2 < s.n_layers && s.layers[i + 2].op == UN_MAXPOOL2))) {
+      why = where(i) + "a residual block may not enclose a max-pool";
       return UN_ERR_UNSUPPORTED;
     }
     if (L.op == UN_CONV2D) {
@@ -639,7 +650,7 @@ static void build_tables(un_ctx* c, Tables& T) {
       size_t b0 = po + k * sizeof(ConvProb);
       for (size_t f : {offsetof(ConvProb, X), offsetof(ConvProb, Wt), offsetof(ConvProb, bias), offsetof(ConvProb, P),
                        offsetof(ConvProb, amax), offsetof(ConvProb, G), offsetof(ConvProb, gam),
-                       offsetof(ConvProb, Gprev), offsetof(ConvProb, ws)})
+                       offsetof(ConvProb, Gprev), offsetof(ConvProb, ws), offsetof(ConvProb, R)})
         fix.push_back(b0 + f);
     }
     size_t mo = put(map.data(), map.size() * 4);
@@ -766,6 +777,7 @@ static void build_tables(un_ctx* c, Tables& T) {
         p.bias = (const float*)ptr(b.b32);
         p.P = ptr(b.Y);
         p.amax = (uint8_t*)ptr(b.amax);
+        if (b.res_from >= 0) p.R = ptr(m.blocks[b.res_from].X);
         plan_halo(p, bf, false);
         cp.push_back(p);
       }
@@ -921,6 +933,7 @@ static void build_tables(un_ctx* c, Tables& T) {
           p.G = ptr(b.G);
           p.gam = (const uint8_t*)ptr(b.amax);
           p.Gprev = ptr(pb.G);
+          if (b.res_to >= 0) p.R = ptr(m.blocks[b.res_to].G);
           plan_halo(p, bf, true);
           dp.push_back(p);
         }

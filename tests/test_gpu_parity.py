@@ -163,6 +163,36 @@ def test_halo_tiled_cnns(precision):
     _report(f"halo_cnns_{precision} run", compare_run(wl, run_gpu(wl, wl.steps), run_oracle(wl, wl.steps, m), m))
 
 
+_RES_CNNS = [
+    {"layers": [("conv", 16, 3, 1), ("relu",), ("pool",), ("res_begin",), ("conv", 16, 3, 1), ("relu",),
+                ("conv", 16, 3, 1), ("res_end",), ("relu",), ("conv", 8, 3, 1), ("relu",), ("pool",),
+                ("flatten",), ("linear", 10)], "num_classes": 10},
+    {"layers": [("conv", 24, 5, 2), ("res_begin",), ("conv", 24, 3, 1), ("res_end",), ("relu",),
+                ("conv", 8, 3, 1), ("pool",), ("flatten",), ("linear", 10)], "num_classes": 10},
+    {"layers": [("conv", 72, 3, 1), ("relu",), ("pool",), ("res_begin",), ("conv", 72, 3, 1), ("res_end",),
+                ("relu",), ("conv", 8, 1, 0), ("flatten",), ("linear", 10)], "num_classes": 10},
+    {"layers": [("conv", 8, 3, 1), ("relu",), ("pool",), ("flatten",), ("linear", 10)], "num_classes": 10},
+]
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
+@pytest.mark.parametrize("batch,in_shape", [(12, (3, 13, 16)), (6, (8, 16, 16))])
+def test_residual_cnns(precision, batch, in_shape):
+    """Residual conv blocks: the skip input joins in the conv forward
+    epilogue, the skip gradient in the data gradient's, on ragged maps and on
+    the row-tiled (halo) shapes, with 72 channels (more than one channel
+    block), a block input without ReLU and a plain model beside them. The
+    rate is small: these unnormalised residual nets diverge within three steps
+    at 0.05 (the oracle's own loss grows a thousandfold), and a diverging run
+    amplifies rounding-order differences without bound."""
+    _need_gpu()
+    wl = _custom(_RES_CNNS, batch, in_shape, precision, steps=3, lr=0.002)
+    m = range(wl.n_models)
+    tag = f"residual_cnns_{precision}_{batch}"
+    _report(f"{tag} 1 step", compare_step(wl, run_gpu(wl, 1), run_oracle(wl, 1, m), m))
+    _report(f"{tag} run", compare_run(wl, run_gpu(wl, wl.steps), run_oracle(wl, wl.steps, m), m))
+
+
 # ---------------------------------------------------------------------------
 # The paper's invariants on the device: no interference, merged == alone
 # ---------------------------------------------------------------------------

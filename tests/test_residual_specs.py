@@ -37,6 +37,34 @@ BAD = [
 ]
 
 
+C = lambda o, k=3, pad=1: ("conv", o, k, pad)
+POOL, FLAT = ("pool",), ("flatten",)
+
+GOOD_CNN = [
+    _spec(C(8), RELU, RB, C(8), RE, RELU, C(8), RELU, POOL, FLAT, L(5)),
+    _spec(C(8), RELU, POOL, RB, C(4), RELU, C(8), RE, RELU, RB, C(8, 1, 0), RE, FLAT, L(5)),
+]
+
+BAD_CNN = [
+    (_spec(C(8), RB, C(8), RE, RELU, POOL, FLAT, L(5)), U.UN_ERR_UNSUPPORTED),          # pool of the sum
+    (_spec(C(8), RB, C(8), RELU, POOL, C(8), RE, FLAT, L(5)), U.UN_ERR_UNSUPPORTED),    # pool inside
+    (_spec(C(8), RB, C(8, 3, 0), RE, FLAT, L(5)), U.UN_ERR_INVALID),                    # map shrinks
+    (_spec(C(8), RB, C(6), RE, FLAT, L(5)), U.UN_ERR_INVALID),                          # channels change
+    (_spec(C(8), FLAT, RB, L(5), RE, L(5)), U.UN_ERR_UNSUPPORTED),                      # after a flatten
+]
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
+def test_residual_conv_specs(precision):
+    _need_lib()
+    for s in GOOD_CNN:
+        assert U.un_plan_bytes([s], 4, (8, 8, 8), precision)[0] > 0
+    for s, status in BAD_CNN:
+        with pytest.raises(U.UnError) as e:
+            U.un_plan_bytes([s], 4, (8, 8, 8), precision)
+        assert e.value.status == status, s
+
+
 @pytest.mark.parametrize("precision", ["f32", "bf16"])
 def test_residual_specs_accepted(precision):
     _need_lib()
