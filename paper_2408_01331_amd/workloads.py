@@ -202,6 +202,30 @@ WORKLOADS = {
 }
 
 
+def resnet8(seed=0):
+    """N=8 small residual CNNs (ResNet-style: two-conv blocks with identity skips,
+    and one residual Linear block in the head) on 3x32x32, base widths from
+    {16, 32}, bf16, batch 64."""
+    rng = np.random.default_rng([seed, 4])
+    RB, RE, R = ("res_begin",), ("res_end",), ("relu",)
+    specs = []
+    for _ in range(8):
+        c = int(rng.choice([16, 32]))
+        h = int(rng.choice([64, 128]))
+        layers = [("conv", c, 3, 1), R, ("pool",),
+                  RB, ("conv", c, 3, 1), R, ("conv", c, 3, 1), RE, R,
+                  ("conv", 2 * c, 3, 1), R, ("pool",),
+                  RB, ("conv", 2 * c, 3, 1), R, ("conv", 2 * c, 3, 1), RE, R,
+                  ("conv", 2 * c, 3, 1), R, ("pool",), ("flatten",),
+                  ("linear", h), R, RB, ("linear", h), R, ("linear", h), RE, R, ("linear", 10)]
+        specs.append({"layers": layers, "num_classes": 10})
+    return Workload("resnet8_b64_bf16", 8, 64, (3, 32, 32), "bf16", specs, 0.001, 10, seed,
+                    "8 residual CNNs (two-conv identity blocks, widths {16,32}/{32,64}) on [64,3,32,32], bf16")
+
+
+WORKLOADS["resnet8"] = resnet8
+
+
 def get(name, seed=0) -> Workload:
     return WORKLOADS[name](seed)
 

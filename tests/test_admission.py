@@ -19,7 +19,7 @@ def _params(wl, idx):
     return sum(int(np.prod(s)) for i in idx for s, _ in W.param_shapes(wl.specs[i], wl.in_shape))
 
 
-@pytest.mark.parametrize("name", ["mlp8", "lenet4", "cifar16", "mlp64"])
+@pytest.mark.parametrize("name", ["mlp8", "lenet4", "cifar16", "mlp64", "resnet8"])
 def test_fused_footprint_is_one_input_plus_the_models(name):
     _need_lib()
     wl = W.get(name)

@@ -14,7 +14,7 @@ def _need_gpu():
     return torch
 
 
-@pytest.mark.parametrize("name", ["mlp2", "mlp8", "lenet4", "cifar16", "mlp64"])
+@pytest.mark.parametrize("name", ["mlp2", "mlp8", "lenet4", "cifar16", "mlp64", "resnet8"])
 def test_plan_bytes_equal_the_arena_and_the_device_allocation(name):
     torch = _need_gpu()
     from paper_2408_01331_amd import unifiednn as U

@@ -32,7 +32,8 @@ def _report(name, worst):
 # The configured number of steps, free running: see compare_run.
 # fp32 workloads check every model; bf16 ones sample models (all N still run).
 # ---------------------------------------------------------------------------
-ONE_STEP = [("mlp2", None), ("mlp8", None), ("lenet4", None), ("mlp64", [0, 17, 63]), ("cifar16", [3])]
+ONE_STEP = [("mlp2", None), ("mlp8", None), ("lenet4", None), ("mlp64", [0, 17, 63]), ("cifar16", [3]),
+            ("resnet8", [0, 5])]
 
 
 @pytest.mark.parametrize("name,sample", ONE_STEP, ids=[n for n, _ in ONE_STEP])
@@ -46,7 +47,7 @@ def test_one_step_strict(name, sample):
 
 
 RUNS = [("mlp2", None, None), ("mlp8", None, None), ("lenet4", None, None), ("mlp64", [0, 63], 3),
-        ("cifar16", [0, 9], 2)]
+        ("cifar16", [0, 9], 2), ("resnet8", [2, 7], 2)]
 
 
 @pytest.mark.parametrize("name,sample,steps", RUNS, ids=[n for n, _, _ in RUNS])
@@ -200,7 +201,7 @@ def _bitwise_equal(a, b):
     return all(np.array_equal(np.asarray(x).view(np.uint32), np.asarray(y).view(np.uint32)) for x, y in zip(a, b))
 
 
-@pytest.mark.parametrize("name", ["mlp8", "lenet4"])
+@pytest.mark.parametrize("name", ["mlp8", "lenet4", "resnet8"])
 def test_perturbing_one_model_leaves_the_others_bitwise_unchanged(name):
     _need_gpu()
     wl = W.get(name)
@@ -215,7 +216,7 @@ def test_perturbing_one_model_leaves_the_others_bitwise_unchanged(name):
         assert same == (i != j), f"model {i}: bitwise equality {same}, expected {i != j}"
 
 
-@pytest.mark.parametrize("name", ["mlp8", "lenet4"])
+@pytest.mark.parametrize("name", ["mlp8", "lenet4", "resnet8"])
 def test_merged_run_equals_each_model_alone_bitwise(name):
     _need_gpu()
     wl = W.get(name)
