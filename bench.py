@@ -1,6 +1,6 @@
 """Benchmark of the fused N-model training step on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload mlp64] [--also cifar16]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload mlp64] [--also cifar16,resnet8]
     python bench.py --copy-probe      # calibration copy for the HBM byte counters only
 
 Prints ONE JSON line. A step is one fused forward + softmax-CE + backward +
@@ -47,7 +47,9 @@ def algorithmic_work(wl):
     weight gradient; its gradient likewise; the weights the products read are
     read once per use (forward, data gradient); the fused update reads and
     writes the fp32 master (8 B per parameter) plus the bf16 copy (2 B) in bf16
-    mode. Returns (flops, bytes, n_params)."""
+    mode. A residual block adds one read of its input x (the forward of its
+    last layer) and one of its output gradient (the data gradient of its first
+    layer). Returns (flops, bytes, n_params)."""
     B = wl.batch
     es = 2 if wl.precision == "bf16" else 4
     upd = 10 if wl.precision == "bf16" else 8
@@ -60,6 +62,8 @@ def algorithmic_work(wl):
         layers = spec["layers"]
         for li, layer in enumerate(layers):
             op = layer[0]
+            ends = li + 1 < len(layers) and layers[li + 1][0] == "res_end"
+            begins = li > 0 and layers[li - 1][0] == "res_begin"
             if op == "linear":
                 K = int(np.prod(shape))
                 N = layer[1]
@@ -74,6 +78,8 @@ def algorithmic_work(wl):
                     nbytes["gemm_bwd"] += B * N * es + N * K * es + B * K * es
                 if last:                                                 # softmax-CE: logits in, dZ out
                     nbytes["ce"] += B * N * 4 + B * N * es
+                nbytes["gemm_fwd"] += B * N * es if ends else 0          # skip input
+                nbytes["gemm_bwd"] += B * K * es if begins else 0        # skip gradient
                 n_params += K * N + N
                 shape = (N,)
                 first = False
@@ -96,6 +102,8 @@ def algorithmic_work(wl):
                 if not first:
                     flops["conv_dgrad"] += f
                     nbytes["conv_dgrad"] += out_b + w_b + in_b
+                nbytes["conv_fwd"] += out_el * es if ends else 0         # skip input
+                nbytes["conv_dgrad"] += in_b if begins else 0            # skip gradient
                 n_params += O * C * k * k + O
                 shape = (O, OH, OW)
                 first = False
@@ -277,7 +285,8 @@ def measure(wl, steps, warmup):
         roof = {"bound": "mfma", "achieved": achieved, "peak": mfma_peak, "unit": "TFLOP/s"}
     roof["frac"] = roof["achieved"] / roof["peak"]
     kname = f"{dom}_{wl.precision}"
-    traffic, tpath = measured_traffic(kname, wl.name)
+    # counter summaries are named for the kernel and the workload's short name (mlp64, cifar16, ...)
+    traffic, tpath = measured_traffic(kname, wl.name.split("_")[0])
     roof["traffic"] = traffic
     roof["traffic_unit"] = "bytes per launch (HBM, rocprofv3 FETCH_SIZE + WRITE_SIZE scaled by a plain copy)"
     roof["kernel"] = dom
@@ -315,7 +324,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="mlp64", choices=list(W.WORKLOADS))
-    ap.add_argument("--also", default="cifar16",
+    ap.add_argument("--also", default="cifar16,resnet8",
                     help="comma-separated workloads also timed and reported under other_workloads ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
