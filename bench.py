@@ -122,7 +122,7 @@ def run_gpu(wl, steps, warmup):
     torch.cuda.set_device(0)
     h = U.Hybrid(wl.specs, wl.batch, wl.in_shape, wl.precision)
     for i in range(wl.n_models):
-        h.set_params(i, U.flatten_params(W.init_params(wl.specs[i], wl.in_shape, wl.seed, i)))
+        h.set_params(i, U.flatten_params(W.init_params(wl.specs[i], wl.in_shape, wl.seed, i, wl.init)))
     x, y = W.make_batch(wl, 0)
     h.load_batch(x, y)                       # resident in HBM before timing
     for _ in range(warmup):
@@ -163,7 +163,7 @@ def run_unfused(wl, steps, warmup):
     x, y = W.make_batch(wl, 0)
     for i in range(wl.n_models):
         h = U.Hybrid([wl.specs[i]], wl.batch, wl.in_shape, wl.precision)
-        h.set_params(0, U.flatten_params(W.init_params(wl.specs[i], wl.in_shape, wl.seed, i)))
+        h.set_params(0, U.flatten_params(W.init_params(wl.specs[i], wl.in_shape, wl.seed, i, wl.init)))
         h.load_batch(x, y)
         hs.append(h)
     for _ in range(warmup):
@@ -237,7 +237,7 @@ def cpu_baseline(wl, budget_s=12.0):
     while True:
         i = done % wl.n_models
         if i not in params:
-            params[i] = W.init_params(wl.specs[i], wl.in_shape, wl.seed, i)
+            params[i] = W.init_params(wl.specs[i], wl.in_shape, wl.seed, i, wl.init)
         oracle.step(wl.specs[i], params[i], x, y, wl.lr, wl.precision)
         done += 1
         if time.perf_counter() - t0 > budget_s:

@@ -53,6 +53,7 @@ class Workload:
     seed: int = 0
     description: str = ""
     extra: dict = field(default_factory=dict)
+    init: str = "kaiming"    # weight init rule of init_params
 
     @property
     def num_classes(self):
@@ -98,12 +99,17 @@ def param_shapes(spec, in_shape):
     return out
 
 
-def init_params(spec, in_shape, seed, model_index):
-    """Kaiming/He-uniform weights U(+-sqrt(6/fan_in)), biases U(+-1/sqrt(fan_in)), fp32."""
+def init_params(spec, in_shape, seed, model_index, rule="kaiming"):
+    """Initial parameters, fp32: biases U(+-1/sqrt(fan_in)); weights
+    U(+-sqrt(6/fan_in)) (Kaiming/He uniform, rule "kaiming") or U(+-1/sqrt(fan_in))
+    (rule "torch", the bound of PyTorch's own Linear / Conv2d initialisation)."""
+    if rule not in ("kaiming", "torch"):
+        raise ValueError(f"unknown init rule {rule!r}")
     rng = np.random.default_rng([seed, 1, model_index])
     params = []
     for shape, fan_in in param_shapes(spec, in_shape):
-        bound = math.sqrt(6.0 / fan_in) if len(shape) > 1 else 1.0 / math.sqrt(fan_in)
+        wbound = math.sqrt(6.0 / fan_in) if rule == "kaiming" else 1.0 / math.sqrt(fan_in)
+        bound = wbound if len(shape) > 1 else 1.0 / math.sqrt(fan_in)
         params.append(rng.uniform(-bound, bound, size=shape).astype(np.float32))
     return params
 
@@ -219,8 +225,13 @@ def resnet8(seed=0):
                   ("conv", 2 * c, 3, 1), R, ("pool",), ("flatten",),
                   ("linear", h), R, RB, ("linear", h), R, ("linear", h), RE, R, ("linear", 10)]
         specs.append({"layers": layers, "num_classes": 10})
-    return Workload("resnet8_b64_bf16", 8, 64, (3, 32, 32), "bf16", specs, 0.001, 10, seed,
-                    "8 residual CNNs (two-conv identity blocks, widths {16,32}/{32,64}) on [64,3,32,32], bf16")
+    # PyTorch's default bound: with Kaiming-uniform weights these unnormalised
+    # residual nets start at a loss of 11-34 (logits up to 55) and train
+    # chaotically in bf16 (a 1-ulp change of the parameters moves the loss by
+    # 2 % within four steps); with this bound they start near ln 10.
+    return Workload("resnet8_b64_bf16", 8, 64, (3, 32, 32), "bf16", specs, 0.01, 10, seed,
+                    "8 residual CNNs (two-conv identity blocks, widths {16,32}/{32,64}) on [64,3,32,32], bf16",
+                    init="torch")
 
 
 WORKLOADS["resnet8"] = resnet8
@@ -234,4 +245,4 @@ def shrink(wl: Workload, n_models=None, batch=None) -> Workload:
     """Same architecture draws on fewer models or a smaller batch (for quick parity cases)."""
     specs = wl.specs if n_models is None else wl.specs[:n_models]
     return Workload(wl.name + "_small", len(specs), batch or wl.batch, wl.in_shape,
-                    wl.precision, specs, wl.lr, wl.steps, wl.seed, wl.description)
+                    wl.precision, specs, wl.lr, wl.steps, wl.seed, wl.description, init=wl.init)

@@ -14,12 +14,22 @@ import numpy as np
 import oracle
 from paper_2408_01331_amd import workloads as W
 
+# The gate: max relative error on losses and parameters.
 TOL = {"f32": 1e-4, "bf16": 2e-2}
+# Extras of multi-step runs (updates theta_k - theta_0 and the last step's
+# gradient, Frobenius) are bounded by SENS_FACTOR times what the oracle itself
+# does under a 1-ulp change of its first step's parameters (oracle_sensitivity),
+# and never tighter than the gate.
+SENS_FACTOR = 4.0
+# Bound of the extras when no sensitivity run is given.
 UPDATE_TOL = {"f32": 1e-2, "bf16": 0.2}
+# A flipped decision changes one sample's contribution to the flagged unit's
+# gradient; those parameters are held to this bound instead of the strict one.
+FLAGGED_TOL = 1e-2
 
 
 def theta0(wl, i):
-    return W.init_params(wl.specs[i], wl.in_shape, wl.seed, i)
+    return W.init_params(wl.specs[i], wl.in_shape, wl.seed, i, wl.init)
 
 
 def run_gpu(wl, steps, lr=None, theta=None, models=None):
@@ -48,11 +58,56 @@ def run_gpu(wl, steps, lr=None, theta=None, models=None):
     return np.array(losses), params, grads
 
 
-def run_oracle(wl, steps, models, lr=None, theta=None):
+def perturb_ulp(params, seed):
+    """Move a random half of the elements of each tensor by one fp32 ulp, up or
+    down at random (an input transformation: no arithmetic of the method)."""
+    rng = np.random.default_rng([seed, 77])
+    out = []
+    for p in params:
+        p = np.asarray(p, dtype=np.float32)
+        pick = rng.random(p.shape) < 0.5
+        toward = np.where(rng.random(p.shape) < 0.5, np.inf, -np.inf).astype(np.float32)
+        out.append(np.where(pick, np.nextafter(p, toward), p).astype(np.float32))
+    return out
+
+
+def oracle_sensitivity(spec, th0, batches, lr, mode, flags, ref):
+    """What the oracle does to itself when its parameters after the first step
+    move by one fp32 ulp (perturb_ulp), carried through the remaining steps:
+    per tensor, the Frobenius relative change of the update theta_k - theta_0
+    and of the last step's gradient over the units `flags` never marked, and
+    the per-step loss change. `ref` = (losses, params, grads) of the
+    unperturbed run. A bf16 run's stored values are discrete: such a change
+    flips roundings (and ReLU / pool decisions) that compound over steps, so
+    this is the scale below which no evaluation order can be told apart from
+    another. Returns {} for a one-step run."""
+    if len(batches) < 2:
+        return {}
+    x, y = batches[0]
+    _, p1, _ = oracle.step(spec, th0, x, y, lr, mode)
+    loss_p, p, g = oracle.train(spec, perturb_ulp(p1, 1), batches[1:], lr, mode)
+    masks = flagged_masks(spec, ref[1], flags)
+    upd, grd = [], []
+    for t, (a, b, ga, gb, t0) in enumerate(zip(p, ref[1], g, ref[2], th0)):
+        keep = ~masks[t]
+        upd.append(fro_err((np.asarray(a, np.float64) - t0)[keep], (np.asarray(b, np.float64) - t0)[keep]))
+        grd.append(fro_err(np.asarray(ga)[keep], np.asarray(gb)[keep]))
+    loss = np.abs(np.asarray(loss_p) - ref[0][1:]) / np.abs(ref[0][1:])
+    return {"update_fro": upd, "grad_fro": grd, "loss": [0.0] + loss.tolist()}
+
+
+def run_oracle(wl, steps, models, lr=None, theta=None, sensitivity=False):
+    """Each listed model trained alone by the oracle. Returns {i: (losses,
+    params, grads, flags)} or, with sensitivity, also {i: oracle_sensitivity}."""
     lr = wl.lr if lr is None else lr
     batches = [W.make_batch(wl, s) for s in range(steps)]
     th = {i: (theta0(wl, i) if theta is None or i not in theta else theta[i]) for i in range(wl.n_models)}
-    return oracle.train_models(wl.specs, th, batches, lr, wl.precision, models=models, with_flags=True)
+    out = oracle.train_models(wl.specs, th, batches, lr, wl.precision, models=models, with_flags=True)
+    if not sensitivity:
+        return out
+    sens = {i: oracle_sensitivity(wl.specs[i], th[i], batches, lr, wl.precision, out[i][3], out[i][:3])
+            for i in out}
+    return out, sens
 
 
 def tensor_err(a, b, mask=None):
@@ -67,32 +122,58 @@ def tensor_err(a, b, mask=None):
     return float(np.max(d) / den) if den > 0 else float(np.max(d))
 
 
-def flagged_masks(params, flags):
-    """Per tensor, True where a parameter belongs to an output unit whose ReLU or
-    max-pool decision the oracle found ill-conditioned in fp32: the unit's weight
-    row and bias entry, and the next layer's weights that read the unit (its
-    input column, input channel, or the block of flattened features of that
-    channel). After a flip those parameters drift apart for the remaining steps."""
+def _param_layers(spec):
+    """The parameterised layers of a spec, in order, and for each one whose
+    output starts a residual block the index (in that order) of the block's
+    last parameterised layer, whose output is the residual sum."""
+    L = spec["layers"]
+    plist = [li for li, l in enumerate(L) if l[0] in ("linear", "conv")]
+    skip_end = {}
+    for k, li in enumerate(plist):
+        nxt = plist[k + 1] if k + 1 < len(plist) else len(L)
+        if any(L[j][0] == "res_begin" for j in range(li + 1, nxt)):
+            j = nxt
+            while L[j][0] != "res_end":
+                j += 1
+            skip_end[k] = plist.index(max(p for p in plist if p < j))
+    return plist, skip_end
+
+
+def flagged_masks(spec, params, flags):
+    """Per tensor, True where a parameter belongs to, or reads, an output unit
+    whose ReLU or max-pool decision the oracle found ill-conditioned in fp32.
+    For a flagged unit u of a layer: the layer's weight row and bias entry u,
+    and the next layer's weights that read u (its input column, input channel,
+    or the block of flattened features of that channel). When the layer's
+    output is the input of a residual block, u also reaches the block's sum
+    through the skip: the block's last layer's row and bias u are marked, and
+    so is everything that reads the sum's unit u, recursively (back-to-back
+    blocks). After a flip those parameters drift apart for the remaining steps."""
     masks = [np.zeros(np.shape(p), dtype=bool) for p in params]
-    for wi, units in flags.items():
-        nxt = wi + 2 if wi + 2 < len(params) else None
-        for u in units:
-            masks[wi][u, ...] = True
-            masks[wi + 1][u] = True
-            if nxt is None:
-                continue
+    plist, skip_end = _param_layers(spec)
+
+    def mark(k, u, seen):
+        if (k, u) in seen:
+            return
+        seen.add((k, u))
+        wi = 2 * k
+        masks[wi][u, ...] = True
+        masks[wi + 1][u] = True
+        if k + 1 < len(plist):
+            nxt = wi + 2
             Wn = params[nxt]
             if np.ndim(Wn) == 4 or np.ndim(params[wi]) == 2:
                 masks[nxt][:, u, ...] = True
             else:  # conv -> flatten -> linear: channel u owns a contiguous block of features
                 S = np.shape(Wn)[1] // np.shape(params[wi])[0]
                 masks[nxt][:, u * S:(u + 1) * S] = True
+        if k in skip_end:
+            mark(skip_end[k], u, seen)
+
+    for wi, units in flags.items():
+        for u in units:
+            mark(wi // 2, u, set())
     return masks
-
-
-# A flipped decision changes one sample's contribution to the flagged unit's
-# gradient; those parameters are held to this bound instead of the strict one.
-FLAGGED_TOL = 1e-2
 
 
 def fro_err(a, b):
@@ -121,7 +202,7 @@ def compare_step(wl, gpu, orc, models, tol=None):
         losses_o, params_o, grads_o, flags = orc[i]
         _losses(wl, losses_g, i, losses_o, tol, worst)
         th0 = theta0(wl, i)
-        fm = flagged_masks(params_o, flags)
+        fm = flagged_masks(wl.specs[i], params_o, flags)
         worst["flagged_units"] += sum(len(v) for v in flags.values())
         for t, (pg, po, gg, go) in enumerate(zip(params_g[i], params_o, grads_g[i], grads_o)):
             strict = ~fm[t]
@@ -136,44 +217,53 @@ def compare_step(wl, gpu, orc, models, tol=None):
     return worst
 
 
-def compare_run(wl, gpu, orc, models, tol=None, update_tol=None):
-    """k free-running steps. Once one fp32 decision has legitimately come out the
-    other way, the trajectories differ by a few ulps of a single unit, which can
-    tip further near-zero decisions; no fp32 order of evaluation can bound the
-    per-element error of every parameter after many steps. So:
-      losses: max relative error <= tol at every step;
-      parameters: Frobenius relative error <= tol per tensor, and per-element
-        max relative error <= FLAGGED_TOL (guard against localised gross errors);
-      updates theta_k - theta_0 and last-step gradients: Frobenius relative
-        error <= update_tol per tensor (UPDATE_TOL by default), over the
-        parameters of units the oracle did not flag. A flipped decision at a
-        flagged unit changes one sample's share of that unit's gradient; an
-        optimizer that normalises the step per element (Adam) turns that into
-        a change of the whole step of those parameters, however small the
-        share, so their updates are held by the per-element guard only.
-    """
+def extra_bound(wl, sens, i, key, t):
+    """Bound of a multi-step extra (update or gradient, Frobenius) of model i's
+    tensor t: SENS_FACTOR times the oracle's own change under a 1-ulp
+    perturbation, never below the gate; UPDATE_TOL without a sensitivity run."""
+    if sens is None or i not in sens or not sens[i]:
+        return UPDATE_TOL[wl.precision]
+    return max(TOL[wl.precision], SENS_FACTOR * sens[i][key][t])
+
+
+def compare_run(wl, gpu, orc, models, tol=None, sens=None):
+    """k free-running steps against the oracle that trained each model alone.
+
+    The gate (the stated metric): losses within `tol` relative error at every
+    step, and every parameter tensor within max |a - b| / max |b| <= tol over
+    the units the oracle never flagged in any step; the parameters of flagged
+    units within FLAGGED_TOL (once an fp32 decision has legitimately come out
+    the other way, the trajectories of those units part by more than rounding).
+
+    Extras, Frobenius relative error over the never-flagged units: the update
+    theta_k - theta_0 and the last step's gradient, each within extra_bound
+    (the oracle's own sensitivity, measured in the same test when `sens` is
+    given). Returns the worst values, and for the extras their worst ratio to
+    the bound."""
     tol = TOL[wl.precision] if tol is None else tol
-    # One flipped decision moves its unit's row of one step's update by a few
-    # per cent (Frobenius share ~1e-3); bf16 storage adds 1-ulp activation
-    # differences that compound over steps. Kernel-level gradient accuracy is
-    # held to `tol` by compare_step.
-    update_tol = UPDATE_TOL[wl.precision] if update_tol is None else update_tol
     losses_g, params_g, grads_g = gpu
-    worst = {"loss": 0.0, "param_fro": 0.0, "param_max": 0.0, "update_fro": 0.0, "grad_fro": 0.0,
-             "flagged_units": 0}
+    worst = {"loss": 0.0, "param_max": 0.0, "flagged_param": 0.0, "update_fro": 0.0, "grad_fro": 0.0,
+             "extra_vs_bound": 0.0, "flagged_units": 0}
     for i in models:
         losses_o, params_o, grads_o, flags = orc[i]
         _losses(wl, losses_g, i, losses_o, tol, worst)
         worst["flagged_units"] += sum(len(v) for v in flags.values())
         th0 = theta0(wl, i)
-        fm = flagged_masks(params_o, flags)
+        fm = flagged_masks(wl.specs[i], params_o, flags)
         for t, (pg, po, gg, go) in enumerate(zip(params_g[i], params_o, grads_g[i], grads_o)):
             keep = ~fm[t]
+            e = tensor_err(pg, po, keep)
+            worst["param_max"] = max(worst["param_max"], e)
+            assert e <= tol, f"model {i} tensor {t}: param max rel err {e:.3g} > {tol} (never-flagged units)"
+            if fm[t].any():
+                ef = tensor_err(pg, po, fm[t])
+                worst["flagged_param"] = max(worst["flagged_param"], ef)
+                assert ef <= FLAGGED_TOL, f"model {i} tensor {t}: flagged param err {ef:.3g} > {FLAGGED_TOL}"
             ug, uo = np.asarray(pg - th0[t])[keep], np.asarray(po - th0[t])[keep]
-            checks = (("param_fro", fro_err(pg, po), tol), ("param_max", tensor_err(pg, po), FLAGGED_TOL),
-                      ("update_fro", fro_err(ug, uo), update_tol),
-                      ("grad_fro", fro_err(np.asarray(gg)[keep], np.asarray(go)[keep]), update_tol))
-            for key, e, bound in checks:
-                worst[key] = max(worst[key], e)
-                assert e <= bound, f"model {i} tensor {t}: {key} {e:.3g} > {bound}"
+            for key, err in (("update_fro", fro_err(ug, uo)),
+                             ("grad_fro", fro_err(np.asarray(gg)[keep], np.asarray(go)[keep]))):
+                bound = extra_bound(wl, sens, i, key, t)
+                worst[key] = max(worst[key], err)
+                worst["extra_vs_bound"] = max(worst["extra_vs_bound"], err / bound)
+                assert err <= bound, f"model {i} tensor {t}: {key} {err:.3g} > {bound:.3g}"
     return worst

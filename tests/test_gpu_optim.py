@@ -11,13 +11,15 @@ import numpy as np
 import pytest
 
 from paper_2408_01331_amd import workloads as W
-from _parity import UPDATE_TOL, compare_run, flagged_masks, fro_err, theta0
+from _parity import TOL, UPDATE_TOL, compare_run, flagged_masks, fro_err, tensor_err, theta0
 
 pytestmark = pytest.mark.gpu
 
 # Adam moves every weight by about lr per step whatever the gradient's size, so
-# a gradient element within fp32 rounding of zero may move either way; lr is
-# kept small enough that such an element stays inside the per-element guard.
+# a gradient element within rounding of zero may move either way. In the
+# multi-step runs below the rate is kept small enough that such an element
+# stays inside the bound of flagged parameters; test_optimizer_step_strict
+# compares one step at the workload's own rate with those elements flagged.
 OPTS = [dict(kind="sgd"), dict(kind="momentum", momentum=0.9),
         dict(kind="adam", betas=(0.9, 0.999), eps=1e-8, lr_scale=0.005)]
 
@@ -130,7 +132,7 @@ def test_mixed_optimizers_match_the_oracle(name, models):
         # optimizer state: momentum buffer or Adam's moments, per tensor, over
         # the parameters of units the oracle did not flag (as the updates)
         s, n = states[i][0], params[i].size
-        fm = flagged_masks(orc[1], orc[3])
+        fm = flagged_masks(wl.specs[i], orc[1], orc[3])
         worst["state_fro"] = 0.0
         for k, key in enumerate(("s1", "s2")[: s.size // n]):
             for t, (a, b) in enumerate(zip(split_params(s[k * n:(k + 1) * n], shapes), st[key])):
@@ -139,6 +141,102 @@ def test_mixed_optimizers_match_the_oracle(name, models):
                 assert e <= UPDATE_TOL[wl.precision], f"model {i} {key} tensor {t}: {e:.3g}"
         print(f"\n[{wl.name} model {i} {_opt(i)['kind']}] " + ", ".join(f"{k}={v:.3g}" for k, v in worst.items()),
               flush=True)
+
+
+def _flat_state(st, key, shapes):
+    return np.concatenate([np.asarray(a, np.float32).ravel() for a in st[key]])
+
+
+def _oracle_update(o, lr, params, grads, st):
+    """The oracle's optimizer step of one model (fp32 mode): new params and state."""
+    import oracle
+    if o["kind"] == "momentum":
+        p, b = oracle.momentum_update(params, grads, st["s1"], lr, o["momentum"], "f32")
+        return p, {"t": st["t"] + 1, "s1": b}
+    b1, b2 = o["betas"]
+    p, m, v = oracle.adam_update(params, grads, st["s1"], st["s2"], st["t"] + 1, lr, b1, b2, o["eps"], "f32")
+    return p, {"t": st["t"] + 1, "s1": m, "s2": v}
+
+
+@pytest.mark.parametrize("kind", ["momentum", "adam"])
+@pytest.mark.parametrize("name,models", [("mlp8", None), ("lenet4", None), ("mlp64_8", [0, 3, 7]),
+                                         ("cifar16_4", [0, 3])])
+def test_optimizer_step_strict(name, models, kind):
+    """One step of momentum / Adam at the workload's own rate, both sides from
+    the oracle's parameters and optimizer state after a first step (injected
+    into the library with un_set_params / un_set_opt_state): loss, gradient,
+    new parameters, update and new state within the gate per tensor (max
+    relative error). Flagged: the oracle's ill-conditioned ReLU / pool units,
+    and elements whose update is an ill-conditioned function of the gradient
+    at the gradient's own tolerance eps = tol * max|g| (the oracle's update at
+    g - eps or g + eps moves by more than tol * max|update|; for Adam, the
+    elements whose gradient is within eps of a sign change); those are held
+    to the oracle's own spread over [g - eps, g + eps]."""
+    _need_gpu()
+    import oracle
+    from paper_2408_01331_amd.unifiednn import Hybrid, flatten_params, split_params
+    wl = _case(name)
+    tol = TOL[wl.precision]
+    o = {"kind": kind, "momentum": 0.9, "betas": (0.9, 0.999), "eps": 1e-8}
+    models = list(range(wl.n_models)) if models is None else models
+    x0, y0 = W.make_batch(wl, 0)
+    x1, y1 = W.make_batch(wl, 1)
+    start = {}
+    for i in range(wl.n_models):
+        _, p1, _, st1 = oracle.step_opt(wl.specs[i], theta0(wl, i), x0, y0, wl.lr, o, {}, wl.precision)
+        start[i] = (p1, st1)
+    with Hybrid(wl.specs, wl.batch, wl.in_shape, wl.precision) as h:
+        h.keep_grads(True)
+        for i in range(wl.n_models):
+            p1, st1 = start[i]
+            h.set_params(i, flatten_params(p1))
+            _set(h, i, o)
+            keys = ("s1",) if kind == "momentum" else ("s1", "s2")
+            h.set_opt_state(i, np.concatenate([_flat_state(st1, k, None) for k in keys]), st1["t"])
+        h.load_batch(x1, y1)
+        losses = h.step(wl.lr)
+        got = {i: (h.get_params(i), h.get_grads(i), h.get_opt_state(i)) for i in models}
+    worst = {"loss": 0.0, "param": 0.0, "update": 0.0, "grad": 0.0, "state": 0.0, "ill_elements": 0,
+             "ill_param": 0.0}
+    for i in models:
+        p1, st1 = start[i]
+        flags = {}
+        lo, p2, g2, st2 = oracle.step_opt(wl.specs[i], p1, x1, y1, wl.lr, o, st1, wl.precision, flags)
+        le = abs(losses[i] - lo) / abs(lo)
+        worst["loss"] = max(worst["loss"], le)
+        assert le <= tol, f"model {i}: loss {losses[i]} vs {lo}"
+        shapes = [sh for sh, _ in W.param_shapes(wl.specs[i], wl.in_shape)]
+        pg, gg = split_params(got[i][0], shapes), split_params(got[i][1], shapes)
+        n = got[i][0].size
+        sg = [split_params(got[i][2][0][k * n:(k + 1) * n], shapes) for k in range(len(st2) - 1)]
+        assert got[i][2][1] == st2["t"] == 2
+        fm = flagged_masks(wl.specs[i], p2, flags)
+        # the update's own conditioning at the gradient's tolerance
+        eps = [tol * np.max(np.abs(g)) for g in g2]
+        lo_p, _ = _oracle_update(o, wl.lr, p1, [np.asarray(g) - e for g, e in zip(g2, eps)], st1)
+        hi_p, _ = _oracle_update(o, wl.lr, p1, [np.asarray(g) + e for g, e in zip(g2, eps)], st1)
+        for t in range(len(p2)):
+            u_o = np.asarray(p2[t], np.float64) - p1[t]
+            spread = np.maximum(np.abs(np.asarray(lo_p[t], np.float64) - p2[t]),
+                                np.abs(np.asarray(hi_p[t], np.float64) - p2[t]))
+            ill = spread > tol * np.max(np.abs(u_o))
+            keep = ~fm[t] & ~ill
+            worst["ill_elements"] += int(np.count_nonzero(ill & ~fm[t]))
+            checks = [("param", pg[t], p2[t]), ("update", np.asarray(pg[t], np.float64) - p1[t], u_o),
+                      ("grad", gg[t], g2[t])]
+            checks += [("state", sg[k][t], st2[key][t]) for k, key in enumerate(("s1", "s2")[:len(sg)])]
+            for key, a, b in checks:
+                mask = ~fm[t] if key == "grad" else keep
+                e = tensor_err(a, b, mask)
+                worst[key] = max(worst[key], e)
+                assert e <= tol, f"model {i} tensor {t}: {key} err {e:.3g} > {tol}"
+            sel = ill & ~fm[t]
+            if sel.any():
+                d = np.abs(np.asarray(pg[t], np.float64) - p2[t])[sel]
+                assert np.all(d <= 1.5 * spread[sel] + tol * np.max(np.abs(u_o))), f"model {i} tensor {t}: ill"
+                worst["ill_param"] = max(worst["ill_param"], float(np.max(d / (spread[sel] + 1e-30))))
+    print(f"\n[{wl.name} {kind} one step at lr {wl.lr}] " + ", ".join(f"{k}={v:.3g}" for k, v in worst.items()),
+          flush=True)
 
 
 def test_adam_counts_only_the_steps_a_model_takes():

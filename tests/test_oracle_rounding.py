@@ -106,7 +106,7 @@ def reference_step(spec, params, x, y, mode):
     logits = grad_round(h, store)             # dL/dz stored fp32 before the last layer reads it
     loss = F.cross_entropy(logits, torch.tensor(np.asarray(y, dtype=np.int64)))
     loss.backward()
-    return float(loss), [_round(p.grad, store).numpy() for p in ps]
+    return float(loss.detach()), [_round(p.grad, store).numpy() for p in ps]
 
 
 def oracle_step(spec, params, x, y, mode):
