@@ -43,6 +43,13 @@ Precision modes:
   softmax-CE arithmetic, all accumulators, dW, db and the fp32 master weights
   stay fp32. Because ReLU, max-pool, flatten and their backward passes are
   exact, rounding at the reader equals rounding the stored tensor.
+
+Accumulation (``acc``): ``"f64"`` (the default, the reference) sums every dot
+product exactly enough to be rounded once; ``"f32"`` evaluates the same
+products and the softmax cross-entropy in fp32 arithmetic (float32 BLAS, its
+own summation order). Both are evaluation orders the reading allows, and
+their difference measures how far two correct implementations of the same
+step may legitimately lie apart.
 """
 from __future__ import annotations
 
@@ -102,10 +109,22 @@ def fma32(a, b, c):
 
 
 class _Mode:
-    def __init__(self, mode):
+    def __init__(self, mode, acc="f64"):
         if mode not in ("f64", "f32", "bf16"):
             raise ValueError(f"unknown precision mode {mode!r}")
+        if acc not in ("f64", "f32"):
+            raise ValueError(f"unknown accumulation {acc!r}")
         self.mode = mode
+        self.acc = acc
+
+    def run(self, fn, *arrays, **kw):
+        """A layer function on fp64 arrays, or in fp32 arithmetic when acc is "f32"."""
+        if self.acc == "f64":
+            return fn(*arrays, **kw)
+        out = fn(*[a.astype(F32) if isinstance(a, np.ndarray) else a for a in arrays], **kw)
+        if isinstance(out, tuple):
+            return tuple(None if o is None else np.asarray(o, dtype=F64) for o in out)
+        return np.asarray(out, dtype=F64)
 
     def operand(self, a):
         """A tensor as a Linear/Conv layer reads it (activation, weight or gradient)."""
@@ -214,13 +233,15 @@ def maxpool2_bwd(dout, am, in_shape):
     return dh
 
 
-def softmax_ce(z, y):
+def softmax_ce(z, y, dtype=F64):
     """Mean softmax cross-entropy and its gradient.
 
     L = (1/B) sum_b (lse(z_b) - z_{b,y_b}), lse(z) = m + log sum exp(z - m);
-    dL/dz = (softmax(z) - onehot(y)) / B.
+    dL/dz = (softmax(z) - onehot(y)) / B. `dtype` is the arithmetic (float64,
+    or float32 for the fp32 evaluation order); the gradient is returned in
+    float64 either way.
     """
-    z = np.asarray(z, dtype=F64)
+    z = np.asarray(z, dtype=dtype)
     B = z.shape[0]
     m = z.max(axis=1, keepdims=True)
     e = np.exp(z - m)
@@ -230,7 +251,7 @@ def softmax_ce(z, y):
     loss = float(np.mean(lse - z[rows, y]))
     p = e / s
     p[rows, y] -= 1.0
-    return loss, p / B
+    return loss, np.asarray(p / dtype(B), dtype=F64)
 
 
 # ---------------------------------------------------------------------------
@@ -265,7 +286,7 @@ def count_params(spec, in_shape):
 U32 = 2.0 ** -24
 
 
-def forward(spec, params, x, mode="f32", flags=None):
+def forward(spec, params, x, mode="f32", flags=None, acc="f64"):
     """Forward pass. Returns (logits as stored, cache for backward).
 
     If `flags` (a dict) is given, it receives, per parameterised layer (keyed by
@@ -276,7 +297,7 @@ def forward(spec, params, x, mode="f32", flags=None):
     Such a decision may legitimately come out either way in any fp32
     evaluation order; everything else is decided identically.
     """
-    R = _Mode(mode)
+    R = _Mode(mode, acc)
     h = np.asarray(x, dtype=F64)
     cache = []
     pi = 0
@@ -290,7 +311,7 @@ def forward(spec, params, x, mode="f32", flags=None):
             hin, Wq = R.operand(h), R.operand(W)
             if hin.ndim != 2:
                 raise ValueError("linear layer needs a 2-D input (add a flatten)")
-            z = linear_fwd(hin, Wq, np.asarray(b, dtype=F64))
+            z = R.run(linear_fwd, hin, Wq, np.asarray(b, dtype=F64))
             ends_block = li + 1 < len(layers) and layers[li + 1][0] == "res_end"
             if ends_block:
                 # the residual sum is the stored tensor: x joins before rounding
@@ -317,7 +338,7 @@ def forward(spec, params, x, mode="f32", flags=None):
         elif op == "conv":
             W, b = params[pi], params[pi + 1]
             hin, Wq = R.operand(h), R.operand(W)
-            z = conv2d_fwd(hin, Wq, np.asarray(b, dtype=F64), layer[3])
+            z = R.run(conv2d_fwd, hin, Wq, np.asarray(b, dtype=F64), layer[3])
             ends_block = li + 1 < len(layers) and layers[li + 1][0] == "res_end"
             if ends_block:
                 if skip is None or skip.shape != z.shape:
@@ -362,9 +383,9 @@ def forward(spec, params, x, mode="f32", flags=None):
     return h, cache
 
 
-def backward(spec, params, cache, dlogits, mode="f32"):
+def backward(spec, params, cache, dlogits, mode="f32", acc="f64"):
     """Backward pass from dL/dlogits. Returns the gradient list (state-dict order)."""
-    R = _Mode(mode)
+    R = _Mode(mode, acc)
     grads = [None] * len(params)
     g = np.asarray(dlogits, dtype=F64)
     first_param_layer = min(e[1] for e in cache if e[0] in ("linear", "conv"))
@@ -384,9 +405,9 @@ def backward(spec, params, cache, dlogits, mode="f32"):
             gq = R.operand(g)
             need_dh = pi != first_param_layer
             if kind == "linear":
-                dW, db, dh = linear_bwd(gq, hin, Wq, need_dh)
+                dW, db, dh = R.run(linear_bwd, gq, hin, Wq, need_dh)
             else:
-                dW, db, dh = conv2d_bwd(gq, hin, Wq, entry[4], need_dh)
+                dW, db, dh = R.run(conv2d_bwd, gq, hin, Wq, entry[4], need_dh)
             grads[pi], grads[pi + 1] = R.store(dW), R.store(db)
             g = R.store(dh) if need_dh else None
         elif kind == "relu":
@@ -450,16 +471,16 @@ def adam_update(params, grads, m, v, t, lr, beta1, beta2, eps, mode="f32"):
     return out_p, out_m, out_v
 
 
-def step_opt(spec, params, x, y, lr, opt, state, mode="f32", flags=None):
+def step_opt(spec, params, x, y, lr, opt, state, mode="f32", flags=None, acc="f64"):
     """One training step of one model under its optimizer.
 
     opt: {"kind": "sgd" | "momentum" | "adam", "momentum", "betas", "eps"};
     state: {"t": updates taken, "s1": [...], "s2": [...]} (zeros / absent at
     the start). Returns (loss, new params, grads, new state)."""
-    logits, cache = forward(spec, params, x, mode, flags)
-    loss, dz = softmax_ce(logits, y)
+    logits, cache = forward(spec, params, x, mode, flags, acc)
+    loss, dz = softmax_ce(logits, y, F64 if acc == "f64" else F32)
     dz = _Mode(mode).store(dz)
-    grads = backward(spec, params, cache, dz, mode)
+    grads = backward(spec, params, cache, dz, mode, acc)
     zeros = [np.zeros(np.shape(p), dtype=F64 if mode == "f64" else F32) for p in params]
     t = state.get("t", 0) + 1
     kind = opt["kind"]
@@ -474,12 +495,12 @@ def step_opt(spec, params, x, y, lr, opt, state, mode="f32", flags=None):
     return loss, newp, grads, {"t": t, "s1": m, "s2": v}
 
 
-def step(spec, params, x, y, lr, mode="f32", flags=None):
+def step(spec, params, x, y, lr, mode="f32", flags=None, acc="f64"):
     """One training step of one model. Returns (loss at pre-update params, new params, grads)."""
-    logits, cache = forward(spec, params, x, mode, flags)
-    loss, dz = softmax_ce(logits, y)
+    logits, cache = forward(spec, params, x, mode, flags, acc)
+    loss, dz = softmax_ce(logits, y, F64 if acc == "f64" else F32)
     dz = _Mode(mode).store(dz)
-    grads = backward(spec, params, cache, dz, mode)
+    grads = backward(spec, params, cache, dz, mode, acc)
     return loss, sgd_update(params, grads, lr, mode), grads
 
 
@@ -488,7 +509,7 @@ def loss_only(spec, params, x, y, mode="f64"):
     return softmax_ce(logits, y)[0]
 
 
-def train(spec, params, batches, lr, mode="f32", flags=None):
+def train(spec, params, batches, lr, mode="f32", flags=None, acc="f64"):
     """Train one model alone over a sequence of (x, y) batches.
 
     Returns (losses per step, final params, grads of the last step). `flags`
@@ -498,7 +519,7 @@ def train(spec, params, batches, lr, mode="f32", flags=None):
     grads = None
     params = [np.array(p, dtype=F64 if mode == "f64" else F32) for p in params]
     for x, y in batches:
-        loss, params, grads = step(spec, params, x, y, lr, mode, flags)
+        loss, params, grads = step(spec, params, x, y, lr, mode, flags, acc)
         losses.append(loss)
     return np.array(losses), params, grads
 

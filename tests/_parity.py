@@ -16,13 +16,17 @@ from paper_2408_01331_amd import workloads as W
 
 # The gate: max relative error on losses and parameters.
 TOL = {"f32": 1e-4, "bf16": 2e-2}
-# Extras of multi-step runs (updates theta_k - theta_0 and the last step's
-# gradient, Frobenius) are bounded by SENS_FACTOR times what the oracle itself
-# does under a 1-ulp change of its first step's parameters (oracle_sensitivity),
-# and never tighter than the gate.
-SENS_FACTOR = 4.0
-# Bound of the extras when no sensitivity run is given.
-UPDATE_TOL = {"f32": 1e-2, "bf16": 0.2}
+# Extras (one step: update and gradient, max relative error; k steps: update
+# theta_k - theta_0 and the last step's gradient, Frobenius) are bounded by
+# SPREAD_FACTOR times the distance between the oracle and the same oracle
+# evaluated in fp32 arithmetic (oracle_spread), and never tighter than a floor:
+# the gate for one step; EXTRA_FLOOR for k steps, the scale of a trajectory in
+# which one discrete decision (a bf16 rounding of a stored value, a ReLU / pool
+# decision) went the other way once: at batch 6 one flipped bf16 value moves a
+# weight gradient by about 2^-8 / sqrt(6), and the runs part from there.
+SPREAD_FACTOR = 4.0
+EXTRA_FLOOR = {"f32": 1e-2, "bf16": 0.1}
+UPDATE_TOL = EXTRA_FLOOR
 # A flipped decision changes one sample's contribution to the flagged unit's
 # gradient; those parameters are held to this bound instead of the strict one.
 FLAGGED_TOL = 1e-2
@@ -71,43 +75,41 @@ def perturb_ulp(params, seed):
     return out
 
 
-def oracle_sensitivity(spec, th0, batches, lr, mode, flags, ref):
-    """What the oracle does to itself when its parameters after the first step
-    move by one fp32 ulp (perturb_ulp), carried through the remaining steps:
-    per tensor, the Frobenius relative change of the update theta_k - theta_0
-    and of the last step's gradient over the units `flags` never marked, and
-    the per-step loss change. `ref` = (losses, params, grads) of the
-    unperturbed run. A bf16 run's stored values are discrete: such a change
-    flips roundings (and ReLU / pool decisions) that compound over steps, so
-    this is the scale below which no evaluation order can be told apart from
-    another. Returns {} for a one-step run."""
-    if len(batches) < 2:
-        return {}
-    x, y = batches[0]
-    _, p1, _ = oracle.step(spec, th0, x, y, lr, mode)
-    loss_p, p, g = oracle.train(spec, perturb_ulp(p1, 1), batches[1:], lr, mode)
+def oracle_spread(spec, th0, batches, lr, mode, flags, ref):
+    """How far two evaluation orders the reading allows lie apart: the oracle's
+    trajectory with fp32 accumulation (float32 BLAS) against its reference
+    trajectory `ref` = (losses, params, grads) (fp64 accumulation), over the
+    units `flags` never marked, per tensor: the update theta_k - theta_0 and
+    the last step's gradient, each as max relative error ("update", "grad")
+    and as Frobenius relative error ("update_fro", "grad_fro"), and the loss
+    of every step. In bf16 the stored values are discrete (roundings, ReLU and
+    pool decisions), so differences of order compound over the steps; this is
+    the scale below which no evaluation order can be told apart from another."""
+    loss_a, p, g = oracle.train(spec, th0, batches, lr, mode, None, "f32")
     masks = flagged_masks(spec, ref[1], flags)
-    upd, grd = [], []
+    out = {"update": [], "grad": [], "update_fro": [], "grad_fro": []}
     for t, (a, b, ga, gb, t0) in enumerate(zip(p, ref[1], g, ref[2], th0)):
         keep = ~masks[t]
-        upd.append(fro_err((np.asarray(a, np.float64) - t0)[keep], (np.asarray(b, np.float64) - t0)[keep]))
-        grd.append(fro_err(np.asarray(ga)[keep], np.asarray(gb)[keep]))
-    loss = np.abs(np.asarray(loss_p) - ref[0][1:]) / np.abs(ref[0][1:])
-    return {"update_fro": upd, "grad_fro": grd, "loss": [0.0] + loss.tolist()}
+        ua, ub = np.asarray(a, np.float64) - t0, np.asarray(b, np.float64) - t0
+        out["update"].append(tensor_err(ua, ub, keep))
+        out["grad"].append(tensor_err(ga, gb, keep))
+        out["update_fro"].append(fro_err(ua[keep], ub[keep]))
+        out["grad_fro"].append(fro_err(np.asarray(ga)[keep], np.asarray(gb)[keep]))
+    out["loss"] = (np.abs(np.asarray(loss_a) - ref[0]) / np.abs(ref[0])).tolist()
+    return out
 
 
-def run_oracle(wl, steps, models, lr=None, theta=None, sensitivity=False):
+def run_oracle(wl, steps, models, lr=None, theta=None, spread=False):
     """Each listed model trained alone by the oracle. Returns {i: (losses,
-    params, grads, flags)} or, with sensitivity, also {i: oracle_sensitivity}."""
+    params, grads, flags)} or, with spread, also {i: oracle_spread}."""
     lr = wl.lr if lr is None else lr
     batches = [W.make_batch(wl, s) for s in range(steps)]
     th = {i: (theta0(wl, i) if theta is None or i not in theta else theta[i]) for i in range(wl.n_models)}
     out = oracle.train_models(wl.specs, th, batches, lr, wl.precision, models=models, with_flags=True)
-    if not sensitivity:
+    if not spread:
         return out
-    sens = {i: oracle_sensitivity(wl.specs[i], th[i], batches, lr, wl.precision, out[i][3], out[i][:3])
-            for i in out}
-    return out, sens
+    sp = {i: oracle_spread(wl.specs[i], th[i], batches, lr, wl.precision, out[i][3], out[i][:3]) for i in out}
+    return out, sp
 
 
 def tensor_err(a, b, mask=None):
@@ -189,11 +191,14 @@ def _losses(wl, losses_g, i, losses_o, tol, worst):
     assert le.max() <= tol, f"model {i}: loss rel err {le.max():.3g} > {tol} ({losses_g[:, i]} vs {losses_o})"
 
 
-def compare_step(wl, gpu, orc, models, tol=None):
+def compare_step(wl, gpu, orc, models, tol=None, spread=None):
     """One step from identical parameters: per-tensor max relative error <= tol
-    on losses, parameters, updates and gradients, except at units whose ReLU /
-    max-pool decision the oracle flagged as ill-conditioned in fp32 (those
-    parameters within FLAGGED_TOL; their gradients are not compared)."""
+    on losses and parameters (the gate), and on updates and gradients, except
+    at units whose ReLU / max-pool decision the oracle flagged as
+    ill-conditioned in fp32 (those parameters within FLAGGED_TOL; their
+    gradients are not compared). With `spread` (oracle_spread of one step), an
+    update or gradient tensor whose two evaluation orders already lie further
+    apart than tol / SPREAD_FACTOR is held to SPREAD_FACTOR times that spread."""
     tol = TOL[wl.precision] if tol is None else tol
     losses_g, params_g, grads_g = gpu
     assert losses_g.shape[0] == 1
@@ -209,7 +214,10 @@ def compare_step(wl, gpu, orc, models, tol=None):
             for key, a, b in (("param", pg, po), ("update", pg - th0[t], po - th0[t]), ("grad", gg, go)):
                 e = tensor_err(a, b, strict)
                 worst[key] = max(worst[key], e)
-                assert e <= tol, f"model {i} tensor {t}: {key} err {e:.3g} > {tol}"
+                bound = tol
+                if key != "param" and spread is not None and i in spread:
+                    bound = max(tol, SPREAD_FACTOR * spread[i][key][t])
+                assert e <= bound, f"model {i} tensor {t}: {key} err {e:.3g} > {bound:.3g}"
             if fm[t].any():
                 ef = tensor_err(pg, po, fm[t])
                 worst["flagged_param"] = max(worst["flagged_param"], ef)
@@ -217,16 +225,17 @@ def compare_step(wl, gpu, orc, models, tol=None):
     return worst
 
 
-def extra_bound(wl, sens, i, key, t):
+def extra_bound(wl, spread, i, key, t):
     """Bound of a multi-step extra (update or gradient, Frobenius) of model i's
-    tensor t: SENS_FACTOR times the oracle's own change under a 1-ulp
-    perturbation, never below the gate; UPDATE_TOL without a sensitivity run."""
-    if sens is None or i not in sens or not sens[i]:
-        return UPDATE_TOL[wl.precision]
-    return max(TOL[wl.precision], SENS_FACTOR * sens[i][key][t])
+    tensor t: SPREAD_FACTOR times the spread between the oracle's two
+    evaluation orders, never below EXTRA_FLOOR."""
+    floor = EXTRA_FLOOR[wl.precision]
+    if spread is None or i not in spread or not spread[i]:
+        return floor
+    return max(floor, SPREAD_FACTOR * spread[i][key][t])
 
 
-def compare_run(wl, gpu, orc, models, tol=None, sens=None):
+def compare_run(wl, gpu, orc, models, tol=None, spread=None):
     """k free-running steps against the oracle that trained each model alone.
 
     The gate (the stated metric): losses within `tol` relative error at every
@@ -237,9 +246,9 @@ def compare_run(wl, gpu, orc, models, tol=None, sens=None):
 
     Extras, Frobenius relative error over the never-flagged units: the update
     theta_k - theta_0 and the last step's gradient, each within extra_bound
-    (the oracle's own sensitivity, measured in the same test when `sens` is
-    given). Returns the worst values, and for the extras their worst ratio to
-    the bound."""
+    (the spread of the oracle's two evaluation orders, oracle_spread, measured
+    in the same test when `spread` is given). Returns the worst values, and
+    for the extras their worst ratio to the bound."""
     tol = TOL[wl.precision] if tol is None else tol
     losses_g, params_g, grads_g = gpu
     worst = {"loss": 0.0, "param_max": 0.0, "flagged_param": 0.0, "update_fro": 0.0, "grad_fro": 0.0,
@@ -262,7 +271,7 @@ def compare_run(wl, gpu, orc, models, tol=None, sens=None):
             ug, uo = np.asarray(pg - th0[t])[keep], np.asarray(po - th0[t])[keep]
             for key, err in (("update_fro", fro_err(ug, uo)),
                              ("grad_fro", fro_err(np.asarray(gg)[keep], np.asarray(go)[keep]))):
-                bound = extra_bound(wl, sens, i, key, t)
+                bound = extra_bound(wl, spread, i, key, t)
                 worst[key] = max(worst[key], err)
                 worst["extra_vs_bound"] = max(worst["extra_vs_bound"], err / bound)
                 assert err <= bound, f"model {i} tensor {t}: {key} {err:.3g} > {bound:.3g}"

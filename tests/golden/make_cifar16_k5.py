@@ -8,7 +8,8 @@ minute and a half per model-step on 8 host cores).
 writes tests/golden/cifar16_k5_m<model>.npz with, for that model trained
 alone from its seeded start: the loss of every step, the final parameters, the
 last step's gradient, the units the oracle flagged as ill-conditioned, and the
-oracle's own sensitivity to a 1-ulp change of its first step's parameters.
+spread between the oracle's two evaluation orders (fp64 and fp32
+accumulation) over the same steps.
 It calls only the oracle and the seeded input generators; nothing here comes
 from the GPU path. The sampled models (1, 4, 6, 11) cover every drawn width:
 first conv 32 / 48 / 64, second 64 / 96 / 128, third 128 / 192 / 256.
@@ -30,9 +31,10 @@ for p in (ROOT, os.path.dirname(HERE)):
 
 import oracle  # noqa: E402
 from paper_2408_01331_amd import workloads as W  # noqa: E402
-from _parity import oracle_sensitivity  # noqa: E402
+from _parity import oracle_spread  # noqa: E402
 
 MODELS = (1, 4, 6, 11)
+SPREAD_KEYS = ("update", "grad", "update_fro", "grad_fro", "loss")
 
 
 def sha(path):
@@ -71,16 +73,16 @@ def main():
     flags = {}
     losses, params, grads = oracle.train(wl.specs[i], th0, batches, wl.lr, wl.precision, flags)
     print(f"model {i}: trajectory in {time.time() - t0:.0f} s, losses {np.round(losses, 5).tolist()}", flush=True)
-    sens = oracle_sensitivity(wl.specs[i], th0, batches, wl.lr, wl.precision, flags, (losses, params, grads))
-    print(f"model {i}: sensitivity run done at {time.time() - t0:.0f} s", flush=True)
+    spread = oracle_spread(wl.specs[i], th0, batches, wl.lr, wl.precision, flags, (losses, params, grads))
+    print(f"model {i}: fp32-accumulation run done at {time.time() - t0:.0f} s", flush=True)
     out = {"losses": np.asarray(losses, np.float64)}
     for t, (p, g) in enumerate(zip(params, grads)):
         out[f"p{t}"] = np.asarray(p, np.float32)
         out[f"g{t}"] = np.asarray(g, np.float32)
     for wi, units in flags.items():
         out[f"flags{wi}"] = np.array(sorted(units), np.int64)
-    for k in ("update_fro", "grad_fro", "loss"):
-        out[f"sens_{k}"] = np.asarray(sens[k], np.float64)
+    for k in SPREAD_KEYS:
+        out[f"spread_{k}"] = np.asarray(spread[k], np.float64)
     meta = dict(model=i, steps=a.steps, lr=wl.lr, seed=wl.seed, precision=wl.precision, workload=wl.name,
                 inputs_sha256=input_digest(wl, i, a.steps),
                 oracle_sha256=sha(os.path.join(ROOT, "oracle", "oracle.py")))
@@ -90,15 +92,15 @@ def main():
 
 
 def load(i):
-    """(losses, params, grads, flags), sensitivity dict, meta of model i."""
+    """(losses, params, grads, flags), spread dict, meta of model i."""
     z = np.load(path_of(i), allow_pickle=False)
     meta = json.loads(str(z["meta"]))
     n = len([k for k in z.files if k.startswith("p")])
     params = [z[f"p{t}"] for t in range(n)]
     grads = [z[f"g{t}"] for t in range(n)]
     flags = {int(k[5:]): set(z[k].tolist()) for k in z.files if k.startswith("flags")}
-    sens = {k: z[f"sens_{k}"].tolist() for k in ("update_fro", "grad_fro", "loss")}
-    return (z["losses"], params, grads, flags), sens, meta
+    spread = {k: z[f"spread_{k}"].tolist() for k in SPREAD_KEYS}
+    return (z["losses"], params, grads, flags), spread, meta
 
 
 if __name__ == "__main__":

@@ -8,7 +8,7 @@ whose fp32 ReLU / max-pool decisions the oracle never found ill-conditioned
 after k free-running steps. Updates theta_k - theta_0 and gradients are
 checked too, because the parameters alone are dominated by their identical
 start values: strictly after one step, and after k steps against the oracle's
-own sensitivity to a 1-ulp change of its parameters.
+spread between two evaluation orders (fp64 and fp32 accumulation).
 """
 import os
 import sys
@@ -49,8 +49,8 @@ def test_one_step_strict(name, sample):
     wl = W.get(name)
     models = list(range(wl.n_models)) if sample is None else sample
     gpu = run_gpu(wl, 1, models=models)
-    orc = run_oracle(wl, 1, models)
-    _report(f"{wl.name} 1 step", compare_step(wl, gpu, orc, models))
+    orc, spread = run_oracle(wl, 1, models, spread=True)
+    _report(f"{wl.name} 1 step", compare_step(wl, gpu, orc, models, spread=spread))
 
 
 RUNS = [("mlp2", None), ("mlp8", None), ("lenet4", None)]
@@ -64,8 +64,8 @@ def test_k_steps(name, steps):
     steps = wl.steps if steps is None else steps
     models = list(range(wl.n_models))
     gpu = run_gpu(wl, steps, models=models)
-    orc, sens = run_oracle(wl, steps, models, sensitivity=True)
-    _report(f"{wl.name} {steps} steps", compare_run(wl, gpu, orc, models, sens=sens))
+    orc, spread = run_oracle(wl, steps, models, spread=True)
+    _report(f"{wl.name} {steps} steps", compare_run(wl, gpu, orc, models, spread=spread))
 
 
 # The larger workloads: one GPU run of every model, compared in chunks of
@@ -91,8 +91,8 @@ def test_k_steps_every_model(name, steps, models):
     _need_gpu()
     wl = W.get(name)
     gpu = _gpu_run(name, steps)
-    orc, sens = run_oracle(wl, steps, models, sensitivity=True)
-    _report(f"{wl.name} {steps} steps models {models[0]}-{models[-1]}", compare_run(wl, gpu, orc, models, sens=sens))
+    orc, spread = run_oracle(wl, steps, models, spread=True)
+    _report(f"{wl.name} {steps} steps models {models[0]}-{models[-1]}", compare_run(wl, gpu, orc, models, spread=spread))
 
 
 def test_cifar16_five_steps_against_oracle_fixtures():
@@ -103,22 +103,27 @@ def test_cifar16_five_steps_against_oracle_fixtures():
     import make_cifar16_k5 as F
     wl = W.get("cifar16")
     steps = 5
-    orc, sens = {}, {}
+    orc, spread = {}, {}
     for i in F.MODELS:
-        orc[i], sens[i], meta = F.load(i)
+        orc[i], spread[i], meta = F.load(i)
         assert meta["steps"] == steps
         assert meta["inputs_sha256"] == F.input_digest(wl, i, steps), \
             f"fixture of model {i} was written for other inputs: rerun tests/golden/make_cifar16_k5.py --model {i}"
     gpu = run_gpu(wl, steps, models=list(F.MODELS))
-    _report(f"{wl.name} {steps} steps (fixtures)", compare_run(wl, gpu, orc, list(F.MODELS), sens=sens))
+    _report(f"{wl.name} {steps} steps (fixtures)", compare_run(wl, gpu, orc, list(F.MODELS), spread=spread))
 
 
 # ---------------------------------------------------------------------------
 # Ragged and degenerate shapes (several tiles plus a ragged tail)
 # ---------------------------------------------------------------------------
+def _step_vs_oracle(wl, models):
+    orc, spread = run_oracle(wl, 1, models, spread=True)
+    return compare_step(wl, run_gpu(wl, 1), orc, models, spread=spread)
+
+
 def _run_vs_oracle(wl, models):
-    orc, sens = run_oracle(wl, wl.steps, models, sensitivity=True)
-    return compare_run(wl, run_gpu(wl, wl.steps), orc, models, sens=sens)
+    orc, spread = run_oracle(wl, wl.steps, models, spread=True)
+    return compare_run(wl, run_gpu(wl, wl.steps), orc, models, spread=spread)
 
 
 def _custom(specs, batch, in_shape, precision, steps=3, lr=0.05, seed=5, init="kaiming"):
@@ -138,7 +143,7 @@ def test_ragged_mlps(precision):
     ]
     wl = _custom(specs, 37, (104,), precision)
     m = range(wl.n_models)
-    _report(f"ragged_mlps_{precision} 1 step", compare_step(wl, run_gpu(wl, 1), run_oracle(wl, 1, m), m))
+    _report(f"ragged_mlps_{precision} 1 step", _step_vs_oracle(wl, m))
     _report(f"ragged_mlps_{precision} run", _run_vs_oracle(wl, m))
 
 
@@ -158,7 +163,7 @@ def test_residual_mlps(precision):
     ]
     wl = _custom(specs, 37, (104,), precision)
     m = range(wl.n_models)
-    _report(f"residual_{precision} 1 step", compare_step(wl, run_gpu(wl, 1), run_oracle(wl, 1, m), m))
+    _report(f"residual_{precision} 1 step", _step_vs_oracle(wl, m))
     _report(f"residual_{precision} run", _run_vs_oracle(wl, m))
 
 
@@ -178,7 +183,7 @@ def test_softmax_ce_fused_and_row_pass(precision):
     ]
     wl = _custom(specs, 45, (72,), precision)      # labels < 10, the first model's classes
     m = range(wl.n_models)
-    _report(f"ce_paths_{precision} 1 step", compare_step(wl, run_gpu(wl, 1), run_oracle(wl, 1, m), m))
+    _report(f"ce_paths_{precision} 1 step", _step_vs_oracle(wl, m))
     _report(f"ce_paths_{precision} run", _run_vs_oracle(wl, m))
 
 
@@ -196,7 +201,7 @@ def test_ragged_cnns(precision):
     ]
     wl = _custom(specs, 12, (3, 13, 16), precision, steps=3)
     m = range(wl.n_models)
-    _report(f"ragged_cnns_{precision} 1 step", compare_step(wl, run_gpu(wl, 1), run_oracle(wl, 1, m), m))
+    _report(f"ragged_cnns_{precision} 1 step", _step_vs_oracle(wl, m))
     _report(f"ragged_cnns_{precision} run", _run_vs_oracle(wl, m))
 
 
@@ -217,7 +222,7 @@ def test_halo_tiled_cnns(precision):
     ]
     wl = _custom(specs, 6, (8, 16, 16), precision, steps=3)
     m = range(wl.n_models)
-    _report(f"halo_cnns_{precision} 1 step", compare_step(wl, run_gpu(wl, 1), run_oracle(wl, 1, m), m))
+    _report(f"halo_cnns_{precision} 1 step", _step_vs_oracle(wl, m))
     _report(f"halo_cnns_{precision} run", _run_vs_oracle(wl, m))
 
 
@@ -247,7 +252,7 @@ def test_residual_cnns(precision, batch, in_shape):
     wl = _custom(_RES_CNNS, batch, in_shape, precision, steps=3, init="torch")
     m = range(wl.n_models)
     tag = f"residual_cnns_{precision}_{batch}"
-    _report(f"{tag} 1 step", compare_step(wl, run_gpu(wl, 1), run_oracle(wl, 1, m), m))
+    _report(f"{tag} 1 step", _step_vs_oracle(wl, m))
     _report(f"{tag} run", _run_vs_oracle(wl, m))
 
 
