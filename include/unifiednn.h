@@ -110,7 +110,13 @@ typedef struct {
  * [Conv2d, optional ReLU, optional MaxPool2] blocks, a Flatten if any conv is
  * present, then one or more [Linear, optional ReLU] blocks, the last Linear
  * having no ReLU and out == num_classes; residual markers may enclose runs of
- * the Linear blocks as UN_RESIDUAL_BEGIN describes.
+ * the Linear blocks or of the Conv2d blocks as UN_RESIDUAL_BEGIN describes.
+ * Size restrictions (UN_ERR_UNSUPPORTED otherwise): when some model starts
+ * with a Linear layer, in_c * in_h * in_w is a multiple of 8; a Linear layer
+ * reading a flattened conv output reads a multiple of 8 features
+ * (channels * height * width of that output); batch <= 2^20.
+ * The context's device is the one current at this call; the context's own
+ * stream is created on it.
  * On success *out owns the context. Errors: UN_ERR_INVALID, UN_ERR_UNSUPPORTED,
  * UN_ERR_OOM, UN_ERR_DEVICE (then *out is NULL). */
 un_status un_create(const un_model_spec* specs, int32_t n_models,
@@ -136,7 +142,11 @@ un_status un_plan_bytes(const un_model_spec* specs, int32_t n_models, const un_i
 un_status un_load_batch(un_ctx* ctx, const float* x, const int32_t* y);
 
 /* As un_load_batch, with x and y already in device memory (same layouts). The
- * labels are range-checked after a device-to-host copy. */
+ * buffers are read on the context's stream (un_get_stream): the caller orders
+ * the work that writes them before this call (e.g. a stream or device
+ * synchronisation, or by running that work on the context's stream). The
+ * labels are range-checked after a device-to-host copy; the call returns when
+ * the batch has been converted, after which x_dev and y_dev may be reused. */
 un_status un_load_batch_device(un_ctx* ctx, const float* x_dev, const int32_t* y_dev);
 
 /* Labels per model for the batch already loaded (Algorithm 2 gives every
@@ -256,8 +266,35 @@ un_status un_arena_bytes(const un_ctx* ctx, size_t* bytes);
 un_status un_sync(un_ctx* ctx);
 
 /* The context's HIP stream (a hipStream_t), so a caller can order its own work
- * or record events around steps. Owned by the context. */
+ * or record events around steps. Owned by the context unless set by
+ * un_set_stream. */
 un_status un_get_stream(const un_ctx* ctx, void** hip_stream);
+
+/* Run the context's work from now on on the caller's stream (a hipStream_t on
+ * the context's device, e.g. a PyTorch stream), so that it is ordered with
+ * the caller's other work without host synchronisation; NULL returns to the
+ * context's own stream. The caller keeps the stream alive while the context
+ * uses it. Waits for the work already enqueued on the previous stream.
+ * Invalidates a captured step (un_graph_capture). */
+un_status un_set_stream(un_ctx* ctx, void* hip_stream);
+
+/* Capture one step (exactly what un_step(ctx, lr, NULL) enqueues) as a HIP
+ * graph owned by the context, for callers whose steps are bounded by launch
+ * latency: un_graph_step then replays it with one launch. The graph holds the
+ * rate lr, the active set, the optimizers, un_keep_grads and the label mode
+ * of this moment; un_set_active, un_set_optimizer state allocation,
+ * un_set_stream, or a change of un_keep_grads or of the label mode
+ * (un_load_labels / un_load_batch) make it stale. The batch, parameters and
+ * labels it reads are the context's buffers: load new batches and set
+ * parameters as usual between replays. Not available while a model has a
+ * momentum or Adam optimizer (their per-step hyper-parameters would be frozen).
+ * Errors: UN_ERR_STATE (no batch), UN_ERR_INVALID (lr), UN_ERR_UNSUPPORTED,
+ * UN_ERR_DEVICE. */
+un_status un_graph_capture(un_ctx* ctx, float lr);
+
+/* Replay the captured step: the same result as the un_step call it recorded
+ * (losses as un_step). Errors: UN_ERR_STATE (nothing captured, or stale). */
+un_status un_graph_step(un_ctx* ctx, float* losses);
 
 /* Kernel classes for per-kernel timing. */
 typedef enum {

@@ -210,29 +210,34 @@ struct SgdTensor {
 // else forward problems (row-major operands only).
 // labels / lab_stride: the labels of the fused softmax-CE (model m's at
 // labels + m * lab_stride; stride 0 when all models share one row).
+// wsoff: byte offset added to every workspace pointer of the descriptors
+// (split-K partials GemmProb::ce_part, ConvProb::ws, ReduceProb::ws), so that
+// one set of tables serves the arena's workspace (0) or another buffer of the
+// same layout.
 hipError_t launch_gemm(bool bf16, bool bwd, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
                        const float* lrv, const OptHp* opt, bool keep_grads, const int32_t* labels, int lab_stride,
-                       hipStream_t s);
+                       int64_t wsoff, hipStream_t s);
 hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                            hipStream_t s);
 hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                              hipStream_t s);
 // mode: 0 any layer; 1 pooled, 2 unpooled, both with O and C whole 16-byte vectors
 hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const int32_t* tile_map, int ntiles,
-                             hipStream_t s);
+                             int64_t wsoff, hipStream_t s);
 // Halo-tiled forward (dgrad = false) or data gradient (dgrad = true); every
 // problem of the launch has halo != 0 (either tile shape).
 hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                             size_t lds_bytes, hipStream_t s);
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
-                         const float* lrv, const OptHp* opt, bool keep_grads, hipStream_t s);
+                         const float* lrv, const OptHp* opt, bool keep_grads, int64_t wsoff, hipStream_t s);
 hipError_t launch_set_values(float* dst, const float* vals, int n, hipStream_t s);
 // probs: the first nrows problems need the row pass (their CE is not fused
 // into the logits GEMM); the loss of every one of the nprobs is finished.
 // Partials of model m are at partial + m * pstride.
 hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, int nrows, const int32_t* labels,
                      bool per_model_labels, int B, float* partial, int pstride, float* losses, hipStream_t s);
-hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int ntiles, float lr,
+// The launch covers tiles [blk0, blk0 + ntiles) of the tile table.
+hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int blk0, int ntiles, float lr,
                       bool use_grad, hipStream_t s);
 // fp32 NCHW batch -> storage type: NHWC X (optional) and NHWC XC with
 // Cs >= C channels (optional; the channels from C on are left untouched).

@@ -1,17 +1,21 @@
 // gfx950 (CDNA4) kernels of the fused N-model training step.
 //
-// One LDS-staged MFMA core (bf16: v_mfma_f32_16x16x32_bf16, fp32:
-// v_mfma_f32_16x16x4_f32; fp32 accumulation in both) is shared by
-//   - the grouped NT GEMM that runs every Linear layer's forward, dgrad and
-//     wgrad for all models of one depth level in one launch, and
-//   - the three implicit-GEMM convolution passes (forward with fused
-//     bias/ReLU/2x2 max-pool epilogue, dgrad with an un-pool gather prologue,
-//     split-K wgrad).
-// A workgroup (256 threads = 4 wave64s in a 2x2 arrangement) owns one output
-// tile of one problem; a flat tile table maps blockIdx.x to (problem, tile).
-// Every output element is reduced over k in a fixed order that depends only
-// on its own problem's shape, so a model's results are bitwise independent of
-// which other models share the launch.
+// LDS-staged MFMA cores with fp32 accumulation serve
+//   - the grouped GEMM that runs every Linear layer's forward, data gradient
+//     and weight gradient (with the optimizer step fused into its epilogue)
+//     for all models of one depth level in one launch: bf16 workgroups of 16
+//     waves, each wave a 32x32 tile of v_mfma_f32_32x32x16_bf16 on a 128x128
+//     workgroup tile; fp32 workgroups of 4 waves (2x2) of
+//     v_mfma_f32_16x16x4_f32 on 64x64;
+//   - the implicit-GEMM convolution passes: forward with the bias / ReLU /
+//     2x2 max-pool epilogue (v_mfma_f32_16x16x32_bf16, whose accumulator rows
+//     hold a pool window), data gradient with the un-pool gather, and the
+//     split-K weight gradient (bf16: the GEMM's 32x32x16 core on k-major
+//     operands), reduced in split order by a kernel that applies the update.
+// A workgroup owns one output tile of one problem; a flat tile table maps
+// blockIdx.x to (problem, tile). Every output element is reduced over k in a
+// fixed order that depends only on its own problem's shape, so a model's
+// results are bitwise independent of which other models share the launch.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -1203,10 +1207,10 @@ __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, 
 // fused into the logits GEMM: CE_LANES lanes per row reduce max and sum with
 // lane shuffles in the same order as ce_rows_kernel, write dL/dz =
 // (softmax - onehot) / B to C, and the row losses of the tile are summed in
-// row order into ce_part[tm].
+// row order into ce_part[tm] (a workspace buffer: wsoff bytes added).
 template <typename T, int BM, int CLD, int NT>
 __device__ __forceinline__ void fused_softmax_ce(float* sC, const GemmProb& p, int m0, int tm,
-                                                 const int32_t* __restrict__ labels, int lab_stride) {
+                                                 const int32_t* __restrict__ labels, int lab_stride, int64_t wsoff) {
   constexpr int RPP = NT / CE_LANES;  // rows per pass
   static_assert(NT % CE_LANES == 0 && BM % RPP == 0, "whole rows per pass");
   __shared__ float s_loss[BM];
@@ -1253,7 +1257,7 @@ __device__ __forceinline__ void fused_softmax_ce(float* sC, const GemmProb& p, i
     const int nrows = min(BM, p.M - m0);
     float t = 0.f;
     for (int r = 0; r < nrows; ++r) t += s_loss[r];
-    p.ce_part[tm] = t;
+    ((float*)((char*)p.ce_part + wsoff))[tm] = t;
   }
 }
 
@@ -1268,7 +1272,7 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
                                                    const int32_t* __restrict__ tile_map, float lr,
                                                    const float* __restrict__ lrv, const OptHp* __restrict__ opt,
                                                    int keep_grads, const int32_t* __restrict__ labels,
-                                                   int lab_stride) {
+                                                   int lab_stride, int64_t wsoff) {
   using TL = Tile<T, BM, BN, BK>;
   using SM = Smem<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[SM::BYTES];
@@ -1360,7 +1364,7 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
 
   if (epi != EPI_WGRAD) {
     if (!BWD && epi == EPI_LOGITS && p.ce_part) {
-      fused_softmax_ce<T, BM, CLD, NT>(sC, p, m0, tm, labels, lab_stride);
+      fused_softmax_ce<T, BM, CLD, NT>(sC, p, m0, tm, labels, lab_stride, wsoff);
       return;
     }
     // Row pass: C[m][n] in 16-byte chunks along n (data gradient: with the
@@ -1885,7 +1889,7 @@ void conv_halo_kernel(const ConvProb* __restrict__ probs, const int32_t* __restr
 
 template <typename T, int BM, int BN, int BK, int MODE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void conv_wgrad_kernel(const ConvProb* __restrict__ probs,
-                                                         const int32_t* __restrict__ tile_map) {
+                                                         const int32_t* __restrict__ tile_map, int64_t wsoff) {
   using TL = Tile<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[Smem<T, BM, BN, BK>::BYTES];
   const int prob = tile_map[2 * blockIdx.x];
@@ -1912,7 +1916,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = (wave >> 1) * TL::WM, wn = (wave & 1) * TL::WN;
-  float* ws = p.ws + (int64_t)split * p.O * p.ldws;
+  float* ws = (float*)((char*)p.ws + wsoff) + (int64_t)split * p.O * p.ldws;
 #pragma unroll
   for (int i = 0; i < TL::FM; ++i) {
     const int mb = m0 + wm + 16 * i + 4 * (lane >> 4);
@@ -2031,7 +2035,8 @@ struct ConvKB {
 // whose blocks have at most that many; else 128 rows (16 waves).
 template <bool POOL, bool NARROW>
 __global__ __launch_bounds__((NARROW ? 512 : 1024)) __attribute__((amdgpu_waves_per_eu((NARROW ? 4 : 8))))
-void conv_wgrad_mfma_kernel(const ConvProb* __restrict__ probs, const int32_t* __restrict__ tile_map) {
+void conv_wgrad_mfma_kernel(const ConvProb* __restrict__ probs, const int32_t* __restrict__ tile_map,
+                            int64_t wsoff) {
   constexpr int BM = NARROW ? CONV_WG_NARROW_BM : CONV_BM_BF16, BN = CONV_BN_BF16, BK = CONV_BK_BF16;
   using MM = GemmMma<bf16_t, BM, BN, BK, NARROW ? 2 : 4, 4>;  // 32x32 wave tiles
   static_assert(MM::NT == (NARROW ? 512 : 1024), "launch bounds");
@@ -2059,7 +2064,7 @@ void conv_wgrad_mfma_kernel(const ConvProb* __restrict__ probs, const int32_t* _
   gemm_loop<bf16_t, BM, BN, BK, D, MM, OP_KMAJ, OP_KMAJ>(la, lb, nkb, (bf16_t*)smem, acc);
 
   // this split's partial sums to ws[split][o][j]
-  float* ws = p.ws + (int64_t)split * p.O * p.ldws;
+  float* ws = (float*)((char*)p.ws + wsoff) + (int64_t)split * p.O * p.ldws;
   MM::for_groups(acc, [&](int rl, int cl, float (&v)[4]) {
     const int mb = m0 + rl, n = n0 + cl;
     if (n >= p.N) return;
@@ -2074,15 +2079,17 @@ template <typename T>
 __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* __restrict__ probs,
                                                               const int32_t* __restrict__ blk_prob, float lr,
                                                               const float* __restrict__ lrv,
-                                                              const OptHp* __restrict__ opt, int keep_grads) {
+                                                              const OptHp* __restrict__ opt, int keep_grads,
+                                                              int64_t wsoff) {
   const ReduceProb& p = probs[blk_prob[blockIdx.x]];
+  const float* ws = (const float*)((const char*)p.ws + wsoff);
   if (lrv) lr = lrv[p.model];
   const int64_t e = (int64_t)(blockIdx.x - p.blk_base) * REDUCE_BLOCK + threadIdx.x;
   const int J1 = p.J + 1;
   if (e >= (int64_t)p.O * J1) return;
   const int o = (int)(e / J1), j = (int)(e - (int64_t)o * J1);
   float s = 0.f;
-  for (int k = 0; k < p.splits; ++k) s += p.ws[((int64_t)k * p.O + o) * p.ldws + j];
+  for (int k = 0; k < p.splits; ++k) s += ws[((int64_t)k * p.O + o) * p.ldws + j];
   if (j < p.J) {
     const int64_t idx = (int64_t)o * p.ldgw + j;
     if (keep_grads) p.gW[idx] = s;
@@ -2181,10 +2188,12 @@ __global__ void ce_finish_kernel(const CeProb* __restrict__ probs, const float* 
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(256) void sgd_kernel(const SgdTensor* __restrict__ ts,
-                                                  const int32_t* __restrict__ tile_tensor, float lr, int use_grad) {
+                                                  const int32_t* __restrict__ tile_tensor, int blk0, float lr,
+                                                  int use_grad) {
   __shared__ float sm[SGD_TILE][SGD_TILE + 1];
-  const SgdTensor& t = ts[tile_tensor[blockIdx.x]];
-  const int local = blockIdx.x - t.tile_base;
+  const int blk = blockIdx.x + blk0;  // the launch covers tiles [blk0, blk0 + gridDim.x) of the table
+  const SgdTensor& t = ts[tile_tensor[blk]];
+  const int local = blk - t.tile_base;
   const int per_tap = t.tiles_r * t.tiles_c;
   const int j = local / per_tap, rem = local - j * per_tap;
   const int tr = rem / t.tiles_c, tc = rem - tr * t.tiles_c;
@@ -2245,11 +2254,11 @@ __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, 
 // ---------------------------------------------------------------------------
 hipError_t launch_gemm(bool bf16, bool bwd, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
                        const float* lrv, const OptHp* opt, bool keep_grads, const int32_t* labels, int lab_stride,
-                       hipStream_t s) {
+                       int64_t wsoff, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   auto go = [&](auto kern, int nt) {
     hipLaunchKernelGGL(kern, dim3(ntiles), dim3(nt), 0, s, probs, tile_map, lr, lrv, opt, (int)keep_grads, labels,
-                       lab_stride);
+                       lab_stride, wsoff);
   };
   if (bf16) {
     constexpr int NT = GemmMma<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16>::NT;
@@ -2327,22 +2336,22 @@ hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const 
 }
 
 hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const int32_t* tile_map, int ntiles,
-                             hipStream_t s) {
+                             int64_t wsoff, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
 #define UN_WGRAD_LAUNCH(T, BM, BN, BK, M) \
-  hipLaunchKernelGGL((conv_wgrad_kernel<T, BM, BN, BK, M>), dim3(ntiles), dim3(256), 0, s, probs, tile_map)
+  hipLaunchKernelGGL((conv_wgrad_kernel<T, BM, BN, BK, M>), dim3(ntiles), dim3(256), 0, s, probs, tile_map, wsoff)
   if (bf16) {
     constexpr int NT = GemmMma<bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, 4, 4>::NT;
     const bool narrow = (mode & WG_NARROW) != 0;
     mode &= ~WG_NARROW;
     if (mode == WG_POOLED && narrow)
-      hipLaunchKernelGGL((conv_wgrad_mfma_kernel<true, true>), dim3(ntiles), dim3(NT / 2), 0, s, probs, tile_map);
+      hipLaunchKernelGGL((conv_wgrad_mfma_kernel<true, true>), dim3(ntiles), dim3(NT / 2), 0, s, probs, tile_map, wsoff);
     else if (mode == WG_POOLED)
-      hipLaunchKernelGGL((conv_wgrad_mfma_kernel<true, false>), dim3(ntiles), dim3(NT), 0, s, probs, tile_map);
+      hipLaunchKernelGGL((conv_wgrad_mfma_kernel<true, false>), dim3(ntiles), dim3(NT), 0, s, probs, tile_map, wsoff);
     else if (mode == WG_PLAIN && narrow)
-      hipLaunchKernelGGL((conv_wgrad_mfma_kernel<false, true>), dim3(ntiles), dim3(NT / 2), 0, s, probs, tile_map);
+      hipLaunchKernelGGL((conv_wgrad_mfma_kernel<false, true>), dim3(ntiles), dim3(NT / 2), 0, s, probs, tile_map, wsoff);
     else if (mode == WG_PLAIN)
-      hipLaunchKernelGGL((conv_wgrad_mfma_kernel<false, false>), dim3(ntiles), dim3(NT), 0, s, probs, tile_map);
+      hipLaunchKernelGGL((conv_wgrad_mfma_kernel<false, false>), dim3(ntiles), dim3(NT), 0, s, probs, tile_map, wsoff);
     else UN_WGRAD_LAUNCH(bf16_t, CONV_BM_BF16, CONV_BN_BF16, CONV_BK_BF16, WG_GENERIC);
   } else {
     if (mode == WG_POOLED) UN_WGRAD_LAUNCH(float, CONV_BM_F32, CONV_BN_F32, CONV_BK_F32, WG_POOLED);
@@ -2354,14 +2363,14 @@ hipError_t launch_conv_wgrad(bool bf16, int mode, const ConvProb* probs, const i
 }
 
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
-                         const float* lrv, const OptHp* opt, bool keep_grads, hipStream_t s) {
+                         const float* lrv, const OptHp* opt, bool keep_grads, int64_t wsoff, hipStream_t s) {
   if (nblocks <= 0) return hipSuccess;
   if (bf16)
     hipLaunchKernelGGL(reduce_kernel<bf16_t>, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob, lr, lrv, opt,
-                       (int)keep_grads);
+                       (int)keep_grads, wsoff);
   else
     hipLaunchKernelGGL(reduce_kernel<float>, dim3(nblocks), dim3(REDUCE_BLOCK), 0, s, probs, blk_prob, lr, lrv, opt,
-                       (int)keep_grads);
+                       (int)keep_grads, wsoff);
   return hipGetLastError();
 }
 
@@ -2403,13 +2412,13 @@ hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, int nrows, cons
   return hipGetLastError();
 }
 
-hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int ntiles, float lr,
+hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int blk0, int ntiles, float lr,
                       bool use_grad, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   if (bf16)
-    hipLaunchKernelGGL(sgd_kernel<bf16_t>, dim3(ntiles), dim3(256), 0, s, t, tile_tensor, lr, (int)use_grad);
+    hipLaunchKernelGGL(sgd_kernel<bf16_t>, dim3(ntiles), dim3(256), 0, s, t, tile_tensor, blk0, lr, (int)use_grad);
   else
-    hipLaunchKernelGGL(sgd_kernel<float>, dim3(ntiles), dim3(256), 0, s, t, tile_tensor, lr, (int)use_grad);
+    hipLaunchKernelGGL(sgd_kernel<float>, dim3(ntiles), dim3(256), 0, s, t, tile_tensor, blk0, lr, (int)use_grad);
   return hipGetLastError();
 }
 

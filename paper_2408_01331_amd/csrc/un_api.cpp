@@ -63,7 +63,7 @@ struct Block {
   int64_t ldy = 0;
   size_t G = NONE;         // gradient at this block's output, row-major
   int64_t ldg = 0;
-  size_t ws = NONE;
+  size_t ws = NONE, ws_size = 0;
   int64_t ldws = 0;
   int splits = 1, kchunk = 0;
   // output geometry
@@ -104,7 +104,19 @@ struct un_ctx {
   // arena
   char* base = nullptr;
   size_t bytes = 0;
-  hipStream_t stream = nullptr;
+  hipStream_t stream = nullptr;      // the stream every call runs on
+  hipStream_t own_stream = nullptr;  // created with the context (stream differs after un_set_stream)
+  int device = 0;
+  // workspace: the buffers a step writes and reads back within the step only
+  // (conv split-K partials, loss partials), one contiguous arena range;
+  // wsoff relocates them (un_step_scratch), 0 otherwise
+  size_t ws_lo = 0, ws_bytes = 0;
+  int64_t wsoff = 0;
+  // a captured step (un_graph_capture)
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t gexec = nullptr;
+  bool graph_valid = false;
+  bool graph_keep = false, graph_labels = false;  // keep_grads / per-model labels when captured
   // fixed buffers
   size_t xstage = NONE, ydev = NONE, losses_dev = NONE, ce_partial = NONE, Xin = NONE;
   size_t XinC = NONE;  // NHWC input with channels padded to a 16-byte multiple (first convs only)
@@ -129,6 +141,7 @@ struct un_ctx {
   // schedule
   std::vector<Launch> fwd, bwd;
   Launch ce{}, refresh{};
+  std::vector<std::pair<int, int>> refresh_rng;  // per model: its tiles [first, first + count) of `refresh`
   std::vector<char> active;          // models in the step (un_set_active)
   size_t tables_off = NONE, tables_cap = 0;  // arena region of the descriptor tables
   // planning results the tables are built from
@@ -509,6 +522,7 @@ struct Tables {
   std::vector<size_t> fix;   // byte offsets of the encoded pointer fields
   std::vector<Launch> fwd, bwd;
   Launch ce{}, refresh{};
+  std::vector<std::pair<int, int>> refresh_rng;
 };
 
 static void build_tables(un_ctx* c, Tables& T) {
@@ -1008,7 +1022,8 @@ static void build_tables(un_ctx* c, Tables& T) {
       for (int k = 0; k < nt; ++k) map.push_back((int32_t)ts.size());
       ts.push_back(t);
     };
-    for (auto& m : c->models)
+    for (auto& m : c->models) {
+      const int first = (int)map.size();
       for (auto& b : m.blocks) {
         SgdTensor w{};
         w.W = (float*)ptr(b.W32);
@@ -1027,6 +1042,8 @@ static void build_tables(un_ctx* c, Tables& T) {
         }
         add(w);
       }
+      T.refresh_rng.push_back({first, (int)map.size() - first});
+    }
     size_t po = put(ts.data(), ts.size() * sizeof(SgdTensor));
     for (size_t k = 0; k < ts.size(); ++k) {
       size_t b0 = po + k * sizeof(SgdTensor);
@@ -1065,6 +1082,8 @@ static un_status install_tables(un_ctx* c, Tables& T) {
   c->bwd = T.bwd;
   c->ce = T.ce;
   c->refresh = T.refresh;
+  c->refresh_rng = T.refresh_rng;
+  c->graph_valid = false;  // a captured step read the previous tables
   return UN_OK;
 }
 
@@ -1086,7 +1105,6 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
   c->lr_dev = A.take(c->models.size() * 4);
   c->opt_dev = A.take(c->models.size() * sizeof(OptHp));
   c->losses_dev = A.take(c->models.size() * 4);
-  c->ce_partial = A.take(c->models.size() * (size_t)cdiv(B, CE_ROWS) * 4);
   bool any_linear0 = false, any_conv0 = false;
   for (auto& m : c->models) {
     if (m.blocks[0].kind == 0) any_linear0 = true;
@@ -1204,7 +1222,7 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
         b.kchunk = cdiv(nkb, splits);
         b.splits = cdiv(nkb, b.kchunk);
         b.ldws = rup(J + 1, 4);
-        b.ws = A.take((size_t)b.splits * b.O * b.ldws * 4);
+        b.ws_size = (size_t)b.splits * b.O * b.ldws * 4;  // placed in the workspace range below
       }
     }
     // wire inputs
@@ -1221,6 +1239,15 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
     }
   }
   c->levels = levels;
+
+  // --- workspace: one contiguous range (relocatable as a whole, un_step_scratch)
+  c->ws_lo = (size_t)rup((int64_t)A.top, 256);
+  A.top = c->ws_lo;
+  c->ce_partial = A.take(c->models.size() * (size_t)cdiv(B, CE_ROWS) * 4);
+  for (auto& m : c->models)
+    for (auto& b : m.blocks)
+      if (b.kind == 1) b.ws = A.take(b.ws_size);
+  c->ws_bytes = A.top - c->ws_lo;
 
   // --- planning results the descriptor tables are built from
   c->plan.in_feat = in_feat;
@@ -1316,9 +1343,12 @@ static void from_internal(const Block& b, const std::vector<float>& w, const std
   }
 }
 
-static un_status refresh_copies(un_ctx* c) {
+// Rewrite the bf16 (and conv transposed) weight copies from the fp32 master:
+// of every model, or of model i only.
+static un_status refresh_copies(un_ctx* c, int i = -1) {
   const Launch& l = c->refresh;
-  HIPCHK(c, launch_sgd(c->bf16, c->at<SgdTensor>(l.probs), c->at<int32_t>(l.map), l.count, 0.f, false, c->stream));
+  const int blk0 = i < 0 ? 0 : c->refresh_rng[i].first, n = i < 0 ? l.count : c->refresh_rng[i].second;
+  HIPCHK(c, launch_sgd(c->bf16, c->at<SgdTensor>(l.probs), c->at<int32_t>(l.map), blk0, n, 0.f, false, c->stream));
   return UN_OK;
 }
 
@@ -1406,7 +1436,7 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
     case 0:
       e = launch_gemm(c->bf16, l.kclass == UN_K_GEMM_BWD, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, lr,
                       c->lrv, c->optp, c->keep_grads, c->at<int32_t>(c->ydev), c->labels_per_model ? c->B : 0,
-                      c->stream);
+                      c->wsoff, c->stream);
       break;
     case 1:
       e = launch_conv_fwd(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
@@ -1415,7 +1445,8 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
       e = launch_conv_dgrad(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
       break;
     case 3:
-      e = launch_conv_wgrad(c->bf16, l.mode, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
+      e = launch_conv_wgrad(c->bf16, l.mode, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->wsoff,
+                            c->stream);
       break;
     case 7:
     case 8:
@@ -1423,15 +1454,16 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
                            c->stream);
       break;
     case 4:
-      e = launch_reduce(c->bf16, c->at<ReduceProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->lrv, c->optp, c->keep_grads,
-                        c->stream);
+      e = launch_reduce(c->bf16, c->at<ReduceProb>(l.probs), c->at<int32_t>(l.map), l.count, lr, c->lrv, c->optp,
+                        c->keep_grads, c->wsoff, c->stream);
       break;
     case 5:
       e = launch_ce(c->bf16, c->at<CeProb>(l.probs), l.count, l.mode, c->at<int32_t>(c->ydev), c->labels_per_model,
-                    c->B, c->at<float>(c->ce_partial), cdiv(c->B, CE_ROWS), c->at<float>(c->losses_dev), c->stream);
+                    c->B, (float*)((char*)c->at<float>(c->ce_partial) + c->wsoff), cdiv(c->B, CE_ROWS),
+                    c->at<float>(c->losses_dev), c->stream);
       break;
     case 6:
-      e = launch_sgd(c->bf16, c->at<SgdTensor>(l.probs), c->at<int32_t>(l.map), l.count, lr, true, c->stream);
+      e = launch_sgd(c->bf16, c->at<SgdTensor>(l.probs), c->at<int32_t>(l.map), 0, l.count, lr, true, c->stream);
       break;
   }
   if (c->profiling && a && b) {
@@ -1529,16 +1561,18 @@ un_status un_create(const un_model_spec* specs, int32_t n_models, const un_input
     un_status ps = parse_all(specs, n_models, in, &c);
     if (ps != UN_OK) return ps;
   }
-  hipError_t e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
+  hipError_t e = hipGetDevice(&c->device);
+  if (e == hipSuccess) e = hipStreamCreateWithFlags(&c->stream, hipStreamNonBlocking);
   if (e != hipSuccess) {
     delete c;
     return fail(nullptr, UN_ERR_DEVICE, std::string("hipStreamCreate: ") + hipGetErrorString(e));
   }
+  c->own_stream = c->stream;
   un_status s = plan_and_alloc(c);
   if (s != UN_OK) {
     std::string msg = c->err.empty() ? g_create_error : c->err;
     if (c->base) hipFree(c->base);
-    hipStreamDestroy(c->stream);
+    hipStreamDestroy(c->own_stream);
     delete c;
     return fail(nullptr, s, msg);
   }
@@ -1597,6 +1631,20 @@ un_status un_load_batch_device(un_ctx* c, const float* x, const int32_t* y) {
   return load_common(c, x, y, true);
 }
 
+// The kernels of one step, in order, on the context's stream.
+static hipError_t enqueue_step(un_ctx* c, float lr) {
+  for (auto& l : c->fwd) {
+    hipError_t e = run_launch(c, l, lr);
+    if (e != hipSuccess) return e;
+  }
+  hipError_t e = run_launch(c, c->ce, lr);
+  for (auto& l : c->bwd) {
+    if (e != hipSuccess) return e;
+    e = run_launch(c, l, lr);
+  }
+  return e;
+}
+
 // The step's launches. Rates: lrs (host, per model) or else lr for every
 // model. With an optimizer other than SGD on some model, every model's
 // OptHp (rate folded in) goes to the device first and the update kernels
@@ -1637,9 +1685,7 @@ static un_status step_common(un_ctx* c, float lr, const float* lrs, float* losse
     HIPCHK(c, launch_set_values(c->at<float>(c->lr_dev), lrs, (int)n, c->stream));
     c->lrv = c->at<float>(c->lr_dev);
   }
-  for (auto& l : c->fwd) HIPCHK(c, run_launch(c, l, lr));
-  HIPCHK(c, run_launch(c, c->ce, lr));
-  for (auto& l : c->bwd) HIPCHK(c, run_launch(c, l, lr));
+  HIPCHK(c, enqueue_step(c, lr));
   for (size_t i = 0; i < n; ++i)
     if (c->active[i]) ++c->opts[i].t;
   c->stepped = true;
@@ -1844,6 +1890,66 @@ un_status un_set_active(un_ctx* c, const uint8_t* mask) {
   return UN_OK;
 }
 
+un_status un_set_stream(un_ctx* c, void* stream) {
+  CHECK_CTX(c);
+  HIPCHK(c, hipStreamSynchronize(c->stream));  // the work enqueued so far completes first
+  c->stream = stream ? (hipStream_t)stream : c->own_stream;
+  c->graph_valid = false;
+  return UN_OK;
+}
+
+un_status un_graph_capture(un_ctx* c, float lr) {
+  CHECK_CTX(c);
+  if (!c->loaded) return fail(c, UN_ERR_STATE, "un_graph_capture before un_load_batch");
+  if (!std::isfinite(lr)) return fail(c, UN_ERR_INVALID, "lr is not finite");
+  if (c->any_opt)
+    return fail(c, UN_ERR_UNSUPPORTED, "a model has a momentum / Adam optimizer (its hyper-parameters change every step)");
+  HIPCHK(c, hipStreamSynchronize(c->stream));
+  if (c->gexec) hipGraphExecDestroy(c->gexec);
+  if (c->graph) hipGraphDestroy(c->graph);
+  c->gexec = nullptr;
+  c->graph = nullptr;
+  c->graph_valid = false;
+  const bool prof = c->profiling;
+  c->profiling = false;  // no event records inside the graph
+  hipError_t e = hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal);
+  hipError_t le = e == hipSuccess ? enqueue_step(c, lr) : hipSuccess;
+  hipGraph_t g = nullptr;
+  if (e == hipSuccess) e = hipStreamEndCapture(c->stream, &g);
+  c->profiling = prof;
+  if (e == hipSuccess) e = le;
+  if (e == hipSuccess) e = hipGraphInstantiate(&c->gexec, g, nullptr, nullptr, 0);
+  if (e != hipSuccess) {
+    if (g) hipGraphDestroy(g);
+    c->gexec = nullptr;
+    c->poisoned = true;
+    return fail(c, UN_ERR_DEVICE, std::string("step capture: ") + hipGetErrorString(e));
+  }
+  c->graph = g;
+  c->graph_valid = true;
+  c->graph_keep = c->keep_grads;
+  c->graph_labels = c->labels_per_model;
+  return UN_OK;
+}
+
+un_status un_graph_step(un_ctx* c, float* losses) {
+  CHECK_CTX(c);
+  if (!c->graph_valid || c->graph_keep != c->keep_grads || c->graph_labels != c->labels_per_model || c->any_opt)
+    return fail(c, UN_ERR_STATE, "no captured step for the current configuration (un_graph_capture)");
+  HIPCHK(c, hipGraphLaunch(c->gexec, c->stream));
+  for (size_t i = 0; i < c->models.size(); ++i)
+    if (c->active[i]) ++c->opts[i].t;
+  c->stepped = true;
+  c->grads_valid = c->keep_grads;
+  if (losses) {
+    HIPCHK(c, hipMemcpyAsync(losses, c->base + c->losses_dev, c->models.size() * 4, hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipStreamSynchronize(c->stream));
+    for (size_t i = 0; i < c->models.size(); ++i)
+      if (!c->active[i]) losses[i] = std::nanf("");
+  }
+  return UN_OK;
+}
+
 un_status un_param_count(const un_ctx* c, int32_t i, size_t* n) {
   if (!c || !n) return fail(const_cast<un_ctx*>(c), UN_ERR_INVALID, "NULL argument");
   if (i < 0 || i >= (int)c->models.size()) return fail(const_cast<un_ctx*>(c), UN_ERR_RANGE, "model index out of range");
@@ -1882,7 +1988,7 @@ un_status un_set_params(un_ctx* c, int32_t i, const float* src, size_t n) {
   HIPCHK(c, hipStreamSynchronize(c->stream));
   un_status s = write_params(c, i, src);
   if (s != UN_OK) return s;
-  s = refresh_copies(c);
+  s = refresh_copies(c, i);
   if (s != UN_OK) return s;
   HIPCHK(c, hipStreamSynchronize(c->stream));
   return UN_OK;
@@ -1943,9 +2049,11 @@ void un_destroy(un_ctx* c) {
     hipEventDestroy(r.b);
   }
   for (auto e : c->free_events) hipEventDestroy(e);
+  if (c->gexec) hipGraphExecDestroy(c->gexec);
+  if (c->graph) hipGraphDestroy(c->graph);
   if (c->base) hipFree(c->base);
   if (c->sbase) hipFree(c->sbase);
-  if (c->stream) hipStreamDestroy(c->stream);
+  if (c->own_stream) hipStreamDestroy(c->own_stream);
   delete c;
 }
 

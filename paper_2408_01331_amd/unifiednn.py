@@ -30,6 +30,7 @@ KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad"
 EXPORTS = ["un_create", "un_plan_bytes", "un_load_batch", "un_load_batch_device", "un_load_labels", "un_step", "un_step_lr",
            "un_set_active", "un_set_optimizer", "un_get_opt_state", "un_set_opt_state", "un_get_params",
            "un_set_params", "un_get_grads", "un_keep_grads", "un_param_count", "un_arena_bytes", "un_sync", "un_get_stream",
+           "un_set_stream", "un_graph_capture", "un_graph_step",
            "un_profile_enable", "un_profile_read", "un_destroy", "un_last_error"]
 
 
@@ -94,6 +95,9 @@ def lib():
             "un_arena_bytes": (ctypes.c_int, [P, c_size_p]),
             "un_sync": (ctypes.c_int, [P]),
             "un_get_stream": (ctypes.c_int, [P, ctypes.POINTER(P)]),
+            "un_set_stream": (ctypes.c_int, [P, P]),
+            "un_graph_capture": (ctypes.c_int, [P, ctypes.c_float]),
+            "un_graph_step": (ctypes.c_int, [P, f]),
             "un_profile_enable": (ctypes.c_int, [P, ctypes.c_int32]),
             "un_profile_read": (ctypes.c_int, [P, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
                                                ctypes.POINTER(ctypes.c_int64)]),
@@ -270,6 +274,26 @@ def un_get_stream(ctx):
     return s.value
 
 
+def un_set_stream(ctx, stream):
+    """Run the context's work on `stream` (a hipStream_t as an int, e.g.
+    torch.cuda.Stream().cuda_stream); None returns to the context's own."""
+    _check(lib().un_set_stream(ctx, ctypes.c_void_p(stream) if stream else None), ctx)
+
+
+def un_graph_capture(ctx, lr):
+    _check(lib().un_graph_capture(ctx, ctypes.c_float(lr)), ctx)
+
+
+def un_graph_step(ctx, n_models=None):
+    """Replay the captured step; returns the losses if n_models is given."""
+    if n_models is None:
+        _check(lib().un_graph_step(ctx, None), ctx)
+        return None
+    out = np.zeros(n_models, dtype=np.float32)
+    _check(lib().un_graph_step(ctx, _fp(out)), ctx)
+    return out
+
+
 def un_arena_bytes(ctx):
     n = ctypes.c_size_t()
     _check(lib().un_arena_bytes(ctx, ctypes.byref(n)), ctx)
@@ -375,6 +399,17 @@ class Hybrid:
 
     def keep_grads(self, on=True):
         un_keep_grads(self.ctx, on)
+
+    def capture(self, lr):
+        """Capture one step at rate lr as a HIP graph (un_graph_capture)."""
+        un_graph_capture(self.ctx, lr)
+
+    def replay(self, losses=True):
+        """One step by replaying the captured graph (un_graph_step)."""
+        return un_graph_step(self.ctx, self.n if losses else None)
+
+    def set_stream(self, stream):
+        un_set_stream(self.ctx, stream)
 
     def sync(self):
         un_sync(self.ctx)
