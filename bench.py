@@ -155,7 +155,11 @@ def run_gpu(wl, steps, warmup):
 
 
 def run_unfused(wl, steps, warmup):
-    """N separate one-model contexts stepped back to back (same kernels, no fusion)."""
+    """N separate one-model contexts stepped back to back (same kernels, no
+    fusion): (a) each model's step waited for before the next one starts, and
+    (b) all contexts on one stream, every step enqueued without host
+    synchronisation (ordered by the stream alone). Returns (seconds of (a),
+    seconds of (b), summed arena bytes)."""
     import torch
     from paper_2408_01331_amd import unifiednn as U
 
@@ -178,11 +182,55 @@ def run_unfused(wl, steps, warmup):
             h.step(wl.lr, losses=False)
             h.sync()        # back to back: each model's step completes before the next starts
     torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
+    synced = time.perf_counter() - t0
+    stream = torch.cuda.Stream()
+    for h in hs:
+        h.set_stream(stream.cuda_stream)
+    for h in hs:
+        h.step(wl.lr, losses=False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        for h in hs:
+            h.step(wl.lr, losses=False)
+    torch.cuda.synchronize()
+    queued = time.perf_counter() - t0
     arena = sum(U.un_arena_bytes(h.ctx) for h in hs)
     for h in hs:
+        h.set_stream(None)
         h.close()
-    return elapsed, arena
+    return synced, queued, arena
+
+
+def run_latency(wl, steps, warmup):
+    """ms per step of a launch-latency-bound workload, enqueued step by step
+    (un_step) and replayed from one captured graph (un_graph_step)."""
+    import torch
+    from paper_2408_01331_amd import unifiednn as U
+
+    torch.cuda.set_device(0)
+    out = {}
+    with U.Hybrid(wl.specs, wl.batch, wl.in_shape, wl.precision) as h:
+        for i in range(wl.n_models):
+            h.set_params(i, U.flatten_params(W.init_params(wl.specs[i], wl.in_shape, wl.seed, i, wl.init)))
+        x, y = W.make_batch(wl, 0)
+        h.load_batch(x, y)
+        h.capture(wl.lr)
+        for mode in ("eager", "graph"):
+            run = (lambda: h.step(wl.lr, losses=False)) if mode == "eager" else (lambda: h.replay(losses=False))
+            for _ in range(warmup):
+                run()
+            h.sync()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                run()
+            h.sync()
+            torch.cuda.synchronize()
+            out[f"ms_per_step_{mode}"] = (time.perf_counter() - t0) / steps * 1e3
+    out["model_samples_per_s_graph"] = wl.n_models * wl.batch / (out["ms_per_step_graph"] / 1e3)
+    out["steps"] = steps
+    return out
 
 
 def copy_probe(nbytes=1 << 30, reps=4):
@@ -219,9 +267,10 @@ def measured_traffic(kernel, workload):
     return rec["hbm_bytes_per_launch"], path
 
 
-def cpu_baseline(wl, budget_s=12.0):
+def cpu_baseline(wl, budget_s=12.0, single_thread_s=6.0):
     """The oracle (as it stands) on a bounded sample: whole one-model steps on
-    the same batch, models taken in turn (cycling) until the budget is spent."""
+    the same batch, models taken in turn (cycling) until the budget is spent;
+    then the same with the BLAS library limited to one thread."""
     import oracle
 
     try:
@@ -243,10 +292,27 @@ def cpu_baseline(wl, budget_s=12.0):
         if time.perf_counter() - t0 > budget_s:
             break
     el = time.perf_counter() - t0
+    one = None
+    try:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            t1, n1 = time.perf_counter(), 0
+            while True:
+                i = n1 % wl.n_models
+                oracle.step(wl.specs[i], params.setdefault(i, W.init_params(wl.specs[i], wl.in_shape, wl.seed, i,
+                                                                            wl.init)), x, y, wl.lr, wl.precision)
+                n1 += 1
+                if time.perf_counter() - t1 > single_thread_s:
+                    break
+            one = {"value": n1 * wl.batch / (time.perf_counter() - t1), "cores": 1,
+                   "sample": f"{n1} one-model steps with BLAS limited to 1 thread"}
+    except Exception:
+        pass
     return {"value": done * wl.batch / el, "unit": "model-samples/s",
             "cores": blas_threads if blas_threads else cores, "host_cpus": cores, "kind": "oracle",
             "sample": f"{done} one-model steps (models 0..{min(done, wl.n_models) - 1} of {wl.n_models} in turn, "
-                      f"batch {wl.batch}) in {el:.1f} s, numpy fp64 with BLAS threads={blas_threads}"}
+                      f"batch {wl.batch}) in {el:.1f} s, numpy fp64 with BLAS threads={blas_threads}",
+            "single_thread": one}
 
 
 def measure(wl, steps, warmup):
@@ -257,9 +323,12 @@ def measure(wl, steps, warmup):
     value = wl.n_models * wl.batch / (ms_step / 1e3)
     mfma_peak = PEAK["bf16_mfma_tflops"] if wl.precision == "bf16" else PEAK["f32_mfma_tflops"]
     total_flops = sum(flops.values())
-    # Kernel symbols: the grouped GEMM serves both gemm_fwd and gemm_bwd launches.
-    sym = {"gemm": ["gemm_fwd", "gemm_bwd"], "conv_fwd": ["conv_fwd"], "conv_dgrad": ["conv_dgrad"],
-           "conv_wgrad": ["conv_wgrad"], "ce": ["ce"], "sgd": ["sgd"], "other": ["other"]}
+    # One entry per kernel: the forward and the backward grouped GEMM are two
+    # instantiations of gemm_kernel (row-major operands / k-major operands
+    # with the update in the epilogue), timed and bounded apart.
+    sym = {"gemm_fwd": ["gemm_fwd"], "gemm_bwd": ["gemm_bwd"], "conv_fwd": ["conv_fwd"],
+           "conv_dgrad": ["conv_dgrad"], "conv_wgrad": ["conv_wgrad"], "ce": ["ce"], "sgd": ["sgd"],
+           "other": ["other"]}
     per_sym = {}
     for name, classes in sym.items():
         ms = sum(kern[c]["ms_per_step"] for c in classes if c in kern)
@@ -326,6 +395,8 @@ def main():
     ap.add_argument("--workload", default="mlp64", choices=list(W.WORKLOADS))
     ap.add_argument("--also", default="cifar16,resnet8",
                     help="comma-separated workloads also timed and reported under other_workloads ('' for none)")
+    ap.add_argument("--latency", default="mlp2,mlp8,lenet4",
+                    help="launch-latency-bound workloads timed with and without graph replay ('' for none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
@@ -360,16 +431,23 @@ def main():
     others = {}
     for name in [w for w in args.also.split(",") if w and w != wl.name]:
         owl = W.get(name)
-        others[name] = measure(owl, max(5, args.steps // 5), max(2, args.warmup // 5))
+        others[name] = measure(owl, args.steps, args.warmup)
     if others:
         out["other_workloads"] = others
+    lat = {}
+    for name in [w for w in args.latency.split(",") if w]:
+        lat[name] = run_latency(W.get(name), args.steps, args.warmup)
+    if lat:
+        out["latency_workloads"] = lat
     if not args.no_unfused:
         usteps = max(3, args.steps // 5)
-        ue, uarena = run_unfused(wl, usteps, 2)
+        ue, uq, uarena = run_unfused(wl, usteps, 2)
         out["unfused_baseline"] = {
             "value": wl.n_models * wl.batch / (ue / usteps), "unit": "model-samples/s",
             "ms_per_round": ue / usteps * 1e3, "arena_bytes_sum": uarena,
-            "what": f"{wl.n_models} one-model contexts, each stepped and synchronised in turn"}
+            "what": f"{wl.n_models} one-model contexts, each stepped and synchronised in turn",
+            "queued": {"value": wl.n_models * wl.batch / (uq / usteps), "ms_per_round": uq / usteps * 1e3,
+                       "what": "the same contexts on one stream, all steps enqueued without host synchronisation"}}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl)
     print(json.dumps(out), flush=True)

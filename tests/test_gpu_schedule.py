@@ -12,7 +12,7 @@ import pytest
 
 from paper_2408_01331_amd import workloads as W
 from paper_2408_01331_amd.scheduler import Schedule, train
-from _parity import compare_run, theta0
+from _parity import compare_run, oracle_spread, theta0
 
 pytestmark = pytest.mark.gpu
 
@@ -128,22 +128,24 @@ def test_masked_run_matches_the_oracle_on_each_models_batches(name, models):
     models = list(range(wl.n_models)) if models is None else models
     for i in models:
         on = [s for s, m in enumerate(masks) if m[i]]
-        orc = _oracle_on_steps(wl, i, on)   # model i alone on the batches of its active steps
+        orc, spread = _oracle_on_steps(wl, i, on)   # model i alone on the batches of its active steps
         shapes = [sh for sh, _ in W.param_shapes(wl.specs[i], wl.in_shape)]
         L = np.full((len(on), wl.n_models), np.nan, dtype=np.float32)
         L[:, i] = losses[on, i]
         gpu = (L, {i: split_params(params[i], shapes)}, {i: split_params(grads[i], shapes)})
-        worst = compare_run(wl, gpu, {i: orc}, [i])
+        worst = compare_run(wl, gpu, {i: orc}, [i], spread={i: spread})
         print(f"\n[{wl.name} model {i}, steps {on}] " + ", ".join(f"{k}={v:.3g}" for k, v in worst.items()),
               flush=True)
 
 
 def _oracle_on_steps(wl, i, steps):
+    """Model i alone on the batches of the listed steps, and the spread of the
+    oracle's two evaluation orders over them."""
     import oracle
     batches = [W.make_batch(wl, s) for s in steps]
     out = oracle.train_models(wl.specs, {i: theta0(wl, i)}, batches, wl.lr, wl.precision, models=[i],
                               with_flags=True)
-    return out[i]
+    return out[i], oracle_spread(wl.specs[i], theta0(wl, i), batches, wl.lr, wl.precision, out[i][3], out[i][:3])
 
 
 def test_fcfs_schedule_releases_each_model_as_trained_alone():
