@@ -256,6 +256,21 @@ un_status un_get_opt_state(un_ctx* ctx, int32_t i, float* dst, size_t cap_elems,
  * UN_ERR_INVALID (negative step, NULL src). */
 un_status un_set_opt_state(un_ctx* ctx, int32_t i, const float* src, size_t n_elems, int64_t step);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): un_step
+ * with the step's workspace - the conv weight-gradient split-K partial sums
+ * and the per-model loss partials, which a step writes and reads back within
+ * itself - in one static device array of the library (32 MiB per device,
+ * held until the process ends) instead of the context's arena. Results equal
+ * un_step's bit for bit. Allocates nothing: the array is a file-scope
+ * device variable whose address is looked up once per device. Every call on
+ * one device shares that array (it keeps the last call's contents; nothing in
+ * it needs to start at zero), so calls that overlap on one device - steps of
+ * two contexts on two streams at once - race; serialise them.
+ * Errors: as un_step, and UN_ERR_UNSUPPORTED (nothing runs) when this
+ * context's workspace exceeds the array (wide CNN hybrids; use un_step). */
+un_status un_step_scratch(un_ctx* ctx, float lr, float* losses);
+
 /* Number of parameters of model i. */
 un_status un_param_count(const un_ctx* ctx, int32_t i, size_t* n_elems);
 

@@ -19,6 +19,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -93,7 +94,18 @@ struct EventRec {
 
 thread_local std::string g_create_error;
 
+constexpr size_t UN_SCRATCH_BYTES = (size_t)32 << 20;
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[MAX_DEVICES] = {};
+
 }  // namespace
+
+// Workspace of un_step_scratch, one array per device for the life of the
+// process. In host code `scratch` is only a stand-in for the device array:
+// its device address comes from hipGetSymbolAddress (scratch_on), once per
+// device, and only that address is ever handed to kernels.
+static __device__ __align__(256) char scratch[UN_SCRATCH_BYTES];
 
 struct un_ctx {
   bool bf16 = false;
@@ -1888,6 +1900,44 @@ un_status un_set_active(un_ctx* c, const uint8_t* mask) {
   HIPCHK(c, hipStreamSynchronize(c->stream));
   c->grads_valid = false;
   return UN_OK;
+}
+
+// Device address of the scratch array on the context's device (looked up with
+// that device current, the first time only).
+static un_status scratch_on(un_ctx* c, char** out) {
+  if (c->device < 0 || c->device >= MAX_DEVICES) return fail(c, UN_ERR_UNSUPPORTED, "device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[c->device]) {
+    int cur = 0;
+    HIPCHK(c, hipGetDevice(&cur));
+    if (cur != c->device) HIPCHK(c, hipSetDevice(c->device));
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (cur != c->device) HIPCHK(c, hipSetDevice(cur));
+    HIPCHK(c, e);
+    if (!p) return fail(c, UN_ERR_DEVICE, "hipGetSymbolAddress returned no address for the scratch array");
+    g_scratch_ptr[c->device] = (char*)p;
+  }
+  *out = g_scratch_ptr[c->device];
+  return UN_OK;
+}
+
+un_status un_step_scratch(un_ctx* c, float lr, float* losses) {
+  CHECK_CTX(c);
+  if (!c->loaded) return fail(c, UN_ERR_STATE, "un_step_scratch before un_load_batch");
+  if (!std::isfinite(lr)) return fail(c, UN_ERR_INVALID, "lr is not finite");
+  if (c->ws_bytes > UN_SCRATCH_BYTES)
+    return fail(c, UN_ERR_UNSUPPORTED, "this context's step workspace (" + std::to_string(c->ws_bytes) +
+                                           " bytes) exceeds the library's static scratch (" +
+                                           std::to_string(UN_SCRATCH_BYTES) + " bytes); use un_step");
+  char* ptr = nullptr;
+  un_status st = scratch_on(c, &ptr);
+  if (st != UN_OK) return st;
+  // every workspace pointer of the tables moves by the same offset into the scratch array
+  c->wsoff = (int64_t)(ptr - (c->base + c->ws_lo));
+  st = step_common(c, lr, nullptr, losses);
+  c->wsoff = 0;
+  return st;
 }
 
 un_status un_set_stream(un_ctx* c, void* stream) {

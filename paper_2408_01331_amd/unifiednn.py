@@ -30,7 +30,7 @@ KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad"
 EXPORTS = ["un_create", "un_plan_bytes", "un_load_batch", "un_load_batch_device", "un_load_labels", "un_step", "un_step_lr",
            "un_set_active", "un_set_optimizer", "un_get_opt_state", "un_set_opt_state", "un_get_params",
            "un_set_params", "un_get_grads", "un_keep_grads", "un_param_count", "un_arena_bytes", "un_sync", "un_get_stream",
-           "un_set_stream", "un_graph_capture", "un_graph_step",
+           "un_set_stream", "un_graph_capture", "un_graph_step", "un_step_scratch",
            "un_profile_enable", "un_profile_read", "un_destroy", "un_last_error"]
 
 
@@ -98,6 +98,7 @@ def lib():
             "un_set_stream": (ctypes.c_int, [P, P]),
             "un_graph_capture": (ctypes.c_int, [P, ctypes.c_float]),
             "un_graph_step": (ctypes.c_int, [P, f]),
+            "un_step_scratch": (ctypes.c_int, [P, ctypes.c_float, f]),
             "un_profile_enable": (ctypes.c_int, [P, ctypes.c_int32]),
             "un_profile_read": (ctypes.c_int, [P, ctypes.c_int32, ctypes.POINTER(ctypes.c_double),
                                                ctypes.POINTER(ctypes.c_int64)]),
@@ -272,6 +273,17 @@ def un_get_stream(ctx):
     s = ctypes.c_void_p()
     _check(lib().un_get_stream(ctx, ctypes.byref(s)), ctx)
     return s.value
+
+
+def un_step_scratch(ctx, lr, n_models=None):
+    """un_step with the step's workspace in the library's static scratch
+    array (no allocation); returns the losses if n_models is given."""
+    if n_models is None:
+        _check(lib().un_step_scratch(ctx, ctypes.c_float(lr), None), ctx)
+        return None
+    out = np.zeros(n_models, dtype=np.float32)
+    _check(lib().un_step_scratch(ctx, ctypes.c_float(lr), _fp(out)), ctx)
+    return out
 
 
 def un_set_stream(ctx, stream):
