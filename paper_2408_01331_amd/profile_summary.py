@@ -10,6 +10,12 @@
         `rocprofv3 --pmc FETCH_SIZE` and one `--pmc WRITE_SIZE` run of the
         benchmark, each scaled by what the same counter reads for a plain
         elementwise copy of known size (`bench.py --copy-probe`)
+
+    python -m paper_2408_01331_amd.profile_summary pmc --trace DIR --counters DIR [DIR ...]
+        per kernel instantiation: dispatches, average kernel time (from the
+        kernel trace), and per dispatch the counters of `rocprofv3 --pmc`
+        runs, with MFMA throughput from the MFMA op counters, MFMA-busy and
+        wait shares, and the HBM request mix (32 / 64 / 128-byte reads)
 """
 from __future__ import annotations
 
@@ -87,17 +93,80 @@ def traffic(a):
     print(json.dumps(rec))
 
 
+def per_kernel(d):
+    """{kernel name: {counter: [value per dispatch]}} of a --pmc run."""
+    rows = collections.defaultdict(lambda: collections.defaultdict(float))
+    names = {}
+    for r in csv.DictReader(open(_one(os.path.join(d, "**", "*counter_collection.csv")))):
+        rows[r["Dispatch_Id"]][r["Counter_Name"]] += float(r["Counter_Value"])
+        names[r["Dispatch_Id"]] = r["Kernel_Name"]
+    out = collections.defaultdict(lambda: collections.defaultdict(list))
+    for disp, cs in rows.items():
+        for c, v in cs.items():
+            out[names[disp]][c].append(v)
+    return out
+
+
+def short(name):
+    return name.replace("unsigned short", "bf16").split("(")[0].replace("void ", "")
+
+
+def pmc(a):
+    """MFMA / wait / request-mix table per kernel instantiation."""
+    trace = list(csv.DictReader(open(_one(os.path.join(a.trace, "**", "*kernel_stats.csv")))))
+    avg_ns = {r["Name"]: float(r["AverageNs"]) for r in trace}
+    merged = collections.defaultdict(dict)
+    for d in a.counters:
+        for k, cs in per_kernel(d).items():
+            for c, vals in cs.items():
+                merged[k][c] = sum(vals) / len(vals)
+    peak_bf16 = 2500.0  # TFLOP/s, dense bf16 MFMA
+    rows = []
+    for k, cs in merged.items():
+        if not any(x in k for x in a.match):
+            continue
+        t = avg_ns.get(k)
+        rec = {"kernel": short(k), "avg_us": t / 1e3 if t else None}
+        rec.update({c: v for c, v in sorted(cs.items())})
+        mops = cs.get("SQ_INSTS_VALU_MFMA_MOPS_BF16")
+        if mops is not None and t:
+            rec["mfma_tflops"] = mops * 512 / (t * 1e-9) / 1e12
+            rec["mfma_frac_bf16_peak"] = rec["mfma_tflops"] / peak_bf16
+        wave = cs.get("SQ_WAVE_CYCLES")
+        if wave:
+            for c in ("SQ_WAIT_ANY", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_VMEM", "SQ_VALU_MFMA_BUSY_CYCLES"):
+                if c in cs:
+                    rec[c + "/SQ_WAVE_CYCLES"] = cs[c] / wave
+        if cs.get("SQ_BUSY_CYCLES") and "SQ_VALU_MFMA_BUSY_CYCLES" in cs:
+            rec["MFMA_BUSY/SQ_BUSY"] = cs["SQ_VALU_MFMA_BUSY_CYCLES"] / cs["SQ_BUSY_CYCLES"]
+        rd = cs.get("TCC_EA0_RDREQ_sum")
+        if rd:
+            b128 = cs.get("TCC_BUBBLE_sum", 0.0)
+            b32 = cs.get("TCC_EA0_RDREQ_32B_sum", 0.0)
+            rec["read_req_mix_32_64_128"] = [b32 / rd, (rd - b32 - b128) / rd, b128 / rd]
+            rec["read_bytes_from_requests"] = b32 * 32 + (rd - b32 - b128) * 64 + b128 * 128
+        rows.append(rec)
+    rows.sort(key=lambda r: -(r["avg_us"] or 0))
+    print(json.dumps(rows, indent=1))
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
     s = sub.add_parser("stats")
     s.add_argument("dir")
+    m = sub.add_parser("pmc")
+    m.add_argument("--trace", required=True)
+    m.add_argument("--counters", nargs="+", required=True)
+    m.add_argument("--match", nargs="+", default=["gemm_kernel", "conv_", "reduce_kernel", "elementwise"])
     t = sub.add_parser("traffic")
     for k in ("kernel", "workload", "fetch", "write", "copy_fetch", "copy_write", "out"):
         t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
     a = ap.parse_args()
     if a.cmd == "stats":
         stats(a.dir)
+    elif a.cmd == "pmc":
+        pmc(a)
     else:
         traffic(a)
 
