@@ -122,6 +122,21 @@ typedef struct {
 un_status un_create(const un_model_spec* specs, int32_t n_models,
                     const un_input_spec* in, un_ctx** out);
 
+/* As un_create, for models that train on different datasets (Algorithm 2
+ * gives every sub-model its own batches; each sub-model's hyper-parameters
+ * include its input size and batch size, Model Unifier section). inputs[g]
+ * (g < n_groups) describes input group g: its batch size and sample shape
+ * (precision equal for all groups). Model i reads group group_of[i] (host
+ * int32 [n_models]; may be NULL when n_groups == 1). Each group is one
+ * dataset: its batch is copied to the device once (un_load_group_batch) and
+ * read by all of its models, and the first hidden Linear layers of a group's
+ * models still run as one GEMM. Models of different groups differ in batch
+ * size and input shape freely. n_groups == 1 is un_create. Every group must
+ * hold at least one model. Errors as un_create, and UN_ERR_RANGE (a group
+ * index out of range). */
+un_status un_create_grouped(const un_model_spec* specs, int32_t n_models, const un_input_spec* inputs,
+                            int32_t n_groups, const int32_t* group_of, un_ctx** out);
+
 /* Device memory a context for these models would take, computed on the host
  * without touching the device (the planner of un_create, dry): *arena_bytes is
  * exactly what un_create allocates (un_arena_bytes), *state_bytes (may be
@@ -134,12 +149,25 @@ un_status un_create(const un_model_spec* specs, int32_t n_models,
 un_status un_plan_bytes(const un_model_spec* specs, int32_t n_models, const un_input_spec* in,
                         size_t* arena_bytes, size_t* state_bytes);
 
+/* un_plan_bytes for un_create_grouped's arguments. */
+un_status un_plan_bytes_grouped(const un_model_spec* specs, int32_t n_models, const un_input_spec* inputs,
+                                int32_t n_groups, const int32_t* group_of, size_t* arena_bytes,
+                                size_t* state_bytes);
+
 /* Copy one shared batch to the device, once for all N models (Memory
  * conservation section: a common dataset is loaded only once). x is host fp32
  * laid out as in un_input_spec, y is host int32 [batch]. Labels are checked on
  * the host: a label outside [0, num_classes) of any model returns UN_ERR_RANGE
- * and leaves the previously loaded batch in place. Synchronous. */
+ * and leaves the previously loaded batch in place. Synchronous. With several
+ * input groups: UN_ERR_INVALID (use un_load_group_batch). */
 un_status un_load_batch(un_ctx* ctx, const float* x, const int32_t* y);
+
+/* un_load_batch for input group g of a un_create_grouped context: x [batch_g,
+ * shape of group g] fp32, y int32 [batch_g], labels checked against the
+ * models of group g. A step runs only once every group has a batch loaded;
+ * loaded batches stay until replaced. Errors as un_load_batch, and
+ * UN_ERR_RANGE (g). */
+un_status un_load_group_batch(un_ctx* ctx, int32_t g, const float* x, const int32_t* y);
 
 /* As un_load_batch, with x and y already in device memory (same layouts). The
  * buffers are read on the context's stream (un_get_stream): the caller orders
@@ -149,12 +177,14 @@ un_status un_load_batch(un_ctx* ctx, const float* x, const int32_t* y);
  * the batch has been converted, after which x_dev and y_dev may be reused. */
 un_status un_load_batch_device(un_ctx* ctx, const float* x_dev, const int32_t* y_dev);
 
-/* Labels per model for the batch already loaded (Algorithm 2 gives every
- * sub-model its own batches; the input x stays shared). y is host int32
- * [N][batch], row i holding model i's labels, each in [0, num_classes of
- * model i) or UN_ERR_RANGE (nothing changes). They replace the labels of the
- * last un_load_batch until the next un_load_batch, which goes back to one
- * label row for all models. Synchronous. UN_ERR_STATE before any batch. */
+/* Labels per model for the batches already loaded (Algorithm 2 gives every
+ * sub-model its own batches; the inputs x stay those of the input groups).
+ * y is host int32: model 0's labels, then model 1's, ..., each row as long as
+ * its model's batch ([N][batch] with one input group), each label in
+ * [0, num_classes of the model) or UN_ERR_RANGE (nothing changes). They
+ * replace the labels of the groups' batches until the next un_load_batch /
+ * un_load_group_batch, which goes back to the group labels. Synchronous.
+ * UN_ERR_STATE before every group has a batch. */
 un_status un_load_labels(un_ctx* ctx, const int32_t* y);
 
 /* One fused training step of all N models on the loaded batch (Algorithm 2's

@@ -8,7 +8,10 @@ companions, or alone.
 
 Tensor names follow the PyTorch ``nn.Sequential`` built from the model's spec:
 ``"<layer index>.weight"`` / ``"<layer index>.bias"`` (the file's parameters
-load into that module with ``load_state_dict``), and the optimizer state is
+load into that module with ``load_state_dict``). A residual block is one
+child of that Sequential, a module with an ``inner`` Sequential of the
+enclosed layers whose forward returns ``inner(x) + x``: its layers are named
+``"<block index>.inner.<layer index in the block>.weight"``. The optimizer state is
 stored as ``"momentum_buffer.<name>"`` (SGD with momentum) or
 ``"exp_avg.<name>"`` / ``"exp_avg_sq.<name>"`` (Adam). The metadata holds the
 spec, the input shape, the precision, the optimizer and the update count.
@@ -28,11 +31,27 @@ STATE_NAMES = {"sgd": [], "momentum": ["momentum_buffer"], "adam": ["exp_avg", "
 
 
 def param_names(spec):
-    """state_dict names of the parameterised layers of ``spec``, in order."""
+    """state_dict names of the parameterised layers of ``spec``, in order: the
+    index of the layer in the Sequential, where a residual block (its markers
+    and the layers between them) is one child holding an ``inner`` Sequential."""
     names = []
-    for k, layer in enumerate(spec["layers"]):
-        if layer[0] in ("linear", "conv"):
-            names += [f"{k}.weight", f"{k}.bias"]
+    k, j, inside = 0, 0, False
+    for layer in spec["layers"]:
+        op = layer[0]
+        if op == "res_begin":
+            inside, j = True, 0
+            continue
+        if op == "res_end":
+            inside = False
+            k += 1
+            continue
+        prefix = f"{k}.inner.{j}" if inside else f"{k}"
+        if op in ("linear", "conv"):
+            names += [f"{prefix}.weight", f"{prefix}.bias"]
+        if inside:
+            j += 1
+        else:
+            k += 1
     return names
 
 
@@ -45,15 +64,16 @@ def model_state(hybrid, i):
     """Model i's checkpoint as (tensors, metadata)."""
     spec = hybrid.specs[i]
     opt = hybrid.optimizers[i]
-    tensors = _tensors(spec, hybrid.in_shape, hybrid.get_params(i))
+    in_shape = hybrid.in_shape_of(i)
+    tensors = _tensors(spec, in_shape, hybrid.get_params(i))
     state, step = hybrid.get_opt_state(i)
     names = STATE_NAMES[opt["kind"]]
     n = len(state) // len(names) if names else 0
     for k, sname in enumerate(names):
-        for pname, t in _tensors(spec, hybrid.in_shape, state[k * n:(k + 1) * n]).items():
+        for pname, t in _tensors(spec, in_shape, state[k * n:(k + 1) * n]).items():
             tensors[f"{sname}.{pname}"] = t
     meta = {"spec": json.dumps({"layers": [list(l) for l in spec["layers"]], "num_classes": spec["num_classes"]}),
-            "in_shape": json.dumps(list(hybrid.in_shape)), "precision": hybrid.precision,
+            "in_shape": json.dumps(list(in_shape)), "precision": hybrid.precision,
             "optimizer": json.dumps(opt), "step": str(int(step))}
     return {k: np.ascontiguousarray(v) for k, v in tensors.items()}, meta
 
@@ -85,7 +105,7 @@ def load(hybrid, i, path):
     spec = hybrid.specs[i]
     if [tuple(l) for l in spec["layers"]] != meta["spec"]["layers"] or spec["num_classes"] != meta["spec"]["num_classes"]:
         raise ValueError(f"checkpoint {path} holds a different architecture than model {i}")
-    if tuple(hybrid.in_shape) != meta["in_shape"]:
+    if tuple(hybrid.in_shape_of(i)) != meta["in_shape"]:
         raise ValueError(f"checkpoint {path} was trained on input shape {meta['in_shape']}")
     opt = meta["optimizer"]
     hybrid.set_optimizer(i, opt["kind"], opt["momentum"], tuple(opt["betas"]), opt["eps"])

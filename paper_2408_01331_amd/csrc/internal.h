@@ -62,6 +62,9 @@ struct GemmProb {
   // the tile's summed row losses go to ce_part[m-tile]. Null: C is the fp32
   // logits and a separate CE pass follows.
   float* ce_part;
+  // labels of the fused softmax-CE: labels + lab_shared (the model's input
+  // group row) or labels + lab_own (its own row, per-model labels)
+  int32_t lab_shared, lab_own;
   // Skip connection (residual blocks), row-major [m][n] in the storage type,
   // added in fp32 before the ReLU (FWD) or before the ReLU' mask (DGRAD):
   // FWD: the block's input x; DGRAD: the gradient at the block's output. Null: none.
@@ -176,6 +179,8 @@ struct CeProb {
   int32_t C;
   int32_t model;
   int32_t nchunks;            // loss partials of this model (row chunks or GEMM m-tiles)
+  int32_t B;                  // the model's batch (its input group's)
+  int32_t lab_shared, lab_own;  // its labels: labels + lab_shared (group row) or + lab_own (own row)
 };
 
 // ---------------------------------------------------------------------------
@@ -208,15 +213,16 @@ struct SgdTensor {
 // `opt` (device, one OptHp per model) replaces lr/lrv when not null.
 // bwd: the launch holds data- and weight-gradient problems (k-major operands),
 // else forward problems (row-major operands only).
-// labels / lab_stride: the labels of the fused softmax-CE (model m's at
-// labels + m * lab_stride; stride 0 when all models share one row).
+// labels / per_model_labels: the label buffer of the fused softmax-CE; a
+// model reads its own row (GemmProb::lab_own) when per_model_labels is set,
+// else its input group's row (lab_shared).
 // wsoff: byte offset added to every workspace pointer of the descriptors
 // (split-K partials GemmProb::ce_part, ConvProb::ws, ReduceProb::ws), so that
 // one set of tables serves the arena's workspace (0) or another buffer of the
 // same layout.
 hipError_t launch_gemm(bool bf16, bool bwd, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
-                       const float* lrv, const OptHp* opt, bool keep_grads, const int32_t* labels, int lab_stride,
-                       int64_t wsoff, hipStream_t s);
+                       const float* lrv, const OptHp* opt, bool keep_grads, const int32_t* labels,
+                       bool per_model_labels, int64_t wsoff, hipStream_t s);
 hipError_t launch_conv_fwd(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
                            hipStream_t s);
 hipError_t launch_conv_dgrad(bool bf16, const ConvProb* probs, const int32_t* tile_map, int ntiles,
@@ -233,9 +239,10 @@ hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_
 hipError_t launch_set_values(float* dst, const float* vals, int n, hipStream_t s);
 // probs: the first nrows problems need the row pass (their CE is not fused
 // into the logits GEMM); the loss of every one of the nprobs is finished.
-// Partials of model m are at partial + m * pstride.
+// Partials of model m are at partial + m * pstride; maxB is the largest
+// batch of the problems (each has its own, CeProb::B).
 hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, int nrows, const int32_t* labels,
-                     bool per_model_labels, int B, float* partial, int pstride, float* losses, hipStream_t s);
+                     bool per_model_labels, int maxB, float* partial, int pstride, float* losses, hipStream_t s);
 // The launch covers tiles [blk0, blk0 + ntiles) of the tile table.
 hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int blk0, int ntiles, float lr,
                       bool use_grad, hipStream_t s);

@@ -1210,13 +1210,14 @@ __device__ __forceinline__ void store_rows(const float* sC, OT* C, int64_t ldc, 
 // row order into ce_part[tm] (a workspace buffer: wsoff bytes added).
 template <typename T, int BM, int CLD, int NT>
 __device__ __forceinline__ void fused_softmax_ce(float* sC, const GemmProb& p, int m0, int tm,
-                                                 const int32_t* __restrict__ labels, int lab_stride, int64_t wsoff) {
+                                                 const int32_t* __restrict__ labels, int per_model_labels,
+                                                 int64_t wsoff) {
   constexpr int RPP = NT / CE_LANES;  // rows per pass
   static_assert(NT % CE_LANES == 0 && BM % RPP == 0, "whole rows per pass");
   __shared__ float s_loss[BM];
   const int sub = threadIdx.x % CE_LANES, C = p.N;
   const float invB = 1.0f / (float)p.M;
-  const int32_t* y = labels + (int64_t)p.model * lab_stride;
+  const int32_t* y = labels + (per_model_labels ? p.lab_own : p.lab_shared);
   for (int r0 = 0; r0 < BM; r0 += RPP) {
     const int rl = r0 + (int)threadIdx.x / CE_LANES, b = m0 + rl;
     const bool valid = b < p.M;
@@ -1272,7 +1273,7 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
                                                    const int32_t* __restrict__ tile_map, float lr,
                                                    const float* __restrict__ lrv, const OptHp* __restrict__ opt,
                                                    int keep_grads, const int32_t* __restrict__ labels,
-                                                   int lab_stride, int64_t wsoff) {
+                                                   int per_model_labels, int64_t wsoff) {
   using TL = Tile<T, BM, BN, BK>;
   using SM = Smem<T, BM, BN, BK>;
   __shared__ __attribute__((aligned(16))) char smem[SM::BYTES];
@@ -1364,7 +1365,7 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
 
   if (epi != EPI_WGRAD) {
     if (!BWD && epi == EPI_LOGITS && p.ce_part) {
-      fused_softmax_ce<T, BM, CLD, NT>(sC, p, m0, tm, labels, lab_stride, wsoff);
+      fused_softmax_ce<T, BM, CLD, NT>(sC, p, m0, tm, labels, per_model_labels, wsoff);
       return;
     }
     // Row pass: C[m][n] in 16-byte chunks along n (data gradient: with the
@@ -2126,15 +2127,18 @@ __device__ __forceinline__ float wave_sum(float v) {
 // classes strided over the row's lanes; max and sum over the row by a fixed
 // butterfly of lane shuffles. dz = (softmax - onehot)/B goes to G. Each
 // block sums its rows' losses in row order into partial[model][chunk];
-// ce_finish_kernel adds the chunks in order.
+// ce_finish_kernel adds the chunks in order. The grid covers the largest
+// batch; a model's blocks beyond its own batch exit.
 template <typename T>
 __global__ __launch_bounds__(CE_ROWS * CE_LANES) void ce_rows_kernel(const CeProb* __restrict__ probs,
                                                                      const int32_t* __restrict__ labels,
-                                                                     int per_model_labels, int B,
+                                                                     int per_model_labels,
                                                                      float* __restrict__ partial, int pstride) {
   __shared__ float rowloss[CE_ROWS];
   const CeProb& p = probs[blockIdx.y];
-  const int32_t* y = labels + (per_model_labels ? (int64_t)p.model * B : 0);
+  const int B = p.B;
+  if ((int)blockIdx.x * CE_ROWS >= B) return;  // uniform over the block
+  const int32_t* y = labels + (per_model_labels ? p.lab_own : p.lab_shared);
   const int rl = threadIdx.x / CE_LANES, sub = threadIdx.x % CE_LANES;
   const int b = blockIdx.x * CE_ROWS + rl;
   const int C = p.C;
@@ -2174,13 +2178,13 @@ __global__ __launch_bounds__(CE_ROWS * CE_LANES) void ce_rows_kernel(const CePro
 // slot: its partials (row chunks, or the m-tiles of its fused logits GEMM)
 // added in order.
 __global__ void ce_finish_kernel(const CeProb* __restrict__ probs, const float* __restrict__ partial, int pstride,
-                                 int nprobs, int B, float* __restrict__ losses) {
+                                 int nprobs, float* __restrict__ losses) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= nprobs) return;
   const int m = probs[i].model, n = probs[i].nchunks;
   float s = 0.f;
   for (int k = 0; k < n; ++k) s += partial[(int64_t)m * pstride + k];
-  losses[m] = s * (1.0f / (float)B);
+  losses[m] = s * (1.0f / (float)probs[i].B);
 }
 
 // ---------------------------------------------------------------------------
@@ -2253,12 +2257,12 @@ __global__ __launch_bounds__(256) void load_kernel(const float* __restrict__ x, 
 // Launch wrappers
 // ---------------------------------------------------------------------------
 hipError_t launch_gemm(bool bf16, bool bwd, const GemmProb* probs, const int32_t* tile_map, int ntiles, float lr,
-                       const float* lrv, const OptHp* opt, bool keep_grads, const int32_t* labels, int lab_stride,
-                       int64_t wsoff, hipStream_t s) {
+                       const float* lrv, const OptHp* opt, bool keep_grads, const int32_t* labels,
+                       bool per_model_labels, int64_t wsoff, hipStream_t s) {
   if (ntiles <= 0) return hipSuccess;
   auto go = [&](auto kern, int nt) {
     hipLaunchKernelGGL(kern, dim3(ntiles), dim3(nt), 0, s, probs, tile_map, lr, lrv, opt, (int)keep_grads, labels,
-                       lab_stride, wsoff);
+                       (int)per_model_labels, wsoff);
   };
   if (bf16) {
     constexpr int NT = GemmMma<bf16_t, GEMM_BM_BF16, GEMM_BN_BF16, GEMM_BK_BF16>::NT;
@@ -2396,19 +2400,19 @@ hipError_t launch_set_values(float* dst, const float* vals, int n, hipStream_t s
 }
 
 hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, int nrows, const int32_t* labels,
-                     bool per_model_labels, int B, float* partial, int pstride, float* losses, hipStream_t s) {
+                     bool per_model_labels, int maxB, float* partial, int pstride, float* losses, hipStream_t s) {
   if (nprobs <= 0) return hipSuccess;
-  const int nchunks = (B + CE_ROWS - 1) / CE_ROWS;
+  const int nchunks = (maxB + CE_ROWS - 1) / CE_ROWS;
   if (nrows > 0) {
     if (bf16)
       hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nrows), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels,
-                         (int)per_model_labels, B, partial, pstride);
+                         (int)per_model_labels, partial, pstride);
     else
       hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nrows), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels,
-                         (int)per_model_labels, B, partial, pstride);
+                         (int)per_model_labels, partial, pstride);
   }
   hipLaunchKernelGGL(ce_finish_kernel, dim3((nprobs + 63) / 64), dim3(64), 0, s, probs, partial, pstride, nprobs,
-                     B, losses);
+                     losses);
   return hipGetLastError();
 }
 

@@ -76,6 +76,29 @@ struct Model {
   int num_classes = 0;
   size_t n_params = 0;
   uint64_t seed = 0;
+  int group = 0;         // its input group
+  int64_t lab_own = 0;   // its own label row (per-model labels): ydev + lab_own int32 elements
+};
+
+// One input group: a dataset with its own batch and sample shape, copied to
+// the device once per batch and read by every model of the group (Memory
+// conservation: a common dataset is loaded only once). One group is the
+// shared-input case; a group per model gives every model its own data.
+struct Group {
+  int B = 0, in_c = 0, in_h = 0, in_w = 0;
+  int64_t in_feat = 0, ldxin = 0;
+  int in_cs = 0;                    // stored channels of XinC
+  size_t xstage = NONE, Xin = NONE, XinC = NONE;
+  int64_t lab_shared = 0;           // its label row: ydev + lab_shared int32 elements
+  int min_classes = 1 << 30;        // of its models (labels are checked against it)
+  bool loaded = false;
+  // the first hidden Linear layers of its models read the same input: their
+  // weights form one concatenated matrix, one GEMM problem per run of active models
+  int64_t kin_p = 0, cat_rows = 0;
+  std::vector<int> cat;             // models in the concatenation
+  size_t catW32 = NONE, catb32 = NONE, catgW = NONE, catgb = NONE, catWb = NONE, catY = NONE, catG = NONE;
+  size_t cat_row_model = NONE;      // int32 per concatenated row: the model owning it
+  size_t catS1 = NONE, catS1b = NONE, catS2 = NONE, catS2b = NONE;  // optimizer state (sbase)
 };
 
 struct Launch {
@@ -109,8 +132,9 @@ static __device__ __align__(256) char scratch[UN_SCRATCH_BYTES];
 
 struct un_ctx {
   bool bf16 = false;
-  int B = 0, in_c = 0, in_h = 0, in_w = 0;
-  int64_t Bp = 0;
+  std::vector<Group> groups;
+  int maxB = 0;                      // largest batch over the groups
+  int64_t lab_elems = 0;             // int32 labels: one row per group, then one per model
   std::vector<Model> models;
   int levels = 0;
   // arena
@@ -130,11 +154,10 @@ struct un_ctx {
   bool graph_valid = false;
   bool graph_keep = false, graph_labels = false;  // keep_grads / per-model labels when captured
   // fixed buffers
-  size_t xstage = NONE, ydev = NONE, losses_dev = NONE, ce_partial = NONE, Xin = NONE;
-  size_t XinC = NONE;  // NHWC input with channels padded to a 16-byte multiple (first convs only)
+  size_t ydev = NONE, losses_dev = NONE, ce_partial = NONE;
   size_t lr_dev = NONE;          // per-model learning rates of the current un_step_lr call
   const float* lrv = nullptr;    // lr_dev while such a step is being launched, else null (one rate)
-  bool labels_per_model = false; // ydev holds N rows of B labels (un_load_labels) instead of one
+  bool labels_per_model = false; // models read their own label rows (un_load_labels), not their group's
   // optimizers (un_set_optimizer): kind and hyper-parameters per model, and
   // the number of updates each model has taken under it
   struct Opt {
@@ -148,27 +171,21 @@ struct un_ctx {
   size_t sbytes = 0;
   size_t opt_dev = NONE;         // OptHp per model
   const OptHp* optp = nullptr;   // opt_dev while a step with optimizers is being launched
-  int in_cs = 0;       // stored channels of XinC
-  int64_t ldxin = 0;
   // schedule
   std::vector<Launch> fwd, bwd;
   Launch ce{}, refresh{};
   std::vector<std::pair<int, int>> refresh_rng;  // per model: its tiles [first, first + count) of `refresh`
   std::vector<char> active;          // models in the step (un_set_active)
   size_t tables_off = NONE, tables_cap = 0;  // arena region of the descriptor tables
-  // planning results the tables are built from
-  struct Plan {
-    int64_t in_feat = 0, kin_p = 0, cat_rows = 0;
-    std::vector<int> cat;        // models whose first layer is in the concatenated level-0 GEMM
-    std::vector<int64_t> cat_off;  // their first row in it (-1: not in it)
-    size_t catW32 = NONE, catb32 = NONE, catgW = NONE, catgb = NONE, catWb = NONE, catY = NONE, catG = NONE;
-    size_t cat_row_model = NONE;  // int32 per concatenated row: the model owning it
-    size_t catS1 = NONE, catS1b = NONE, catS2 = NONE, catS2b = NONE;  // state of the concatenation (sbase)
-  } plan;
+  std::vector<int64_t> cat_off;      // per model: its first row in its group's concatenation (-1: not in it)
   bool keep_grads = false, grads_valid = false;
   int ce_count = 0;
-  bool loaded = false, stepped = false, poisoned = false;
-  int min_classes = 0;
+  bool stepped = false, poisoned = false;
+  bool all_loaded() const {
+    for (auto& g : groups)
+      if (!g.loaded) return false;
+    return true;
+  }
   std::string err;
   // profiling
   bool profiling = false;
@@ -539,24 +556,21 @@ struct Tables {
 
 static void build_tables(un_ctx* c, Tables& T) {
   const bool bf = c->bf16;
-  const int B = c->B;
-  const int64_t Bp = c->Bp;
   const int levels = c->levels;
   const size_t es = bf ? 2 : 4;
-  const int64_t in_feat = c->plan.in_feat, kin_p = c->plan.kin_p, cat_rows = c->plan.cat_rows;
   auto sub = [](size_t off, int64_t bytes) { return off == NONE ? NONE : off + (size_t)bytes; };
-  const size_t catW32 = c->plan.catW32, catb32 = c->plan.catb32, catgW = c->plan.catgW, catgb = c->plan.catgb,
-               catWb = c->plan.catWb, catY = c->plan.catY, catG = c->plan.catG;
-  // runs of consecutive active models of the concatenated level-0 GEMM: [first row, rows)
-  std::vector<std::pair<int64_t, int64_t>> cat_runs;
-  {
-    const auto& cat = c->plan.cat;
-    for (size_t k = 0; k < cat.size(); ++k) {
-      if (!c->active[cat[k]]) continue;
-      const int64_t r0 = c->plan.cat_off[cat[k]];
-      const int64_t r1 = k + 1 < cat.size() ? c->plan.cat_off[cat[k + 1]] : c->plan.cat_rows;
-      if (!cat_runs.empty() && cat_runs.back().first + cat_runs.back().second == r0) cat_runs.back().second += r1 - r0;
-      else cat_runs.push_back({r0, r1 - r0});
+  // per input group: runs of consecutive active models of its concatenated
+  // level-0 GEMM, [first row, rows)
+  std::vector<std::vector<std::pair<int64_t, int64_t>>> cat_runs(c->groups.size());
+  for (size_t gi = 0; gi < c->groups.size(); ++gi) {
+    const Group& g = c->groups[gi];
+    auto& runs = cat_runs[gi];
+    for (size_t k = 0; k < g.cat.size(); ++k) {
+      if (!c->active[g.cat[k]]) continue;
+      const int64_t r0 = c->cat_off[g.cat[k]];
+      const int64_t r1 = k + 1 < g.cat.size() ? c->cat_off[g.cat[k + 1]] : g.cat_rows;
+      if (!runs.empty() && runs.back().first + runs.back().second == r0) runs.back().second += r1 - r0;
+      else runs.push_back({r0, r1 - r0});
     }
   }
   std::vector<char>& host_tables = T.host;
@@ -580,7 +594,7 @@ static void build_tables(un_ctx* c, Tables& T) {
   const int CBM = bf ? CONV_BM_BF16 : CONV_BM_F32, CBN = bf ? CONV_BN_BF16 : CONV_BN_F32;
   // softmax-CE is fused into a model's logits GEMM when a tile holds whole
   // rows of logits; the loss partials of model m start at m * ce_pstride
-  const int ce_pstride = cdiv(B, CE_ROWS);
+  const int ce_pstride = cdiv(c->maxB, CE_ROWS);
   auto ce_fused = [&](const Block& b) { return b.kind == 0 && b.N <= GBN; };
 
   // Problems of one launch are ordered longest-K first (their tiles are the
@@ -717,7 +731,7 @@ static void build_tables(un_ctx* c, Tables& T) {
 
   auto conv_base = [&](const Block& b) {
     ConvProb p{};
-    p.Nb = B;
+    p.Nb = c->groups[c->models[b.model].group].B;
     p.C = b.C;
     p.H = b.H;
     p.W = b.W;
@@ -739,29 +753,31 @@ static void build_tables(un_ctx* c, Tables& T) {
   for (int lv = 0; lv < levels; ++lv) {
     std::vector<GemmProb> gp;
     std::vector<ConvProb> cp;
-    bool cat_done = false;
+    std::vector<char> cat_done(c->groups.size(), 0);
     for (auto& m : c->models) {
       if (lv >= (int)m.blocks.size() || !c->active[m.blocks[0].model]) continue;
+      const Group& g = c->groups[m.group];
+      const int B = g.B;
       Block& b = m.blocks[lv];
       if (b.kind == 0) {
         if (b.concat) {
-          // one problem per run of consecutive active models of the concatenation
-          if (cat_done) continue;
-          cat_done = true;
-          for (const auto& run : cat_runs) {
+          // one problem per run of consecutive active models of the group's concatenation
+          if (cat_done[m.group]) continue;
+          cat_done[m.group] = 1;
+          for (const auto& run : cat_runs[m.group]) {
             GemmProb p{};
-            p.A = ptr(c->Xin);
-            p.lda = c->ldxin;
-            p.B = ptr(bf ? sub(catWb, run.first * kin_p * 2) : sub(catW32, run.first * kin_p * 4));
-            p.ldb = kin_p;
+            p.A = ptr(g.Xin);
+            p.lda = g.ldxin;
+            p.B = ptr(bf ? sub(g.catWb, run.first * g.kin_p * 2) : sub(g.catW32, run.first * g.kin_p * 4));
+            p.ldb = g.kin_p;
             p.M = B;
             p.N = (int)run.second;
-            p.K = (int)in_feat;
+            p.K = (int)g.in_feat;
             p.epi = EPI_FWD;
             p.relu = 1;
-            p.C = ptr(sub(catY, run.first * (int64_t)es));
-            p.ldc = cat_rows;
-            p.bias = (const float*)ptr(sub(catb32, run.first * 4));
+            p.C = ptr(sub(g.catY, run.first * (int64_t)es));
+            p.ldc = g.cat_rows;
+            p.bias = (const float*)ptr(sub(g.catb32, run.first * 4));
             gp.push_back(p);
           }
           continue;
@@ -790,6 +806,8 @@ static void build_tables(un_ctx* c, Tables& T) {
           p.ldc = b.ldg;
           p.model = b.model;
           p.ce_part = (float*)ptr(sub(c->ce_partial, (int64_t)b.model * ce_pstride * 4));
+          p.lab_shared = (int32_t)g.lab_shared;
+          p.lab_own = (int32_t)m.lab_own;
         }
         gp.push_back(p);
       } else {
@@ -819,7 +837,9 @@ static void build_tables(un_ctx* c, Tables& T) {
   for (int pass = 0; pass < 2; ++pass)
     for (size_t mi = 0; mi < c->models.size(); ++mi) {
       if (!c->active[mi]) continue;
-      Block& b = c->models[mi].blocks.back();
+      const Model& m = c->models[mi];
+      const Group& g = c->groups[m.group];
+      const Block& b = m.blocks.back();
       if (ce_fused(b) != (pass == 1)) continue;
       CeProb p{};
       p.logits = (const float*)ptr(b.Y);
@@ -828,7 +848,10 @@ static void build_tables(un_ctx* c, Tables& T) {
       p.ldg = b.ldg;
       p.C = b.N;
       p.model = (int)mi;
-      p.nchunks = pass == 1 ? cdiv(B, GBM) : ce_pstride;
+      p.nchunks = pass == 1 ? cdiv(g.B, GBM) : cdiv(g.B, CE_ROWS);
+      p.B = g.B;
+      p.lab_shared = (int32_t)g.lab_shared;
+      p.lab_own = (int32_t)m.lab_own;
       ces.push_back(p);
       if (pass == 0) ++ce_rows;
     }
@@ -849,35 +872,39 @@ static void build_tables(un_ctx* c, Tables& T) {
   // writes the same weights. Conv blocks keep their own per-level launches
   // (data gradient, then split-K weight gradient, then the reduction with the
   // update).
-  auto add_wgrad = [&](const Block& b, std::vector<GemmProb>& gp, bool& cat_done) {
+  auto add_wgrad = [&](const Block& b, std::vector<GemmProb>& gp, std::vector<char>& cat_done) {
+    const int gi = c->models[b.model].group;
+    const Group& g = c->groups[gi];
+    const int B = g.B;
     if (b.concat) {
-      // one problem per run of consecutive active models of the concatenation
-      if (cat_done) return;
-      cat_done = true;
-      for (const auto& run : cat_runs) {
+      // one problem per run of consecutive active models of the group's concatenation
+      if (cat_done[gi]) return;
+      cat_done[gi] = 1;
+      const int64_t kin_p = g.kin_p;
+      for (const auto& run : cat_runs[gi]) {
         GemmProb p{};
-        p.A = ptr(sub(catG, run.first * (int64_t)es));
-        p.lda = cat_rows;
+        p.A = ptr(sub(g.catG, run.first * (int64_t)es));
+        p.lda = g.cat_rows;
         p.amode = OP_KMAJ;
-        p.B = ptr(c->Xin);
-        p.ldb = c->ldxin;
+        p.B = ptr(g.Xin);
+        p.ldb = g.ldxin;
         p.bmode = OP_KMAJ;
         p.M = (int)run.second;
-        p.N = (int)in_feat + 1;
+        p.N = (int)g.in_feat + 1;
         p.K = B;
         p.epi = EPI_WGRAD;
-        p.nsplit = (int)in_feat;
-        p.C = ptr(sub(catgW, run.first * kin_p * 4));
+        p.nsplit = (int)g.in_feat;
+        p.C = ptr(sub(g.catgW, run.first * kin_p * 4));
         p.ldc = kin_p;
-        p.dbias = (float*)ptr(sub(catgb, run.first * 4));
-        p.W = (float*)ptr(sub(catW32, run.first * kin_p * 4));
-        p.Wb = ptr(sub(catWb, run.first * kin_p * 2));
-        p.bmaster = (float*)ptr(sub(catb32, run.first * 4));
-        p.row_model = (const int32_t*)ptr(sub(c->plan.cat_row_model, run.first * 4));
-        p.s1 = sp(c->plan.catS1, run.first * kin_p * 4);
-        p.s2 = sp(c->plan.catS2, run.first * kin_p * 4);
-        p.sb1 = sp(c->plan.catS1b, run.first * 4);
-        p.sb2 = sp(c->plan.catS2b, run.first * 4);
+        p.dbias = (float*)ptr(sub(g.catgb, run.first * 4));
+        p.W = (float*)ptr(sub(g.catW32, run.first * kin_p * 4));
+        p.Wb = ptr(sub(g.catWb, run.first * kin_p * 2));
+        p.bmaster = (float*)ptr(sub(g.catb32, run.first * 4));
+        p.row_model = (const int32_t*)ptr(sub(g.cat_row_model, run.first * 4));
+        p.s1 = sp(g.catS1, run.first * kin_p * 4);
+        p.s2 = sp(g.catS2, run.first * kin_p * 4);
+        p.sb1 = sp(g.catS1b, run.first * 4);
+        p.sb2 = sp(g.catS2b, run.first * 4);
         gp.push_back(p);
       }
       return;
@@ -911,9 +938,10 @@ static void build_tables(un_ctx* c, Tables& T) {
     std::vector<GemmProb> gp;
     std::vector<ConvProb> dp, wp;
     std::vector<ReduceProb> rp;
-    bool cat_done = false;
+    std::vector<char> cat_done(c->groups.size(), 0);
     for (auto& m : c->models) {
       if (!c->active[m.blocks[0].model]) continue;
+      const int B = c->groups[m.group].B;
       const int depth = (int)m.blocks.size();
       if (lv + 1 < depth && m.blocks[lv + 1].kind == 0) add_wgrad(m.blocks[lv + 1], gp, cat_done);
       if (lv >= depth) continue;
@@ -1107,85 +1135,102 @@ static un_status install_tables(un_ctx* c, Tables& T) {
 static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
   const bool bf = c->bf16;
   const size_t es = bf ? 2 : 4;  // storage element size
-  const int B = c->B;
-  const int64_t Bp = c->Bp;
   Arena A;
-  const int64_t in_feat = (int64_t)c->in_c * c->in_h * c->in_w;
+  const size_t N = c->models.size();
 
-  c->xstage = A.take((size_t)B * in_feat * 4);
-  c->ydev = A.take(c->models.size() * (size_t)B * 4);  // one row of labels, or one per model
-  c->lr_dev = A.take(c->models.size() * 4);
-  c->opt_dev = A.take(c->models.size() * sizeof(OptHp));
-  c->losses_dev = A.take(c->models.size() * 4);
-  bool any_linear0 = false, any_conv0 = false;
+  // labels: one row per input group (un_load_batch), then one per model (un_load_labels)
+  c->lab_elems = 0;
+  for (auto& g : c->groups) {
+    g.lab_shared = c->lab_elems;
+    c->lab_elems += g.B;
+  }
   for (auto& m : c->models) {
-    if (m.blocks[0].kind == 0) any_linear0 = true;
-    else any_conv0 = true;
+    m.lab_own = c->lab_elems;
+    c->lab_elems += c->groups[m.group].B;
   }
-  // A first conv whose input channels are not a whole number of 16-byte
-  // vectors (RGB, grey-scale) reads a copy of the input with zero channels
-  // appended: its loaders then take whole vectors, and the padded weight
-  // columns meet zeros only, so their gradient is exactly 0 and they stay 0.
+  c->ydev = A.take((size_t)c->lab_elems * 4);
+  c->lr_dev = A.take(N * 4);
+  c->opt_dev = A.take(N * sizeof(OptHp));
+  c->losses_dev = A.take(N * 4);
+  c->cat_off.assign(N, -1);
   const int vec = bf ? 8 : 4;
-  c->in_cs = c->in_c;
-  if (any_conv0 && c->in_c % vec != 0) {
-    c->in_cs = (int)rup(c->in_c, vec);
-    c->XinC = A.take((size_t)B * c->in_h * c->in_w * c->in_cs * es);
-    for (auto& m : c->models)
-      if (m.blocks[0].kind == 1) m.blocks[0].C = c->in_cs;
-  }
-  if (c->XinC == NONE || any_linear0) c->Xin = A.take((size_t)B * in_feat * es);
-  c->ldxin = in_feat;
-  if (any_linear0 && in_feat % 8 != 0)
-    return fail(nullptr, UN_ERR_UNSUPPORTED, "input features must be a multiple of 8 when a model starts with Linear");
+  for (size_t gi = 0; gi < c->groups.size(); ++gi) {
+    Group& g = c->groups[gi];
+    const int B = g.B;
+    g.in_feat = (int64_t)g.in_c * g.in_h * g.in_w;
+    g.xstage = A.take((size_t)B * g.in_feat * 4);
+    bool any_linear0 = false, any_conv0 = false;
+    for (auto& m : c->models) {
+      if (m.group != (int)gi) continue;
+      if (m.blocks[0].kind == 0) any_linear0 = true;
+      else any_conv0 = true;
+    }
+    // A first conv whose input channels are not a whole number of 16-byte
+    // vectors (RGB, grey-scale) reads a copy of the input with zero channels
+    // appended: its loaders then take whole vectors, and the padded weight
+    // columns meet zeros only, so their gradient is exactly 0 and they stay 0.
+    g.in_cs = g.in_c;
+    if (any_conv0 && g.in_c % vec != 0) {
+      g.in_cs = (int)rup(g.in_c, vec);
+      g.XinC = A.take((size_t)B * g.in_h * g.in_w * g.in_cs * es);
+      for (auto& m : c->models)
+        if (m.group == (int)gi && m.blocks[0].kind == 1) m.blocks[0].C = g.in_cs;
+    }
+    if (g.XinC == NONE || any_linear0) g.Xin = A.take((size_t)B * g.in_feat * es);
+    g.ldxin = g.in_feat;
+    if (any_linear0 && g.in_feat % 8 != 0)
+      return fail(nullptr, UN_ERR_UNSUPPORTED,
+                  "input features must be a multiple of 8 when a model starts with Linear (input group " +
+                      std::to_string(gi) + ")");
 
-  // --- level-0 concatenation group: hidden Linear + ReLU reading the shared input
-  std::vector<int> cat;  // model indices
-  for (size_t i = 0; i < c->models.size(); ++i) {
-    const Block& b = c->models[i].blocks[0];
-    if (b.kind == 0 && !b.last && b.relu) cat.push_back((int)i);
-  }
-  std::vector<int64_t> cat_off(c->models.size(), -1);
-  int64_t cat_rows = 0;
-  for (int i : cat) {
-    cat_off[i] = cat_rows;
-    cat_rows += rup(c->models[i].blocks[0].N + 1, 8);  // >= 1 spare row: the ones row of YT
-  }
-  const int64_t kin_p = rup(in_feat, 8);
-  size_t catW32 = NONE, catb32 = NONE, catgW = NONE, catgb = NONE, catWb = NONE, catY = NONE, catG = NONE;
-  if (!cat.empty()) {
-    catW32 = A.take((size_t)cat_rows * kin_p * 4);
-    catb32 = A.take((size_t)cat_rows * 4);
-    catgW = A.take((size_t)cat_rows * kin_p * 4);
-    catgb = A.take((size_t)cat_rows * 4);
-    if (bf) catWb = A.take((size_t)cat_rows * kin_p * 2);
-    catY = A.take((size_t)B * cat_rows * es);
-    catG = A.take((size_t)B * cat_rows * es);
-    c->plan.cat_row_model = A.take((size_t)cat_rows * 4);
+    // level-0 concatenation: the group's hidden Linear + ReLU first layers
+    g.cat.clear();
+    for (size_t i = 0; i < N; ++i) {
+      const Block& b = c->models[i].blocks[0];
+      if (c->models[i].group == (int)gi && b.kind == 0 && !b.last && b.relu) g.cat.push_back((int)i);
+    }
+    g.cat_rows = 0;
+    for (int i : g.cat) {
+      c->cat_off[i] = g.cat_rows;
+      g.cat_rows += rup(c->models[i].blocks[0].N + 1, 8);  // >= 1 spare row
+    }
+    g.kin_p = rup(g.in_feat, 8);
+    if (!g.cat.empty()) {
+      g.catW32 = A.take((size_t)g.cat_rows * g.kin_p * 4);
+      g.catb32 = A.take((size_t)g.cat_rows * 4);
+      g.catgW = A.take((size_t)g.cat_rows * g.kin_p * 4);
+      g.catgb = A.take((size_t)g.cat_rows * 4);
+      if (bf) g.catWb = A.take((size_t)g.cat_rows * g.kin_p * 2);
+      g.catY = A.take((size_t)B * g.cat_rows * es);
+      g.catG = A.take((size_t)B * g.cat_rows * es);
+      g.cat_row_model = A.take((size_t)g.cat_rows * 4);
+    }
   }
 
   // --- per block buffers
   int levels = 0;
   for (size_t mi = 0; mi < c->models.size(); ++mi) {
     Model& m = c->models[mi];
+    const Group& g = c->groups[m.group];
+    const int B = g.B;
     levels = std::max(levels, (int)m.blocks.size());
     for (size_t j = 0; j < m.blocks.size(); ++j) {
       Block& b = m.blocks[j];
       if (b.kind == 0) {
         b.rows = b.N;
         b.ldw = rup(b.K, 8);
-        if (j == 0 && cat_off[mi] >= 0) {
+        if (j == 0 && c->cat_off[mi] >= 0) {
           b.concat = true;
-          const size_t roff = (size_t)cat_off[mi];
-          b.W32 = catW32 + roff * b.ldw * 4;
-          b.b32 = catb32 + roff * 4;
-          b.gW = catgW + roff * b.ldw * 4;
-          b.gb = catgb + roff * 4;
-          if (bf) b.Wb = catWb + roff * b.ldw * 2;
-          b.ldy = cat_rows;
-          b.Y = catY + roff * es;
-          b.ldg = cat_rows;
-          b.G = catG + roff * es;
+          const size_t roff = (size_t)c->cat_off[mi];
+          b.W32 = g.catW32 + roff * b.ldw * 4;
+          b.b32 = g.catb32 + roff * 4;
+          b.gW = g.catgW + roff * b.ldw * 4;
+          b.gb = g.catgb + roff * 4;
+          if (bf) b.Wb = g.catWb + roff * b.ldw * 2;
+          b.ldy = g.cat_rows;
+          b.Y = g.catY + roff * es;
+          b.ldg = g.cat_rows;
+          b.G = g.catG + roff * es;
         } else {
           b.W32 = A.take((size_t)b.N * b.ldw * 4);
           b.b32 = A.take((size_t)b.N * 4);
@@ -1241,8 +1286,8 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
     for (size_t j = 0; j < m.blocks.size(); ++j) {
       Block& b = m.blocks[j];
       if (j == 0) {
-        b.X = (b.kind == 1 && c->XinC != NONE) ? c->XinC : c->Xin;
-        b.ldx = c->ldxin;
+        b.X = (b.kind == 1 && g.XinC != NONE) ? g.XinC : g.Xin;
+        b.ldx = g.ldxin;
       } else {
         Block& p = m.blocks[j - 1];
         b.X = p.Y;
@@ -1255,25 +1300,12 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
   // --- workspace: one contiguous range (relocatable as a whole, un_step_scratch)
   c->ws_lo = (size_t)rup((int64_t)A.top, 256);
   A.top = c->ws_lo;
-  c->ce_partial = A.take(c->models.size() * (size_t)cdiv(B, CE_ROWS) * 4);
+  c->ce_partial = A.take(c->models.size() * (size_t)cdiv(c->maxB, CE_ROWS) * 4);
   for (auto& m : c->models)
     for (auto& b : m.blocks)
       if (b.kind == 1) b.ws = A.take(b.ws_size);
   c->ws_bytes = A.top - c->ws_lo;
 
-  // --- planning results the descriptor tables are built from
-  c->plan.in_feat = in_feat;
-  c->plan.kin_p = kin_p;
-  c->plan.cat_rows = cat_rows;
-  c->plan.cat = cat;
-  c->plan.cat_off = cat_off;
-  c->plan.catW32 = catW32;
-  c->plan.catb32 = catb32;
-  c->plan.catgW = catgW;
-  c->plan.catgb = catgb;
-  c->plan.catWb = catWb;
-  c->plan.catY = catY;
-  c->plan.catG = catG;
   c->active.assign(c->models.size(), 1);
   Tables T;
   build_tables(c, T);
@@ -1294,18 +1326,21 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
     un_status st = install_tables(c, T);
     if (st != UN_OK) return st;
   }
-  std::vector<int32_t> row_model((size_t)cat_rows);
-  if (!cat.empty()) {
-    for (size_t k = 0; k < cat.size(); ++k) {
-      const int64_t r1 = k + 1 < cat.size() ? cat_off[cat[k + 1]] : cat_rows;
-      for (int64_t r = cat_off[cat[k]]; r < r1; ++r) row_model[(size_t)r] = cat[k];
+  for (auto& g : c->groups) {
+    if (!g.cat.empty()) {
+      std::vector<int32_t> row_model((size_t)g.cat_rows);
+      for (size_t k = 0; k < g.cat.size(); ++k) {
+        const int64_t r1 = k + 1 < g.cat.size() ? c->cat_off[g.cat[k + 1]] : g.cat_rows;
+        for (int64_t r = c->cat_off[g.cat[k]]; r < r1; ++r) row_model[(size_t)r] = g.cat[k];
+      }
+      HIPCHK(c, hipMemcpyAsync(c->base + g.cat_row_model, row_model.data(), row_model.size() * 4,
+                               hipMemcpyHostToDevice, c->stream));
+      HIPCHK(c, hipStreamSynchronize(c->stream));  // row_model is freed at the end of this scope
     }
-    HIPCHK(c, hipMemcpyAsync(c->base + c->plan.cat_row_model, row_model.data(), row_model.size() * 4,
-                             hipMemcpyHostToDevice, c->stream));
+    // the padding channels of XinC are written here only, once
+    if (g.XinC != NONE)
+      HIPCHK(c, hipMemsetAsync(c->base + g.XinC, 0, (size_t)g.B * g.in_h * g.in_w * g.in_cs * es, c->stream));
   }
-  // the padding channels of XinC are written here only, once
-  if (c->XinC != NONE)
-    HIPCHK(c, hipMemsetAsync(c->base + c->XinC, 0, (size_t)B * c->in_h * c->in_w * c->in_cs * es, c->stream));
   HIPCHK(c, hipStreamSynchronize(c->stream));
   return UN_OK;
 }
@@ -1447,8 +1482,8 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
   switch (l.kind) {
     case 0:
       e = launch_gemm(c->bf16, l.kclass == UN_K_GEMM_BWD, c->at<GemmProb>(l.probs), c->at<int32_t>(l.map), l.count, lr,
-                      c->lrv, c->optp, c->keep_grads, c->at<int32_t>(c->ydev), c->labels_per_model ? c->B : 0,
-                      c->wsoff, c->stream);
+                      c->lrv, c->optp, c->keep_grads, c->at<int32_t>(c->ydev), c->labels_per_model, c->wsoff,
+                      c->stream);
       break;
     case 1:
       e = launch_conv_fwd(c->bf16, c->at<ConvProb>(l.probs), c->at<int32_t>(l.map), l.count, c->stream);
@@ -1471,7 +1506,7 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
       break;
     case 5:
       e = launch_ce(c->bf16, c->at<CeProb>(l.probs), l.count, l.mode, c->at<int32_t>(c->ydev), c->labels_per_model,
-                    c->B, (float*)((char*)c->at<float>(c->ce_partial) + c->wsoff), cdiv(c->B, CE_ROWS),
+                    c->maxB, (float*)((char*)c->at<float>(c->ce_partial) + c->wsoff), cdiv(c->maxB, CE_ROWS),
                     c->at<float>(c->losses_dev), c->stream);
       break;
     case 6:
@@ -1516,42 +1551,64 @@ static size_t state_layout(un_ctx* c);
 
 // Validation and parsing shared by un_create and un_plan_bytes: a context
 // with its models parsed and nothing on the device.
-static un_status parse_all(const un_model_spec* specs, int32_t n_models, const un_input_spec* in, un_ctx** out) {
+static un_status parse_all(const un_model_spec* specs, int32_t n_models, const un_input_spec* ins, int32_t n_groups,
+                           const int32_t* group_of, un_ctx** out) {
   *out = nullptr;
-  if (!specs || !in || n_models <= 0) return fail(nullptr, UN_ERR_INVALID, "specs/in NULL or n_models <= 0");
-  if (in->batch <= 0 || in->in_c <= 0 || in->in_h <= 0 || in->in_w <= 0)
-    return fail(nullptr, UN_ERR_INVALID, "input dimensions must be positive");
-  if (in->batch > CE_MAX_BATCH) return fail(nullptr, UN_ERR_UNSUPPORTED, "batch larger than 2^20");
-  if (in->precision != UN_F32 && in->precision != UN_BF16_F32MASTER)
-    return fail(nullptr, UN_ERR_INVALID, "unknown precision");
+  if (!specs || !ins || n_models <= 0) return fail(nullptr, UN_ERR_INVALID, "specs/inputs NULL or n_models <= 0");
+  if (n_groups <= 0 || n_groups > n_models) return fail(nullptr, UN_ERR_INVALID, "need 1 <= n_groups <= n_models");
+  if (n_groups > 1 && !group_of) return fail(nullptr, UN_ERR_INVALID, "group_of is NULL with several input groups");
+  for (int g = 0; g < n_groups; ++g) {
+    const un_input_spec& in = ins[g];
+    if (in.batch <= 0 || in.in_c <= 0 || in.in_h <= 0 || in.in_w <= 0)
+      return fail(nullptr, UN_ERR_INVALID, "input group " + std::to_string(g) + ": dimensions must be positive");
+    if (in.batch > CE_MAX_BATCH) return fail(nullptr, UN_ERR_UNSUPPORTED, "batch larger than 2^20");
+    if (in.precision != UN_F32 && in.precision != UN_BF16_F32MASTER)
+      return fail(nullptr, UN_ERR_INVALID, "unknown precision");
+    if (in.precision != ins[0].precision)
+      return fail(nullptr, UN_ERR_INVALID, "every input group must have the same precision");
+  }
+  std::vector<int> used(n_groups, 0);
+  for (int i = 0; i < n_models; ++i) {
+    const int g = group_of ? group_of[i] : 0;
+    if (g < 0 || g >= n_groups)
+      return fail(nullptr, UN_ERR_RANGE, "model " + std::to_string(i) + ": input group out of range");
+    used[g] = 1;
+  }
+  for (int g = 0; g < n_groups; ++g)
+    if (!used[g]) return fail(nullptr, UN_ERR_INVALID, "input group " + std::to_string(g) + " has no model");
   un_ctx* c = new un_ctx();
-  c->bf16 = in->precision == UN_BF16_F32MASTER;
-  c->B = in->batch;
-  c->Bp = rup(in->batch, 8);
-  c->in_c = in->in_c;
-  c->in_h = in->in_h;
-  c->in_w = in->in_w;
+  c->bf16 = ins[0].precision == UN_BF16_F32MASTER;
+  c->groups.resize(n_groups);
+  for (int g = 0; g < n_groups; ++g) {
+    Group& gr = c->groups[g];
+    gr.B = ins[g].batch;
+    gr.in_c = ins[g].in_c;
+    gr.in_h = ins[g].in_h;
+    gr.in_w = ins[g].in_w;
+    c->maxB = std::max(c->maxB, gr.B);
+  }
   c->models.resize(n_models);
   c->opts.resize(n_models);
-  c->min_classes = 1 << 30;
   for (int i = 0; i < n_models; ++i) {
+    const int g = group_of ? group_of[i] : 0;
     std::string why;
-    un_status s = parse_model(specs[i], *in, i, c->models[i], why);
+    un_status s = parse_model(specs[i], ins[g], i, c->models[i], why);
     if (s != UN_OK) {
       delete c;
       return fail(nullptr, s, why);
     }
-    c->min_classes = std::min(c->min_classes, c->models[i].num_classes);
+    c->models[i].group = g;
+    c->groups[g].min_classes = std::min(c->groups[g].min_classes, c->models[i].num_classes);
   }
   *out = c;
   return UN_OK;
 }
 
-un_status un_plan_bytes(const un_model_spec* specs, int32_t n_models, const un_input_spec* in, size_t* arena_bytes,
-                        size_t* state_bytes) {
+un_status un_plan_bytes_grouped(const un_model_spec* specs, int32_t n_models, const un_input_spec* inputs,
+                                int32_t n_groups, const int32_t* group_of, size_t* arena_bytes, size_t* state_bytes) {
   if (!arena_bytes) return fail(nullptr, UN_ERR_INVALID, "arena_bytes is NULL");
   un_ctx* c = nullptr;
-  un_status s = parse_all(specs, n_models, in, &c);
+  un_status s = parse_all(specs, n_models, inputs, n_groups, group_of, &c);
   if (s != UN_OK) return s;
   s = plan_and_alloc(c, true);
   if (s == UN_OK) {
@@ -1566,11 +1623,22 @@ un_status un_plan_bytes(const un_model_spec* specs, int32_t n_models, const un_i
   return UN_OK;
 }
 
+un_status un_plan_bytes(const un_model_spec* specs, int32_t n_models, const un_input_spec* in, size_t* arena_bytes,
+                        size_t* state_bytes) {
+  return un_plan_bytes_grouped(specs, n_models, in, 1, nullptr, arena_bytes, state_bytes);
+}
+
 un_status un_create(const un_model_spec* specs, int32_t n_models, const un_input_spec* in, un_ctx** out) {
+  return un_create_grouped(specs, n_models, in, 1, nullptr, out);
+}
+
+un_status un_create_grouped(const un_model_spec* specs, int32_t n_models, const un_input_spec* inputs,
+                            int32_t n_groups, const int32_t* group_of, un_ctx** out) {
   if (!out) return fail(nullptr, UN_ERR_INVALID, "out is NULL");
+  *out = nullptr;
   un_ctx* c = nullptr;
   {
-    un_status ps = parse_all(specs, n_models, in, &c);
+    un_status ps = parse_all(specs, n_models, inputs, n_groups, group_of, &c);
     if (ps != UN_OK) return ps;
   }
   hipError_t e = hipGetDevice(&c->device);
@@ -1605,28 +1673,30 @@ un_status un_create(const un_model_spec* specs, int32_t n_models, const un_input
   return UN_OK;
 }
 
-static un_status load_common(un_ctx* c, const float* x, const int32_t* y, bool device) {
-  const size_t nx = (size_t)c->B * c->in_c * c->in_h * c->in_w;
-  std::vector<int32_t> yh(c->B);
+static un_status load_common(un_ctx* c, int gi, const float* x, const int32_t* y, bool device) {
+  Group& g = c->groups[gi];
+  const size_t nx = (size_t)g.B * g.in_feat;
+  std::vector<int32_t> yh(g.B);
   if (device) {
-    HIPCHK(c, hipMemcpyAsync(yh.data(), y, (size_t)c->B * 4, hipMemcpyDeviceToHost, c->stream));
+    HIPCHK(c, hipMemcpyAsync(yh.data(), y, (size_t)g.B * 4, hipMemcpyDeviceToHost, c->stream));
     HIPCHK(c, hipStreamSynchronize(c->stream));
   } else {
-    memcpy(yh.data(), y, (size_t)c->B * 4);
+    memcpy(yh.data(), y, (size_t)g.B * 4);
   }
-  for (int b = 0; b < c->B; ++b)
-    if (yh[b] < 0 || yh[b] >= c->min_classes)
+  for (int b = 0; b < g.B; ++b)
+    if (yh[b] < 0 || yh[b] >= g.min_classes)
       return fail(c, UN_ERR_RANGE, "label " + std::to_string(yh[b]) + " at " + std::to_string(b) + " out of range");
   const float* xsrc = x;
   if (!device) {
-    HIPCHK(c, hipMemcpyAsync(c->base + c->xstage, x, nx * 4, hipMemcpyHostToDevice, c->stream));
-    xsrc = c->at<float>(c->xstage);
+    HIPCHK(c, hipMemcpyAsync(c->base + g.xstage, x, nx * 4, hipMemcpyHostToDevice, c->stream));
+    xsrc = c->at<float>(g.xstage);
   }
-  HIPCHK(c, hipMemcpyAsync(c->base + c->ydev, yh.data(), (size_t)c->B * 4, hipMemcpyHostToDevice, c->stream));
-  HIPCHK(c, launch_load(c->bf16, xsrc, c->B, c->in_c, c->in_h, c->in_w, c->Xin == NONE ? nullptr : c->base + c->Xin,
-                        c->XinC == NONE ? nullptr : c->base + c->XinC, c->in_cs, c->stream));
+  HIPCHK(c, hipMemcpyAsync(c->base + c->ydev + g.lab_shared * 4, yh.data(), (size_t)g.B * 4, hipMemcpyHostToDevice,
+                           c->stream));
+  HIPCHK(c, launch_load(c->bf16, xsrc, g.B, g.in_c, g.in_h, g.in_w, g.Xin == NONE ? nullptr : c->base + g.Xin,
+                        g.XinC == NONE ? nullptr : c->base + g.XinC, g.in_cs, c->stream));
   HIPCHK(c, hipStreamSynchronize(c->stream));
-  c->loaded = true;
+  g.loaded = true;
   c->labels_per_model = false;
   return UN_OK;
 }
@@ -1634,13 +1704,22 @@ static un_status load_common(un_ctx* c, const float* x, const int32_t* y, bool d
 un_status un_load_batch(un_ctx* c, const float* x, const int32_t* y) {
   CHECK_CTX(c);
   if (!x || !y) return fail(c, UN_ERR_INVALID, "x or y is NULL");
-  return load_common(c, x, y, false);
+  if (c->groups.size() != 1) return fail(c, UN_ERR_INVALID, "several input groups: use un_load_group_batch");
+  return load_common(c, 0, x, y, false);
 }
 
 un_status un_load_batch_device(un_ctx* c, const float* x, const int32_t* y) {
   CHECK_CTX(c);
   if (!x || !y) return fail(c, UN_ERR_INVALID, "x or y is NULL");
-  return load_common(c, x, y, true);
+  if (c->groups.size() != 1) return fail(c, UN_ERR_INVALID, "several input groups: use un_load_group_batch");
+  return load_common(c, 0, x, y, true);
+}
+
+un_status un_load_group_batch(un_ctx* c, int32_t g, const float* x, const int32_t* y) {
+  CHECK_CTX(c);
+  if (!x || !y) return fail(c, UN_ERR_INVALID, "x or y is NULL");
+  if (g < 0 || g >= (int)c->groups.size()) return fail(c, UN_ERR_RANGE, "input group out of range");
+  return load_common(c, g, x, y, false);
 }
 
 // The kernels of one step, in order, on the context's stream.
@@ -1717,7 +1796,7 @@ static un_status step_common(un_ctx* c, float lr, const float* lrs, float* losse
 
 un_status un_step(un_ctx* c, float lr, float* losses) {
   CHECK_CTX(c);
-  if (!c->loaded) return fail(c, UN_ERR_STATE, "un_step before un_load_batch");
+  if (!c->all_loaded()) return fail(c, UN_ERR_STATE, "un_step before a batch of every input group is loaded");
   if (!std::isfinite(lr)) return fail(c, UN_ERR_INVALID, "lr is not finite");
   return step_common(c, lr, nullptr, losses);
 }
@@ -1725,7 +1804,7 @@ un_status un_step(un_ctx* c, float lr, float* losses) {
 un_status un_step_lr(un_ctx* c, const float* lrs, float* losses) {
   CHECK_CTX(c);
   if (!lrs) return fail(c, UN_ERR_INVALID, "lrs is NULL");
-  if (!c->loaded) return fail(c, UN_ERR_STATE, "un_step_lr before un_load_batch");
+  if (!c->all_loaded()) return fail(c, UN_ERR_STATE, "un_step_lr before a batch of every input group is loaded");
   for (size_t i = 0; i < c->models.size(); ++i)
     if (!std::isfinite(lrs[i])) return fail(c, UN_ERR_INVALID, "lr of model " + std::to_string(i) + " is not finite");
   // the rates travel in kernel arguments, ordered before the step on the stream
@@ -1739,21 +1818,22 @@ un_status un_step_lr(un_ctx* c, const float* lrs, float* losses) {
 // at it).
 static size_t state_layout(un_ctx* c) {
   Arena S;
-  auto& pl = c->plan;
-  if (!pl.cat.empty()) {
-    pl.catS1 = S.take((size_t)pl.cat_rows * pl.kin_p * 4);
-    pl.catS1b = S.take((size_t)pl.cat_rows * 4);
-    pl.catS2 = S.take((size_t)pl.cat_rows * pl.kin_p * 4);
-    pl.catS2b = S.take((size_t)pl.cat_rows * 4);
+  for (auto& g : c->groups) {
+    if (g.cat.empty()) continue;
+    g.catS1 = S.take((size_t)g.cat_rows * g.kin_p * 4);
+    g.catS1b = S.take((size_t)g.cat_rows * 4);
+    g.catS2 = S.take((size_t)g.cat_rows * g.kin_p * 4);
+    g.catS2b = S.take((size_t)g.cat_rows * 4);
   }
   for (size_t mi = 0; mi < c->models.size(); ++mi)
     for (auto& b : c->models[mi].blocks) {
       if (b.concat) {
-        const size_t roff = (size_t)pl.cat_off[mi];
-        b.S1 = pl.catS1 + roff * b.ldw * 4;
-        b.S2 = pl.catS2 + roff * b.ldw * 4;
-        b.S1b = pl.catS1b + roff * 4;
-        b.S2b = pl.catS2b + roff * 4;
+        const Group& g = c->groups[c->models[mi].group];
+        const size_t roff = (size_t)c->cat_off[mi];
+        b.S1 = g.catS1 + roff * b.ldw * 4;
+        b.S2 = g.catS2 + roff * b.ldw * 4;
+        b.S1b = g.catS1b + roff * 4;
+        b.S2b = g.catS2b + roff * 4;
       } else {
         b.S1 = S.take((size_t)b.rows * b.ldw * 4);
         b.S1b = S.take((size_t)b.rows * 4);
@@ -1857,16 +1937,22 @@ un_status un_set_opt_state(un_ctx* c, int32_t i, const float* src, size_t n, int
 un_status un_load_labels(un_ctx* c, const int32_t* y) {
   CHECK_CTX(c);
   if (!y) return fail(c, UN_ERR_INVALID, "y is NULL");
-  if (!c->loaded) return fail(c, UN_ERR_STATE, "un_load_labels before un_load_batch");
-  const size_t n = c->models.size(), B = (size_t)c->B;
-  for (size_t i = 0; i < n; ++i)
+  if (!c->all_loaded()) return fail(c, UN_ERR_STATE, "un_load_labels before a batch of every input group is loaded");
+  const size_t n = c->models.size();
+  size_t off = 0;
+  for (size_t i = 0; i < n; ++i) {
+    const size_t B = (size_t)c->groups[c->models[i].group].B;
     for (size_t b = 0; b < B; ++b) {
-      const int32_t v = y[i * B + b];
+      const int32_t v = y[off + b];
       if (v < 0 || v >= c->models[i].num_classes)
         return fail(c, UN_ERR_RANGE, "label " + std::to_string(v) + " of model " + std::to_string(i) + " at " +
                                          std::to_string(b) + " out of range");
     }
-  HIPCHK(c, hipMemcpyAsync(c->base + c->ydev, y, n * B * 4, hipMemcpyHostToDevice, c->stream));
+    off += B;
+  }
+  // the model rows follow the group rows and are laid out in model order, as y
+  HIPCHK(c, hipMemcpyAsync(c->base + c->ydev + c->models[0].lab_own * 4, y, off * 4, hipMemcpyHostToDevice,
+                           c->stream));
   HIPCHK(c, hipStreamSynchronize(c->stream));
   c->labels_per_model = true;
   return UN_OK;
@@ -1924,7 +2010,7 @@ static un_status scratch_on(un_ctx* c, char** out) {
 
 un_status un_step_scratch(un_ctx* c, float lr, float* losses) {
   CHECK_CTX(c);
-  if (!c->loaded) return fail(c, UN_ERR_STATE, "un_step_scratch before un_load_batch");
+  if (!c->all_loaded()) return fail(c, UN_ERR_STATE, "un_step_scratch before a batch of every input group is loaded");
   if (!std::isfinite(lr)) return fail(c, UN_ERR_INVALID, "lr is not finite");
   if (c->ws_bytes > UN_SCRATCH_BYTES)
     return fail(c, UN_ERR_UNSUPPORTED, "this context's step workspace (" + std::to_string(c->ws_bytes) +
@@ -1950,7 +2036,7 @@ un_status un_set_stream(un_ctx* c, void* stream) {
 
 un_status un_graph_capture(un_ctx* c, float lr) {
   CHECK_CTX(c);
-  if (!c->loaded) return fail(c, UN_ERR_STATE, "un_graph_capture before un_load_batch");
+  if (!c->all_loaded()) return fail(c, UN_ERR_STATE, "un_graph_capture before a batch of every input group is loaded");
   if (!std::isfinite(lr)) return fail(c, UN_ERR_INVALID, "lr is not finite");
   if (c->any_opt)
     return fail(c, UN_ERR_UNSUPPORTED, "a model has a momentum / Adam optimizer (its hyper-parameters change every step)");

@@ -27,7 +27,8 @@ OPS = {"linear": 0, "conv": 1, "relu": 2, "pool": 3, "flatten": 4, "res_begin": 
 KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad", "ce", "sgd", "other"]
 
 # Every symbol the header declares.
-EXPORTS = ["un_create", "un_plan_bytes", "un_load_batch", "un_load_batch_device", "un_load_labels", "un_step", "un_step_lr",
+EXPORTS = ["un_create", "un_create_grouped", "un_plan_bytes", "un_plan_bytes_grouped", "un_load_group_batch",
+           "un_load_batch", "un_load_batch_device", "un_load_labels", "un_step", "un_step_lr",
            "un_set_active", "un_set_optimizer", "un_get_opt_state", "un_set_opt_state", "un_get_params",
            "un_set_params", "un_get_grads", "un_keep_grads", "un_param_count", "un_arena_bytes", "un_sync", "un_get_stream",
            "un_set_stream", "un_graph_capture", "un_graph_step", "un_step_scratch",
@@ -75,6 +76,12 @@ def lib():
         sig = {
             "un_create": (ctypes.c_int, [ctypes.POINTER(un_model_spec), ctypes.c_int32, ctypes.POINTER(un_input_spec),
                                          ctypes.POINTER(P)]),
+            "un_create_grouped": (ctypes.c_int, [ctypes.POINTER(un_model_spec), ctypes.c_int32,
+                                                 ctypes.POINTER(un_input_spec), ctypes.c_int32, i32, ctypes.POINTER(P)]),
+            "un_plan_bytes_grouped": (ctypes.c_int, [ctypes.POINTER(un_model_spec), ctypes.c_int32,
+                                                     ctypes.POINTER(un_input_spec), ctypes.c_int32, i32, c_size_p,
+                                                     c_size_p]),
+            "un_load_group_batch": (ctypes.c_int, [P, ctypes.c_int32, f, i32]),
             "un_load_batch": (ctypes.c_int, [P, f, i32]),
             "un_load_batch_device": (ctypes.c_int, [P, P, P]),
             "un_step": (ctypes.c_int, [P, ctypes.c_float, f]),
@@ -143,23 +150,47 @@ def make_specs(specs, seeds=None):
     return arr, keep
 
 
-def un_create(specs, batch, in_shape, precision, seeds=None):
-    arr, keep = make_specs(specs, seeds)
+def _input_spec(batch, in_shape, precision):
     c, h, w = (tuple(in_shape) + (1, 1))[:3] if len(in_shape) != 3 else tuple(in_shape)
-    ins = un_input_spec(batch, c, h, w, UN_BF16_F32MASTER if precision == "bf16" else UN_F32)
+    return un_input_spec(batch, c, h, w, UN_BF16_F32MASTER if precision == "bf16" else UN_F32)
+
+
+def _groups(specs, batch, in_shape, precision, inputs, group_of):
+    """(input spec array, n_groups, group_of int32 array or None)."""
+    if inputs is None:
+        return (un_input_spec * 1)(_input_spec(batch, in_shape, precision)), 1, None
+    arr = (un_input_spec * len(inputs))(*[_input_spec(b, sh, precision) for b, sh in inputs])
+    go = np.ascontiguousarray(group_of, dtype=np.int32)
+    if go.shape != (len(specs),):
+        raise ValueError(f"group_of needs one entry per model ({len(specs)})")
+    return arr, len(inputs), go
+
+
+def un_create(specs, batch, in_shape, precision, seeds=None, inputs=None, group_of=None):
+    """A context; with inputs = [(batch, in_shape) per input group] and
+    group_of (a group per model) it is un_create_grouped."""
+    arr, keep = make_specs(specs, seeds)
+    ins, ng, go = _groups(specs, batch, in_shape, precision, inputs, group_of)
     ctx = ctypes.c_void_p()
-    _check(lib().un_create(arr, len(specs), ctypes.byref(ins), ctypes.byref(ctx)))
+    if go is None:
+        _check(lib().un_create(arr, len(specs), ins, ctypes.byref(ctx)))
+    else:
+        _check(lib().un_create_grouped(arr, len(specs), ins, ng, go.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                       ctypes.byref(ctx)))
     return ctx
 
 
-def un_plan_bytes(specs, batch, in_shape, precision):
+def un_plan_bytes(specs, batch, in_shape, precision, inputs=None, group_of=None):
     """(arena bytes, optimizer-state bytes) a context for these models would
     take; host only (no device needed)."""
     arr, keep = make_specs(specs, None)
-    c, h, w = (tuple(in_shape) + (1, 1))[:3] if len(in_shape) != 3 else tuple(in_shape)
-    ins = un_input_spec(batch, c, h, w, UN_BF16_F32MASTER if precision == "bf16" else UN_F32)
+    ins, ng, go = _groups(specs, batch, in_shape, precision, inputs, group_of)
     a, st = ctypes.c_size_t(), ctypes.c_size_t()
-    _check(lib().un_plan_bytes(arr, len(specs), ctypes.byref(ins), ctypes.byref(a), ctypes.byref(st)))
+    if go is None:
+        _check(lib().un_plan_bytes(arr, len(specs), ins, ctypes.byref(a), ctypes.byref(st)))
+    else:
+        _check(lib().un_plan_bytes_grouped(arr, len(specs), ins, ng, go.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                           ctypes.byref(a), ctypes.byref(st)))
     return a.value, st.value
 
 
@@ -169,16 +200,24 @@ def un_load_batch(ctx, x, y):
     _check(lib().un_load_batch(ctx, _fp(x), y.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))), ctx)
 
 
+def un_load_group_batch(ctx, g, x, y):
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    y = np.ascontiguousarray(y, dtype=np.int32)
+    _check(lib().un_load_group_batch(ctx, g, _fp(x), y.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))), ctx)
+
+
 def un_load_batch_device(ctx, x_ptr, y_ptr):
     _check(lib().un_load_batch_device(ctx, ctypes.c_void_p(x_ptr), ctypes.c_void_p(y_ptr)), ctx)
 
 
-def un_load_labels(ctx, y, n_models, batch):
-    """Per-model labels [n_models][batch] for the loaded batch."""
-    y = np.ascontiguousarray(y, dtype=np.int32)
-    if y.shape != (n_models, batch):
-        raise ValueError(f"labels must have shape ({n_models}, {batch}), got {y.shape}")
-    _check(lib().un_load_labels(ctx, y.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))), ctx)
+def un_load_labels(ctx, y, batches):
+    """Per-model labels for the loaded batches: y[i] holds batches[i] labels
+    of model i (a [N][B] array when every model has batch B)."""
+    rows = [np.ascontiguousarray(r, dtype=np.int32).reshape(-1) for r in y]
+    if [r.size for r in rows] != list(batches):
+        raise ValueError(f"label rows must have lengths {list(batches)}, got {[r.size for r in rows]}")
+    flat = np.ascontiguousarray(np.concatenate(rows), dtype=np.int32)
+    _check(lib().un_load_labels(ctx, flat.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))), ctx)
 
 
 def un_step_lr(ctx, lrs, n_models, losses=True):
@@ -347,14 +386,24 @@ def split_params(flat, shapes):
 class Hybrid:
     """N models merged into one fused training step on the GPU."""
 
-    def __init__(self, specs, batch, in_shape, precision="f32", seeds=None):
+    def __init__(self, specs, batch, in_shape, precision="f32", seeds=None, inputs=None, group_of=None):
+        """One shared input [batch, *in_shape], or input groups: inputs =
+        [(batch, in_shape) per group] and group_of = the group of each model."""
         self.specs = list(specs)
         self.n = len(self.specs)
-        self.batch = int(batch)
-        self.in_shape = tuple(in_shape)
         self.precision = precision
+        self.inputs = None if inputs is None else [(int(b), tuple(sh)) for b, sh in inputs]
+        self.group_of = None if group_of is None else [int(g) for g in group_of]
+        self.ctx = None
+        self.ctx = un_create(self.specs, batch, in_shape, precision, seeds, self.inputs, self.group_of)
+        if self.inputs is None:
+            self.batch = int(batch)
+            self.in_shape = tuple(in_shape)
+            self.batches = [self.batch] * self.n
+        else:
+            self.batch, self.in_shape = None, None
+            self.batches = [self.inputs[g][0] for g in self.group_of]
         self.optimizers = {i: dict(kind="sgd", momentum=0.0, betas=[0.9, 0.999], eps=1e-8) for i in range(self.n)}
-        self.ctx = un_create(self.specs, batch, in_shape, precision, seeds)
 
     def close(self):
         if self.ctx:
@@ -373,8 +422,12 @@ class Hybrid:
         except Exception:
             pass
 
-    def load_batch(self, x, y):
-        un_load_batch(self.ctx, x, y)
+    def load_batch(self, x, y, group=None):
+        """The shared batch, or input group `group`'s batch."""
+        if group is None:
+            un_load_batch(self.ctx, x, y)
+        else:
+            un_load_group_batch(self.ctx, group, x, y)
 
     def step(self, lr, losses=True):
         """lr: one rate for every model, or a sequence of N per-model rates."""
@@ -382,8 +435,12 @@ class Hybrid:
             return un_step(self.ctx, lr, self.n if losses else None)
         return un_step_lr(self.ctx, lr, self.n, losses)
 
+    def in_shape_of(self, i):
+        """Model i's input sample shape (its input group's)."""
+        return self.in_shape if self.inputs is None else self.inputs[self.group_of[i]][1]
+
     def load_labels(self, y):
-        un_load_labels(self.ctx, y, self.n, self.batch)
+        un_load_labels(self.ctx, y, self.batches)
 
     def set_active(self, mask):
         un_set_active(self.ctx, mask, self.n)

@@ -10,9 +10,27 @@ from paper_2408_01331_amd.unifiednn import flatten_params
 torch = pytest.importorskip("torch")
 
 
+class _Residual(torch.nn.Module):
+    """inner(x) + x"""
+
+    def __init__(self, inner):
+        super().__init__()
+        self.inner = inner
+
+    def forward(self, x):
+        return self.inner(x) + x
+
+
 def _sequential(spec, in_shape):
-    layers, shape = [], tuple(in_shape)
+    layers, shape, outer = [], tuple(in_shape), None
     for l in spec["layers"]:
+        if l[0] == "res_begin":
+            outer, layers = layers, []
+            continue
+        if l[0] == "res_end":
+            outer.append(_Residual(torch.nn.Sequential(*layers)))
+            layers, outer = outer, None
+            continue
         if l[0] == "linear":
             layers.append(torch.nn.Linear(int(np.prod(shape)), l[1]))
             shape = (l[1],)
@@ -35,6 +53,7 @@ class _Host:
 
     def __init__(self, wl):
         self.specs, self.in_shape, self.precision = wl.specs, tuple(wl.in_shape), wl.precision
+        self.in_shape_of = lambda i: self.in_shape
         self.params = {i: flatten_params(W.init_params(s, wl.in_shape, 3, i)) for i, s in enumerate(wl.specs)}
         self.optimizers = {i: dict(kind="sgd", momentum=0.0, betas=[0.9, 0.999], eps=1e-8) for i in range(len(wl.specs))}
         self.state = {i: (np.zeros(0, np.float32), 0) for i in range(len(wl.specs))}
@@ -58,7 +77,7 @@ class _Host:
         self.state[i] = (np.zeros(k * self.params[i].size, np.float32), 0)
 
 
-@pytest.mark.parametrize("name", ["lenet4", "mlp8"])
+@pytest.mark.parametrize("name", ["lenet4", "mlp8", "resnet8"])
 def test_checkpoint_names_load_into_torch_sequential(name, tmp_path):
     wl = W.get(name)
     h = _Host(wl)
