@@ -26,7 +26,15 @@ paper's PyTorch prototype, whose defaults these are):
 * convolution is cross-correlation, stride 1, zero padding;
 * max-pool is 2x2 / stride 2 / floor mode, the first maximum in row-major
   window order wins ties; ReLU'(0) = 0;
-* flatten is NCHW (c, h, w) order;
+* flatten is NCHW (c, h, w) order, and a sequence [T, d] flattens token by
+  token (t, j); ``unflatten`` views the flat features as a sequence of T
+  tokens of F / T features (PyTorch's Unflatten), on which a Linear layer
+  acts token by token;
+* ``attention`` is single-head self-attention on a sequence, PyTorch's
+  MultiheadAttention with one head (no mask, no dropout): [Q K V] =
+  x W_in^T + b_in (in-projection [3d, d]), A = softmax(Q K^T / sqrt(d)) V,
+  y = A W_out^T + b_out; its parameters are in_proj_weight, in_proj_bias,
+  out_proj.weight, out_proj.bias;
 * a residual block (``res_begin`` ... ``res_end``) is a module returning
   inner(x) + x, the standard skip connection: the sum is formed before any
   ReLU that follows the block, and in backward the gradient at the sum flows
@@ -42,7 +50,11 @@ Precision modes:
   are rounded to bf16 (round to nearest, ties to even) when read. Logits, the
   softmax-CE arithmetic, all accumulators, dW, db and the fp32 master weights
   stay fp32. Because ReLU, max-pool, flatten and their backward passes are
-  exact, rounding at the reader equals rounding the stored tensor.
+  exact, rounding at the reader equals rounding the stored tensor. In an
+  attention layer the two projections are Linear layers; the core reads Q, K,
+  V and the gradient dA at its output as bf16 operands, keeps the scores S and
+  the probabilities P in fp32 (both modes), and stores A and dQKV (read as
+  operands by the projections).
 
 Accumulation (``acc``): ``"f64"`` (the default, the reference) sums every dot
 product exactly enough to be rounded once; ``"f32"`` evaluates the same
@@ -151,11 +163,39 @@ def linear_fwd(h, W, b):
 
 
 def linear_bwd(dz, h, W, need_dh=True):
-    """dW = dz^T h, db = sum_b dz, dh = dz W."""
-    dW = dz.T @ h
-    db = dz.sum(axis=0)
+    """dW = dz^T h, db = sum_b dz, dh = dz W. On a sequence [B, T, d] the layer
+    acts on every token (PyTorch's Linear on a 3-D input): dW and db sum over
+    every sample and token."""
+    d2, h2 = dz.reshape(-1, dz.shape[-1]), h.reshape(-1, h.shape[-1])
+    dW = d2.T @ h2
+    db = d2.sum(axis=0)
     dh = dz @ W if need_dh else None
     return dW, db, dh
+
+
+def attention_core_fwd(q, k, v, rnd=lambda t: t):
+    """Scaled dot-product attention of one head over a sequence, per sample:
+    S = Q K^T / sqrt(d), P = softmax(S) over the keys, A = P V (q, k, v:
+    [B, T, d]). `rnd` rounds S and P as they are stored. Returns (A, P)."""
+    d = q.shape[-1]
+    s = rnd((q @ np.swapaxes(k, -1, -2)) / np.sqrt(d))
+    m = s.max(axis=-1, keepdims=True)
+    e = np.exp(s - m)
+    p = rnd(e / e.sum(axis=-1, keepdims=True))
+    return p @ v, p
+
+
+def attention_core_bwd(da, q, k, v, p):
+    """Gradients of A = softmax(Q K^T / sqrt(d)) V: dP = dA V^T, dV = P^T dA,
+    dS = P * (dP - rowsum(P * dP)) (softmax's Jacobian), dQ = dS K / sqrt(d),
+    dK = dS^T Q / sqrt(d). Returns (dQ, dK, dV)."""
+    d = q.shape[-1]
+    dp = da @ np.swapaxes(v, -1, -2)
+    dv = np.swapaxes(p, -1, -2) @ da
+    ds = p * (dp - (p * dp).sum(axis=-1, keepdims=True))
+    dq = (ds @ k) / np.sqrt(d)
+    dk = (np.swapaxes(ds, -1, -2) @ q) / np.sqrt(d)
+    return dq, dk, dv
 
 
 def conv2d_fwd(h, W, b, pad):
@@ -264,9 +304,9 @@ def count_params(spec, in_shape):
     for layer in spec["layers"]:
         op = layer[0]
         if op == "linear":
-            fin = int(np.prod(shape))
+            fin = shape[-1] if len(shape) == 2 else int(np.prod(shape))
             total += layer[1] * fin + layer[1]
-            shape = (layer[1],)
+            shape = (shape[0], layer[1]) if len(shape) == 2 else (layer[1],)
         elif op == "conv":
             c, H, W = shape
             o, k, pad = layer[1], layer[2], layer[3]
@@ -277,6 +317,11 @@ def count_params(spec, in_shape):
             shape = (c, H // 2, W // 2)
         elif op == "flatten":
             shape = (int(np.prod(shape)),)
+        elif op == "unflatten":
+            shape = (layer[1], shape[0] // layer[1])
+        elif op == "attention":
+            d = shape[-1]
+            total += 4 * d * d + 4 * d
         elif op not in ("relu", "res_begin", "res_end"):
             raise ValueError(f"unknown op {op!r}")
     return total
@@ -309,8 +354,8 @@ def forward(spec, params, x, mode="f32", flags=None, acc="f64"):
         if op == "linear":
             W, b = params[pi], params[pi + 1]
             hin, Wq = R.operand(h), R.operand(W)
-            if hin.ndim != 2:
-                raise ValueError("linear layer needs a 2-D input (add a flatten)")
+            if hin.ndim not in (2, 3):
+                raise ValueError("linear layer needs flat features or a sequence (add a flatten)")
             z = R.run(linear_fwd, hin, Wq, np.asarray(b, dtype=F64))
             ends_block = li + 1 < len(layers) and layers[li + 1][0] == "res_end"
             if ends_block:
@@ -331,8 +376,8 @@ def forward(spec, params, x, mode="f32", flags=None, acc="f64"):
             skip = h
             cache.append(("res_begin",))
         elif op == "res_end":
-            if skip is None or layers[li - 1][0] not in ("linear", "conv"):
-                raise ValueError("residual end must directly follow the block's last linear or conv")
+            if skip is None or layers[li - 1][0] not in ("linear", "conv", "attention"):
+                raise ValueError("residual end must directly follow the block's last linear, conv or attention")
             skip = None
             cache.append(("res_end",))
         elif op == "conv":
@@ -355,7 +400,7 @@ def forward(spec, params, x, mode="f32", flags=None, acc="f64"):
         elif op == "relu":
             if flags is not None and mag is not None:
                 bad = np.abs(h) <= U32 * mag
-                axes = (0,) if h.ndim == 2 else (0, 2, 3)
+                axes = (0,) if h.ndim == 2 else (0, 1) if h.ndim == 3 else (0, 2, 3)
                 flags.setdefault(last_pi, set()).update(np.nonzero(bad.any(axis=axes))[0].tolist())
             h = relu_fwd(h)
             cache.append(("relu", h))
@@ -378,6 +423,34 @@ def forward(spec, params, x, mode="f32", flags=None, acc="f64"):
         elif op == "flatten":
             cache.append(("flatten", h.shape))
             h = h.reshape(h.shape[0], -1)
+        elif op == "unflatten":
+            if h.ndim != 2 or h.shape[1] % layer[1]:
+                raise ValueError("unflatten needs flat features divisible into the tokens")
+            cache.append(("flatten", h.shape))
+            h = h.reshape(h.shape[0], layer[1], -1)
+        elif op == "attention":
+            if h.ndim != 3:
+                raise ValueError("attention needs a sequence (add an unflatten)")
+            Wi, bi, Wo, bo = params[pi:pi + 4]
+            hin, Wiq, Woq = R.operand(h), R.operand(Wi), R.operand(Wo)
+            d = hin.shape[2]
+            qkv = R.store(R.run(linear_fwd, hin, Wiq, np.asarray(bi, dtype=F64)))
+            q, k, v = (R.operand(qkv[..., j * d:(j + 1) * d]) for j in range(3))
+            a, p = R.run(attention_core_fwd, q, k, v, R.store)
+            aq = R.operand(R.store(a))
+            z = R.run(linear_fwd, aq, Woq, np.asarray(bo, dtype=F64))
+            ends_block = li + 1 < len(layers) and layers[li + 1][0] == "res_end"
+            if ends_block:
+                if skip is None or skip.shape != z.shape:
+                    raise ValueError("residual block: missing begin or shape mismatch")
+                z = z + R.operand(skip)
+            h = R.store(z)
+            if flags is not None:
+                mag, last_pi = linear_fwd(np.abs(aq), np.abs(Woq), np.abs(np.asarray(bo, dtype=F64))), pi + 2
+                if ends_block:
+                    mag = mag + np.abs(R.operand(skip))
+            cache.append(("attention", pi, hin, Wiq, q, k, v, p, aq, Woq))
+            pi += 4
         else:
             raise ValueError(f"unknown op {op!r}")
     return h, cache
@@ -388,7 +461,7 @@ def backward(spec, params, cache, dlogits, mode="f32", acc="f64"):
     R = _Mode(mode, acc)
     grads = [None] * len(params)
     g = np.asarray(dlogits, dtype=F64)
-    first_param_layer = min(e[1] for e in cache if e[0] in ("linear", "conv"))
+    first_param_layer = min(e[1] for e in cache if e[0] in ("linear", "conv", "attention"))
     gskip = None  # gradient at the sum of the open residual block
     for entry in reversed(cache):
         kind = entry[0]
@@ -409,6 +482,17 @@ def backward(spec, params, cache, dlogits, mode="f32", acc="f64"):
             else:
                 dW, db, dh = R.run(conv2d_bwd, gq, hin, Wq, entry[4], need_dh)
             grads[pi], grads[pi + 1] = R.store(dW), R.store(db)
+            g = R.store(dh) if need_dh else None
+        elif kind == "attention":
+            pi, hin, Wiq, q, k, v, p, aq, Woq = entry[1:]
+            gq = R.operand(g)
+            dWo, dbo, da = R.run(linear_bwd, gq, aq, Woq, True)
+            grads[pi + 2], grads[pi + 3] = R.store(dWo), R.store(dbo)
+            dq, dk, dv = R.run(attention_core_bwd, R.operand(R.store(da)), q, k, v, p)
+            gqi = R.operand(R.store(np.concatenate([dq, dk, dv], axis=-1)))
+            need_dh = pi != first_param_layer
+            dWi, dbi, dh = R.run(linear_bwd, gqi, hin, Wiq, need_dh)
+            grads[pi], grads[pi + 1] = R.store(dWi), R.store(dbi)
             g = R.store(dh) if need_dh else None
         elif kind == "relu":
             if g is not None:

@@ -37,7 +37,8 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-OP_CODES = {"linear": 0, "conv": 1, "relu": 2, "pool": 3, "flatten": 4, "res_begin": 5, "res_end": 6}
+OP_CODES = {"linear": 0, "conv": 1, "relu": 2, "pool": 3, "flatten": 4, "res_begin": 5, "res_end": 6,
+            "unflatten": 7, "attention": 8}
 
 
 @dataclass
@@ -80,10 +81,11 @@ def param_shapes(spec, in_shape):
     for layer in spec["layers"]:
         op = layer[0]
         if op == "linear":
-            f_in = int(np.prod(shape))
+            seq = len(shape) == 2          # a sequence [T, d]: the layer acts on every token
+            f_in = shape[-1] if seq else int(np.prod(shape))
             out.append(((layer[1], f_in), f_in))
             out.append(((layer[1],), f_in))
-            shape = (layer[1],)
+            shape = (shape[0], layer[1]) if seq else (layer[1],)
         elif op == "conv":
             c, h, w = shape
             o, k, pad = layer[1], layer[2], layer[3]
@@ -96,6 +98,11 @@ def param_shapes(spec, in_shape):
             shape = (c, h // 2, w // 2)
         elif op == "flatten":
             shape = (int(np.prod(shape)),)
+        elif op == "unflatten":
+            shape = (layer[1], shape[0] // layer[1])
+        elif op == "attention":
+            d = shape[-1]
+            out += [((3 * d, d), d), ((3 * d,), d), ((d, d), d), ((d,), d)]
     return out
 
 
