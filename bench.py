@@ -31,7 +31,7 @@ if ROOT not in sys.path:
 from paper_2408_01331_amd import workloads as W  # noqa: E402
 
 PEAK = {"bf16_mfma_tflops": 2500.0, "f32_mfma_tflops": 157.3, "hbm_gbs": 8000.0}
-KCLASS = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad", "ce", "sgd", "other"]
+KCLASS = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad", "ce", "sgd", "other", "attn"]
 
 
 # ---------------------------------------------------------------------------
@@ -64,24 +64,36 @@ def algorithmic_work(wl):
             op = layer[0]
             ends = li + 1 < len(layers) and layers[li + 1][0] == "res_end"
             begins = li > 0 and layers[li - 1][0] == "res_begin"
-            if op == "linear":
-                K = int(np.prod(shape))
-                N = layer[1]
+            if op in ("linear", "attention"):
+                # a sequence (T, d): token-wise products over B * T rows
+                R, K = (B * shape[0], shape[1]) if len(shape) == 2 else (B, int(np.prod(shape)))
                 last = li == len(layers) - 1
-                f = 2.0 * B * K * N
-                flops["gemm_fwd"] += f
-                nbytes["gemm_fwd"] += B * K * es + N * K * es + N * 4 + B * N * (4 if last else es)
-                flops["gemm_bwd"] += f                                   # weight gradient + update
-                nbytes["gemm_bwd"] += B * N * es + B * K * es + (N * K + N) * upd
-                if not first:                                            # data gradient
-                    flops["gemm_bwd"] += f
-                    nbytes["gemm_bwd"] += B * N * es + N * K * es + B * K * es
-                if last:                                                 # softmax-CE: logits in, dZ out
-                    nbytes["ce"] += B * N * 4 + B * N * es
-                nbytes["gemm_fwd"] += B * N * es if ends else 0          # skip input
-                nbytes["gemm_bwd"] += B * K * es if begins else 0        # skip gradient
-                n_params += K * N + N
-                shape = (N,)
+                # (N, rows stored fp32?) per projection: Linear, or in- and out-projection
+                projs = [(layer[1], last)] if op == "linear" else [(3 * K, False), (K, False)]
+                for pj, (N, fp32_out) in enumerate(projs):
+                    f = 2.0 * R * K * N
+                    flops["gemm_fwd"] += f
+                    nbytes["gemm_fwd"] += R * K * es + N * K * es + N * 4 + R * N * (4 if fp32_out else es)
+                    flops["gemm_bwd"] += f                               # weight gradient + update
+                    nbytes["gemm_bwd"] += R * N * es + R * K * es + (N * K + N) * upd
+                    if not (first and pj == 0):                          # data gradient
+                        flops["gemm_bwd"] += f
+                        nbytes["gemm_bwd"] += R * N * es + N * K * es + R * K * es
+                    n_params += K * N + N
+                if op == "attention":
+                    T, d = shape
+                    # core: S = Q K^T and A = P V forward; dP, dQ, dK, dV backward
+                    flops["attn"] += 4.0 * B * T * T * d + 8.0 * B * T * T * d
+                    nbytes["attn"] += B * T * 3 * d * es + B * T * d * es + B * T * T * 4          # forward, P fp32
+                    nbytes["attn"] += B * T * 3 * d * es * 2 + B * T * d * es + B * T * T * 4      # backward
+                else:
+                    N = layer[1]
+                    if last:                                             # softmax-CE: logits in, dZ out
+                        nbytes["ce"] += B * N * 4 + B * N * es
+                    shape = (shape[0], N) if len(shape) == 2 else (N,)
+                out_el = R * shape[-1]
+                nbytes["gemm_fwd"] += out_el * es if ends else 0         # skip input
+                nbytes["gemm_bwd"] += R * K * es if begins else 0        # skip gradient
                 first = False
             elif op == "conv":
                 C, H, Wd = shape
@@ -112,6 +124,8 @@ def algorithmic_work(wl):
                 shape = (C, H // 2, Wd // 2)
             elif op == "flatten":
                 shape = (int(np.prod(shape)),)
+            elif op == "unflatten":
+                shape = (layer[1], int(np.prod(shape)) // layer[1])
     return flops, nbytes, n_params
 
 
@@ -328,7 +342,7 @@ def measure(wl, steps, warmup):
     # with the update in the epilogue), timed and bounded apart.
     sym = {"gemm_fwd": ["gemm_fwd"], "gemm_bwd": ["gemm_bwd"], "conv_fwd": ["conv_fwd"],
            "conv_dgrad": ["conv_dgrad"], "conv_wgrad": ["conv_wgrad"], "ce": ["ce"], "sgd": ["sgd"],
-           "other": ["other"]}
+           "other": ["other"], "attn": ["attn"]}
     per_sym = {}
     for name, classes in sym.items():
         ms = sum(kern[c]["ms_per_step"] for c in classes if c in kern)

@@ -76,12 +76,29 @@ typedef enum {
    * return UN_ERR_UNSUPPORTED (shape mismatches UN_ERR_INVALID). The markers
    * have no parameters. */
   UN_RESIDUAL_BEGIN = 5,
-  UN_RESIDUAL_END = 6
+  UN_RESIDUAL_END = 6,
+  /* View flat features as a sequence of `out` tokens of F / out features each
+   * (PyTorch's Unflatten(1, (out, F / out)); F must divide). A Linear layer on
+   * a sequence acts on every token (PyTorch's Linear on [B, T, d]); Flatten
+   * turns a sequence back into T * d features, token by token. Allowed on the
+   * network input or on a Linear layer's flat output. Token features (the
+   * result of UN_UNFLATTEN and every Linear on a sequence) must be a multiple
+   * of 8. */
+  UN_UNFLATTEN = 7,
+  /* Single-head self-attention on a sequence [T, d] (PyTorch's
+   * MultiheadAttention(d, 1 head) called on (x, x, x), no mask, no dropout):
+   * [Q K V] = x W_in^T + b_in, A = softmax(Q K^T / sqrt(d)) V over the
+   * tokens of each sample, y = A W_out^T + b_out. Parameters in state_dict
+   * order: in_proj_weight [3d, d], in_proj_bias [3d], out_proj.weight
+   * [d, d], out_proj.bias [d]. A ReLU may follow, and residual markers may
+   * enclose it (x + attn(x)). T <= 64 and the per-sample working set
+   * (4 T (d + 1) + 2 T (T + 1) floats) must fit 160 KiB of LDS. */
+  UN_SELF_ATTENTION = 8
 } un_op;
 
 typedef struct {
   int32_t op;      /* un_op */
-  int32_t out;     /* UN_LINEAR: out features; UN_CONV2D: out channels; else 0 */
+  int32_t out;     /* UN_LINEAR: out features; UN_CONV2D: out channels; UN_UNFLATTEN: tokens; else 0 */
   int32_t kernel;  /* UN_CONV2D only */
   int32_t pad;     /* UN_CONV2D only */
 } un_layer;
@@ -351,7 +368,8 @@ typedef enum {
   UN_K_CE = 5,          /* softmax cross-entropy */
   UN_K_SGD = 6,         /* weight copy refresh (SGD kernel without gradient) */
   UN_K_OTHER = 7,       /* split-K reduction with the fused conv update */
-  UN_K_COUNT = 8
+  UN_K_ATTN = 8,        /* self-attention core, forward and backward */
+  UN_K_COUNT = 9
 } un_kernel_class;
 
 /* Enable (1) or disable (0) per-kernel timing: while enabled, every launch is

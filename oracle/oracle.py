@@ -469,8 +469,9 @@ def backward(spec, params, cache, dlogits, mode="f32", acc="f64"):
             gskip = g
             continue
         if kind == "res_begin":
-            # both paths reach the block's input: the enclosed layers' and the skip
-            g = R.store(g + R.operand(gskip))
+            # both paths reach the block's input: the enclosed layers' and the
+            # skip (a block opened at the network input needs no input gradient)
+            g = None if g is None else R.store(g + R.operand(gskip))
             gskip = None
             continue
         if kind in ("linear", "conv"):

@@ -152,6 +152,34 @@ struct ReduceProb {
 };
 
 // ---------------------------------------------------------------------------
+// Self-attention core of one model, per sample b (one workgroup each):
+//   forward:  S = Q K^T * scale, P = softmax(S) over the keys, A = P V
+//   backward: dP = dA V^T, dS = P * (dP - rowsum(P * dP)), dQ = dS K * scale,
+//             dK = dS^T Q * scale, dV = P^T dA
+// Q | K | V are the three d-column parts of the in-projection's token rows
+// (QKV [B*T][ldq], storage type); A and dA are [B*T][lda]; dQKV has QKV's
+// layout; P [B][T][T] fp32 is written by the forward and read by the backward.
+// Every output element is one fmaf chain in a fixed order.
+// ---------------------------------------------------------------------------
+struct AttnProb {
+  const void* QKV;
+  int64_t ldq;
+  void* A;
+  int64_t lda;
+  const void* dA;
+  void* dQKV;
+  float* P;
+  int32_t T, d, B;
+  float scale;
+};
+
+// LDS of one workgroup: Q, K, V (and dA) as fp32 rows of d + 1, and one (two)
+// T x (T + 1) fp32 score tiles.
+inline size_t attn_lds_bytes(int T, int d, bool bwd) {
+  return ((size_t)(bwd ? 4 : 3) * T * (d + 1) + (size_t)(bwd ? 2 : 1) * T * (T + 1)) * 4;
+}
+
+// ---------------------------------------------------------------------------
 // Optimizer of one model for one step, computed on the host per step (all
 // fields fp32 so that the array travels as plain floats):
 //   kind 0  SGD:           w <- fma(-lr, g, w)
@@ -237,6 +265,9 @@ hipError_t launch_conv_halo(bool bf16, bool dgrad, const ConvProb* probs, const 
 hipError_t launch_reduce(bool bf16, const ReduceProb* probs, const int32_t* blk_prob, int nblocks, float lr,
                          const float* lrv, const OptHp* opt, bool keep_grads, int64_t wsoff, hipStream_t s);
 hipError_t launch_set_values(float* dst, const float* vals, int n, hipStream_t s);
+// tile_map: one (problem, sample) pair per workgroup.
+hipError_t launch_attn(bool bf16, bool bwd, const AttnProb* probs, const int32_t* tile_map, int nblocks,
+                       size_t lds_bytes, hipStream_t s);
 // probs: the first nrows problems need the row pass (their CE is not fused
 // into the logits GEMM); the loss of every one of the nprobs is finished.
 // Partials of model m are at partial + m * pstride; maxB is the largest

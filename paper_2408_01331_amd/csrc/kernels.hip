@@ -2188,6 +2188,129 @@ __global__ void ce_finish_kernel(const CeProb* __restrict__ probs, const float* 
 }
 
 // ---------------------------------------------------------------------------
+// Self-attention core (AttnProb), one workgroup of 256 threads per (problem,
+// sample). The sample's Q, K, V (and dA) rows are staged in LDS as fp32 with
+// rows padded to d + 1 floats; every output element is one fmaf chain over
+// its contraction index in ascending order, and the softmax row reductions
+// are fixed lane-shuffle butterflies, so the result depends on nothing but
+// the sample's own values.
+// ---------------------------------------------------------------------------
+template <typename T>
+__device__ __forceinline__ void attn_stage(const AttnProb& p, int b, float* sQ, float* sK, float* sV) {
+  const int Tn = p.T, d = p.d, ld = d + 1;
+  const T* qkv = (const T*)p.QKV + (int64_t)b * Tn * p.ldq;
+  for (int e = threadIdx.x; e < Tn * d; e += blockDim.x) {
+    const int t = e / d, j = e - t * d;
+    const T* row = qkv + (int64_t)t * p.ldq;
+    sQ[t * ld + j] = TT<T>::to_f(row[j]);
+    sK[t * ld + j] = TT<T>::to_f(row[d + j]);
+    sV[t * ld + j] = TT<T>::to_f(row[2 * d + j]);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void attn_fwd_kernel(const AttnProb* __restrict__ probs,
+                                                       const int32_t* __restrict__ tile_map) {
+  extern __shared__ float sm[];
+  const int pi = tile_map[2 * blockIdx.x], b = tile_map[2 * blockIdx.x + 1];
+  if (pi < 0) return;
+  const AttnProb& p = probs[pi];
+  const int Tn = p.T, d = p.d, ld = d + 1, ls = Tn + 1;
+  float* sQ = sm;
+  float* sK = sQ + Tn * ld;
+  float* sV = sK + Tn * ld;
+  float* sS = sV + Tn * ld;  // [T][T + 1]: scores, then probabilities
+  attn_stage<T>(p, b, sQ, sK, sV);
+  __syncthreads();
+  for (int e = threadIdx.x; e < Tn * Tn; e += blockDim.x) {
+    const int i = e / Tn, t = e - i * Tn;
+    float acc = 0.f;
+    for (int k = 0; k < d; ++k) acc = fmaf(sQ[i * ld + k], sK[t * ld + k], acc);
+    sS[i * ls + t] = acc * p.scale;
+  }
+  __syncthreads();
+  // softmax over the keys: one wave per query row, lanes over the keys (T <= 64)
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  float* Pg = p.P + (int64_t)b * Tn * Tn;
+  for (int i = wave; i < Tn; i += nw) {
+    const float v = lane < Tn ? sS[i * ls + lane] : -INFINITY;
+    const float mx = wave_max(v);
+    const float ex = lane < Tn ? expf(v - mx) : 0.f;
+    const float inv = 1.0f / wave_sum(ex);
+    if (lane < Tn) {
+      const float pr = ex * inv;
+      sS[i * ls + lane] = pr;
+      Pg[(int64_t)i * Tn + lane] = pr;
+    }
+  }
+  __syncthreads();
+  T* A = (T*)p.A + (int64_t)b * Tn * p.lda;
+  for (int e = threadIdx.x; e < Tn * d; e += blockDim.x) {
+    const int i = e / d, j = e - i * d;
+    float acc = 0.f;
+    for (int t = 0; t < Tn; ++t) acc = fmaf(sS[i * ls + t], sV[t * ld + j], acc);
+    A[(int64_t)i * p.lda + j] = TT<T>::from_f(acc);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void attn_bwd_kernel(const AttnProb* __restrict__ probs,
+                                                       const int32_t* __restrict__ tile_map) {
+  extern __shared__ float sm[];
+  const int pi = tile_map[2 * blockIdx.x], b = tile_map[2 * blockIdx.x + 1];
+  if (pi < 0) return;
+  const AttnProb& p = probs[pi];
+  const int Tn = p.T, d = p.d, ld = d + 1, ls = Tn + 1;
+  float* sQ = sm;
+  float* sK = sQ + Tn * ld;
+  float* sV = sK + Tn * ld;
+  float* sD = sV + Tn * ld;   // dA
+  float* sP = sD + Tn * ld;   // [T][T + 1] probabilities
+  float* sG = sP + Tn * ls;   // [T][T + 1] dP, then dS
+  attn_stage<T>(p, b, sQ, sK, sV);
+  const T* dA = (const T*)p.dA + (int64_t)b * Tn * p.lda;
+  const float* Pg = p.P + (int64_t)b * Tn * Tn;
+  for (int e = threadIdx.x; e < Tn * d; e += blockDim.x) {
+    const int i = e / d, j = e - i * d;
+    sD[i * ld + j] = TT<T>::to_f(dA[(int64_t)i * p.lda + j]);
+  }
+  for (int e = threadIdx.x; e < Tn * Tn; e += blockDim.x) {
+    const int i = e / Tn, t = e - i * Tn;
+    sP[i * ls + t] = Pg[e];
+  }
+  __syncthreads();
+  // dP[i][t] = sum_j dA[i][j] V[t][j]
+  for (int e = threadIdx.x; e < Tn * Tn; e += blockDim.x) {
+    const int i = e / Tn, t = e - i * Tn;
+    float acc = 0.f;
+    for (int j = 0; j < d; ++j) acc = fmaf(sD[i * ld + j], sV[t * ld + j], acc);
+    sG[i * ls + t] = acc;
+  }
+  __syncthreads();
+  // dS = P * (dP - rowsum(P * dP)), one wave per row
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  for (int i = wave; i < Tn; i += nw) {
+    const float pr = lane < Tn ? sP[i * ls + lane] : 0.f;
+    const float dp = lane < Tn ? sG[i * ls + lane] : 0.f;
+    const float rd = wave_sum(pr * dp);
+    if (lane < Tn) sG[i * ls + lane] = pr * (dp - rd);
+  }
+  __syncthreads();
+  T* dqkv = (T*)p.dQKV + (int64_t)b * Tn * p.ldq;
+  for (int e = threadIdx.x; e < Tn * d; e += blockDim.x) {
+    const int r = e / d, k = e - r * d;
+    float q = 0.f, kk = 0.f, v = 0.f;
+    for (int t = 0; t < Tn; ++t) q = fmaf(sG[r * ls + t], sK[t * ld + k], q);        // dQ[r][k]
+    for (int i = 0; i < Tn; ++i) kk = fmaf(sG[i * ls + r], sQ[i * ld + k], kk);      // dK[r][k]
+    for (int i = 0; i < Tn; ++i) v = fmaf(sP[i * ls + r], sD[i * ld + k], v);        // dV[r][k]
+    T* row = dqkv + (int64_t)r * p.ldq;
+    row[k] = TT<T>::from_f(q * p.scale);
+    row[d + k] = TT<T>::from_f(kk * p.scale);
+    row[2 * d + k] = TT<T>::from_f(v);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Multi-tensor SGD (64x64 tiles; the transposed copy goes through LDS).
 // ---------------------------------------------------------------------------
 template <typename T>
@@ -2395,6 +2518,38 @@ hipError_t launch_set_values(float* dst, const float* vals, int n, hipStream_t s
     SetValues sv{};
     for (int i = 0; i < k; ++i) sv.v[i] = vals[i0 + i];
     hipLaunchKernelGGL(set_values_kernel, dim3(1), dim3(SETV_CHUNK), 0, s, dst + i0, sv, k);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attn(bool bf16, bool bwd, const AttnProb* probs, const int32_t* tile_map, int nblocks,
+                       size_t lds_bytes, hipStream_t s) {
+  if (nblocks <= 0) return hipSuccess;
+  if (lds_bytes > (size_t)160 * 1024) return hipErrorInvalidValue;
+  // allow dynamic LDS up to the whole 160 KiB of a CU (above the default cap)
+  static const hipError_t attr = [] {
+    hipError_t e = hipSuccess, r;
+    const void* k[4] = {reinterpret_cast<const void*>(&attn_fwd_kernel<bf16_t>),
+                        reinterpret_cast<const void*>(&attn_fwd_kernel<float>),
+                        reinterpret_cast<const void*>(&attn_bwd_kernel<bf16_t>),
+                        reinterpret_cast<const void*>(&attn_bwd_kernel<float>)};
+    for (const void* f : k) {
+      r = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+      if (r != hipSuccess) e = r;
+    }
+    return e;
+  }();
+  if (attr != hipSuccess) return attr;
+  if (bwd) {
+    if (bf16)
+      hipLaunchKernelGGL(attn_bwd_kernel<bf16_t>, dim3(nblocks), dim3(256), lds_bytes, s, probs, tile_map);
+    else
+      hipLaunchKernelGGL(attn_bwd_kernel<float>, dim3(nblocks), dim3(256), lds_bytes, s, probs, tile_map);
+  } else {
+    if (bf16)
+      hipLaunchKernelGGL(attn_fwd_kernel<bf16_t>, dim3(nblocks), dim3(256), lds_bytes, s, probs, tile_map);
+    else
+      hipLaunchKernelGGL(attn_fwd_kernel<float>, dim3(nblocks), dim3(256), lds_bytes, s, probs, tile_map);
   }
   return hipGetLastError();
 }

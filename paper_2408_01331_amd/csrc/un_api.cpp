@@ -35,7 +35,8 @@ inline int64_t rup(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 inline int cdiv(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 struct Block {
-  int kind = 0;  // 0 linear, 1 conv
+  int kind = 0;  // 0 linear, 1 conv, 2 self-attention core (between its two projections)
+  int tokens = 1;  // a Linear on a sequence acts on every token: its GEMM rows are batch * tokens
   int level = 0, model = 0;
   bool relu = false, pool = false, last = false, prev_relu = false, concat = false;
   bool next_linear = false;  // the following block is a Linear (needs transposed output)
@@ -61,6 +62,7 @@ struct Block {
   size_t X = NONE;         // input (the previous block's output), row-major
   int64_t ldx = 0;
   size_t Y = NONE, amax = NONE;
+  size_t P = NONE;         // attention core: softmax probabilities [batch][T][T] fp32
   int64_t ldy = 0;
   size_t G = NONE;         // gradient at this block's output, row-major
   int64_t ldg = 0;
@@ -233,6 +235,8 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
   // h = w = 1. After a Flatten or a Linear the tensor is flat.
   int c = in.in_c, h = in.in_h, w = in.in_w;
   bool flat = false;
+  int seq = 0;            // a sequence of `seq` tokens of c features (h = w = 1)
+  bool torch_order = in.in_h == 1 && in.in_w == 1;  // flat storage equals PyTorch's flatten order
   size_t pt = 0;
   int i = 0;
   int res_open = -1, res_c = 0, res_h = 0, res_w = 0;  // first block and input shape of an open residual block
@@ -244,8 +248,12 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
         why = where(i) + "nested residual blocks are not supported";
         return UN_ERR_UNSUPPORTED;
       }
-      if (m.blocks.empty() || s.layers[i - 1].op == UN_FLATTEN) {
-        why = where(i) + "a residual block must start at the output of a Linear or Conv2d block";
+      // the skip reads the first enclosed block's input: a block's output, or
+      // the network's input when that is flat or a sequence (an image input
+      // is staged channel-padded for the convolutions)
+      if ((m.blocks.empty() && !(seq || (h == 1 && w == 1))) || s.layers[i - 1].op == UN_FLATTEN) {
+        why = where(i) + "a residual block must start at the output of a Linear, Conv2d or attention block, "
+                         "or at a flat or sequence input";
         return UN_ERR_UNSUPPORTED;
       }
       res_open = (int)m.blocks.size();
@@ -264,12 +272,12 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
         why = where(i) + "empty residual block";
         return UN_ERR_INVALID;
       }
-      if (s.layers[i - 1].op != UN_LINEAR && s.layers[i - 1].op != UN_CONV2D) {
-        why = where(i) + "a residual block must end with a Linear or Conv2d (a ReLU goes after the end marker)";
+      if (s.layers[i - 1].op != UN_LINEAR && s.layers[i - 1].op != UN_CONV2D && s.layers[i - 1].op != UN_SELF_ATTENTION) {
+        why = where(i) + "a residual block must end with a Linear, Conv2d or attention (a ReLU goes after the end marker)";
         return UN_ERR_UNSUPPORTED;
       }
       Block& e = m.blocks.back();
-      if (e.kind == 0 ? e.N != res_c : (e.O != res_c || e.OH != res_h || e.OW != res_w)) {
+      if (e.kind == 0 ? (e.N != res_c || e.tokens != std::max(seq, 1)) : (e.O != res_c || e.OH != res_h || e.OW != res_w)) {
         why = where(i) + "a residual block's output shape differs from its input's";
         return UN_ERR_INVALID;
       }
@@ -287,8 +295,8 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
       }
       continue;
     }
-    if (res_open >= 0 && L.op != UN_LINEAR && L.op != UN_CONV2D && L.op != UN_RELU) {
-      why = where(i) + "a residual block may enclose only Linear, Conv2d and ReLU layers";
+    if (res_open >= 0 && L.op != UN_LINEAR && L.op != UN_CONV2D && L.op != UN_RELU && L.op != UN_SELF_ATTENTION) {
+      why = where(i) + "a residual block may enclose only Linear, Conv2d, attention and ReLU layers";
       return UN_ERR_UNSUPPORTED;
     }
     if (res_open >= 0 && L.op == UN_CONV2D && i + 1 < s.n_layers &&
@@ -298,8 +306,8 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
       return UN_ERR_UNSUPPORTED;
     }
     if (L.op == UN_CONV2D) {
-      if (flat) {
-        why = where(i) + "conv needs an image input (got a flat tensor)";
+      if (flat || seq) {
+        why = where(i) + "conv needs an image input (got a flat tensor or a sequence)";
         return UN_ERR_INVALID;
       }
       if (L.out <= 0 || L.kernel <= 0 || L.pad < 0) {
@@ -346,8 +354,74 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
       w = b.pool ? b.PW : b.OW;
       flat = false;
       m.blocks.push_back(b);
+    } else if (L.op == UN_UNFLATTEN) {
+      if (seq || !(flat || (h == 1 && w == 1)) || !torch_order) {
+        why = where(i) + "unflatten reads the network's flat input or a Linear layer's flat output";
+        return UN_ERR_UNSUPPORTED;
+      }
+      const int F = c * h * w;
+      if (L.out <= 0 || F % L.out != 0) {
+        why = where(i) + "unflatten: the tokens must divide the features";
+        return UN_ERR_INVALID;
+      }
+      seq = L.out;
+      c = F / L.out;
+      h = w = 1;
+      flat = false;
+      if (c % 8 != 0) {
+        why = where(i) + "token features must be a multiple of 8";
+        return UN_ERR_UNSUPPORTED;
+      }
+      ++i;
+    } else if (L.op == UN_SELF_ATTENTION) {
+      if (!seq) {
+        why = where(i) + "attention needs a sequence (add an unflatten)";
+        return UN_ERR_INVALID;
+      }
+      const int d = c;
+      const size_t lds = ((size_t)4 * seq * (d + 1) + (size_t)2 * seq * (seq + 1)) * 4;
+      if (seq > 64 || lds > (size_t)160 * 1024) {
+        why = where(i) + "attention supports up to 64 tokens whose working set fits 160 KiB of LDS";
+        return UN_ERR_UNSUPPORTED;
+      }
+      // in-projection, core, out-projection: three blocks (levels)
+      Block bi;
+      bi.kind = 0;
+      bi.tokens = seq;
+      bi.in_c = d;
+      bi.K = d;
+      bi.N = 3 * d;
+      bi.n_w = (size_t)3 * d * d;
+      bi.n_b = (size_t)3 * d;
+      bi.pt_w = pt;
+      bi.pt_b = pt + bi.n_w;
+      pt += bi.n_w + bi.n_b;
+      m.blocks.push_back(bi);
+      Block bc;
+      bc.kind = 2;
+      bc.tokens = seq;
+      bc.K = d;
+      bc.N = d;
+      m.blocks.push_back(bc);
+      Block bo;
+      bo.kind = 0;
+      bo.tokens = seq;
+      bo.in_c = d;
+      bo.K = d;
+      bo.N = d;
+      bo.n_w = (size_t)d * d;
+      bo.n_b = (size_t)d;
+      bo.pt_w = pt;
+      bo.pt_b = pt + bo.n_w;
+      pt += bo.n_w + bo.n_b;
+      ++i;
+      if (i < s.n_layers && s.layers[i].op == UN_RELU) {
+        bo.relu = true;
+        ++i;
+      }
+      m.blocks.push_back(bo);
     } else if (L.op == UN_LINEAR) {
-      if (!flat && !(h == 1 && w == 1)) {
+      if (!seq && !flat && !(h == 1 && w == 1)) {
         why = where(i) + "linear on an image needs a flatten first";
         return UN_ERR_INVALID;
       }
@@ -355,8 +429,13 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
         why = where(i) + "bad linear out";
         return UN_ERR_INVALID;
       }
+      if (seq && L.out % 8 != 0) {
+        why = where(i) + "token features must be a multiple of 8";
+        return UN_ERR_UNSUPPORTED;
+      }
       Block b;
       b.kind = 0;
+      b.tokens = std::max(seq, 1);
       b.in_c = c;
       b.in_h = h;
       b.in_w = w;
@@ -374,9 +453,17 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
       }
       c = b.N;
       h = w = 1;
-      flat = true;
+      flat = !seq;
+      torch_order = true;
       m.blocks.push_back(b);
     } else if (L.op == UN_FLATTEN) {
+      if (seq) {
+        // token by token: the storage [T][d] is already PyTorch's flatten order
+        c = seq * c;
+        seq = 0;
+      } else {
+        torch_order = h == 1 && w == 1;
+      }
       flat = true;  // keep (c, h, w): the next Linear maps NCHW order onto NHWC storage
       ++i;
     } else if (L.op == UN_RELU || L.op == UN_MAXPOOL2) {
@@ -391,8 +478,8 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
     why = "model " + std::to_string(mi) + ": residual block without an end";
     return UN_ERR_INVALID;
   }
-  if (m.blocks.empty() || m.blocks.back().kind != 0) {
-    why = "model " + std::to_string(mi) + ": the last parameterised layer must be Linear";
+  if (m.blocks.empty() || m.blocks.back().kind != 0 || m.blocks.back().tokens != 1) {
+    why = "model " + std::to_string(mi) + ": the last layer must be a Linear on flat features";
     return UN_ERR_UNSUPPORTED;
   }
   if (m.blocks.back().res_from >= 0) {
@@ -415,7 +502,7 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
     b.model = mi;
     b.prev_relu = j > 0 && m.blocks[j - 1].relu;
     b.next_linear = j + 1 < m.blocks.size() && m.blocks[j + 1].kind == 0;
-    if (j + 1 < m.blocks.size() && m.blocks[j + 1].kind == 1 && b.kind == 0) {
+    if (j + 1 < m.blocks.size() && m.blocks[j + 1].kind == 1 && b.kind != 1) {
       why = "model " + std::to_string(mi) + ": Conv2d after Linear is not supported";
       return UN_ERR_UNSUPPORTED;
     }
@@ -729,6 +816,28 @@ static void build_tables(un_ctx* c, Tables& T) {
     }
   };
 
+  // attention core: one workgroup per (problem, sample)
+  auto emit_attn = [&](std::vector<AttnProb>& ps, std::vector<Launch>& out, int kind) {
+    if (ps.empty()) return;
+    std::vector<int32_t> map;
+    for (size_t k = 0; k < ps.size(); ++k)
+      for (int b = 0; b < ps[k].B; ++b) {
+        map.push_back((int32_t)k);
+        map.push_back(b);
+      }
+    size_t lds = 0;
+    for (auto& p : ps) lds = std::max(lds, attn_lds_bytes(p.T, p.d, kind == 10));
+    size_t po = put(ps.data(), ps.size() * sizeof(AttnProb));
+    for (size_t k = 0; k < ps.size(); ++k) {
+      size_t b0 = po + k * sizeof(AttnProb);
+      for (size_t f : {offsetof(AttnProb, QKV), offsetof(AttnProb, A), offsetof(AttnProb, dA), offsetof(AttnProb, dQKV),
+                       offsetof(AttnProb, P)})
+        fix.push_back(b0 + f);
+    }
+    size_t mo = put(map.data(), map.size() * 4);
+    out.push_back(Launch{kind, UN_K_ATTN, po, mo, (int)(map.size() / 2)});
+    out.back().lds = lds;
+  };
   auto conv_base = [&](const Block& b) {
     ConvProb p{};
     p.Nb = c->groups[c->models[b.model].group].B;
@@ -753,6 +862,7 @@ static void build_tables(un_ctx* c, Tables& T) {
   for (int lv = 0; lv < levels; ++lv) {
     std::vector<GemmProb> gp;
     std::vector<ConvProb> cp;
+    std::vector<AttnProb> ap;
     std::vector<char> cat_done(c->groups.size(), 0);
     for (auto& m : c->models) {
       if (lv >= (int)m.blocks.size() || !c->active[m.blocks[0].model]) continue;
@@ -787,7 +897,7 @@ static void build_tables(un_ctx* c, Tables& T) {
         p.lda = b.ldx;
         p.B = ptr(bf ? b.Wb : b.W32);
         p.ldb = b.ldw;
-        p.M = B;
+        p.M = B * b.tokens;
         p.N = b.N;
         p.K = b.K;
         p.epi = b.last ? EPI_LOGITS : EPI_FWD;
@@ -810,6 +920,19 @@ static void build_tables(un_ctx* c, Tables& T) {
           p.lab_own = (int32_t)m.lab_own;
         }
         gp.push_back(p);
+      } else if (b.kind == 2) {
+        const Block& bi = m.blocks[lv - 1];  // the in-projection: Q | K | V per token row
+        AttnProb p{};
+        p.QKV = ptr(bi.Y);
+        p.ldq = bi.ldy;
+        p.A = ptr(b.Y);
+        p.lda = b.ldy;
+        p.P = (float*)ptr(b.P);
+        p.T = b.tokens;
+        p.d = b.N;
+        p.B = B;
+        p.scale = (float)(1.0 / std::sqrt((double)b.N));
+        ap.push_back(p);
       } else {
         ConvProb p = conv_base(b);
         p.M = b.pool ? B * b.PH * b.PW * 4 : B * b.OH * b.OW;
@@ -828,6 +951,7 @@ static void build_tables(un_ctx* c, Tables& T) {
     }
     emit_gemm(gp, fwd, UN_K_GEMM_FWD);
     emit_conv(cp, fwd, 1, UN_K_CONV_FWD);
+    emit_attn(ap, fwd, 9);
   }
 
   // softmax-CE: the row pass for the models whose CE is not fused (listed
@@ -918,7 +1042,7 @@ static void build_tables(un_ctx* c, Tables& T) {
     p.bmode = OP_KMAJ;
     p.M = b.N;
     p.N = b.K + 1;
-    p.K = B;
+    p.K = B * b.tokens;
     p.epi = EPI_WGRAD;
     p.nsplit = b.K;
     p.C = ptr(b.gW);
@@ -938,6 +1062,7 @@ static void build_tables(un_ctx* c, Tables& T) {
     std::vector<GemmProb> gp;
     std::vector<ConvProb> dp, wp;
     std::vector<ReduceProb> rp;
+    std::vector<AttnProb> ap;
     std::vector<char> cat_done(c->groups.size(), 0);
     for (auto& m : c->models) {
       if (!c->active[m.blocks[0].model]) continue;
@@ -956,7 +1081,7 @@ static void build_tables(un_ctx* c, Tables& T) {
           p.B = ptr(bf ? b.Wb : b.W32);
           p.ldb = b.ldw;
           p.bmode = OP_KMAJ;
-          p.M = B;
+          p.M = B * b.tokens;
           p.N = b.K;
           p.K = b.N;
           p.epi = EPI_DGRAD;
@@ -964,7 +1089,7 @@ static void build_tables(un_ctx* c, Tables& T) {
           p.mask = ptr(b.X);  // the previous block's stored output, row-major
           p.ldmask = b.ldx;
           p.C = ptr(pb.G);
-          p.ldc = pb.kind == 0 ? pb.ldg : pb.out_elems_per_sample();
+          p.ldc = pb.kind == 1 ? pb.out_elems_per_sample() : pb.ldg * pb.tokens / b.tokens;
           if (b.res_to >= 0) {
             const Block& eb = m.blocks[b.res_to];
             p.R = ptr(eb.G);
@@ -973,6 +1098,22 @@ static void build_tables(un_ctx* c, Tables& T) {
           gp.push_back(p);
         }
         if (lv == 0) add_wgrad(b, gp, cat_done);
+      } else if (b.kind == 2) {
+        // attention core backward: dA (written by the out-projection's data
+        // gradient) -> dQ | dK | dV, the gradient at the in-projection's output
+        const Block& bi = m.blocks[lv - 1];
+        AttnProb p{};
+        p.QKV = ptr(bi.Y);
+        p.ldq = bi.ldy;
+        p.dA = ptr(b.G);
+        p.lda = b.ldg;
+        p.dQKV = ptr(bi.G);
+        p.P = (float*)ptr(b.P);
+        p.T = b.tokens;
+        p.d = b.N;
+        p.B = B;
+        p.scale = (float)(1.0 / std::sqrt((double)b.N));
+        ap.push_back(p);
       } else {
         const int J = b.KH * b.KH * b.C;
         if (lv > 0) {
@@ -1027,6 +1168,7 @@ static void build_tables(un_ctx* c, Tables& T) {
       }
     }
     emit_gemm(gp, bwd, UN_K_GEMM_BWD);
+    emit_attn(ap, bwd, 10);
     emit_conv(dp, bwd, 2, UN_K_CONV_DGRAD);
     emit_conv(wp, bwd, 3, UN_K_CONV_WGRAD);
     if (!rp.empty()) {
@@ -1184,10 +1326,16 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
                       std::to_string(gi) + ")");
 
     // level-0 concatenation: the group's hidden Linear + ReLU first layers
+    // whose output is read as flat rows (a sequence view needs rows of one
+    // token, which the concatenated output's row stride cannot give) and
+    // that add no skip of their own (the joint GEMM has no per-model operand)
     g.cat.clear();
     for (size_t i = 0; i < N; ++i) {
-      const Block& b = c->models[i].blocks[0];
-      if (c->models[i].group == (int)gi && b.kind == 0 && !b.last && b.relu) g.cat.push_back((int)i);
+      const auto& bl = c->models[i].blocks;
+      const Block& b = bl[0];
+      if (c->models[i].group == (int)gi && b.kind == 0 && b.tokens == 1 && !b.last && b.relu && b.res_from < 0 &&
+          bl[1].tokens == 1)
+        g.cat.push_back((int)i);
     }
     g.cat_rows = 0;
     for (int i : g.cat) {
@@ -1216,7 +1364,15 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
     levels = std::max(levels, (int)m.blocks.size());
     for (size_t j = 0; j < m.blocks.size(); ++j) {
       Block& b = m.blocks[j];
-      if (b.kind == 0) {
+      const int64_t R = (int64_t)B * b.tokens;  // GEMM rows: samples, or samples x tokens
+      if (b.kind == 2) {
+        // attention core: A [R][d] and its gradient, P [B][T][T] fp32; no weights
+        b.ldy = b.N;
+        b.Y = A.take((size_t)R * b.ldy * es);
+        b.ldg = b.N;
+        b.G = A.take((size_t)R * b.ldg * es);
+        b.P = A.take((size_t)B * b.tokens * b.tokens * 4);
+      } else if (b.kind == 0) {
         b.rows = b.N;
         b.ldw = rup(b.K, 8);
         if (j == 0 && c->cat_off[mi] >= 0) {
@@ -1239,13 +1395,13 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
           if (bf) b.Wb = A.take((size_t)b.N * b.ldw * 2);
           if (b.last) {
             b.ldy = rup(b.N, 8);
-            b.Y = A.take((size_t)B * b.ldy * 4);  // fp32 logits
+            b.Y = A.take((size_t)R * b.ldy * 4);  // fp32 logits
           } else {
             b.ldy = rup(b.N, 8);
-            b.Y = A.take((size_t)B * b.ldy * es);
+            b.Y = A.take((size_t)R * b.ldy * es);
           }
           b.ldg = rup(b.N, 8);
-          b.G = A.take((size_t)B * b.ldg * es);
+          b.G = A.take((size_t)R * b.ldg * es);
         }
       } else {
         const int J = b.KH * b.KH * b.C;
@@ -1285,13 +1441,15 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
     // wire inputs
     for (size_t j = 0; j < m.blocks.size(); ++j) {
       Block& b = m.blocks[j];
+      // row strides: a token-wise layer reads rows of one token, a flat one
+      // rows of one sample (a sequence's storage [T][d] is its flat view)
       if (j == 0) {
         b.X = (b.kind == 1 && g.XinC != NONE) ? g.XinC : g.Xin;
-        b.ldx = g.ldxin;
+        b.ldx = b.kind == 1 ? g.ldxin : g.ldxin / b.tokens;
       } else {
         Block& p = m.blocks[j - 1];
         b.X = p.Y;
-        b.ldx = p.kind == 0 ? p.ldy : p.out_elems_per_sample();
+        b.ldx = p.kind == 1 ? p.out_elems_per_sample() : p.ldy * p.tokens / b.tokens;
       }
     }
   }
@@ -1405,6 +1563,7 @@ static un_status write_blocks(un_ctx* c, int i, char* base, size_t Block::*wf, s
   Model& m = c->models[i];
   std::vector<float> w, bias;
   for (auto& b : m.blocks) {
+    if (b.kind == 2) continue;  // the attention core has no parameters
     to_internal(b, src, w, bias);
     // on the context's stream, completed before the host buffers go away
     HIPCHK(c, hipMemcpyAsync(base + b.*wf, w.data(), w.size() * 4, hipMemcpyHostToDevice, c->stream));
@@ -1419,6 +1578,7 @@ static un_status read_blocks(un_ctx* c, int i, const char* base, size_t Block::*
   HIPCHK(c, hipStreamSynchronize(c->stream));
   std::vector<float> w, bias;
   for (auto& b : m.blocks) {
+    if (b.kind == 2) continue;
     w.resize((size_t)b.rows * b.ldw);
     bias.resize(b.rows);
     HIPCHK(c, hipMemcpyAsync(w.data(), base + b.*wf, w.size() * 4, hipMemcpyDeviceToHost, c->stream));
@@ -1444,6 +1604,7 @@ static void init_host(const Model& m, std::vector<float>& pt) {
   pt.assign(m.n_params, 0.f);
   int t = 0;
   for (auto& b : m.blocks) {
+    if (b.kind == 2) continue;
     const double fan_in = b.kind == 0 ? (double)b.K : (double)b.Cr * b.KH * b.KH;
     const double wb = std::sqrt(6.0 / fan_in), bb = 1.0 / std::sqrt(fan_in);
     for (int part = 0; part < 2; ++part, ++t) {
@@ -1511,6 +1672,11 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
       break;
     case 6:
       e = launch_sgd(c->bf16, c->at<SgdTensor>(l.probs), c->at<int32_t>(l.map), 0, l.count, lr, true, c->stream);
+      break;
+    case 9:
+    case 10:
+      e = launch_attn(c->bf16, l.kind == 10, c->at<AttnProb>(l.probs), c->at<int32_t>(l.map), l.count, l.lds,
+                      c->stream);
       break;
   }
   if (c->profiling && a && b) {
@@ -1827,6 +1993,7 @@ static size_t state_layout(un_ctx* c) {
   }
   for (size_t mi = 0; mi < c->models.size(); ++mi)
     for (auto& b : c->models[mi].blocks) {
+      if (b.kind == 2) continue;
       if (b.concat) {
         const Group& g = c->groups[c->models[mi].group];
         const size_t roff = (size_t)c->cat_off[mi];
@@ -1862,6 +2029,7 @@ static un_status alloc_state(un_ctx* c) {
 static un_status clear_state(un_ctx* c, int i) {
   if (!c->sbase) return UN_OK;
   for (auto& b : c->models[i].blocks) {
+    if (b.kind == 2) continue;
     HIPCHK(c, hipMemsetAsync(c->sbase + b.S1, 0, (size_t)b.rows * b.ldw * 4, c->stream));
     HIPCHK(c, hipMemsetAsync(c->sbase + b.S2, 0, (size_t)b.rows * b.ldw * 4, c->stream));
     HIPCHK(c, hipMemsetAsync(c->sbase + b.S1b, 0, (size_t)b.rows * 4, c->stream));

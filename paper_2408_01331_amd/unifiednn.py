@@ -23,8 +23,9 @@ STATUS_NAMES = ["UN_OK", "UN_ERR_INVALID", "UN_ERR_STATE", "UN_ERR_OOM", "UN_ERR
 UN_F32, UN_BF16_F32MASTER = 0, 1
 UN_OPT_SGD, UN_OPT_MOMENTUM, UN_OPT_ADAM = 0, 1, 2
 OPT_KINDS = {"sgd": UN_OPT_SGD, "momentum": UN_OPT_MOMENTUM, "adam": UN_OPT_ADAM}
-OPS = {"linear": 0, "conv": 1, "relu": 2, "pool": 3, "flatten": 4, "res_begin": 5, "res_end": 6}
-KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad", "ce", "sgd", "other"]
+OPS = {"linear": 0, "conv": 1, "relu": 2, "pool": 3, "flatten": 4, "res_begin": 5, "res_end": 6, "unflatten": 7,
+       "attention": 8}
+KERNEL_CLASSES = ["gemm_fwd", "gemm_bwd", "conv_fwd", "conv_dgrad", "conv_wgrad", "ce", "sgd", "other", "attn"]
 
 # Every symbol the header declares.
 EXPORTS = ["un_create", "un_create_grouped", "un_plan_bytes", "un_plan_bytes_grouped", "un_load_group_batch",

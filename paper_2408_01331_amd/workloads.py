@@ -26,8 +26,11 @@ Design overview):
 * ``("pool",)``                    2x2 max-pool, stride 2, floor mode
 * ``("flatten",)``                 NCHW flatten order
 * ``("res_begin",)`` ... ``("res_end",)``  a residual block: the enclosed
-  Linear layers' result plus the block's input (a module returning
+  layers' result plus the block's input (a module returning
   ``inner(x) + x``); a ReLU after ``res_end`` applies to the sum
+* ``("unflatten", T)``             flat features as T tokens (a sequence); a
+  following ``linear`` acts on every token
+* ``("attention",)``               single-head self-attention on a sequence
 """
 from __future__ import annotations
 
@@ -242,6 +245,34 @@ def resnet8(seed=0):
 
 
 WORKLOADS["resnet8"] = resnet8
+
+
+def attn8(seed=0):
+    """N=8 transformer-style classifiers on synthetic token sequences: the
+    input [128, 2048] is 32 tokens of 64 features; each model embeds the
+    tokens (token-wise Linear to a width from {64, 128}), then 1-2 blocks of
+    [residual self-attention, residual token-wise MLP of twice the width],
+    then a token-wise Linear to 16, flatten and Linear-10. bf16 with fp32
+    master weights. Stands in for the paper's Transformer / XLM-R models
+    (Evaluation setup, Table 2), whose datasets are not available."""
+    rng = np.random.default_rng([seed, 5])
+    T, d0 = 32, 64
+    RB, RE, R = ("res_begin",), ("res_end",), ("relu",)
+    specs = []
+    for _ in range(8):
+        width = int(rng.choice([64, 128]))
+        blocks = int(rng.integers(1, 3))
+        layers = [("unflatten", T), ("linear", width), R]
+        for _ in range(blocks):
+            layers += [RB, ("attention",), RE, R, RB, ("linear", 2 * width), R, ("linear", width), RE, R]
+        layers += [("linear", 16), R, ("flatten",), ("linear", 10)]
+        specs.append({"layers": layers, "num_classes": 10})
+    return Workload("attn8_b128_bf16", 8, 128, (T * d0,), "bf16", specs, 0.01, 5, seed,
+                    "8 transformer-style classifiers (32 tokens x 64 features, 1-2 residual attention + MLP blocks, "
+                    "widths {64,128}) on [128,2048], bf16 with fp32 master", init="torch")
+
+
+WORKLOADS["attn8"] = attn8
 
 
 def get(name, seed=0) -> Workload:

@@ -126,56 +126,98 @@ def tensor_err(a, b, mask=None):
 
 
 def _param_layers(spec):
-    """The parameterised layers of a spec, in order, and for each one whose
-    output starts a residual block the index (in that order) of the block's
-    last parameterised layer, whose output is the residual sum."""
+    """The parameterised layers of a spec, in order, as dicts:
+    ``out_w``/``out_b``: the tensors whose row / entry u produce output unit u
+    (feature, channel or token feature); ``in_w``: the weight that reads the
+    layer's input (an attention layer reads through its in-projection and
+    produces through its out-projection); ``view``: how the previous
+    parameterised layer's unit u appears in this layer's input -
+    "same" (column / input channel u), "img_flat" (a flattened NCHW channel:
+    a block of H*W features), "seq_flat" (a flattened [T, d] sequence: every
+    d-th feature) or "unflat" (flat features read as tokens of d: feature
+    u mod d); ``skip_end``: for a layer whose output starts a residual block,
+    the index of the block's last parameterised layer (its output is the sum)
+    and the view of the skip."""
     L = spec["layers"]
-    plist = [li for li, l in enumerate(L) if l[0] in ("linear", "conv")]
-    skip_end = {}
-    for k, li in enumerate(plist):
-        nxt = plist[k + 1] if k + 1 < len(plist) else len(L)
-        if any(L[j][0] == "res_begin" for j in range(li + 1, nxt)):
-            j = nxt
-            while L[j][0] != "res_end":
+    ents, t, state, view = [], 0, "flat", "same"
+    for li, layer in enumerate(L):
+        op = layer[0]
+        if op in ("linear", "conv", "attention"):
+            n = 4 if op == "attention" else 2
+            ents.append({"li": li, "in_w": t, "out_w": t + n - 2, "out_b": t + n - 1, "view": view})
+            t += n
+            view = "same"
+            if op == "conv":
+                state = "image"
+        elif op == "flatten":
+            if state != "flat":
+                view = "img_flat" if state == "image" else "seq_flat"
+            state = "flat"
+        elif op == "unflatten":
+            if ents:
+                view = "unflat"
+            state = "seq"
+    for k, e in enumerate(ents):
+        nxt = ents[k + 1]["li"] if k + 1 < len(ents) else len(L)
+        rb = [j for j in range(e["li"] + 1, nxt) if L[j][0] == "res_begin"]
+        if rb:
+            j, depth = rb[0] + 1, 1
+            while depth:
+                depth += {"res_begin": 1, "res_end": -1}.get(L[j][0], 0)
                 j += 1
-            skip_end[k] = plist.index(max(p for p in plist if p < j))
-    return plist, skip_end
+            last = max(q for q, f in enumerate(ents) if f["li"] < j - 1)
+            sv = "unflat" if any(L[q][0] == "unflatten" for q in range(e["li"] + 1, rb[0])) else "same"
+            e["skip_end"] = (last, sv)
+    return ents
+
+
+def _units_seen(view, u, n_prev, w_next):
+    """Input columns (or channels) of the next weight that read unit u of a
+    layer with n_prev output units, under the view between them."""
+    if view == "same":
+        return [u]
+    if view == "unflat":
+        return [u % w_next.shape[1]]
+    if view == "seq_flat":
+        return list(range(u, w_next.shape[1], n_prev))
+    S = w_next.shape[1] // n_prev                      # img_flat: channel u's block of features
+    return list(range(u * S, (u + 1) * S))
 
 
 def flagged_masks(spec, params, flags):
     """Per tensor, True where a parameter belongs to, or reads, an output unit
     whose ReLU or max-pool decision the oracle found ill-conditioned in fp32.
     For a flagged unit u of a layer: the layer's weight row and bias entry u,
-    and the next layer's weights that read u (its input column, input channel,
-    or the block of flattened features of that channel). When the layer's
-    output is the input of a residual block, u also reaches the block's sum
-    through the skip: the block's last layer's row and bias u are marked, and
-    so is everything that reads the sum's unit u, recursively (back-to-back
-    blocks). After a flip those parameters drift apart for the remaining steps."""
+    and the next layer's weights that read u (its input column or channel, the
+    features of a flattened channel or token feature, or the token feature of
+    a flat unit read as a sequence). When the layer's output is the input of
+    a residual block, u also reaches the block's sum through the skip: the
+    block's last layer's rows of u are marked, and so is everything that reads
+    the sum's unit, recursively (back-to-back blocks). After a flip those
+    parameters drift apart for the remaining steps."""
     masks = [np.zeros(np.shape(p), dtype=bool) for p in params]
-    plist, skip_end = _param_layers(spec)
+    ents = _param_layers(spec)
+    by_out = {e["out_w"]: k for k, e in enumerate(ents)}
 
     def mark(k, u, seen):
         if (k, u) in seen:
             return
         seen.add((k, u))
-        wi = 2 * k
-        masks[wi][u, ...] = True
-        masks[wi + 1][u] = True
-        if k + 1 < len(plist):
-            nxt = wi + 2
-            Wn = params[nxt]
-            if np.ndim(Wn) == 4 or np.ndim(params[wi]) == 2:
-                masks[nxt][:, u, ...] = True
-            else:  # conv -> flatten -> linear: channel u owns a contiguous block of features
-                S = np.shape(Wn)[1] // np.shape(params[wi])[0]
-                masks[nxt][:, u * S:(u + 1) * S] = True
-        if k in skip_end:
-            mark(skip_end[k], u, seen)
+        e = ents[k]
+        n_prev = np.shape(params[e["out_w"]])[0]
+        masks[e["out_w"]][u, ...] = True
+        masks[e["out_b"]][u] = True
+        if k + 1 < len(ents):
+            nx = ents[k + 1]
+            for col in _units_seen(nx["view"], u, n_prev, params[nx["in_w"]]):
+                masks[nx["in_w"]][:, col, ...] = True
+        if "skip_end" in e:
+            last, sv = e["skip_end"]
+            mark(last, u % np.shape(params[ents[last]["out_w"]])[0] if sv == "unflat" else u, seen)
 
     for wi, units in flags.items():
         for u in units:
-            mark(wi // 2, u, set())
+            mark(by_out[wi], u, set())
     return masks
 
 

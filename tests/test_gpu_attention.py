@@ -1,0 +1,93 @@
+"""GPU: the attention layer family (sequences, token-wise Linear layers and
+single-head self-attention, the layers of the paper's transformer models,
+Evaluation setup, Table 2) in the fused step, against the oracle and bitwise
+against each model alone.
+
+The projections run on the grouped GEMM (rows = samples x tokens); the core
+softmax(Q K^T / sqrt(d)) V and its backward run in their own per-sample
+kernel between them."""
+import numpy as np
+import pytest
+
+from paper_2408_01331_amd import workloads as W
+from _parity import compare_run, compare_step, run_gpu, run_oracle, theta0
+
+pytestmark = pytest.mark.gpu
+
+U, A, L, RELU, FLAT, RB, RE = (lambda t: ("unflatten", t)), ("attention",), (lambda n: ("linear", n)), ("relu",), \
+    ("flatten",), ("res_begin",), ("res_end",)
+# one shared input of 192 features, read as different sequences
+SPECS_192 = [
+    {"layers": [U(8), A, FLAT, L(10)], "num_classes": 10},                                   # 8 tokens x 24
+    {"layers": [U(12), A, RELU, FLAT, L(32), RELU, L(10)], "num_classes": 10},              # 12 x 16
+    {"layers": [L(64), RELU, U(4), RB, A, RE, RELU, FLAT, L(10)], "num_classes": 10},       # after a flat Linear
+    {"layers": [U(6), L(48), RELU, RB, A, RE, RELU, RB, L(48), RELU, L(48), RE, FLAT, L(10)],
+     "num_classes": 10},                                                                     # 6 x 32 -> 48
+    {"layers": [U(8), A, RB, A, RE, RELU, FLAT, L(10)], "num_classes": 10},                 # two attention layers
+    {"layers": [L(32), RELU, L(10)], "num_classes": 10},                                    # a plain MLP beside them
+    {"layers": [RB, L(192), RE, RELU, L(10)], "num_classes": 10},                            # a skip from the input
+]
+# 64 tokens of 32 features
+SPECS_2048 = [
+    {"layers": [U(64), RB, A, RE, RELU, L(16), RELU, FLAT, L(10)], "num_classes": 10},
+    {"layers": [U(64), A, FLAT, L(10)], "num_classes": 10},
+]
+
+
+def _need_gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _bits(a):
+    return np.asarray(a, dtype=np.float32).view(np.uint32)
+
+
+def _wl(specs, batch, features, precision, steps=3, lr=0.05):
+    return W.Workload("attention", len(specs), batch, (features,), precision, specs, lr, steps, 9, init="torch")
+
+
+CASES = [("192", SPECS_192, 37, 192), ("2048", SPECS_2048, 12, 2048)]
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
+@pytest.mark.parametrize("case", [c[0] for c in CASES])
+def test_attention_models_match_the_oracle(case, precision):
+    _need_gpu()
+    _, specs, batch, feat = next(c for c in CASES if c[0] == case)
+    wl = _wl(specs, batch, feat, precision)
+    m = list(range(wl.n_models))
+    orc, spread = run_oracle(wl, 1, m, spread=True)
+    rep = compare_step(wl, run_gpu(wl, 1), orc, m, spread=spread)
+    print(f"\n[attention {case} {precision} 1 step] " + ", ".join(f"{k}={v:.3g}" for k, v in rep.items()), flush=True)
+    orc, spread = run_oracle(wl, wl.steps, m, spread=True)
+    rep = compare_run(wl, run_gpu(wl, wl.steps), orc, m, spread=spread)
+    print(f"[attention {case} {precision} {wl.steps} steps] " + ", ".join(f"{k}={v:.3g}" for k, v in rep.items()),
+          flush=True)
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
+def test_attention_model_equals_itself_alone_bitwise(precision):
+    _need_gpu()
+    wl = _wl(SPECS_192, 37, 192, precision)
+    merged = run_gpu(wl, 2)
+    for i in range(wl.n_models):
+        alone_wl = W.Workload("alone", 1, wl.batch, wl.in_shape, precision, [wl.specs[i]], wl.lr, 2, wl.seed,
+                              init=wl.init)
+        alone = run_gpu(alone_wl, 2, theta={0: theta0(wl, i)})
+        assert np.array_equal(_bits(merged[0][:, i]), _bits(alone[0][:, 0])), f"model {i}: losses"
+        for a, b in zip(merged[1][i], alone[1][0]):
+            assert np.array_equal(_bits(a), _bits(b)), f"model {i}: params"
+        for a, b in zip(merged[2][i], alone[2][0]):
+            assert np.array_equal(_bits(a), _bits(b)), f"model {i}: grads"
+
+
+def test_attention_workload_one_step():
+    """The 8-model transformer-style workload (synthetic token sequences) at
+    its own size: one step against the oracle for two of its models."""
+    _need_gpu()
+    wl = W.get("attn8")
+    orc, spread = run_oracle(wl, 1, [0, 5], spread=True)
+    rep = compare_step(wl, run_gpu(wl, 1, models=[0, 5]), orc, [0, 5], spread=spread)
+    print(f"\n[{wl.name} 1 step] " + ", ".join(f"{k}={v:.3g}" for k, v in rep.items()), flush=True)

@@ -30,6 +30,9 @@ SPECS = {
     "residual_attn": ({"layers": [U(4), L(8), RB, A, RE, RELU, RB, L(8), RELU, L(8), RE, FLAT, L(3)],
                        "num_classes": 3}, (4 * 5,)),
     "two_attn": ({"layers": [U(7), A, RB, A, RE, FLAT, L(6)], "num_classes": 6}, (7 * 4,)),
+    # residual blocks opened at the network input (flat, and read as a sequence)
+    "input_skip": ({"layers": [RB, L(6), RE, RELU, L(3)], "num_classes": 3}, (6,)),
+    "input_skip_attn": ({"layers": [U(3), RB, A, RE, FLAT, L(3)], "num_classes": 3}, (3 * 4,)),
 }
 
 

@@ -66,6 +66,32 @@ def test_residual_conv_block():
     assert m[4][:, 1].all()                                  # the 1x1 conv after the block reads channel 1
 
 
+U, A = (lambda t: ("unflatten", t)), ("attention",)
+
+
+def test_flat_unit_read_as_a_token_feature_and_its_residual_attention():
+    # W0 [8, 5] -> relu -> 2 tokens of 4 -> [attention] + skip -> relu -> flatten -> W
+    spec = {"layers": [L(8), RELU, U(2), RB, A, RE, RELU, FLAT, L(3)], "num_classes": 3}
+    params = W.init_params(spec, (5,), 0, 0)
+    assert [np.shape(p) for p in params] == [(8, 5), (8,), (12, 4), (12,), (4, 4), (4,), (3, 8), (3,)]
+    m = flagged_masks(spec, params, {0: {6}})                # flat unit 6 = token 1, feature 2
+    assert m[0][6].all() and m[0].sum() == 5 and m[1][6] and m[1].sum() == 1
+    assert m[2][:, 2].all() and m[2].sum() == 12             # the in-projection reads feature 2
+    assert m[4][2].all() and m[5][2] and m[4].sum() == 4     # the sum's feature 2: out-projection row
+    assert m[6][:, [2, 6]].all() and m[6].sum() == 6         # flattened: feature 2 of both tokens
+    assert not m[3].any() and not m[7].any()
+
+
+def test_token_feature_flagged_at_the_attention_output():
+    spec = {"layers": [U(3), A, RELU, L(8), RELU, FLAT, L(2)], "num_classes": 2}
+    params = W.init_params(spec, (3 * 8,), 0, 0)
+    m = flagged_masks(spec, params, {2: {5}})                # out-projection unit 5
+    assert m[2][5].all() and m[3][5] and m[2].sum() == 8 and not m[0].any()
+    assert m[4][:, 5].all() and m[4].sum() == 8              # the token-wise Linear reads feature 5
+    m2 = flagged_masks(spec, params, {4: {1}})                # token-wise Linear unit 1, 3 tokens
+    assert m2[4][1].all() and m2[6][:, [1, 9, 17]].all() and m2[6].sum() == 6
+
+
 def test_perturb_ulp_moves_half_the_elements_by_one_ulp():
     p = [np.linspace(-1, 1, 10001, dtype=np.float32)]
     q = perturb_ulp(p, 3)[0]
