@@ -133,7 +133,7 @@ def make_batch(wl: Workload, step: int):
 
 
 # ---------------------------------------------------------------------------
-# The five workloads.
+# The workloads.
 # ---------------------------------------------------------------------------
 def _mlp(widths, classes):
     layers = []
