@@ -400,12 +400,19 @@ struct GemmMma<float, BM, BN, BK, WGM_, WGN_> {
 // the loop every load and store is unconditional (loads past the last block
 // re-read it and the copies made of them are never read), so the compiler's
 // wait counts stay exact. One barrier per k-block.
-template <typename T, int BM, int BN, int BK, int DEPTH, class MM, int AM, int BMODE, class LA, class LB>
-__device__ __forceinline__ void gemm_loop(LA& la, LB& lb, int nkb, T* smem, typename MM::Acc& acc) {
+struct NoTail {
+  __device__ __forceinline__ void operator()() const {}
+};
+
+template <typename T, int BM, int BN, int BK, int DEPTH, class MM, int AM, int BMODE, class LA, class LB, class Tail>
+__device__ __forceinline__ void gemm_loop(LA& la, LB& lb, int nkb, T* smem, typename MM::Acc& acc, Tail&& tail) {
   using TL = Tile<T, BM, BN, BK>;
   constexpr int STAGE = TL::A_ELEMS + TL::B_ELEMS;
   static_assert(DEPTH >= 1 && DEPTH <= 4, "prefetch depth 1 to 4");
-  if (nkb <= 0) return;
+  if (nkb <= 0) {
+    tail();
+    return;
+  }
   // slot S takes block b (clamped to the last block)
   auto issue = [&](auto slot, int b) {
     constexpr int S = decltype(slot)::value;
@@ -434,6 +441,16 @@ __device__ __forceinline__ void gemm_loop(LA& la, LB& lb, int nkb, T* smem, type
     lb.template store<N1>(d + TL::A_ELEMS);
     __syncthreads();
   };
+  // the last iteration: no block left to load or stage; it starts with the
+  // caller's tail() (epilogue loads, whose latency then overlaps the last
+  // block while the slot registers are free)
+  auto last = [&](auto pos, int kb) {
+    constexpr int BUF = decltype(pos)::value & 1;
+    tail();
+    const T* st = smem + BUF * STAGE;
+    MM::template block<AM, BMODE>(st, st + TL::A_ELEMS, acc);
+    __syncthreads();
+  };
   // a group of G iterations: a multiple of DEPTH (slots) and of 2 (buffers)
   constexpr int G = DEPTH == 1 ? 2 : (DEPTH == 3 ? 6 : DEPTH);
   using I0 = std::integral_constant<int, 0>;
@@ -443,7 +460,32 @@ __device__ __forceinline__ void gemm_loop(LA& la, LB& lb, int nkb, T* smem, type
   using I4 = std::integral_constant<int, 4>;
   using I5 = std::integral_constant<int, 5>;
   int kb = 0;
-  for (; kb + G <= nkb; kb += G) {
+  if constexpr (std::is_same_v<std::decay_t<Tail>, NoTail>) {
+    // no tail action: every block in the loop, the last nkb % G after it
+    for (; kb + G <= nkb; kb += G) {
+      step(I0{}, kb);
+      step(I1{}, kb + 1);
+      if constexpr (G > 2) {
+        step(I2{}, kb + 2);
+        step(I3{}, kb + 3);
+      }
+      if constexpr (G > 4) {
+        step(I4{}, kb + 4);
+        step(I5{}, kb + 5);
+      }
+    }
+    if (kb < nkb) step(I0{}, kb);
+    if (kb + 1 < nkb) step(I1{}, kb + 1);
+    if constexpr (G > 2) {
+      if (kb + 2 < nkb) step(I2{}, kb + 2);
+      if (kb + 3 < nkb) step(I3{}, kb + 3);
+    }
+    if constexpr (G > 4) {
+      if (kb + 4 < nkb) step(I4{}, kb + 4);
+    }
+    return;
+  }
+  for (; kb + G < nkb; kb += G) {
     step(I0{}, kb);
     step(I1{}, kb + 1);
     if constexpr (G > 2) {
@@ -455,16 +497,43 @@ __device__ __forceinline__ void gemm_loop(LA& la, LB& lb, int nkb, T* smem, type
       step(I5{}, kb + 5);
     }
   }
-  // the last nkb % G blocks (no loop back-edge follows them)
-  if (kb < nkb) step(I0{}, kb);
-  if (kb + 1 < nkb) step(I1{}, kb + 1);
+  // the last 1..G blocks (no loop back-edge follows them); the final one
+  // without a load or a stage
+  if (kb + 1 == nkb) {
+    last(I0{}, kb);
+    return;
+  }
+  step(I0{}, kb);
+  if (kb + 2 == nkb) {
+    last(I1{}, kb + 1);
+    return;
+  }
   if constexpr (G > 2) {
-    if (kb + 2 < nkb) step(I2{}, kb + 2);
-    if (kb + 3 < nkb) step(I3{}, kb + 3);
+    step(I1{}, kb + 1);
+    if (kb + 3 == nkb) {
+      last(I2{}, kb + 2);
+      return;
+    }
+    step(I2{}, kb + 2);
+    if (kb + 4 == nkb) {
+      last(I3{}, kb + 3);
+      return;
+    }
   }
   if constexpr (G > 4) {
-    if (kb + 4 < nkb) step(I4{}, kb + 4);
+    step(I3{}, kb + 3);
+    if (kb + 5 == nkb) {
+      last(I4{}, kb + 4);
+      return;
+    }
+    step(I4{}, kb + 4);
+    last(I5{}, kb + 5);
   }
+}
+
+template <typename T, int BM, int BN, int BK, int DEPTH, class MM, int AM, int BMODE, class LA, class LB>
+__device__ __forceinline__ void gemm_loop(LA& la, LB& lb, int nkb, T* smem, typename MM::Acc& acc) {
+  gemm_loop<T, BM, BN, BK, DEPTH, MM, AM, BMODE>(la, lb, nkb, smem, acc, NoTail{});
 }
 
 // LDS of one MFMA kernel: the double-buffered operand tiles, reused by the
@@ -1291,6 +1360,9 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
   constexpr int NT = MM::NT, D = UN_GEMM_DEPTH;
   constexpr int PAD = sizeof(T) == 2 ? KMAJ_PAD_BF16 : KMAJ_PAD_F32;
   const int nkb = (p.K + BK - 1) / BK;
+  constexpr int CPR = BN / 4, NCH = BM * CPR / NT;  // epilogue float4 chunks per row, per thread
+  const int ns = p.nsplit;
+  f32x4 w0[NCH];  // master weights of the fused update (weight gradient only)
   if constexpr (!BWD) {
     RowLoader<T, BM, BK, NT, D> la;
     RowLoader<T, BN, BK, NT, D> lb;
@@ -1306,31 +1378,32 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
     gemm_loop<T, BM, BN, BK, D, MM, OP_ROW, OP_KMAJ>(la, lb, nkb, (T*)smem, acc);
   } else {
     // weight gradient: A = G k-major, B = X k-major (rows k = batch), with
-    // the ones column of the bias gradient at n == nsplit
+    // the ones column of the bias gradient at n == nsplit. The fused
+    // update's master-weight loads (this thread's float4 chunks of
+    // W[m][n..n+3]) are issued at the start of the k loop's last block, so
+    // their latency overlaps that block and the staging below. Master
+    // weights, their bf16 copies and the optimizer state are touched once per
+    // step: they are loaded and stored non-temporally, so they do not evict
+    // the launch's reused operands from L2.
     KRowLoader<T, BM, BK, NT, D, PAD> la;
     KRowLoader<T, BN, BK, NT, D, PAD> lb;
     const int bcol = p.nsplit - n0;
     la.init((const T*)p.A, p.lda, m0, p.K, -1);
     lb.init((const T*)p.B, p.ldb, n0, p.K, bcol >= 0 && bcol < BN ? bcol : -1);
-    gemm_loop<T, BM, BN, BK, D, MM, OP_KMAJ, OP_KMAJ>(la, lb, nkb, (T*)smem, acc);
+    gemm_loop<T, BM, BN, BK, D, MM, OP_KMAJ, OP_KMAJ>(la, lb, nkb, (T*)smem, acc, [&] {
+#pragma unroll
+      for (int q = 0; q < NCH; ++q) {
+        const int idx = threadIdx.x + NT * q, r = idx / CPR, n = n0 + (idx - r * CPR) * 4, m = m0 + r;
+        w0[q] = (m < p.M && n + 4 <= ns) ? __builtin_nontemporal_load((gptr<const f32x4>)(p.W + (int64_t)m * p.ldc + n))
+                                         : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    });
   }
 
-  // Weight gradient with the SGD update fused: the master-weight loads of
-  // this thread's float4 chunks of W[m][n..n+3] (and, with per-model rates,
-  // each tile row's rate, to LDS) are issued first, so their latency
-  // overlaps the staging below. Master weights, their bf16 copies and the
-  // optimizer state are touched once per step: they are loaded and stored
-  // non-temporally, so they do not evict the launch's reused operands from L2.
-  constexpr int CPR = BN / 4, NCH = BM * CPR / NT;
-  const int ns = p.nsplit;
-  f32x4 w0[NCH];
+  // Weight gradient with the update fused: with per-model rates, each tile
+  // row's rate goes to LDS.
   __shared__ float s_lr[BM];
   if (p.epi == EPI_WGRAD) {
-#pragma unroll
-    for (int q = 0; q < NCH; ++q) {
-      const int idx = threadIdx.x + NT * q, r = idx / CPR, n = n0 + (idx - r * CPR) * 4, m = m0 + r;
-      w0[q] = (m < p.M && n + 4 <= ns) ? __builtin_nontemporal_load((gptr<const f32x4>)(p.W + (int64_t)m * p.ldc + n)) : f32x4{0.f, 0.f, 0.f, 0.f};
-    }
     if constexpr (!OPT) {
       if (lrv && (int)threadIdx.x < BM) {
         const int m = m0 + threadIdx.x;

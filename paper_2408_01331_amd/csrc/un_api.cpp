@@ -696,20 +696,36 @@ static void build_tables(un_ctx* c, Tables& T) {
     // interleaved so that run r lands on XCD r % 8 with its members 8 launch
     // slots apart - they run together on one XCD and read their B tile from
     // its L2 once - while the order stays longest-first at the grain of 8 runs.
-    std::vector<int32_t> nat;  // (problem, tile) pairs in natural order, with run ids
+    std::vector<int32_t> nat;  // (problem, tile) pairs in run order, with run ids
     std::vector<int32_t> run_of;
     int runs = 0;
     for (size_t k = 0; k < ps.size(); ++k) {
       GemmProb& p = ps[k];
       const int tm = cdiv(p.M, GBM), tn = cdiv(p.N, GBN);
       p.tiles_n = tn;
-      const int rl = std::min(tm, 8);
-      for (int t = 0; t < tm * tn; ++t) {
-        nat.push_back((int32_t)k);
-        nat.push_back(t);
-        const int col = t / tm, row = t - col * tm;
-        if (row % rl == 0) ++runs;
-        run_of.push_back(runs - 1);
+      if (p.M >= 4 * p.N && tm >= 16) {
+        // A (M x K) is much the larger operand (the weight gradient of a
+        // concatenated first layer): a run is one m-tile's row of n-tiles (up
+        // to 16, balanced), so each A tile is read by one XCD
+        const int nr = cdiv(tn, 16), rl = cdiv(tn, nr);
+        for (int row = 0; row < tm; ++row)
+          for (int c0 = 0; c0 < tn; c0 += rl) {
+            ++runs;
+            for (int col = c0; col < std::min(tn, c0 + rl); ++col) {
+              nat.push_back((int32_t)k);
+              nat.push_back(col * tm + row);
+              run_of.push_back(runs - 1);
+            }
+          }
+      } else {
+        const int rl = std::min(tm, 8);
+        for (int t = 0; t < tm * tn; ++t) {
+          nat.push_back((int32_t)k);
+          nat.push_back(t);
+          const int col = t / tm, row = t - col * tm;
+          if (row % rl == 0) ++runs;
+          run_of.push_back(runs - 1);
+        }
       }
     }
     std::vector<std::vector<int32_t>> members(runs);
