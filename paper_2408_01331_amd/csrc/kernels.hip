@@ -2162,8 +2162,19 @@ __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* 
   const int J1 = p.J + 1;
   if (e >= (int64_t)p.O * J1) return;
   const int o = (int)(e / J1), j = (int)(e - (int64_t)o * J1);
+  // the sum in split order, eight loads in flight ahead of their adds
   float s = 0.f;
-  for (int k = 0; k < p.splits; ++k) s += ws[((int64_t)k * p.O + o) * p.ldws + j];
+  const float* col = ws + (int64_t)o * p.ldws + j;
+  const int64_t sstride = (int64_t)p.O * p.ldws;
+  int k = 0;
+  for (; k + 8 <= p.splits; k += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = col[(int64_t)(k + u) * sstride];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) s += v[u];
+  }
+  for (; k < p.splits; ++k) s += col[(int64_t)k * sstride];
   if (j < p.J) {
     const int64_t idx = (int64_t)o * p.ldgw + j;
     if (keep_grads) p.gW[idx] = s;

@@ -1446,8 +1446,15 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
         const int tiles = cdiv(b.O, BMc) * cdiv(J + 1, BNc);
         // >= 4 k-blocks per split and at most 64 workgroups: 64 is the
         // concurrent capacity of one XCD (32 CUs x 2), so the problems of a
-        // launch fill whole rounds instead of leaving a short extra one
+        // launch fill whole rounds instead of leaving a short extra one.
+        // Blocks whose channel counts are not whole 16-byte vectors take the
+        // element-wise loaders (several times slower per k-block): chunks of
+        // 8 k-blocks, up to 512 workgroups. fp32 blocks with small partials
+        // (<= 64 KiB per split): chunks of 16 k-blocks, up to 256 workgroups.
         int splits = std::max(1, std::min(nkb / 4, 64 / tiles));
+        const int vec = bf ? 8 : 4;
+        if (b.O % vec != 0 || b.C % vec != 0) splits = std::max(splits, std::min(nkb / 8, 512 / tiles));
+        else if (!bf && (int64_t)b.O * rup(J + 1, 4) * 4 <= 65536) splits = std::max(splits, std::min(nkb / 16, 256 / tiles));
         b.kchunk = cdiv(nkb, splits);
         b.splits = cdiv(nkb, b.kchunk);
         b.ldws = rup(J + 1, 4);

@@ -23,10 +23,11 @@ GOOD = [
     _spec(L(8), RELU, RB, L(8), RE, RELU, L(5)),
     _spec(L(8), RB, L(3), RELU, L(8), RE, RB, L(8), RE, L(5)),       # two blocks, no ReLUs after them
     _spec(L(8), RELU, RB, L(8), RE, RELU, RB, L(8), RE, RELU, L(5)),
+    _spec(RB, L(16), RE, RELU, L(5)),                                  # a skip from the flat 16-feature input
 ]
 
 BAD = [
-    (_spec(RB, L(8), RE, L(5)), U.UN_ERR_UNSUPPORTED),                 # starts at the network input
+    (_spec(RB, L(8), RE, L(5)), U.UN_ERR_INVALID),                     # at the 16-feature input, width changes
     (_spec(L(8), RB, L(8), RELU, RE, L(5)), U.UN_ERR_UNSUPPORTED),     # ReLU inside, right before the end
     (_spec(L(8), RB, L(7), RE, L(5)), U.UN_ERR_INVALID),               # width changes
     (_spec(L(8), RB, RE, L(5)), U.UN_ERR_INVALID),                     # empty
@@ -51,6 +52,7 @@ BAD_CNN = [
     (_spec(C(8), RB, C(8, 3, 0), RE, FLAT, L(5)), U.UN_ERR_INVALID),                    # map shrinks
     (_spec(C(8), RB, C(6), RE, FLAT, L(5)), U.UN_ERR_INVALID),                          # channels change
     (_spec(C(8), FLAT, RB, L(5), RE, L(5)), U.UN_ERR_UNSUPPORTED),                      # after a flatten
+    (_spec(RB, C(8), RE, FLAT, L(5)), U.UN_ERR_UNSUPPORTED),                            # at an image input
 ]
 
 
