@@ -1534,6 +1534,15 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
   const int lane = threadIdx.x & 63;
   const int wm = TL::wave_m(), wn = TL::wave_n();
   const int O = p.O;
+  // this lane's biases, loaded before the first store: loads and stores
+  // share one in-order counter, so a load issued after the stores would wait
+  // for all of them (once per fragment row)
+  float bias[TL::FN];
+#pragma unroll
+  for (int j = 0; j < TL::FN; ++j) {
+    const int o = n0 + wn + 16 * j + (lane & 15);
+    bias[j] = o < O ? p.bias[o] : 0.f;
+  }
 #pragma unroll
   for (int i = 0; i < TL::FM; ++i) {
     const int mb = m0 + wm + 16 * i + 4 * (lane >> 4);
@@ -1542,7 +1551,7 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
     for (int j = 0; j < TL::FN; ++j) {
       const int o = n0 + wn + 16 * j + (lane & 15);
       if (o >= O) continue;
-      const float b = p.bias[o];
+      const float b = bias[j];
       float v[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
@@ -1614,26 +1623,39 @@ __device__ __forceinline__ void conv_dgrad_epilogue(const ConvProb& p, int m0, i
   const T* X = (const T*)p.X;
   T* Gp = (T*)p.Gprev;
   const bool vec = (C % VE) == 0;
+  if (vec) {
+    // the ReLU' chunks of all of this thread's steps before its first store
+    // (loads and stores share one in-order counter)
+    constexpr int NI = (BM * CPR + TL::NT - 1) / TL::NT;
+    u32x4 xs[NI];
+#pragma unroll
+    for (int s = 0; s < NI; ++s) {
+      const int idx = threadIdx.x + TL::NT * s, r = idx / CPR, c = n0 + (idx - r * CPR) * VE, m = m0 + r;
+      xs[s] = (p.prev_relu && idx < BM * CPR && m < p.M && c < C) ? *(gptr<const u32x4>)(X + (int64_t)m * C + c) : zero4();
+    }
+#pragma unroll
+    for (int s = 0; s < NI; ++s) {
+      const int idx = threadIdx.x + TL::NT * s, r = idx / CPR, c = n0 + (idx - r * CPR) * VE, m = m0 + r;
+      if (idx >= BM * CPR || m >= p.M || c >= C) continue;
+      u32x4 v = *(const u32x4*)(sG + r * ES::SLD + (c - n0));
+      if (p.prev_relu) {
+#pragma unroll
+        for (int e = 0; e < VE; ++e)
+          if (!(vget<T>(xs[s], e) > 0.f)) vset_bits<T>(v, e, 0u);
+      }
+      *(gptr<u32x4>)(Gp + (int64_t)m * C + c) = v;
+    }
+    return;
+  }
   for (int idx = threadIdx.x; idx < BM * CPR; idx += TL::NT) {
     const int r = idx / CPR, c = n0 + (idx - r * CPR) * VE, m = m0 + r;
     if (m >= p.M || c >= C) continue;
     const int64_t g = (int64_t)m * C + c;
     const T* sv = sG + r * ES::SLD + (c - n0);
-    if (vec) {
-      u32x4 v = *(const u32x4*)sv;
-      if (p.prev_relu) {
-        const u32x4 x = *(gptr<const u32x4>)(X + g);
-#pragma unroll
-        for (int e = 0; e < VE; ++e)
-          if (!(vget<T>(x, e) > 0.f)) vset_bits<T>(v, e, 0u);
-      }
-      *(gptr<u32x4>)(Gp + g) = v;
-    } else {
-      for (int e = 0; e < VE && c + e < C; ++e) {
-        T v = sv[e];
-        if (p.prev_relu && !(TT<T>::to_f(X[g + e]) > 0.f)) v = TT<T>::from_f(0.f);
-        Gp[g + e] = v;
-      }
+    for (int e = 0; e < VE && c + e < C; ++e) {
+      T v = sv[e];
+      if (p.prev_relu && !(TT<T>::to_f(X[g + e]) > 0.f)) v = TT<T>::from_f(0.f);
+      Gp[g + e] = v;
     }
   }
 }
