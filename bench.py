@@ -407,7 +407,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="mlp64", choices=list(W.WORKLOADS))
-    ap.add_argument("--also", default="cifar16,resnet8",
+    ap.add_argument("--also", default="cifar16,resnet8,attn8",
                     help="comma-separated workloads also timed and reported under other_workloads ('' for none)")
     ap.add_argument("--latency", default="mlp2,mlp8,lenet4",
                     help="launch-latency-bound workloads timed with and without graph replay ('' for none)")

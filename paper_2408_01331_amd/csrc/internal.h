@@ -31,7 +31,10 @@ enum Epi : int32_t {
   EPI_FWD = 0,     // + bias, optional ReLU, store C (T)
   EPI_LOGITS = 1,  // + bias, store C as fp32
   EPI_DGRAD = 2,   // optional ReLU' mask from `mask` (row-major [m][n], keep where > 0), store C (T)
-  EPI_WGRAD = 3    // store C as fp32 for n < nsplit; column nsplit -> dbias[m]
+  EPI_WGRAD = 3,   // store C as fp32 for n < nsplit; column nsplit -> dbias[m]
+  EPI_WPART = 4    // split-K weight gradient: the fp32 partial sums of k-chunk `split`
+                   // (bias column included) to ws[split][m][n]; a reduction adds the
+                   // splits in order and applies the update
 };
 
 struct GemmProb {
@@ -76,6 +79,12 @@ struct GemmProb {
   float* s2;
   float* sb1;
   float* sb2;
+  // WPART: k-blocks [split * kchunk, (split + 1) * kchunk) of `splits` per
+  // tile (tile map entry: split * tiles + tile); partials at ws (a workspace
+  // buffer: the step's byte offset added), row stride ldws floats
+  int32_t splits, kchunk;
+  float* ws;
+  int64_t ldws;
 };
 
 // ---------------------------------------------------------------------------

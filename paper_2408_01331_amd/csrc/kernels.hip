@@ -1350,7 +1350,12 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
   if (prob < 0) return;  // padding of the XCD-ordered tile list
   const GemmProb& p = probs[prob];
   const int tiles_m = (p.M + BM - 1) / BM;
-  const int tn = local / tiles_m, tm = local - tn * tiles_m;   // m fastest: neighbours share B
+  int split = 0, tile = local;
+  if (p.epi == EPI_WPART) {  // split-K weight gradient: entry = split * tiles + tile
+    split = local / (tiles_m * p.tiles_n);
+    tile = local - split * (tiles_m * p.tiles_n);
+  }
+  const int tn = tile / tiles_m, tm = tile - tn * tiles_m;   // m fastest: neighbours share B
   const int m0 = tm * BM, n0 = tn * BN;
 
   using MM = GemmMma<T, BM, BN, BK>;
@@ -1359,7 +1364,10 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
 
   constexpr int NT = MM::NT, D = UN_GEMM_DEPTH;
   constexpr int PAD = sizeof(T) == 2 ? KMAJ_PAD_BF16 : KMAJ_PAD_F32;
-  const int nkb = (p.K + BK - 1) / BK;
+  // the k range of this tile: all of K, or the split's chunk (rows kb0 * BK ..)
+  const int kb0 = split * p.kchunk;
+  const int kc = p.epi == EPI_WPART ? min(p.K - kb0 * BK, p.kchunk * BK) : p.K;
+  const int nkb = (kc + BK - 1) / BK;
   constexpr int CPR = BN / 4, NCH = BM * CPR / NT;  // epilogue float4 chunks per row, per thread
   const int ns = p.nsplit;
   f32x4 w0[NCH];  // master weights of the fused update (weight gradient only)
@@ -1388,9 +1396,11 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
     KRowLoader<T, BM, BK, NT, D, PAD> la;
     KRowLoader<T, BN, BK, NT, D, PAD> lb;
     const int bcol = p.nsplit - n0;
-    la.init((const T*)p.A, p.lda, m0, p.K, -1);
-    lb.init((const T*)p.B, p.ldb, n0, p.K, bcol >= 0 && bcol < BN ? bcol : -1);
+    const int64_t k0 = (int64_t)kb0 * BK;  // k-major: rows k0 .. of both operands
+    la.init((const T*)p.A + k0 * p.lda, p.lda, m0, kc, -1);
+    lb.init((const T*)p.B + k0 * p.ldb, p.ldb, n0, kc, bcol >= 0 && bcol < BN ? bcol : -1);
     gemm_loop<T, BM, BN, BK, D, MM, OP_KMAJ, OP_KMAJ>(la, lb, nkb, (T*)smem, acc, [&] {
+      if (p.epi != EPI_WGRAD) return;
 #pragma unroll
       for (int q = 0; q < NCH; ++q) {
         const int idx = threadIdx.x + NT * q, r = idx / CPR, n = n0 + (idx - r * CPR) * 4, m = m0 + r;
@@ -1436,6 +1446,22 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
   });
   __syncthreads();
 
+  if (epi == EPI_WPART) {
+    // this split's partial sums, bias column included, as float4 rows
+    float* ws = (float*)((char*)p.ws + wsoff) + (int64_t)split * p.M * p.ldws;
+#pragma unroll
+    for (int q = 0; q < NCH; ++q) {
+      const int idx = threadIdx.x + NT * q, r = idx / CPR, cc = idx - r * CPR;
+      const int m = m0 + r, n = n0 + cc * 4;
+      if (m >= p.M || n >= p.N) continue;
+      const f32x4 g = *(const f32x4*)(sC + r * CLD + sc_col(r, cc * 4));
+      float* d = ws + (int64_t)m * p.ldws + n;
+      if (n + 4 <= p.N) *(gptr<f32x4>)d = g;
+      else
+        for (int e = 0; e < p.N - n; ++e) d[e] = g[e];
+    }
+    return;
+  }
   if (epi != EPI_WGRAD) {
     if (!BWD && epi == EPI_LOGITS && p.ce_part) {
       fused_softmax_ce<T, BM, CLD, NT>(sC, p, m0, tm, labels, per_model_labels, wsoff);

@@ -689,7 +689,10 @@ static void build_tables(un_ctx* c, Tables& T) {
   // Order affects scheduling only: every tile computes the same values.
   auto emit_gemm = [&](std::vector<GemmProb>& ps, std::vector<Launch>& out, int kclass) {
     if (ps.empty()) return;
-    std::stable_sort(ps.begin(), ps.end(), [](const GemmProb& x, const GemmProb& y) { return x.K > y.K; });
+    // k length of one tile: K, or one split's chunk
+    const int BKg = bf ? GEMM_BK_BF16 : GEMM_BK_F32;
+    auto klen = [&](const GemmProb& x) { return x.epi == EPI_WPART ? std::min(x.K, x.kchunk * BKg) : x.K; };
+    std::stable_sort(ps.begin(), ps.end(), [&](const GemmProb& x, const GemmProb& y) { return klen(x) > klen(y); });
     // Launch order = problem order (longest K first), tiles m-fastest, then
     // swizzled for the XCDs: the tiles are cut into runs of up to 8 that share
     // a B tile (one column of m-tiles), and every 8 consecutive runs are
@@ -703,28 +706,34 @@ static void build_tables(un_ctx* c, Tables& T) {
       GemmProb& p = ps[k];
       const int tm = cdiv(p.M, GBM), tn = cdiv(p.N, GBN);
       p.tiles_n = tn;
-      if (p.M >= 4 * p.N && tm >= 16) {
-        // A (M x K) is much the larger operand (the weight gradient of a
-        // concatenated first layer): a run is one m-tile's row of n-tiles (up
-        // to 16, balanced), so each A tile is read by one XCD
-        const int nr = cdiv(tn, 16), rl = cdiv(tn, nr);
-        for (int row = 0; row < tm; ++row)
-          for (int c0 = 0; c0 < tn; c0 += rl) {
-            ++runs;
-            for (int col = c0; col < std::min(tn, c0 + rl); ++col) {
-              nat.push_back((int32_t)k);
-              nat.push_back(col * tm + row);
-              run_of.push_back(runs - 1);
+      // a split-K problem's splits are tile sets of their own (entry
+      // split * tiles + tile); runs stay within one split
+      const int nsp = p.epi == EPI_WPART ? p.splits : 1;
+      for (int sp = 0; sp < nsp; ++sp) {
+        const int base = sp * tm * tn;
+        if (p.M >= 4 * p.N && tm >= 16) {
+          // A (M x K) is much the larger operand (the weight gradient of a
+          // concatenated first layer): a run is one m-tile's row of n-tiles (up
+          // to 16, balanced), so each A tile is read by one XCD
+          const int nr = cdiv(tn, 16), rl = cdiv(tn, nr);
+          for (int row = 0; row < tm; ++row)
+            for (int c0 = 0; c0 < tn; c0 += rl) {
+              ++runs;
+              for (int col = c0; col < std::min(tn, c0 + rl); ++col) {
+                nat.push_back((int32_t)k);
+                nat.push_back(base + col * tm + row);
+                run_of.push_back(runs - 1);
+              }
             }
+        } else {
+          const int rl = std::min(tm, 8);
+          for (int t = 0; t < tm * tn; ++t) {
+            nat.push_back((int32_t)k);
+            nat.push_back(base + t);
+            const int col = t / tm, row = t - col * tm;
+            if (row % rl == 0) ++runs;
+            run_of.push_back(runs - 1);
           }
-      } else {
-        const int rl = std::min(tm, 8);
-        for (int t = 0; t < tm * tn; ++t) {
-          nat.push_back((int32_t)k);
-          nat.push_back(t);
-          const int col = t / tm, row = t - col * tm;
-          if (row % rl == 0) ++runs;
-          run_of.push_back(runs - 1);
         }
       }
     }
@@ -753,7 +762,7 @@ static void build_tables(un_ctx* c, Tables& T) {
       for (size_t f : {offsetof(GemmProb, A), offsetof(GemmProb, B), offsetof(GemmProb, C), offsetof(GemmProb, bias),
                        offsetof(GemmProb, mask), offsetof(GemmProb, dbias), offsetof(GemmProb, W), offsetof(GemmProb, Wb),
                        offsetof(GemmProb, bmaster), offsetof(GemmProb, row_model), offsetof(GemmProb, ce_part),
-                       offsetof(GemmProb, R)})
+                       offsetof(GemmProb, R), offsetof(GemmProb, ws)})
         fix.push_back(b0 + f);
     }
     size_t mo = put(map.data(), map.size() * 4);
@@ -1012,7 +1021,8 @@ static void build_tables(un_ctx* c, Tables& T) {
   // writes the same weights. Conv blocks keep their own per-level launches
   // (data gradient, then split-K weight gradient, then the reduction with the
   // update).
-  auto add_wgrad = [&](const Block& b, std::vector<GemmProb>& gp, std::vector<char>& cat_done) {
+  auto add_wgrad = [&](const Block& b, std::vector<GemmProb>& gp, std::vector<char>& cat_done,
+                       std::vector<ReduceProb>& rp) {
     const int gi = c->models[b.model].group;
     const Group& g = c->groups[gi];
     const int B = g.B;
@@ -1072,6 +1082,34 @@ static void build_tables(un_ctx* c, Tables& T) {
     p.s2 = sp(b.S2, 0);
     p.sb1 = sp(b.S1b, 0);
     p.sb2 = sp(b.S2b, 0);
+    if (b.splits > 1) {
+      // partial sums per k-chunk; the reduction below applies the update
+      p.epi = EPI_WPART;
+      p.splits = b.splits;
+      p.kchunk = b.kchunk;
+      p.ws = (float*)ptr(b.ws);
+      p.ldws = b.ldws;
+      ReduceProb r{};
+      r.ws = (const float*)ptr(b.ws);
+      r.ldws = b.ldws;
+      r.splits = b.splits;
+      r.O = b.N;
+      r.J = b.K;
+      r.C = 1;
+      r.gW = (float*)ptr(b.gW);
+      r.ldgw = b.ldw;
+      r.gb = (float*)ptr(b.gb);
+      r.W = (float*)ptr(b.W32);
+      r.Wb = ptr(b.Wb);
+      r.WT = nullptr;
+      r.bmaster = (float*)ptr(b.b32);
+      r.model = b.model;
+      r.s1 = sp(b.S1, 0);
+      r.s2 = sp(b.S2, 0);
+      r.sb1 = sp(b.S1b, 0);
+      r.sb2 = sp(b.S2b, 0);
+      rp.push_back(r);
+    }
     gp.push_back(p);
   };
   for (int lv = levels - 1; lv >= 0; --lv) {
@@ -1084,7 +1122,7 @@ static void build_tables(un_ctx* c, Tables& T) {
       if (!c->active[m.blocks[0].model]) continue;
       const int B = c->groups[m.group].B;
       const int depth = (int)m.blocks.size();
-      if (lv + 1 < depth && m.blocks[lv + 1].kind == 0) add_wgrad(m.blocks[lv + 1], gp, cat_done);
+      if (lv + 1 < depth && m.blocks[lv + 1].kind == 0) add_wgrad(m.blocks[lv + 1], gp, cat_done, rp);
       if (lv >= depth) continue;
       Block& b = m.blocks[lv];
       if (b.kind == 0) {
@@ -1113,7 +1151,7 @@ static void build_tables(un_ctx* c, Tables& T) {
           }
           gp.push_back(p);
         }
-        if (lv == 0) add_wgrad(b, gp, cat_done);
+        if (lv == 0) add_wgrad(b, gp, cat_done, rp);
       } else if (b.kind == 2) {
         // attention core backward: dA (written by the out-projection's data
         // gradient) -> dQ | dK | dV, the gradient at the in-projection's output
@@ -1418,6 +1456,19 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
           }
           b.ldg = rup(b.N, 8);
           b.G = A.take((size_t)R * b.ldg * es);
+          // split-K weight gradient for a long contraction (rows = samples x
+          // tokens): chunks of at most 16 k-blocks, partials in the workspace,
+          // summed in split order by the level's reduction launch, which
+          // applies the update. Depends only on this block's shape.
+          const int BKg = bf ? GEMM_BK_BF16 : GEMM_BK_F32, KCH = bf ? 16 : 32;
+          const int nkb = cdiv(R, BKg);
+          if (nkb > KCH) {
+            b.splits = cdiv(nkb, KCH);
+            b.kchunk = cdiv(nkb, b.splits);
+            b.splits = cdiv(nkb, b.kchunk);
+            b.ldws = rup(b.K + 1, 4);
+            b.ws_size = (size_t)b.splits * b.N * b.ldws * 4;  // placed in the workspace range below
+          }
         }
       } else {
         const int J = b.KH * b.KH * b.C;
@@ -1484,7 +1535,7 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
   c->ce_partial = A.take(c->models.size() * (size_t)cdiv(c->maxB, CE_ROWS) * 4);
   for (auto& m : c->models)
     for (auto& b : m.blocks)
-      if (b.kind == 1) b.ws = A.take(b.ws_size);
+      if (b.ws_size) b.ws = A.take(b.ws_size);
   c->ws_bytes = A.top - c->ws_lo;
 
   c->active.assign(c->models.size(), 1);

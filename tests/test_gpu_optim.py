@@ -37,6 +37,10 @@ def _bits(a):
 def _case(name):
     if name == "mlp64_8":
         return W.shrink(W.get("mlp64"), n_models=8)
+    if name == "mlp8_b1100":
+        # more than 1024 rows: the weight gradients are split-K, their
+        # updates (each model's optimizer and rate) done by the reduction
+        return W.shrink(W.get("mlp8"), batch=1100)
     if name == "cifar16_4":
         return W.shrink(W.get("cifar16"), n_models=4, batch=64)
     return W.get(name)
@@ -82,7 +86,7 @@ def _run(wl, steps, models=None, masks=None, start=0, h=None):
     return np.array(losses), params, grads, states
 
 
-@pytest.mark.parametrize("name", ["mlp8", "lenet4", "mlp64_8", "cifar16_4"])
+@pytest.mark.parametrize("name", ["mlp8", "lenet4", "mlp64_8", "cifar16_4", "mlp8_b1100"])
 def test_mixed_optimizers_equal_each_model_alone_bitwise(name):
     _need_gpu()
     wl = _case(name)
@@ -116,7 +120,7 @@ def _oracle(wl, i, steps):
 
 
 @pytest.mark.parametrize("name,models", [("mlp8", None), ("lenet4", None), ("mlp64_8", [0, 1, 2, 5]),
-                                         ("cifar16_4", [1, 2])])
+                                         ("cifar16_4", [1, 2]), ("mlp8_b1100", None)])
 def test_mixed_optimizers_match_the_oracle(name, models):
     _need_gpu()
     from paper_2408_01331_amd.unifiednn import split_params

@@ -168,6 +168,37 @@ def test_residual_mlps(precision):
 
 
 @pytest.mark.parametrize("precision", ["f32", "bf16"])
+def test_split_k_weight_gradients(precision):
+    """Batches of more than 1024 rows: a Linear block's weight gradient, whose
+    contraction runs over the batch (or batch x tokens), is cut into chunks of
+    at most 16 k-blocks (32 in fp32); a reduction adds their partial sums in
+    split order and applies the update. Hidden and logits layers, a first
+    layer outside the concatenated one (no ReLU), a residual block and a
+    token-wise model (4 x 1100 rows), beside a concatenated first layer that
+    is not split. Against the oracle, and bit for bit against each model
+    trained alone."""
+    _need_gpu()
+    L, RELU, RB, RE, FLAT = (lambda n: ("linear", n)), ("relu",), ("res_begin",), ("res_end",), ("flatten",)
+    specs = [
+        {"layers": [L(96), RELU, L(200), RELU, L(13)], "num_classes": 13},
+        {"layers": [L(13)], "num_classes": 13},
+        {"layers": [L(64), RELU, RB, L(64), RE, RELU, L(13)], "num_classes": 13},
+        {"layers": [("unflatten", 4), L(24), RELU, L(16), RELU, FLAT, L(13)], "num_classes": 13},
+    ]
+    wl = _custom(specs, 1100, (64,), precision, lr=0.02)
+    m = list(range(wl.n_models))
+    _report(f"split_k_{precision} 1 step", _step_vs_oracle(wl, m))
+    _report(f"split_k_{precision} run", _run_vs_oracle(wl, m))
+    merged = run_gpu(wl, 2)
+    for i in m:
+        alone = W.Workload("alone", 1, wl.batch, wl.in_shape, precision, [wl.specs[i]], wl.lr, 2, wl.seed)
+        solo = run_gpu(alone, 2, theta={0: theta0(wl, i)})
+        assert _bitwise_equal([merged[0][:, i]], [solo[0][:, 0]]), f"model {i}: losses"
+        for a, b in zip(merged[1][i] + merged[2][i], solo[1][0] + solo[2][0]):
+            assert _bitwise_equal(a, b), f"model {i}: parameters or gradients"
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
 def test_softmax_ce_fused_and_row_pass(precision):
     """Class counts on both sides of one GEMM tile's width (bf16 128, fp32 64):
     the models whose classes fit get softmax-CE in their logits GEMM's
