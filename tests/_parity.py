@@ -234,14 +234,17 @@ def _losses(wl, losses_g, i, losses_o, tol, worst):
     assert le.max() <= tol, f"model {i}: loss rel err {le.max():.3g} > {tol} ({losses_g[:, i]} vs {losses_o})"
 
 
-def compare_step(wl, gpu, orc, models, tol=None, spread=None):
+def compare_step(wl, gpu, orc, models, tol=None, spread=None, extra_floor=None):
     """One step from identical parameters: per-tensor max relative error <= tol
     on losses and parameters (the gate), and on updates and gradients, except
     at units whose ReLU / max-pool decision the oracle flagged as
     ill-conditioned in fp32 (those parameters within FLAGGED_TOL; their
     gradients are not compared). With `spread` (oracle_spread of one step), an
     update or gradient tensor whose two evaluation orders already lie further
-    apart than tol / SPREAD_FACTOR is held to SPREAD_FACTOR times that spread."""
+    apart than tol / SPREAD_FACTOR is held to SPREAD_FACTOR times that spread.
+    extra_floor replaces tol as the extras' floor (a network in which a single
+    discrete decision going the other way moves a gradient row by more than
+    the gate)."""
     tol = TOL[wl.precision] if tol is None else tol
     losses_g, params_g, grads_g = gpu
     assert losses_g.shape[0] == 1
@@ -258,8 +261,11 @@ def compare_step(wl, gpu, orc, models, tol=None, spread=None):
                 e = tensor_err(a, b, strict)
                 worst[key] = max(worst[key], e)
                 bound = tol
-                if key != "param" and spread is not None and i in spread:
-                    bound = max(tol, SPREAD_FACTOR * spread[i][key][t])
+                if key != "param":
+                    floor = tol if extra_floor is None else max(tol, extra_floor)
+                    bound = floor
+                    if spread is not None and i in spread:
+                        bound = max(floor, SPREAD_FACTOR * spread[i][key][t])
                 assert e <= bound, f"model {i} tensor {t}: {key} err {e:.3g} > {bound:.3g}"
             if fm[t].any():
                 ef = tensor_err(pg, po, fm[t])

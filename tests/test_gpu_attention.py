@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 
 from paper_2408_01331_amd import workloads as W
-from _parity import compare_run, compare_step, run_gpu, run_oracle, theta0
+from _parity import EXTRA_FLOOR, compare_run, compare_step, run_gpu, run_oracle, theta0
 
 pytestmark = pytest.mark.gpu
 
@@ -83,11 +83,27 @@ def test_attention_model_equals_itself_alone_bitwise(precision):
             assert np.array_equal(_bits(a), _bits(b)), f"model {i}: grads"
 
 
-def test_attention_workload_one_step():
+# In this bf16 workload one discrete decision going the other way moves a
+# one-step update by a few per cent: the oracle's own one-step updates move by
+# up to 3.1 % when it starts from parameters one fp32 ulp away (model 3), and
+# a residual sum's ReLU input lies 8.7e-7 from zero (model 2, median 0.19),
+# well inside the 4e-4 change that one stored bf16 value rounding the other
+# way makes there; forcing that one decision in the oracle moves the same
+# tensors by 0.6-0.9 %. The one-step extras take the floor of the multi-step
+# ones (a trajectory in which one discrete decision went the other way).
+
+
+def test_attention_workload_all_models():
     """The 8-model transformer-style workload (synthetic token sequences) at
-    its own size: one step against the oracle for two of its models."""
+    its own size, every model: one step and three free-running steps against
+    the oracle. Its token-wise weight gradients contract over 128 x 32 rows
+    and run split-K."""
     _need_gpu()
     wl = W.get("attn8")
-    orc, spread = run_oracle(wl, 1, [0, 5], spread=True)
-    rep = compare_step(wl, run_gpu(wl, 1, models=[0, 5]), orc, [0, 5], spread=spread)
+    m = list(range(wl.n_models))
+    orc, spread = run_oracle(wl, 1, m, spread=True)
+    rep = compare_step(wl, run_gpu(wl, 1), orc, m, spread=spread, extra_floor=EXTRA_FLOOR[wl.precision])
     print(f"\n[{wl.name} 1 step] " + ", ".join(f"{k}={v:.3g}" for k, v in rep.items()), flush=True)
+    orc, spread = run_oracle(wl, 3, m, spread=True)
+    rep = compare_run(wl, run_gpu(wl, 3), orc, m, spread=spread)
+    print(f"[{wl.name} 3 steps] " + ", ".join(f"{k}={v:.3g}" for k, v in rep.items()), flush=True)
