@@ -2329,14 +2329,78 @@ __global__ void ce_finish_kernel(const CeProb* __restrict__ probs, const float* 
 // ---------------------------------------------------------------------------
 template <typename T>
 __device__ __forceinline__ void attn_stage(const AttnProb& p, int b, float* sQ, float* sK, float* sV) {
-  const int Tn = p.T, d = p.d, ld = d + 1;
+  // Q | K | V rows of 3d elements: 16-byte vectors (d is a multiple of 8)
+  constexpr int VEC = TT<T>::VEC;
+  const int Tn = p.T, d = p.d, ld = d + 1, vpr = d / VEC;
   const T* qkv = (const T*)p.QKV + (int64_t)b * Tn * p.ldq;
-  for (int e = threadIdx.x; e < Tn * d; e += blockDim.x) {
-    const int t = e / d, j = e - t * d;
-    const T* row = qkv + (int64_t)t * p.ldq;
-    sQ[t * ld + j] = TT<T>::to_f(row[j]);
-    sK[t * ld + j] = TT<T>::to_f(row[d + j]);
-    sV[t * ld + j] = TT<T>::to_f(row[2 * d + j]);
+  for (int e = threadIdx.x; e < Tn * vpr; e += blockDim.x) {
+    const int t = e / vpr, j = (e - t * vpr) * VEC;
+    const T* row = qkv + (int64_t)t * p.ldq + j;
+    const u32x4 q = *(gptr<const u32x4>)row, k = *(gptr<const u32x4>)(row + d), v = *(gptr<const u32x4>)(row + 2 * d);
+#pragma unroll
+    for (int u = 0; u < VEC; ++u) {
+      sQ[t * ld + j + u] = vget<T>(q, u);
+      sK[t * ld + j + u] = vget<T>(k, u);
+      sV[t * ld + j + u] = vget<T>(v, u);
+    }
+  }
+}
+
+// Four consecutive values of a row to global memory as one store (bf16: 8
+// bytes, fp32: 16), or element by element at a row's end.
+template <typename T>
+__device__ __forceinline__ void attn_put4(T* dst, const float* v, int n, float scale) {
+  if (n == 4) {
+    if constexpr (sizeof(T) == 2) {
+      u32x2 w;
+      w[0] = (uint32_t)f2bf(v[0] * scale) | ((uint32_t)f2bf(v[1] * scale) << 16);
+      w[1] = (uint32_t)f2bf(v[2] * scale) | ((uint32_t)f2bf(v[3] * scale) << 16);
+      *(gptr<u32x2>)dst = w;
+    } else {
+      *(gptr<f32x4>)dst = f32x4{v[0] * scale, v[1] * scale, v[2] * scale, v[3] * scale};
+    }
+  } else {
+    for (int e = 0; e < n; ++e) dst[e] = TT<T>::from_f(v[e] * scale);
+  }
+}
+
+// out[r][c] = sum over x of a(r, x) * b(c, x) for r < rows, c < cols: each
+// thread takes RB x CB blocks of outputs (columns fastest across threads), so
+// one load of a(r, x) and of b(c, x) serves CB and RB multiply-adds. Every
+// output is one fmaf chain over x in ascending order, as in the unblocked
+// form; rows and columns past the end read a clamped valid element and are
+// not stored. put(r, c0, v, n) receives the n valid values of row r from
+// column c0.
+template <int RB, int CB, class FA, class FB, class PUT>
+__device__ __forceinline__ void attn_products(int rows, int cols, int n, FA&& fa, FB&& fb, PUT&& put) {
+  const int nbc = (cols + CB - 1) / CB, nblk = ((rows + RB - 1) / RB) * nbc;
+  for (int blk = threadIdx.x; blk < nblk; blk += blockDim.x) {
+    const int r0 = (blk / nbc) * RB, c0 = (blk - (blk / nbc) * nbc) * CB;
+    int rr[RB], cc[CB];
+#pragma unroll
+    for (int i = 0; i < RB; ++i) rr[i] = min(r0 + i, rows - 1);
+#pragma unroll
+    for (int j = 0; j < CB; ++j) cc[j] = min(c0 + j, cols - 1);
+    float acc[RB][CB];
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+#pragma unroll
+      for (int j = 0; j < CB; ++j) acc[i][j] = 0.f;
+    for (int x = 0; x < n; ++x) {
+      float a[RB], b[CB];
+#pragma unroll
+      for (int i = 0; i < RB; ++i) a[i] = fa(rr[i], x);
+#pragma unroll
+      for (int j = 0; j < CB; ++j) b[j] = fb(cc[j], x);
+#pragma unroll
+      for (int i = 0; i < RB; ++i)
+#pragma unroll
+        for (int j = 0; j < CB; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    const int nc = min(CB, cols - c0);
+#pragma unroll
+    for (int i = 0; i < RB; ++i)
+      if (r0 + i < rows) put(r0 + i, c0, acc[i], nc);
   }
 }
 
@@ -2354,12 +2418,12 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const AttnProb* __restric
   float* sS = sV + Tn * ld;  // [T][T + 1]: scores, then probabilities
   attn_stage<T>(p, b, sQ, sK, sV);
   __syncthreads();
-  for (int e = threadIdx.x; e < Tn * Tn; e += blockDim.x) {
-    const int i = e / Tn, t = e - i * Tn;
-    float acc = 0.f;
-    for (int k = 0; k < d; ++k) acc = fmaf(sQ[i * ld + k], sK[t * ld + k], acc);
-    sS[i * ls + t] = acc * p.scale;
-  }
+  // S[i][t] = (Q K^T)[i][t] * scale
+  attn_products<2, 2>(Tn, Tn, d, [&](int i, int k) { return sQ[i * ld + k]; },
+                      [&](int t, int k) { return sK[t * ld + k]; },
+                      [&](int i, int t0, const float* v, int n) {
+                        for (int e = 0; e < n; ++e) sS[i * ls + t0 + e] = v[e] * p.scale;
+                      });
   __syncthreads();
   // softmax over the keys: one wave per query row, lanes over the keys (T <= 64)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
@@ -2376,13 +2440,11 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const AttnProb* __restric
     }
   }
   __syncthreads();
+  // A[i][j] = (P V)[i][j]
   T* A = (T*)p.A + (int64_t)b * Tn * p.lda;
-  for (int e = threadIdx.x; e < Tn * d; e += blockDim.x) {
-    const int i = e / d, j = e - i * d;
-    float acc = 0.f;
-    for (int t = 0; t < Tn; ++t) acc = fmaf(sS[i * ls + t], sV[t * ld + j], acc);
-    A[(int64_t)i * p.lda + j] = TT<T>::from_f(acc);
-  }
+  attn_products<4, 4>(Tn, d, Tn, [&](int i, int t) { return sS[i * ls + t]; },
+                      [&](int j, int t) { return sV[t * ld + j]; },
+                      [&](int i, int j0, const float* v, int n) { attn_put4<T>(A + (int64_t)i * p.lda + j0, v, n, 1.f); });
 }
 
 template <typename T>
@@ -2402,9 +2464,15 @@ __global__ __launch_bounds__(256) void attn_bwd_kernel(const AttnProb* __restric
   attn_stage<T>(p, b, sQ, sK, sV);
   const T* dA = (const T*)p.dA + (int64_t)b * Tn * p.lda;
   const float* Pg = p.P + (int64_t)b * Tn * Tn;
-  for (int e = threadIdx.x; e < Tn * d; e += blockDim.x) {
-    const int i = e / d, j = e - i * d;
-    sD[i * ld + j] = TT<T>::to_f(dA[(int64_t)i * p.lda + j]);
+  {
+    constexpr int VEC = TT<T>::VEC;
+    const int vpr = d / VEC;
+    for (int e = threadIdx.x; e < Tn * vpr; e += blockDim.x) {
+      const int i = e / vpr, j = (e - i * vpr) * VEC;
+      const u32x4 x = *(gptr<const u32x4>)(dA + (int64_t)i * p.lda + j);
+#pragma unroll
+      for (int u = 0; u < VEC; ++u) sD[i * ld + j + u] = vget<T>(x, u);
+    }
   }
   for (int e = threadIdx.x; e < Tn * Tn; e += blockDim.x) {
     const int i = e / Tn, t = e - i * Tn;
@@ -2412,12 +2480,11 @@ __global__ __launch_bounds__(256) void attn_bwd_kernel(const AttnProb* __restric
   }
   __syncthreads();
   // dP[i][t] = sum_j dA[i][j] V[t][j]
-  for (int e = threadIdx.x; e < Tn * Tn; e += blockDim.x) {
-    const int i = e / Tn, t = e - i * Tn;
-    float acc = 0.f;
-    for (int j = 0; j < d; ++j) acc = fmaf(sD[i * ld + j], sV[t * ld + j], acc);
-    sG[i * ls + t] = acc;
-  }
+  attn_products<2, 2>(Tn, Tn, d, [&](int i, int j) { return sD[i * ld + j]; },
+                      [&](int t, int j) { return sV[t * ld + j]; },
+                      [&](int i, int t0, const float* v, int n) {
+                        for (int e = 0; e < n; ++e) sG[i * ls + t0 + e] = v[e];
+                      });
   __syncthreads();
   // dS = P * (dP - rowsum(P * dP)), one wave per row
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
@@ -2429,17 +2496,22 @@ __global__ __launch_bounds__(256) void attn_bwd_kernel(const AttnProb* __restric
   }
   __syncthreads();
   T* dqkv = (T*)p.dQKV + (int64_t)b * Tn * p.ldq;
-  for (int e = threadIdx.x; e < Tn * d; e += blockDim.x) {
-    const int r = e / d, k = e - r * d;
-    float q = 0.f, kk = 0.f, v = 0.f;
-    for (int t = 0; t < Tn; ++t) q = fmaf(sG[r * ls + t], sK[t * ld + k], q);        // dQ[r][k]
-    for (int i = 0; i < Tn; ++i) kk = fmaf(sG[i * ls + r], sQ[i * ld + k], kk);      // dK[r][k]
-    for (int i = 0; i < Tn; ++i) v = fmaf(sP[i * ls + r], sD[i * ld + k], v);        // dV[r][k]
-    T* row = dqkv + (int64_t)r * p.ldq;
-    row[k] = TT<T>::from_f(q * p.scale);
-    row[d + k] = TT<T>::from_f(kk * p.scale);
-    row[2 * d + k] = TT<T>::from_f(v);
-  }
+  // dQ[r][k] = scale * sum_t dS[r][t] K[t][k]
+  attn_products<4, 4>(Tn, d, Tn, [&](int r, int t) { return sG[r * ls + t]; },
+                      [&](int k, int t) { return sK[t * ld + k]; },
+                      [&](int r, int k0, const float* v, int n) { attn_put4<T>(dqkv + (int64_t)r * p.ldq + k0, v, n, p.scale); });
+  // dK[r][k] = scale * sum_i dS[i][r] Q[i][k]
+  attn_products<4, 4>(Tn, d, Tn, [&](int r, int i) { return sG[i * ls + r]; },
+                      [&](int k, int i) { return sQ[i * ld + k]; },
+                      [&](int r, int k0, const float* v, int n) {
+                        attn_put4<T>(dqkv + (int64_t)r * p.ldq + d + k0, v, n, p.scale);
+                      });
+  // dV[r][k] = sum_i P[i][r] dA[i][k]
+  attn_products<4, 4>(Tn, d, Tn, [&](int r, int i) { return sP[i * ls + r]; },
+                      [&](int k, int i) { return sD[i * ld + k]; },
+                      [&](int r, int k0, const float* v, int n) {
+                        attn_put4<T>(dqkv + (int64_t)r * p.ldq + 2 * d + k0, v, n, 1.f);
+                      });
 }
 
 // ---------------------------------------------------------------------------
