@@ -182,10 +182,11 @@ struct AttnProb {
   float scale;
 };
 
-// LDS of one workgroup: Q, K, V (and dA) as fp32 rows of d + 1, and one (two)
-// T x (T + 1) fp32 score tiles.
-inline size_t attn_lds_bytes(int T, int d, bool bwd) {
-  return ((size_t)(bwd ? 4 : 3) * T * (d + 1) + (size_t)(bwd ? 2 : 1) * T * (T + 1)) * 4;
+// LDS of one workgroup: Q, K, V (and dA) in the storage type (es bytes per
+// element) as rows of d plus one 16-byte chunk, and one (two) T x (T + 1)
+// fp32 score tiles. The parser's bound takes es = 4.
+inline size_t attn_lds_bytes(int T, int d, bool bwd, int es) {
+  return (size_t)(bwd ? 4 : 3) * T * (d + 16 / es) * es + (size_t)(bwd ? 2 : 1) * T * (T + 1) * 4;
 }
 
 // ---------------------------------------------------------------------------

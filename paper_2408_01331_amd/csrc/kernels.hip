@@ -2328,21 +2328,18 @@ __global__ void ce_finish_kernel(const CeProb* __restrict__ probs, const float* 
 // the sample's own values.
 // ---------------------------------------------------------------------------
 template <typename T>
-__device__ __forceinline__ void attn_stage(const AttnProb& p, int b, float* sQ, float* sK, float* sV) {
-  // Q | K | V rows of 3d elements: 16-byte vectors (d is a multiple of 8)
+__device__ __forceinline__ void attn_stage(const AttnProb& p, int b, T* sQ, T* sK, T* sV) {
+  // Q | K | V rows of 3d elements, copied as 16-byte vectors (d is a multiple
+  // of 8) into LDS rows of d plus one 16-byte chunk, in the storage type
   constexpr int VEC = TT<T>::VEC;
-  const int Tn = p.T, d = p.d, ld = d + 1, vpr = d / VEC;
+  const int Tn = p.T, d = p.d, ld = d + VEC, vpr = d / VEC;
   const T* qkv = (const T*)p.QKV + (int64_t)b * Tn * p.ldq;
   for (int e = threadIdx.x; e < Tn * vpr; e += blockDim.x) {
     const int t = e / vpr, j = (e - t * vpr) * VEC;
     const T* row = qkv + (int64_t)t * p.ldq + j;
-    const u32x4 q = *(gptr<const u32x4>)row, k = *(gptr<const u32x4>)(row + d), v = *(gptr<const u32x4>)(row + 2 * d);
-#pragma unroll
-    for (int u = 0; u < VEC; ++u) {
-      sQ[t * ld + j + u] = vget<T>(q, u);
-      sK[t * ld + j + u] = vget<T>(k, u);
-      sV[t * ld + j + u] = vget<T>(v, u);
-    }
+    *(u32x4*)(sQ + t * ld + j) = *(gptr<const u32x4>)row;
+    *(u32x4*)(sK + t * ld + j) = *(gptr<const u32x4>)(row + d);
+    *(u32x4*)(sV + t * ld + j) = *(gptr<const u32x4>)(row + 2 * d);
   }
 }
 
@@ -2411,16 +2408,16 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const AttnProb* __restric
   const int pi = tile_map[2 * blockIdx.x], b = tile_map[2 * blockIdx.x + 1];
   if (pi < 0) return;
   const AttnProb& p = probs[pi];
-  const int Tn = p.T, d = p.d, ld = d + 1, ls = Tn + 1;
-  float* sQ = sm;
-  float* sK = sQ + Tn * ld;
-  float* sV = sK + Tn * ld;
-  float* sS = sV + Tn * ld;  // [T][T + 1]: scores, then probabilities
+  const int Tn = p.T, d = p.d, ld = d + TT<T>::VEC, ls = Tn + 1;
+  T* sQ = (T*)sm;  // Q, K, V rows in the storage type, then [T][T + 1] fp32 scores
+  T* sK = sQ + Tn * ld;
+  T* sV = sK + Tn * ld;
+  float* sS = (float*)(sV + Tn * ld);
   attn_stage<T>(p, b, sQ, sK, sV);
   __syncthreads();
   // S[i][t] = (Q K^T)[i][t] * scale
-  attn_products<2, 2>(Tn, Tn, d, [&](int i, int k) { return sQ[i * ld + k]; },
-                      [&](int t, int k) { return sK[t * ld + k]; },
+  attn_products<2, 2>(Tn, Tn, d, [&](int i, int k) { return TT<T>::to_f(sQ[i * ld + k]); },
+                      [&](int t, int k) { return TT<T>::to_f(sK[t * ld + k]); },
                       [&](int i, int t0, const float* v, int n) {
                         for (int e = 0; e < n; ++e) sS[i * ls + t0 + e] = v[e] * p.scale;
                       });
@@ -2443,7 +2440,7 @@ __global__ __launch_bounds__(256) void attn_fwd_kernel(const AttnProb* __restric
   // A[i][j] = (P V)[i][j]
   T* A = (T*)p.A + (int64_t)b * Tn * p.lda;
   attn_products<4, 4>(Tn, d, Tn, [&](int i, int t) { return sS[i * ls + t]; },
-                      [&](int j, int t) { return sV[t * ld + j]; },
+                      [&](int j, int t) { return TT<T>::to_f(sV[t * ld + j]); },
                       [&](int i, int j0, const float* v, int n) { attn_put4<T>(A + (int64_t)i * p.lda + j0, v, n, 1.f); });
 }
 
@@ -2454,24 +2451,22 @@ __global__ __launch_bounds__(256) void attn_bwd_kernel(const AttnProb* __restric
   const int pi = tile_map[2 * blockIdx.x], b = tile_map[2 * blockIdx.x + 1];
   if (pi < 0) return;
   const AttnProb& p = probs[pi];
-  const int Tn = p.T, d = p.d, ld = d + 1, ls = Tn + 1;
-  float* sQ = sm;
-  float* sK = sQ + Tn * ld;
-  float* sV = sK + Tn * ld;
-  float* sD = sV + Tn * ld;   // dA
-  float* sP = sD + Tn * ld;   // [T][T + 1] probabilities
-  float* sG = sP + Tn * ls;   // [T][T + 1] dP, then dS
+  constexpr int VEC = TT<T>::VEC;
+  const int Tn = p.T, d = p.d, ld = d + VEC, ls = Tn + 1;
+  T* sQ = (T*)sm;  // Q, K, V, dA rows in the storage type, then two fp32 tiles
+  T* sK = sQ + Tn * ld;
+  T* sV = sK + Tn * ld;
+  T* sD = sV + Tn * ld;                       // dA
+  float* sP = (float*)(sD + Tn * ld);         // [T][T + 1] probabilities
+  float* sG = sP + Tn * ls;                   // [T][T + 1] dP, then dS
   attn_stage<T>(p, b, sQ, sK, sV);
   const T* dA = (const T*)p.dA + (int64_t)b * Tn * p.lda;
   const float* Pg = p.P + (int64_t)b * Tn * Tn;
   {
-    constexpr int VEC = TT<T>::VEC;
     const int vpr = d / VEC;
     for (int e = threadIdx.x; e < Tn * vpr; e += blockDim.x) {
       const int i = e / vpr, j = (e - i * vpr) * VEC;
-      const u32x4 x = *(gptr<const u32x4>)(dA + (int64_t)i * p.lda + j);
-#pragma unroll
-      for (int u = 0; u < VEC; ++u) sD[i * ld + j + u] = vget<T>(x, u);
+      *(u32x4*)(sD + i * ld + j) = *(gptr<const u32x4>)(dA + (int64_t)i * p.lda + j);
     }
   }
   for (int e = threadIdx.x; e < Tn * Tn; e += blockDim.x) {
@@ -2480,8 +2475,8 @@ __global__ __launch_bounds__(256) void attn_bwd_kernel(const AttnProb* __restric
   }
   __syncthreads();
   // dP[i][t] = sum_j dA[i][j] V[t][j]
-  attn_products<2, 2>(Tn, Tn, d, [&](int i, int j) { return sD[i * ld + j]; },
-                      [&](int t, int j) { return sV[t * ld + j]; },
+  attn_products<2, 2>(Tn, Tn, d, [&](int i, int j) { return TT<T>::to_f(sD[i * ld + j]); },
+                      [&](int t, int j) { return TT<T>::to_f(sV[t * ld + j]); },
                       [&](int i, int t0, const float* v, int n) {
                         for (int e = 0; e < n; ++e) sG[i * ls + t0 + e] = v[e];
                       });
@@ -2498,17 +2493,17 @@ __global__ __launch_bounds__(256) void attn_bwd_kernel(const AttnProb* __restric
   T* dqkv = (T*)p.dQKV + (int64_t)b * Tn * p.ldq;
   // dQ[r][k] = scale * sum_t dS[r][t] K[t][k]
   attn_products<4, 4>(Tn, d, Tn, [&](int r, int t) { return sG[r * ls + t]; },
-                      [&](int k, int t) { return sK[t * ld + k]; },
+                      [&](int k, int t) { return TT<T>::to_f(sK[t * ld + k]); },
                       [&](int r, int k0, const float* v, int n) { attn_put4<T>(dqkv + (int64_t)r * p.ldq + k0, v, n, p.scale); });
   // dK[r][k] = scale * sum_i dS[i][r] Q[i][k]
   attn_products<4, 4>(Tn, d, Tn, [&](int r, int i) { return sG[i * ls + r]; },
-                      [&](int k, int i) { return sQ[i * ld + k]; },
+                      [&](int k, int i) { return TT<T>::to_f(sQ[i * ld + k]); },
                       [&](int r, int k0, const float* v, int n) {
                         attn_put4<T>(dqkv + (int64_t)r * p.ldq + d + k0, v, n, p.scale);
                       });
   // dV[r][k] = sum_i P[i][r] dA[i][k]
   attn_products<4, 4>(Tn, d, Tn, [&](int r, int i) { return sP[i * ls + r]; },
-                      [&](int k, int i) { return sD[i * ld + k]; },
+                      [&](int k, int i) { return TT<T>::to_f(sD[i * ld + k]); },
                       [&](int r, int k0, const float* v, int n) {
                         attn_put4<T>(dqkv + (int64_t)r * p.ldq + 2 * d + k0, v, n, 1.f);
                       });

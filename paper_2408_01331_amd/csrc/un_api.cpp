@@ -379,7 +379,7 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
         return UN_ERR_INVALID;
       }
       const int d = c;
-      const size_t lds = ((size_t)4 * seq * (d + 1) + (size_t)2 * seq * (seq + 1)) * 4;
+      const size_t lds = attn_lds_bytes(seq, d, true, 4);  // the fp32 layout, the larger one
       if (seq > 64 || lds > (size_t)160 * 1024) {
         why = where(i) + "attention supports up to 64 tokens whose working set fits 160 KiB of LDS";
         return UN_ERR_UNSUPPORTED;
@@ -851,7 +851,7 @@ static void build_tables(un_ctx* c, Tables& T) {
         map.push_back(b);
       }
     size_t lds = 0;
-    for (auto& p : ps) lds = std::max(lds, attn_lds_bytes(p.T, p.d, kind == 10));
+    for (auto& p : ps) lds = std::max(lds, attn_lds_bytes(p.T, p.d, kind == 10, bf ? 2 : 4));
     size_t po = put(ps.data(), ps.size() * sizeof(AttnProb));
     for (size_t k = 0; k < ps.size(); ++k) {
       size_t b0 = po + k * sizeof(AttnProb);
