@@ -305,8 +305,9 @@ un_status un_set_opt_state(un_ctx* ctx, int32_t i, const float* src, size_t n_el
 
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid allocation): un_step
- * with the step's workspace - the conv weight-gradient split-K partial sums
- * and the per-model loss partials, which a step writes and reads back within
+ * with the step's workspace - the split-K partial sums of conv weight
+ * gradients and of Linear weight gradients with long contractions, and the
+ * per-model loss partials, which a step writes and reads back within
  * itself - in one static device array of the library (32 MiB per device,
  * held until the process ends) instead of the context's arena. Results equal
  * un_step's bit for bit. Allocates nothing: the array is a file-scope
@@ -367,7 +368,7 @@ typedef enum {
   UN_K_CONV_WGRAD = 4,
   UN_K_CE = 5,          /* softmax cross-entropy */
   UN_K_SGD = 6,         /* weight copy refresh (SGD kernel without gradient) */
-  UN_K_OTHER = 7,       /* split-K reduction with the fused conv update */
+  UN_K_OTHER = 7,       /* split-K reduction with the fused update (conv, long-contraction Linear) */
   UN_K_ATTN = 8,        /* self-attention core, forward and backward */
   UN_K_COUNT = 9
 } un_kernel_class;

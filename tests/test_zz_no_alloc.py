@@ -1,5 +1,6 @@
-"""GPU: un_step_scratch, the step whose workspace (conv split-K partials, loss
-partials) lives in the library's static device array instead of the
+"""GPU: un_step_scratch, the step whose workspace (split-K partials of conv
+and long-contraction Linear weight gradients, loss partials) lives in the
+library's static device array instead of the
 context's arena, for callers that cannot allocate. It must equal un_step bit
 for bit, call after call, with a smaller input after a larger one (the array
 keeps the previous call's contents), and refuse a context whose workspace
@@ -47,7 +48,8 @@ def test_scratch_step_equals_un_step_large_then_small():
     big = W.shrink(W.get("cifar16"), n_models=4, batch=64)      # bf16 CNNs, several split-K partial sets
     small = W.shrink(W.get("cifar16"), n_models=3, batch=24)    # fewer models, smaller batch and workspace
     lenet = W.get("lenet4")                                     # fp32 CNNs
-    cases = [(big, _pair(big)), (small, _pair(small)), (lenet, _pair(lenet))]
+    attn = W.get("attn8")                                       # split-K Linear weight gradients, attention
+    cases = [(attn, _pair(attn)), (big, _pair(big)), (small, _pair(small)), (lenet, _pair(lenet))]
     try:
         for rnd in range(2):
             for wl, (ref, got) in cases:
