@@ -129,7 +129,10 @@ def algorithmic_work(wl):
     return flops, nbytes, n_params
 
 
-def run_gpu(wl, steps, warmup):
+def run_gpu(wl, steps, warmup, repeats=0):
+    """Time `steps` steps after `warmup`; then `repeats` more windows of the
+    same steps (their ms per step, a noise indicator beside the reported
+    window) and a pass with per-launch HIP events."""
     import torch
     from paper_2408_01331_amd import unifiednn as U
 
@@ -149,6 +152,15 @@ def run_gpu(wl, steps, warmup):
     h.sync()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    windows = []
+    for _ in range(repeats):
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(steps):
+            h.step(wl.lr, losses=False)
+        h.sync()
+        torch.cuda.synchronize()
+        windows.append((time.perf_counter() - t1) / steps * 1e3)
 
     # the same K steps again with every launch bracketed by HIP events on the
     # library's stream (per-kernel durations for the roofline)
@@ -165,6 +177,8 @@ def run_gpu(wl, steps, warmup):
     losses = h.step(wl.lr, losses=True)
     arena = U.un_arena_bytes(h.ctx)
     h.close()
+    if repeats:
+        return elapsed, kern, losses, arena, windows
     return elapsed, kern, losses, arena
 
 
@@ -329,10 +343,13 @@ def cpu_baseline(wl, budget_s=12.0, single_thread_s=6.0):
             "single_thread": one}
 
 
-def measure(wl, steps, warmup):
-    """Time `steps` fused steps of workload `wl`; per-kernel rooflines."""
+def measure(wl, steps, warmup, repeats=0):
+    """Time `steps` fused steps of workload `wl`; per-kernel rooflines. With
+    repeats, that many more windows of the same steps are timed and reported
+    beside the first (median, min, max ms per step): the run-to-run spread."""
     flops, nbytes, n_params = algorithmic_work(wl)
-    elapsed, kern, losses, arena = run_gpu(wl, steps, warmup)
+    out = run_gpu(wl, steps, warmup, repeats)
+    elapsed, kern, losses, arena = out[:4]
     ms_step = elapsed / steps * 1e3
     value = wl.n_models * wl.batch / (ms_step / 1e3)
     mfma_peak = PEAK["bf16_mfma_tflops"] if wl.precision == "bf16" else PEAK["f32_mfma_tflops"]
@@ -398,6 +415,9 @@ def measure(wl, steps, warmup):
         "train_gflop_per_step": total_flops / 1e9,
         "roofline": roof, "kernels": per_kernel, "arena_bytes": arena,
         "final_losses_mean": float(np.mean(losses)),
+        **({"repeat_windows_ms_per_step": {"n": repeats, "median": float(np.median(out[4])),
+                                           "min": float(np.min(out[4])), "max": float(np.max(out[4]))}}
+           if repeats else {}),
     }
 
 
@@ -411,6 +431,8 @@ def main():
                     help="comma-separated workloads also timed and reported under other_workloads ('' for none)")
     ap.add_argument("--latency", default="mlp2,mlp8,lenet4",
                     help="launch-latency-bound workloads timed with and without graph replay ('' for none)")
+    ap.add_argument("--repeats", type=int, default=3,
+                    help="further timing windows of the headline workload, reported as their median / min / max")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
@@ -425,7 +447,7 @@ def main():
         return
 
     wl = W.get(args.workload)
-    rec = measure(wl, args.steps, args.warmup)
+    rec = measure(wl, args.steps, args.warmup, repeats=args.repeats)
     out = {
         "metric": "model-samples/sec (N x batch / step time) at 1 GPU",
         "value": rec["value"],
@@ -442,6 +464,8 @@ def main():
     }
     out.update({k: rec[k] for k in ("config", "mfma_util_step", "train_gflop_per_step", "roofline", "kernels",
                                     "arena_bytes", "final_losses_mean")})
+    if "repeat_windows_ms_per_step" in rec:
+        out["repeat_windows_ms_per_step"] = rec["repeat_windows_ms_per_step"]
     others = {}
     for name in [w for w in args.also.split(",") if w and w != wl.name]:
         owl = W.get(name)
