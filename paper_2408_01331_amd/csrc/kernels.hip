@@ -778,9 +778,13 @@ template <> __device__ __forceinline__ void select_am<float>(u32x4& v, uint64_t 
     if (!((am >> (8 * e + d)) & 1u)) v[e] = 0u;
 }
 template <> __device__ __forceinline__ void select_am<bf16_t>(u32x4& v, uint64_t am, int d) {
-  // byte masks (0x00 / 0xff) of elements 0-3 and 4-7, widened to 16 bits by byte permutes
-  const uint32_t ml = ((uint32_t)(am >> d) & 0x01010101u) * 0xffu;
-  const uint32_t mh = ((uint32_t)(am >> (32 + d)) & 0x01010101u) * 0xffu;
+  // byte masks (0x00 / 0xff) of elements 0-3 and 4-7, widened to 16 bits by
+  // byte permutes; x * 0xff as (x << 8) - x, kept from being folded back
+  // into a multiply (quarter-rate) by an empty asm operand
+  const uint32_t bl = (uint32_t)(am >> d) & 0x01010101u, bh = (uint32_t)(am >> (32 + d)) & 0x01010101u;
+  uint32_t sl = bl << 8, sh = bh << 8;
+  asm("" : "+v"(sl), "+v"(sh));
+  const uint32_t ml = sl - bl, mh = sh - bh;
   v[0] &= __builtin_amdgcn_perm(ml, ml, 0x01010000u);
   v[1] &= __builtin_amdgcn_perm(ml, ml, 0x03030202u);
   v[2] &= __builtin_amdgcn_perm(mh, mh, 0x01010000u);
@@ -1559,7 +1563,16 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
   using TL = Tile<T, BM, BN, BK, NW>;
   const int lane = threadIdx.x & 63;
   const int wm = TL::wave_m(), wn = TL::wave_n();
-  const int O = p.O;
+  // the problem's fields as values and its tensors as global pointers: read
+  // through the problem reference, every field would be loaded again after
+  // each store (the stores might alias it), and generic pointers give flat
+  // accesses, whose stores the next scalar load waits for
+  const int O = p.O, M = p.M;
+  const bool relu = p.relu != 0, pool = p.pool != 0;
+  const gptr<const T> R = G((const T*)p.R);
+  const gptr<T> P = G((T*)p.P);
+  const gptr<uint8_t> AM = G(p.amax);
+  const gptr<const float> BIAS = G(p.bias);
   // this lane's biases, loaded before the first store: loads and stores
   // share one in-order counter, so a load issued after the stores would wait
   // for all of them (once per fragment row)
@@ -1567,12 +1580,12 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
 #pragma unroll
   for (int j = 0; j < TL::FN; ++j) {
     const int o = n0 + wn + 16 * j + (lane & 15);
-    bias[j] = o < O ? p.bias[o] : 0.f;
+    bias[j] = o < O ? BIAS[o] : 0.f;
   }
 #pragma unroll
   for (int i = 0; i < TL::FM; ++i) {
     const int mb = m0 + wm + 16 * i + 4 * (lane >> 4);
-    if (mb >= p.M) continue;
+    if (mb >= M) continue;
 #pragma unroll
     for (int j = 0; j < TL::FN; ++j) {
       const int o = n0 + wn + 16 * j + (lane & 15);
@@ -1583,10 +1596,10 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
       for (int r = 0; r < 4; ++r) {
         v[r] = acc[i][j][r] + b;
         // skip input of a residual block (never pooled): rows are pixels
-        if (p.R && mb + r < p.M) v[r] += TT<T>::to_f(((const T*)p.R)[(int64_t)(mb + r) * O + o]);
-        if (p.relu) v[r] = fmaxf(v[r], 0.f);
+        if (R && mb + r < M) v[r] += TT<T>::to_f(R[(int64_t)(mb + r) * O + o]);
+        if (relu) v[r] = fmaxf(v[r], 0.f);
       }
-      if (p.pool) {
+      if (pool) {
         // rows mb..mb+3 are one 2x2 window; the first maximum in (dy,dx) order wins
         int am = 0;
         float mx = v[0];
@@ -1596,15 +1609,15 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
             mx = v[r];
             am = r;
           }
-        const int w = mb >> 2;
-        store_t<T>(p.P, (int64_t)w * O + o, mx);
-        p.amax[(int64_t)w * O + o] = (uint8_t)(1u << am);
+        const int64_t w = mb >> 2;
+        P[w * O + o] = TT<T>::from_f(mx);
+        AM[w * O + o] = (uint8_t)(1u << am);
       } else {
-        const int nv = min(4, p.M - mb);
+        const int nv = min(4, M - mb);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           if (r >= nv) break;
-          store_t<T>(p.P, (int64_t)(mb + r) * O + o, v[r]);
+          P[(int64_t)(mb + r) * O + o] = TT<T>::from_f(v[r]);
         }
       }
     }
@@ -2068,6 +2081,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 // Each thread moves one 16-byte chunk of each operand per k-block: pixel
 // k = t / CPR of the block, rows 8*(t % CPR) .. +7. Pixels of a pooled block
 // are ordered m = 4*w + (dy*2 + dx), so k % 4 is the window position.
+// The k-loop is bound by vector-instruction issue, not by the MFMA units:
+// the loaders keep their addresses as running offsets and the operand pixel
+// coordinates as counters stepped once per k-block (uniform steps, carries by
+// compare and subtract), with no per-block division or 32-bit multiply (both
+// quarter-rate). Offsets are 32-bit: every conv tensor is under 2^31 bytes.
 template <int ROWS, int BK, int NT, int SLOTS, int PAD, bool POOL>
 struct ConvKA {
   static constexpr int VEC = 8, CPR = ROWS / VEC, LDR = ROWS + PAD;
@@ -2075,81 +2093,113 @@ struct ConvKA {
   static_assert(BK * CPR == NT, "one chunk per thread and k-block");
   static_assert(BK % 4 == 0, "k-blocks hold whole windows");
   __amdgpu_buffer_rsrc_t rs, rs_am;
-  int O, K, o, k, kpix0;
+  int off, step, sm_off;
+  bool oin;
   u32x4 r[SLOTS];
   uint64_t am[SLOTS];
   __device__ __forceinline__ void init(const ConvProb& p, int o0, int kb0) {
-    k = threadIdx.x / CPR;
-    o = o0 + (threadIdx.x % CPR) * VEC;
-    O = p.O;
-    K = p.K;
-    kpix0 = kb0 * BK + k;
+    const int k = threadIdx.x / CPR, o = o0 + (threadIdx.x % CPR) * VEC;
+    oin = o < p.O;
+    const int pix = kb0 * BK + k;
+    off = (POOL ? pix >> 2 : pix) * p.O + o;  // element offset of this chunk in G
+    step = (POOL ? BK / 4 : BK) * p.O;
+    sm_off = kmaj_bf16<LDR>(k, (threadIdx.x % CPR) * VEC);
     const int64_t rows = POOL ? (int64_t)p.Nb * p.PH * p.PW : (int64_t)p.Nb * p.OH * p.OW;
     rs = make_rsrc(p.G, rows * p.O * (int64_t)sizeof(bf16_t));
     if constexpr (POOL) rs_am = make_rsrc(p.gam, rows * p.O);
   }
+  // the next k-block (the loop issues blocks in order, one call each);
+  // pixels past the last one lie past both buffers' ranges and read zero
   template <int S>
-  __device__ __forceinline__ void load(int kb) {
-    const int pix = kpix0 + kb * BK;
-    const bool in = o < O && pix < K;
-    const int row = POOL ? pix >> 2 : pix, off = row * O + o;
-    r[S] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? off * 2 : OOB, 0, 0));
-    if constexpr (POOL) am[S] = in ? load_am_buf<bf16_t>(rs_am, off) : 0ull;
+  __device__ __forceinline__ void load(int) {
+    r[S] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, oin ? off * 2 : OOB, 0, 0));
+    if constexpr (POOL) am[S] = oin ? load_am_buf<bf16_t>(rs_am, off) : 0ull;
+    off += step;
   }
   template <int S>
   __device__ __forceinline__ void store(bf16_t* sm) const {
     u32x4 v = r[S];
-    if constexpr (POOL) select_am<bf16_t>(v, am[S], k & 3);
-    *(u32x4*)(sm + kmaj_bf16<LDR>(k, (threadIdx.x % CPR) * VEC)) = v;
+    if constexpr (POOL) select_am<bf16_t>(v, am[S], (threadIdx.x / CPR) & 3);
+    *(u32x4*)(sm + sm_off) = v;
   }
 };
 
+// Chunk s of a thread: output pixel k + s * (NT / CPR) of the block. Its
+// position is kept as (n, a, b) - a pooled block's window row and column
+// (pixel order 4 * window + (dy, dx)), else the pixel's row and column - and as
+// the element offset q that the chunk's tap and channels read for it, input
+// position (n, y + u - pad, x + v - pad), y = F*a + dy, x = F*b + dx (F = 2
+// pooled, else 1; dy = dx = 0 unpooled); every k-block moves it by BK pixels. Pixels past the last one have n >= Nb: their input rows lie past
+// the buffer's range and read zero (the gradient operand is zero there too).
 template <int ROWS, int BK, int NT, int SLOTS, int PAD, bool POOL>
 struct ConvKB {
-  static constexpr int VEC = 8, CPR = ROWS / VEC, LDR = ROWS + PAD, NV = BK * CPR / NT;
+  static constexpr int VEC = 8, CPR = ROWS / VEC, LDR = ROWS + PAD, NV = BK * CPR / NT, F = POOL ? 2 : 1;
   static constexpr int OOB = 0x7ffffff0;
   static_assert(NV >= 1 && BK * CPR == NV * NT, "whole chunks per thread and k-block");
-  static_assert(NT % CPR == 0, "a thread's chunks share one row set");
-  // chunk s of a thread: pixel k + s * (NT / CPR) of the block, the same rows
+  static_assert(NT % CPR == 0 && (NT / CPR) % 4 == 0, "a thread's chunks share one row set and window position");
   __amdgpu_buffer_rsrc_t rs;
-  const ConvProb* p;
-  int k, kpix0, c0, u, v;
+  int H, W, A, B, sa, sb, q0, q1, q2, ey, ex, sm_off;
   bool jin, bias;
+  int a[NV], b[NV], q[NV];
   u32x4 r[SLOTS][NV];
   __device__ __forceinline__ void init(const ConvProb& pr, int j0, int kb0) {
-    p = &pr;
-    k = threadIdx.x / CPR;
+    const int k = threadIdx.x / CPR;
     const int j = j0 + (threadIdx.x % CPR) * VEC, J = pr.KH * pr.KH * pr.C;
     jin = j < J;
     bias = j == J;
-    const int tap = j / pr.C;
-    c0 = j - tap * pr.C;
-    u = tap / pr.KH;
-    v = tap - u * pr.KH;
-    kpix0 = kb0 * BK + k;
-    rs = make_rsrc(pr.X, (int64_t)pr.Nb * pr.H * pr.W * pr.C * (int64_t)sizeof(bf16_t));
-  }
-  template <int S>
-  __device__ __forceinline__ void load(int kb) {
+    const int tap = j / pr.C, c0 = j - tap * pr.C, u = tap / pr.KH, v = tap - u * pr.KH;
+    H = pr.H;
+    W = pr.W;
+    A = POOL ? pr.PH : pr.OH;
+    B = POOL ? pr.PW : pr.OW;
+    const int d = POOL ? (k & 3) : 0, dy = d >> 1, dx = d & 1;
+    ey = dy + u - pr.pad;  // input row of the chunk's pixel: F * a + ey
+    ex = dx + v - pr.pad;
+    sm_off = kmaj_bf16<LDR>(k, (threadIdx.x % CPR) * VEC);
+    // the step of BK pixels (BK / 4 windows) in (n, a, b) and its offsets
+    const int st = POOL ? BK / 4 : BK, plane = A * B;
+    const int sn = st / plane, rem = st - sn * plane;
+    sa = rem / B;
+    sb = rem - sa * B;
+    q0 = (sn * H * W + F * sa * W + F * sb) * pr.C;  // every step
+    q1 = (F * W - F * B) * pr.C;                      // b wrapped: next row of windows
+    q2 = (H * W - F * A * W) * pr.C;                  // a wrapped: next image
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
-      const int pix = kpix0 + kb * BK + s * (NT / CPR);
-      const bool pin = pix < p->K;
-      int n, y, x;
-      decode_out_pixel(*p, pin ? pix : 0, n, y, x);
-      const int iy = y + u - p->pad, ix = x + v - p->pad;
-      const bool in = jin && pin && iy >= 0 && iy < p->H && ix >= 0 && ix < p->W;
+      const int pix = kb0 * BK + k + s * (NT / CPR), m = POOL ? pix >> 2 : pix;
+      const int n = m / plane, r2 = m - n * plane;
+      a[s] = r2 / B;
+      b[s] = r2 - a[s] * B;
+      q[s] = ((n * H + F * a[s] + ey) * W + F * b[s] + ex) * pr.C + c0;
+    }
+    rs = make_rsrc(pr.X, (int64_t)pr.Nb * pr.H * pr.W * pr.C * (int64_t)sizeof(bf16_t));
+  }
+  // the next k-block (the loop issues blocks in order, one call each)
+  template <int S>
+  __device__ __forceinline__ void load(int) {
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      const int iy = F * a[s] + ey, ix = F * b[s] + ex;
+      const bool in = jin && (unsigned)iy < (unsigned)H && (unsigned)ix < (unsigned)W;
       u32x4 val = __builtin_bit_cast(
-          u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? (((n * p->H + iy) * p->W + ix) * p->C + c0) * 2 : OOB, 0, 0));
-      if (bias && pin) vset_bits<bf16_t>(val, 0, bits_of<bf16_t>(TT<bf16_t>::from_f(1.0f)));
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? q[s] * 2 : OOB, 0, 0));
+      if (bias) vset_bits<bf16_t>(val, 0, bits_of<bf16_t>(TT<bf16_t>::from_f(1.0f)));
       r[S][s] = val;
+      q[s] += q0;
+      b[s] += sb;
+      const bool cb = b[s] >= B;
+      b[s] -= cb ? B : 0;
+      q[s] += cb ? q1 : 0;
+      a[s] += sa + (cb ? 1 : 0);
+      const bool ca = a[s] >= A;
+      a[s] -= ca ? A : 0;
+      q[s] += ca ? q2 : 0;
     }
   }
   template <int S>
   __device__ __forceinline__ void store(bf16_t* sm) const {
 #pragma unroll
-    for (int s = 0; s < NV; ++s)
-      *(u32x4*)(sm + kmaj_bf16<LDR>(k + s * (NT / CPR), (threadIdx.x % CPR) * VEC)) = r[S][s];
+    for (int s = 0; s < NV; ++s) *(u32x4*)(sm + sm_off + (s * (NT / CPR)) * LDR) = r[S][s];
   }
 };
 
@@ -2185,14 +2235,17 @@ void conv_wgrad_mfma_kernel(const ConvProb* __restrict__ probs, const int32_t* _
   lb.init(p, n0, kb0);
   gemm_loop<bf16_t, BM, BN, BK, D, MM, OP_KMAJ, OP_KMAJ>(la, lb, nkb, (bf16_t*)smem, acc);
 
-  // this split's partial sums to ws[split][o][j]
-  float* ws = (float*)((char*)p.ws + wsoff) + (int64_t)split * p.O * p.ldws;
+  // this split's partial sums to ws[split][o][j] (32-bit offsets within the
+  // split's block of partials)
+  const gptr<float> ws = G((float*)((char*)p.ws + wsoff) + (int64_t)split * p.O * p.ldws);
+  const int M = p.M, N = p.N, ldws = (int)p.ldws;
   MM::for_groups(acc, [&](int rl, int cl, float (&v)[4]) {
     const int mb = m0 + rl, n = n0 + cl;
-    if (n >= p.N) return;
+    if (n >= N) return;
+    const int o = mb * ldws + n;
 #pragma unroll
     for (int r = 0; r < 4; ++r)
-      if (mb + r < p.M) ws[(int64_t)(mb + r) * p.ldws + n] = v[r];
+      if (mb + r < M) ws[o + r * ldws] = v[r];
   });
 }
 

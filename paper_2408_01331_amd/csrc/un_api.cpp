@@ -329,6 +329,18 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
         why = where(i) + "kernel larger than padded input";
         return UN_ERR_INVALID;
       }
+      {
+        // the conv kernels address each activation, gradient and weight tensor
+        // with 32-bit offsets (buffer loads take byte offsets below 2^31), and
+        // an output row of elements with 24-bit multiplies
+        const int64_t es = in.precision == UN_BF16_F32MASTER ? 2 : 4, lim = (int64_t)1 << 31;
+        const int64_t biggest = std::max({(int64_t)in.batch * c * h * w, (int64_t)in.batch * b.O * b.OH * b.OW,
+                                          (int64_t)b.O * (L.kernel * L.kernel * c + 8)});
+        if (biggest * es >= lim || (int64_t)b.OW * b.O >= ((int64_t)1 << 24)) {
+          why = where(i) + "conv tensors of 2^31 bytes or more, or output rows of 2^24 elements or more, are not supported";
+          return UN_ERR_UNSUPPORTED;
+        }
+      }
       b.n_w = (size_t)b.O * c * L.kernel * L.kernel;
       b.n_b = b.O;
       b.pt_w = pt;
