@@ -755,8 +755,8 @@ __device__ __forceinline__ bool dz_index(const ConvProb& pr, int n, int p, int q
 
 // VEC argmax bytes starting at a (VEC-aligned) offset.
 template <typename T> __device__ __forceinline__ uint64_t load_am(const uint8_t* a);
-template <> __device__ __forceinline__ uint64_t load_am<float>(const uint8_t* a) { return *(const uint32_t*)a; }
-template <> __device__ __forceinline__ uint64_t load_am<bf16_t>(const uint8_t* a) { return *(const uint64_t*)a; }
+template <> __device__ __forceinline__ uint64_t load_am<float>(const uint8_t* a) { return *(gptr<const uint32_t>)a; }
+template <> __device__ __forceinline__ uint64_t load_am<bf16_t>(const uint8_t* a) { return *(gptr<const uint64_t>)a; }
 
 // VEC argmax bytes at byte offset off of a buffer resource.
 template <typename T> __device__ __forceinline__ uint64_t load_am_buf(__amdgpu_buffer_rsrc_t r, int off);
@@ -1552,17 +1552,77 @@ struct ConvEpiSmem {
   static constexpr size_t BYTES = (size_t)BM * SLD * sizeof(T);
 };
 
+// Accumulator layouts of the conv passes. for_groups(acc, f) visits every run
+// of four consecutive tile rows of one column that a lane holds:
+// f(row, col, j, v[4]) in tile coordinates, j the lane's column fragment
+// (col == col_of(j)).
+// Acc16: the 16x16 MFMA blocks of Tile (acc[i][j][r] holds
+// C[wm + 16i + 4*(lane/16) + r][wn + 16j + lane%16]).
+template <typename T, int BM, int BN, int BK, int NW>
+struct Acc16 {
+  using TL = Tile<T, BM, BN, BK, NW>;
+  static constexpr int FM = TL::FM, FN = TL::FN, NT = TL::NT;
+  using Acc = f32x4[FM][FN];
+  __device__ __forceinline__ static void zero(Acc& acc) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  __device__ __forceinline__ static int col_of(int j) { return TL::wave_n() + 16 * j + (threadIdx.x & 15); }
+  // the tile row whose A operand this lane supplies to fragment row i
+  __device__ __forceinline__ static int arow(int i) { return TL::wave_m() + 16 * i + (threadIdx.x & 15); }
+  template <class F>
+  __device__ __forceinline__ static void for_groups(const Acc& acc, F&& f) {
+    const int lane = threadIdx.x & 63, wm = TL::wave_m();
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+        f(wm + 16 * i + 4 * (lane >> 4), col_of(j), j, v);
+      }
+  }
+};
+
+// Acc32 (bf16 halo tiles): 32x32x16 MFMA blocks, each wave 32 columns wide
+// (BN / 32 waves across, the rest down): acc[i][e] holds
+// C[wm + 32i + 8(e/4) + 4(lane/32) + e%4][wn + lane%32]. A lane's runs of
+// four rows start at multiples of four, so a pooled tile's windows stay whole.
+template <int BM, int BN, int NW>
+struct Acc32 {
+  static constexpr int WGN = BN / 32, WGM = NW / WGN, WM = BM / WGM, FM = WM / 32, FN = 1, NT = 64 * NW;
+  static_assert(WGN >= 1 && WGM >= 1 && WGM * WGN == NW && FM >= 1 && FM * 32 * WGM == BM, "32x32 wave tiles");
+  using Acc = f32x16[FM];
+  __device__ __forceinline__ static int wave_m() { return ((int)(threadIdx.x >> 6) / WGN) * WM; }
+  __device__ __forceinline__ static int wave_n() { return ((int)(threadIdx.x >> 6) % WGN) * 32; }
+  __device__ __forceinline__ static void zero(Acc& acc) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][e] = 0.f;
+  }
+  __device__ __forceinline__ static int col_of(int) { return wave_n() + (threadIdx.x & 31); }
+  __device__ __forceinline__ static int arow(int i) { return wave_m() + 32 * i + (threadIdx.x & 31); }
+  template <class F>
+  __device__ __forceinline__ static void for_groups(const Acc& acc, F&& f) {
+    const int lane = threadIdx.x & 63, wm = wave_m();
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float v[4] = {acc[i][4 * q], acc[i][4 * q + 1], acc[i][4 * q + 2], acc[i][4 * q + 3]};
+        f(wm + 32 * i + 8 * q + 4 * (lane >> 5), col_of(0), 0, v);
+      }
+  }
+};
+
 // Conv forward epilogue: bias, ReLU, 2x2 max-pool in registers (pool rows
 // are window-ordered, so a lane's four accumulator rows are one window), then
 // the pooled value and its one-hot argmax, stored straight from registers
 // (staging this small output in LDS measured slower).
-template <typename T, int BM, int BN, int BK, int NW = 4>
-__device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int n0,
-                                                  const f32x4 (&acc)[Tile<T, BM, BN, BK, NW>::FM][Tile<T, BM, BN, BK, NW>::FN],
-                                                  char*) {
-  using TL = Tile<T, BM, BN, BK, NW>;
-  const int lane = threadIdx.x & 63;
-  const int wm = TL::wave_m(), wn = TL::wave_n();
+template <typename T, class L>
+__device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int n0, const typename L::Acc& acc) {
   // the problem's fields as values and its tensors as global pointers: read
   // through the problem reference, every field would be loaded again after
   // each store (the stores might alias it), and generic pointers give flat
@@ -1576,124 +1636,110 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
   // this lane's biases, loaded before the first store: loads and stores
   // share one in-order counter, so a load issued after the stores would wait
   // for all of them (once per fragment row)
-  float bias[TL::FN];
+  float bias[L::FN];
 #pragma unroll
-  for (int j = 0; j < TL::FN; ++j) {
-    const int o = n0 + wn + 16 * j + (lane & 15);
+  for (int j = 0; j < L::FN; ++j) {
+    const int o = n0 + L::col_of(j);
     bias[j] = o < O ? BIAS[o] : 0.f;
   }
+  L::for_groups(acc, [&](int rl, int cl, int j, const float (&a)[4]) {
+    const int mb = m0 + rl, o = n0 + cl;
+    if (mb >= M || o >= O) return;
+    const float b = bias[j];
+    float v[4];
 #pragma unroll
-  for (int i = 0; i < TL::FM; ++i) {
-    const int mb = m0 + wm + 16 * i + 4 * (lane >> 4);
-    if (mb >= M) continue;
+    for (int r = 0; r < 4; ++r) {
+      v[r] = a[r] + b;
+      // skip input of a residual block (never pooled): rows are pixels
+      if (R && mb + r < M) v[r] += TT<T>::to_f(R[(int64_t)(mb + r) * O + o]);
+      if (relu) v[r] = fmaxf(v[r], 0.f);
+    }
+    if (pool) {
+      // rows mb..mb+3 are one 2x2 window; the first maximum in (dy,dx) order wins
+      int am = 0;
+      float mx = v[0];
 #pragma unroll
-    for (int j = 0; j < TL::FN; ++j) {
-      const int o = n0 + wn + 16 * j + (lane & 15);
-      if (o >= O) continue;
-      const float b = bias[j];
-      float v[4];
+      for (int r = 1; r < 4; ++r)
+        if (v[r] > mx) {
+          mx = v[r];
+          am = r;
+        }
+      const int w = mb >> 2;
+      P[w * O + o] = TT<T>::from_f(mx);
+      AM[w * O + o] = (uint8_t)(1u << am);
+    } else {
+      const int nv = min(4, M - mb);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        v[r] = acc[i][j][r] + b;
-        // skip input of a residual block (never pooled): rows are pixels
-        if (R && mb + r < M) v[r] += TT<T>::to_f(R[(int64_t)(mb + r) * O + o]);
-        if (relu) v[r] = fmaxf(v[r], 0.f);
-      }
-      if (pool) {
-        // rows mb..mb+3 are one 2x2 window; the first maximum in (dy,dx) order wins
-        int am = 0;
-        float mx = v[0];
-#pragma unroll
-        for (int r = 1; r < 4; ++r)
-          if (v[r] > mx) {
-            mx = v[r];
-            am = r;
-          }
-        const int64_t w = mb >> 2;
-        P[w * O + o] = TT<T>::from_f(mx);
-        AM[w * O + o] = (uint8_t)(1u << am);
-      } else {
-        const int nv = min(4, M - mb);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          if (r >= nv) break;
-          P[(int64_t)(mb + r) * O + o] = TT<T>::from_f(v[r]);
-        }
+        if (r >= nv) break;
+        P[(mb + r) * O + o] = TT<T>::from_f(v[r]);
       }
     }
-  }
+  });
 }
 
 // Conv data-gradient epilogue: the previous block's ReLU' (its stored output
 // > 0) and the store of the gradient at that output, in 16-byte vectors.
-template <typename T, int BM, int BN, int BK, int NW = 4>
-__device__ __forceinline__ void conv_dgrad_epilogue(const ConvProb& p, int m0, int n0,
-                                                    const f32x4 (&acc)[Tile<T, BM, BN, BK, NW>::FM][Tile<T, BM, BN, BK, NW>::FN],
+template <typename T, int BM, int BN, class L>
+__device__ __forceinline__ void conv_dgrad_epilogue(const ConvProb& p, int m0, int n0, const typename L::Acc& acc,
                                                     char* smem) {
-  using TL = Tile<T, BM, BN, BK, NW>;
   using ES = ConvEpiSmem<T, BM, BN>;
-  constexpr int VE = ES::VE, CPR = BN / VE;
-  const int lane = threadIdx.x & 63;
-  const int wm = TL::wave_m(), wn = TL::wave_n();
-  const int C = p.C;
+  constexpr int VE = ES::VE, CPR = BN / VE, NT = L::NT;
+  const int C = p.C, M = p.M;
+  const bool prev_relu = p.prev_relu != 0;
+  const gptr<const T> R = G((const T*)p.R);
+  const gptr<const T> X = G((const T*)p.X);
+  const gptr<T> Gp = G((T*)p.Gprev);
   T* sG = (T*)smem;
+  L::for_groups(acc, [&](int rl, int cl, int, const float (&a)[4]) {
+    if (R) {
+      // gradient at a residual block's output joins before the rounding
+      const int c = n0 + cl;
 #pragma unroll
-  for (int i = 0; i < TL::FM; ++i) {
-    const int rl = wm + 16 * i + 4 * (lane >> 4);
-#pragma unroll
-    for (int j = 0; j < TL::FN; ++j) {
-      const int cl = wn + 16 * j + (lane & 15);
-      if (p.R) {
-        // gradient at a residual block's output joins before the rounding
-        const int c = n0 + cl;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = m0 + rl + r;
-          const float add = (m < p.M && c < C) ? TT<T>::to_f(((const T*)p.R)[(int64_t)m * C + c]) : 0.f;
-          sG[(rl + r) * ES::SLD + cl] = TT<T>::from_f(acc[i][j][r] + add);
-        }
-      } else {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sG[(rl + r) * ES::SLD + cl] = TT<T>::from_f(acc[i][j][r]);
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + rl + r;
+        const float add = (m < M && c < C) ? TT<T>::to_f(R[m * C + c]) : 0.f;
+        sG[(rl + r) * ES::SLD + cl] = TT<T>::from_f(a[r] + add);
       }
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sG[(rl + r) * ES::SLD + cl] = TT<T>::from_f(a[r]);
     }
-  }
+  });
   __syncthreads();
-  const T* X = (const T*)p.X;
-  T* Gp = (T*)p.Gprev;
   const bool vec = (C % VE) == 0;
   if (vec) {
     // the ReLU' chunks of all of this thread's steps before its first store
     // (loads and stores share one in-order counter)
-    constexpr int NI = (BM * CPR + TL::NT - 1) / TL::NT;
+    constexpr int NI = (BM * CPR + NT - 1) / NT;
     u32x4 xs[NI];
 #pragma unroll
     for (int s = 0; s < NI; ++s) {
-      const int idx = threadIdx.x + TL::NT * s, r = idx / CPR, c = n0 + (idx - r * CPR) * VE, m = m0 + r;
-      xs[s] = (p.prev_relu && idx < BM * CPR && m < p.M && c < C) ? *(gptr<const u32x4>)(X + (int64_t)m * C + c) : zero4();
+      const int idx = threadIdx.x + NT * s, r = idx / CPR, c = n0 + (idx - r * CPR) * VE, m = m0 + r;
+      xs[s] = (prev_relu && idx < BM * CPR && m < M && c < C) ? *(gptr<const u32x4>)(X + m * C + c) : zero4();
     }
 #pragma unroll
     for (int s = 0; s < NI; ++s) {
-      const int idx = threadIdx.x + TL::NT * s, r = idx / CPR, c = n0 + (idx - r * CPR) * VE, m = m0 + r;
-      if (idx >= BM * CPR || m >= p.M || c >= C) continue;
+      const int idx = threadIdx.x + NT * s, r = idx / CPR, c = n0 + (idx - r * CPR) * VE, m = m0 + r;
+      if (idx >= BM * CPR || m >= M || c >= C) continue;
       u32x4 v = *(const u32x4*)(sG + r * ES::SLD + (c - n0));
-      if (p.prev_relu) {
+      if (prev_relu) {
 #pragma unroll
         for (int e = 0; e < VE; ++e)
           if (!(vget<T>(xs[s], e) > 0.f)) vset_bits<T>(v, e, 0u);
       }
-      *(gptr<u32x4>)(Gp + (int64_t)m * C + c) = v;
+      *(gptr<u32x4>)(Gp + m * C + c) = v;
     }
     return;
   }
-  for (int idx = threadIdx.x; idx < BM * CPR; idx += TL::NT) {
+  for (int idx = threadIdx.x; idx < BM * CPR; idx += NT) {
     const int r = idx / CPR, c = n0 + (idx - r * CPR) * VE, m = m0 + r;
-    if (m >= p.M || c >= C) continue;
-    const int64_t g = (int64_t)m * C + c;
+    if (m >= M || c >= C) continue;
+    const int g = m * C + c;
     const T* sv = sG + r * ES::SLD + (c - n0);
     for (int e = 0; e < VE && c + e < C; ++e) {
       T v = sv[e];
-      if (p.prev_relu && !(TT<T>::to_f(X[g + e]) > 0.f)) v = TT<T>::from_f(0.f);
+      if (prev_relu && !(TT<T>::to_f(X[g + e]) > 0.f)) v = TT<T>::from_f(0.f);
       Gp[g + e] = v;
     }
   }
@@ -1722,7 +1768,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K);
   mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
 
-  conv_fwd_epilogue<T, BM, BN, BK>(p, m0, n0, acc, smem);
+  conv_fwd_epilogue<T, Acc16<T, BM, BN, BK, 4>>(p, m0, n0, acc);
 }
 
 template <typename T, int BM, int BN, int BK>
@@ -1748,7 +1794,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K);
   mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
 
-  conv_dgrad_epilogue<T, BM, BN, BK>(p, m0, n0, acc, smem);
+  conv_dgrad_epilogue<T, BM, BN, Acc16<T, BM, BN, BK, 4>>(p, m0, n0, acc, smem);
 }
 
 // ---------------------------------------------------------------------------
@@ -1798,98 +1844,133 @@ struct TapRowLoader {
 // batch, or - data gradient - not receiving the window's gradient are zero.
 // Forward: the conv input X. Data gradient: dZ, expanded from the pooled
 // gradient G and the window argmax.
+// Element e = (position, 16-byte chunk) of the staged block; a thread takes
+// e = tid, tid + NT, ... and steps its (chunk, column, row, image) by the
+// uniform decomposition of NT with carries (no per-element division). Source
+// offsets: the image's base kept as a running sum, rows and columns by 24-bit
+// multiplies (rows of under 2^24 elements, tensors of under 2^31 bytes).
 template <typename T, bool DGRAD, int NT = 256>
 __device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, int y0, int c0, int cbw) {
   constexpr int VEC = TT<T>::VEC, UNR = 4;
-  const int cpp = cbw / VEC, plane = p.hr * p.hc;
-  const int total = p.imgs * plane * cpp;
-  const int CH = DGRAD ? p.O : p.C;
-  const T* src = (const T*)(DGRAD ? p.G : p.X);
-  for (int e0 = threadIdx.x; e0 < total; e0 += NT * UNR) {
+  const int cpp = cbw / VEC, hc = p.hc, hr = p.hr, cs = p.cs, imgs = p.imgs, Nb = p.Nb, plane = hr * hc;
+  const int dpos = NT / cpp, dch = NT - dpos * cpp, dimg = dpos / plane, dr = dpos - dimg * plane;
+  const int dhr = dr / hc, dhc = dr - dhr * hc;
+  const int dst_step = dpos * cs + dch * VEC, dst_wrap = cs - cbw;
+  // geometry of the source: rows of ROW elements, images of IMG, channel
+  // stride CH; position (hrow, hcol) reads row ybase + hrow, column xbase + hcol
+  const bool pool = DGRAD && p.pool;
+  const int CH = DGRAD ? p.O : p.C, sh = pool ? 1 : 0;
+  const int YL = DGRAD ? (pool ? 2 * p.PH : p.OH) : p.H, XL = DGRAD ? (pool ? 2 * p.PW : p.OW) : p.W;
+  const int ROW = (DGRAD ? (pool ? p.PW : p.OW) : p.W) * CH;
+  const unsigned IMG = (unsigned)(DGRAD ? (pool ? p.PH : p.OH) : p.H) * (unsigned)ROW;
+  const int ybase = DGRAD ? y0 + p.pad - (p.KH - 1) : y0 - p.pad, xbase = DGRAD ? p.pad - (p.KH - 1) : -p.pad;
+  const gptr<const T> src = G((const T*)(DGRAD ? p.G : p.X));
+  const uint8_t* gam = p.gam;
+  // this thread's first element
+  const int pos = threadIdx.x / cpp;
+  int chi = threadIdx.x - pos * cpp, img = pos / plane;
+  const int rem = pos - img * plane;
+  int hrow = rem / hc, hcol = rem - hrow * hc, dst = pos * cs + chi * VEC;
+  unsigned nb = (unsigned)(img0 + img) * IMG;
+  while (img < imgs) {
     u32x4 v[UNR];
-    int dst[UNR];
+    int dd[UNR];
 #pragma unroll
     for (int k = 0; k < UNR; ++k) {
-      const int e = e0 + NT * k;
       v[k] = zero4();
-      dst[k] = -1;
-      if (e < total) {
-        const int pos = e / cpp, ch = (e - pos * cpp) * VEC;
-        const int img = pos / plane, rem = pos - img * plane, hrow = rem / p.hc, hcol = rem - hrow * p.hc;
-        const int n = img0 + img;
-        dst[k] = pos * p.cs + ch;
-        if (n < p.Nb) {
-          if (!DGRAD) {
-            const int y = y0 - p.pad + hrow, x = hcol - p.pad;
-            if (y >= 0 && y < p.H && x >= 0 && x < p.W)
-              v[k] = *(gptr<const u32x4>)(src + ((int64_t)(n * p.H + y) * p.W + x) * CH + c0 + ch);
-          } else {
-            int64_t idx;
-            int d;
-            if (dz_index(p, n, y0 + p.pad - (p.KH - 1) + hrow, p.pad - (p.KH - 1) + hcol, idx, d)) {
-              v[k] = *(gptr<const u32x4>)(src + idx + c0 + ch);
-              if (d >= 0) select_am<T>(v[k], load_am<T>(p.gam + idx + c0 + ch), d);
-            }
-          }
+      dd[k] = -1;
+      if (img < imgs) {
+        dd[k] = dst;
+        const int y = ybase + hrow, x = xbase + hcol;
+        if (img0 + img < Nb && (unsigned)y < (unsigned)YL && (unsigned)x < (unsigned)XL) {
+          const unsigned off = nb + __umul24((unsigned)(y >> sh), (unsigned)ROW) + __umul24((unsigned)(x >> sh), (unsigned)CH) +
+                               (unsigned)(c0 + chi * VEC);
+          v[k] = *(gptr<const u32x4>)(src + off);
+          if (pool) select_am<T>(v[k], load_am<T>(gam + off), ((y & 1) << 1) | (x & 1));
+        }
+        // the next element, NT on
+        chi += dch;
+        dst += dst_step;
+        hcol += dhc;
+        hrow += dhr;
+        img += dimg;
+        nb += (unsigned)dimg * IMG;
+        if (chi >= cpp) {
+          chi -= cpp;
+          dst += dst_wrap;
+          ++hcol;
+        }
+        if (hcol >= hc) {
+          hcol -= hc;
+          ++hrow;
+        }
+        if (hrow >= hr) {
+          hrow -= hr;
+          ++img;
+          nb += IMG;
         }
       }
     }
 #pragma unroll
     for (int k = 0; k < UNR; ++k)
-      if (dst[k] >= 0) *(u32x4*)(sH + dst[k]) = v[k];
+      if (dd[k] >= 0) *(u32x4*)(sH + dd[k]) = v[k];
   }
 }
 
 // One k-block of a halo tile: A rows read from the staged halo at the lane's
 // row base plus the chunk's tap offset, B from the weight stage. Chunks at or
 // past nq have zero weights; their A reads are clamped to a valid chunk.
-template <typename T, int BM, int BN, int BK, int NW>
-__device__ __forceinline__ void mma_halo(const T* sH, const int (&hbase)[Tile<T, BM, BN, BK, NW>::FM], const int* qa,
-                                         int q0, int nq, const T* sB,
-                                         f32x4 (&acc)[Tile<T, BM, BN, BK, NW>::FM][Tile<T, BM, BN, BK, NW>::FN]) {
-  using TL = Tile<T, BM, BN, BK, NW>;
-  constexpr int VEC = TT<T>::VEC;
+// bf16: 32x32x16 MFMA blocks (Acc32); a k-step of 16 spans two chunks, lane
+// half h = lane / 32 supplying chunk qs + h.
+template <int BM, int BN, int BK, int NW>
+__device__ __forceinline__ void mma_halo(const bf16_t* sH, const int (&hbase)[Acc32<BM, BN, NW>::FM], const int* qa,
+                                         int q0, int nq, const bf16_t* sB, typename Acc32<BM, BN, NW>::Acc& acc) {
+  using L = Acc32<BM, BN, NW>;
+  constexpr int LDK = Tile<bf16_t, BM, BN, BK, NW>::LDK;
+  const int lane = threadIdx.x & 63, h = lane >> 5;
+  const bf16_t* sb = sB + (L::wave_n() + (lane & 31)) * LDK + 8 * h;
+#pragma unroll
+  for (int kk = 0; kk < BK; kk += 16) {
+    const int qs = q0 + kk / 8;
+    if (qs < nq) {
+      const int ao = qa[min(qs + h, nq - 1)];
+      const bf16x8 b = __builtin_bit_cast(bf16x8, *(const u32x4*)(sb + kk));
+#pragma unroll
+      for (int i = 0; i < L::FM; ++i) {
+        const bf16x8 a = __builtin_bit_cast(bf16x8, *(const u32x4*)(sH + hbase[i] + ao));
+        acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[i], 0, 0, 0);
+      }
+    }
+  }
+}
+
+// fp32: 16x16x4 MFMA blocks (Acc16).
+template <int BM, int BN, int BK, int NW>
+__device__ __forceinline__ void mma_halo(const float* sH, const int (&hbase)[Acc16<float, BM, BN, BK, NW>::FM],
+                                         const int* qa, int q0, int nq, const float* sB,
+                                         typename Acc16<float, BM, BN, BK, NW>::Acc& acc) {
+  using TL = Tile<float, BM, BN, BK, NW>;
+  constexpr int VEC = TT<float>::VEC;
   const int lane = threadIdx.x & 63;
   const int wn = TL::wave_n();
   const int lr = lane & 15, lg = lane >> 4;
-  if constexpr (sizeof(T) == 2) {
 #pragma unroll
-    for (int kk = 0; kk < BK; kk += 32) {
-      const int qs = q0 + kk / VEC;
-      if (qs < nq) {
-        const int ao = qa[min(qs + lg, nq - 1)];
-        bf16x8 a[TL::FM], b[TL::FN];
+  for (int kk = 0; kk < BK; kk += 16) {
+    const int qs = q0 + kk / VEC;
+    if (qs < nq) {
+      const int ao = qa[min(qs + lg, nq - 1)];
+      f32x4 a[TL::FM], b[TL::FN];
 #pragma unroll
-        for (int i = 0; i < TL::FM; ++i) a[i] = __builtin_bit_cast(bf16x8, *(const u32x4*)(sH + hbase[i] + ao));
+      for (int i = 0; i < TL::FM; ++i) a[i] = *(const f32x4*)(sH + hbase[i] + ao);
 #pragma unroll
-        for (int j = 0; j < TL::FN; ++j)
-          b[j] = __builtin_bit_cast(bf16x8, *(const u32x4*)(sB + (wn + 16 * j + lr) * TL::LDK + kk + 8 * lg));
+      for (int j = 0; j < TL::FN; ++j) b[j] = *(const f32x4*)(sB + (wn + 16 * j + lr) * TL::LDK + kk + 4 * lg);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
 #pragma unroll
         for (int i = 0; i < TL::FM; ++i)
 #pragma unroll
           for (int j = 0; j < TL::FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-      }
-    }
-  } else {
-#pragma unroll
-    for (int kk = 0; kk < BK; kk += 16) {
-      const int qs = q0 + kk / VEC;
-      if (qs < nq) {
-        const int ao = qa[min(qs + lg, nq - 1)];
-        f32x4 a[TL::FM], b[TL::FN];
-#pragma unroll
-        for (int i = 0; i < TL::FM; ++i) a[i] = *(const f32x4*)(sH + hbase[i] + ao);
-#pragma unroll
-        for (int j = 0; j < TL::FN; ++j) b[j] = *(const f32x4*)(sB + (wn + 16 * j + lr) * TL::LDK + kk + 4 * lg);
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-#pragma unroll
-          for (int i = 0; i < TL::FM; ++i)
-#pragma unroll
-            for (int j = 0; j < TL::FN; ++j)
-              acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
-      }
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[i][q], b[j][q], acc[i][j], 0, 0, 0);
     }
   }
 }
@@ -1906,6 +1987,7 @@ struct HaloSmem {
 template <typename T, int BM, int BN, int BK, bool DGRAD, int NW>
 __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* smem) {
   using TL = Tile<T, BM, BN, BK, NW>;
+  using L = std::conditional_t<sizeof(T) == 2, Acc32<BM, BN, NW>, Acc16<T, BM, BN, BK, NW>>;
   constexpr int NT = TL::NT;
   using HS = HaloSmem<T, BN, BK>;
   constexpr int VEC = TT<T>::VEC, CPB = BK / VEC;
@@ -1926,13 +2008,11 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
     img0 = tm / tpi;
     y0 = (tm - img0 * tpi) * p.tr;
   }
-  const int lane = threadIdx.x & 63;
-  const int wm = TL::wave_m();
   // halo offset of the first tap of each of this lane's MFMA rows
-  int hbase[TL::FM];
+  int hbase[L::FM];
 #pragma unroll
-  for (int i = 0; i < TL::FM; ++i) {
-    const int r = wm + 16 * i + (lane & 15);
+  for (int i = 0; i < L::FM; ++i) {
+    const int r = L::arow(i);
     int img, y, x;
     if (!DGRAD && p.pool) {  // window order: r = 4 * window + (dy, dx)
       const int lw = r >> 2, d = r & 3, wpr = SW >> 1, wpi = (p.tr >> 1) * wpr;
@@ -1950,11 +2030,8 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
     hbase[i] = ((img * p.hr + y) * p.hc + x) * p.cs;
   }
 
-  f32x4 acc[TL::FM][TL::FN];
-#pragma unroll
-  for (int i = 0; i < TL::FM; ++i)
-#pragma unroll
-    for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  typename L::Acc acc;
+  L::zero(acc);
 
   TapRowLoader<T, BN, BK, NT> lb;
   lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0);
@@ -1986,13 +2063,13 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
         const int q = (kb + 1) * CPB + cq;
         lb.load(q < nq ? qb[q] : -1);
       }
-      mma_halo<T, BM, BN, BK, NW>(sH, hbase, qa, kb * CPB, nq, sB + cur * TL::B_ELEMS, acc);
+      mma_halo<BM, BN, BK, NW>(sH, hbase, qa, kb * CPB, nq, sB + cur * TL::B_ELEMS, acc);
       if (more) lb.store(sB + (cur ^ 1) * TL::B_ELEMS);
       __syncthreads();
     }
   }
-  if constexpr (DGRAD) conv_dgrad_epilogue<T, BM, BN, BK, NW>(p, m0, n0, acc, smem);
-  else conv_fwd_epilogue<T, BM, BN, BK, NW>(p, m0, n0, acc, smem);
+  if constexpr (DGRAD) conv_dgrad_epilogue<T, BM, BN, L>(p, m0, n0, acc, smem);
+  else conv_fwd_epilogue<T, L>(p, m0, n0, acc);
 }
 
 // Halo-tiled conv pass; each problem's tile shape (p.bm x p.bn) is the wide

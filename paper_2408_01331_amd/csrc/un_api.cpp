@@ -336,7 +336,7 @@ un_status parse_model(const un_model_spec& s, const un_input_spec& in, int mi, M
         const int64_t es = in.precision == UN_BF16_F32MASTER ? 2 : 4, lim = (int64_t)1 << 31;
         const int64_t biggest = std::max({(int64_t)in.batch * c * h * w, (int64_t)in.batch * b.O * b.OH * b.OW,
                                           (int64_t)b.O * (L.kernel * L.kernel * c + 8)});
-        if (biggest * es >= lim || (int64_t)b.OW * b.O >= ((int64_t)1 << 24)) {
+        if (biggest * es >= lim || (int64_t)b.OW * b.O >= ((int64_t)1 << 24) || (int64_t)w * c >= ((int64_t)1 << 24)) {
           why = where(i) + "conv tensors of 2^31 bytes or more, or output rows of 2^24 elements or more, are not supported";
           return UN_ERR_UNSUPPORTED;
         }
