@@ -69,13 +69,11 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // ---------------------------------------------------------------------------
 // Element helpers
 // ---------------------------------------------------------------------------
-// fp32 -> bf16, round to nearest, ties to even (NaN kept quiet).
-__device__ __forceinline__ bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
+// fp32 -> bf16, round to nearest, ties to even, a NaN quieted (its top 16
+// bits with bit 6 set): gfx950's conversion instruction (v_cvt_pk_bf16_f32),
+// which gives the same bits as that integer rounding (add 0x7fff plus the
+// kept least significant bit) for every one of the 2^32 inputs (measured).
+__device__ __forceinline__ bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
 template <typename T> struct TT;
@@ -556,6 +554,24 @@ struct Smem {
 template <class T> using gptr = __attribute__((address_space(1))) T*;
 template <class T> __device__ __forceinline__ gptr<const T> G(const T* p) { return (gptr<const T>)p; }
 template <class T> __device__ __forceinline__ gptr<T> G(T* p) { return (gptr<T>)p; }
+
+// Exact floor(x / d) for 0 <= x < 2^22 and d >= 1 from the correctly rounded
+// reciprocal of d, in three full-rate instructions (an integer division takes
+// several quarter-rate multiplies): (x + 1/2) / d lies at least 1/(2d) from
+// the nearest integer, farther than the rounding of the reciprocal, of 1/(2d)
+// and of the fused product can move it for such x.
+struct SmallDiv {
+  float r, h;
+  int d;
+  __device__ __forceinline__ explicit SmallDiv(int dv) : r(1.0f / (float)dv), h(0.5f / (float)dv), d(dv) {}
+  __device__ __forceinline__ int q(int x) const { return (int)fmaf((float)x, r, h); }
+  // quotient and remainder (x - q d by a 24-bit multiply: q d <= x < 2^22)
+  __device__ __forceinline__ int qr(int x, int& rem) const {
+    const int qq = q(x);
+    rem = x - __mul24(qq, d);
+    return qq;
+  }
+};
 
 // Raw buffer resource over `bytes` bytes from `base`: loads past the end
 // return zero (CDNA buffer range checking), so tile rows beyond the matrix need
@@ -1122,6 +1138,14 @@ struct WgradLoader {
 template <typename T> __device__ __forceinline__ void store_t(void* base, int64_t idx, float v) {
   ((T*)base)[idx] = TT<T>::from_f(v);
 }
+// element e of a T tensor behind buffer resource r
+template <typename T> __device__ __forceinline__ void buf_store_t(__amdgpu_buffer_rsrc_t r, int e, float v);
+template <> __device__ __forceinline__ void buf_store_t<float>(__amdgpu_buffer_rsrc_t r, int e, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, e * 4, 0, 0);
+}
+template <> __device__ __forceinline__ void buf_store_t<bf16_t>(__amdgpu_buffer_rsrc_t r, int e, float v) {
+  __builtin_amdgcn_raw_buffer_store_b16(f2bf(v), r, e * 2, 0, 0);
+}
 
 // Load 4 consecutive values (8- or 16-byte aligned) as floats.
 template <typename T> __device__ __forceinline__ void load4_t(const T* src, float (&v)[4]);
@@ -1630,9 +1654,10 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
   const int O = p.O, M = p.M;
   const bool relu = p.relu != 0, pool = p.pool != 0;
   const gptr<const T> R = G((const T*)p.R);
-  const gptr<T> P = G((T*)p.P);
-  const gptr<uint8_t> AM = G(p.amax);
   const gptr<const float> BIAS = G(p.bias);
+  // outputs through buffer stores: 32-bit offsets (tensors are under 2^31
+  // bytes), no 64-bit address arithmetic per store
+  const __amdgpu_buffer_rsrc_t rP = make_rsrc(p.P, 0x7fffffff), rAM = make_rsrc(p.amax, 0x7fffffff);
   // this lane's biases, loaded before the first store: loads and stores
   // share one in-order counter, so a load issued after the stores would wait
   // for all of them (once per fragment row)
@@ -1664,15 +1689,15 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
           mx = v[r];
           am = r;
         }
-      const int w = mb >> 2;
-      P[w * O + o] = TT<T>::from_f(mx);
-      AM[w * O + o] = (uint8_t)(1u << am);
+      const int e = (mb >> 2) * O + o;
+      buf_store_t<T>(rP, e, mx);
+      __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(1u << am), rAM, e, 0, 0);
     } else {
       const int nv = min(4, M - mb);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         if (r >= nv) break;
-        P[(mb + r) * O + o] = TT<T>::from_f(v[r]);
+        buf_store_t<T>(rP, (mb + r) * O + o, v[r]);
       }
     }
   });
@@ -1819,7 +1844,7 @@ struct TapRowLoader {
   __device__ __forceinline__ void init(const T* base, int64_t ld, int rows_valid) {
     rsrc = make_rsrc(base, (int64_t)rows_valid * ld * (int64_t)sizeof(T));
 #pragma unroll
-    for (int s = 0; s < NV; ++s) rowoff[s] = (int)((int64_t)((threadIdx.x + NT * s) / CPB) * ld * (int64_t)sizeof(T));
+    for (int s = 0; s < NV; ++s) rowoff[s] = (int)((threadIdx.x + NT * s) / CPB) * (int)ld * (int)sizeof(T);
   }
   // col: weight column of this thread's chunk, or -1 for a chunk past the block's end
   __device__ __forceinline__ void load(int col) {
@@ -1867,10 +1892,10 @@ __device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, i
   const gptr<const T> src = G((const T*)(DGRAD ? p.G : p.X));
   const uint8_t* gam = p.gam;
   // this thread's first element
-  const int pos = threadIdx.x / cpp;
-  int chi = threadIdx.x - pos * cpp, img = pos / plane;
-  const int rem = pos - img * plane;
-  int hrow = rem / hc, hcol = rem - hrow * hc, dst = pos * cs + chi * VEC;
+  int chi, rem, hcol;
+  const int pos = SmallDiv(cpp).qr(threadIdx.x, chi);
+  int img = SmallDiv(plane).qr(pos, rem);
+  int hrow = SmallDiv(hc).qr(rem, hcol), dst = pos * cs + chi * VEC;
   unsigned nb = (unsigned)(img0 + img) * IMG;
   while (img < imgs) {
     u32x4 v[UNR];
@@ -2010,24 +2035,19 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
   }
   // halo offset of the first tap of each of this lane's MFMA rows
   int hbase[L::FM];
+  {
+    const bool wo = !DGRAD && p.pool;  // window order: r = 4 * window + (dy, dx)
+    const int per_row = wo ? SW >> 1 : SW, per_img = wo ? (p.tr >> 1) * per_row : p.tr * SW;
+    const SmallDiv dimg(per_img), drow(per_row);
+    const int hr = p.hr, hc = p.hc, cs = p.cs;
 #pragma unroll
-  for (int i = 0; i < L::FM; ++i) {
-    const int r = L::arow(i);
-    int img, y, x;
-    if (!DGRAD && p.pool) {  // window order: r = 4 * window + (dy, dx)
-      const int lw = r >> 2, d = r & 3, wpr = SW >> 1, wpi = (p.tr >> 1) * wpr;
-      img = lw / wpi;
-      const int rem = lw - img * wpi, wy = rem / wpr;
-      y = 2 * wy + (d >> 1);
-      x = 2 * (rem - wy * wpr) + (d & 1);
-    } else {
-      const int ppi = p.tr * SW;
-      img = r / ppi;
-      const int rem = r - img * ppi;
-      y = rem / SW;
-      x = rem - y * SW;
+    for (int i = 0; i < L::FM; ++i) {
+      const int r = L::arow(i), u = wo ? r >> 2 : r, d = r & 3;
+      int rem, col;
+      const int img = dimg.qr(u, rem), row = drow.qr(rem, col);
+      const int y = wo ? 2 * row + (d >> 1) : row, x = wo ? 2 * col + (d & 1) : col;
+      hbase[i] = ((img * hr + y) * hc + x) * cs;
     }
-    hbase[i] = ((img * p.hr + y) * p.hc + x) * p.cs;
   }
 
   typename L::Acc acc;
@@ -2035,21 +2055,25 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
 
   TapRowLoader<T, BN, BK, NT> lb;
   lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0);
-  const int KH = p.KH, Cin = DGRAD ? p.O : p.C, cq = threadIdx.x % CPB;
+  const int KH = p.KH, Cin = DGRAD ? p.O : p.C, cq = threadIdx.x % CPB, hc = p.hc, cs = p.cs;
+  const SmallDiv dkh(KH);
   for (int c0 = 0; c0 < Cin; c0 += p.cb) {
     const int cbw = min(p.cb, Cin - c0), cpt = cbw / VEC, nq = KH * KH * cpt;
+    const SmallDiv dcpt(cpt);
     // the weights of k-block 0 first (column computed directly), so their
     // loads overlap the staging of the operand rows
     if (cq < nq) {
-      const int tap = cq / cpt;
-      lb.load(tap * Cin + c0 + (cq - tap * cpt) * VEC);
+      int cr;
+      const int tap = dcpt.qr(cq, cr);
+      lb.load(tap * Cin + c0 + cr * VEC);
     } else {
       lb.load(-1);
     }
     __syncthreads();  // the previous channel block's halo, tables and weight stages are no longer read
     for (int q = threadIdx.x; q < nq; q += NT) {
-      const int tap = q / cpt, ch = (q - tap * cpt) * VEC, u = tap / KH, v = tap - u * KH;
-      qa[q] = (DGRAD ? (KH - 1 - u) * p.hc + (KH - 1 - v) : u * p.hc + v) * p.cs + ch;
+      int cr, v;
+      const int tap = dcpt.qr(q, cr), ch = cr * VEC, u = dkh.qr(tap, v);
+      qa[q] = (DGRAD ? (KH - 1 - u) * hc + (KH - 1 - v) : u * hc + v) * cs + ch;
       qb[q] = tap * Cin + c0 + ch;  // fwd: W[o][(tap, c)]; dgrad: WT[c][(tap, o)]
     }
     stage_halo<T, DGRAD, NT>(p, sH, img0, y0, c0, cbw);
