@@ -1644,15 +1644,14 @@ struct Acc32 {
 // Conv forward epilogue: bias, ReLU, 2x2 max-pool in registers (pool rows
 // are window-ordered, so a lane's four accumulator rows are one window), then
 // the pooled value and its one-hot argmax, stored straight from registers
-// (staging this small output in LDS measured slower).
-template <typename T, class L>
-__device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int n0, const typename L::Acc& acc) {
-  // the problem's fields as values and its tensors as global pointers: read
-  // through the problem reference, every field would be loaded again after
-  // each store (the stores might alias it), and generic pointers give flat
-  // accesses, whose stores the next scalar load waits for
+// (staging this small output in LDS measured slower). One straight-line
+// variant per (ReLU, pool, skip input) pattern, chosen by a uniform branch.
+template <typename T, class L, bool RELU, bool POOL, bool RES>
+__device__ __forceinline__ void conv_fwd_epi(const ConvProb& p, int m0, int n0, const typename L::Acc& acc) {
+  // the problem's fields as values: read through the problem reference,
+  // every field would be loaded again after each store (the stores might
+  // alias it)
   const int O = p.O, M = p.M;
-  const bool relu = p.relu != 0, pool = p.pool != 0;
   const gptr<const T> R = G((const T*)p.R);
   const gptr<const float> BIAS = G(p.bias);
   // outputs through buffer stores: 32-bit offsets (tensors are under 2^31
@@ -1676,31 +1675,47 @@ __device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int
     for (int r = 0; r < 4; ++r) {
       v[r] = a[r] + b;
       // skip input of a residual block (never pooled): rows are pixels
-      if (R && mb + r < M) v[r] += TT<T>::to_f(R[(int64_t)(mb + r) * O + o]);
-      if (relu) v[r] = fmaxf(v[r], 0.f);
+      if constexpr (RES) v[r] += mb + r < M ? TT<T>::to_f(R[__mul24(mb + r, O) + o]) : 0.f;
+      if constexpr (RELU) v[r] = fmaxf(v[r], 0.f);
     }
-    if (pool) {
+    if constexpr (POOL) {
       // rows mb..mb+3 are one 2x2 window; the first maximum in (dy,dx) order wins
-      int am = 0;
+      uint32_t am = 1u;
       float mx = v[0];
 #pragma unroll
       for (int r = 1; r < 4; ++r)
         if (v[r] > mx) {
           mx = v[r];
-          am = r;
+          am = 1u << r;
         }
-      const int e = (mb >> 2) * O + o;
+      // 24-bit multiplies (full rate): pixel and channel counts are under 2^24
+      const int e = __mul24(mb >> 2, O) + o;
       buf_store_t<T>(rP, e, mx);
-      __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(1u << am), rAM, e, 0, 0);
+      __builtin_amdgcn_raw_buffer_store_b8((uint8_t)am, rAM, e, 0, 0);
     } else {
       const int nv = min(4, M - mb);
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         if (r >= nv) break;
-        buf_store_t<T>(rP, (mb + r) * O + o, v[r]);
+        buf_store_t<T>(rP, __mul24(mb + r, O) + o, v[r]);
       }
     }
   });
+}
+
+template <typename T, class L>
+__device__ __forceinline__ void conv_fwd_epilogue(const ConvProb& p, int m0, int n0, const typename L::Acc& acc) {
+  const bool relu = p.relu != 0;
+  if (p.R) {  // residual blocks are never pooled
+    if (relu) conv_fwd_epi<T, L, true, false, true>(p, m0, n0, acc);
+    else conv_fwd_epi<T, L, false, false, true>(p, m0, n0, acc);
+  } else if (p.pool) {
+    if (relu) conv_fwd_epi<T, L, true, true, false>(p, m0, n0, acc);
+    else conv_fwd_epi<T, L, false, true, false>(p, m0, n0, acc);
+  } else {
+    if (relu) conv_fwd_epi<T, L, true, false, false>(p, m0, n0, acc);
+    else conv_fwd_epi<T, L, false, false, false>(p, m0, n0, acc);
+  }
 }
 
 // Conv data-gradient epilogue: the previous block's ReLU' (its stored output
