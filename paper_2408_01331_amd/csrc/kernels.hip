@@ -1564,6 +1564,33 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
   }
 }
 
+// Zero the elements of v whose element of x is not > 0 (ReLU', x the stored
+// output). bf16: two elements per 32-bit word with packed 16-bit integer
+// operations: x > 0 exactly when its bits lie in [0x0001, 0x7f80] (positive,
+// not NaN), i.e. when 0x7f80 - (x - 1), saturating at 0, is not 0.
+template <typename T> __device__ __forceinline__ void relu_mask(u32x4& v, const u32x4& x);
+template <> __device__ __forceinline__ void relu_mask<float>(u32x4& v, const u32x4& x) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+    if (!(__uint_as_float(x[e]) > 0.f)) v[e] = 0u;
+}
+// (each word passed by value: bit-casting the vector's elements in place
+// produced one mask for all four words)
+__device__ __forceinline__ uint32_t relu_mask_word(uint32_t xw) {
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  const u16x2 one = {1, 1}, top = {0x7f80, 0x7f80}, zero = {0, 0};
+  const u16x2 xv = __builtin_bit_cast(u16x2, xw);
+  const u16x2 pos = __builtin_elementwise_min(__builtin_elementwise_sub_sat(top, xv - one), one);  // 1 where x > 0
+  return __builtin_bit_cast(uint32_t, zero - pos);
+}
+template <> __device__ __forceinline__ void relu_mask<bf16_t>(u32x4& v, const u32x4& x) {
+  const uint32_t x0 = x[0], x1 = x[1], x2 = x[2], x3 = x[3];
+  v[0] &= relu_mask_word(x0);
+  v[1] &= relu_mask_word(x1);
+  v[2] &= relu_mask_word(x2);
+  v[3] &= relu_mask_word(x3);
+}
+
 // ---------------------------------------------------------------------------
 // Convolution passes
 // ---------------------------------------------------------------------------
@@ -1763,11 +1790,7 @@ __device__ __forceinline__ void conv_dgrad_epilogue(const ConvProb& p, int m0, i
       const int idx = threadIdx.x + NT * s, r = idx / CPR, c = n0 + (idx - r * CPR) * VE, m = m0 + r;
       if (idx >= BM * CPR || m >= M || c >= C) continue;
       u32x4 v = *(const u32x4*)(sG + r * ES::SLD + (c - n0));
-      if (prev_relu) {
-#pragma unroll
-        for (int e = 0; e < VE; ++e)
-          if (!(vget<T>(xs[s], e) > 0.f)) vset_bits<T>(v, e, 0u);
-      }
+      if (prev_relu) relu_mask<T>(v, xs[s]);
       *(gptr<u32x4>)(Gp + m * C + c) = v;
     }
     return;
@@ -1891,6 +1914,8 @@ struct TapRowLoader {
 // multiplies (rows of under 2^24 elements, tensors of under 2^31 bytes).
 template <typename T, bool DGRAD, int NT = 256>
 __device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, int y0, int c0, int cbw) {
+  // four loads in flight per thread (six or eight measured no faster for
+  // the data gradient's larger blocks)
   constexpr int VEC = TT<T>::VEC, UNR = 4;
   const int cpp = cbw / VEC, hc = p.hc, hr = p.hr, cs = p.cs, imgs = p.imgs, Nb = p.Nb, plane = hr * hc;
   const int dpos = NT / cpp, dch = NT - dpos * cpp, dimg = dpos / plane, dr = dpos - dimg * plane;
