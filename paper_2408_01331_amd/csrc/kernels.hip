@@ -939,12 +939,34 @@ struct WgradLoader {
   u32x4 raw[2][VEC];       // A pooled: raw[S][0..NW) = window gradients; else the pixel vectors
   uint64_t am[2][NW];      // A pooled: window argmaxes
   int wkb, wn, wph, wpw;   // B pooled: (image, row, column) of this thread's first window of k-block wkb
+  // B generic: column r0 + q's tap offsets (du, dv) and element offset from
+  // the pixel's first channel (fixed per thread, so computed once); a column
+  // past J gets a dv no pixel brings in range; bq: the bias column's q or -1
+  int gdu[VEC], gdv[VEC], goff[VEC], bq;
   __device__ __forceinline__ void init(const ConvProb& pr, int m0, int n0) {
     p = &pr;
     isA = __builtin_amdgcn_readfirstlane(threadIdx.x) < 128;  // waves 0-1: A, waves 2-3: B (wave-uniform)
     microtile_of(threadIdx.x % 128, rg, pg);
     r0 = (isA ? m0 : n0) + rg * VEC;
     wkb = -1;
+    if constexpr (MODE == WG_GENERIC) {
+      const int C = pr.C, KW = pr.KH, J = pr.KH * pr.KH * C;
+      bq = J - r0 >= 0 && J - r0 < VEC ? J - r0 : -1;
+#pragma unroll
+      for (int q = 0; q < VEC; ++q) {
+        const int j = r0 + q;
+        if (j < J) {
+          const int tq = j / C, c = j - tq * C, uq = tq / KW, vq = tq - uq * KW;
+          gdu[q] = uq - pr.pad;
+          gdv[q] = vq - pr.pad;
+          goff[q] = (gdu[q] * pr.W + gdv[q]) * C + c;
+        } else {
+          gdu[q] = 0;
+          gdv[q] = -(1 << 29);
+          goff[q] = 0;
+        }
+      }
+    }
   }
   // advance a pooled window position by `by` windows (row-major over images)
   __device__ __forceinline__ void win_step(int& n, int& ph, int& pw, int by) const {
@@ -1077,33 +1099,53 @@ struct WgradLoader {
       raw[S][e] = v;
     }
   }
-  // B, any channel count, pooled or not: element by element
+  // B, any channel count, pooled or not: element by element; the pixels'
+  // positions decoded once per k-block and stepped (a pooled block's pixels
+  // run through each window's four positions, else along the row)
   template <int S>
   __device__ __forceinline__ void loadB_generic(int kb) {
-    const T* X = (const T*)p->X;
-    const int C = p->C, H = p->H, W = p->W, KW = p->KH, pad = p->pad, J = p->KH * p->KH * C, j0 = r0;
+    const gptr<const T> X = G((const T*)p->X);
+    const int C = p->C, H = p->H, W = p->W, K = p->K;
+    const bool pool = p->pool != 0;
     const int pix0 = kb * BK + pg * VEC;
+    int n, y, x;
+    decode_out_pixel(*p, pix0, n, y, x);
 #pragma unroll
     for (int e = 0; e < VEC; ++e) {
       const int pix = pix0 + e;
       u32x4 val = zero4();
-      if (pix < p->K && j0 <= J) {
-        int n, y, x;
-        decode_out_pixel(*p, pix, n, y, x);
-#pragma unroll 1
+      if (pix < K) {
+        const int base = ((n * H + y) * W + x) * C;
+#pragma unroll
         for (int q = 0; q < VEC; ++q) {
-          const int j = j0 + q;
-          if (j < J) {
-            const int tq = j / C, c = j - tq * C, uq = tq / KW, vq = tq - uq * KW;
-            const int iy = y + uq - pad, ix = x + vq - pad;
-            if (iy >= 0 && iy < H && ix >= 0 && ix < W)
-              vset_bits<T>(val, q, bits_of<T>(X[((int64_t)(n * H + iy) * W + ix) * C + c]));
-          } else if (j == J) {
-            vset_bits<T>(val, q, bits_of<T>(TT<T>::from_f(1.0f)));
-          }
+          const int iy = y + gdu[q], ix = x + gdv[q];
+          if ((unsigned)iy < (unsigned)H && (unsigned)ix < (unsigned)W)
+            vset_bits<T>(val, q, bits_of<T>(X[base + goff[q]]));
         }
+#pragma unroll
+        for (int q = 0; q < VEC; ++q)
+          if (q == bq) vset_bits<T>(val, q, bits_of<T>(TT<T>::from_f(1.0f)));
       }
       raw[S][e] = val;
+      if (e + 1 == VEC) break;
+      // the next pixel: pooled order (a window's four positions, then the
+      // next window), else along the row
+      if (pool) {
+        if ((pix & 1) == 0) {
+          ++x;
+        } else if ((pix & 3) == 1) {
+          --x;
+          ++y;
+        } else {
+          decode_out_pixel(*p, pix + 1, n, y, x);
+        }
+      } else if (++x == p->OW) {
+        x = 0;
+        if (++y == p->OH) {
+          y = 0;
+          ++n;
+        }
+      }
     }
   }
   // stage: A tile at stage[0], B tile at stage[BM * LDK]
