@@ -74,6 +74,13 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 // which gives the same bits as that integer rounding (add 0x7fff plus the
 // kept least significant bit) for every one of the 2^32 inputs (measured).
 __device__ __forceinline__ bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
+// two values rounded as f2bf, lo in bits 0-15 and hi in 16-31: one
+// instruction for the pair
+__device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
+  typedef float f32x2 __attribute__((ext_vector_type(2)));
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
+}
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
 template <typename T> struct TT;
@@ -1211,8 +1218,8 @@ template <typename T> __device__ __forceinline__ void store4_t(T* dst, const flo
   if (nvalid == 4) {
     if constexpr (sizeof(T) == 2) {
       u32x2 w;
-      w[0] = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-      w[1] = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+      w[0] = f2bf2(v[0], v[1]);
+      w[1] = f2bf2(v[2], v[3]);
       *(u32x2*)dst = w;
     } else {
       *(f32x4*)dst = f32x4{v[0], v[1], v[2], v[3]};
@@ -1225,18 +1232,18 @@ template <typename T> __device__ __forceinline__ void store4_t(T* dst, const flo
 // 16-byte chunk of VE consecutive outputs from fp32 values, as storage type OT.
 template <typename OT> __device__ __forceinline__ void store_chunk(OT* dst, const float* v, int nvalid);
 template <> __device__ __forceinline__ void store_chunk<float>(float* dst, const float* v, int nvalid) {
-  if (nvalid == 4) *(f32x4*)dst = f32x4{v[0], v[1], v[2], v[3]};
+  if (nvalid == 4) *(gptr<f32x4>)dst = f32x4{v[0], v[1], v[2], v[3]};
   else
-    for (int e = 0; e < nvalid; ++e) dst[e] = v[e];
+    for (int e = 0; e < nvalid; ++e) G(dst)[e] = v[e];
 }
 template <> __device__ __forceinline__ void store_chunk<bf16_t>(bf16_t* dst, const float* v, int nvalid) {
   if (nvalid == 8) {
     u32x4 w;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) w[q] = (uint32_t)f2bf(v[2 * q]) | ((uint32_t)f2bf(v[2 * q + 1]) << 16);
-    *(u32x4*)dst = w;
+    for (int q = 0; q < 4; ++q) w[q] = f2bf2(v[2 * q], v[2 * q + 1]);
+    *(gptr<u32x4>)dst = w;
   } else {
-    for (int e = 0; e < nvalid; ++e) dst[e] = f2bf(v[e]);
+    for (int e = 0; e < nvalid; ++e) G(dst)[e] = f2bf(v[e]);
   }
 }
 
@@ -1582,8 +1589,8 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
       __builtin_nontemporal_store(w, (gptr<f32x4>)(p.W + base));
       if (p.Wb) {
         u32x2 hb;
-        hb[0] = (uint32_t)f2bf(w[0]) | ((uint32_t)f2bf(w[1]) << 16);
-        hb[1] = (uint32_t)f2bf(w[2]) | ((uint32_t)f2bf(w[3]) << 16);
+        hb[0] = f2bf2(w[0], w[1]);
+        hb[1] = f2bf2(w[2], w[3]);
         __builtin_nontemporal_store(hb, (gptr<u32x2>)((bf16_t*)p.Wb + base));
       }
     } else {
@@ -2440,27 +2447,27 @@ __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* 
                                                               const OptHp* __restrict__ opt, int keep_grads,
                                                               int64_t wsoff) {
   const ReduceProb& p = probs[blk_prob[blockIdx.x]];
-  const float* ws = (const float*)((const char*)p.ws + wsoff);
+  const gptr<const float> ws = G((const float*)((const char*)p.ws + wsoff));
   if (lrv) lr = lrv[p.model];
-  const int64_t e = (int64_t)(blockIdx.x - p.blk_base) * REDUCE_BLOCK + threadIdx.x;
-  const int J1 = p.J + 1;
-  if (e >= (int64_t)p.O * J1) return;
-  const int o = (int)(e / J1), j = (int)(e - (int64_t)o * J1);
+  // 32-bit element indices: a problem's partials are far below 2^31 floats
+  const int e = (blockIdx.x - p.blk_base) * REDUCE_BLOCK + threadIdx.x;
+  const int J1 = p.J + 1, splits = p.splits, ldws = (int)p.ldws;
+  if (e >= p.O * J1) return;
+  const int o = (int)((unsigned)e / (unsigned)J1), j = e - o * J1;
   // the sum in split order, eight loads in flight ahead of their adds
   float s = 0.f;
-  const float* col = ws + (int64_t)o * p.ldws + j;
-  const int64_t sstride = (int64_t)p.O * p.ldws;
+  const int col = o * ldws + j, sstride = p.O * ldws;
   int k = 0;
-  for (; k + 8 <= p.splits; k += 8) {
+  for (; k + 8 <= splits; k += 8) {
     float v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = col[(int64_t)(k + u) * sstride];
+    for (int u = 0; u < 8; ++u) v[u] = ws[col + (k + u) * sstride];
 #pragma unroll
     for (int u = 0; u < 8; ++u) s += v[u];
   }
-  for (; k < p.splits; ++k) s += col[(int64_t)k * sstride];
+  for (; k < splits; ++k) s += ws[col + k * sstride];
   if (j < p.J) {
-    const int64_t idx = (int64_t)o * p.ldgw + j;
+    const int idx = o * (int)p.ldgw + j;
     if (keep_grads) p.gW[idx] = s;
     // master weight and its copies: touched once per step (non-temporal)
     const float w0 = __builtin_nontemporal_load(G(p.W + idx));
@@ -2468,8 +2475,8 @@ __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* 
     __builtin_nontemporal_store(w, G(p.W + idx));
     if (p.Wb) __builtin_nontemporal_store(f2bf(w), G((bf16_t*)p.Wb + idx));
     if (p.WT) {
-      const int tap = j / p.C, c = j - tap * p.C;
-      store_t<T>(p.WT, (int64_t)c * p.ldwt + (int64_t)tap * p.O + o, w);
+      const int tap = (int)((unsigned)j / (unsigned)p.C), c = j - tap * p.C;
+      G((T*)p.WT)[c * (int)p.ldwt + tap * p.O + o] = TT<T>::from_f(w);
     }
   } else {
     if (keep_grads) p.gb[o] = s;
@@ -2586,8 +2593,8 @@ __device__ __forceinline__ void attn_put4(T* dst, const float* v, int n, float s
   if (n == 4) {
     if constexpr (sizeof(T) == 2) {
       u32x2 w;
-      w[0] = (uint32_t)f2bf(v[0] * scale) | ((uint32_t)f2bf(v[1] * scale) << 16);
-      w[1] = (uint32_t)f2bf(v[2] * scale) | ((uint32_t)f2bf(v[3] * scale) << 16);
+      w[0] = f2bf2(v[0] * scale, v[1] * scale);
+      w[1] = f2bf2(v[2] * scale, v[3] * scale);
       *(gptr<u32x2>)dst = w;
     } else {
       *(gptr<f32x4>)dst = f32x4{v[0] * scale, v[1] * scale, v[2] * scale, v[3] * scale};
