@@ -137,6 +137,19 @@ def pmc(a):
             for c in ("SQ_WAIT_ANY", "SQ_WAIT_INST_LDS", "SQ_ACTIVE_INST_VMEM", "SQ_VALU_MFMA_BUSY_CYCLES"):
                 if c in cs:
                     rec[c + "/SQ_WAVE_CYCLES"] = cs[c] / wave
+        waves = cs.get("SQ_WAVES")
+        if waves and "SQ_INSTS_VALU" in cs:
+            # vector instructions per wave, and the time the whole dispatch's
+            # vector instructions take to issue: a wave64 instruction occupies
+            # its SIMD for 4 cycles; 1024 SIMDs at 2.4 GHz
+            rec["valu_per_wave"] = cs["SQ_INSTS_VALU"] / waves
+            rec["valu_issue_us"] = cs["SQ_INSTS_VALU"] * 4 / (1024 * 2.4e9) * 1e6
+            if t:
+                rec["valu_issue_frac"] = rec["valu_issue_us"] / (t / 1e3)
+            if "SQ_INSTS_SALU" in cs:
+                rec["salu_per_wave"] = cs["SQ_INSTS_SALU"] / waves
+            if "SQ_INSTS_MFMA" in cs:
+                rec["mfma_insts_per_wave"] = cs["SQ_INSTS_MFMA"] / waves
         if cs.get("SQ_BUSY_CYCLES") and "SQ_VALU_MFMA_BUSY_CYCLES" in cs:
             rec["MFMA_BUSY/SQ_BUSY"] = cs["SQ_VALU_MFMA_BUSY_CYCLES"] / cs["SQ_BUSY_CYCLES"]
         rd = cs.get("TCC_EA0_RDREQ_sum")
