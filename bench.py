@@ -277,10 +277,10 @@ def copy_probe(nbytes=1 << 30, reps=4):
 
 
 def source_digest():
-    """sha256 of the HIP kernel source (identifies the kernels a profile was taken on)."""
-    import hashlib
-    path = os.path.join(ROOT, "paper_2408_01331_amd", "csrc", "kernels.hip")
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+    """sha256 of the kernel, planner and interface sources (identifies the
+    launches a counter summary was taken on)."""
+    from paper_2408_01331_amd.profile_summary import sources_digest
+    return sources_digest()
 
 
 def measured_traffic(kernel, workload):
@@ -290,7 +290,7 @@ def measured_traffic(kernel, workload):
     if not os.path.exists(path):
         return None, None
     rec = json.load(open(path))
-    if rec.get("kernels_sha256") != source_digest():
+    if rec.get("sources_sha256") != source_digest():
         return None, path
     return rec["hbm_bytes_per_launch"], path
 

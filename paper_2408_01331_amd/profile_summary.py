@@ -31,6 +31,20 @@ import sys
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
+SOURCES = ("paper_2408_01331_amd/csrc/kernels.hip", "paper_2408_01331_amd/csrc/un_api.cpp",
+           "paper_2408_01331_amd/csrc/internal.h", "include/unifiednn.h")
+
+
+def sources_digest():
+    """sha256 over the kernel, planner and interface sources, in a fixed order:
+    a counter summary holds for the launches those sources produce."""
+    h = hashlib.sha256()
+    for rel in SOURCES:
+        h.update(rel.encode())
+        h.update(open(os.path.join(ROOT, rel), "rb").read())
+    return h.hexdigest()
+
+
 def _one(pattern):
     files = sorted(glob.glob(pattern, recursive=True))
     if not files:
@@ -80,8 +94,7 @@ def traffic(a):
     fkib, wkib = sum(f) / len(f), sum(w) / len(w)
     rec = {
         "kernel": a.kernel, "workload": a.workload,
-        "kernels_sha256": hashlib.sha256(
-            open(os.path.join(ROOT, "paper_2408_01331_amd", "csrc", "kernels.hip"), "rb").read()).hexdigest(),
+        "sources_sha256": sources_digest(),
         "dispatches": [len(f), len(w)],
         "fetch_kib_per_dispatch": fkib, "write_kib_per_dispatch": wkib,
         "copy_fetch_factor": ff, "copy_write_factor": wf,
