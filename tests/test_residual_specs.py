@@ -86,3 +86,24 @@ def test_residual_specs_rejected(case):
     with pytest.raises(U.UnError) as e:
         U.un_plan_bytes([spec], 16, (16,), "f32")
     assert e.value.status == status
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
+def test_conv_tensor_size_limits(precision):
+    """The conv kernels address every activation, gradient and weight tensor
+    with 32-bit byte offsets and an output row of elements with 24-bit
+    multiplies: the planner refuses larger conv layers before anything is
+    allocated, and takes the largest ones below the limits."""
+    _need_lib()
+    es = 2 if precision == "bf16" else 4
+    conv = _spec(C(8), RELU, FLAT, L(5))
+    # the largest batch of 8-channel 64x64 maps whose conv output stays under 2^31 bytes
+    ok_batch = ((1 << 31) - 1) // (8 * 64 * 64 * es)
+    assert U.un_plan_bytes([conv], ok_batch, (8, 64, 64), precision)[0] > 0
+    with pytest.raises(U.UnError) as e:
+        U.un_plan_bytes([conv], ok_batch + 1, (8, 64, 64), precision)
+    assert e.value.status == U.UN_ERR_UNSUPPORTED
+    # an output row of 2^24 elements (8192 columns x 2048 channels)
+    with pytest.raises(U.UnError) as e:
+        U.un_plan_bytes([_spec(C(2048, 1, 0), FLAT, L(5))], 1, (8, 1, 8192), precision)
+    assert e.value.status == U.UN_ERR_UNSUPPORTED
