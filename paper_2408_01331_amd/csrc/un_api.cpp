@@ -707,10 +707,11 @@ static void build_tables(un_ctx* c, Tables& T) {
     std::stable_sort(ps.begin(), ps.end(), [&](const GemmProb& x, const GemmProb& y) { return klen(x) > klen(y); });
     // Launch order = problem order (longest K first), tiles m-fastest, then
     // swizzled for the XCDs: the tiles are cut into runs of up to 8 that share
-    // a B tile (one column of m-tiles), and every 8 consecutive runs are
-    // interleaved so that run r lands on XCD r % 8 with its members 8 launch
-    // slots apart - they run together on one XCD and read their B tile from
-    // its L2 once - while the order stays longest-first at the grain of 8 runs.
+    // a B tile (one column of m-tiles, or a few short columns), and every 8
+    // consecutive runs are interleaved so that run r lands on XCD r % 8 with
+    // its members 8 launch slots apart - they run together on one XCD and read
+    // their shared tiles from its L2 once - while the order stays
+    // longest-first at the grain of 8 runs.
     std::vector<int32_t> nat;  // (problem, tile) pairs in run order, with run ids
     std::vector<int32_t> run_of;
     int runs = 0;
@@ -738,12 +739,15 @@ static void build_tables(un_ctx* c, Tables& T) {
               }
             }
         } else {
-          const int rl = std::min(tm, 8);
+          // a column shorter than 8 m-tiles is joined with its neighbours up
+          // to about 8 tiles per run, so that the run's A tiles are shared as
+          // well as its B tiles
+          const int rl = std::min(tm, 8), cpr = tm < 8 ? std::max(1, 8 / tm) : 1;
           for (int t = 0; t < tm * tn; ++t) {
             nat.push_back((int32_t)k);
             nat.push_back(base + t);
             const int col = t / tm, row = t - col * tm;
-            if (row % rl == 0) ++runs;
+            if (row % rl == 0 && col % cpr == 0) ++runs;
             run_of.push_back(runs - 1);
           }
         }
