@@ -801,17 +801,16 @@ template <> __device__ __forceinline__ void select_am<float>(u32x4& v, uint64_t 
     if (!((am >> (8 * e + d)) & 1u)) v[e] = 0u;
 }
 template <> __device__ __forceinline__ void select_am<bf16_t>(u32x4& v, uint64_t am, int d) {
-  // byte masks (0x00 / 0xff) of elements 0-3 and 4-7, widened to 16 bits by
-  // byte permutes; x * 0xff as (x << 8) - x, kept from being folded back
-  // into a multiply (quarter-rate) by an empty asm operand
-  const uint32_t bl = (uint32_t)(am >> d) & 0x01010101u, bh = (uint32_t)(am >> (32 + d)) & 0x01010101u;
-  uint32_t sl = bl << 8, sh = bh << 8;
-  asm("" : "+v"(sl), "+v"(sh));
-  const uint32_t ml = sl - bl, mh = sh - bh;
-  v[0] &= __builtin_amdgcn_perm(ml, ml, 0x01010000u);
-  v[1] &= __builtin_amdgcn_perm(ml, ml, 0x03030202u);
-  v[2] &= __builtin_amdgcn_perm(mh, mh, 0x01010000u);
-  v[3] &= __builtin_amdgcn_perm(mh, mh, 0x03030202u);
+  // bit d of byte c (element c's byte) is shifted to the top bit of byte c
+  // (m1) and of byte c + 1 (m2); the sign-copy selectors of the byte permute
+  // (8 / 9: bit 15 / 31 of the second source, 10 / 11: bit 15 / 31 of the
+  // first) spread it over the two bytes of element c
+  const uint64_t m1 = am << (7 - d), m2 = m1 << 8;
+  const uint32_t l1 = (uint32_t)m1, h1 = (uint32_t)(m1 >> 32), l2 = (uint32_t)m2, h2 = (uint32_t)(m2 >> 32);
+  v[0] &= __builtin_amdgcn_perm(l1, l2, 0x0A0A0808u);
+  v[1] &= __builtin_amdgcn_perm(l1, l2, 0x0B0B0909u);
+  v[2] &= __builtin_amdgcn_perm(h1, h2, 0x0A0A0808u);
+  v[3] &= __builtin_amdgcn_perm(h1, h2, 0x0B0B0909u);
 }
 // Is pixel d the maximum of its window (argmax byte a)?
 __device__ __forceinline__ bool am_is(uint8_t a, int d) { return (a >> d) & 1u; }
@@ -2279,32 +2278,37 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 template <int ROWS, int BK, int NT, int SLOTS, int PAD, bool POOL>
 struct ConvKA {
   static constexpr int VEC = 8, CPR = ROWS / VEC, LDR = ROWS + PAD;
-  static constexpr int OOB = 0x7ffffff0;  // a buffer offset past every range: the load returns zero
   static_assert(BK * CPR == NT, "one chunk per thread and k-block");
   static_assert(BK % 4 == 0, "k-blocks hold whole windows");
   __amdgpu_buffer_rsrc_t rs, rs_am;
-  int off, step, sm_off;
-  bool oin;
+  uint32_t offb, offa, stepb, stepa;  // byte offsets of the chunk in G and in the argmax bytes, and their steps
+  int sm_off;
   u32x4 r[SLOTS];
   uint64_t am[SLOTS];
+  // Channels o >= O are read without a range test: they feed accumulator rows
+  // that are never stored. Pixels past the last one lie past both buffers'
+  // ranges and read zero.
   __device__ __forceinline__ void init(const ConvProb& p, int o0, int kb0) {
     const int k = threadIdx.x / CPR, o = o0 + (threadIdx.x % CPR) * VEC;
-    oin = o < p.O;
     const int pix = kb0 * BK + k;
-    off = (POOL ? pix >> 2 : pix) * p.O + o;  // element offset of this chunk in G
-    step = (POOL ? BK / 4 : BK) * p.O;
+    const uint32_t e = (uint32_t)((POOL ? pix >> 2 : pix) * p.O + o);  // element offset of this chunk in G
+    const uint32_t step = (uint32_t)((POOL ? BK / 4 : BK) * p.O);
+    offb = 2 * e;
+    offa = e;
+    stepb = 2 * step;
+    stepa = step;
     sm_off = kmaj_bf16<LDR>(k, (threadIdx.x % CPR) * VEC);
     const int64_t rows = POOL ? (int64_t)p.Nb * p.PH * p.PW : (int64_t)p.Nb * p.OH * p.OW;
     rs = make_rsrc(p.G, rows * p.O * (int64_t)sizeof(bf16_t));
     if constexpr (POOL) rs_am = make_rsrc(p.gam, rows * p.O);
   }
-  // the next k-block (the loop issues blocks in order, one call each);
-  // pixels past the last one lie past both buffers' ranges and read zero
+  // the next k-block (the loop issues blocks in order, one call each)
   template <int S>
   __device__ __forceinline__ void load(int) {
-    r[S] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, oin ? off * 2 : OOB, 0, 0));
-    if constexpr (POOL) am[S] = oin ? load_am_buf<bf16_t>(rs_am, off) : 0ull;
-    off += step;
+    r[S] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, offb, 0, 0));
+    if constexpr (POOL) am[S] = load_am_buf<bf16_t>(rs_am, offa);
+    offb += stepb;
+    offa += stepa;
   }
   template <int S>
   __device__ __forceinline__ void store(bf16_t* sm) const {
@@ -2314,29 +2318,50 @@ struct ConvKA {
   }
 };
 
-// Chunk s of a thread: output pixel k + s * (NT / CPR) of the block. Its
-// position is kept as (n, a, b) - a pooled block's window row and column
-// (pixel order 4 * window + (dy, dx)), else the pixel's row and column - and as
-// the element offset q that the chunk's tap and channels read for it, input
-// position (n, y + u - pad, x + v - pad), y = F*a + dy, x = F*b + dx (F = 2
-// pooled, else 1; dy = dx = 0 unpooled); every k-block moves it by BK pixels. Pixels past the last one have n >= Nb: their input rows lie past
-// the buffer's range and read zero (the gradient operand is zero there too).
-template <int ROWS, int BK, int NT, int SLOTS, int PAD, bool POOL>
+// Chunk s of a thread: output pixel k + s * (NT / CPR) of the block, input
+// position (n, y + u - pad, x + v - pad) of the chunk's tap (u, v), with
+// y = F*a + dy, x = F*b + dx: (a, b) is a pooled block's window (pixel order
+// 4 * window + (dy, dx)), else the pixel itself (F = 1, dy = dx = 0). Pixels
+// past the last one have n >= Nb: their input rows lie past the buffer's range
+// and read zero (the gradient operand is zero there too). The bias column
+// J reads ones; columns past it feed output columns that are never stored.
+//
+// Every k-block moves a chunk by BK pixels. UNI: the k-blocks are whole rows
+// of windows within one image, or whole images, so every lane moves by the
+// same rows and the wrap to the next image is the same for all: a lane keeps
+// its input row and byte offset, stepped by wave-uniform amounts. Otherwise a
+// lane keeps (a, b) and the element offset q and wraps them itself.
+template <int ROWS, int BK, int NT, int SLOTS, int PAD, bool POOL, bool UNI>
 struct ConvKB {
   static constexpr int VEC = 8, CPR = ROWS / VEC, LDR = ROWS + PAD, NV = BK * CPR / NT, F = POOL ? 2 : 1;
-  static constexpr int OOB = 0x7ffffff0;
+  static constexpr int ST = POOL ? BK / 4 : BK;  // windows (or pixels) per k-block
+  static constexpr uint32_t OOB = 0x7ffffff0u;   // a byte offset past every range: the load returns zero
   static_assert(NV >= 1 && BK * CPR == NV * NT, "whole chunks per thread and k-block");
   static_assert(NT % CPR == 0 && (NT / CPR) % 4 == 0, "a thread's chunks share one row set and window position");
+  __device__ __forceinline__ static bool uniform(const ConvProb& pr) {
+    const int A = POOL ? pr.PH : pr.OH, B = POOL ? pr.PW : pr.OW, plane = A * B;
+    return (ST % B == 0 && plane % ST == 0) || ST % plane == 0;
+  }
   __amdgpu_buffer_rsrc_t rs;
-  int H, W, A, B, sa, sb, q0, q1, q2, ey, ex, sm_off;
-  bool jin, bias;
+  int H, W, A, B, ey, ex, sm_off;
+  uint32_t orm;  // ORed into the first word: the bias column's 1.0, else 0
+  bool jin;
+  // general stepping
+  int sa, sb, q0, q1, q2;
   int a[NV], b[NV], q[NV];
+  // uniform stepping: the block's first window row ablk, rows per block ra,
+  // and the row / byte steps of a block without (n) and with (w) the wrap
+  int ablk, ra, dyn, dyw;
+  uint32_t dqn, dqw;
+  int iy[NV];
+  uint32_t qb[NV];
+  bool xin[NV];
   u32x4 r[SLOTS][NV];
   __device__ __forceinline__ void init(const ConvProb& pr, int j0, int kb0) {
     const int k = threadIdx.x / CPR;
     const int j = j0 + (threadIdx.x % CPR) * VEC, J = pr.KH * pr.KH * pr.C;
     jin = j < J;
-    bias = j == J;
+    orm = j == J ? bits_of<bf16_t>(TT<bf16_t>::from_f(1.0f)) : 0u;
     const int tap = j / pr.C, c0 = j - tap * pr.C, u = tap / pr.KH, v = tap - u * pr.KH;
     H = pr.H;
     W = pr.W;
@@ -2346,44 +2371,89 @@ struct ConvKB {
     ey = dy + u - pr.pad;  // input row of the chunk's pixel: F * a + ey
     ex = dx + v - pr.pad;
     sm_off = kmaj_bf16<LDR>(k, (threadIdx.x % CPR) * VEC);
-    // the step of BK pixels (BK / 4 windows) in (n, a, b) and its offsets
-    const int st = POOL ? BK / 4 : BK, plane = A * B;
-    const int sn = st / plane, rem = st - sn * plane;
-    sa = rem / B;
-    sb = rem - sa * B;
-    q0 = (sn * H * W + F * sa * W + F * sb) * pr.C;  // every step
-    q1 = (F * W - F * B) * pr.C;                      // b wrapped: next row of windows
-    q2 = (H * W - F * A * W) * pr.C;                  // a wrapped: next image
+    const int plane = A * B;
+    if constexpr (UNI) {
+      const int C2 = 2 * pr.C;
+      if (ST % plane == 0) {  // whole images per block
+        ra = 0;
+        dyn = dyw = 0;
+        dqn = dqw = (uint32_t)((ST / plane) * H * W * C2);
+      } else {  // whole rows of one image per block
+        ra = ST / B;
+        dyn = F * ra;
+        dyw = F * ra - F * A;
+        dqn = (uint32_t)(F * ra * W * C2);
+        dqw = (uint32_t)((F * ra * W + H * W - F * A * W) * C2);
+      }
+      ablk = ((kb0 * ST) % plane) / B;
+    } else {
+      // the step of BK pixels (BK / 4 windows) in (n, a, b) and its offsets
+      const int sn = ST / plane, rem = ST - sn * plane;
+      sa = rem / B;
+      sb = rem - sa * B;
+      q0 = (sn * H * W + F * sa * W + F * sb) * pr.C;  // every step
+      q1 = (F * W - F * B) * pr.C;                      // b wrapped: next row of windows
+      q2 = (H * W - F * A * W) * pr.C;                  // a wrapped: next image
+    }
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int pix = kb0 * BK + k + s * (NT / CPR), m = POOL ? pix >> 2 : pix;
       const int n = m / plane, r2 = m - n * plane;
-      a[s] = r2 / B;
-      b[s] = r2 - a[s] * B;
-      q[s] = ((n * H + F * a[s] + ey) * W + F * b[s] + ex) * pr.C + c0;
+      const int aa = r2 / B, bb = r2 - aa * B;
+      if constexpr (UNI) {
+        iy[s] = F * aa + ey;
+        const int ix = F * bb + ex;
+        xin[s] = jin && (unsigned)ix < (unsigned)W;
+        // modulo 2^32: exact again once the row is inside the image
+        qb[s] = 2u * (uint32_t)(((n * H + iy[s]) * W + ix) * pr.C + c0);
+      } else {
+        a[s] = aa;
+        b[s] = bb;
+        q[s] = ((n * H + F * aa + ey) * W + F * bb + ex) * pr.C + c0;
+      }
     }
     rs = make_rsrc(pr.X, (int64_t)pr.Nb * pr.H * pr.W * pr.C * (int64_t)sizeof(bf16_t));
   }
   // the next k-block (the loop issues blocks in order, one call each)
   template <int S>
   __device__ __forceinline__ void load(int) {
+    if constexpr (UNI) {
+      int dy = dyn;
+      uint32_t dq = dqn;
+      ablk += ra;
+      if (ablk >= A) {  // wave-uniform: the next block starts the next image
+        ablk -= A;
+        dy = dyw;
+        dq = dqw;
+      }
 #pragma unroll
-    for (int s = 0; s < NV; ++s) {
-      const int iy = F * a[s] + ey, ix = F * b[s] + ex;
-      const bool in = jin && (unsigned)iy < (unsigned)H && (unsigned)ix < (unsigned)W;
-      u32x4 val = __builtin_bit_cast(
-          u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? q[s] * 2 : OOB, 0, 0));
-      if (bias) vset_bits<bf16_t>(val, 0, bits_of<bf16_t>(TT<bf16_t>::from_f(1.0f)));
-      r[S][s] = val;
-      q[s] += q0;
-      b[s] += sb;
-      const bool cb = b[s] >= B;
-      b[s] -= cb ? B : 0;
-      q[s] += cb ? q1 : 0;
-      a[s] += sa + (cb ? 1 : 0);
-      const bool ca = a[s] >= A;
-      a[s] -= ca ? A : 0;
-      q[s] += ca ? q2 : 0;
+      for (int s = 0; s < NV; ++s) {
+        const bool in = xin[s] && (unsigned)iy[s] < (unsigned)H;
+        u32x4 val = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? qb[s] : OOB, 0, 0));
+        val[0] |= orm;
+        r[S][s] = val;
+        iy[s] += dy;
+        qb[s] += dq;
+      }
+    } else {
+#pragma unroll
+      for (int s = 0; s < NV; ++s) {
+        const int iyy = F * a[s] + ey, ix = F * b[s] + ex;
+        const bool in = jin && (unsigned)iyy < (unsigned)H && (unsigned)ix < (unsigned)W;
+        u32x4 val = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? (uint32_t)q[s] * 2u : OOB, 0, 0));
+        val[0] |= orm;
+        r[S][s] = val;
+        q[s] += q0;
+        b[s] += sb;
+        const bool cb = b[s] >= B;
+        b[s] -= cb ? B : 0;
+        q[s] += cb ? q1 : 0;
+        a[s] += sa + (cb ? 1 : 0);
+        const bool ca = a[s] >= A;
+        a[s] -= ca ? A : 0;
+        q[s] += ca ? q2 : 0;
+      }
     }
   }
   template <int S>
@@ -2420,10 +2490,17 @@ void conv_wgrad_mfma_kernel(const ConvProb* __restrict__ probs, const int32_t* _
   typename MM::Acc acc;
   MM::zero(acc);
   ConvKA<BM, BK, NT, D, KMAJ_PAD_BF16, POOL> la;
-  ConvKB<BN, BK, NT, D, KMAJ_PAD_BF16, POOL> lb;
   la.init(p, m0, kb0);
-  lb.init(p, n0, kb0);
-  gemm_loop<bf16_t, BM, BN, BK, D, MM, OP_KMAJ, OP_KMAJ>(la, lb, nkb, (bf16_t*)smem, acc);
+  using KBU = ConvKB<BN, BK, NT, D, KMAJ_PAD_BF16, POOL, true>;
+  if (KBU::uniform(p)) {
+    KBU lb;
+    lb.init(p, n0, kb0);
+    gemm_loop<bf16_t, BM, BN, BK, D, MM, OP_KMAJ, OP_KMAJ>(la, lb, nkb, (bf16_t*)smem, acc);
+  } else {
+    ConvKB<BN, BK, NT, D, KMAJ_PAD_BF16, POOL, false> lb;
+    lb.init(p, n0, kb0);
+    gemm_loop<bf16_t, BM, BN, BK, D, MM, OP_KMAJ, OP_KMAJ>(la, lb, nkb, (bf16_t*)smem, acc);
+  }
 
   // this split's partial sums to ws[split][o][j] (32-bit offsets within the
   // split's block of partials)
