@@ -117,6 +117,11 @@ struct ConvProb {
   int32_t tiles_m, tiles_n, splits, kchunk;
   int32_t halo, tr, imgs, hr, hc, cb, cs;  // halo tiling (see above)
   int32_t bm, bn;                          // halo tile shape
+  // fl(1/d) (correctly rounded) for the halo tile's small divisors, computed
+  // once on the host: tile rows per image and per image row (pooled forward:
+  // windows), KH, 16-byte chunks per position of a full and of the last
+  // channel block, staged positions per image (hr * hc) and hc
+  float rc_img, rc_row, rc_kh, rc_cpt, rc_cpt_last, rc_plane, rc_hc;
   const void* X;              // conv input, NHWC, channel stride C
   const void* Wt;             // fwd: W [O][ldw]; dgrad: WT [C][ldw]
   int64_t ldw;

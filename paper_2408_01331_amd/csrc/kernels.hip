@@ -570,7 +570,9 @@ template <class T> __device__ __forceinline__ gptr<T> G(T* p) { return (gptr<T>)
 struct SmallDiv {
   float r, h;
   int d;
-  __device__ __forceinline__ explicit SmallDiv(int dv) : r(1.0f / (float)dv), h(0.5f / (float)dv), d(dv) {}
+  // rv = fl(1/dv), rounded on the host (a correctly rounded division costs
+  // a dozen vector instructions); 0.5 fl(1/dv) = fl(0.5/dv) exactly
+  __device__ __forceinline__ SmallDiv(int dv, float rv) : r(rv), h(0.5f * rv), d(dv) {}
   __device__ __forceinline__ int q(int x) const { return (int)fmaf((float)x, r, h); }
   // quotient and remainder (x - q d by a 24-bit multiply: q d <= x < 2^22)
   __device__ __forceinline__ int qr(int x, int& rem) const {
@@ -1194,6 +1196,14 @@ template <> __device__ __forceinline__ void buf_store_t<float>(__amdgpu_buffer_r
 template <> __device__ __forceinline__ void buf_store_t<bf16_t>(__amdgpu_buffer_rsrc_t r, int e, float v) {
   __builtin_amdgcn_raw_buffer_store_b16(f2bf(v), r, e * 2, 0, 0);
 }
+// The same at byte offset vb (per lane) + sb (wave-uniform, a scalar operand).
+template <typename T> __device__ __forceinline__ void buf_store_ts(__amdgpu_buffer_rsrc_t r, uint32_t vb, int sb, float v);
+template <> __device__ __forceinline__ void buf_store_ts<float>(__amdgpu_buffer_rsrc_t r, uint32_t vb, int sb, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(v), r, vb, sb, 0);
+}
+template <> __device__ __forceinline__ void buf_store_ts<bf16_t>(__amdgpu_buffer_rsrc_t r, uint32_t vb, int sb, float v) {
+  __builtin_amdgcn_raw_buffer_store_b16(f2bf(v), r, vb, sb, 0);
+}
 
 // Load 4 consecutive values (8- or 16-byte aligned) as floats.
 template <typename T> __device__ __forceinline__ void load4_t(const T* src, float (&v)[4]);
@@ -1660,7 +1670,7 @@ struct ConvEpiSmem {
 template <typename T, int BM, int BN, int BK, int NW>
 struct Acc16 {
   using TL = Tile<T, BM, BN, BK, NW>;
-  static constexpr int FM = TL::FM, FN = TL::FN, NT = TL::NT;
+  static constexpr int FM = TL::FM, FN = TL::FN, NT = TL::NT, ROWS = BM;
   using Acc = f32x4[FM][FN];
   __device__ __forceinline__ static void zero(Acc& acc) {
 #pragma unroll
@@ -1682,6 +1692,19 @@ struct Acc16 {
         f(wm + 16 * i + 4 * (lane >> 4), col_of(j), j, v);
       }
   }
+  // the same groups, first row lrow + urow: lrow per lane, urow a constant
+  // of the unrolled loop
+  template <class F>
+  __device__ __forceinline__ static void for_groups_split(const Acc& acc, F&& f) {
+    const int lane = threadIdx.x & 63, lrow = TL::wave_m() + 4 * (lane >> 4);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        float v[4] = {acc[i][j][0], acc[i][j][1], acc[i][j][2], acc[i][j][3]};
+        f(lrow, 16 * i, col_of(j), j, v);
+      }
+  }
 };
 
 // Acc32 (bf16 halo tiles): 32x32x16 MFMA blocks, each wave 32 columns wide
@@ -1690,7 +1713,7 @@ struct Acc16 {
 // four rows start at multiples of four, so a pooled tile's windows stay whole.
 template <int BM, int BN, int NW>
 struct Acc32 {
-  static constexpr int WGN = BN / 32, WGM = NW / WGN, WM = BM / WGM, FM = WM / 32, FN = 1, NT = 64 * NW;
+  static constexpr int WGN = BN / 32, WGM = NW / WGN, WM = BM / WGM, FM = WM / 32, FN = 1, NT = 64 * NW, ROWS = BM;
   static_assert(WGN >= 1 && WGM >= 1 && WGM * WGN == NW && FM >= 1 && FM * 32 * WGM == BM, "32x32 wave tiles");
   using Acc = f32x16[FM];
   __device__ __forceinline__ static int wave_m() { return ((int)(threadIdx.x >> 6) / WGN) * WM; }
@@ -1714,58 +1737,149 @@ struct Acc32 {
         f(wm + 32 * i + 8 * q + 4 * (lane >> 5), col_of(0), 0, v);
       }
   }
+  // the same groups, first row lrow + urow: lrow per lane, urow a constant
+  // of the unrolled loop
+  template <class F>
+  __device__ __forceinline__ static void for_groups_split(const Acc& acc, F&& f) {
+    const int lane = threadIdx.x & 63, lrow = wave_m() + 4 * (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        float v[4] = {acc[i][4 * q], acc[i][4 * q + 1], acc[i][4 * q + 2], acc[i][4 * q + 3]};
+        f(lrow, 32 * i + 8 * q, col_of(0), 0, v);
+      }
+  }
 };
 
-// Conv forward epilogue: bias, ReLU, 2x2 max-pool in registers (pool rows
-// are window-ordered, so a lane's four accumulator rows are one window), then
-// the pooled value and its one-hot argmax, stored straight from registers
+// Conv forward epilogue: ReLU, 2x2 max-pool in registers (pool rows are
+// window-ordered, so a lane's four accumulator rows are one window), then the
+// pooled value and its one-hot argmax, stored straight from registers
 // (staging this small output in LDS measured slower). One straight-line
 // variant per (ReLU, pool, skip input) pattern, chosen by a uniform branch.
+//
+// Pooling takes the maximum of the raw sums, then adds the bias and applies
+// the ReLU once: rounding a + b is monotone in a, so the pooled value is
+// fl(max a + b) either way, and the ReLU commutes with the maximum. The
+// argmax is the first maximum in (dy, dx) order of the raw sums (two sums
+// that differ but round to the same value with the bias pick the larger),
+// and the first member (byte 1) where the pooled value is <= 0: the ReLU'd
+// window is then all zeros.
+// pool4 returns the window's maximum plus the bias, before the ReLU
+// (store_relu applies it), and its argmax byte.
+template <bool RELU>
+__device__ __forceinline__ float pool4(const float (&v)[4], float b, uint32_t& am) {
+  am = 1u;
+  float mx = v[0];
+#pragma unroll
+  for (int r = 1; r < 4; ++r)
+    if (v[r] > mx) {
+      mx = v[r];
+      am = 1u << r;
+    }
+  mx += b;
+  if constexpr (RELU) am = mx > 0.f ? am : 1u;
+  return mx;
+}
+
+// ReLU of two packed bf16 values, on their bits: a negative value (sign bit
+// set) is a negative 16-bit integer. Rounding commutes with it: rounding is
+// monotone and keeps the sign.
+__device__ __forceinline__ uint32_t relu_bf16x2(uint32_t w) {
+  typedef short s16x2 __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s16x2, w), (s16x2){0, 0}));
+}
+
+// Store v, after the ReLU if RELU, at byte offset vb + sb.
+template <typename T, bool RELU>
+__device__ __forceinline__ void store_relu(__amdgpu_buffer_rsrc_t r, uint32_t vb, int sb, float v) {
+  if constexpr (sizeof(T) == 2) {
+    uint32_t w = f2bf2(v, 0.f);
+    if constexpr (RELU) w = relu_bf16x2(w);
+    __builtin_amdgcn_raw_buffer_store_b16((uint16_t)w, r, vb, sb, 0);
+  } else {
+    buf_store_ts<T>(r, vb, sb, RELU ? fmaxf(v, 0.f) : v);
+  }
+}
+
 template <typename T, class L, bool RELU, bool POOL, bool RES>
 __device__ __forceinline__ void conv_fwd_epi(const ConvProb& p, int m0, int n0, const typename L::Acc& acc) {
   // the problem's fields as values: read through the problem reference,
   // every field would be loaded again after each store (the stores might
   // alias it)
   const int O = p.O, M = p.M;
-  const gptr<const T> R = G((const T*)p.R);
-  const gptr<const float> BIAS = G(p.bias);
   // outputs through buffer stores: 32-bit offsets (tensors are under 2^31
   // bytes), no 64-bit address arithmetic per store
   const __amdgpu_buffer_rsrc_t rP = make_rsrc(p.P, 0x7fffffff), rAM = make_rsrc(p.amax, 0x7fffffff);
   // this lane's biases, loaded before the first store: loads and stores
   // share one in-order counter, so a load issued after the stores would wait
   // for all of them (once per fragment row)
+  const gptr<const float> BIAS = G(p.bias);
   float bias[L::FN];
 #pragma unroll
   for (int j = 0; j < L::FN; ++j) {
     const int o = n0 + L::col_of(j);
     bias[j] = o < O ? BIAS[o] : 0.f;
   }
+  if (!RES && m0 + L::ROWS <= M) {
+    // a whole tile: no row test. A lane's stores sit at a fixed offset of
+    // its own plus a uniform one per group (the scalar operand); lanes past
+    // column O store past the buffer's range, where the store is dropped.
+    constexpr uint32_t OUT = 0x80000000u;
+    L::for_groups_split(acc, [&](int lrow, int urow, int cl, int j, const float (&a)[4]) {
+      const int o = n0 + cl;
+      float v[4] = {a[0], a[1], a[2], a[3]};
+      if constexpr (POOL) {
+        // window (m0 + lrow + urow) / 4; 24-bit multiplies (pixel and
+        // channel counts are under 2^24)
+        const uint32_t e = (uint32_t)(__mul24((m0 + lrow) >> 2, O) + o);
+        const int se = (urow >> 2) * O;
+        uint32_t am;
+        const float mx = pool4<RELU>(v, bias[j], am);
+        store_relu<T, RELU>(rP, o < O ? e * (uint32_t)sizeof(T) : OUT, se * (int)sizeof(T), mx);
+        __builtin_amdgcn_raw_buffer_store_b8((uint8_t)am, rAM, o < O ? e : OUT, se, 0);
+      } else {
+        const uint32_t e = (uint32_t)(__mul24(m0 + lrow, O) + o), vb = o < O ? e * (uint32_t)sizeof(T) : OUT;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] += bias[j];
+        if constexpr (sizeof(T) == 2) {
+          // two rows per conversion; the second from the high half
+#pragma unroll
+          for (int r = 0; r < 4; r += 2) {
+            uint32_t w = f2bf2(v[r], v[r + 1]);
+            if constexpr (RELU) w = relu_bf16x2(w);
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)w, rP, vb, (urow + r) * O * 2, 0);
+            __builtin_amdgcn_raw_buffer_store_b16((uint16_t)(w >> 16), rP, vb, (urow + r + 1) * O * 2, 0);
+          }
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            if constexpr (RELU) v[r] = fmaxf(v[r], 0.f);
+            buf_store_ts<T>(rP, vb, (urow + r) * O * (int)sizeof(T), v[r]);
+          }
+        }
+      }
+    });
+    return;
+  }
+  const gptr<const T> R = G((const T*)p.R);
   L::for_groups(acc, [&](int rl, int cl, int j, const float (&a)[4]) {
     const int mb = m0 + rl, o = n0 + cl;
     if (mb >= M || o >= O) return;
-    const float b = bias[j];
     float v[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      v[r] = a[r] + b;
+      v[r] = POOL ? a[r] : a[r] + bias[j];
       // skip input of a residual block (never pooled): rows are pixels
       if constexpr (RES) v[r] += mb + r < M ? TT<T>::to_f(R[__mul24(mb + r, O) + o]) : 0.f;
-      if constexpr (RELU) v[r] = fmaxf(v[r], 0.f);
+      if constexpr (RELU && !POOL) v[r] = fmaxf(v[r], 0.f);
     }
     if constexpr (POOL) {
-      // rows mb..mb+3 are one 2x2 window; the first maximum in (dy,dx) order wins
-      uint32_t am = 1u;
-      float mx = v[0];
-#pragma unroll
-      for (int r = 1; r < 4; ++r)
-        if (v[r] > mx) {
-          mx = v[r];
-          am = 1u << r;
-        }
-      // 24-bit multiplies (full rate): pixel and channel counts are under 2^24
+      // rows mb..mb+3 are one 2x2 window
+      uint32_t am;
+      const float mx = pool4<RELU>(v, bias[j], am);
       const int e = __mul24(mb >> 2, O) + o;
-      buf_store_t<T>(rP, e, mx);
+      store_relu<T, RELU>(rP, (uint32_t)e * (uint32_t)sizeof(T), 0, mx);
       __builtin_amdgcn_raw_buffer_store_b8((uint8_t)am, rAM, e, 0, 0);
     } else {
       const int nv = min(4, M - mb);
@@ -1867,11 +1981,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
   const int m0 = tm * BM, n0 = tn * BN;
 
-  f32x4 acc[TL::FM][TL::FN];
-#pragma unroll
-  for (int i = 0; i < TL::FM; ++i)
-#pragma unroll
-    for (int j = 0; j < TL::FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  using L = Acc16<T, BM, BN, BK, 4>;
+  typename L::Acc acc;
+  L::zero(acc);
 
   Im2colLoader<T, BM, BK> la;
   la.init(p, m0);
@@ -1879,7 +1991,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
   lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0, p.K);
   mma_loop<T, BM, BN, BK>(la, lb, 0, (p.K + BK - 1) / BK, (T*)smem, acc);
 
-  conv_fwd_epilogue<T, Acc16<T, BM, BN, BK, 4>>(p, m0, n0, acc);
+  conv_fwd_epilogue<T, L>(p, m0, n0, acc);
 }
 
 template <typename T, int BM, int BN, int BK>
@@ -1961,7 +2073,7 @@ struct TapRowLoader {
 // offsets: the image's base kept as a running sum, rows and columns by 24-bit
 // multiplies (rows of under 2^24 elements, tensors of under 2^31 bytes).
 template <typename T, bool DGRAD, int NT = 256>
-__device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, int y0, int c0, int cbw) {
+__device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, int y0, int c0, int cbw, float rc_cpp) {
   // four loads in flight per thread (six or eight measured no faster for
   // the data gradient's larger blocks)
   constexpr int VEC = TT<T>::VEC, UNR = 4;
@@ -1981,9 +2093,9 @@ __device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, i
   const uint8_t* gam = p.gam;
   // this thread's first element
   int chi, rem, hcol;
-  const int pos = SmallDiv(cpp).qr(threadIdx.x, chi);
-  int img = SmallDiv(plane).qr(pos, rem);
-  int hrow = SmallDiv(hc).qr(rem, hcol), dst = pos * cs + chi * VEC;
+  const int pos = SmallDiv(cpp, rc_cpp).qr(threadIdx.x, chi);
+  int img = SmallDiv(plane, p.rc_plane).qr(pos, rem);
+  int hrow = SmallDiv(hc, p.rc_hc).qr(rem, hcol), dst = pos * cs + chi * VEC;
   unsigned nb = (unsigned)(img0 + img) * IMG;
   while (img < imgs) {
     u32x4 v[UNR];
@@ -2126,7 +2238,7 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
   {
     const bool wo = !DGRAD && p.pool;  // window order: r = 4 * window + (dy, dx)
     const int per_row = wo ? SW >> 1 : SW, per_img = wo ? (p.tr >> 1) * per_row : p.tr * SW;
-    const SmallDiv dimg(per_img), drow(per_row);
+    const SmallDiv dimg(per_img, p.rc_img), drow(per_row, p.rc_row);
     const int hr = p.hr, hc = p.hc, cs = p.cs;
 #pragma unroll
     for (int i = 0; i < L::FM; ++i) {
@@ -2144,10 +2256,10 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
   TapRowLoader<T, BN, BK, NT> lb;
   lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0);
   const int KH = p.KH, Cin = DGRAD ? p.O : p.C, cq = threadIdx.x % CPB, hc = p.hc, cs = p.cs;
-  const SmallDiv dkh(KH);
+  const SmallDiv dkh(KH, p.rc_kh);
   for (int c0 = 0; c0 < Cin; c0 += p.cb) {
     const int cbw = min(p.cb, Cin - c0), cpt = cbw / VEC, nq = KH * KH * cpt;
-    const SmallDiv dcpt(cpt);
+    const SmallDiv dcpt(cpt, c0 + p.cb >= Cin ? p.rc_cpt_last : p.rc_cpt);
     // the weights of k-block 0 first (column computed directly), so their
     // loads overlap the staging of the operand rows
     if (cq < nq) {
@@ -2164,7 +2276,7 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
       qa[q] = (DGRAD ? (KH - 1 - u) * hc + (KH - 1 - v) : u * hc + v) * cs + ch;
       qb[q] = tap * Cin + c0 + ch;  // fwd: W[o][(tap, c)]; dgrad: WT[c][(tap, o)]
     }
-    stage_halo<T, DGRAD, NT>(p, sH, img0, y0, c0, cbw);
+    stage_halo<T, DGRAD, NT>(p, sH, img0, y0, c0, cbw, dcpt.r);
     lb.store(sB);
     __syncthreads();
     const int nkb = (nq + CPB - 1) / CPB;

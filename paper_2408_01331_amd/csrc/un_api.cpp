@@ -627,6 +627,19 @@ static bool try_halo(ConvProb& p, bool bf, bool dgrad, int BM, int BN) {
   p.cs = cs;
   p.bm = BM;
   p.bn = BN;
+  // the tile's divisors (the same definitions as the kernel's) and their
+  // reciprocals, rounded once here instead of by every workgroup
+  const bool wo = !dgrad && p.pool;  // window-ordered rows
+  const int per_row = wo ? SW / 2 : SW, per_img = wo ? (tr / 2) * per_row : tr * SW;
+  const int cbw_last = Cin - ((Cin - 1) / cb) * cb;
+  auto rc = [](int d) { return 1.0f / (float)d; };
+  p.rc_img = rc(per_img);
+  p.rc_row = rc(per_row);
+  p.rc_kh = rc(p.KH);
+  p.rc_cpt = rc(cb / VEC);
+  p.rc_cpt_last = rc(cbw_last / VEC);
+  p.rc_plane = rc(hr * hc);
+  p.rc_hc = rc(hc);
   return true;
 }
 
