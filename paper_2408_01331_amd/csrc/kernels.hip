@@ -2037,7 +2037,7 @@ struct TapRowLoader {
                 "chunks must spread evenly over whole waves");
   __amdgpu_buffer_rsrc_t rsrc;
   int rowoff[NV];
-  u32x4 r[NV];
+  u32x4 r[2][NV];  // two k-blocks in flight (register slots 0 and 1)
   __device__ __forceinline__ bool active() const { return !PART || (int)threadIdx.x < CHUNKS; }
   __device__ __forceinline__ void init(const T* base, int64_t ld, int rows_valid) {
     rsrc = make_rsrc(base, (int64_t)rows_valid * ld * (int64_t)sizeof(T));
@@ -2045,19 +2045,21 @@ struct TapRowLoader {
     for (int s = 0; s < NV; ++s) rowoff[s] = (int)((threadIdx.x + NT * s) / CPB) * (int)ld * (int)sizeof(T);
   }
   // col: weight column of this thread's chunk, or -1 for a chunk past the block's end
+  template <int S>
   __device__ __forceinline__ void load(int col) {
     if (!active()) return;
 #pragma unroll
     for (int s = 0; s < NV; ++s)
-      r[s] = col < 0 ? zero4()
-                     : __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, rowoff[s] + col * (int)sizeof(T), 0, 0));
+      r[S][s] = col < 0 ? zero4()
+                        : __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, rowoff[s] + col * (int)sizeof(T), 0, 0));
   }
+  template <int S>
   __device__ __forceinline__ void store(T* sm) const {
     if (!active()) return;
 #pragma unroll
     for (int s = 0; s < NV; ++s) {
       const int v = threadIdx.x + NT * s;
-      *(u32x4*)(sm + (v / CPB) * LDK + (v % CPB) * VEC) = r[s];
+      *(u32x4*)(sm + (v / CPB) * LDK + (v % CPB) * VEC) = r[S][s];
     }
   }
 };
@@ -2069,14 +2071,18 @@ struct TapRowLoader {
 // gradient G and the window argmax.
 // Element e = (position, 16-byte chunk) of the staged block; a thread takes
 // e = tid, tid + NT, ... and steps its (chunk, column, row, image) by the
-// uniform decomposition of NT with carries (no per-element division). Source
+// uniform decomposition of NT with carries (no per-element division; when
+// the chunks per position divide NT a thread's chunk never changes). Source
 // offsets: the image's base kept as a running sum, rows and columns by 24-bit
 // multiplies (rows of under 2^24 elements, tensors of under 2^31 bytes).
+// Every element is loaded through buffer resources: one outside the image
+// reads at an offset past the range, which returns zero.
 template <typename T, bool DGRAD, int NT = 256>
 __device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, int y0, int c0, int cbw, float rc_cpp) {
   // four loads in flight per thread (six or eight measured no faster for
   // the data gradient's larger blocks)
   constexpr int VEC = TT<T>::VEC, UNR = 4;
+  constexpr uint32_t OOB = 0x80000000u;
   const int cpp = cbw / VEC, hc = p.hc, hr = p.hr, cs = p.cs, imgs = p.imgs, Nb = p.Nb, plane = hr * hc;
   const int dpos = NT / cpp, dch = NT - dpos * cpp, dimg = dpos / plane, dr = dpos - dimg * plane;
   const int dhr = dr / hc, dhc = dr - dhr * hc;
@@ -2089,41 +2095,42 @@ __device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, i
   const int ROW = (DGRAD ? (pool ? p.PW : p.OW) : p.W) * CH;
   const unsigned IMG = (unsigned)(DGRAD ? (pool ? p.PH : p.OH) : p.H) * (unsigned)ROW;
   const int ybase = DGRAD ? y0 + p.pad - (p.KH - 1) : y0 - p.pad, xbase = DGRAD ? p.pad - (p.KH - 1) : -p.pad;
-  const gptr<const T> src = G((const T*)(DGRAD ? p.G : p.X));
-  const uint8_t* gam = p.gam;
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(DGRAD ? p.G : p.X, (int64_t)Nb * IMG * (int64_t)sizeof(T));
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.gam, pool ? (int64_t)Nb * IMG : 0);
   // this thread's first element
   int chi, rem, hcol;
   const int pos = SmallDiv(cpp, rc_cpp).qr(threadIdx.x, chi);
   int img = SmallDiv(plane, p.rc_plane).qr(pos, rem);
   int hrow = SmallDiv(hc, p.rc_hc).qr(rem, hcol), dst = pos * cs + chi * VEC;
   unsigned nb = (unsigned)(img0 + img) * IMG;
-  while (img < imgs) {
-    u32x4 v[UNR];
-    int dd[UNR];
+  auto run = [&](auto fixed_chunk) {
+    constexpr bool FIX = decltype(fixed_chunk)::value;
+    const unsigned cofs = (unsigned)(c0 + chi * VEC);
+    while (img < imgs) {
+      u32x4 v[UNR];
+      int dd[UNR];
 #pragma unroll
-    for (int k = 0; k < UNR; ++k) {
-      v[k] = zero4();
-      dd[k] = -1;
-      if (img < imgs) {
-        dd[k] = dst;
+      for (int k = 0; k < UNR; ++k) {
+        dd[k] = img < imgs ? dst : -1;
         const int y = ybase + hrow, x = xbase + hcol;
-        if (img0 + img < Nb && (unsigned)y < (unsigned)YL && (unsigned)x < (unsigned)XL) {
-          const unsigned off = nb + __umul24((unsigned)(y >> sh), (unsigned)ROW) + __umul24((unsigned)(x >> sh), (unsigned)CH) +
-                               (unsigned)(c0 + chi * VEC);
-          v[k] = *(gptr<const u32x4>)(src + off);
-          if (pool) select_am<T>(v[k], load_am<T>(gam + off), ((y & 1) << 1) | (x & 1));
-        }
+        const bool in = img < imgs && img0 + img < Nb && (unsigned)y < (unsigned)YL && (unsigned)x < (unsigned)XL;
+        const unsigned off = nb + __umul24((unsigned)(y >> sh), (unsigned)ROW) +
+                             __umul24((unsigned)(x >> sh), (unsigned)CH) + (FIX ? cofs : (unsigned)(c0 + chi * VEC));
+        v[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? off * (unsigned)sizeof(T) : OOB, 0, 0));
+        if (pool) select_am<T>(v[k], load_am_buf<T>(ra, in ? off : OOB), ((y & 1) << 1) | (x & 1));
         // the next element, NT on
-        chi += dch;
         dst += dst_step;
         hcol += dhc;
         hrow += dhr;
         img += dimg;
         nb += (unsigned)dimg * IMG;
-        if (chi >= cpp) {
-          chi -= cpp;
-          dst += dst_wrap;
-          ++hcol;
+        if constexpr (!FIX) {
+          chi += dch;
+          if (chi >= cpp) {
+            chi -= cpp;
+            dst += dst_wrap;
+            ++hcol;
+          }
         }
         if (hcol >= hc) {
           hcol -= hc;
@@ -2135,34 +2142,43 @@ __device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, i
           nb += IMG;
         }
       }
-    }
 #pragma unroll
-    for (int k = 0; k < UNR; ++k)
-      if (dd[k] >= 0) *(u32x4*)(sH + dd[k]) = v[k];
-  }
+      for (int k = 0; k < UNR; ++k)
+        if (dd[k] >= 0) *(u32x4*)(sH + dd[k]) = v[k];
+    }
+  };
+  if (dch == 0) run(std::true_type{});
+  else run(std::false_type{});
 }
 
 // One k-block of a halo tile: A rows read from the staged halo at the lane's
 // row base plus the chunk's tap offset, B from the weight stage. Chunks at or
-// past nq have zero weights; their A reads are clamped to a valid chunk.
+// past nq have zero weights.
 // bf16: 32x32x16 MFMA blocks (Acc32); a k-step of 16 spans two chunks, lane
-// half h = lane / 32 supplying chunk qs + h.
+// half h = lane / 32 supplying chunk qs + h. Row bases and tap offsets are in
+// bytes; the offsets of k-block kb are laid out as qa[8 kb + 4 h + s] = the
+// offset of chunk 8 kb + 2 s + h (clamped to the last chunk), so a lane reads
+// the four it needs at once.
 template <int BM, int BN, int BK, int NW>
 __device__ __forceinline__ void mma_halo(const bf16_t* sH, const int (&hbase)[Acc32<BM, BN, NW>::FM], const int* qa,
                                          int q0, int nq, const bf16_t* sB, typename Acc32<BM, BN, NW>::Acc& acc) {
   using L = Acc32<BM, BN, NW>;
   constexpr int LDK = Tile<bf16_t, BM, BN, BK, NW>::LDK;
+  static_assert(BK == 64, "eight chunks per k-block, four k-steps");
   const int lane = threadIdx.x & 63, h = lane >> 5;
-  const bf16_t* sb = sB + (L::wave_n() + (lane & 31)) * LDK + 8 * h;
+  const char* hp[L::FM];
 #pragma unroll
-  for (int kk = 0; kk < BK; kk += 16) {
-    const int qs = q0 + kk / 8;
-    if (qs < nq) {
-      const int ao = qa[min(qs + h, nq - 1)];
-      const bf16x8 b = __builtin_bit_cast(bf16x8, *(const u32x4*)(sb + kk));
+  for (int i = 0; i < L::FM; ++i) hp[i] = (const char*)sH + hbase[i];
+  const bf16_t* sb = sB + (L::wave_n() + (lane & 31)) * LDK + 8 * h;
+  const u32x4 t = *(const u32x4*)(qa + q0 + 4 * h);
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    if (q0 + 2 * s < nq) {
+      const int ao = (int)t[s];
+      const bf16x8 b = __builtin_bit_cast(bf16x8, *(const u32x4*)(sb + 16 * s));
 #pragma unroll
       for (int i = 0; i < L::FM; ++i) {
-        const bf16x8 a = __builtin_bit_cast(bf16x8, *(const u32x4*)(sH + hbase[i] + ao));
+        const bf16x8 a = __builtin_bit_cast(bf16x8, *(const u32x4*)(hp[i] + ao));
         acc[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc[i], 0, 0, 0);
       }
     }
@@ -2246,7 +2262,7 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
       int rem, col;
       const int img = dimg.qr(u, rem), row = drow.qr(rem, col);
       const int y = wo ? 2 * row + (d >> 1) : row, x = wo ? 2 * col + (d & 1) : col;
-      hbase[i] = ((img * hr + y) * hc + x) * cs;
+      hbase[i] = ((img * hr + y) * hc + x) * cs * (sizeof(T) == 2 ? 2 : 1);  // bf16: bytes
     }
   }
 
@@ -2260,37 +2276,67 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
   for (int c0 = 0; c0 < Cin; c0 += p.cb) {
     const int cbw = min(p.cb, Cin - c0), cpt = cbw / VEC, nq = KH * KH * cpt;
     const SmallDiv dcpt(cpt, c0 + p.cb >= Cin ? p.rc_cpt_last : p.rc_cpt);
-    // the weights of k-block 0 first (column computed directly), so their
-    // loads overlap the staging of the operand rows
-    if (cq < nq) {
+    // the weights of k-blocks 0 and 1 first (columns computed directly), so
+    // their loads overlap the staging of the operand rows; k-block kb sits in
+    // register slot kb & 1 and LDS buffer kb & 1
+    auto col_of = [&](int q) {
       int cr;
-      const int tap = dcpt.qr(cq, cr);
-      lb.load(tap * Cin + c0 + cr * VEC);
-    } else {
-      lb.load(-1);
-    }
+      const int tap = dcpt.qr(q, cr);
+      return q < nq ? tap * Cin + c0 + cr * VEC : -1;
+    };
+    lb.template load<0>(col_of(cq));
+    lb.template load<1>(col_of(CPB + cq));
     __syncthreads();  // the previous channel block's halo, tables and weight stages are no longer read
-    for (int q = threadIdx.x; q < nq; q += NT) {
+    // qa: the halo offset of a chunk's tap and channels (bf16: in bytes, in
+    // the k-block layout of mma_halo, padded to whole k-blocks); qb: its
+    // weight column (fwd: W[o][(tap, c)]; dgrad: WT[c][(tap, o)])
+    auto tap_off = [&](int q, int& col) {
       int cr, v;
       const int tap = dcpt.qr(q, cr), ch = cr * VEC, u = dkh.qr(tap, v);
-      qa[q] = (DGRAD ? (KH - 1 - u) * hc + (KH - 1 - v) : u * hc + v) * cs + ch;
-      qb[q] = tap * Cin + c0 + ch;  // fwd: W[o][(tap, c)]; dgrad: WT[c][(tap, o)]
+      col = tap * Cin + c0 + ch;
+      return (DGRAD ? (KH - 1 - u) * hc + (KH - 1 - v) : u * hc + v) * cs + ch;
+    };
+    if constexpr (sizeof(T) == 2) {
+      static_assert(CPB == 8, "bf16 table layout");
+      const int nqa = (nq + 7) & ~7;
+      for (int e = threadIdx.x; e < nqa; e += NT) {
+        int col;
+        qa[e] = 2 * tap_off(min((e & ~7) + 2 * (e & 3) + ((e >> 2) & 1), nq - 1), col);
+        if (e < nq) {
+          tap_off(e, col);
+          qb[e] = col;
+        }
+      }
+    } else {
+      for (int q = threadIdx.x; q < nq; q += NT) {
+        int col;
+        qa[q] = tap_off(q, col);
+        qb[q] = col;
+      }
     }
     stage_halo<T, DGRAD, NT>(p, sH, img0, y0, c0, cbw, dcpt.r);
-    lb.store(sB);
+    lb.template store<0>(sB);
     __syncthreads();
     const int nkb = (nq + CPB - 1) / CPB;
-    for (int kb = 0; kb < nkb; ++kb) {
-      const int cur = kb & 1;
-      const bool more = kb + 1 < nkb;
-      if (more) {
-        const int q = (kb + 1) * CPB + cq;
-        lb.load(q < nq ? qb[q] : -1);
+    // iteration kb (P = kb & 1): load k-block kb + 2 into slot P (its k-block
+    // kb is in LDS already), run k-block kb from LDS buffer P, move k-block
+    // kb + 1 from slot P ^ 1 to LDS buffer P ^ 1 (last read in iteration kb - 1)
+    auto step = [&](auto par, int kb) {
+      constexpr int P = decltype(par)::value;
+      if (kb + 2 < nkb) {
+        const int q = (kb + 2) * CPB + cq;
+        lb.template load<P>(q < nq ? qb[q] : -1);
       }
-      mma_halo<BM, BN, BK, NW>(sH, hbase, qa, kb * CPB, nq, sB + cur * TL::B_ELEMS, acc);
-      if (more) lb.store(sB + (cur ^ 1) * TL::B_ELEMS);
+      mma_halo<BM, BN, BK, NW>(sH, hbase, qa, kb * CPB, nq, sB + P * TL::B_ELEMS, acc);
+      if (kb + 1 < nkb) lb.template store<P ^ 1>(sB + (P ^ 1) * TL::B_ELEMS);
       __syncthreads();
+    };
+    int kb = 0;
+    for (; kb + 1 < nkb; kb += 2) {
+      step(std::integral_constant<int, 0>{}, kb);
+      step(std::integral_constant<int, 1>{}, kb + 1);
     }
+    if (kb < nkb) step(std::integral_constant<int, 0>{}, kb);
   }
   if constexpr (DGRAD) conv_dgrad_epilogue<T, BM, BN, L>(p, m0, n0, acc, smem);
   else conv_fwd_epilogue<T, L>(p, m0, n0, acc);
@@ -2389,26 +2435,30 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2))) void c
 // quarter-rate). Offsets are 32-bit: every conv tensor is under 2^31 bytes.
 template <int ROWS, int BK, int NT, int SLOTS, int PAD, bool POOL>
 struct ConvKA {
-  static constexpr int VEC = 8, CPR = ROWS / VEC, LDR = ROWS + PAD;
-  static_assert(BK * CPR == NT, "one chunk per thread and k-block");
-  static_assert(BK % 4 == 0, "k-blocks hold whole windows");
+  static constexpr int VEC = 8, CPR = ROWS / VEC, LDR = ROWS + PAD, NV = BK * CPR / NT;
+  static_assert(NV >= 1 && BK * CPR == NV * NT, "whole chunks per thread and k-block");
+  static_assert(BK % 4 == 0 && (NT / CPR) % 4 == 0, "k-blocks hold whole windows; a thread's chunks share one window position");
   __amdgpu_buffer_rsrc_t rs, rs_am;
-  uint32_t offb, offa, stepb, stepa;  // byte offsets of the chunk in G and in the argmax bytes, and their steps
+  uint32_t offb, offa, stepb, stepa;  // byte offsets of chunk 0 in G and in the argmax bytes, and their steps
+  uint32_t sb1, sa1;                  // from chunk s to chunk s + 1 (NT / CPR pixels on)
   int sm_off;
-  u32x4 r[SLOTS];
-  uint64_t am[SLOTS];
-  // Channels o >= O are read without a range test: they feed accumulator rows
-  // that are never stored. Pixels past the last one lie past both buffers'
-  // ranges and read zero.
+  u32x4 r[SLOTS][NV];
+  uint64_t am[SLOTS][NV];
+  // Chunk s of a thread: pixel k + s * (NT / CPR) of the block. Channels
+  // o >= O are read without a range test: they feed accumulator rows that
+  // are never stored. Pixels past the last one lie past both buffers' ranges
+  // and read zero.
   __device__ __forceinline__ void init(const ConvProb& p, int o0, int kb0) {
     const int k = threadIdx.x / CPR, o = o0 + (threadIdx.x % CPR) * VEC;
     const int pix = kb0 * BK + k;
-    const uint32_t e = (uint32_t)((POOL ? pix >> 2 : pix) * p.O + o);  // element offset of this chunk in G
-    const uint32_t step = (uint32_t)((POOL ? BK / 4 : BK) * p.O);
+    const uint32_t e = (uint32_t)((POOL ? pix >> 2 : pix) * p.O + o);  // element offset of chunk 0 in G
+    const uint32_t step = (uint32_t)((POOL ? BK / 4 : BK) * p.O), s1 = (uint32_t)((POOL ? NT / CPR / 4 : NT / CPR) * p.O);
     offb = 2 * e;
     offa = e;
     stepb = 2 * step;
     stepa = step;
+    sb1 = 2 * s1;
+    sa1 = s1;
     sm_off = kmaj_bf16<LDR>(k, (threadIdx.x % CPR) * VEC);
     const int64_t rows = POOL ? (int64_t)p.Nb * p.PH * p.PW : (int64_t)p.Nb * p.OH * p.OW;
     rs = make_rsrc(p.G, rows * p.O * (int64_t)sizeof(bf16_t));
@@ -2417,16 +2467,22 @@ struct ConvKA {
   // the next k-block (the loop issues blocks in order, one call each)
   template <int S>
   __device__ __forceinline__ void load(int) {
-    r[S] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, offb, 0, 0));
-    if constexpr (POOL) am[S] = load_am_buf<bf16_t>(rs_am, offa);
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      r[S][s] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, offb + s * sb1, 0, 0));
+      if constexpr (POOL) am[S][s] = load_am_buf<bf16_t>(rs_am, offa + s * sa1);
+    }
     offb += stepb;
     offa += stepa;
   }
   template <int S>
   __device__ __forceinline__ void store(bf16_t* sm) const {
-    u32x4 v = r[S];
-    if constexpr (POOL) select_am<bf16_t>(v, am[S], (threadIdx.x / CPR) & 3);
-    *(u32x4*)(sm + sm_off) = v;
+#pragma unroll
+    for (int s = 0; s < NV; ++s) {
+      u32x4 v = r[S][s];
+      if constexpr (POOL) select_am<bf16_t>(v, am[S][s], (threadIdx.x / CPR) & 3);
+      *(u32x4*)(sm + sm_off + (s * (NT / CPR)) * LDR) = v;
+    }
   }
 };
 
