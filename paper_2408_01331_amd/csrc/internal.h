@@ -224,6 +224,13 @@ struct CeProb {
   int32_t nchunks;            // loss partials of this model (row chunks or GEMM m-tiles)
   int32_t B;                  // the model's batch (its input group's)
   int32_t lab_shared, lab_own;  // its labels: labels + lab_shared (group row) or + lab_own (own row)
+  // split-K logits (nparts > 0): the logits are the partials parts[s][b][c]
+  // (row stride ldp, nparts slices of B rows) added in split order, plus
+  // bias[c]; the row pass writes them to `logits` first. Else null / 0.
+  const float* parts;
+  int64_t ldp;
+  int32_t nparts;
+  const float* bias;
 };
 
 // ---------------------------------------------------------------------------
@@ -287,8 +294,10 @@ hipError_t launch_attn(bool bf16, bool bwd, const AttnProb* probs, const int32_t
 // into the logits GEMM); the loss of every one of the nprobs is finished.
 // Partials of model m are at partial + m * pstride; maxB is the largest
 // batch of the problems (each has its own, CeProb::B).
+// Split-K logit partials (CeProb::parts) are read at parts + wsoff bytes.
 hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, int nrows, const int32_t* labels,
-                     bool per_model_labels, int maxB, float* partial, int pstride, float* losses, hipStream_t s);
+                     bool per_model_labels, int maxB, float* partial, int pstride, float* losses, int64_t wsoff,
+                     hipStream_t s);
 // The launch covers tiles [blk0, blk0 + ntiles) of the tile table.
 hipError_t launch_sgd(bool bf16, const SgdTensor* t, const int32_t* tile_tensor, int blk0, int ntiles, float lr,
                       bool use_grad, hipStream_t s);

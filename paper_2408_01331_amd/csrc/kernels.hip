@@ -1458,10 +1458,12 @@ void gemm_kernel(const GemmProb* __restrict__ probs,
   const int ns = p.nsplit;
   f32x4 w0[NCH];  // master weights of the fused update (weight gradient only)
   if constexpr (!BWD) {
+    // row-major operands from column k0 on (a split's chunk, else 0), kc of them
+    const int64_t k0 = (int64_t)kb0 * BK;
     RowLoader<T, BM, BK, NT, D> la;
     RowLoader<T, BN, BK, NT, D> lb;
-    la.init((const T*)p.A + (int64_t)m0 * p.lda, p.lda, p.M - m0, p.K);
-    lb.init((const T*)p.B + (int64_t)n0 * p.ldb, p.ldb, p.N - n0, p.K);
+    la.init((const T*)p.A + (int64_t)m0 * p.lda + k0, p.lda, p.M - m0, kc);
+    lb.init((const T*)p.B + (int64_t)n0 * p.ldb + k0, p.ldb, p.N - n0, kc);
     gemm_loop<T, BM, BN, BK, D, MM, OP_ROW, OP_ROW>(la, lb, nkb, (T*)smem, acc);
   } else if (p.amode == OP_ROW) {
     // data gradient: A = G row-major, B = W k-major (rows k = output units)
@@ -2753,7 +2755,8 @@ template <typename T>
 __global__ __launch_bounds__(CE_ROWS * CE_LANES) void ce_rows_kernel(const CeProb* __restrict__ probs,
                                                                      const int32_t* __restrict__ labels,
                                                                      int per_model_labels,
-                                                                     float* __restrict__ partial, int pstride) {
+                                                                     float* __restrict__ partial, int pstride,
+                                                                     int64_t wsoff) {
   __shared__ float rowloss[CE_ROWS];
   const CeProb& p = probs[blockIdx.y];
   const int B = p.B;
@@ -2763,7 +2766,18 @@ __global__ __launch_bounds__(CE_ROWS * CE_LANES) void ce_rows_kernel(const CePro
   const int b = blockIdx.x * CE_ROWS + rl;
   const int C = p.C;
   const bool valid = b < B;
-  const float* z = p.logits + (int64_t)(valid ? b : 0) * p.ldl;
+  float* zw = (float*)p.logits + (int64_t)(valid ? b : 0) * p.ldl;
+  if (valid && p.nparts > 0) {
+    // split-K logits: the chunks' partial sums in split order, then the bias
+    const float* pp = (const float*)((const char*)p.parts + wsoff) + (int64_t)b * p.ldp;
+    const int64_t ps = (int64_t)B * p.ldp;
+    for (int c = sub; c < C; c += CE_LANES) {
+      float t = pp[c];
+      for (int k = 1; k < p.nparts; ++k) t += pp[k * ps + c];
+      zw[c] = t + p.bias[c];
+    }
+  }
+  const float* z = zw;
   float mx = -INFINITY;
   if (valid)
     for (int c = sub; c < C; c += CE_LANES) mx = fmaxf(mx, z[c]);
@@ -3242,16 +3256,17 @@ hipError_t launch_attn(bool bf16, bool bwd, const AttnProb* probs, const int32_t
 }
 
 hipError_t launch_ce(bool bf16, const CeProb* probs, int nprobs, int nrows, const int32_t* labels,
-                     bool per_model_labels, int maxB, float* partial, int pstride, float* losses, hipStream_t s) {
+                     bool per_model_labels, int maxB, float* partial, int pstride, float* losses, int64_t wsoff,
+                     hipStream_t s) {
   if (nprobs <= 0) return hipSuccess;
   const int nchunks = (maxB + CE_ROWS - 1) / CE_ROWS;
   if (nrows > 0) {
     if (bf16)
       hipLaunchKernelGGL(ce_rows_kernel<bf16_t>, dim3(nchunks, nrows), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels,
-                         (int)per_model_labels, partial, pstride);
+                         (int)per_model_labels, partial, pstride, wsoff);
     else
       hipLaunchKernelGGL(ce_rows_kernel<float>, dim3(nchunks, nrows), dim3(CE_ROWS * CE_LANES), 0, s, probs, labels,
-                         (int)per_model_labels, partial, pstride);
+                         (int)per_model_labels, partial, pstride, wsoff);
   }
   hipLaunchKernelGGL(ce_finish_kernel, dim3((nprobs + 63) / 64), dim3(64), 0, s, probs, partial, pstride, nprobs,
                      losses);

@@ -69,6 +69,11 @@ struct Block {
   size_t ws = NONE, ws_size = 0;
   int64_t ldws = 0;
   int splits = 1, kchunk = 0;
+  // split-K of a long logits product (forward): its partials, summed by the
+  // softmax-CE row pass
+  size_t fws = NONE, fws_size = 0;
+  int64_t fldws = 0;
+  int fsplits = 0, fkchunk = 0;
   // output geometry
   int out_elems_per_sample() const { return kind == 0 ? N : (pool ? PH * PW * O : OH * OW * O); }
 };
@@ -707,7 +712,7 @@ static void build_tables(un_ctx* c, Tables& T) {
   // softmax-CE is fused into a model's logits GEMM when a tile holds whole
   // rows of logits; the loss partials of model m start at m * ce_pstride
   const int ce_pstride = cdiv(c->maxB, CE_ROWS);
-  auto ce_fused = [&](const Block& b) { return b.kind == 0 && b.N <= GBN; };
+  auto ce_fused = [&](const Block& b) { return b.kind == 0 && b.N <= GBN && b.fsplits == 0; };
 
   // Problems of one launch are ordered longest-K first (their tiles are the
   // longest-running), so the ragged tail of a level is made of short tiles.
@@ -718,9 +723,9 @@ static void build_tables(un_ctx* c, Tables& T) {
     const int BKg = bf ? GEMM_BK_BF16 : GEMM_BK_F32;
     auto klen = [&](const GemmProb& x) { return x.epi == EPI_WPART ? std::min(x.K, x.kchunk * BKg) : x.K; };
     std::stable_sort(ps.begin(), ps.end(), [&](const GemmProb& x, const GemmProb& y) { return klen(x) > klen(y); });
-    // Launch order = problem order (longest K first), tiles m-fastest, then
-    // swizzled for the XCDs: the tiles are cut into runs of up to 8 that share
-    // a B tile (one column of m-tiles, or a few short columns), and every 8
+    // Launch order = problem order (longest K first), then swizzled for the
+    // XCDs: the tiles are cut into runs of up to 8 that share A and B tiles
+    // (4 m-tiles x 2 n-tiles, or short columns side by side), and every 8
     // consecutive runs are interleaved so that run r lands on XCD r % 8 with
     // its members 8 launch slots apart - they run together on one XCD and read
     // their shared tiles from its L2 once - while the order stays
@@ -752,17 +757,21 @@ static void build_tables(un_ctx* c, Tables& T) {
               }
             }
         } else {
-          // a column shorter than 8 m-tiles is joined with its neighbours up
-          // to about 8 tiles per run, so that the run's A tiles are shared as
-          // well as its B tiles
-          const int rl = std::min(tm, 8), cpr = tm < 8 ? std::max(1, 8 / tm) : 1;
-          for (int t = 0; t < tm * tn; ++t) {
-            nat.push_back((int32_t)k);
-            nat.push_back(base + t);
-            const int col = t / tm, row = t - col * tm;
-            if (row % rl == 0 && col % cpr == 0) ++runs;
-            run_of.push_back(runs - 1);
-          }
+          // runs of up to 8 tiles: 4 m-tiles x 2 n-tiles, or a shorter
+          // column with its neighbours. An A tile (128 x K) and a B tile
+          // (K x 128) are the same size, and a run of r x c tiles reads r + c
+          // of them: 4 x 2 reads 6 where a column of 8 reads 9
+          const int rl = std::min(tm, 4), cpr = std::max(1, 8 / rl);
+          for (int c0 = 0; c0 < tn; c0 += cpr)
+            for (int r0 = 0; r0 < tm; r0 += rl) {
+              ++runs;
+              for (int col = c0; col < std::min(tn, c0 + cpr); ++col)
+                for (int row = r0; row < std::min(tm, r0 + rl); ++row) {
+                  nat.push_back((int32_t)k);
+                  nat.push_back(base + col * tm + row);
+                  run_of.push_back(runs - 1);
+                }
+            }
         }
       }
     }
@@ -964,6 +973,14 @@ static void build_tables(un_ctx* c, Tables& T) {
           p.R = ptr(rb.X);
           p.ldr = rb.ldx;
         }
+        if (b.last && b.fsplits > 0) {
+          // split-K logits: the partial sums of each k-chunk (no bias)
+          p.epi = EPI_WPART;
+          p.splits = b.fsplits;
+          p.kchunk = b.fkchunk;
+          p.ws = (float*)ptr(b.fws);
+          p.ldws = b.fldws;
+        }
         if (b.last && ce_fused(b)) {
           // softmax-CE in the logits GEMM's epilogue: it writes dL/dz
           p.C = ptr(b.G);
@@ -1030,6 +1047,12 @@ static void build_tables(un_ctx* c, Tables& T) {
       p.B = g.B;
       p.lab_shared = (int32_t)g.lab_shared;
       p.lab_own = (int32_t)m.lab_own;
+      if (b.fsplits > 0) {
+        p.parts = (const float*)ptr(b.fws);
+        p.ldp = b.fldws;
+        p.nparts = b.fsplits;
+        p.bias = (const float*)ptr(b.b32);
+      }
       ces.push_back(p);
       if (pass == 0) ++ce_rows;
     }
@@ -1037,7 +1060,8 @@ static void build_tables(un_ctx* c, Tables& T) {
     size_t po = put(ces.data(), ces.size() * sizeof(CeProb));
     for (size_t k = 0; k < ces.size(); ++k) {
       size_t b0 = po + k * sizeof(CeProb);
-      for (size_t f : {offsetof(CeProb, logits), offsetof(CeProb, G)}) fix.push_back(b0 + f);
+      for (size_t f : {offsetof(CeProb, logits), offsetof(CeProb, G), offsetof(CeProb, parts), offsetof(CeProb, bias)})
+        fix.push_back(b0 + f);
     }
     T.ce = Launch{5, UN_K_CE, po, NONE, (int)ces.size()};
     T.ce.mode = ce_rows;
@@ -1479,6 +1503,22 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
           if (b.last) {
             b.ldy = rup(b.N, 8);
             b.Y = A.take((size_t)R * b.ldy * 4);  // fp32 logits
+            // split-K of a long logits contraction with few classes: chunks
+            // of at most 8 (fp32: 16) k-blocks, whose partials go to the
+            // workspace; the softmax-CE row pass adds them in split order,
+            // then the bias. A few tiles with a long K would otherwise run
+            // alone at the end of their level; the row pass's work grows with
+            // classes x splits, so many classes keep the fused CE. Depends
+            // only on this block's shape.
+            const int BKf = bf ? GEMM_BK_BF16 : GEMM_BK_F32, FKCH = bf ? 8 : 16;
+            const int nkbf = cdiv(b.K, BKf);
+            if (nkbf > FKCH && b.N <= 32 && b.tokens == 1) {  // rows = samples (the row pass's layout)
+              b.fsplits = cdiv(nkbf, FKCH);
+              b.fkchunk = cdiv(nkbf, b.fsplits);
+              b.fsplits = cdiv(nkbf, b.fkchunk);
+              b.fldws = rup(b.N, 4);
+              b.fws_size = (size_t)b.fsplits * R * b.fldws * 4;  // placed in the workspace range below
+            }
           } else {
             b.ldy = rup(b.N, 8);
             b.Y = A.take((size_t)R * b.ldy * es);
@@ -1564,7 +1604,10 @@ static un_status plan_and_alloc(un_ctx* c, bool dry = false) {
   c->ce_partial = A.take(c->models.size() * (size_t)cdiv(c->maxB, CE_ROWS) * 4);
   for (auto& m : c->models)
     for (auto& b : m.blocks)
-      if (b.ws_size) b.ws = A.take(b.ws_size);
+      {
+        if (b.ws_size) b.ws = A.take(b.ws_size);
+        if (b.fws_size) b.fws = A.take(b.fws_size);
+      }
   c->ws_bytes = A.top - c->ws_lo;
 
   c->active.assign(c->models.size(), 1);
@@ -1771,7 +1814,7 @@ static hipError_t run_launch(un_ctx* c, const Launch& l, float lr) {
     case 5:
       e = launch_ce(c->bf16, c->at<CeProb>(l.probs), l.count, l.mode, c->at<int32_t>(c->ydev), c->labels_per_model,
                     c->maxB, (float*)((char*)c->at<float>(c->ce_partial) + c->wsoff), cdiv(c->maxB, CE_ROWS),
-                    c->at<float>(c->losses_dev), c->stream);
+                    c->at<float>(c->losses_dev), c->wsoff, c->stream);
       break;
     case 6:
       e = launch_sgd(c->bf16, c->at<SgdTensor>(l.probs), c->at<int32_t>(l.map), 0, l.count, lr, true, c->stream);

@@ -199,6 +199,38 @@ def test_split_k_weight_gradients(precision):
 
 
 @pytest.mark.parametrize("precision", ["f32", "bf16"])
+def test_split_k_logits(precision):
+    """A logits layer with a long contraction (more than 8 k-blocks of 64 in
+    bf16, 16 of 32 in fp32) and at most 32 classes is computed in chunks whose
+    partial sums the softmax-CE row pass adds in split order, then the bias.
+    K = 1100 leaves a ragged last chunk. Beside logits layers that are not
+    split: a short K (fused softmax-CE) and a long K with 150 classes (row
+    pass). Against the oracle, and bit for bit against each model trained
+    alone (those with the first model's class count: a workload draws labels
+    below it)."""
+    _need_gpu()
+    L, RELU = (lambda n: ("linear", n)), ("relu",)
+    specs = [
+        {"layers": [L(1100), RELU, L(10)], "num_classes": 10},
+        {"layers": [L(1100), RELU, L(30)], "num_classes": 30},
+        {"layers": [L(40), RELU, L(10)], "num_classes": 10},
+        {"layers": [L(10)], "num_classes": 10},
+        {"layers": [L(1100), RELU, L(150)], "num_classes": 150},
+    ]
+    wl = _custom(specs, 45, (72,), precision, lr=0.02)
+    m = list(range(wl.n_models))
+    _report(f"split_logits_{precision} 1 step", _step_vs_oracle(wl, m))
+    _report(f"split_logits_{precision} run", _run_vs_oracle(wl, m))
+    merged = run_gpu(wl, 2)
+    for i in (0, 2, 3):
+        alone = W.Workload("alone", 1, wl.batch, wl.in_shape, precision, [wl.specs[i]], wl.lr, 2, wl.seed)
+        solo = run_gpu(alone, 2, theta={0: theta0(wl, i)})
+        assert _bitwise_equal([merged[0][:, i]], [solo[0][:, 0]]), f"model {i}: losses"
+        for a, b in zip(merged[1][i] + merged[2][i], solo[1][0] + solo[2][0]):
+            assert _bitwise_equal(a, b), f"model {i}: parameters or gradients"
+
+
+@pytest.mark.parametrize("precision", ["f32", "bf16"])
 def test_softmax_ce_fused_and_row_pass(precision):
     """Class counts on both sides of one GEMM tile's width (bf16 128, fp32 64):
     the models whose classes fit get softmax-CE in their logits GEMM's
