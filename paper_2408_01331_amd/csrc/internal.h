@@ -117,6 +117,10 @@ struct ConvProb {
   int32_t tiles_m, tiles_n, splits, kchunk;
   int32_t halo, tr, imgs, hr, hc, cb, cs;  // halo tiling (see above)
   int32_t bm, bn;                          // halo tile shape
+  // forward halo passes with one channel block: consecutive m-tiles of one
+  // n-column per workgroup (weights and tap tables loaded once, the next
+  // tile's rows fetched during this tile's epilogue); else 1
+  int32_t mt;
   // fl(1/d) (correctly rounded) for the halo tile's small divisors, computed
   // once on the host: tile rows per image and per image row (pooled forward:
   // windows), KH, 16-byte chunks per position of a full and of the last
@@ -325,6 +329,10 @@ constexpr int CE_LANES = 8;           // lanes per row
 // LDS per workgroup: the double-buffered weight stage, two chunk tables of
 // HALO_QMAX ints, and the staged rows - halo_elems() elements.
 constexpr int HALO_QMAX = 256;
+// Threads of a halo workgroup (bf16: 8 waves, fp32: 4) and the 16-byte
+// chunks per thread that a multi-tile forward workgroup fetches ahead: its
+// staged rows must fit HALO_PF * threads chunks.
+constexpr int HALO_NT_BF16 = 512, HALO_NT_F32 = 256, HALO_PF = 4;
 constexpr int HALO_LDS_BF16 = 80 * 1024, HALO_LDS_F32 = 52 * 1024;  // two (bf16) / three (fp32) per CU
 constexpr int halo_elems(int es, int BN, int BK) {
   return ((es == 2 ? HALO_LDS_BF16 : HALO_LDS_F32) - 2 * HALO_QMAX * 4 - 2 * BN * (BK + 16 / es) * es) / es;

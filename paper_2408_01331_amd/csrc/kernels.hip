@@ -2066,91 +2066,170 @@ struct TapRowLoader {
   }
 };
 
+// The elements e = (position, 16-byte chunk) of a staged halo block that one
+// thread moves: e = tid, tid + NT, ... The thread steps its (chunk, column,
+// row, image) by the uniform decomposition of NT with carries (no per-element
+// division; when the chunks per position divide NT, FIX, a thread's chunk
+// never changes). Source offsets: the image's base kept as a running sum,
+// rows and columns by 24-bit multiplies (rows of under 2^24 elements, tensors
+// of under 2^31 bytes). Staged block: LDS [img][hr][hc][cs], channels
+// [c0, c0 + cbw) of the source. Forward: the conv input X. Data gradient: dZ,
+// expanded from the pooled gradient G and the window argmax.
+template <typename T, bool DGRAD, int NT>
+struct HaloWalk {
+  static constexpr int VEC = TT<T>::VEC;
+  int cpp, imgs, hc, hr, dch, dhc, dhr, dimg, dst_step, dst_wrap;
+  // source geometry: rows of ROW elements, images of IMG, channel stride CH;
+  // position (hrow, hcol) reads row ybase + hrow, column xbase + hcol
+  int YL, XL, ROW, CH, ybase, xbase, lastimg, c0;
+  unsigned IMG;
+  // this thread's element
+  int chi, hcol, hrow, img, dst;
+  unsigned nb;
+  __device__ __forceinline__ HaloWalk(const ConvProb& p, int img0, int y0, int c0_, int cbw, float rc_cpp) {
+    const bool pool = DGRAD && p.pool;
+    cpp = cbw / VEC;
+    imgs = p.imgs;
+    hc = p.hc;
+    hr = p.hr;
+    c0 = c0_;
+    const int cs = p.cs, plane = hr * hc, dpos = NT / cpp, dr0 = dpos - (dpos / plane) * plane;
+    dch = NT - dpos * cpp;
+    dimg = dpos / plane;
+    dhr = dr0 / hc;
+    dhc = dr0 - dhr * hc;
+    dst_step = dpos * cs + dch * VEC;
+    dst_wrap = cs - cbw;
+    CH = DGRAD ? p.O : p.C;
+    YL = DGRAD ? (pool ? 2 * p.PH : p.OH) : p.H;
+    XL = DGRAD ? (pool ? 2 * p.PW : p.OW) : p.W;
+    ROW = (DGRAD ? (pool ? p.PW : p.OW) : p.W) * CH;
+    IMG = (unsigned)(DGRAD ? (pool ? p.PH : p.OH) : p.H) * (unsigned)ROW;
+    ybase = DGRAD ? y0 + p.pad - (p.KH - 1) : y0 - p.pad;
+    xbase = DGRAD ? p.pad - (p.KH - 1) : -p.pad;
+    lastimg = p.Nb - img0;  // images at or past it are past the batch
+    int rem;
+    const int pos = SmallDiv(cpp, rc_cpp).qr(threadIdx.x, chi);
+    img = SmallDiv(plane, p.rc_plane).qr(pos, rem);
+    hrow = SmallDiv(hc, p.rc_hc).qr(rem, hcol);
+    dst = pos * cs + chi * VEC;
+    nb = (unsigned)(img0 + img) * IMG;
+  }
+  __device__ __forceinline__ bool live() const { return img < imgs; }
+  // source element offset of the current element (shift sh: un-pooled rows
+  // and columns of a pooled gradient) and whether it lies in the image
+  template <int SH>
+  __device__ __forceinline__ unsigned src(bool& in, int& y, int& x) const {
+    y = ybase + hrow;
+    x = xbase + hcol;
+    in = img < imgs && img < lastimg && (unsigned)y < (unsigned)YL && (unsigned)x < (unsigned)XL;
+    return nb + __umul24((unsigned)(y >> SH), (unsigned)ROW) + __umul24((unsigned)(x >> SH), (unsigned)CH) +
+           (unsigned)(c0 + chi * VEC);
+  }
+  // the next element, NT on
+  template <bool FIX>
+  __device__ __forceinline__ void next() {
+    dst += dst_step;
+    hcol += dhc;
+    hrow += dhr;
+    img += dimg;
+    nb += (unsigned)dimg * IMG;
+    if constexpr (!FIX) {
+      chi += dch;
+      if (chi >= cpp) {
+        chi -= cpp;
+        dst += dst_wrap;
+        ++hcol;
+      }
+    }
+    if (hcol >= hc) {
+      hcol -= hc;
+      ++hrow;
+    }
+    if (hrow >= hr) {
+      hrow -= hr;
+      ++img;
+      nb += IMG;
+    }
+  }
+};
+
 // Stage channels [c0, c0 + cbw) of the operand rows a halo tile reads into
 // LDS, [img][hr][hc][cs]; positions outside the image (padding), past the
 // batch, or - data gradient - not receiving the window's gradient are zero.
-// Forward: the conv input X. Data gradient: dZ, expanded from the pooled
-// gradient G and the window argmax.
-// Element e = (position, 16-byte chunk) of the staged block; a thread takes
-// e = tid, tid + NT, ... and steps its (chunk, column, row, image) by the
-// uniform decomposition of NT with carries (no per-element division; when
-// the chunks per position divide NT a thread's chunk never changes). Source
-// offsets: the image's base kept as a running sum, rows and columns by 24-bit
-// multiplies (rows of under 2^24 elements, tensors of under 2^31 bytes).
 // Every element is loaded through buffer resources: one outside the image
 // reads at an offset past the range, which returns zero.
 template <typename T, bool DGRAD, int NT = 256>
 __device__ __forceinline__ void stage_halo(const ConvProb& p, T* sH, int img0, int y0, int c0, int cbw, float rc_cpp) {
   // four loads in flight per thread (six or eight measured no faster for
   // the data gradient's larger blocks)
-  constexpr int VEC = TT<T>::VEC, UNR = 4;
+  constexpr int UNR = 4;
   constexpr uint32_t OOB = 0x80000000u;
-  const int cpp = cbw / VEC, hc = p.hc, hr = p.hr, cs = p.cs, imgs = p.imgs, Nb = p.Nb, plane = hr * hc;
-  const int dpos = NT / cpp, dch = NT - dpos * cpp, dimg = dpos / plane, dr = dpos - dimg * plane;
-  const int dhr = dr / hc, dhc = dr - dhr * hc;
-  const int dst_step = dpos * cs + dch * VEC, dst_wrap = cs - cbw;
-  // geometry of the source: rows of ROW elements, images of IMG, channel
-  // stride CH; position (hrow, hcol) reads row ybase + hrow, column xbase + hcol
+  HaloWalk<T, DGRAD, NT> w(p, img0, y0, c0, cbw, rc_cpp);
   const bool pool = DGRAD && p.pool;
-  const int CH = DGRAD ? p.O : p.C, sh = pool ? 1 : 0;
-  const int YL = DGRAD ? (pool ? 2 * p.PH : p.OH) : p.H, XL = DGRAD ? (pool ? 2 * p.PW : p.OW) : p.W;
-  const int ROW = (DGRAD ? (pool ? p.PW : p.OW) : p.W) * CH;
-  const unsigned IMG = (unsigned)(DGRAD ? (pool ? p.PH : p.OH) : p.H) * (unsigned)ROW;
-  const int ybase = DGRAD ? y0 + p.pad - (p.KH - 1) : y0 - p.pad, xbase = DGRAD ? p.pad - (p.KH - 1) : -p.pad;
-  const __amdgpu_buffer_rsrc_t rs = make_rsrc(DGRAD ? p.G : p.X, (int64_t)Nb * IMG * (int64_t)sizeof(T));
-  const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.gam, pool ? (int64_t)Nb * IMG : 0);
-  // this thread's first element
-  int chi, rem, hcol;
-  const int pos = SmallDiv(cpp, rc_cpp).qr(threadIdx.x, chi);
-  int img = SmallDiv(plane, p.rc_plane).qr(pos, rem);
-  int hrow = SmallDiv(hc, p.rc_hc).qr(rem, hcol), dst = pos * cs + chi * VEC;
-  unsigned nb = (unsigned)(img0 + img) * IMG;
-  auto run = [&](auto fixed_chunk) {
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(DGRAD ? p.G : p.X, (int64_t)p.Nb * w.IMG * (int64_t)sizeof(T));
+  const __amdgpu_buffer_rsrc_t ra = make_rsrc(p.gam, pool ? (int64_t)p.Nb * w.IMG : 0);
+  auto run = [&](auto fixed_chunk, auto shift) {
     constexpr bool FIX = decltype(fixed_chunk)::value;
-    const unsigned cofs = (unsigned)(c0 + chi * VEC);
-    while (img < imgs) {
+    constexpr int SH = decltype(shift)::value;
+    while (w.live()) {
       u32x4 v[UNR];
       int dd[UNR];
 #pragma unroll
       for (int k = 0; k < UNR; ++k) {
-        dd[k] = img < imgs ? dst : -1;
-        const int y = ybase + hrow, x = xbase + hcol;
-        const bool in = img < imgs && img0 + img < Nb && (unsigned)y < (unsigned)YL && (unsigned)x < (unsigned)XL;
-        const unsigned off = nb + __umul24((unsigned)(y >> sh), (unsigned)ROW) +
-                             __umul24((unsigned)(x >> sh), (unsigned)CH) + (FIX ? cofs : (unsigned)(c0 + chi * VEC));
+        dd[k] = w.live() ? w.dst : -1;
+        bool in;
+        int y, x;
+        const unsigned off = w.template src<SH>(in, y, x);
         v[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? off * (unsigned)sizeof(T) : OOB, 0, 0));
-        if (pool) select_am<T>(v[k], load_am_buf<T>(ra, in ? off : OOB), ((y & 1) << 1) | (x & 1));
-        // the next element, NT on
-        dst += dst_step;
-        hcol += dhc;
-        hrow += dhr;
-        img += dimg;
-        nb += (unsigned)dimg * IMG;
-        if constexpr (!FIX) {
-          chi += dch;
-          if (chi >= cpp) {
-            chi -= cpp;
-            dst += dst_wrap;
-            ++hcol;
-          }
-        }
-        if (hcol >= hc) {
-          hcol -= hc;
-          ++hrow;
-        }
-        if (hrow >= hr) {
-          hrow -= hr;
-          ++img;
-          nb += IMG;
-        }
+        if (SH) select_am<T>(v[k], load_am_buf<T>(ra, in ? off : OOB), ((y & 1) << 1) | (x & 1));
+        w.template next<FIX>();
       }
 #pragma unroll
       for (int k = 0; k < UNR; ++k)
         if (dd[k] >= 0) *(u32x4*)(sH + dd[k]) = v[k];
     }
   };
-  if (dch == 0) run(std::true_type{});
-  else run(std::false_type{});
+  using F = std::false_type;
+  using Tr = std::true_type;
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  if (pool) {
+    if (w.dch == 0) run(Tr{}, S1{});
+    else run(F{}, S1{});
+  } else {
+    if (w.dch == 0) run(Tr{}, S0{});
+    else run(F{}, S0{});
+  }
+}
+
+// The forward halo block of a tile (origin img0, y0), loaded into registers
+// only: this thread's first PF elements, v[k] bound for LDS element dd[k]
+// (-1: none). Multi-tile workgroups fetch the next tile's rows this way before
+// the current tile's epilogue stores (loads and stores share one in-order
+// counter), and write them to LDS after it (put_halo); the host enables them
+// only where PF elements per thread cover the block.
+template <typename T, int NT, int PF>
+__device__ __forceinline__ void fetch_halo(const ConvProb& p, int img0, int y0, float rc_cpp, u32x4 (&v)[PF],
+                                           int (&dd)[PF]) {
+  constexpr uint32_t OOB = 0x80000000u;
+  HaloWalk<T, false, NT> w(p, img0, y0, 0, p.C, rc_cpp);
+  const __amdgpu_buffer_rsrc_t rs = make_rsrc(p.X, (int64_t)p.Nb * w.IMG * (int64_t)sizeof(T));
+#pragma unroll
+  for (int k = 0; k < PF; ++k) {
+    dd[k] = w.live() ? w.dst : -1;
+    bool in;
+    int y, x;
+    const unsigned off = w.template src<0>(in, y, x);
+    v[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, in ? off * (unsigned)sizeof(T) : OOB, 0, 0));
+    w.template next<false>();
+  }
+}
+template <typename T, int PF>
+__device__ __forceinline__ void put_halo(T* sH, const u32x4 (&v)[PF], const int (&dd)[PF]) {
+#pragma unroll
+  for (int k = 0; k < PF; ++k)
+    if (dd[k] >= 0) *(u32x4*)(sH + dd[k]) = v[k];
 }
 
 // One k-block of a halo tile: A rows read from the staged halo at the lane's
@@ -2226,7 +2305,11 @@ struct HaloSmem {
   static constexpr size_t BYTES = (2 * (size_t)B_ELEMS + HALO) * sizeof(T) + 2 * HALO_QMAX * sizeof(int);
 };
 
-// One BM x BN halo tile `local` of problem p.
+// The BM x BN halo tile `local` of problem p and, for a multi-tile forward
+// workgroup (p.mt > 1: one channel block), the next p.mt - 1 m-tiles of the
+// same n-column. Those reuse the tap tables and row bases, and (at most two
+// k-blocks) the weights in LDS; their rows are fetched into registers before
+// the previous tile's epilogue.
 template <typename T, int BM, int BN, int BK, bool DGRAD, int NW>
 __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* smem) {
   using TL = Tile<T, BM, BN, BK, NW>;
@@ -2235,22 +2318,31 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
   using HS = HaloSmem<T, BN, BK>;
   constexpr int VEC = TT<T>::VEC, CPB = BK / VEC;
   static_assert(TL::B_ELEMS == HS::B_ELEMS, "halo LDS budget assumes one pad chunk per row");
+  static_assert(NT == (sizeof(T) == 2 ? HALO_NT_BF16 : HALO_NT_F32), "halo workgroup size");
   T* sB = (T*)smem;
   int* qa = (int*)(sB + 2 * TL::B_ELEMS);
   int* qb = qa + HALO_QMAX;
   T* sH = (T*)(qb + HALO_QMAX);
-  const int tm = local / p.tiles_n, tn = local - tm * p.tiles_n;
-  const int m0 = tm * BM, n0 = tn * BN;
+  const int tm0 = local / p.tiles_n, tn = local - tm0 * p.tiles_n;
+  const int n0 = tn * BN;
   const int SH = DGRAD ? p.H : p.OH, SW = DGRAD ? p.W : p.OW;
+  // (not the tall tiles: their accumulators leave no registers for the
+  // fetched rows across the epilogue; the host plans none)
+  constexpr bool MULTI = !DGRAD && BM <= 2 * (sizeof(T) == 2 ? CONV_BM_BF16 : CONV_BM_F32);
+  const int mt = MULTI ? max(1, min(p.mt, p.tiles_m - tm0)) : 1;
+  // first operand image and row of m-tile tm
+  auto origin = [&](int tm, int& img0, int& y0) {
+    if (p.imgs > 1) {
+      img0 = tm * p.imgs;
+      y0 = 0;
+    } else {
+      const int tpi = SH / p.tr;
+      img0 = tm / tpi;
+      y0 = (tm - img0 * tpi) * p.tr;
+    }
+  };
   int img0, y0;
-  if (p.imgs > 1) {
-    img0 = tm * p.imgs;
-    y0 = 0;
-  } else {
-    const int tpi = SH / p.tr;
-    img0 = tm / tpi;
-    y0 = (tm - img0 * tpi) * p.tr;
-  }
+  origin(tm0, img0, y0);
   // halo offset of the first tap of each of this lane's MFMA rows
   int hbase[L::FM];
   {
@@ -2275,19 +2367,44 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
   lb.init((const T*)p.Wt + (int64_t)n0 * p.ldw, p.ldw, p.N - n0);
   const int KH = p.KH, Cin = DGRAD ? p.O : p.C, cq = threadIdx.x % CPB, hc = p.hc, cs = p.cs;
   const SmallDiv dkh(KH, p.rc_kh);
+  // weight column of chunk q of the channel block at c0 (cpt chunks per tap;
+  // -1 past its nq chunks)
+  auto col_of = [&](int q, const SmallDiv& dcpt, int nq, int c0) {
+    int cr;
+    const int tap = dcpt.qr(q, cr);
+    return q < nq ? tap * Cin + c0 + cr * VEC : -1;
+  };
+  // the k loop of a channel block of nq chunks (nkb k-blocks), whose first
+  // k-block is in LDS buffer 0 and second in register slot 1. Iteration kb
+  // (P = kb & 1): load k-block kb + 2 into slot P (its k-block kb is in LDS
+  // already), run k-block kb from LDS buffer P, move k-block kb + 1 from slot
+  // P ^ 1 to LDS buffer P ^ 1 (last read in iteration kb - 1)
+  auto kloop = [&](int nq, int nkb) {
+    auto step = [&](auto par, int kb) {
+      constexpr int P = decltype(par)::value;
+      if (kb + 2 < nkb) {
+        const int q = (kb + 2) * CPB + cq;
+        lb.template load<P>(q < nq ? qb[q] : -1);
+      }
+      mma_halo<BM, BN, BK, NW>(sH, hbase, qa, kb * CPB, nq, sB + P * TL::B_ELEMS, acc);
+      if (kb + 1 < nkb) lb.template store<P ^ 1>(sB + (P ^ 1) * TL::B_ELEMS);
+      __syncthreads();
+    };
+    int kb = 0;
+    for (; kb + 1 < nkb; kb += 2) {
+      step(std::integral_constant<int, 0>{}, kb);
+      step(std::integral_constant<int, 1>{}, kb + 1);
+    }
+    if (kb < nkb) step(std::integral_constant<int, 0>{}, kb);
+  };
   for (int c0 = 0; c0 < Cin; c0 += p.cb) {
     const int cbw = min(p.cb, Cin - c0), cpt = cbw / VEC, nq = KH * KH * cpt;
     const SmallDiv dcpt(cpt, c0 + p.cb >= Cin ? p.rc_cpt_last : p.rc_cpt);
     // the weights of k-blocks 0 and 1 first (columns computed directly), so
     // their loads overlap the staging of the operand rows; k-block kb sits in
     // register slot kb & 1 and LDS buffer kb & 1
-    auto col_of = [&](int q) {
-      int cr;
-      const int tap = dcpt.qr(q, cr);
-      return q < nq ? tap * Cin + c0 + cr * VEC : -1;
-    };
-    lb.template load<0>(col_of(cq));
-    lb.template load<1>(col_of(CPB + cq));
+    lb.template load<0>(col_of(cq, dcpt, nq, c0));
+    lb.template load<1>(col_of(CPB + cq, dcpt, nq, c0));
     __syncthreads();  // the previous channel block's halo, tables and weight stages are no longer read
     // qa: the halo offset of a chunk's tap and channels (bf16: in bytes, in
     // the k-block layout of mma_halo, padded to whole k-blocks); qb: its
@@ -2319,29 +2436,39 @@ __device__ __forceinline__ void halo_tile(const ConvProb& p, int local, char* sm
     stage_halo<T, DGRAD, NT>(p, sH, img0, y0, c0, cbw, dcpt.r);
     lb.template store<0>(sB);
     __syncthreads();
-    const int nkb = (nq + CPB - 1) / CPB;
-    // iteration kb (P = kb & 1): load k-block kb + 2 into slot P (its k-block
-    // kb is in LDS already), run k-block kb from LDS buffer P, move k-block
-    // kb + 1 from slot P ^ 1 to LDS buffer P ^ 1 (last read in iteration kb - 1)
-    auto step = [&](auto par, int kb) {
-      constexpr int P = decltype(par)::value;
-      if (kb + 2 < nkb) {
-        const int q = (kb + 2) * CPB + cq;
-        lb.template load<P>(q < nq ? qb[q] : -1);
-      }
-      mma_halo<BM, BN, BK, NW>(sH, hbase, qa, kb * CPB, nq, sB + P * TL::B_ELEMS, acc);
-      if (kb + 1 < nkb) lb.template store<P ^ 1>(sB + (P ^ 1) * TL::B_ELEMS);
-      __syncthreads();
-    };
-    int kb = 0;
-    for (; kb + 1 < nkb; kb += 2) {
-      step(std::integral_constant<int, 0>{}, kb);
-      step(std::integral_constant<int, 1>{}, kb + 1);
-    }
-    if (kb < nkb) step(std::integral_constant<int, 0>{}, kb);
+    kloop(nq, (nq + CPB - 1) / CPB);
   }
-  if constexpr (DGRAD) conv_dgrad_epilogue<T, BM, BN, L>(p, m0, n0, acc, smem);
-  else conv_fwd_epilogue<T, L>(p, m0, n0, acc);
+  if constexpr (DGRAD) {
+    conv_dgrad_epilogue<T, BM, BN, L>(p, tm0 * BM, n0, acc, smem);
+  } else {
+    // the epilogue, then any further m-tiles (mt > 1: one channel block, whose
+    // tables stay in LDS). The k loop's last barrier has freed the staged
+    // rows; at most two k-blocks leave both weight buffers (and register slot
+    // 1) as they are.
+    const int cpt = Cin / VEC, nq = KH * KH * cpt, nkb = (nq + CPB - 1) / CPB;
+    const SmallDiv dcpt(cpt, p.rc_cpt_last);
+    for (int t = 1;; ++t) {
+      const bool more = MULTI && t < mt;
+      u32x4 hv[HALO_PF];
+      int hd[HALO_PF];
+      if (more) {
+        int nimg0, ny0;
+        origin(tm0 + t, nimg0, ny0);
+        fetch_halo<T, NT, HALO_PF>(p, nimg0, ny0, dcpt.r, hv, hd);
+        if (nkb > 2) {
+          lb.template load<0>(col_of(cq, dcpt, nq, 0));
+          lb.template load<1>(col_of(CPB + cq, dcpt, nq, 0));
+        }
+      }
+      conv_fwd_epilogue<T, L>(p, (tm0 + t - 1) * BM, n0, acc);
+      if (!more) break;
+      L::zero(acc);
+      put_halo<T, HALO_PF>(sH, hv, hd);
+      if (nkb > 2) lb.template store<0>(sB);
+      __syncthreads();
+      kloop(nq, nkb);
+    }
+  }
 }
 
 // Halo-tiled conv pass; each problem's tile shape (p.bm x p.bn) is the wide

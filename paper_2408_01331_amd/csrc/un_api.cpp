@@ -25,6 +25,15 @@
 
 #include "internal.h"
 
+// Multi-tile halo forward workgroups: at most UN_HALO_MT m-tiles each, as
+// many as leave about UN_HALO_WPS workgroups per slot (two per CU).
+#ifndef UN_HALO_MT
+#define UN_HALO_MT 4
+#endif
+#ifndef UN_HALO_WPS
+#define UN_HALO_WPS 4
+#endif
+
 using namespace un;
 
 namespace {
@@ -648,6 +657,14 @@ static bool try_halo(ConvProb& p, bool bf, bool dgrad, int BM, int BN) {
   return true;
 }
 
+// A halo forward problem that a multi-tile workgroup can run: one channel
+// block, wide or narrow tiles (a tall tile's accumulators leave no registers
+// for the rows fetched ahead), staged rows within the fetch-ahead registers.
+static bool halo_multi_ok(const ConvProb& p, bool bf) {
+  const int BM = bf ? CONV_BM_BF16 : CONV_BM_F32, vec = bf ? 8 : 4, nt = bf ? HALO_NT_BF16 : HALO_NT_F32;
+  return p.halo && p.C <= p.cb && p.bm <= 2 * BM && (int64_t)p.imgs * p.hr * p.hc * (p.cb / vec) <= (int64_t)HALO_PF * nt;
+}
+
 static void plan_halo(ConvProb& p, bool bf, bool dgrad) {
   const int BM = bf ? CONV_BM_BF16 : CONV_BM_F32, BN = bf ? CONV_BN_BF16 : CONV_BN_F32;
   p.halo = 0;
@@ -811,13 +828,25 @@ static void build_tables(un_ctx* c, Tables& T) {
     std::stable_sort(ps.begin(), ps.end(),
                      [](const ConvProb& x, const ConvProb& y) { return (int64_t)x.K * x.splits > (int64_t)y.K * y.splits; });
     const int BK = bf ? CONV_BK_BF16 : CONV_BK_F32;
+    int64_t total = 0;
+    for (ConvProb& p : ps) {
+      p.tiles_m = cdiv(p.M, p.bm ? p.bm : CBM);  // halo tiles and narrow weight-gradient tiles set bm
+      p.tiles_n = cdiv(p.N, p.halo ? p.bn : CBN);
+      total += (int64_t)p.tiles_m * p.tiles_n;
+    }
+    // halo forward passes that a multi-tile workgroup can run: mt consecutive
+    // m-tiles per workgroup
+    const int mt = kind == 7 ? (int)std::max<int64_t>(1, std::min<int64_t>(UN_HALO_MT, total / (UN_HALO_WPS * 2 * 256))) : 1;
     std::vector<TileGroup> gs;
     for (size_t k = 0; k < ps.size(); ++k) {
       ConvProb& p = ps[k];
-      p.tiles_m = cdiv(p.M, p.bm ? p.bm : CBM);  // halo tiles and narrow weight-gradient tiles set bm
-      p.tiles_n = cdiv(p.N, p.halo ? p.bn : CBN);
       const int per_split = p.tiles_m * p.tiles_n;
-      if (kind == 3) {
+      if (kind == 7 && mt > 1 && halo_multi_ok(p, bf)) {
+        p.mt = mt;
+        for (int g = 0; g < p.tiles_m; g += mt)
+          for (int tn = 0; tn < p.tiles_n; ++tn)
+            gs.push_back(TileGroup{(int32_t)k, g * p.tiles_n + tn, 1, (cdiv(p.K, BK) + 2.0) * mt});
+      } else if (kind == 3) {
         // weight gradient: one group per split (its tiles read the same pixels)
         for (int sp = 0; sp < p.splits; ++sp)
           gs.push_back(TileGroup{(int32_t)k, sp * per_split, per_split, per_split * (p.kchunk + 1.0)});
@@ -918,6 +947,7 @@ static void build_tables(un_ctx* c, Tables& T) {
     p.relu = b.relu;
     p.prev_relu = b.prev_relu;
     p.splits = 1;
+    p.mt = 1;
     return p;
   };
 
