@@ -8,12 +8,15 @@
 //     workgroup tile; fp32 workgroups of 4 waves (2x2) of
 //     v_mfma_f32_16x16x4_f32 on 64x64;
 //   - the implicit-GEMM convolution passes: forward with the bias / ReLU /
-//     2x2 max-pool epilogue (v_mfma_f32_16x16x32_bf16, whose accumulator rows
-//     hold a pool window), data gradient with the un-pool gather, and the
-//     split-K weight gradient (bf16: the GEMM's 32x32x16 core on k-major
-//     operands), reduced in split order by a kernel that applies the update.
-// A workgroup owns one output tile of one problem; a flat tile table maps
-// blockIdx.x to (problem, tile). Every output element is reduced over k in a
+//     2x2 max-pool epilogue and data gradient with the un-pool gather, on
+//     halo tiles staged in LDS (bf16: 8 waves of v_mfma_f32_32x32x16_bf16
+//     blocks, a lane's runs of four accumulator rows holding a pool window;
+//     the gathered passes for other shapes: 16x16x32), and the split-K weight
+//     gradient (bf16: the GEMM's 32x32x16 core on k-major operands), reduced
+//     in split order by a kernel that applies the update.
+// A workgroup owns one output tile of one problem (a halo forward workgroup
+// may own several consecutive m-tiles); a flat tile table maps blockIdx.x to
+// (problem, first tile). Every output element is reduced over k in a
 // fixed order that depends only on its own problem's shape, so a model's
 // results are bitwise independent of which other models share the launch.
 #include <hip/hip_runtime.h>
@@ -256,8 +259,8 @@ __device__ __forceinline__ void mma_loop1(L& ld, int kb0, int kb1, T* smem,
 
 // The grouped GEMM's MFMA policy. bf16 runs v_mfma_f32_32x32x16_bf16, which
 // sustains about twice the rate of the 16x16x32 form on gfx950 (2.2 vs 1.2
-// PFLOP/s with register operands): each of the 4 waves owns a (BM/2) x (BN/2)
-// tile of 32x32 blocks, acc[I][J][e] holding
+// PFLOP/s with register operands): each of the WGM x WGN waves owns a
+// (BM/WGM) x (BN/WGN) tile of 32x32 blocks, acc[I][J][e] holding
 //   C[wm + 32I + 8(e/4) + 4(lane/32) + e%4][wn + 32J + lane%32].
 // fp32 keeps the 16x16x4 blocks of mma_block. for_groups visits every run of
 // four consecutive rows of one column a lane holds: f(row, col, v[4]) in tile
