@@ -289,6 +289,29 @@ def test_halo_tiled_cnns(precision):
     _report(f"halo_cnns_{precision} run", _run_vs_oracle(wl, m))
 
 
+@pytest.mark.parametrize("precision,n_models", [("bf16", 62), ("f32", 35)])
+def test_multi_tile_halo_forward(precision, n_models):
+    """Forward halo passes that run several m-tiles per workgroup. A batch of 25
+    keeps each first conv below the rows that take tall tiles (32768), so its
+    narrow tiles (whole image rows) number 100 (bf16) or 200 (fp32) per model;
+    with this many models the launch holds enough of them for three per
+    workgroup, and neither count is a multiple of three (a last, shorter
+    group). Its K (9 taps of one padded channel vector) is at most two
+    k-blocks, the case whose weights stay in LDS across the tiles; the second
+    conv's K of 9 x 16 or 9 x 8 streams its weights per tile."""
+    _need_gpu()
+    specs = [
+        {"layers": [("conv", 16, 3, 1), ("relu",), ("pool",), ("conv", 32, 3, 1), ("relu",), ("pool",),
+                    ("flatten",), ("linear", 10)], "num_classes": 10},
+        {"layers": [("conv", 8, 3, 1), ("relu",), ("pool",), ("conv", 48, 3, 1), ("relu",), ("pool",),
+                    ("flatten",), ("linear", 10)], "num_classes": 10},
+    ]
+    wl = _custom([specs[i % 2] for i in range(n_models)], 25, (3, 32, 32), precision, steps=2)
+    m = range(wl.n_models)
+    _report(f"multi_tile_{precision} 1 step", _step_vs_oracle(wl, m))
+    _report(f"multi_tile_{precision} run", _run_vs_oracle(wl, m))
+
+
 _RES_CNNS = [
     {"layers": [("conv", 16, 3, 1), ("relu",), ("pool",), ("res_begin",), ("conv", 16, 3, 1), ("relu",),
                 ("conv", 16, 3, 1), ("res_end",), ("relu",), ("conv", 8, 3, 1), ("relu",), ("pool",),
