@@ -1102,8 +1102,8 @@ static void build_tables(un_ctx* c, Tables& T) {
   // (at lv == 0 also those of level 0). A block's weights are updated one
   // launch after its data gradient has read them, so no launch both reads and
   // writes the same weights. Conv blocks keep their own per-level launches
-  // (data gradient, then split-K weight gradient, then the reduction with the
-  // update).
+  // (data gradient, then split-K weight gradient); the split-K reductions
+  // with their updates run in one launch after the last level.
   auto add_wgrad = [&](const Block& b, std::vector<GemmProb>& gp, std::vector<char>& cat_done,
                        std::vector<ReduceProb>& rp) {
     const int gi = c->models[b.model].group;
@@ -1195,10 +1195,14 @@ static void build_tables(un_ctx* c, Tables& T) {
     }
     gp.push_back(p);
   };
+  // the split-K reductions (and their updates) of all levels: one launch at
+  // the end of the backward pass. Each block's partials have a workspace
+  // range of their own, and no later launch of the step reads the weights of
+  // a deeper level (a conv block's data gradient has read them before).
+  std::vector<ReduceProb> rp;
   for (int lv = levels - 1; lv >= 0; --lv) {
     std::vector<GemmProb> gp;
     std::vector<ConvProb> dp, wp;
-    std::vector<ReduceProb> rp;
     std::vector<AttnProb> ap;
     std::vector<char> cat_done(c->groups.size(), 0);
     for (auto& m : c->models) {
@@ -1308,24 +1312,24 @@ static void build_tables(un_ctx* c, Tables& T) {
     emit_attn(ap, bwd, 10);
     emit_conv(dp, bwd, 2, UN_K_CONV_DGRAD);
     emit_conv(wp, bwd, 3, UN_K_CONV_WGRAD);
-    if (!rp.empty()) {
-      std::vector<int32_t> map;
-      for (size_t k = 0; k < rp.size(); ++k) {
-        rp[k].blk_base = (int32_t)map.size();
-        const int nb = cdiv((int64_t)rp[k].O * (rp[k].J + 1), REDUCE_BLOCK);
-        for (int t = 0; t < nb; ++t) map.push_back((int32_t)k);
-      }
-      size_t po = put(rp.data(), rp.size() * sizeof(ReduceProb));
-      for (size_t k = 0; k < rp.size(); ++k) {
-        size_t b0 = po + k * sizeof(ReduceProb);
-        for (size_t f : {offsetof(ReduceProb, ws), offsetof(ReduceProb, gW), offsetof(ReduceProb, gb),
-                         offsetof(ReduceProb, W), offsetof(ReduceProb, Wb), offsetof(ReduceProb, WT),
-                         offsetof(ReduceProb, bmaster)})
-          fix.push_back(b0 + f);
-      }
-      size_t mo = put(map.data(), map.size() * 4);
-      bwd.push_back(Launch{4, UN_K_OTHER, po, mo, (int)map.size()});
+  }
+  if (!rp.empty()) {
+    std::vector<int32_t> map;
+    for (size_t k = 0; k < rp.size(); ++k) {
+      rp[k].blk_base = (int32_t)map.size();
+      const int nb = cdiv((int64_t)rp[k].O * (rp[k].J + 1), REDUCE_BLOCK);
+      for (int t = 0; t < nb; ++t) map.push_back((int32_t)k);
     }
+    size_t po = put(rp.data(), rp.size() * sizeof(ReduceProb));
+    for (size_t k = 0; k < rp.size(); ++k) {
+      size_t b0 = po + k * sizeof(ReduceProb);
+      for (size_t f : {offsetof(ReduceProb, ws), offsetof(ReduceProb, gW), offsetof(ReduceProb, gb),
+                       offsetof(ReduceProb, W), offsetof(ReduceProb, Wb), offsetof(ReduceProb, WT),
+                       offsetof(ReduceProb, bmaster)})
+        fix.push_back(b0 + f);
+    }
+    size_t mo = put(map.data(), map.size() * 4);
+    bwd.push_back(Launch{4, UN_K_OTHER, po, mo, (int)map.size()});
   }
   // Copy refresh (after un_set_params / initialisation / a set change):
   // rewrite the bf16 copy (and a conv block's transposed copy) of every weight
