@@ -2842,7 +2842,16 @@ __global__ __launch_bounds__(REDUCE_BLOCK) void reduce_kernel(const ReduceProb* 
 #pragma unroll
     for (int u = 0; u < 8; ++u) s += v[u];
   }
-  for (; k < splits; ++k) s += ws[col + k * sstride];
+  if (k < splits) {
+    // the last (splits - k < 8) partials: loads issued together, then added
+    // in split order
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = k + u < splits ? ws[col + (k + u) * sstride] : 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (k + u < splits) s += v[u];
+  }
   if (j < p.J) {
     const int idx = o * (int)p.ldgw + j;
     if (keep_grads) p.gW[idx] = s;
